@@ -1,0 +1,186 @@
+#!/usr/bin/env python3
+"""Benchmark of the diffusion-map hot path on one MI355X.
+
+One step = one pass of the path over the flat 6-torus workload (65,536
+points in R^12, block width 16, bandwidth sweep beta in {0.5, 1, 2, 4, 8},
+alpha = 1/2): for every beta the two normalisation passes (q = K 1,
+d = q^-a K q^-a) and one fused normalised product Y = diag(s) K diag(s) V.
+Inputs are resident in HBM before the timed region.
+
+Printed value: whole-step throughput in kernel pair-columns per second,
+sum over the sweep of N^2 * b divided by the step time (the normalisation
+passes are inside the step time).  The roofline object is for the fused
+product kernel, timed with HIP events on its launch stream.
+
+``--lanczos`` adds the time to the top-16 eigenpairs on the 2-torus
+workload (N = 2048, beta = 8, b = 8) as an extra field.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_FP32_MFMA_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or "unknown"
+
+
+def cpu_baseline(X: np.ndarray, beta: float, b: int, seconds: float) -> dict:
+    """Time the oracle's product on a bounded sample of rows (float64, CPU)."""
+    from oracle import kernel as ok
+    from paper_2609_38198_amd import inputs
+
+    cores = min(len(os.sched_getaffinity(0)), 16)
+    N = X.shape[0]
+    V = inputs.random_block(N, b, seed=2)
+    rng = np.random.default_rng(0)
+    probe_rows = rng.choice(N, 64 * cores, replace=False)
+    t0 = time.perf_counter()
+    ok.kernel_matmul(X, None, beta, V, rows=probe_rows, block=64, threads=cores)
+    t_probe = time.perf_counter() - t0
+    nrows = int(min(N, max(64 * cores, len(probe_rows) * seconds / max(t_probe, 1e-3))))
+    rows = rng.choice(N, nrows, replace=False)
+    t0 = time.perf_counter()
+    ok.kernel_matmul(X, None, beta, V, rows=rows, block=64, threads=cores)
+    t = time.perf_counter() - t0
+    return {"value": nrows * N * b / t, "unit": "pair-cols/s", "cores": cores, "kind": "oracle",
+            "sample": f"float64 difference-form product K V on {nrows} seeded rows x all {N} "
+                      f"columns, b={b}, beta={beta}, {t:.1f} s on {cores} threads of {cpu_model()}"}
+
+
+def lanczos_leg(fd, torch, dev) -> dict:
+    from paper_2609_38198_amd import inputs
+    w = inputs.torus2()
+    X = torch.from_numpy(w.X).to(dev)
+    fd.fd_block_lanczos(X, w.betas[0], w.k, w.b)  # warm-up (code objects, allocator)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    e = fd.fd_block_lanczos(X, w.betas[0], w.k, w.b)
+    torch.cuda.synchronize()
+    t = time.perf_counter() - t0
+    return {"workload": "torus2 N=2048 D=4 beta=8 b=8 k=16", "seconds": t,
+            "block_matvecs": e.info["block_matvecs"], "restarts": e.info["restarts"],
+            "max_residual": e.info["max_residual"]}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--lanczos", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+              "(row sharding is a design note, not code).", file=sys.stderr)
+        return 2
+
+    import torch
+
+    from paper_2609_38198_amd import _lib as fd
+    from paper_2609_38198_amd import inputs
+
+    dev = torch.device("cuda:0")
+    wl = inputs.torus6()
+    N, D, b = wl.N, wl.D, wl.b
+    betas = wl.betas
+    alpha = wl.alpha
+    X = torch.from_numpy(wl.X).to(dev)
+    V = torch.from_numpy(inputs.random_block(N, b)).to(dev)
+    Y = torch.empty((N, b), dtype=torch.float32, device=dev)
+    ws_p = torch.empty(fd.fd_workspace_size(fd.FD_OP_KERNEL_MATMUL, N, N, D, b),
+                       dtype=torch.uint8, device=dev)
+    ws_d = torch.empty(fd.fd_workspace_size(fd.FD_OP_DEGREE, N, N, D), dtype=torch.uint8,
+                       device=dev)
+
+    def step():
+        for beta in betas:
+            deg = fd.fd_degree(X, beta, alpha, ws=ws_d)
+            fd.fd_kernel_matmul(X, None, beta, V, sl=deg.s, sr=deg.s, Y=Y, ws=ws_p)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    fd.fd_profile_read(fd.FD_KERNEL_PRODUCT)
+    fd.fd_profile_read(fd.FD_KERNEL_ROWSUM)
+    fd.fd_profile_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    fd.fd_profile_enable(False)
+    prod_ms, prod_n = fd.fd_profile_read(fd.FD_KERNEL_PRODUCT)
+    row_ms, row_n = fd.fd_profile_read(fd.FD_KERNEL_ROWSUM)
+
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    pair_cols = len(betas) * float(N) * N * b
+    value = pair_cols / (ms_per_step * 1e-3)
+    avg_prod_s = prod_ms * 1e-3 / max(prod_n, 1)
+    flops = 2.0 * N * N * (D + b)
+    achieved = flops / avg_prod_s / 1e12
+    avg_row_s = row_ms * 1e-3 / max(row_n, 1)
+
+    rec = {
+        "metric": "fused K*V pair-cols/sec (N^2*b per sec)",
+        "value": value,
+        "unit": "pair-cols/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"flat 6-torus N={N} D={D} b={b} beta sweep {list(betas)} "
+                               f"alpha={alpha}: per beta 2 normalisation passes + 1 fused "
+                               f"normalised product", "N": N, "D": D, "b": b,
+                   "betas": list(betas), "alpha": alpha, "parallelism": "single GPU"},
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_FP32_MFMA_TFLOPS,
+                     "unit": "TFLOP/s", "frac": achieved / PEAK_FP32_MFMA_TFLOPS,
+                     "traffic": None},
+        "kernels": {
+            "product": {"launches": prod_n, "avg_ms": avg_prod_s * 1e3,
+                        "pair_cols_per_s": float(N) * N * b / avg_prod_s,
+                        "exp_per_s": float(N) * N / avg_prod_s,
+                        "flops_per_launch": flops},
+            "rowsum": {"launches": row_n, "avg_ms": avg_row_s * 1e3,
+                       "pairs_per_s": float(N) * N / avg_row_s,
+                       "tflops": 2.0 * N * N * D / avg_row_s / 1e12},
+        },
+    }
+    if args.lanczos:
+        rec["lanczos"] = lanczos_leg(fd, torch, dev)
+    if not args.no_cpu_baseline:
+        rec["cpu_baseline"] = cpu_baseline(wl.X, 2.0, b, args.cpu_seconds)
+    print(json.dumps(rec), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,199 @@
+/*
+ * flashdiff.h -- C ABI of the diffusion-map kernel library for MI355X (gfx950).
+ *
+ * The library applies the Gaussian affinity K_ij = exp(-beta ||x_i - x_j||^2)
+ * of a point cloud X (N x D) to blocks of vectors without ever forming the
+ * N x N matrix, builds the Coifman-Lafon normalisation from it, and runs a
+ * block Lanczos eigensolver and a warm-started (n, beta) continuation on top.
+ * Paper: FlashDiffusion, Sec. 2 ("FlashDiffusion Algorithm").
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Device pointers are caller-owned HIP device memory on the current device.
+ *    Host pointers are marked "host".  The library allocates no device memory:
+ *    every temporary lives in the caller's workspace `ws` of `ws_bytes` bytes,
+ *    at least fd_workspace_size(...) bytes, 256-byte aligned.
+ *  - Matrices are row-major.  X is N x D with leading dimension ldx >= D
+ *    (elements, not bytes); V, Y, eigenvector blocks are N x b with their own
+ *    leading dimensions.  X holds float32 (FD_F32) or bfloat16 bit patterns
+ *    (FD_BF16); all other floating-point arrays are float32 unless stated.
+ *  - Work is enqueued on `stream` (a hipStream_t; NULL = the null stream).
+ *    fd_kernel_matmul and fd_degree are asynchronous.  fd_block_lanczos and
+ *    fd_continuation synchronise `stream` at every restart cycle to read a few
+ *    scalars back, and return after all their work has completed.
+ *  - Every function returns an fd_status and never throws.  On a non-OK status
+ *    fd_last_error() returns a thread-local message; output contents are then
+ *    unspecified unless the status says otherwise.
+ *  - X should be centred (subtract the column mean): the method is stated for
+ *    centred observations (Sec. 2.1, eq. rbf_gram) and the Gram-form
+ *    evaluation loses accuracy on data far from the origin.  Not enforced.
+ */
+#ifndef FLASHDIFF_H
+#define FLASHDIFF_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum fd_status {
+  FD_OK = 0,
+  FD_ERR_INVALID_ARG = 1,    /* bad size, pointer, or parameter value */
+  FD_ERR_UNSUPPORTED = 2,    /* valid request this build does not implement */
+  FD_ERR_WORKSPACE = 3,      /* workspace missing, too small or misaligned */
+  FD_ERR_HIP = 4,            /* a HIP runtime or launch error (message has it) */
+  FD_ERR_NOT_CONVERGED = 5,  /* eigensolver stopped early; outputs hold best Ritz pairs */
+  FD_ERR_PERRON_WALL = 6     /* continuation stopped at the precision wall */
+} fd_status;
+
+typedef enum fd_dtype {
+  FD_F32 = 0,   /* X in float32 */
+  FD_BF16 = 1   /* X as bfloat16 bit patterns (uint16) */
+} fd_dtype;
+
+typedef enum fd_op {
+  FD_OP_KERNEL_MATMUL = 0,
+  FD_OP_DEGREE = 1,
+  FD_OP_BLOCK_LANCZOS = 2,
+  FD_OP_CONTINUATION = 3
+} fd_op;
+
+/* Options of the block Lanczos eigensolver (Sec. 2.3, first paragraph: block
+ * implicitly restarted Lanczos; realised as thick-restart block Lanczos with
+ * full reorthogonalisation).  fd_lanczos_default_opts fills the defaults. */
+typedef struct fd_lanczos_opts {
+  double tol;               /* converged when ||M phi - theta phi||_2 <= tol (||M||_2 = 1). Default 1e-5 */
+  int32_t max_restarts;     /* restart cycles before FD_ERR_NOT_CONVERGED. Default 200 */
+  int32_t max_basis_blocks; /* basis capacity in blocks of b (0 = automatic: k + keep + 4b, rounded) */
+  int32_t keep;             /* Ritz vectors kept at restart beyond k (-1 = automatic: b) */
+  int32_t max_matvecs;      /* stop after this many block products (0 = no limit). A run that
+                               stops this way returns FD_ERR_NOT_CONVERGED with valid Ritz pairs */
+  int32_t reserved;
+  uint64_t seed;            /* seed of the counter-based generator for start/fill vectors */
+} fd_lanczos_opts;
+
+/* Per-solve report (host memory). */
+typedef struct fd_lanczos_info {
+  int32_t restarts;         /* restart cycles run */
+  int32_t block_matvecs;    /* applications of M to a block of b vectors */
+  int32_t nconv;            /* leading Ritz pairs with residual <= tol */
+  int32_t wall;             /* 1 when g_P <= kappa_P * eta_fp32 (Sec. 2.3, eq. perronwall) */
+  double gap_perron;        /* g_P = (theta_0 - theta_1) / |theta_0| */
+  double s_off;             /* S_off = sum_{i != j} K_ij = sum(q) - N (Sec. 2.3) */
+  double max_residual;      /* largest residual among the k returned pairs */
+  double seconds;           /* wall time of the call, host clock */
+} fd_lanczos_info;
+
+/* Fill *opts with the defaults listed above. */
+void fd_lanczos_default_opts(fd_lanczos_opts* opts);
+
+/* Bytes of workspace an entry point needs.
+ *   op = FD_OP_KERNEL_MATMUL: Nr output rows, Nc columns, D, b; k ignored.
+ *   op = FD_OP_DEGREE:        Nr = Nc = N, D; b, k ignored.
+ *   op = FD_OP_BLOCK_LANCZOS: Nr = Nc = N, D, b, k, opts (NULL = defaults).
+ *   op = FD_OP_CONTINUATION:  Nr = Nc = largest n of the schedule, D, b, k, opts.
+ * Returns 0 for arguments the entry point would reject. */
+size_t fd_workspace_size(fd_op op, int64_t Nr, int64_t Nc, int64_t D, int64_t b, int64_t k,
+                         const fd_lanczos_opts* opts);
+
+/* Fused Gaussian-kernel block product (Sec. 2.1 eq. matmat; Sec. 2.2 eq. tiled_rbf):
+ *
+ *     Y = diag(sl) K(Xr, Xc) diag(sr) V,   K_ij = exp(-beta ||xr_i - xc_j||^2),
+ *
+ * evaluated tile by tile in the Gram form of eq. rbf_gram (row norms plus a
+ * matrix-core contraction), exponentiated and multiplied into V on chip.
+ *   Xr  : Nr x D rows (device, dtype xt, ldx);  Xc : Nc x D columns (same D, ldx, xt).
+ *         When Xr == Xc and Nr == Nc the diagonal K_ii is taken as exactly 1.
+ *   beta: >= 0 (beta = 0 gives K = ones).
+ *   sl  : Nr scale of output rows, or NULL for ones.  sr : Nc scale of V rows, or NULL.
+ *   V   : Nc x b (device, ldv >= b), 1 <= b <= 64.   Y : Nr x b output (device, ldy >= b).
+ *         Y must not overlap V, sl, sr or X.
+ * Float32 accumulation.  Deterministic: repeated calls give identical bits. */
+fd_status fd_kernel_matmul(const void* Xr, int64_t Nr, const void* Xc, int64_t Nc, int64_t D,
+                           int64_t ldx, fd_dtype xt, float beta, const float* sl, const float* sr,
+                           const float* V, int64_t b, int64_t ldv, float* Y, int64_t ldy,
+                           void* ws, size_t ws_bytes, void* stream);
+
+/* Normalisation passes (Sec. 2.1, the two "entry fee" applications):
+ *     q = K 1;  w = q^-alpha;  d = w * (K w);  s = w * d^-1/2,
+ * so that M = diag(s) K diag(s) and P = diag(d)^-1 diag(w) K diag(w).
+ * With alpha = 0 the second application is skipped (d = q).
+ *   X: N x D (device).  beta > 0.  0 <= alpha <= 1.
+ *   q, d, s: N-vectors (device) or NULL each.
+ *   s_off: one double (device) receiving sum(q) - N = sum_{i != j} K_ij (Sec. 2.3), or NULL. */
+fd_status fd_degree(const void* X, fd_dtype xt, int64_t N, int64_t D, int64_t ldx, float beta,
+                    float alpha, float* q, float* d, float* s, double* s_off, void* ws,
+                    size_t ws_bytes, void* stream);
+
+/* Top-k eigenpairs of M = diag(s) K diag(s) by thick-restart block Lanczos
+ * (Sec. 2.3, first paragraph; Sec. 2.1 eq. symmetric), including the Perron
+ * pair theta_0 = 1.  Computes the normalisation itself (fd_degree) and then
+ * applies M to blocks of b vectors, one fused product per block.
+ *   X: N x D (device).  beta > 0, 0 <= alpha <= 1, 1 <= b <= 64, 1 <= k <= N.
+ *   V0: optional warm start, N x k0 (device, ldv0 >= k0); NULL or k0 = 0 for a
+ *       seeded random start.  Interpreted as Markov right eigenvectors psi
+ *       (warm_is_psi = 1: converted with the new d^1/2) or as eigenvectors of M.
+ *   evals: k doubles (host), descending.  evecs: N x k (device, ld k) orthonormal
+ *       eigenvectors phi of M.  psi: N x k (device, ld k) Markov right eigenvectors
+ *       d^-1/2 phi (last paragraph of Sec. 2.3), or NULL.
+ *   residuals: k doubles (host) or NULL.  info: host report or NULL.
+ * Returns FD_ERR_NOT_CONVERGED (outputs valid, info->nconv < k) when the restart
+ * or product budget runs out. */
+fd_status fd_block_lanczos(const void* X, fd_dtype xt, int64_t N, int64_t D, int64_t ldx,
+                           float beta, float alpha, int64_t b, int64_t k, const float* V0,
+                           int64_t k0, int64_t ldv0, int32_t warm_is_psi,
+                           const fd_lanczos_opts* opts, double* evals, float* evecs, float* psi,
+                           double* residuals, fd_lanczos_info* info, void* ws, size_t ws_bytes,
+                           void* stream);
+
+/* Warm-started (n, beta) ladder (Sec. 1, last paragraph; Sec. 2.3, dyadic
+ * continuation with warm starts and the Perron wall of eq. perronwall).
+ * Step t solves for the top-k eigenpairs on the prefix X[0:n_t] at beta_t.
+ * Its start is the previous step's Markov eigenvectors psi: unchanged when
+ * n_t equals the previous n, extended by the Nystrom formula (one rectangular
+ * fused product over the previous prefix) when n_t grows; when n_t grows the
+ * start is taken from the last step solved at n_{t-1} whose beta equals beta_t
+ * if one exists, else the previous step.
+ *   n_steps: nsteps prefix sizes (host), non-decreasing, 2 <= n_t <= N.
+ *   beta_steps: nsteps bandwidths (host), > 0.
+ *   V0/k0: optional warm start for step 0 (Markov form, N x k0 device) or NULL.
+ *   evals: nsteps x k doubles (host).  evecs: n_last x k (device) eigenvectors of M
+ *   at the final step.  psi: n_last x k Markov eigenvectors at the final step or NULL.
+ *   per_step: nsteps reports (host) or NULL.
+ *   stop_at_wall: when non-zero, stop after the first step whose Perron gap is at or
+ *   below kappa_P * eta_fp32 and return FD_ERR_PERRON_WALL; evals of the steps run
+ *   so far are valid and *steps_done tells how many ran.
+ *   steps_done: host int64 or NULL. */
+fd_status fd_continuation(const void* X, fd_dtype xt, int64_t N, int64_t D, int64_t ldx,
+                          float alpha, const int64_t* n_steps, const float* beta_steps,
+                          int64_t nsteps, int64_t b, int64_t k, const float* V0, int64_t k0,
+                          int64_t ldv0, const fd_lanczos_opts* opts, double* evals,
+                          float* evecs, float* psi, fd_lanczos_info* per_step,
+                          int32_t stop_at_wall, int64_t* steps_done, void* ws, size_t ws_bytes,
+                          void* stream);
+
+/* ---- diagnostics: kernel timing with HIP events ----
+ * When enabled, every launch of the fused product kernel (FD_KERNEL_PRODUCT)
+ * and of the row-sum kernel of the normalisation passes (FD_KERNEL_ROWSUM) is
+ * bracketed by two HIP events recorded on the launch stream (at most 65536
+ * brackets per kind are kept; later launches are not timed).
+ * fd_profile_read waits for the recorded events, returns the summed kernel time
+ * in milliseconds (host) and the number of timed launches (host), and clears
+ * the record of that kind. */
+typedef enum fd_kernel_kind { FD_KERNEL_PRODUCT = 0, FD_KERNEL_ROWSUM = 1 } fd_kernel_kind;
+void fd_profile_enable(int32_t on);
+fd_status fd_profile_read(fd_kernel_kind kind, double* total_ms, int64_t* launches);
+
+/* Thread-local message describing the last non-OK status ("" if none). */
+const char* fd_last_error(void);
+
+/* Static name of a status code. */
+const char* fd_status_string(fd_status s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FLASHDIFF_H */

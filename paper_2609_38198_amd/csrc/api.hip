@@ -1,0 +1,222 @@
+// C ABI entry points: argument validation, workspace carving and the
+// composition of the kernels into the operations declared in flashdiff.h.
+#include <cmath>
+#include <exception>
+#include <string>
+
+#include "fd_internal.hpp"
+#include "fd_solver.hpp"
+
+namespace fd {
+
+static thread_local std::string g_err;
+void set_error(const std::string& msg) { g_err = msg; }
+const char* get_error() { return g_err.c_str(); }
+
+template <class F>
+static fd_status guarded(F&& f) {
+  try {
+    f();
+    set_error("");
+    return FD_OK;
+  } catch (const Error& e) {
+    set_error(e.msg);
+    return e.status;
+  } catch (const std::exception& e) {
+    set_error(std::string("internal error: ") + e.what());
+    return FD_ERR_HIP;
+  } catch (...) {
+    set_error("internal error");
+    return FD_ERR_HIP;
+  }
+}
+
+constexpr int64_t MAX_POINTS = int64_t(1) << 30;
+
+void check_points(const void* X, fd_dtype xt, int64_t N, int64_t D, int64_t ldx,
+                  const char* what) {
+  FD_REQUIRE(X != nullptr, FD_ERR_INVALID_ARG, std::string(what) + " is NULL");
+  FD_REQUIRE(xt == FD_F32 || xt == FD_BF16, FD_ERR_INVALID_ARG, "unknown dtype");
+  FD_REQUIRE(N >= 1 && N <= MAX_POINTS, FD_ERR_INVALID_ARG,
+             std::string("number of points of ") + what + " out of range [1, 2^30]");
+  FD_REQUIRE(D >= 1, FD_ERR_INVALID_ARG, "D must be >= 1");
+  FD_REQUIRE(D <= MAX_D, FD_ERR_UNSUPPORTED, "D above 64 is not supported");
+  FD_REQUIRE(ldx >= D, FD_ERR_INVALID_ARG, "ldx must be >= D");
+}
+
+void check_workspace(const void* ws, size_t ws_bytes, size_t need) {
+  FD_REQUIRE(ws_bytes >= need, FD_ERR_WORKSPACE,
+             "workspace too small: need " + std::to_string(need) + " bytes, got " +
+                 std::to_string(ws_bytes));
+  FD_REQUIRE(need == 0 || ws != nullptr, FD_ERR_WORKSPACE, "workspace is NULL");
+  FD_REQUIRE((reinterpret_cast<uintptr_t>(ws) & 255) == 0, FD_ERR_WORKSPACE,
+             "workspace must be 256-byte aligned");
+}
+
+// ---------------------------------------------------------------- products
+
+ProductWs carve_product(Arena& a, int64_t Nr, int64_t Nc, int64_t D, int b) {
+  ProductWs w;
+  const int dp = padded_dim(D);
+  w.plan = plan_product(Nr, Nc, dp, b);
+  w.rows = carve_pack(a, Nr, dp, ROW_PAD);
+  w.cols = carve_pack(a, Nc, dp, TILE);
+  w.vp = a.fspan(size_t(w.cols.npad) * w.plan.ncb * 16);
+  if (w.plan.nsplit > 1) w.part = a.fspan(size_t(w.plan.nsplit) * w.rows.npad * w.plan.ncb * 16);
+  return w;
+}
+
+void product_apply(ProductWs& w, const float* sl, const float* sr, const float* V, int64_t ldv,
+                   int b, float* Y, int64_t ldy, bool diag, hipStream_t stream) {
+  launch_pack_v(V, w.cols.n, b, ldv, sr, w.plan.ncb, w.cols.npad, w.vp, stream);
+  launch_product(w.plan, w.rows, w.cols, w.vp, diag, sl, Y, ldy, b, w.part, stream);
+}
+
+// ---------------------------------------------------------------- degree
+
+DegreeWs carve_degree(Arena& a, int64_t N, int64_t D) {
+  DegreeWs w;
+  const int dp = padded_dim(D);
+  w.plan = plan_product(N, N, dp, 1);
+  w.rows = carve_pack(a, N, dp, ROW_PAD);
+  w.cols = carve_pack(a, N, dp, TILE);
+  w.wp = a.fspan(size_t(w.cols.npad) * 16);  // one float4 per lane per 16-point tile
+  w.q = a.take<float>(size_t(N));
+  w.t = a.take<float>(size_t(N));
+  w.w = a.take<float>(size_t(N));
+  if (w.plan.nsplit > 1) w.part = a.fspan(size_t(w.plan.nsplit) * w.rows.npad);
+  return w;
+}
+
+void degree_run(DegreeWs& w, const void* X, fd_dtype xt, int64_t N, int64_t D, int64_t ldx,
+                double beta, double alpha, float* q, float* d, float* s, double* s_off,
+                bool pack, hipStream_t stream) {
+  if (pack) {
+    launch_pack_points(X, xt, N, D, ldx, beta, true, w.rows, stream);
+    launch_pack_points(X, xt, N, D, ldx, beta, false, w.cols, stream);
+  }
+  float* qq = q != nullptr ? q : w.q;
+  launch_rowsum(w.plan, w.rows, w.cols, FSpan{}, true, qq, w.part, stream);
+  if (s_off != nullptr) launch_sum_minus_n(qq, N, s_off, stream);
+  if (alpha == 0.0) {
+    launch_degree_finish(qq, qq, N, 0.0, d, s, stream);
+    return;
+  }
+  launch_pow_neg(qq, N, alpha, w.w, stream);
+  launch_pack_w(w.w, N, w.cols.npad, w.wp, stream);
+  launch_rowsum(w.plan, w.rows, w.cols, w.wp, true, w.t, w.part, stream);
+  launch_degree_finish(qq, w.t, N, alpha, d, s, stream);
+}
+
+}  // namespace fd
+
+using namespace fd;
+
+extern "C" {
+
+const char* fd_last_error(void) { return get_error(); }
+
+const char* fd_status_string(fd_status s) {
+  switch (s) {
+    case FD_OK: return "FD_OK";
+    case FD_ERR_INVALID_ARG: return "FD_ERR_INVALID_ARG";
+    case FD_ERR_UNSUPPORTED: return "FD_ERR_UNSUPPORTED";
+    case FD_ERR_WORKSPACE: return "FD_ERR_WORKSPACE";
+    case FD_ERR_HIP: return "FD_ERR_HIP";
+    case FD_ERR_NOT_CONVERGED: return "FD_ERR_NOT_CONVERGED";
+    case FD_ERR_PERRON_WALL: return "FD_ERR_PERRON_WALL";
+  }
+  return "FD_UNKNOWN_STATUS";
+}
+
+void fd_lanczos_default_opts(fd_lanczos_opts* opts) {
+  if (opts == nullptr) return;
+  opts->tol = 1e-5;
+  opts->max_restarts = 200;
+  opts->max_basis_blocks = 0;
+  opts->keep = -1;
+  opts->max_matvecs = 0;
+  opts->reserved = 0;
+  opts->seed = 0x5eed;
+}
+
+size_t fd_workspace_size(fd_op op, int64_t Nr, int64_t Nc, int64_t D, int64_t b, int64_t k,
+                         const fd_lanczos_opts* opts) {
+  size_t out = 0;
+  fd_status st = guarded([&] {
+    Arena a;
+    a.measuring = true;
+    FD_REQUIRE(Nr >= 1 && Nr <= MAX_POINTS && D >= 1 && D <= MAX_D, FD_ERR_INVALID_ARG, "size");
+    switch (op) {
+      case FD_OP_KERNEL_MATMUL:
+        FD_REQUIRE(Nc >= 1 && Nc <= MAX_POINTS && b >= 1 && b <= MAX_B, FD_ERR_INVALID_ARG, "size");
+        carve_product(a, Nr, Nc, D, int(b));
+        break;
+      case FD_OP_DEGREE:
+        carve_degree(a, Nr, D);
+        break;
+      case FD_OP_BLOCK_LANCZOS:
+      case FD_OP_CONTINUATION: {
+        fd_lanczos_opts o;
+        fd_lanczos_default_opts(&o);
+        if (opts != nullptr) o = *opts;
+        FD_REQUIRE(b >= 1 && b <= MAX_B && k >= 1 && k <= Nr, FD_ERR_INVALID_ARG, "size");
+        carve_solver(a, Nr, D, int(b), int(k), o, op == FD_OP_CONTINUATION);
+        break;
+      }
+      default:
+        throw Error{FD_ERR_INVALID_ARG, "unknown op"};
+    }
+    out = a.used;
+  });
+  return st == FD_OK ? out : 0;
+}
+
+fd_status fd_kernel_matmul(const void* Xr, int64_t Nr, const void* Xc, int64_t Nc, int64_t D,
+                           int64_t ldx, fd_dtype xt, float beta, const float* sl, const float* sr,
+                           const float* V, int64_t b, int64_t ldv, float* Y, int64_t ldy,
+                           void* ws, size_t ws_bytes, void* stream) {
+  return guarded([&] {
+    check_points(Xr, xt, Nr, D, ldx, "Xr");
+    check_points(Xc, xt, Nc, D, ldx, "Xc");
+    FD_REQUIRE(std::isfinite(beta) && beta >= 0.f, FD_ERR_INVALID_ARG, "beta must be finite and >= 0");
+    FD_REQUIRE(V != nullptr && Y != nullptr, FD_ERR_INVALID_ARG, "V and Y must not be NULL");
+    FD_REQUIRE(b >= 1 && b <= MAX_B, FD_ERR_INVALID_ARG, "b must be in [1, 64]");
+    FD_REQUIRE(ldv >= b && ldy >= b, FD_ERR_INVALID_ARG, "ldv and ldy must be >= b");
+    Arena m;
+    m.measuring = true;
+    carve_product(m, Nr, Nc, D, int(b));
+    check_workspace(ws, ws_bytes, m.used);
+    Arena a;
+    a.base = static_cast<char*>(ws);
+    a.cap = ws_bytes;
+    ProductWs w = carve_product(a, Nr, Nc, D, int(b));
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    launch_pack_points(Xr, xt, Nr, D, ldx, beta, true, w.rows, st);
+    launch_pack_points(Xc, xt, Nc, D, ldx, beta, false, w.cols, st);
+    const bool diag = (Xr == Xc) && (Nr == Nc);
+    product_apply(w, sl, sr, V, ldv, int(b), Y, ldy, diag, st);
+  });
+}
+
+fd_status fd_degree(const void* X, fd_dtype xt, int64_t N, int64_t D, int64_t ldx, float beta,
+                    float alpha, float* q, float* d, float* s, double* s_off, void* ws,
+                    size_t ws_bytes, void* stream) {
+  return guarded([&] {
+    check_points(X, xt, N, D, ldx, "X");
+    FD_REQUIRE(std::isfinite(beta) && beta > 0.f, FD_ERR_INVALID_ARG, "beta must be finite and > 0");
+    FD_REQUIRE(alpha >= 0.f && alpha <= 1.f, FD_ERR_INVALID_ARG, "alpha must be in [0, 1]");
+    Arena m;
+    m.measuring = true;
+    carve_degree(m, N, D);
+    check_workspace(ws, ws_bytes, m.used);
+    Arena a;
+    a.base = static_cast<char*>(ws);
+    a.cap = ws_bytes;
+    DegreeWs w = carve_degree(a, N, D);
+    degree_run(w, X, xt, N, D, ldx, beta, alpha, q, d, s, s_off, true,
+               static_cast<hipStream_t>(stream));
+  });
+}
+
+}  // extern "C"

@@ -1,0 +1,125 @@
+// Internal declarations shared by the library's translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include <string>
+
+#include "flashdiff.h"
+
+namespace fd {
+
+// ---------------------------------------------------------------- errors
+void set_error(const std::string& msg);
+const char* get_error();
+
+struct Error {
+  fd_status status;
+  std::string msg;
+};
+
+#define FD_HIP_CHECK(expr)                                                               \
+  do {                                                                                   \
+    hipError_t e_ = (expr);                                                              \
+    if (e_ != hipSuccess)                                                                \
+      throw ::fd::Error{FD_ERR_HIP, std::string(#expr) + ": " + hipGetErrorString(e_)}; \
+  } while (0)
+
+#define FD_LAUNCH_CHECK() FD_HIP_CHECK(hipGetLastError())
+
+#define FD_REQUIRE(cond, status, msg)                 \
+  do {                                                \
+    if (!(cond)) throw ::fd::Error{(status), (msg)}; \
+  } while (0)
+
+// ---------------------------------------------------------------- workspace
+// A carved region of float32 elements.
+struct FSpan {
+  float* p = nullptr;
+  size_t n = 0;
+};
+
+inline void check_span(const FSpan& s, size_t need, const char* what) {
+  if (s.p == nullptr || s.n < need)
+    throw Error{FD_ERR_WORKSPACE, std::string("internal: region '") + what +
+                                      "' smaller than the extent its kernel touches"};
+}
+
+// Bump allocator over the caller's workspace (never allocates device memory).
+struct Arena {
+  char* base = nullptr;
+  size_t cap = 0;
+  size_t used = 0;
+  bool measuring = false;  // when true only counts bytes
+  template <class T>
+  T* take(size_t count) {
+    size_t bytes = (count * sizeof(T) + 255) & ~size_t(255);
+    size_t off = used;
+    used += bytes;
+    if (measuring) return nullptr;
+    if (used > cap) throw Error{FD_ERR_WORKSPACE, "workspace too small"};
+    return reinterpret_cast<T*>(base + off);
+  }
+  FSpan fspan(size_t count) { return FSpan{take<float>(count), count}; }
+};
+
+// ---------------------------------------------------------------- geometry
+constexpr int TILE = 16;          // points per MFMA tile
+constexpr int WG_THREADS = 256;   // four wave64 per workgroup
+constexpr int ROW_PAD = 256;      // row packs are padded to this many points
+
+inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+inline int64_t ceil_div(int64_t x, int64_t m) { return (x + m - 1) / m; }
+
+// Padded contraction width used for a feature dimension D (multiple of 4).
+int padded_dim(int64_t D);
+// Supported feature dimensions and block widths.
+constexpr int MAX_D = 64;
+constexpr int MAX_B = 64;
+
+// Packed operands of one point set, produced by pack_points.
+//   xp : [tiles][DP/4][64] contraction operand (scaled by `scale`)
+//   ap : [tiles][64][4]    a_j = -beta*log2(e)*||x_j||^2 in accumulator order
+//   ar : [npad]            a_i in plain order
+struct PointPack {
+  FSpan xp, ap, ar;
+  int64_t n = 0;      // real points
+  int64_t npad = 0;   // padded points
+  int dp = 0;         // padded contraction width
+};
+
+// Plan of one fused product / degree launch.
+struct KVPlan {
+  int dp = 0, ncb = 0, nib = 0;
+  int64_t njb = 0;        // column tiles of 16
+  int64_t nrt = 0;        // row tiles of 64*nib
+  int nsplit = 1;         // column splits
+  int64_t jb_per_split = 0;
+};
+
+KVPlan plan_product(int64_t Nr, int64_t Nc, int dp, int b);
+
+// Workspace carving helpers (size when arena.measuring).
+PointPack carve_pack(Arena& a, int64_t n, int dp, int64_t pad);
+
+// Launchers (enqueue on stream; throw Error on failure).
+void launch_pack_points(const void* X, fd_dtype xt, int64_t n, int64_t D, int64_t ldx,
+                        double beta, bool row_side, PointPack& out, hipStream_t stream);
+void launch_pack_v(const float* V, int64_t n, int64_t b, int64_t ldv, const float* sr,
+                   int ncb, int64_t npad, FSpan vp, hipStream_t stream);
+void launch_pack_w(const float* w, int64_t n, int64_t npad, FSpan wp, hipStream_t stream);
+// Y = diag(sl) K diag(sr) V from packed operands (V packed with sr applied).
+void launch_product(const KVPlan& p, const PointPack& rows, const PointPack& cols, FSpan vp,
+                    bool diag, const float* sl, float* Y, int64_t ldy, int b, FSpan part,
+                    hipStream_t stream);
+// out = K w (wp.p == NULL: w = 1).
+void launch_rowsum(const KVPlan& p, const PointPack& rows, const PointPack& cols, FSpan wp,
+                   bool diag, float* out, FSpan part, hipStream_t stream);
+void launch_degree_finish(const float* q, const float* t, int64_t n, double alpha, float* d,
+                          float* s, hipStream_t stream);
+void launch_pow_neg(const float* q, int64_t n, double alpha, float* w, hipStream_t stream);
+void launch_sum_minus_n(const float* q, int64_t n, double* out, hipStream_t stream);
+
+}  // namespace fd

@@ -1,0 +1,608 @@
+// Fused Gaussian-kernel products on gfx950 matrix cores (float32 path).
+//
+// Operation (FlashDiffusion Sec. 2.1 eq. matmat, Sec. 2.2 eq. tiled_rbf):
+//   Y_I = diag(sl_I) * sum_J exp(-beta * (r_I 1^T + 1 r_J^T - 2 X_I X_J^T)) * (sr_J * V_J)
+// with r the squared row norms (Gram form, eq. rbf_gram).  The N x N kernel
+// matrix is never stored: each 16 x 16 tile of it lives in four registers of
+// one wave and is consumed by the next matrix-core instruction.
+//
+// Register-level fusion.  The exponent tile is computed transposed,
+//   T^T[j][i] = a_i + a_j + sum_k xa[j][k] * xb[i][k],
+//   a = -beta*log2(e)*r,  xa = x,  xb = 2*beta*log2(e)*x,
+// with v_mfma_f32_16x16x4_f32 taking A = point tile J and B = point tile I.
+// Its accumulator gives lane (g = lane/16, p = lane%16) the entries
+// T^T[4g + r][p], r = 0..3.  After k = exp2(min(t, 0)) those four values are,
+// unchanged, the A operands of four further 16x16x4 MFMAs that contract over j
+// (A[m = p][kk = g] = K[i = p][j = 4g + r]); the V tile is pre-packed so that
+// its B operand for instruction r is V[4g + r][c].  No LDS round trip and no
+// cross-lane movement is needed between the two contractions.
+//
+// Operands are pre-packed in HBM in exactly the per-lane order of the MFMA
+// operands, so every load is a fully coalesced 256-byte (or 1-KiB float4)
+// wave load that the L1/L2 serve to all row tiles streaming the same columns.
+//
+// Accuracy: accumulation is float32 with a two-level sum (a fresh accumulator
+// per chunk of 1024 columns, added into a running total), which keeps the
+// rounding growth at about sqrt(chunk) + sqrt(N/chunk) units.  When rows and
+// columns are the same point set the diagonal exponent is set to its exact
+// value 0 (K_ii = 1).
+#include <hip/hip_runtime.h>
+
+#include "fd_internal.hpp"
+#include "fd_profile.hpp"
+
+namespace fd {
+
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+constexpr double LOG2E = 1.4426950408889634073599;
+constexpr int CHUNK_TILES = 64;  // column tiles per partial accumulator
+
+int padded_dim(int64_t D) {
+  static const int dims[] = {4, 8, 12, 16, 24, 32, 48, 64};
+  for (int d : dims)
+    if (D <= d) return d;
+  return 0;
+}
+
+PointPack carve_pack(Arena& a, int64_t n, int dp, int64_t pad) {
+  PointPack p;
+  p.n = n;
+  p.npad = round_up(n, pad);
+  p.dp = dp;
+  p.xp = a.fspan(size_t(p.npad) * dp);
+  p.ap = a.fspan(size_t(p.npad) * 16);  // [tiles][64][4]: 16 floats per point
+  p.ar = a.fspan(size_t(p.npad));
+  return p;
+}
+
+// Workgroups of one dispatch are spread over the eight XCDs round-robin by
+// id.  Re-number them so that each XCD owns a contiguous block of logical
+// work items (same column split, hence a shared working set in its L2).
+__device__ __forceinline__ int xcd_remap(int w, int total) {
+  if ((total & 7) != 0) return w;
+  const int per = total >> 3;
+  return (w & 7) * per + (w >> 3);
+}
+
+// ------------------------------------------------------------------ packing
+
+__device__ __forceinline__ float load_x(const float* X, int64_t idx) { return X[idx]; }
+__device__ __forceinline__ float load_x(const uint16_t* X, int64_t idx) {
+  return __uint_as_float(uint32_t(X[idx]) << 16);
+}
+
+template <typename TIn>
+__global__ void pack_points_kernel(const TIn* __restrict__ X, int64_t n, int D, int64_t ldx,
+                                   double beta_log2e, double scale, float* __restrict__ xp,
+                                   float* __restrict__ ap, float* __restrict__ ar, int64_t npad,
+                                   int dp) {
+  const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i >= npad) return;
+  const int S = dp / 4;
+  const int64_t tile = i / TILE;
+  const int p = int(i % TILE);
+  float* dst = xp + tile * S * 64;
+  double r = 0.0;
+  for (int k = 0; k < dp; ++k) {
+    float v = 0.f;
+    if (i < n && k < D) {
+      const double x = double(load_x(X, i * ldx + k));
+      r += x * x;
+      v = float(x * scale);
+    }
+    dst[(k >> 2) * 64 + (k & 3) * 16 + p] = v;
+  }
+  // padded points get a huge negative offset: their kernel values are exactly 0,
+  // also in the unit-weight row sums where no zero V row masks them
+  const float a = (i < n) ? float(-beta_log2e * r) : -1e30f;
+  ar[i] = a;
+  if (ap != nullptr) {
+    // accumulator order: lane 16g+q holds rows j = 4g + r of the tile
+    const int g = p >> 2, rr = p & 3;
+    float* base = ap + (tile * 64 + 16 * g) * 4 + rr;
+    for (int q = 0; q < 16; ++q) base[q * 4] = a;
+  }
+}
+
+__global__ void pack_v_kernel(const float* __restrict__ V, int64_t n, int b, int64_t ldv,
+                              const float* __restrict__ sr, int ncb, int64_t ntiles,
+                              floatx4* __restrict__ vp) {
+  const int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (idx >= ntiles * ncb * 64) return;
+  const int lane = int(idx & 63);
+  const int cb = int((idx >> 6) % ncb);
+  const int64_t jb = idx / (64 * ncb);
+  const int g = lane >> 4, p = lane & 15;
+  const int c = cb * 16 + p;
+  floatx4 out;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int64_t j = jb * TILE + 4 * g + r;
+    float v = 0.f;
+    if (j < n && c < b) {
+      v = V[j * ldv + c];
+      if (sr != nullptr) v *= sr[j];
+    }
+    out[r] = v;
+  }
+  vp[idx] = out;
+}
+
+__global__ void pack_w_kernel(const float* __restrict__ w, int64_t n, int64_t ntiles,
+                              floatx4* __restrict__ wp) {
+  const int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (idx >= ntiles * 64) return;
+  const int lane = int(idx & 63);
+  const int64_t jb = idx >> 6;
+  const int g = lane >> 4;
+  floatx4 out;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int64_t j = jb * TILE + 4 * g + r;
+    out[r] = (j < n) ? w[j] : 0.f;
+  }
+  wp[idx] = out;
+}
+
+// ------------------------------------------------------------------ products
+
+// One workgroup = 4 waves; wave w owns row tiles [ib0, ib0 + NIB) of 16 rows.
+// Column tiles [jb_begin, jb_end) of the workgroup's split are streamed.
+template <int DP, int NCB, int NIB>
+__global__ __launch_bounds__(WG_THREADS) void product_f32_kernel(
+    const float* __restrict__ xa, const floatx4* __restrict__ aj, const floatx4* __restrict__ vp,
+    const float* __restrict__ xb, const float* __restrict__ ar, int64_t nrt, int64_t njb,
+    int64_t jb_per_split, int diag, const float* __restrict__ sl, float* __restrict__ Y,
+    int64_t ldy, int64_t Nr, int b, float* __restrict__ part, int64_t nrpad) {
+  constexpr int S = DP / 4;
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int wr = xcd_remap(blockIdx.x, gridDim.x);
+  const int64_t split = wr / nrt;
+  const int64_t rt = wr % nrt;
+  const int64_t ib0 = (rt * 4 + wave) * NIB;
+  const int64_t jb_begin = split * jb_per_split;
+  const int64_t jb_end = min(njb, jb_begin + jb_per_split);
+
+  float xbr[NIB][S];
+  float ai[NIB];
+#pragma unroll
+  for (int ib = 0; ib < NIB; ++ib) {
+#pragma unroll
+    for (int s = 0; s < S; ++s) xbr[ib][s] = xb[((ib0 + ib) * S + s) * 64 + lane];
+    ai[ib] = ar[(ib0 + ib) * TILE + (lane & 15)];
+  }
+
+  floatx4 acc[NIB][NCB];
+  floatx4 tot[NIB][NCB];
+#pragma unroll
+  for (int ib = 0; ib < NIB; ++ib)
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) {
+      acc[ib][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
+      tot[ib][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
+    }
+
+  const int g = lane >> 4, p = lane & 15;
+  int chunk = 0;
+  for (int64_t jb = jb_begin; jb < jb_end; ++jb) {
+    float xar[S];
+#pragma unroll
+    for (int s = 0; s < S; ++s) xar[s] = xa[(jb * S + s) * 64 + lane];
+    const floatx4 ajr = aj[jb * 64 + lane];
+    floatx4 vr[NCB];
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) vr[cb] = vp[(jb * NCB + cb) * 64 + lane];
+
+#pragma unroll
+    for (int ib = 0; ib < NIB; ++ib) {
+      floatx4 t;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) t[r] = ai[ib] + ajr[r];
+#pragma unroll
+      for (int s = 0; s < S; ++s)
+        t = __builtin_amdgcn_mfma_f32_16x16x4f32(xar[s], xbr[ib][s], t, 0, 0, 0);
+      if (diag && jb == ib0 + ib) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (4 * g + r == p) t[r] = 0.f;
+      }
+      float kk[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) kk[r] = __builtin_amdgcn_exp2f(fminf(t[r], 0.f));
+#pragma unroll
+      for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          acc[ib][cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(kk[r], vr[cb][r], acc[ib][cb], 0, 0, 0);
+    }
+    if (++chunk == CHUNK_TILES) {
+      chunk = 0;
+#pragma unroll
+      for (int ib = 0; ib < NIB; ++ib)
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb) {
+          tot[ib][cb] += acc[ib][cb];
+          acc[ib][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
+        }
+    }
+  }
+
+#pragma unroll
+  for (int ib = 0; ib < NIB; ++ib)
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) {
+      const floatx4 v = tot[ib][cb] + acc[ib][cb];
+      const int c = cb * 16 + p;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int64_t i = (ib0 + ib) * TILE + 4 * g + e;
+        if (part != nullptr) {
+          part[(split * nrpad + i) * (NCB * 16) + c] = v[e];
+        } else if (i < Nr && c < b) {
+          Y[i * ldy + c] = (sl != nullptr) ? v[e] * sl[i] : v[e];
+        }
+      }
+    }
+}
+
+// Row sums sum_j K_ij w_j (b = 1, the normalisation passes): the same
+// exponent tiles, reduced on the vector ALUs instead of a second MFMA.
+template <int DP, int NIB, bool UNIT>
+__global__ __launch_bounds__(WG_THREADS) void rowsum_f32_kernel(
+    const float* __restrict__ xa, const floatx4* __restrict__ aj, const floatx4* __restrict__ wp,
+    const float* __restrict__ xb, const float* __restrict__ ar, int64_t nrt, int64_t njb,
+    int64_t jb_per_split, int diag, float* __restrict__ out, int64_t Nr,
+    float* __restrict__ part, int64_t nrpad) {
+  constexpr int S = DP / 4;
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int wr = xcd_remap(blockIdx.x, gridDim.x);
+  const int64_t split = wr / nrt;
+  const int64_t rt = wr % nrt;
+  const int64_t ib0 = (rt * 4 + wave) * NIB;
+  const int64_t jb_begin = split * jb_per_split;
+  const int64_t jb_end = min(njb, jb_begin + jb_per_split);
+
+  float xbr[NIB][S];
+  float ai[NIB];
+#pragma unroll
+  for (int ib = 0; ib < NIB; ++ib) {
+#pragma unroll
+    for (int s = 0; s < S; ++s) xbr[ib][s] = xb[((ib0 + ib) * S + s) * 64 + lane];
+    ai[ib] = ar[(ib0 + ib) * TILE + (lane & 15)];
+  }
+  float acc[NIB], tot[NIB];
+#pragma unroll
+  for (int ib = 0; ib < NIB; ++ib) acc[ib] = tot[ib] = 0.f;
+
+  const int g = lane >> 4, p = lane & 15;
+  int chunk = 0;
+  for (int64_t jb = jb_begin; jb < jb_end; ++jb) {
+    float xar[S];
+#pragma unroll
+    for (int s = 0; s < S; ++s) xar[s] = xa[(jb * S + s) * 64 + lane];
+    const floatx4 ajr = aj[jb * 64 + lane];
+    floatx4 wr4 = floatx4{1.f, 1.f, 1.f, 1.f};
+    if (!UNIT) wr4 = wp[jb * 64 + lane];
+#pragma unroll
+    for (int ib = 0; ib < NIB; ++ib) {
+      floatx4 t;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) t[r] = ai[ib] + ajr[r];
+#pragma unroll
+      for (int s = 0; s < S; ++s)
+        t = __builtin_amdgcn_mfma_f32_16x16x4f32(xar[s], xbr[ib][s], t, 0, 0, 0);
+      if (diag && jb == ib0 + ib) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (4 * g + r == p) t[r] = 0.f;
+      }
+      float sum = 0.f;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float k = __builtin_amdgcn_exp2f(fminf(t[r], 0.f));
+        sum = UNIT ? sum + k : fmaf(k, wr4[r], sum);
+      }
+      acc[ib] += sum;
+    }
+    if (++chunk == CHUNK_TILES) {
+      chunk = 0;
+#pragma unroll
+      for (int ib = 0; ib < NIB; ++ib) {
+        tot[ib] += acc[ib];
+        acc[ib] = 0.f;
+      }
+    }
+  }
+#pragma unroll
+  for (int ib = 0; ib < NIB; ++ib) {
+    float v = tot[ib] + acc[ib];
+    // lanes p, p+16, p+32, p+48 hold partial sums of row p
+    v += __shfl_xor(v, 16);
+    v += __shfl_xor(v, 32);
+    if (g == 0) {
+      const int64_t i = (ib0 + ib) * TILE + p;
+      if (part != nullptr)
+        part[split * nrpad + i] = v;
+      else if (i < Nr)
+        out[i] = v;
+    }
+  }
+}
+
+__global__ void reduce_product_kernel(const float* __restrict__ part, int nsplit, int64_t nrpad,
+                                      int width, const float* __restrict__ sl,
+                                      float* __restrict__ Y, int64_t ldy, int64_t Nr, int b) {
+  const int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (idx >= Nr * b) return;
+  const int64_t i = idx / b;
+  const int c = int(idx % b);
+  double s = 0.0;
+  for (int k = 0; k < nsplit; ++k) s += double(part[(k * nrpad + i) * width + c]);
+  if (sl != nullptr) s *= double(sl[i]);
+  Y[i * ldy + c] = float(s);
+}
+
+__global__ void reduce_rowsum_kernel(const float* __restrict__ part, int nsplit, int64_t nrpad,
+                                     float* __restrict__ out, int64_t Nr) {
+  const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i >= Nr) return;
+  double s = 0.0;
+  for (int k = 0; k < nsplit; ++k) s += double(part[k * nrpad + i]);
+  out[i] = float(s);
+}
+
+// w = q^-alpha
+__global__ void pow_neg_kernel(const float* __restrict__ q, int64_t n, double alpha,
+                               float* __restrict__ w) {
+  const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i < n) w[i] = float(pow(double(q[i]), -alpha));
+}
+
+// d = w * t, s = w * d^-1/2 (w = q^-alpha recomputed in double from q)
+__global__ void degree_finish_kernel(const float* __restrict__ q, const float* __restrict__ t,
+                                     int64_t n, double alpha, float* __restrict__ d,
+                                     float* __restrict__ s) {
+  const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const double w = pow(double(q[i]), -alpha);
+  const double dd = w * double(t[i]);
+  if (d != nullptr) d[i] = float(dd);
+  if (s != nullptr) s[i] = float(w / sqrt(dd));
+}
+
+// sum(q) - n in double, one workgroup, fixed order (deterministic)
+__global__ __launch_bounds__(1024) void sum_minus_n_kernel(const float* __restrict__ q, int64_t n,
+                                                            double* __restrict__ out) {
+  __shared__ double red[1024];
+  double s = 0.0;
+  for (int64_t i = threadIdx.x; i < n; i += 1024) s += double(q[i]);
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int w = 512; w > 0; w >>= 1) {
+    if (int(threadIdx.x) < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) *out = red[0] - double(n);
+}
+
+// ------------------------------------------------------------------ host side
+
+KVPlan plan_product(int64_t Nr, int64_t Nc, int dp, int b) {
+  KVPlan p;
+  p.dp = dp;
+  p.ncb = int(ceil_div(b, 16));
+  p.nib = 4;
+  p.njb = ceil_div(Nc, TILE);
+  const int64_t rows_per_wg = 4 * p.nib * TILE;
+  p.nrt = ceil_div(round_up(Nr, ROW_PAD), rows_per_wg);
+  // aim for >= 2048 workgroups (eight per CU), keep >= 8 column tiles per split
+  const int64_t target = 2048;
+  int64_t ns = std::max<int64_t>(1, ceil_div(target, p.nrt));
+  ns = std::min<int64_t>(ns, std::max<int64_t>(1, p.njb / 8));
+  ns = std::min<int64_t>(ns, 64);
+  p.jb_per_split = ceil_div(p.njb, ns);
+  p.nsplit = int(ceil_div(p.njb, p.jb_per_split));
+  return p;
+}
+
+static inline unsigned blocks_for(int64_t n, int t) { return unsigned(ceil_div(n, t)); }
+
+// Extents (in floats) the kernels touch, checked against the carved regions
+// before every launch.
+static inline size_t xp_extent(int64_t tiles, int dp) { return size_t(tiles) * dp * TILE; }
+static inline size_t lane4_extent(int64_t tiles, int groups) {
+  return size_t(tiles) * groups * 64 * 4;
+}
+
+void launch_pack_points(const void* X, fd_dtype xt, int64_t n, int64_t D, int64_t ldx,
+                        double beta, bool row_side, PointPack& out, hipStream_t stream) {
+  const double bl = beta * LOG2E;
+  // rows carry the factor 2*beta*log2(e) of the cross term; columns are plain
+  const double scale = row_side ? 2.0 * bl : 1.0;
+  const bool with_ap = !row_side;
+  FD_REQUIRE(out.npad % TILE == 0 && out.npad >= n && out.dp % 4 == 0 && D <= out.dp,
+             FD_ERR_INVALID_ARG, "internal: bad point pack geometry");
+  check_span(out.xp, xp_extent(out.npad / TILE, out.dp), "point pack");
+  check_span(out.ar, size_t(out.npad), "row offsets");
+  if (with_ap) check_span(out.ap, lane4_extent(out.npad / TILE, 1), "column offsets");
+  const unsigned grid = blocks_for(out.npad, 256);
+  float* ap = with_ap ? out.ap.p : nullptr;
+  if (xt == FD_F32)
+    hipLaunchKernelGGL(pack_points_kernel<float>, dim3(grid), dim3(256), 0, stream,
+                       static_cast<const float*>(X), n, int(D), ldx, bl, scale, out.xp.p, ap,
+                       out.ar.p, out.npad, out.dp);
+  else
+    hipLaunchKernelGGL(pack_points_kernel<uint16_t>, dim3(grid), dim3(256), 0, stream,
+                       static_cast<const uint16_t*>(X), n, int(D), ldx, bl, scale, out.xp.p, ap,
+                       out.ar.p, out.npad, out.dp);
+  FD_LAUNCH_CHECK();
+}
+
+void launch_pack_v(const float* V, int64_t n, int64_t b, int64_t ldv, const float* sr, int ncb,
+                   int64_t npad, FSpan vp, hipStream_t stream) {
+  FD_REQUIRE(npad % TILE == 0 && npad >= n && b <= ncb * 16, FD_ERR_INVALID_ARG,
+             "internal: bad V pack geometry");
+  const int64_t ntiles = npad / TILE;
+  check_span(vp, lane4_extent(ntiles, ncb), "V pack");
+  const int64_t total = ntiles * ncb * 64;
+  hipLaunchKernelGGL(pack_v_kernel, dim3(blocks_for(total, 256)), dim3(256), 0, stream, V, n,
+                     int(b), ldv, sr, ncb, ntiles, reinterpret_cast<floatx4*>(vp.p));
+  FD_LAUNCH_CHECK();
+}
+
+void launch_pack_w(const float* w, int64_t n, int64_t npad, FSpan wp, hipStream_t stream) {
+  FD_REQUIRE(npad % TILE == 0 && npad >= n, FD_ERR_INVALID_ARG, "internal: bad w pack geometry");
+  const int64_t ntiles = npad / TILE;
+  check_span(wp, lane4_extent(ntiles, 1), "weight pack");
+  hipLaunchKernelGGL(pack_w_kernel, dim3(blocks_for(ntiles * 64, 256)), dim3(256), 0, stream, w,
+                     n, ntiles, reinterpret_cast<floatx4*>(wp.p));
+  FD_LAUNCH_CHECK();
+}
+
+// Geometry shared by the product and row-sum launches.
+static void check_tiles(const KVPlan& p, const PointPack& rows, const PointPack& cols) {
+  const int64_t row_tiles = p.nrt * 4 * p.nib;  // 16-row tiles the grid reads
+  FD_REQUIRE(rows.dp == p.dp && cols.dp == p.dp, FD_ERR_INVALID_ARG, "internal: pack width");
+  FD_REQUIRE(row_tiles * TILE == rows.npad, FD_ERR_INVALID_ARG,
+             "internal: row pack not padded to the workgroup tile");
+  FD_REQUIRE(p.njb * TILE <= cols.npad && cols.n <= p.njb * TILE, FD_ERR_INVALID_ARG,
+             "internal: column pack does not match the plan");
+  FD_REQUIRE(p.nsplit >= 1 && (p.nsplit - 1) * p.jb_per_split < p.njb &&
+                 p.nsplit * p.jb_per_split >= p.njb,
+             FD_ERR_INVALID_ARG, "internal: bad column split");
+  check_span(rows.xp, xp_extent(row_tiles, p.dp), "row pack");
+  check_span(rows.ar, size_t(rows.npad), "row offsets");
+  check_span(cols.xp, xp_extent(p.njb, p.dp), "column pack");
+  check_span(cols.ap, lane4_extent(p.njb, 1), "column offsets");
+}
+
+template <int DP, int NCB>
+static void product_dispatch_nib(const KVPlan& p, const PointPack& rows, const PointPack& cols,
+                                 const float* vp, bool diag, const float* sl, float* Y,
+                                 int64_t ldy, int b, float* part, hipStream_t stream) {
+  const unsigned grid = unsigned(p.nrt * p.nsplit);
+  ProfScope prof(FD_KERNEL_PRODUCT, stream);
+  hipLaunchKernelGGL((product_f32_kernel<DP, NCB, 4>), dim3(grid), dim3(WG_THREADS), 0, stream,
+                     cols.xp.p, reinterpret_cast<const floatx4*>(cols.ap.p),
+                     reinterpret_cast<const floatx4*>(vp), rows.xp.p, rows.ar.p, p.nrt, p.njb,
+                     p.jb_per_split, int(diag), sl, Y, ldy, rows.n, b, part, rows.npad);
+  FD_LAUNCH_CHECK();
+}
+
+template <int DP>
+static void product_dispatch_ncb(const KVPlan& p, const PointPack& rows, const PointPack& cols,
+                                 const float* vp, bool diag, const float* sl, float* Y,
+                                 int64_t ldy, int b, float* part, hipStream_t stream) {
+  switch (p.ncb) {
+    case 1: return product_dispatch_nib<DP, 1>(p, rows, cols, vp, diag, sl, Y, ldy, b, part, stream);
+    case 2: return product_dispatch_nib<DP, 2>(p, rows, cols, vp, diag, sl, Y, ldy, b, part, stream);
+    case 3: return product_dispatch_nib<DP, 3>(p, rows, cols, vp, diag, sl, Y, ldy, b, part, stream);
+    case 4: return product_dispatch_nib<DP, 4>(p, rows, cols, vp, diag, sl, Y, ldy, b, part, stream);
+  }
+  throw Error{FD_ERR_UNSUPPORTED, "block width above 64"};
+}
+
+void launch_product(const KVPlan& p, const PointPack& rows, const PointPack& cols, FSpan vp,
+                    bool diag, const float* sl, float* Y, int64_t ldy, int b, FSpan part,
+                    hipStream_t stream) {
+  check_tiles(p, rows, cols);
+  FD_REQUIRE(b >= 1 && b <= p.ncb * 16 && p.nib == 4, FD_ERR_INVALID_ARG,
+             "internal: block width does not match the plan");
+  check_span(vp, lane4_extent(p.njb, p.ncb), "V pack");
+  float* pp = nullptr;
+  if (p.nsplit > 1) {
+    check_span(part, size_t(p.nsplit) * rows.npad * p.ncb * 16, "partial products");
+    pp = part.p;
+  }
+  switch (p.dp) {
+    case 4: product_dispatch_ncb<4>(p, rows, cols, vp.p, diag, sl, Y, ldy, b, pp, stream); break;
+    case 8: product_dispatch_ncb<8>(p, rows, cols, vp.p, diag, sl, Y, ldy, b, pp, stream); break;
+    case 12: product_dispatch_ncb<12>(p, rows, cols, vp.p, diag, sl, Y, ldy, b, pp, stream); break;
+    case 16: product_dispatch_ncb<16>(p, rows, cols, vp.p, diag, sl, Y, ldy, b, pp, stream); break;
+    case 24: product_dispatch_ncb<24>(p, rows, cols, vp.p, diag, sl, Y, ldy, b, pp, stream); break;
+    case 32: product_dispatch_ncb<32>(p, rows, cols, vp.p, diag, sl, Y, ldy, b, pp, stream); break;
+    case 48: product_dispatch_ncb<48>(p, rows, cols, vp.p, diag, sl, Y, ldy, b, pp, stream); break;
+    case 64: product_dispatch_ncb<64>(p, rows, cols, vp.p, diag, sl, Y, ldy, b, pp, stream); break;
+    default: throw Error{FD_ERR_UNSUPPORTED, "feature dimension above 64"};
+  }
+  if (p.nsplit > 1) {
+    const int64_t total = rows.n * b;
+    hipLaunchKernelGGL(reduce_product_kernel, dim3(blocks_for(total, 256)), dim3(256), 0, stream,
+                       pp, p.nsplit, rows.npad, p.ncb * 16, sl, Y, ldy, rows.n, b);
+    FD_LAUNCH_CHECK();
+  }
+}
+
+template <int DP, bool UNIT>
+static void rowsum_dispatch(const KVPlan& p, const PointPack& rows, const PointPack& cols,
+                            const float* wp, bool diag, float* out, float* part,
+                            hipStream_t stream) {
+  const unsigned grid = unsigned(p.nrt * p.nsplit);
+  ProfScope prof(FD_KERNEL_ROWSUM, stream);
+  hipLaunchKernelGGL((rowsum_f32_kernel<DP, 4, UNIT>), dim3(grid), dim3(WG_THREADS), 0, stream,
+                     cols.xp.p, reinterpret_cast<const floatx4*>(cols.ap.p),
+                     reinterpret_cast<const floatx4*>(wp), rows.xp.p, rows.ar.p, p.nrt, p.njb,
+                     p.jb_per_split, int(diag), out, rows.n, part, rows.npad);
+  FD_LAUNCH_CHECK();
+}
+
+template <int DP>
+static void rowsum_dispatch_u(const KVPlan& p, const PointPack& rows, const PointPack& cols,
+                              const float* wp, bool diag, float* out, float* part,
+                              hipStream_t stream) {
+  if (wp == nullptr)
+    rowsum_dispatch<DP, true>(p, rows, cols, wp, diag, out, part, stream);
+  else
+    rowsum_dispatch<DP, false>(p, rows, cols, wp, diag, out, part, stream);
+}
+
+void launch_rowsum(const KVPlan& p, const PointPack& rows, const PointPack& cols, FSpan wp,
+                   bool diag, float* out, FSpan part, hipStream_t stream) {
+  check_tiles(p, rows, cols);
+  FD_REQUIRE(p.nib == 4, FD_ERR_INVALID_ARG, "internal: plan");
+  if (wp.p != nullptr) check_span(wp, lane4_extent(p.njb, 1), "weight pack");
+  float* pp = nullptr;
+  if (p.nsplit > 1) {
+    check_span(part, size_t(p.nsplit) * rows.npad, "partial row sums");
+    pp = part.p;
+  }
+  switch (p.dp) {
+    case 4: rowsum_dispatch_u<4>(p, rows, cols, wp.p, diag, out, pp, stream); break;
+    case 8: rowsum_dispatch_u<8>(p, rows, cols, wp.p, diag, out, pp, stream); break;
+    case 12: rowsum_dispatch_u<12>(p, rows, cols, wp.p, diag, out, pp, stream); break;
+    case 16: rowsum_dispatch_u<16>(p, rows, cols, wp.p, diag, out, pp, stream); break;
+    case 24: rowsum_dispatch_u<24>(p, rows, cols, wp.p, diag, out, pp, stream); break;
+    case 32: rowsum_dispatch_u<32>(p, rows, cols, wp.p, diag, out, pp, stream); break;
+    case 48: rowsum_dispatch_u<48>(p, rows, cols, wp.p, diag, out, pp, stream); break;
+    case 64: rowsum_dispatch_u<64>(p, rows, cols, wp.p, diag, out, pp, stream); break;
+    default: throw Error{FD_ERR_UNSUPPORTED, "feature dimension above 64"};
+  }
+  if (p.nsplit > 1) {
+    hipLaunchKernelGGL(reduce_rowsum_kernel, dim3(blocks_for(rows.n, 256)), dim3(256), 0, stream,
+                       pp, p.nsplit, rows.npad, out, rows.n);
+    FD_LAUNCH_CHECK();
+  }
+}
+
+void launch_pow_neg(const float* q, int64_t n, double alpha, float* w, hipStream_t stream) {
+  hipLaunchKernelGGL(pow_neg_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, stream, q, n, alpha,
+                     w);
+  FD_LAUNCH_CHECK();
+}
+
+void launch_degree_finish(const float* q, const float* t, int64_t n, double alpha, float* d,
+                          float* s, hipStream_t stream) {
+  hipLaunchKernelGGL(degree_finish_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, stream, q, t,
+                     n, alpha, d, s);
+  FD_LAUNCH_CHECK();
+}
+
+void launch_sum_minus_n(const float* q, int64_t n, double* out, hipStream_t stream) {
+  hipLaunchKernelGGL(sum_minus_n_kernel, dim3(1), dim3(1024), 0, stream, q, n, out);
+  FD_LAUNCH_CHECK();
+}
+
+}  // namespace fd

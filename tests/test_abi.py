@@ -1,0 +1,73 @@
+"""The C ABI: the library builds for gfx950, loads, exports every declared
+symbol, and validates arguments on the host (no GPU needed)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_38198_amd import _lib as fd
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "flashdiff.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(fd_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_entry_points():
+    names = declared_functions()
+    for n in ("fd_degree", "fd_kernel_matmul", "fd_block_lanczos", "fd_continuation"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = fd.load()
+    for n in declared_functions():
+        assert hasattr(lib, n), n
+    assert set(declared_functions()) <= set(fd.EXPORTS)
+
+
+def test_status_strings_and_defaults():
+    lib = fd.load()
+    assert lib.fd_status_string(0) == b"FD_OK"
+    assert lib.fd_status_string(5) == b"FD_ERR_NOT_CONVERGED"
+    o = fd.default_opts()
+    assert o.tol == 1e-5 and o.max_restarts > 0
+
+
+def test_workspace_sizes():
+    s1 = fd.fd_workspace_size(fd.FD_OP_KERNEL_MATMUL, 65536, 65536, 12, 16)
+    s2 = fd.fd_workspace_size(fd.FD_OP_KERNEL_MATMUL, 65536, 65536, 12, 32)
+    assert 0 < s1 < s2
+    assert fd.fd_workspace_size(fd.FD_OP_KERNEL_MATMUL, 10, 10, 65, 4) == 0   # D > 64
+    assert fd.fd_workspace_size(fd.FD_OP_KERNEL_MATMUL, 10, 10, 4, 65) == 0   # b > 64
+    assert fd.fd_workspace_size(fd.FD_OP_DEGREE, 1 << 20, 1 << 20, 30) > 0
+
+
+def test_host_validation_without_gpu():
+    lib = fd.load()
+    c = ctypes.c_void_p
+    # NULL X
+    assert lib.fd_kernel_matmul(None, 10, None, 10, 4, 4, 0, 1.0, None, None, None, 8, 8, None, 8,
+                                None, 0, None) == 1
+    fake = c(256)
+    # bad b, bad ldx, negative beta, unknown dtype
+    assert lib.fd_kernel_matmul(fake, 10, fake, 10, 4, 4, 0, 1.0, None, None, fake, 0, 8, fake, 8,
+                                None, 0, None) == 1
+    assert lib.fd_kernel_matmul(fake, 10, fake, 10, 4, 3, 0, 1.0, None, None, fake, 8, 8, fake, 8,
+                                None, 0, None) == 1
+    assert lib.fd_kernel_matmul(fake, 10, fake, 10, 4, 4, 0, -1.0, None, None, fake, 8, 8, fake, 8,
+                                None, 0, None) == 1
+    assert lib.fd_kernel_matmul(fake, 10, fake, 10, 4, 4, 7, 1.0, None, None, fake, 8, 8, fake, 8,
+                                None, 0, None) == 1
+    # missing workspace
+    assert lib.fd_kernel_matmul(fake, 10, fake, 10, 4, 4, 0, 1.0, None, None, fake, 8, 8, fake, 8,
+                                None, 0, None) == 3
+    # degree: alpha out of range, beta = 0
+    assert lib.fd_degree(fake, 0, 10, 4, 4, 1.0, 1.5, None, None, None, None, None, 0, None) == 1
+    assert lib.fd_degree(fake, 0, 10, 4, 4, 0.0, 0.5, None, None, None, None, None, 0, None) == 1
+    assert b"alpha" in lib.fd_last_error() or b"beta" in lib.fd_last_error()

@@ -1,0 +1,144 @@
+"""Parity of fd_kernel_matmul (fused Gaussian-kernel block product) with the oracle.
+
+Y = diag(sl) K diag(sr) V against the float64 difference-form oracle:
+relative Frobenius error <= 1e-5 for float32 inputs.  Full products at small
+sizes (several tiles and a ragged tail), sampled rows at the 65,536-point
+6-torus for every bandwidth of its sweep, the exact Kronecker-circulant
+product at the full size on a grid torus, and the edge cases (one point,
+beta = 0, b = 1 and 64, D = 1 and 64, strided operands, rectangular).
+"""
+import numpy as np
+import pytest
+import torch
+
+from gpu_util import TOL_F32, case, device, rel_fro, to_dev, to_np
+from oracle import kernel as ok
+from oracle import torus_grid as tg
+from paper_2609_38198_amd import _lib as fd
+from paper_2609_38198_amd import inputs
+
+pytestmark = pytest.mark.gpu
+
+
+def _run(Xr, Xc, beta, V, sl=None, sr=None):
+    dev = device()
+    tXr = to_dev(Xr, dev)
+    tXc = None if Xc is None else to_dev(Xc, dev)
+    out = fd.fd_kernel_matmul(tXr, tXc, beta, to_dev(V, dev),
+                              sl=None if sl is None else to_dev(sl, dev),
+                              sr=None if sr is None else to_dev(sr, dev))
+    return to_np(out)
+
+
+def test_torus2_full_product():
+    w = inputs.torus2()
+    V = inputs.random_block(w.N, w.b)
+    rng = np.random.default_rng(3)
+    sl = rng.uniform(0.5, 2, w.N).astype(np.float32)
+    sr = rng.uniform(0.5, 2, w.N).astype(np.float32)
+    for beta in (0.5, 8.0):
+        case(f"torus2 N=2048 D=4 b=8 beta={beta}")
+        Y = _run(w.X, None, beta, V)
+        ref = ok.kernel_matmul(w.X, None, beta, V)
+        assert rel_fro(Y, ref) <= TOL_F32
+        Y = _run(w.X, None, beta, V, sl, sr)
+        ref = ok.kernel_matmul(w.X, None, beta, V, sl=sl, sr=sr)
+        assert rel_fro(Y, ref) <= TOL_F32
+
+
+@pytest.mark.parametrize("beta", [0.5, 1.0, 2.0, 4.0, 8.0])
+def test_torus6_full_size_sampled_rows(beta):
+    w = inputs.torus6()
+    V = inputs.random_block(w.N, w.b)
+    case(f"torus6 N=65536 D=12 b=16 beta={beta}")
+    Y = _run(w.X, None, beta, V)
+    rows = np.random.default_rng(11).choice(w.N, 256, replace=False)
+    ref = ok.kernel_matmul(w.X, None, beta, V, rows=rows, threads=8)
+    assert rel_fro(Y[rows], ref) <= TOL_F32
+
+
+def test_grid_torus_full_size_closed_form():
+    counts = (8, 8, 8, 8, 4, 4)  # 65,536 points in R^12
+    X = inputs.grid_torus_points(counts).astype(np.float32)
+    V = inputs.random_block(X.shape[0], 16, seed=5)
+    for beta in (0.5, 2.0):
+        case(f"grid torus {counts} beta={beta}")
+        Y = _run(X, None, beta, V)
+        ref = tg.kernel_apply(counts, beta, V.astype(np.float64))
+        assert rel_fro(Y, ref) <= TOL_F32
+
+
+@pytest.mark.parametrize("N,D,b,beta", [(1000, 5, 3, 0.7), (17, 1, 1, 2.0), (300, 64, 64, 0.05),
+                                        (4099, 30, 32, 0.3), (1, 3, 5, 1.0), (2, 2, 1, 100.0)])
+def test_ragged_and_edge_shapes(N, D, b, beta):
+    rng = np.random.default_rng(N + D + b)
+    X = rng.normal(size=(N, D)).astype(np.float32)
+    X -= X.mean(0)
+    V = rng.normal(size=(N, b)).astype(np.float32)
+    case(f"ragged N={N} D={D} b={b} beta={beta}")
+    Y = _run(X, None, beta, V)
+    ref = ok.kernel_matmul(X, None, beta, V)
+    assert rel_fro(Y, ref) <= TOL_F32
+
+
+def test_beta_zero_gives_column_sums():
+    rng = np.random.default_rng(1)
+    X = rng.normal(size=(513, 7)).astype(np.float32)
+    V = rng.normal(size=(513, 4)).astype(np.float32)
+    case("beta=0")
+    Y = _run(X, None, 0.0, V)
+    ref = np.tile(V.astype(np.float64).sum(0), (513, 1))
+    assert rel_fro(Y, ref) <= TOL_F32
+
+
+def test_rectangular_product():
+    rng = np.random.default_rng(2)
+    Xr = rng.normal(size=(777, 12)).astype(np.float32)
+    Xc = rng.normal(size=(1234, 12)).astype(np.float32)
+    V = rng.normal(size=(1234, 17)).astype(np.float32)
+    sl = rng.uniform(0.5, 2, 777).astype(np.float32)
+    case("rectangular 777 x 1234")
+    Y = _run(Xr, Xc, 0.4, V, sl=sl)
+    ref = ok.kernel_matmul(Xr, Xc, 0.4, V, sl=sl)
+    assert rel_fro(Y, ref) <= TOL_F32
+
+
+def test_strided_operands_and_determinism():
+    dev = device()
+    rng = np.random.default_rng(4)
+    big = rng.normal(size=(3000, 20)).astype(np.float32)
+    X = big[:, :9]  # ldx = 20
+    Vbig = rng.normal(size=(3000, 40)).astype(np.float32)
+    tX = to_dev(big, dev)[:, :9]
+    tV = to_dev(Vbig, dev)[:, 5:21]  # ldv = 40, b = 16
+    Ybig = torch.zeros((3000, 24), dtype=torch.float32, device=dev)
+    tY = Ybig[:, 2:18]  # ldy = 24
+    case("strided X/V/Y")
+    fd.fd_kernel_matmul(tX, None, 0.6, tV, Y=tY)
+    Y1 = to_np(tY)
+    ref = ok.kernel_matmul(X, None, 0.6, Vbig[:, 5:21])
+    assert rel_fro(Y1, ref) <= TOL_F32
+    # columns outside the output window untouched
+    assert np.all(to_np(Ybig[:, :2]) == 0) and np.all(to_np(Ybig[:, 18:]) == 0)
+    fd.fd_kernel_matmul(tX, None, 0.6, tV, Y=tY)
+    assert np.array_equal(to_np(tY), Y1)
+
+
+def test_bf16_input_uses_exact_bf16_values():
+    s = inputs.stress(N=4096)
+    V = inputs.random_block(4096, 16)
+    beta = s.betas[0]
+    case("bf16 X N=4096 D=64 b=16")
+    Y = _run(s.X, None, beta, V)
+    ref = ok.kernel_matmul(s.X_f64(), None, beta, V)
+    assert rel_fro(Y, ref) <= TOL_F32
+
+
+def test_invalid_arguments_raise():
+    dev = device()
+    X = torch.zeros((10, 4), device=dev)
+    V = torch.zeros((10, 65), device=dev)
+    with pytest.raises(fd.FdError):
+        fd.fd_kernel_matmul(X, None, 1.0, V)
+    with pytest.raises(fd.FdError):
+        fd.fd_kernel_matmul(X, None, -1.0, V[:, :4])
