@@ -147,8 +147,80 @@ __global__ void pack_w_kernel(const float* __restrict__ w, int64_t n, int64_t nt
 
 // ------------------------------------------------------------------ products
 
+// 2^t clamped to [0, 1]: the exponent of a true kernel value is <= 0 and
+// rounding can only push it a few ulps above.  The median-of-three with 0 and 1
+// folds into the output clamp bit of v_exp_f32 (one instruction).  Written with
+// builtins, not inline asm, so the compiler sees the read of the MFMA result
+// and inserts the wait states that hazard requires.
+__device__ __forceinline__ float exp2_unit(float t) {
+  return __builtin_amdgcn_fmed3f(__builtin_amdgcn_exp2f(t), 0.f, 1.f);
+}
+
+// Column-tile operands of one 16-point tile, per lane.
+template <int S, int NW>
+struct ColTile {
+  float xa[S];     // contraction operand (A of the exponent MFMA)
+  floatx4 aj;      // a_j for the four accumulator rows of this lane
+  floatx4 w[NW];   // V (B operand of the product MFMA) or row-sum weights
+};
+
+template <int S, int NW>
+__device__ __forceinline__ void load_cols(ColTile<S, NW>& c, const float* __restrict__ xa,
+                                          const floatx4* __restrict__ aj,
+                                          const floatx4* __restrict__ wv, int64_t jb, int lane) {
+#pragma unroll
+  for (int s = 0; s < S; ++s) c.xa[s] = xa[(jb * S + s) * 64 + lane];
+  c.aj = aj[jb * 64 + lane];
+  if (wv != nullptr) {
+#pragma unroll
+    for (int k = 0; k < NW; ++k) c.w[k] = wv[(jb * NW + k) * 64 + lane];
+  }
+}
+
+// Exponent tile T^T[4g + r][p] for row tile ib against the loaded column tile;
+// DIAG: rows and columns are the same 16 points, so entry j == i is set to 0.
+template <int S, int NW, bool DIAG>
+__device__ __forceinline__ floatx4 exponent_tile(const ColTile<S, NW>& c, const float* xb,
+                                                 float ai, int g, int p) {
+  floatx4 t;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) t[r] = ai + c.aj[r];
+#pragma unroll
+  for (int s = 0; s < S; ++s) t = __builtin_amdgcn_mfma_f32_16x16x4f32(c.xa[s], xb[s], t, 0, 0, 0);
+  if (DIAG) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      if (4 * g + r == p) t[r] = 0.f;
+  }
+  return t;
+}
+
+template <int DP, int NCB, int NIB, bool DIAG>
+__device__ __forceinline__ void product_tile(const ColTile<DP / 4, NCB>& c,
+                                             const float (&xbr)[NIB][DP / 4],
+                                             const float (&ai)[NIB], floatx4 (&acc)[NIB][NCB],
+                                             int64_t jb, int64_t ib0, int g, int p) {
+#pragma unroll
+  for (int ib = 0; ib < NIB; ++ib) {
+    floatx4 t;
+    if (DIAG && jb == ib0 + ib)
+      t = exponent_tile<DP / 4, NCB, true>(c, xbr[ib], ai[ib], g, p);
+    else
+      t = exponent_tile<DP / 4, NCB, false>(c, xbr[ib], ai[ib], g, p);
+    float kk[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) kk[r] = exp2_unit(t[r]);
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        acc[ib][cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(kk[r], c.w[cb][r], acc[ib][cb], 0, 0, 0);
+  }
+}
+
 // One workgroup = 4 waves; wave w owns row tiles [ib0, ib0 + NIB) of 16 rows.
-// Column tiles [jb_begin, jb_end) of the workgroup's split are streamed.
+// Column tiles [jb_begin, jb_end) of the workgroup's split are streamed, the
+// next tile's operands being loaded while the current one is computed.
 template <int DP, int NCB, int NIB>
 __global__ __launch_bounds__(WG_THREADS) void product_f32_kernel(
     const float* __restrict__ xa, const floatx4* __restrict__ aj, const floatx4* __restrict__ vp,
@@ -164,6 +236,7 @@ __global__ __launch_bounds__(WG_THREADS) void product_f32_kernel(
   const int64_t ib0 = (rt * 4 + wave) * NIB;
   const int64_t jb_begin = split * jb_per_split;
   const int64_t jb_end = min(njb, jb_begin + jb_per_split);
+  const int g = lane >> 4, p = lane & 15;
 
   float xbr[NIB][S];
   float ai[NIB];
@@ -171,7 +244,7 @@ __global__ __launch_bounds__(WG_THREADS) void product_f32_kernel(
   for (int ib = 0; ib < NIB; ++ib) {
 #pragma unroll
     for (int s = 0; s < S; ++s) xbr[ib][s] = xb[((ib0 + ib) * S + s) * 64 + lane];
-    ai[ib] = ar[(ib0 + ib) * TILE + (lane & 15)];
+    ai[ib] = ar[(ib0 + ib) * TILE + p];
   }
 
   floatx4 acc[NIB][NCB];
@@ -184,39 +257,15 @@ __global__ __launch_bounds__(WG_THREADS) void product_f32_kernel(
       tot[ib][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
     }
 
-  const int g = lane >> 4, p = lane & 15;
+  ColTile<S, NCB> cur, nxt;
+  load_cols(cur, xa, aj, vp, jb_begin, lane);
   int chunk = 0;
   for (int64_t jb = jb_begin; jb < jb_end; ++jb) {
-    float xar[S];
-#pragma unroll
-    for (int s = 0; s < S; ++s) xar[s] = xa[(jb * S + s) * 64 + lane];
-    const floatx4 ajr = aj[jb * 64 + lane];
-    floatx4 vr[NCB];
-#pragma unroll
-    for (int cb = 0; cb < NCB; ++cb) vr[cb] = vp[(jb * NCB + cb) * 64 + lane];
-
-#pragma unroll
-    for (int ib = 0; ib < NIB; ++ib) {
-      floatx4 t;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) t[r] = ai[ib] + ajr[r];
-#pragma unroll
-      for (int s = 0; s < S; ++s)
-        t = __builtin_amdgcn_mfma_f32_16x16x4f32(xar[s], xbr[ib][s], t, 0, 0, 0);
-      if (diag && jb == ib0 + ib) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-          if (4 * g + r == p) t[r] = 0.f;
-      }
-      float kk[4];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) kk[r] = __builtin_amdgcn_exp2f(fminf(t[r], 0.f));
-#pragma unroll
-      for (int cb = 0; cb < NCB; ++cb)
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-          acc[ib][cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(kk[r], vr[cb][r], acc[ib][cb], 0, 0, 0);
-    }
+    load_cols(nxt, xa, aj, vp, min(jb + 1, jb_end - 1), lane);
+    if (diag && jb >= ib0 && jb < ib0 + NIB)
+      product_tile<DP, NCB, NIB, true>(cur, xbr, ai, acc, jb, ib0, g, p);
+    else
+      product_tile<DP, NCB, NIB, false>(cur, xbr, ai, acc, jb, ib0, g, p);
     if (++chunk == CHUNK_TILES) {
       chunk = 0;
 #pragma unroll
@@ -227,6 +276,7 @@ __global__ __launch_bounds__(WG_THREADS) void product_f32_kernel(
           acc[ib][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
         }
     }
+    cur = nxt;
   }
 
 #pragma unroll
@@ -247,6 +297,28 @@ __global__ __launch_bounds__(WG_THREADS) void product_f32_kernel(
     }
 }
 
+template <int DP, int NIB, bool UNIT, bool DIAG>
+__device__ __forceinline__ void rowsum_tile(const ColTile<DP / 4, 1>& c,
+                                            const float (&xbr)[NIB][DP / 4],
+                                            const float (&ai)[NIB], float (&acc)[NIB],
+                                            int64_t jb, int64_t ib0, int g, int p) {
+#pragma unroll
+  for (int ib = 0; ib < NIB; ++ib) {
+    floatx4 t;
+    if (DIAG && jb == ib0 + ib)
+      t = exponent_tile<DP / 4, 1, true>(c, xbr[ib], ai[ib], g, p);
+    else
+      t = exponent_tile<DP / 4, 1, false>(c, xbr[ib], ai[ib], g, p);
+    float sum = 0.f;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float k = exp2_unit(t[r]);
+      sum = UNIT ? sum + k : fmaf(k, c.w[0][r], sum);
+    }
+    acc[ib] += sum;
+  }
+}
+
 // Row sums sum_j K_ij w_j (b = 1, the normalisation passes): the same
 // exponent tiles, reduced on the vector ALUs instead of a second MFMA.
 template <int DP, int NIB, bool UNIT>
@@ -264,6 +336,7 @@ __global__ __launch_bounds__(WG_THREADS) void rowsum_f32_kernel(
   const int64_t ib0 = (rt * 4 + wave) * NIB;
   const int64_t jb_begin = split * jb_per_split;
   const int64_t jb_end = min(njb, jb_begin + jb_per_split);
+  const int g = lane >> 4, p = lane & 15;
 
   float xbr[NIB][S];
   float ai[NIB];
@@ -271,42 +344,23 @@ __global__ __launch_bounds__(WG_THREADS) void rowsum_f32_kernel(
   for (int ib = 0; ib < NIB; ++ib) {
 #pragma unroll
     for (int s = 0; s < S; ++s) xbr[ib][s] = xb[((ib0 + ib) * S + s) * 64 + lane];
-    ai[ib] = ar[(ib0 + ib) * TILE + (lane & 15)];
+    ai[ib] = ar[(ib0 + ib) * TILE + p];
   }
   float acc[NIB], tot[NIB];
 #pragma unroll
   for (int ib = 0; ib < NIB; ++ib) acc[ib] = tot[ib] = 0.f;
 
-  const int g = lane >> 4, p = lane & 15;
+  const floatx4* wsrc = UNIT ? nullptr : wp;
+  ColTile<S, 1> cur, nxt;
+  cur.w[0] = nxt.w[0] = floatx4{1.f, 1.f, 1.f, 1.f};
+  load_cols(cur, xa, aj, wsrc, jb_begin, lane);
   int chunk = 0;
   for (int64_t jb = jb_begin; jb < jb_end; ++jb) {
-    float xar[S];
-#pragma unroll
-    for (int s = 0; s < S; ++s) xar[s] = xa[(jb * S + s) * 64 + lane];
-    const floatx4 ajr = aj[jb * 64 + lane];
-    floatx4 wr4 = floatx4{1.f, 1.f, 1.f, 1.f};
-    if (!UNIT) wr4 = wp[jb * 64 + lane];
-#pragma unroll
-    for (int ib = 0; ib < NIB; ++ib) {
-      floatx4 t;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) t[r] = ai[ib] + ajr[r];
-#pragma unroll
-      for (int s = 0; s < S; ++s)
-        t = __builtin_amdgcn_mfma_f32_16x16x4f32(xar[s], xbr[ib][s], t, 0, 0, 0);
-      if (diag && jb == ib0 + ib) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-          if (4 * g + r == p) t[r] = 0.f;
-      }
-      float sum = 0.f;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float k = __builtin_amdgcn_exp2f(fminf(t[r], 0.f));
-        sum = UNIT ? sum + k : fmaf(k, wr4[r], sum);
-      }
-      acc[ib] += sum;
-    }
+    load_cols(nxt, xa, aj, wsrc, min(jb + 1, jb_end - 1), lane);
+    if (diag && jb >= ib0 && jb < ib0 + NIB)
+      rowsum_tile<DP, NIB, UNIT, true>(cur, xbr, ai, acc, jb, ib0, g, p);
+    else
+      rowsum_tile<DP, NIB, UNIT, false>(cur, xbr, ai, acc, jb, ib0, g, p);
     if (++chunk == CHUNK_TILES) {
       chunk = 0;
 #pragma unroll
@@ -315,6 +369,7 @@ __global__ __launch_bounds__(WG_THREADS) void rowsum_f32_kernel(
         acc[ib] = 0.f;
       }
     }
+    cur = nxt;
   }
 #pragma unroll
   for (int ib = 0; ib < NIB; ++ib) {
