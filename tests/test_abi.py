@@ -46,6 +46,8 @@ def test_workspace_sizes():
     assert fd.fd_workspace_size(fd.FD_OP_KERNEL_MATMUL, 10, 10, 65, 4) == 0   # D > 64
     assert fd.fd_workspace_size(fd.FD_OP_KERNEL_MATMUL, 10, 10, 4, 65) == 0   # b > 64
     assert fd.fd_workspace_size(fd.FD_OP_DEGREE, 1 << 20, 1 << 20, 30) > 0
+    assert fd.fd_workspace_size(fd.FD_OP_BLOCK_LANCZOS, 2048, 2048, 4, 8, 16) > 0
+    assert fd.fd_workspace_size(fd.FD_OP_BLOCK_LANCZOS, 10, 10, 4, 8, 11) == 0  # k > N
 
 
 def test_host_validation_without_gpu():

@@ -1,0 +1,152 @@
+"""Parity of fd_block_lanczos with the oracle's dense eigensolve.
+
+Eigenvalues: |d lambda_i| <= max(1e-5 |lambda_i|, 1e-6) (1e-6 is the float32
+Perron-wall resolution kappa_P * eta of Sec. 2.3).  Eigenvectors: principal
+angles < 1e-3 rad between the leading invariant subspaces, compared only up to
+cut points where the spectrum has a gap >= 1e-2 (inside a cluster the basis is
+not unique).  Also: orthonormality, true residuals, Markov vectors
+psi = d^-1/2 phi, the grid-torus closed form at 65,536 points, warm starts,
+the product budget, the two-point closed form and determinism.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from gpu_util import case, device, to_dev, to_np
+from oracle import diagnostics as od
+from oracle import eig as oe
+from oracle import kernel as ok
+from oracle import torus_grid as tg
+from paper_2609_38198_amd import _lib as fd
+from paper_2609_38198_amd import inputs
+
+pytestmark = pytest.mark.gpu
+
+
+def eval_ok(got, ref):
+    got = np.asarray(got)
+    ref = np.asarray(ref)
+    tol = np.maximum(1e-5 * np.abs(ref), 1e-6)
+    return np.all(np.abs(got - ref) <= tol), np.max(np.abs(got - ref) / tol)
+
+
+def clean_cuts(ev, kmax, gap=1e-2):
+    return [c for c in range(1, kmax) if ev[c - 1] - ev[c] >= gap]
+
+
+@pytest.fixture(scope="module")
+def torus2_ref():
+    w = inputs.torus2()
+    sp = oe.spectrum(w.X, 8.0, 0.5, 40)
+    return w, sp
+
+
+def test_torus2_top16(torus2_ref):
+    w, sp = torus2_ref
+    dev = device()
+    case("lanczos torus2 N=2048 beta=8 b=8 k=16")
+    e = fd.fd_block_lanczos(to_dev(w.X, dev), 8.0, 16, 8)
+    ok_, worst = eval_ok(e.evals, sp.evals[:16])
+    assert ok_, (worst, e.evals, sp.evals[:16], e.info)
+    phi = to_np(e.evecs)
+    assert np.abs(phi.T @ phi - np.eye(16)).max() <= 1e-5
+    assert max(e.residuals) <= 1e-5
+    cuts = clean_cuts(sp.evals, 16)
+    assert cuts, "no clean cut point"
+    for c in cuts:
+        ang = od.principal_angles(phi[:, :c], sp.phi[:, :c]).max()
+        assert ang < 1e-3, (c, ang)
+    psi = to_np(e.psi)
+    for c in cuts:
+        assert od.principal_angles(psi[:, :c], sp.psi[:, :c]).max() < 1e-3
+    # Markov vectors are d^-1/2 phi: the Perron one is constant
+    p0 = psi[:, 0]
+    assert np.abs(p0 / p0.mean() - 1).max() < 1e-4
+    assert abs(e.evals[0] - 1.0) <= 1e-6
+    assert e.info["s_off"] == pytest.approx(sp.norm.s_off, rel=1e-5)
+
+
+def test_two_point_closed_form():
+    X = np.array([[0.3, -0.2], [-0.4, 0.5]], dtype=np.float32)
+    dev = device()
+    beta = 0.9
+    h = float(np.sum((X[0].astype(np.float64) - X[1]) ** 2))
+    e_ = math.exp(-beta * h)
+    case("lanczos two points")
+    e = fd.fd_block_lanczos(to_dev(X, dev), beta, 2, 8)
+    ok_, _ = eval_ok(e.evals, [1.0, (1 - e_) / (1 + e_)])
+    assert ok_, e.evals
+
+
+@pytest.mark.parametrize("N,D,b,k,beta,alpha", [(100, 3, 8, 5, 1.0, 0.5), (700, 5, 4, 6, 2.0, 1.0),
+                                                (1500, 2, 16, 20, 4.0, 0.0)])
+def test_small_problems(N, D, b, k, beta, alpha):
+    rng = np.random.default_rng(N)
+    X = rng.normal(size=(N, D)).astype(np.float32)
+    X -= X.mean(0)
+    sp = oe.spectrum(X, beta, alpha, k + 8)
+    dev = device()
+    case(f"lanczos small N={N} b={b} k={k}")
+    e = fd.fd_block_lanczos(to_dev(X, dev), beta, k, b, alpha=alpha)
+    ok_, worst = eval_ok(e.evals, sp.evals[:k])
+    assert ok_, (worst, e.info)
+    phi = to_np(e.evecs)
+    for c in clean_cuts(sp.evals, k):
+        assert od.principal_angles(phi[:, :c], sp.phi[:, :c]).max() < 1e-3
+
+
+def test_grid_torus_65536_closed_form():
+    counts = (8, 8, 8, 8, 4, 4)
+    X = inputs.grid_torus_points(counts).astype(np.float32)
+    beta = 0.5
+    ref = tg.operator_eigs(counts, beta)[:16]
+    dev = device()
+    case("lanczos grid torus 65536 b=16 k=16")
+    e = fd.fd_block_lanczos(to_dev(X, dev), beta, 16, 16)
+    ok_, worst = eval_ok(e.evals, ref)
+    assert ok_, (worst, e.evals, ref, e.info)
+    assert max(e.residuals) <= 1e-5
+
+
+def test_warm_start_matches_cold(torus2_ref):
+    w, sp = torus2_ref
+    dev = device()
+    X = to_dev(w.X, dev)
+    case("lanczos warm start beta 4 -> 8")
+    prev = fd.fd_block_lanczos(X, 4.0, 16, 8)
+    cold = fd.fd_block_lanczos(X, 8.0, 16, 8)
+    warm = fd.fd_block_lanczos(X, 8.0, 16, 8, V0=prev.psi, warm_is_psi=True)
+    ok_, _ = eval_ok(warm.evals, sp.evals[:16])
+    assert ok_
+    ok_, _ = eval_ok(warm.evals, cold.evals)
+    assert ok_
+    # restarting from the converged answer needs no restart cycle
+    again = fd.fd_block_lanczos(X, 8.0, 16, 8, V0=cold.evecs, warm_is_psi=False)
+    assert again.info["restarts"] == 0
+    assert again.info["block_matvecs"] <= cold.info["block_matvecs"]
+
+
+def test_product_budget_reports_not_converged(torus2_ref):
+    w, _ = torus2_ref
+    dev = device()
+    case("lanczos max_matvecs=3")
+    o = fd.default_opts(max_matvecs=3)
+    e = fd.fd_block_lanczos(to_dev(w.X, dev), 8.0, 16, 8, opts=o, allow_not_converged=True)
+    assert e.status == 5
+    assert e.info["block_matvecs"] <= 4
+    assert all(np.isfinite(e.evals))
+    with pytest.raises(fd.FdError):
+        fd.fd_block_lanczos(to_dev(w.X, dev), 8.0, 16, 8, opts=o)
+
+
+def test_deterministic(torus2_ref):
+    w, _ = torus2_ref
+    dev = device()
+    X = to_dev(w.X, dev)
+    case("lanczos determinism")
+    a = fd.fd_block_lanczos(X, 8.0, 16, 8)
+    b = fd.fd_block_lanczos(X, 8.0, 16, 8)
+    assert a.evals == b.evals
+    assert torch.equal(a.evecs, b.evecs)
