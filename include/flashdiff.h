@@ -93,7 +93,8 @@ void fd_lanczos_default_opts(fd_lanczos_opts* opts);
  *   op = FD_OP_KERNEL_MATMUL: Nr output rows, Nc columns, D, b; k ignored.
  *   op = FD_OP_DEGREE:        Nr = Nc = N, D; b, k ignored.
  *   op = FD_OP_BLOCK_LANCZOS: Nr = Nc = N, D, b, k, opts (NULL = defaults).
- *   op = FD_OP_CONTINUATION:  Nr = Nc = largest n of the schedule, D, b, k, opts.
+ *   op = FD_OP_CONTINUATION:  Nr = largest n of the schedule, Nc = number of steps,
+ *                             D, b, k (<= 64), opts.
  * Returns 0 for arguments the entry point would reject. */
 size_t fd_workspace_size(fd_op op, int64_t Nr, int64_t Nc, int64_t D, int64_t b, int64_t k,
                          const fd_lanczos_opts* opts);
@@ -105,7 +106,8 @@ size_t fd_workspace_size(fd_op op, int64_t Nr, int64_t Nc, int64_t D, int64_t b,
  * evaluated tile by tile in the Gram form of eq. rbf_gram (row norms plus a
  * matrix-core contraction), exponentiated and multiplied into V on chip.
  *   Xr  : Nr x D rows (device, dtype xt, ldx);  Xc : Nc x D columns (same D, ldx, xt).
- *         When Xr == Xc and Nr == Nc the diagonal K_ii is taken as exactly 1.
+ *         When Xr == Xc (the same array; the shorter set is then a prefix of the
+ *         longer) every K_ii with i < min(Nr, Nc) is taken as exactly 1.
  *   beta: >= 0 (beta = 0 gives K = ones).
  *   sl  : Nr scale of output rows, or NULL for ones.  sr : Nc scale of V rows, or NULL.
  *   V   : Nc x b (device, ldv >= b), 1 <= b <= 64.   Y : Nr x b output (device, ldy >= b).
@@ -159,8 +161,10 @@ fd_status fd_block_lanczos(const void* X, fd_dtype xt, int64_t N, int64_t D, int
  *   n_steps: nsteps prefix sizes (host), non-decreasing, 2 <= n_t <= N.
  *   beta_steps: nsteps bandwidths (host), > 0.
  *   V0/k0: optional warm start for step 0 (Markov form, N x k0 device) or NULL.
- *   evals: nsteps x k doubles (host).  evecs: n_last x k (device) eigenvectors of M
- *   at the final step.  psi: n_last x k Markov eigenvectors at the final step or NULL.
+ *   k: 1 <= k <= 64 (the Nystrom pass applies the kernel to k + 1 columns).
+ *   evals: nsteps x k doubles (host).  evecs: n_last x k (device, ld k) eigenvectors of
+ *   M at the last step run (its first n rows are written).  psi: the matching Markov
+ *   eigenvectors (same layout) or NULL.
  *   per_step: nsteps reports (host) or NULL.
  *   stop_at_wall: when non-zero, stop after the first step whose Perron gap is at or
  *   below kappa_P * eta_fp32 and return FD_ERR_PERRON_WALL; evals of the steps run

@@ -317,7 +317,7 @@ def fd_continuation(X: torch.Tensor, n_steps: Sequence[int], beta_steps: Sequenc
     done = ctypes.c_int64(0)
     k0 = 0 if V0 is None else V0.shape[1]
     ldv0 = 0 if V0 is None else V0.stride(0)
-    need = fd_workspace_size(FD_OP_CONTINUATION, max(int(n) for n in n_steps), 0, D, b, k, o)
+    need = fd_workspace_size(FD_OP_CONTINUATION, max(int(n) for n in n_steps), T, D, b, k, o)
     if need == 0:
         raise FdError(1, "unsupported sizes")
     if ws is None or ws.numel() < need:

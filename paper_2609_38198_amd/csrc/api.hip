@@ -62,7 +62,35 @@ ProductWs carve_product(Arena& a, int64_t Nr, int64_t Nc, int64_t D, int b) {
   w.rows = carve_pack(a, Nr, dp, ROW_PAD);
   w.cols = carve_pack(a, Nc, dp, TILE);
   w.vp = a.fspan(size_t(w.cols.npad) * w.plan.ncb * 16);
-  if (w.plan.nsplit > 1) w.part = a.fspan(size_t(w.plan.nsplit) * w.rows.npad * w.plan.ncb * 16);
+  w.part = a.fspan(part_rows_bound(w.rows.npad) * w.plan.ncb * 16);
+  return w;
+}
+
+// Every plan has nsplit * (row tiles) <= 2048 + (row tiles), so the partial
+// buffers of any problem with at most npad rows fit in this many row slots.
+size_t part_rows_bound(int64_t npad) { return size_t(2048) * ROW_PAD + size_t(npad); }
+
+PointPack pack_view(const PointPack& big, int64_t n, int64_t pad) {
+  PointPack p = big;
+  p.n = n;
+  p.npad = round_up(n, pad);
+  return p;
+}
+
+DegreeWs degree_view(const DegreeWs& big, int64_t n) {
+  DegreeWs w = big;
+  w.rows = pack_view(big.rows, n, ROW_PAD);
+  w.cols = pack_view(big.cols, n, TILE);
+  w.plan = plan_product(n, n, big.rows.dp, 1);
+  return w;
+}
+
+ProductWs product_view(const ProductWs& big, const PointPack& rows, const PointPack& cols,
+                       int width) {
+  ProductWs w = big;
+  w.rows = rows;
+  w.cols = cols;
+  w.plan = plan_product(rows.n, cols.n, rows.dp, width);
   return w;
 }
 
@@ -84,7 +112,7 @@ DegreeWs carve_degree(Arena& a, int64_t N, int64_t D) {
   w.q = a.take<float>(size_t(N));
   w.t = a.take<float>(size_t(N));
   w.w = a.take<float>(size_t(N));
-  if (w.plan.nsplit > 1) w.part = a.fspan(size_t(w.plan.nsplit) * w.rows.npad);
+  w.part = a.fspan(part_rows_bound(w.rows.npad));
   return w;
 }
 
@@ -155,13 +183,21 @@ size_t fd_workspace_size(fd_op op, int64_t Nr, int64_t Nc, int64_t D, int64_t b,
       case FD_OP_DEGREE:
         carve_degree(a, Nr, D);
         break;
-      case FD_OP_BLOCK_LANCZOS:
-      case FD_OP_CONTINUATION: {
+      case FD_OP_BLOCK_LANCZOS: {
         fd_lanczos_opts o;
         fd_lanczos_default_opts(&o);
         if (opts != nullptr) o = *opts;
         FD_REQUIRE(b >= 1 && b <= MAX_B && k >= 1 && k <= Nr, FD_ERR_INVALID_ARG, "size");
-        carve_solver(a, Nr, D, int(b), int(k), o, op == FD_OP_CONTINUATION);
+        carve_solver(a, Nr, D, int(b), int(k), o);
+        break;
+      }
+      case FD_OP_CONTINUATION: {
+        fd_lanczos_opts o;
+        fd_lanczos_default_opts(&o);
+        if (opts != nullptr) o = *opts;
+        FD_REQUIRE(b >= 1 && b <= MAX_B && k >= 1 && k <= 64 && k <= Nr && Nc >= 1,
+                   FD_ERR_INVALID_ARG, "size");
+        carve_continuation_ws(a, Nr, Nc, D, int(b), int(k), o);
         break;
       }
       default:
@@ -194,7 +230,8 @@ fd_status fd_kernel_matmul(const void* Xr, int64_t Nr, const void* Xc, int64_t N
     hipStream_t st = static_cast<hipStream_t>(stream);
     launch_pack_points(Xr, xt, Nr, D, ldx, beta, true, w.rows, st);
     launch_pack_points(Xc, xt, Nc, D, ldx, beta, false, w.cols, st);
-    const bool diag = (Xr == Xc) && (Nr == Nc);
+    // same base pointer and ldx: index i names the same point in both sets
+    const bool diag = (Xr == Xc);
     product_apply(w, sl, sr, V, ldv, int(b), Y, ldy, diag, st);
   });
 }

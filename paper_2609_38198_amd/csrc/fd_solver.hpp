@@ -36,8 +36,18 @@ void degree_run(DegreeWs& w, const void* X, fd_dtype xt, int64_t N, int64_t D, i
                 double beta, double alpha, float* q, float* d, float* s, double* s_off,
                 bool pack, hipStream_t stream);
 
+// Row slots of a partial-sum buffer large enough for every plan with at most
+// npad rows (see plan_product).
+size_t part_rows_bound(int64_t npad);
+// Views of workspace carved for a larger problem, for n <= the carved size.
+PointPack pack_view(const PointPack& big, int64_t n, int64_t pad);
+DegreeWs degree_view(const DegreeWs& big, int64_t n);
+ProductWs product_view(const ProductWs& big, const PointPack& rows, const PointPack& cols,
+                       int width);
+
 // Eigensolver workspace (sizes only when a.measuring).
-void carve_solver(Arena& a, int64_t N, int64_t D, int b, int k, const fd_lanczos_opts& o,
-                  bool continuation);
+void carve_solver(Arena& a, int64_t N, int64_t D, int b, int k, const fd_lanczos_opts& o);
+void carve_continuation_ws(Arena& a, int64_t nmax, int64_t nsteps, int64_t D, int b, int k,
+                           const fd_lanczos_opts& o);
 
 }  // namespace fd

@@ -85,8 +85,7 @@ static SolverWs carve_solver_ws(Arena& a, int64_t N, int64_t D, int b, int mm_ca
   w.prod.rows = w.deg.rows;
   w.prod.cols = w.deg.cols;
   w.prod.vp = a.fspan(size_t(w.prod.cols.npad) * w.prod.plan.ncb * 16);
-  if (w.prod.plan.nsplit > 1)
-    w.prod.part = a.fspan(size_t(w.prod.plan.nsplit) * w.prod.rows.npad * w.prod.plan.ncb * 16);
+  w.prod.part = a.fspan(part_rows_bound(w.prod.rows.npad) * w.prod.plan.ncb * 16);
   w.d = a.take<float>(size_t(N));
   w.s = a.take<float>(size_t(N));
   w.s_off = a.take<double>(1);
@@ -117,24 +116,16 @@ static SolverWs carve_solver_ws(Arena& a, int64_t N, int64_t D, int b, int mm_ca
   return w;
 }
 
-static int cap_for(int64_t N, int b, int k, const fd_lanczos_opts& o) {
+void carve_solver(Arena& a, int64_t N, int64_t D, int b, int k, const fd_lanczos_opts& o) {
   const SolverLayout L = solver_layout(N, b, k, o);
-  return L.mm;
-}
-
-void carve_solver(Arena& a, int64_t N, int64_t D, int b, int k, const fd_lanczos_opts& o,
-                  bool continuation) {
-  // the widest basis any prefix can need is the iterative one (dense bases are
-  // at most that wide); continuation also runs a 64-wide Nystrom product
-  fd_lanczos_opts big = o;
-  const SolverLayout L = solver_layout(N, b, k, big);
-  carve_solver_ws(a, N, D, b, L.mm, continuation ? 64 : b);
+  carve_solver_ws(a, N, D, b, L.mm, b);
 }
 
 // ----------------------------------------------------------------- solver
 
 struct Lanczos {
   SolverWs& w;
+  ProductWs prod;  // product view for the current number of points
   hipStream_t st;
   int64_t N;
   int b, mm;
@@ -143,12 +134,12 @@ struct Lanczos {
   int matvecs = 0;
   bool diag = true;
 
-  Lanczos(SolverWs& ws, hipStream_t s, int64_t n, int bb, int m, uint64_t sd)
-      : w(ws), st(s), N(n), b(bb), mm(m), seed(sd) {}
+  Lanczos(SolverWs& ws, const ProductWs& pv, hipStream_t s, int64_t n, int bb, int m, uint64_t sd)
+      : w(ws), prod(pv), st(s), N(n), b(bb), mm(m), seed(sd) {}
 
   // Y[:, 0:nb] (ld mm) = M V[:, 0:nb] (ld mm)
   void matvec(const float* V, float* Y, int nb) {
-    product_apply(w.prod, w.s, w.s, V, mm, nb, Y, mm, diag, st);
+    product_apply(prod, w.s, w.s, V, mm, nb, Y, mm, diag, st);
     ++matvecs;
   }
 
@@ -322,6 +313,88 @@ static void validate_opts(const fd_lanczos_opts& o) {
              FD_ERR_INVALID_ARG, "negative option");
 }
 
+// ----------------------------------------------------------------- continuation
+
+struct ContWs {
+  SolverWs sw;
+  float* store_psi = nullptr;  // nsteps x (nmax x k): Markov vectors of every step
+  float* store_q = nullptr;    // nsteps x nmax: degrees q of every step
+  float* ext = nullptr;        // nmax x k: Nystrom-extended start
+  float* den = nullptr;        // nmax: K w of the extension
+  float* wv = nullptr;         // nmax: w = q^-alpha of the source step
+  float* num = nullptr;        // nmax x 64: K (w psi) of the extension
+  double* lam = nullptr;       // k: source eigenvalues
+  int64_t nmax = 0;
+  int k = 0;
+  float* psi(int64_t t) const { return store_psi + size_t(t) * nmax * k; }
+  float* q(int64_t t) const { return store_q + size_t(t) * nmax; }
+};
+
+static ContWs carve_continuation(Arena& a, int64_t nmax, int64_t nsteps, int64_t D, int b, int k,
+                                 const fd_lanczos_opts& o) {
+  ContWs c;
+  c.nmax = nmax;
+  c.k = k;
+  const SolverLayout L = solver_layout(nmax, b, k, o);
+  c.sw = carve_solver_ws(a, nmax, D, b, L.mm, 64);
+  c.store_psi = a.take<float>(size_t(nsteps) * nmax * k);
+  c.store_q = a.take<float>(size_t(nsteps) * nmax);
+  c.ext = a.take<float>(size_t(nmax) * k);
+  c.den = a.take<float>(size_t(nmax));
+  c.wv = a.take<float>(size_t(nmax));
+  c.num = a.take<float>(size_t(nmax) * 64);
+  c.lam = a.take<double>(64);
+  return c;
+}
+
+// ext[i, c] = (1/lambda_c) sum_j K_ij w_j psi_jc / sum_j K_ij w_j
+__global__ void nystrom_finish_kernel(const float* __restrict__ num, int ldn,
+                                      const float* __restrict__ den,
+                                      const double* __restrict__ lam, int64_t n, int c0, int nc,
+                                      float* __restrict__ ext, int lde) {
+  const int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (idx >= n * nc) return;
+  const int64_t i = idx / nc;
+  const int c = int(idx % nc);
+  ext[i * lde + c0 + c] = float(double(num[i * ldn + c]) / double(den[i]) / lam[c0 + c]);
+}
+
+// Extend Markov vectors psi (n_old x k, ld k) of the step solved at beta on the
+// prefix n_old to the prefix n_new (formula of the oracle's Nystrom module):
+// one row-sum pass for the denominators and ceil(k / 64) fused products.
+static void nystrom_extend(ContWs& c, const void* X, fd_dtype xt, int64_t D, int64_t ldx,
+                           int64_t n_old, int64_t n_new, double beta, double alpha,
+                           const float* psi, const float* q_old, const std::vector<double>& lam,
+                           int k, hipStream_t st) {
+  SolverWs& w = c.sw;
+  PointPack rows = pack_view(w.deg.rows, n_new, ROW_PAD);
+  PointPack cols = pack_view(w.deg.cols, n_old, TILE);
+  launch_pack_points(X, xt, n_new, D, ldx, beta, true, rows, st);
+  launch_pack_points(X, xt, n_old, D, ldx, beta, false, cols, st);
+  launch_pow_neg(q_old, n_old, alpha, c.wv, st);
+  // denominators K w
+  launch_pack_w(c.wv, n_old, cols.npad, w.deg.wp, st);
+  KVPlan rp = plan_product(n_new, n_old, rows.dp, 1);
+  launch_rowsum(rp, rows, cols, w.deg.wp, true, c.den, w.deg.part, st);
+  // numerators K (w psi), 64 columns at a time
+  std::vector<double> l(lam.begin(), lam.begin() + k);
+  FD_HIP_CHECK(hipMemcpyAsync(c.lam, l.data(), sizeof(double) * k, hipMemcpyHostToDevice, st));
+  ProductWs pv = product_view(w.prod, rows, cols, 64);
+  for (int c0 = 0; c0 < k; c0 += 64) {
+    const int nc = std::min(64, k - c0);
+    product_apply(pv, nullptr, c.wv, psi + c0, k, nc, c.num, 64, true, st);
+    hipLaunchKernelGGL(nystrom_finish_kernel, dim3(unsigned((n_new * nc + 255) / 256)), dim3(256),
+                       0, st, c.num, 64, c.den, c.lam, n_new, c0, nc, c.ext, k);
+    FD_LAUNCH_CHECK();
+  }
+  FD_HIP_CHECK(hipStreamSynchronize(st));
+}
+
+void carve_continuation_ws(Arena& a, int64_t nmax, int64_t nsteps, int64_t D, int b, int k,
+                           const fd_lanczos_opts& o) {
+  carve_continuation(a, nmax, nsteps, D, b, k, o);
+}
+
 }  // namespace fd
 
 using namespace fd;
@@ -354,7 +427,7 @@ fd_status fd_block_lanczos(const void* X, fd_dtype xt, int64_t N, int64_t D, int
       FD_REQUIRE(lay.dense || k <= lay.kk, FD_ERR_INVALID_ARG, "k too large for the basis");
       Arena m;
       m.measuring = true;
-      carve_solver(m, N, D, int(b), int(k), o, false);
+      carve_solver(m, N, D, int(b), int(k), o);
       check_workspace(ws, ws_bytes, m.used);
       Arena a;
       a.base = static_cast<char*>(ws);
@@ -363,7 +436,7 @@ fd_status fd_block_lanczos(const void* X, fd_dtype xt, int64_t N, int64_t D, int
       hipStream_t st = static_cast<hipStream_t>(stream);
 
       degree_run(w.deg, X, xt, N, D, ldx, beta, alpha, nullptr, w.d, w.s, w.s_off, true, st);
-      Lanczos L(w, st, N, int(b), lay.mm, o.seed);
+      Lanczos L(w, w.prod, st, N, int(b), lay.mm, o.seed);
       SolveResult R = lanczos_solve(w, L, lay, int(k), V0, V0 ? k0 : 0, ldv0,
                                     warm_is_psi ? 0.5 : 0.0, o);
       copy_cols(w.Q, lay.mm, evecs, k, N, int(k), nullptr, 0.0, st);
@@ -396,12 +469,138 @@ fd_status fd_block_lanczos(const void* X, fd_dtype xt, int64_t N, int64_t D, int
   return status;
 }
 
-fd_status fd_continuation(const void*, fd_dtype, int64_t, int64_t, int64_t, float, const int64_t*,
-                          const float*, int64_t, int64_t, int64_t, const float*, int64_t, int64_t,
-                          const fd_lanczos_opts*, double*, float*, float*, fd_lanczos_info*,
-                          int32_t, int64_t*, void*, size_t, void*) {
-  set_error("continuation not built yet");
-  return FD_ERR_UNSUPPORTED;
+fd_status fd_continuation(const void* X, fd_dtype xt, int64_t N, int64_t D, int64_t ldx,
+                          float alpha, const int64_t* n_steps, const float* beta_steps,
+                          int64_t nsteps, int64_t b, int64_t k, const float* V0, int64_t k0,
+                          int64_t ldv0, const fd_lanczos_opts* opts, double* evals,
+                          float* evecs, float* psi, fd_lanczos_info* per_step,
+                          int32_t stop_at_wall, int64_t* steps_done, void* ws, size_t ws_bytes,
+                          void* stream) {
+  try {
+    check_points(X, xt, N, D, ldx, "X");
+    FD_REQUIRE(alpha >= 0.f && alpha <= 1.f, FD_ERR_INVALID_ARG, "alpha must be in [0, 1]");
+    FD_REQUIRE(b >= 1 && b <= MAX_B, FD_ERR_INVALID_ARG, "b must be in [1, 64]");
+    FD_REQUIRE(nsteps >= 1 && n_steps != nullptr && beta_steps != nullptr, FD_ERR_INVALID_ARG,
+               "empty schedule");
+    FD_REQUIRE(evals != nullptr && evecs != nullptr, FD_ERR_INVALID_ARG, "evals / evecs NULL");
+    FD_REQUIRE(k >= 1 && k <= 64, FD_ERR_INVALID_ARG, "k must be in [1, 64] for the continuation");
+    int64_t nmax = 0;
+    for (int64_t t = 0; t < nsteps; ++t) {
+      FD_REQUIRE(n_steps[t] >= 2 && n_steps[t] <= N, FD_ERR_INVALID_ARG, "n_t out of [2, N]");
+      FD_REQUIRE(t == 0 || n_steps[t] >= n_steps[t - 1], FD_ERR_INVALID_ARG,
+                 "n_steps must be non-decreasing");
+      FD_REQUIRE(std::isfinite(beta_steps[t]) && beta_steps[t] > 0.f, FD_ERR_INVALID_ARG,
+                 "beta_t must be finite and > 0");
+      FD_REQUIRE(k <= n_steps[t], FD_ERR_INVALID_ARG, "k larger than a prefix");
+      nmax = std::max(nmax, n_steps[t]);
+    }
+    FD_REQUIRE(V0 == nullptr || k0 == 0 || (k0 > 0 && ldv0 >= k0), FD_ERR_INVALID_ARG,
+               "bad warm start");
+    fd_lanczos_opts o;
+    fd_lanczos_default_opts(&o);
+    if (opts != nullptr) o = *opts;
+    validate_opts(o);
+    Arena m;
+    m.measuring = true;
+    carve_continuation(m, nmax, nsteps, D, int(b), int(k), o);
+    check_workspace(ws, ws_bytes, m.used);
+    Arena a;
+    a.base = static_cast<char*>(ws);
+    a.cap = ws_bytes;
+    ContWs c = carve_continuation(a, nmax, nsteps, D, int(b), int(k), o);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const int kk = int(k);
+    std::vector<std::vector<double>> lam(nsteps);
+    std::vector<float> level_beta;
+    std::vector<int64_t> level_slot;
+    int64_t n_prev = 0;
+    bool any_unconverged = false;
+    int64_t done = 0;
+    int64_t last = -1;
+    fd_status status = FD_OK;
+    for (int64_t t = 0; t < nsteps; ++t) {
+      const auto t0 = std::chrono::steady_clock::now();
+      const int64_t n = n_steps[t];
+      const double beta = beta_steps[t];
+      const float* warm = nullptr;
+      int64_t warm_ld = 0, warm_k = 0;
+      if (t == 0) {
+        if (V0 != nullptr && k0 > 0) {
+          warm = V0;
+          warm_ld = ldv0;
+          warm_k = k0;
+        }
+      } else if (n == n_prev) {
+        warm = c.psi(last);
+        warm_ld = kk;
+        warm_k = kk;
+      } else {
+        // Nystrom extension of the matching-beta step of the previous prefix
+        int64_t src = last;
+        for (size_t e = 0; e < level_beta.size(); ++e)
+          if (level_beta[e] == beta_steps[t]) src = level_slot[e];
+        nystrom_extend(c, X, xt, D, ldx, n_prev, n, beta_steps[src], alpha, c.psi(src), c.q(src),
+                       lam[src], kk, st);
+        warm = c.ext;
+        warm_ld = kk;
+        warm_k = kk;
+        level_beta.clear();
+        level_slot.clear();
+      }
+      // normalisation and eigensolve on the prefix
+      DegreeWs dv = degree_view(c.sw.deg, n);
+      degree_run(dv, X, xt, n, D, ldx, beta, alpha, c.q(t), c.sw.d, c.sw.s, c.sw.s_off, true, st);
+      const SolverLayout lay = solver_layout(n, int(b), kk, o);
+      FD_REQUIRE(lay.mm <= c.sw.mm_cap, FD_ERR_INVALID_ARG, "internal: basis wider than carved");
+      ProductWs pv = product_view(c.sw.prod, dv.rows, dv.cols, int(b));
+      Lanczos L(c.sw, pv, st, n, int(b), lay.mm, o.seed + uint64_t(t) * 7919u);
+      SolveResult R = lanczos_solve(c.sw, L, lay, kk, warm, warm_k, warm_ld, 0.5, o);
+      copy_cols(c.sw.Q, lay.mm, c.psi(t), kk, n, kk, c.sw.d, -0.5, st);
+      double s_off = 0.0;
+      FD_HIP_CHECK(hipMemcpyAsync(&s_off, c.sw.s_off, sizeof(double), hipMemcpyDeviceToHost, st));
+      FD_HIP_CHECK(hipStreamSynchronize(st));
+      lam[t] = R.theta;
+      lam[t].resize(kk, 0.0);
+      for (int i = 0; i < kk; ++i) evals[t * kk + i] = lam[t][i];
+      const double secs =
+          std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
+      fd_lanczos_info info{};
+      fill_info(&info, R, s_off, secs, kk);
+      if (per_step != nullptr) per_step[t] = info;
+      any_unconverged = any_unconverged || !R.converged;
+      level_beta.push_back(beta_steps[t]);
+      level_slot.push_back(t);
+      n_prev = n;
+      last = t;
+      done = t + 1;
+      if (t == nsteps - 1 || (stop_at_wall && info.wall)) {
+        copy_cols(c.sw.Q, lay.mm, evecs, kk, n, kk, nullptr, 0.0, st);
+        if (psi != nullptr) copy_cols(c.psi(t), kk, psi, kk, n, kk, nullptr, 0.0, st);
+        FD_HIP_CHECK(hipStreamSynchronize(st));
+      }
+      if (stop_at_wall && info.wall) {
+        status = FD_ERR_PERRON_WALL;
+        break;
+      }
+    }
+    if (steps_done != nullptr) *steps_done = done;
+    if (status == FD_ERR_PERRON_WALL) {
+      set_error("stopped at the Perron wall after step " + std::to_string(done - 1));
+      return status;
+    }
+    if (any_unconverged) {
+      set_error("at least one step stopped before all k pairs converged");
+      return FD_ERR_NOT_CONVERGED;
+    }
+    set_error("");
+    return FD_OK;
+  } catch (const Error& e) {
+    set_error(e.msg);
+    return e.status;
+  } catch (const std::exception& e) {
+    set_error(std::string("internal error: ") + e.what());
+    return FD_ERR_HIP;
+  }
 }
 
 }  // extern "C"
