@@ -33,6 +33,10 @@ PEAK_FP32_MFMA_TFLOPS = 157.3
 PEAK_HBM_GBS = 8000.0
 
 
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
 def cpu_model() -> str:
     try:
         with open("/proc/cpuinfo") as fh:
@@ -82,6 +86,61 @@ def lanczos_leg(fd, torch, dev) -> dict:
             "max_residual": e.info["max_residual"]}
 
 
+def molecule_leg(fd, torch, dev) -> dict:
+    """Top-64 eigenpairs at N = 2^20 (molecule-like manifold, D = 30, b = 32)."""
+    from paper_2609_38198_amd import inputs
+    w = inputs.molecule()
+    X = torch.from_numpy(w.X).to(dev)
+    beta = float(w.betas[0])
+    torch.cuda.synchronize()
+    fd.fd_profile_read(fd.FD_KERNEL_PRODUCT)
+    fd.fd_profile_read(fd.FD_KERNEL_ROWSUM)
+    fd.fd_profile_enable(True)
+    t0 = time.perf_counter()
+    log(f"molecule leg: N={w.N} beta={beta:.5f} start")
+    e = fd.fd_block_lanczos(X, beta, w.k, w.b, allow_not_converged=True,
+                            opts=fd.default_opts(verbose=1))
+    torch.cuda.synchronize()
+    t = time.perf_counter() - t0
+    fd.fd_profile_enable(False)
+    pms, pn = fd.fd_profile_read(fd.FD_KERNEL_PRODUCT)
+    rms, rn = fd.fd_profile_read(fd.FD_KERNEL_ROWSUM)
+    N, D, b = w.N, w.D, w.b
+    avg = pms * 1e-3 / max(pn, 1)
+    flops = 2.0 * N * N * (D + b)
+    return {"workload": f"molecule-like N={N} D={D} beta={beta:.5f} b={b} k={w.k} alpha=0.5",
+            "seconds": t, "status": e.status, "block_matvecs": e.info["block_matvecs"],
+            "restarts": e.info["restarts"], "nconv": e.info["nconv"],
+            "max_residual": e.info["max_residual"], "gap_perron": e.info["gap_perron"],
+            "product_avg_ms": avg * 1e3, "product_tflops": flops / avg / 1e12,
+            "product_frac_fp32_mfma": flops / avg / 1e12 / PEAK_FP32_MFMA_TFLOPS,
+            "product_total_s": pms * 1e-3, "rowsum_total_s": rms * 1e-3,
+            "evals_head": e.evals[:4], "evals_tail": e.evals[-2:]}
+
+
+def continuation_leg(fd, torch, dev) -> dict:
+    """Noisy 6-torus ladder: n in {16K, 65K, 262K} x beta doubling 0.5 -> 8, k = 64, b = 32."""
+    from paper_2609_38198_amd import inputs
+    w = inputs.torus6_noisy()
+    X = torch.from_numpy(w.X).to(dev)
+    ns, bs = [], []
+    for n in w.extra["n_ladder"]:
+        for beta in w.betas:
+            ns.append(n)
+            bs.append(beta)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    log("continuation leg: start")
+    lad = fd.fd_continuation(X, ns, bs, w.k, w.b, allow=(0, 5), opts=fd.default_opts(verbose=1))
+    torch.cuda.synchronize()
+    t = time.perf_counter() - t0
+    return {"workload": "noisy 6-torus N=262144 D=12 k=64 b=32, n in {16384, 65536, 262144} x "
+                        "beta in {0.5, 1, 2, 4, 8}", "seconds": t, "status": lad.status,
+            "steps": [{"n": n, "beta": beta, "matvecs": i["block_matvecs"], "nconv": i["nconv"],
+                       "gap": i["gap_perron"], "wall": i["wall"], "s": i["seconds"]}
+                      for n, beta, i in zip(ns, bs, lad.info)]}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -90,6 +149,8 @@ def main() -> int:
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--lanczos", action="store_true")
+    ap.add_argument("--molecule", action="store_true")
+    ap.add_argument("--continuation", action="store_true")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -176,6 +237,10 @@ def main() -> int:
     }
     if args.lanczos:
         rec["lanczos"] = lanczos_leg(fd, torch, dev)
+    if args.molecule:
+        rec["lanczos_molecule"] = molecule_leg(fd, torch, dev)
+    if args.continuation:
+        rec["continuation"] = continuation_leg(fd, torch, dev)
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(wl.X, 2.0, b, args.cpu_seconds)
     print(json.dumps(rec), flush=True)

@@ -70,7 +70,7 @@ typedef struct fd_lanczos_opts {
   int32_t keep;             /* Ritz vectors kept at restart beyond k (-1 = automatic: b) */
   int32_t max_matvecs;      /* stop after this many block products (0 = no limit). A run that
                                stops this way returns FD_ERR_NOT_CONVERGED with valid Ritz pairs */
-  int32_t reserved;
+  int32_t verbose;          /* non-zero: one progress line per restart cycle on stderr */
   uint64_t seed;            /* seed of the counter-based generator for start/fill vectors */
 } fd_lanczos_opts;
 

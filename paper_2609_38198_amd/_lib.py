@@ -47,7 +47,7 @@ class FdError(RuntimeError):
 class LanczosOpts(ctypes.Structure):
     _fields_ = [("tol", ctypes.c_double), ("max_restarts", ctypes.c_int32),
                 ("max_basis_blocks", ctypes.c_int32), ("keep", ctypes.c_int32),
-                ("max_matvecs", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("max_matvecs", ctypes.c_int32), ("verbose", ctypes.c_int32),
                 ("seed", ctypes.c_uint64)]
 
 

@@ -164,7 +164,7 @@ void fd_lanczos_default_opts(fd_lanczos_opts* opts) {
   opts->max_basis_blocks = 0;
   opts->keep = -1;
   opts->max_matvecs = 0;
-  opts->reserved = 0;
+  opts->verbose = 0;
   opts->seed = 0x5eed;
 }
 

@@ -20,6 +20,7 @@
 #include <algorithm>
 #include <chrono>
 #include <cmath>
+#include <cstdio>
 #include <vector>
 
 #include "fd_linalg.hpp"
@@ -252,6 +253,16 @@ static SolveResult lanczos_solve(SolverWs& w, Lanczos& L, const SolverLayout& la
       std::swap(w.W, w.Wa);
       int nconv = 0;
       while (nconv < k && rs[nconv] <= o.tol) ++nconv;
+      if (o.verbose) {
+        double worst = 0.0;
+        for (int c = 0; c < std::min(k, nkeep); ++c) worst = std::max(worst, rs[c]);
+        std::fprintf(stderr,
+                     "[fd_lanczos] N=%lld cycle=%d basis=%d products=%d converged=%d/%d "
+                     "max_residual=%.3e theta0=%.9f theta_k-1=%.6e\n",
+                     (long long)N, R.restarts, m, L.matvecs, nconv, k, worst, th[0],
+                     th[std::min(k, m) - 1]);
+        std::fflush(stderr);
+      }
       R.nconv = nconv;
       R.theta.assign(th.begin(), th.begin() + std::min(m, std::max(k, 2)));
       R.res.assign(rs.begin(), rs.begin() + std::min(nkeep, k));
