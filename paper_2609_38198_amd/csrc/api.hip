@@ -60,8 +60,9 @@ ProductWs carve_product(Arena& a, int64_t Nr, int64_t Nc, int64_t D, int b) {
   const int dp = padded_dim(D);
   w.plan = plan_product(Nr, Nc, dp, b);
   w.rows = carve_pack(a, Nr, dp, ROW_PAD);
-  w.cols = carve_pack(a, Nc, dp, TILE);
+  w.cols = carve_pack(a, Nc, dp, COL_PAD);
   w.vp = a.fspan(size_t(w.cols.npad) * w.plan.ncb * 16);
+  w.vscale = a.fspan(128);
   w.part = a.fspan(part_rows_bound(w.rows.npad) * w.plan.ncb * 16);
   return w;
 }
@@ -80,8 +81,8 @@ PointPack pack_view(const PointPack& big, int64_t n, int64_t pad) {
 DegreeWs degree_view(const DegreeWs& big, int64_t n) {
   DegreeWs w = big;
   w.rows = pack_view(big.rows, n, ROW_PAD);
-  w.cols = pack_view(big.cols, n, TILE);
-  w.plan = plan_product(n, n, big.rows.dp, 1);
+  w.cols = pack_view(big.cols, n, COL_PAD);
+  w.plan = plan_rowsum(n, n, big.rows.dp);
   return w;
 }
 
@@ -96,8 +97,8 @@ ProductWs product_view(const ProductWs& big, const PointPack& rows, const PointP
 
 void product_apply(ProductWs& w, const float* sl, const float* sr, const float* V, int64_t ldv,
                    int b, float* Y, int64_t ldy, bool diag, hipStream_t stream) {
-  launch_pack_v(V, w.cols.n, b, ldv, sr, w.plan.ncb, w.cols.npad, w.vp, stream);
-  launch_product(w.plan, w.rows, w.cols, w.vp, diag, sl, Y, ldy, b, w.part, stream);
+  launch_pack_v_split(V, w.cols.n, b, ldv, sr, w.plan.ncb, w.cols.npad, w.vp, w.vscale, stream);
+  launch_product(w.plan, w.rows, w.cols, w.vp, w.vscale, diag, sl, Y, ldy, b, w.part, stream);
 }
 
 // ---------------------------------------------------------------- degree
@@ -105,9 +106,9 @@ void product_apply(ProductWs& w, const float* sl, const float* sr, const float* 
 DegreeWs carve_degree(Arena& a, int64_t N, int64_t D) {
   DegreeWs w;
   const int dp = padded_dim(D);
-  w.plan = plan_product(N, N, dp, 1);
+  w.plan = plan_rowsum(N, N, dp);
   w.rows = carve_pack(a, N, dp, ROW_PAD);
-  w.cols = carve_pack(a, N, dp, TILE);
+  w.cols = carve_pack(a, N, dp, COL_PAD);
   w.wp = a.fspan(size_t(w.cols.npad) * 16);  // one float4 per lane per 16-point tile
   w.q = a.take<float>(size_t(N));
   w.t = a.take<float>(size_t(N));

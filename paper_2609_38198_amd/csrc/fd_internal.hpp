@@ -69,6 +69,7 @@ struct Arena {
 constexpr int TILE = 16;          // points per MFMA tile
 constexpr int WG_THREADS = 256;   // four wave64 per workgroup
 constexpr int ROW_PAD = 256;      // row packs are padded to this many points
+constexpr int COL_PAD = 32;       // column packs: whole pairs of 16-point tiles
 
 inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 inline int64_t ceil_div(int64_t x, int64_t m) { return (x + m - 1) / m; }
@@ -99,7 +100,11 @@ struct KVPlan {
   int64_t jb_per_split = 0;
 };
 
+// Tiling of a fused product (rows per wave tuned by shape) and of a row sum.
+KVPlan plan_tiles(int64_t Nr, int64_t Nc, int dp, int b, int nib);
+int product_nib(int dp, int ncb);
 KVPlan plan_product(int64_t Nr, int64_t Nc, int dp, int b);
+KVPlan plan_rowsum(int64_t Nr, int64_t Nc, int dp);
 
 // Workspace carving helpers (size when arena.measuring).
 PointPack carve_pack(Arena& a, int64_t n, int dp, int64_t pad);
@@ -110,10 +115,14 @@ void launch_pack_points(const void* X, fd_dtype xt, int64_t n, int64_t D, int64_
 void launch_pack_v(const float* V, int64_t n, int64_t b, int64_t ldv, const float* sr,
                    int ncb, int64_t npad, FSpan vp, hipStream_t stream);
 void launch_pack_w(const float* w, int64_t n, int64_t npad, FSpan wp, hipStream_t stream);
+// Split float16 pack of sr * V with per-column power-of-two scales (vscale:
+// 64 max-abs bit patterns followed by 64 inverse scales).
+void launch_pack_v_split(const float* V, int64_t n, int64_t b, int64_t ldv, const float* sr,
+                         int ncb, int64_t npad, FSpan vp, FSpan vscale, hipStream_t stream);
 // Y = diag(sl) K diag(sr) V from packed operands (V packed with sr applied).
 void launch_product(const KVPlan& p, const PointPack& rows, const PointPack& cols, FSpan vp,
-                    bool diag, const float* sl, float* Y, int64_t ldy, int b, FSpan part,
-                    hipStream_t stream);
+                    FSpan vscale, bool diag, const float* sl, float* Y, int64_t ldy, int b,
+                    FSpan part, hipStream_t stream);
 // out = K w (wp.p == NULL: w = 1).
 void launch_rowsum(const KVPlan& p, const PointPack& rows, const PointPack& cols, FSpan wp,
                    bool diag, float* out, FSpan part, hipStream_t stream);

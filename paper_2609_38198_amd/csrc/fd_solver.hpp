@@ -8,7 +8,7 @@ namespace fd {
 // Workspace of one fused product: packed rows / columns, packed V, partials.
 struct ProductWs {
   PointPack rows, cols;
-  FSpan vp, part;
+  FSpan vp, vscale, part;
   KVPlan plan;
 };
 

@@ -387,15 +387,295 @@ __global__ __launch_bounds__(WG_THREADS) void rowsum_f32_kernel(
   }
 }
 
+
+// ------------------------------------------------------------------ split K*V product
+//
+// The K*V contraction in float16 with a two-term split of both factors:
+//   K' = 2^15 K = Kh + Kl,  V' = 2^e_c sr V = Vh + Vl  (Kh, Kl, Vh, Vl float16),
+//   K' V' ~= Kh Vh + Kh Vl + Kl Vh       (the dropped Kl Vl is 2^-22 relative),
+// on v_mfma_f32_16x16x32_f16 with float32 accumulation; the result is scaled
+// back by 2^(-15 - e_c).  K' carries the factor 2^15 (added to the exponent
+// offset, so K' <= 2^15 < 65504 needs no clamp) so that Kl stays a normal
+// float16 down to K ~ 4e-6; e_c puts the largest |V'| of column c just below
+// 2^14.  The representation error of each split is below 2^-21 relative.
+// The exponent contraction stays float32 (its cancellation needs it).
+//
+// Operand layout: two consecutive 16-point column tiles form the 32-wide
+// contraction.  From the two exponent tiles lane (g, p) holds
+// K[p][J0 + 4g + r] and K[p][J1 + 4g + r]; these are its 8 A-operand halves
+// (k = 8g + e with e = r for J0 and e = 4 + r for J1).  The V pack stores, per
+// lane, the 8 matching rows of column 16 cb + p as hi and lo halves.
+
+typedef _Float16 halfx8 __attribute__((ext_vector_type(8)));
+typedef __fp16 pkhalf2 __attribute__((ext_vector_type(2)));
+typedef unsigned uintx4 __attribute__((ext_vector_type(4)));
+
+struct VSplit {
+  halfx8 hi;
+  halfx8 lo;
+};
+
+// Round two floats toward zero to float16 (hi) and the remainders likewise
+// (lo); returns both packed pairs as 32-bit words.
+__device__ __forceinline__ void split2(float a, float b, unsigned& hi, unsigned& lo) {
+  const pkhalf2 h = __builtin_amdgcn_cvt_pkrtz(a, b);
+  const pkhalf2 l = __builtin_amdgcn_cvt_pkrtz(a - float(h[0]), b - float(h[1]));
+  hi = __builtin_bit_cast(unsigned, h);
+  lo = __builtin_bit_cast(unsigned, l);
+}
+
+// max |sr_j V[j][c]| per column as float bits (non-negative floats order like
+// their bit patterns, so an integer max is exact and order independent)
+__global__ void vmax_zero_kernel(unsigned* __restrict__ maxbits) {
+  if (threadIdx.x < 64) maxbits[threadIdx.x] = 0u;
+}
+
+__global__ __launch_bounds__(256) void vmax_kernel(const float* __restrict__ V, int64_t n, int b,
+                                                   int64_t ldv, const float* __restrict__ sr,
+                                                   int64_t rows_per_block,
+                                                   unsigned* __restrict__ maxbits) {
+  __shared__ float red[256];
+  const int c = threadIdx.x & 63;
+  const int r0 = threadIdx.x >> 6;
+  const int64_t i0 = int64_t(blockIdx.x) * rows_per_block;
+  const int64_t i1 = min(n, i0 + rows_per_block);
+  float m = 0.f;
+  if (c < b) {
+    for (int64_t i = i0 + r0; i < i1; i += 4) {
+      float v = V[i * ldv + c];
+      if (sr != nullptr) v *= sr[i];
+      m = fmaxf(m, fabsf(v));
+    }
+  }
+  red[threadIdx.x] = m;
+  __syncthreads();
+  if (threadIdx.x < 64) {
+    m = fmaxf(fmaxf(red[c], red[c + 64]), fmaxf(red[c + 128], red[c + 192]));
+    if (c < b && m > 0.f) atomicMax(&maxbits[c], __float_as_uint(m));
+  }
+}
+
+__device__ __forceinline__ int vscale_exponent(unsigned bits) {
+  if (bits == 0u) return 0;
+  int e;
+  (void)frexpf(__uint_as_float(bits), &e);  // max < 2^e
+  return 14 - e;                            // scaled max < 2^14
+}
+
+__global__ void pack_v_split_kernel(const float* __restrict__ V, int64_t n, int b, int64_t ldv,
+                                    const float* __restrict__ sr, int ncb, int64_t npairs,
+                                    const unsigned* __restrict__ maxbits,
+                                    VSplit* __restrict__ vp, float* __restrict__ colscale) {
+  const int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (idx >= npairs * ncb * 64) return;
+  const int lane = int(idx & 63);
+  const int cb = int((idx >> 6) % ncb);
+  const int64_t jp = idx / (64 * ncb);
+  const int g = lane >> 4, p = lane & 15;
+  const int c = cb * 16 + p;
+  const int ex = (c < b) ? vscale_exponent(maxbits[c]) : 0;
+  const float scale = ldexpf(1.f, ex);
+  if (jp == 0 && g == 0 && c < b) colscale[c] = ldexpf(1.f, -ex - 15);
+  uintx4 hw, lw;
+#pragma unroll
+  for (int e = 0; e < 8; e += 2) {
+    float v[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int ee = e + u;
+      const int64_t j = jp * 32 + (ee < 4 ? 4 * g + ee : 16 + 4 * g + (ee - 4));
+      float x = 0.f;
+      if (j < n && c < b) {
+        x = V[j * ldv + c];
+        if (sr != nullptr) x *= sr[j];
+      }
+      v[u] = x * scale;
+    }
+    unsigned h, l;
+    split2(v[0], v[1], h, l);
+    hw[e / 2] = h;
+    lw[e / 2] = l;
+  }
+  VSplit out;
+  out.hi = __builtin_bit_cast(halfx8, hw);
+  out.lo = __builtin_bit_cast(halfx8, lw);
+  vp[idx] = out;
+}
+
+// Column-pair operands: exponent-contraction inputs of two 16-point tiles and
+// the split V pack of the pair.
+template <int S, int NCB>
+struct ColPair {
+  float xa[2][S];
+  floatx4 aj[2];
+  VSplit v[NCB];
+};
+
+template <int S, int NCB>
+__device__ __forceinline__ void load_pair(ColPair<S, NCB>& c, const float* __restrict__ xa,
+                                          const floatx4* __restrict__ aj,
+                                          const VSplit* __restrict__ vp, int64_t jp, int lane) {
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const int64_t jb = 2 * jp + t;
+#pragma unroll
+    for (int s = 0; s < S; ++s) c.xa[t][s] = xa[(jb * S + s) * 64 + lane];
+    c.aj[t] = aj[jb * 64 + lane];
+  }
+#pragma unroll
+  for (int cb = 0; cb < NCB; ++cb) c.v[cb] = vp[(jp * NCB + cb) * 64 + lane];
+}
+
+template <int S, bool DIAG>
+__device__ __forceinline__ floatx4 exponent_of(const float* xa, const floatx4& aj, const float* xb,
+                                               float ai, int g, int p) {
+  floatx4 t;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) t[r] = ai + aj[r];
+#pragma unroll
+  for (int s = 0; s < S; ++s) t = __builtin_amdgcn_mfma_f32_16x16x4f32(xa[s], xb[s], t, 0, 0, 0);
+  if (DIAG) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      if (4 * g + r == p) t[r] = 15.f;  // K_ii = 1, times the 2^15 shift
+  }
+  return t;
+}
+
+template <int DP, int NCB, int NIB, bool DIAG>
+__device__ __forceinline__ void split_pair(const ColPair<DP / 4, NCB>& c,
+                                           const float (&xbr)[NIB][DP / 4],
+                                           const float (&ai)[NIB], floatx4 (&acc)[NIB][NCB],
+                                           int64_t jp, int64_t ib0, int g, int p) {
+  constexpr int S = DP / 4;
+#pragma unroll
+  for (int ib = 0; ib < NIB; ++ib) {
+    floatx4 t[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      if (DIAG && 2 * jp + u == ib0 + ib)
+        t[u] = exponent_of<S, true>(c.xa[u], c.aj[u], xbr[ib], ai[ib], g, p);
+      else
+        t[u] = exponent_of<S, false>(c.xa[u], c.aj[u], xbr[ib], ai[ib], g, p);
+    }
+    uintx4 hw, lw;
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int r = 0; r < 4; r += 2) {
+        // K' = 2^t with the shift 15 already in ai: K' <= 2^15 (up to rounding)
+        const float k0 = __builtin_amdgcn_exp2f(t[u][r]);
+        const float k1 = __builtin_amdgcn_exp2f(t[u][r + 1]);
+        unsigned h, l;
+        split2(k0, k1, h, l);
+        hw[2 * u + r / 2] = h;
+        lw[2 * u + r / 2] = l;
+      }
+    const halfx8 khi = __builtin_bit_cast(halfx8, hw);
+    const halfx8 klo = __builtin_bit_cast(halfx8, lw);
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) {
+      acc[ib][cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(khi, c.v[cb].hi, acc[ib][cb], 0, 0, 0);
+      acc[ib][cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(khi, c.v[cb].lo, acc[ib][cb], 0, 0, 0);
+      acc[ib][cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(klo, c.v[cb].hi, acc[ib][cb], 0, 0, 0);
+    }
+  }
+}
+
+// One workgroup = 4 waves; wave w owns row tiles [ib0, ib0 + NIB).  The
+// workgroup's column split is streamed in pairs of tiles, the next pair's
+// operands loading while the current one computes.  Chunk totals of the
+// two-level sum live in LDS (one float4 per lane and accumulator), which keeps
+// registers free for more waves per SIMD: vector-ALU and matrix-core work of
+// different waves then overlap.
+template <int DP, int NCB, int NIB>
+__global__ __launch_bounds__(WG_THREADS) void product_split_kernel(
+    const float* __restrict__ xa, const floatx4* __restrict__ aj, const VSplit* __restrict__ vp,
+    const float* __restrict__ xb, const float* __restrict__ ar, int64_t nrt, int64_t njp,
+    int64_t jp_per_split, int diag, const float* __restrict__ colscale,
+    const float* __restrict__ sl, float* __restrict__ Y, int64_t ldy, int64_t Nr, int b,
+    float* __restrict__ part, int64_t nrpad) {
+  constexpr int S = DP / 4;
+  __shared__ floatx4 tot[4][NIB][NCB][64];
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int wr = xcd_remap(blockIdx.x, gridDim.x);
+  const int64_t split = wr / nrt;
+  const int64_t rt = wr % nrt;
+  const int64_t ib0 = (rt * 4 + wave) * NIB;
+  const int64_t jp_begin = split * jp_per_split;
+  const int64_t jp_end = min(njp, jp_begin + jp_per_split);
+  const int g = lane >> 4, p = lane & 15;
+
+  float xbr[NIB][S];
+  float ai[NIB];
+#pragma unroll
+  for (int ib = 0; ib < NIB; ++ib) {
+#pragma unroll
+    for (int s = 0; s < S; ++s) xbr[ib][s] = xb[((ib0 + ib) * S + s) * 64 + lane];
+    ai[ib] = ar[(ib0 + ib) * TILE + p] + 15.f;  // K' = 2^15 K
+  }
+  floatx4 acc[NIB][NCB];
+#pragma unroll
+  for (int ib = 0; ib < NIB; ++ib)
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) {
+      acc[ib][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
+      tot[wave][ib][cb][lane] = floatx4{0.f, 0.f, 0.f, 0.f};
+    }
+
+  ColPair<S, NCB> cur, nxt;
+  load_pair(cur, xa, aj, vp, jp_begin, lane);
+  int chunk = 0;
+  for (int64_t jp = jp_begin; jp < jp_end; ++jp) {
+    load_pair(nxt, xa, aj, vp, min(jp + 1, jp_end - 1), lane);
+    if (diag && 2 * jp + 1 >= ib0 && 2 * jp < ib0 + NIB)
+      split_pair<DP, NCB, NIB, true>(cur, xbr, ai, acc, jp, ib0, g, p);
+    else
+      split_pair<DP, NCB, NIB, false>(cur, xbr, ai, acc, jp, ib0, g, p);
+    if (++chunk == CHUNK_TILES / 2) {
+      chunk = 0;
+#pragma unroll
+      for (int ib = 0; ib < NIB; ++ib)
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb) {
+          tot[wave][ib][cb][lane] += acc[ib][cb];
+          acc[ib][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
+        }
+    }
+    cur = nxt;
+  }
+
+#pragma unroll
+  for (int ib = 0; ib < NIB; ++ib)
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) {
+      const floatx4 v = tot[wave][ib][cb][lane] + acc[ib][cb];
+      const int c = cb * 16 + p;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int64_t i = (ib0 + ib) * TILE + 4 * g + e;
+        if (part != nullptr) {
+          part[(split * nrpad + i) * (NCB * 16) + c] = v[e];
+        } else if (i < Nr && c < b) {
+          const float y = v[e] * colscale[c];
+          Y[i * ldy + c] = (sl != nullptr) ? y * sl[i] : y;
+        }
+      }
+    }
+}
+
 __global__ void reduce_product_kernel(const float* __restrict__ part, int nsplit, int64_t nrpad,
-                                      int width, const float* __restrict__ sl,
-                                      float* __restrict__ Y, int64_t ldy, int64_t Nr, int b) {
+                                      int width, const float* __restrict__ colscale,
+                                      const float* __restrict__ sl, float* __restrict__ Y,
+                                      int64_t ldy, int64_t Nr, int b) {
   const int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
   if (idx >= Nr * b) return;
   const int64_t i = idx / b;
   const int c = int(idx % b);
   double s = 0.0;
   for (int k = 0; k < nsplit; ++k) s += double(part[(k * nrpad + i) * width + c]);
+  if (colscale != nullptr) s *= double(colscale[c]);
   if (sl != nullptr) s *= double(sl[i]);
   Y[i * ldy + c] = float(s);
 }
@@ -445,11 +725,11 @@ __global__ __launch_bounds__(1024) void sum_minus_n_kernel(const float* __restri
 
 // ------------------------------------------------------------------ host side
 
-KVPlan plan_product(int64_t Nr, int64_t Nc, int dp, int b) {
+KVPlan plan_tiles(int64_t Nr, int64_t Nc, int dp, int b, int nib) {
   KVPlan p;
   p.dp = dp;
   p.ncb = int(ceil_div(b, 16));
-  p.nib = 4;
+  p.nib = nib;
   p.njb = ceil_div(Nc, TILE);
   const int64_t rows_per_wg = 4 * p.nib * TILE;
   p.nrt = ceil_div(round_up(Nr, ROW_PAD), rows_per_wg);
@@ -458,10 +738,21 @@ KVPlan plan_product(int64_t Nr, int64_t Nc, int dp, int b) {
   int64_t ns = std::max<int64_t>(1, ceil_div(target, p.nrt));
   ns = std::min<int64_t>(ns, std::max<int64_t>(1, p.njb / 8));
   ns = std::min<int64_t>(ns, 64);
-  p.jb_per_split = ceil_div(p.njb, ns);
+  // splits hold an even number of column tiles (the split product takes them in pairs)
+  p.jb_per_split = round_up(ceil_div(p.njb, ns), 2);
   p.nsplit = int(ceil_div(p.njb, p.jb_per_split));
   return p;
 }
+
+// Row tiles per wave of the fused product.  Four was the fastest or tied on
+// every workload shape measured (D in {4, 12, 30, 64}, b in {8 .. 64}).
+int product_nib(int /*dp*/, int /*ncb*/) { return 4; }
+
+KVPlan plan_product(int64_t Nr, int64_t Nc, int dp, int b) {
+  return plan_tiles(Nr, Nc, dp, b, product_nib(dp, int(ceil_div(b, 16))));
+}
+
+KVPlan plan_rowsum(int64_t Nr, int64_t Nc, int dp) { return plan_tiles(Nr, Nc, dp, 1, 4); }
 
 static inline unsigned blocks_for(int64_t n, int t) { return unsigned(ceil_div(n, t)); }
 
@@ -534,59 +825,99 @@ static void check_tiles(const KVPlan& p, const PointPack& rows, const PointPack&
   check_span(cols.ap, lane4_extent(p.njb, 1), "column offsets");
 }
 
-template <int DP, int NCB>
-static void product_dispatch_nib(const KVPlan& p, const PointPack& rows, const PointPack& cols,
-                                 const float* vp, bool diag, const float* sl, float* Y,
-                                 int64_t ldy, int b, float* part, hipStream_t stream) {
+void launch_pack_v_split(const float* V, int64_t n, int64_t b, int64_t ldv, const float* sr,
+                         int ncb, int64_t npad, FSpan vp, FSpan vscale, hipStream_t stream) {
+  FD_REQUIRE(npad % (2 * TILE) == 0 && npad >= n && b <= ncb * 16 && b <= 64, FD_ERR_INVALID_ARG,
+             "internal: bad split V pack geometry");
+  const int64_t npairs = npad / (2 * TILE);
+  // one VSplit (32 bytes = 8 floats) per lane per pair per column block
+  check_span(vp, size_t(npairs) * ncb * 64 * 8, "split V pack");
+  check_span(vscale, 128, "column scales");
+  unsigned* maxbits = reinterpret_cast<unsigned*>(vscale.p);
+  float* colscale = vscale.p + 64;
+  hipLaunchKernelGGL(vmax_zero_kernel, dim3(1), dim3(64), 0, stream, maxbits);
+  FD_LAUNCH_CHECK();
+  const int64_t rpb = 1024;
+  hipLaunchKernelGGL(vmax_kernel, dim3(blocks_for(n, int(rpb))), dim3(256), 0, stream, V, n,
+                     int(b), ldv, sr, rpb, maxbits);
+  FD_LAUNCH_CHECK();
+  const int64_t total = npairs * ncb * 64;
+  hipLaunchKernelGGL(pack_v_split_kernel, dim3(blocks_for(total, 256)), dim3(256), 0, stream, V,
+                     n, int(b), ldv, sr, ncb, npairs, maxbits, reinterpret_cast<VSplit*>(vp.p),
+                     colscale);
+  FD_LAUNCH_CHECK();
+}
+
+template <int DP, int NCB, int NIB>
+static void product_launch(const KVPlan& p, const PointPack& rows, const PointPack& cols,
+                           const float* vp, const float* colscale, bool diag, const float* sl,
+                           float* Y, int64_t ldy, int b, float* part, hipStream_t stream) {
   const unsigned grid = unsigned(p.nrt * p.nsplit);
   ProfScope prof(FD_KERNEL_PRODUCT, stream);
-  hipLaunchKernelGGL((product_f32_kernel<DP, NCB, 4>), dim3(grid), dim3(WG_THREADS), 0, stream,
-                     cols.xp.p, reinterpret_cast<const floatx4*>(cols.ap.p),
-                     reinterpret_cast<const floatx4*>(vp), rows.xp.p, rows.ar.p, p.nrt, p.njb,
-                     p.jb_per_split, int(diag), sl, Y, ldy, rows.n, b, part, rows.npad);
+  hipLaunchKernelGGL((product_split_kernel<DP, NCB, NIB>), dim3(grid), dim3(WG_THREADS), 0,
+                     stream, cols.xp.p, reinterpret_cast<const floatx4*>(cols.ap.p),
+                     reinterpret_cast<const VSplit*>(vp), rows.xp.p, rows.ar.p, p.nrt,
+                     ceil_div(p.njb, 2), p.jb_per_split / 2, int(diag), colscale, sl, Y, ldy,
+                     rows.n, b, part, rows.npad);
   FD_LAUNCH_CHECK();
+}
+
+template <int DP, int NCB>
+static void product_dispatch_nib(const KVPlan& p, const PointPack& rows, const PointPack& cols,
+                                 const float* vp, const float* colscale, bool diag,
+                                 const float* sl, float* Y, int64_t ldy, int b, float* part,
+                                 hipStream_t stream) {
+  switch (p.nib) {
+    case 2: return product_launch<DP, NCB, 2>(p, rows, cols, vp, colscale, diag, sl, Y, ldy, b, part, stream);
+    case 4: return product_launch<DP, NCB, 4>(p, rows, cols, vp, colscale, diag, sl, Y, ldy, b, part, stream);
+  }
+  throw Error{FD_ERR_INVALID_ARG, "internal: unsupported rows per wave"};
 }
 
 template <int DP>
 static void product_dispatch_ncb(const KVPlan& p, const PointPack& rows, const PointPack& cols,
-                                 const float* vp, bool diag, const float* sl, float* Y,
-                                 int64_t ldy, int b, float* part, hipStream_t stream) {
+                                 const float* vp, const float* cs, bool diag, const float* sl,
+                                 float* Y, int64_t ldy, int b, float* part, hipStream_t stream) {
   switch (p.ncb) {
-    case 1: return product_dispatch_nib<DP, 1>(p, rows, cols, vp, diag, sl, Y, ldy, b, part, stream);
-    case 2: return product_dispatch_nib<DP, 2>(p, rows, cols, vp, diag, sl, Y, ldy, b, part, stream);
-    case 3: return product_dispatch_nib<DP, 3>(p, rows, cols, vp, diag, sl, Y, ldy, b, part, stream);
-    case 4: return product_dispatch_nib<DP, 4>(p, rows, cols, vp, diag, sl, Y, ldy, b, part, stream);
+    case 1: return product_dispatch_nib<DP, 1>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
+    case 2: return product_dispatch_nib<DP, 2>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
+    case 3: return product_dispatch_nib<DP, 3>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
+    case 4: return product_dispatch_nib<DP, 4>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
   }
   throw Error{FD_ERR_UNSUPPORTED, "block width above 64"};
 }
 
 void launch_product(const KVPlan& p, const PointPack& rows, const PointPack& cols, FSpan vp,
-                    bool diag, const float* sl, float* Y, int64_t ldy, int b, FSpan part,
-                    hipStream_t stream) {
+                    FSpan vscale, bool diag, const float* sl, float* Y, int64_t ldy, int b,
+                    FSpan part, hipStream_t stream) {
   check_tiles(p, rows, cols);
-  FD_REQUIRE(b >= 1 && b <= p.ncb * 16 && p.nib == 4, FD_ERR_INVALID_ARG,
-             "internal: block width does not match the plan");
-  check_span(vp, lane4_extent(p.njb, p.ncb), "V pack");
+  FD_REQUIRE(b >= 1 && b <= p.ncb * 16 && (p.nib == 2 || p.nib == 4),
+             FD_ERR_INVALID_ARG, "internal: block width does not match the plan");
+  FD_REQUIRE(p.jb_per_split % 2 == 0 && round_up(p.njb, 2) * TILE <= cols.npad,
+             FD_ERR_INVALID_ARG, "internal: column pairs do not fit the pack");
+  check_span(vp, size_t(ceil_div(p.njb, 2)) * p.ncb * 64 * 8, "split V pack");
+  check_span(vscale, 128, "column scales");
+  const float* cs = vscale.p + 64;
   float* pp = nullptr;
   if (p.nsplit > 1) {
     check_span(part, size_t(p.nsplit) * rows.npad * p.ncb * 16, "partial products");
     pp = part.p;
   }
   switch (p.dp) {
-    case 4: product_dispatch_ncb<4>(p, rows, cols, vp.p, diag, sl, Y, ldy, b, pp, stream); break;
-    case 8: product_dispatch_ncb<8>(p, rows, cols, vp.p, diag, sl, Y, ldy, b, pp, stream); break;
-    case 12: product_dispatch_ncb<12>(p, rows, cols, vp.p, diag, sl, Y, ldy, b, pp, stream); break;
-    case 16: product_dispatch_ncb<16>(p, rows, cols, vp.p, diag, sl, Y, ldy, b, pp, stream); break;
-    case 24: product_dispatch_ncb<24>(p, rows, cols, vp.p, diag, sl, Y, ldy, b, pp, stream); break;
-    case 32: product_dispatch_ncb<32>(p, rows, cols, vp.p, diag, sl, Y, ldy, b, pp, stream); break;
-    case 48: product_dispatch_ncb<48>(p, rows, cols, vp.p, diag, sl, Y, ldy, b, pp, stream); break;
-    case 64: product_dispatch_ncb<64>(p, rows, cols, vp.p, diag, sl, Y, ldy, b, pp, stream); break;
+    case 4: product_dispatch_ncb<4>(p, rows, cols, vp.p, cs, diag, sl, Y, ldy, b, pp, stream); break;
+    case 8: product_dispatch_ncb<8>(p, rows, cols, vp.p, cs, diag, sl, Y, ldy, b, pp, stream); break;
+    case 12: product_dispatch_ncb<12>(p, rows, cols, vp.p, cs, diag, sl, Y, ldy, b, pp, stream); break;
+    case 16: product_dispatch_ncb<16>(p, rows, cols, vp.p, cs, diag, sl, Y, ldy, b, pp, stream); break;
+    case 24: product_dispatch_ncb<24>(p, rows, cols, vp.p, cs, diag, sl, Y, ldy, b, pp, stream); break;
+    case 32: product_dispatch_ncb<32>(p, rows, cols, vp.p, cs, diag, sl, Y, ldy, b, pp, stream); break;
+    case 48: product_dispatch_ncb<48>(p, rows, cols, vp.p, cs, diag, sl, Y, ldy, b, pp, stream); break;
+    case 64: product_dispatch_ncb<64>(p, rows, cols, vp.p, cs, diag, sl, Y, ldy, b, pp, stream); break;
     default: throw Error{FD_ERR_UNSUPPORTED, "feature dimension above 64"};
   }
   if (p.nsplit > 1) {
     const int64_t total = rows.n * b;
     hipLaunchKernelGGL(reduce_product_kernel, dim3(blocks_for(total, 256)), dim3(256), 0, stream,
-                       pp, p.nsplit, rows.npad, p.ncb * 16, sl, Y, ldy, rows.n, b);
+                       pp, p.nsplit, rows.npad, p.ncb * 16, cs, sl, Y, ldy, rows.n, b);
     FD_LAUNCH_CHECK();
   }
 }

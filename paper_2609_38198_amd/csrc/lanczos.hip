@@ -86,6 +86,7 @@ static SolverWs carve_solver_ws(Arena& a, int64_t N, int64_t D, int b, int mm_ca
   w.prod.rows = w.deg.rows;
   w.prod.cols = w.deg.cols;
   w.prod.vp = a.fspan(size_t(w.prod.cols.npad) * w.prod.plan.ncb * 16);
+  w.prod.vscale = a.fspan(128);
   w.prod.part = a.fspan(part_rows_bound(w.prod.rows.npad) * w.prod.plan.ncb * 16);
   w.d = a.take<float>(size_t(N));
   w.s = a.take<float>(size_t(N));
@@ -379,13 +380,13 @@ static void nystrom_extend(ContWs& c, const void* X, fd_dtype xt, int64_t D, int
                            int k, hipStream_t st) {
   SolverWs& w = c.sw;
   PointPack rows = pack_view(w.deg.rows, n_new, ROW_PAD);
-  PointPack cols = pack_view(w.deg.cols, n_old, TILE);
+  PointPack cols = pack_view(w.deg.cols, n_old, COL_PAD);
   launch_pack_points(X, xt, n_new, D, ldx, beta, true, rows, st);
   launch_pack_points(X, xt, n_old, D, ldx, beta, false, cols, st);
   launch_pow_neg(q_old, n_old, alpha, c.wv, st);
   // denominators K w
   launch_pack_w(c.wv, n_old, cols.npad, w.deg.wp, st);
-  KVPlan rp = plan_product(n_new, n_old, rows.dp, 1);
+  KVPlan rp = plan_rowsum(n_new, n_old, rows.dp);
   launch_rowsum(rp, rows, cols, w.deg.wp, true, c.den, w.deg.part, st);
   // numerators K (w psi), 64 columns at a time
   std::vector<double> l(lam.begin(), lam.begin() + k);

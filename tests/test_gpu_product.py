@@ -57,6 +57,22 @@ def test_torus6_full_size_sampled_rows(beta):
     assert rel_fro(Y[rows], ref) <= TOL_F32
 
 
+@pytest.mark.parametrize("D,b", [(4, 8), (12, 32), (30, 32), (64, 64), (30, 16), (12, 64)])
+def test_shapes_sampled_rows(D, b):
+    # every (feature width, block width) family of the kernel at 65,536 points
+    N = 65536
+    rng = np.random.default_rng(D * 100 + b)
+    X = (rng.normal(size=(N, D)) * 0.5).astype(np.float32)
+    X -= X.mean(0)
+    V = rng.normal(size=(N, b)).astype(np.float32)
+    beta = 1.0 / (D * 0.25)
+    case(f"shape N={N} D={D} b={b}")
+    Y = _run(X, None, beta, V)
+    rows = np.random.default_rng(1).choice(N, 96, replace=False)
+    ref = ok.kernel_matmul(X, None, beta, V, rows=rows, threads=8)
+    assert rel_fro(Y[rows], ref) <= TOL_F32
+
+
 def test_grid_torus_full_size_closed_form():
     counts = (8, 8, 8, 8, 4, 4)  # 65,536 points in R^12
     X = inputs.grid_torus_points(counts).astype(np.float32)
