@@ -97,7 +97,8 @@ ProductWs product_view(const ProductWs& big, const PointPack& rows, const PointP
 
 void product_apply(ProductWs& w, const float* sl, const float* sr, const float* V, int64_t ldv,
                    int b, float* Y, int64_t ldy, bool diag, hipStream_t stream) {
-  launch_pack_v_split(V, w.cols.n, b, ldv, sr, w.plan.ncb, w.cols.npad, w.vp, w.vscale, stream);
+  launch_pack_v_for(w.rows, V, w.cols.n, b, ldv, sr, w.plan.ncb, w.cols.npad, w.vp, w.vscale,
+                    stream);
   launch_product(w.plan, w.rows, w.cols, w.vp, w.vscale, diag, sl, Y, ldy, b, w.part, stream);
 }
 

@@ -88,8 +88,14 @@ struct PointPack {
   FSpan xp, ap, ar;
   int64_t n = 0;      // real points
   int64_t npad = 0;   // padded points
-  int dp = 0;         // padded contraction width
+  int dp = 0;         // padded contraction width (float32 packs)
+  bool bf16 = false;  // filled from bfloat16 X: 16x16x32 bf16 layout, dc chunks of 32
+  int dc = 0;
+  double beta = 0.0;  // bandwidth the pack was made for
 };
+
+// Floats per point of a pack region (large enough for either pack kind).
+int pack_floats_per_point(int64_t D);
 
 // Plan of one fused product / degree launch.
 struct KVPlan {
@@ -115,6 +121,10 @@ void launch_pack_points(const void* X, fd_dtype xt, int64_t n, int64_t D, int64_
 void launch_pack_v(const float* V, int64_t n, int64_t b, int64_t ldv, const float* sr,
                    int ncb, int64_t npad, FSpan vp, hipStream_t stream);
 void launch_pack_w(const float* w, int64_t n, int64_t npad, FSpan wp, hipStream_t stream);
+// Pack sr * V for the product that matches the row pack's kind.
+void launch_pack_v_for(const PointPack& rows, const float* V, int64_t n, int64_t b, int64_t ldv,
+                       const float* sr, int ncb, int64_t npad, FSpan vp, FSpan vscale,
+                       hipStream_t stream);
 // Split float16 pack of sr * V with per-column power-of-two scales (vscale:
 // 64 max-abs bit patterns followed by 64 inverse scales).
 void launch_pack_v_split(const float* V, int64_t n, int64_t b, int64_t ldv, const float* sr,

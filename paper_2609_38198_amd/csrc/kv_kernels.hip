@@ -45,12 +45,18 @@ int padded_dim(int64_t D) {
   return 0;
 }
 
+int pack_floats_per_point(int64_t D) {
+  const int dp = padded_dim(D);
+  const int dc16 = int(ceil_div(D, 32)) * 16;
+  return std::max(dp, dc16);
+}
+
 PointPack carve_pack(Arena& a, int64_t n, int dp, int64_t pad) {
   PointPack p;
   p.n = n;
   p.npad = round_up(n, pad);
   p.dp = dp;
-  p.xp = a.fspan(size_t(p.npad) * dp);
+  p.xp = a.fspan(size_t(p.npad) * std::max(dp, int(ceil_div(dp, 32)) * 16));
   p.ap = a.fspan(size_t(p.npad) * 16);  // [tiles][64][4]: 16 floats per point
   p.ar = a.fspan(size_t(p.npad));
   return p;
@@ -665,6 +671,295 @@ __global__ __launch_bounds__(WG_THREADS) void product_split_kernel(
     }
 }
 
+
+// ------------------------------------------------------------------ bfloat16 inputs
+//
+// For X in bfloat16 the exponent contraction runs on v_mfma_f32_16x16x32_bf16:
+// products of bfloat16 values are exact in float32, so the tile
+//   C[j][i] = -(r_i + r_j) / 2 + x_j . x_i = -||x_i - x_j||^2 / 2
+// is computed on raw (unscaled) bfloat16 operands with float32 accumulation,
+// and t = 2 beta log2(e) C is applied afterwards on the vector ALUs.  In the
+// K*V contraction K' = 2^15 K is rounded once to the nearest float16 (relative
+// error <= 2^-12, well inside the bfloat16-input tolerance) and multiplied by
+// the split V (hi + lo): the product is then a fixed matrix applied linearly
+// to 2^-22, so an eigensolver built on it can converge to its tolerance.
+//
+// Pack layout (per 16-point tile and 32-feature chunk c): lane (g, p) holds
+// the 8 bfloat16 x[16 tile + p][32 c + 8 g + e], e = 0..7, as one uint4; that
+// is the A operand of the column tile and the B operand of the row tile.
+
+__global__ void norms_bf16_kernel(const uint16_t* __restrict__ X, int64_t n, int D, int64_t ldx,
+                                  float* __restrict__ ap, float* __restrict__ ar, int64_t npad) {
+  const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i >= npad) return;
+  double r = 0.0;
+  if (i < n)
+    for (int k = 0; k < D; ++k) {
+      const double x = double(__uint_as_float(uint32_t(X[i * ldx + k]) << 16));
+      r += x * x;
+    }
+  // padded points: a huge negative offset makes their kernel values exactly 0
+  const float a = (i < n) ? float(-0.5 * r) : -1e30f;
+  ar[i] = a;
+  if (ap != nullptr) {
+    const int64_t tile = i / TILE;
+    const int p = int(i % TILE);
+    const int g = p >> 2, rr = p & 3;
+    float* base = ap + (tile * 64 + 16 * g) * 4 + rr;
+    for (int q = 0; q < 16; ++q) base[q * 4] = a;
+  }
+}
+
+__global__ void pack_bf16_kernel(const uint16_t* __restrict__ X, int64_t n, int D, int64_t ldx,
+                                 int dc, int64_t ntiles, uintx4* __restrict__ xp) {
+  const int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (idx >= ntiles * dc * 64) return;
+  const int lane = int(idx & 63);
+  const int c = int((idx >> 6) % dc);
+  const int64_t tile = idx / (64 * dc);
+  const int g = lane >> 4, p = lane & 15;
+  const int64_t i = tile * TILE + p;
+  uintx4 out;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    uint32_t word = 0;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int k = 32 * c + 8 * g + 2 * w + h;
+      const uint32_t v = (i < n && k < D) ? uint32_t(X[i * ldx + k]) : 0u;
+      word |= v << (16 * h);
+    }
+    out[w] = word;
+  }
+  xp[idx] = out;
+}
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+template <int DC, bool DIAG>
+__device__ __forceinline__ floatx4 half_sqdist(const uintx4* xa, const floatx4& aj,
+                                               const uintx4* xb, float ai, int g, int p) {
+  floatx4 t;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) t[r] = ai + aj[r];
+#pragma unroll
+  for (int c = 0; c < DC; ++c)
+    t = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, xa[c]),
+                                                __builtin_bit_cast(bf16x8, xb[c]), t, 0, 0, 0);
+  if (DIAG) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      if (4 * g + r == p) t[r] = 0.f;
+  }
+  return t;
+}
+
+template <int DC, int NCB>
+struct ColPairB {
+  uintx4 xa[2][DC];
+  floatx4 aj[2];
+  VSplit v[NCB];
+};
+
+template <int DC, int NCB>
+__device__ __forceinline__ void load_pair_b(ColPairB<DC, NCB>& cp, const uintx4* __restrict__ xa,
+                                            const floatx4* __restrict__ aj,
+                                            const VSplit* __restrict__ vp, int64_t jp, int lane) {
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const int64_t jb = 2 * jp + t;
+#pragma unroll
+    for (int c = 0; c < DC; ++c) cp.xa[t][c] = xa[(jb * DC + c) * 64 + lane];
+    cp.aj[t] = aj[jb * 64 + lane];
+  }
+  if (vp != nullptr) {
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) cp.v[cb] = vp[(jp * NCB + cb) * 64 + lane];
+  }
+}
+
+template <int DC, int NCB, int NIB, bool DIAG>
+__device__ __forceinline__ void bf16_pair(const ColPairB<DC, NCB>& c, const uintx4 (&xbr)[NIB][DC],
+                                          const float (&ai)[NIB], float scale2,
+                                          floatx4 (&acc)[NIB][NCB], int64_t jp, int64_t ib0,
+                                          int g, int p) {
+#pragma unroll
+  for (int ib = 0; ib < NIB; ++ib) {
+    floatx4 t[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      if (DIAG && 2 * jp + u == ib0 + ib)
+        t[u] = half_sqdist<DC, true>(c.xa[u], c.aj[u], xbr[ib], ai[ib], g, p);
+      else
+        t[u] = half_sqdist<DC, false>(c.xa[u], c.aj[u], xbr[ib], ai[ib], g, p);
+    }
+    halfx8 k;
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)  // K' = 2^(2 beta log2e C + 15) <= 2^15
+        k[4 * u + r] = _Float16(__builtin_amdgcn_exp2f(fmaf(t[u][r], scale2, 15.f)));
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) {
+      acc[ib][cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(k, c.v[cb].hi, acc[ib][cb], 0, 0, 0);
+      acc[ib][cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(k, c.v[cb].lo, acc[ib][cb], 0, 0, 0);
+    }
+  }
+}
+
+template <int DC, int NCB, int NIB>
+__global__ __launch_bounds__(WG_THREADS) void product_bf16_kernel(
+    const uintx4* __restrict__ xa, const floatx4* __restrict__ aj, const VSplit* __restrict__ vp,
+    const uintx4* __restrict__ xb, const float* __restrict__ ar, int64_t nrt, int64_t njp,
+    int64_t jp_per_split, int diag, float scale2, const float* __restrict__ colscale,
+    const float* __restrict__ sl, float* __restrict__ Y, int64_t ldy, int64_t Nr, int b,
+    float* __restrict__ part, int64_t nrpad) {
+  __shared__ floatx4 tot[4][NIB][NCB][64];
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int wr = xcd_remap(blockIdx.x, gridDim.x);
+  const int64_t split = wr / nrt;
+  const int64_t rt = wr % nrt;
+  const int64_t ib0 = (rt * 4 + wave) * NIB;
+  const int64_t jp_begin = split * jp_per_split;
+  const int64_t jp_end = min(njp, jp_begin + jp_per_split);
+  const int g = lane >> 4, p = lane & 15;
+
+  uintx4 xbr[NIB][DC];
+  float ai[NIB];
+#pragma unroll
+  for (int ib = 0; ib < NIB; ++ib) {
+#pragma unroll
+    for (int c = 0; c < DC; ++c) xbr[ib][c] = xb[((ib0 + ib) * DC + c) * 64 + lane];
+    ai[ib] = ar[(ib0 + ib) * TILE + p];
+  }
+  floatx4 acc[NIB][NCB];
+#pragma unroll
+  for (int ib = 0; ib < NIB; ++ib)
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) {
+      acc[ib][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
+      tot[wave][ib][cb][lane] = floatx4{0.f, 0.f, 0.f, 0.f};
+    }
+
+  ColPairB<DC, NCB> cur, nxt;
+  load_pair_b(cur, xa, aj, vp, jp_begin, lane);
+  int chunk = 0;
+  for (int64_t jp = jp_begin; jp < jp_end; ++jp) {
+    load_pair_b(nxt, xa, aj, vp, min(jp + 1, jp_end - 1), lane);
+    if (diag && 2 * jp + 1 >= ib0 && 2 * jp < ib0 + NIB)
+      bf16_pair<DC, NCB, NIB, true>(cur, xbr, ai, scale2, acc, jp, ib0, g, p);
+    else
+      bf16_pair<DC, NCB, NIB, false>(cur, xbr, ai, scale2, acc, jp, ib0, g, p);
+    if (++chunk == CHUNK_TILES / 2) {
+      chunk = 0;
+#pragma unroll
+      for (int ib = 0; ib < NIB; ++ib)
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb) {
+          tot[wave][ib][cb][lane] += acc[ib][cb];
+          acc[ib][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
+        }
+    }
+    cur = nxt;
+  }
+
+#pragma unroll
+  for (int ib = 0; ib < NIB; ++ib)
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) {
+      const floatx4 v = tot[wave][ib][cb][lane] + acc[ib][cb];
+      const int c = cb * 16 + p;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int64_t i = (ib0 + ib) * TILE + 4 * g + e;
+        if (part != nullptr) {
+          part[(split * nrpad + i) * (NCB * 16) + c] = v[e];
+        } else if (i < Nr && c < b) {
+          const float y = v[e] * colscale[c];
+          Y[i * ldy + c] = (sl != nullptr) ? y * sl[i] : y;
+        }
+      }
+    }
+}
+
+// Row sums for bfloat16 inputs: the same half squared distances, K = 2^t
+// clamped to [0, 1], summed (times the weights) on the vector ALUs.
+template <int DC, int NIB, bool UNIT>
+__global__ __launch_bounds__(WG_THREADS) void rowsum_bf16_kernel(
+    const uintx4* __restrict__ xa, const floatx4* __restrict__ aj, const floatx4* __restrict__ wp,
+    const uintx4* __restrict__ xb, const float* __restrict__ ar, int64_t nrt, int64_t njb,
+    int64_t jb_per_split, int diag, float scale2, float* __restrict__ out, int64_t Nr,
+    float* __restrict__ part, int64_t nrpad) {
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int wr = xcd_remap(blockIdx.x, gridDim.x);
+  const int64_t split = wr / nrt;
+  const int64_t rt = wr % nrt;
+  const int64_t ib0 = (rt * 4 + wave) * NIB;
+  const int64_t jb_begin = split * jb_per_split;
+  const int64_t jb_end = min(njb, jb_begin + jb_per_split);
+  const int g = lane >> 4, p = lane & 15;
+
+  uintx4 xbr[NIB][DC];
+  float ai[NIB];
+#pragma unroll
+  for (int ib = 0; ib < NIB; ++ib) {
+#pragma unroll
+    for (int c = 0; c < DC; ++c) xbr[ib][c] = xb[((ib0 + ib) * DC + c) * 64 + lane];
+    ai[ib] = ar[(ib0 + ib) * TILE + p];
+  }
+  float acc[NIB], tot[NIB];
+#pragma unroll
+  for (int ib = 0; ib < NIB; ++ib) acc[ib] = tot[ib] = 0.f;
+  int chunk = 0;
+  for (int64_t jb = jb_begin; jb < jb_end; ++jb) {
+    uintx4 xar[DC];
+#pragma unroll
+    for (int c = 0; c < DC; ++c) xar[c] = xa[(jb * DC + c) * 64 + lane];
+    const floatx4 ajr = aj[jb * 64 + lane];
+    floatx4 w4 = floatx4{1.f, 1.f, 1.f, 1.f};
+    if (!UNIT) w4 = wp[jb * 64 + lane];
+    const bool dtile = diag && jb >= ib0 && jb < ib0 + NIB;
+#pragma unroll
+    for (int ib = 0; ib < NIB; ++ib) {
+      floatx4 t;
+      if (dtile && jb == ib0 + ib)
+        t = half_sqdist<DC, true>(xar, ajr, xbr[ib], ai[ib], g, p);
+      else
+        t = half_sqdist<DC, false>(xar, ajr, xbr[ib], ai[ib], g, p);
+      float sum = 0.f;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float k = exp2_unit(t[r] * scale2);
+        sum = UNIT ? sum + k : fmaf(k, w4[r], sum);
+      }
+      acc[ib] += sum;
+    }
+    if (++chunk == CHUNK_TILES) {
+      chunk = 0;
+#pragma unroll
+      for (int ib = 0; ib < NIB; ++ib) {
+        tot[ib] += acc[ib];
+        acc[ib] = 0.f;
+      }
+    }
+  }
+#pragma unroll
+  for (int ib = 0; ib < NIB; ++ib) {
+    float v = tot[ib] + acc[ib];
+    v += __shfl_xor(v, 16);
+    v += __shfl_xor(v, 32);
+    if (g == 0) {
+      const int64_t i = (ib0 + ib) * TILE + p;
+      if (part != nullptr)
+        part[split * nrpad + i] = v;
+      else if (i < Nr)
+        out[i] = v;
+    }
+  }
+}
+
 __global__ void reduce_product_kernel(const float* __restrict__ part, int nsplit, int64_t nrpad,
                                       int width, const float* __restrict__ colscale,
                                       const float* __restrict__ sl, float* __restrict__ Y,
@@ -763,8 +1058,34 @@ static inline size_t lane4_extent(int64_t tiles, int groups) {
   return size_t(tiles) * groups * 64 * 4;
 }
 
+static void pack_points_bf16(const uint16_t* X, int64_t n, int64_t D, int64_t ldx, bool row_side,
+                             PointPack& out, hipStream_t stream) {
+  const int dc = int(ceil_div(D, 32));
+  FD_REQUIRE(out.npad % TILE == 0 && out.npad >= n && dc <= 2, FD_ERR_INVALID_ARG,
+             "internal: bad bf16 pack geometry");
+  const int64_t ntiles = out.npad / TILE;
+  check_span(out.xp, size_t(ntiles) * dc * 64 * 4, "bf16 point pack");
+  check_span(out.ar, size_t(out.npad), "row offsets");
+  if (!row_side) check_span(out.ap, lane4_extent(ntiles, 1), "column offsets");
+  hipLaunchKernelGGL(norms_bf16_kernel, dim3(blocks_for(out.npad, 256)), dim3(256), 0, stream, X,
+                     n, int(D), ldx, row_side ? nullptr : out.ap.p, out.ar.p, out.npad);
+  FD_LAUNCH_CHECK();
+  hipLaunchKernelGGL(pack_bf16_kernel, dim3(blocks_for(ntiles * dc * 64, 256)), dim3(256), 0,
+                     stream, X, n, int(D), ldx, dc, ntiles, reinterpret_cast<uintx4*>(out.xp.p));
+  FD_LAUNCH_CHECK();
+  out.bf16 = true;
+  out.dc = dc;
+}
+
 void launch_pack_points(const void* X, fd_dtype xt, int64_t n, int64_t D, int64_t ldx,
                         double beta, bool row_side, PointPack& out, hipStream_t stream) {
+  out.beta = beta;
+  if (xt == FD_BF16) {
+    pack_points_bf16(static_cast<const uint16_t*>(X), n, D, ldx, row_side, out, stream);
+    return;
+  }
+  out.bf16 = false;
+  out.dc = 0;
   const double bl = beta * LOG2E;
   // rows carry the factor 2*beta*log2(e) of the cross term; columns are plain
   const double scale = row_side ? 2.0 * bl : 1.0;
@@ -776,14 +1097,9 @@ void launch_pack_points(const void* X, fd_dtype xt, int64_t n, int64_t D, int64_
   if (with_ap) check_span(out.ap, lane4_extent(out.npad / TILE, 1), "column offsets");
   const unsigned grid = blocks_for(out.npad, 256);
   float* ap = with_ap ? out.ap.p : nullptr;
-  if (xt == FD_F32)
-    hipLaunchKernelGGL(pack_points_kernel<float>, dim3(grid), dim3(256), 0, stream,
-                       static_cast<const float*>(X), n, int(D), ldx, bl, scale, out.xp.p, ap,
-                       out.ar.p, out.npad, out.dp);
-  else
-    hipLaunchKernelGGL(pack_points_kernel<uint16_t>, dim3(grid), dim3(256), 0, stream,
-                       static_cast<const uint16_t*>(X), n, int(D), ldx, bl, scale, out.xp.p, ap,
-                       out.ar.p, out.npad, out.dp);
+  hipLaunchKernelGGL(pack_points_kernel<float>, dim3(grid), dim3(256), 0, stream,
+                     static_cast<const float*>(X), n, int(D), ldx, bl, scale, out.xp.p, ap,
+                     out.ar.p, out.npad, out.dp);
   FD_LAUNCH_CHECK();
 }
 
@@ -819,10 +1135,15 @@ static void check_tiles(const KVPlan& p, const PointPack& rows, const PointPack&
   FD_REQUIRE(p.nsplit >= 1 && (p.nsplit - 1) * p.jb_per_split < p.njb &&
                  p.nsplit * p.jb_per_split >= p.njb,
              FD_ERR_INVALID_ARG, "internal: bad column split");
-  check_span(rows.xp, xp_extent(row_tiles, p.dp), "row pack");
+  if (rows.bf16) {
+    check_span(rows.xp, size_t(row_tiles) * rows.dc * 64 * 4, "bf16 row pack");
+    check_span(cols.xp, size_t(round_up(p.njb, 2)) * cols.dc * 64 * 4, "bf16 column pack");
+  } else {
+    check_span(rows.xp, xp_extent(row_tiles, p.dp), "row pack");
+    check_span(cols.xp, xp_extent(round_up(p.njb, 2), p.dp), "column pack");
+  }
   check_span(rows.ar, size_t(rows.npad), "row offsets");
-  check_span(cols.xp, xp_extent(p.njb, p.dp), "column pack");
-  check_span(cols.ap, lane4_extent(p.njb, 1), "column offsets");
+  check_span(cols.ap, lane4_extent(round_up(p.njb, 2), 1), "column offsets");
 }
 
 void launch_pack_v_split(const float* V, int64_t n, int64_t b, int64_t ldv, const float* sr,
@@ -846,6 +1167,44 @@ void launch_pack_v_split(const float* V, int64_t n, int64_t b, int64_t ldv, cons
                      n, int(b), ldv, sr, ncb, npairs, maxbits, reinterpret_cast<VSplit*>(vp.p),
                      colscale);
   FD_LAUNCH_CHECK();
+}
+
+void launch_pack_v_for(const PointPack& /*rows*/, const float* V, int64_t n, int64_t b,
+                       int64_t ldv, const float* sr, int ncb, int64_t npad, FSpan vp,
+                       FSpan vscale, hipStream_t stream) {
+  // both product kinds take the split V (hi + lo float16 halves)
+  launch_pack_v_split(V, n, b, ldv, sr, ncb, npad, vp, vscale, stream);
+}
+
+template <int DC, int NCB>
+static void product_bf16_launch(const KVPlan& p, const PointPack& rows, const PointPack& cols,
+                                const float* vp, const float* colscale, bool diag,
+                                const float* sl, float* Y, int64_t ldy, int b, float* part,
+                                hipStream_t stream) {
+  const unsigned grid = unsigned(p.nrt * p.nsplit);
+  const float scale2 = float(2.0 * rows.beta * LOG2E);
+  ProfScope prof(FD_KERNEL_PRODUCT, stream);
+  hipLaunchKernelGGL((product_bf16_kernel<DC, NCB, 4>), dim3(grid), dim3(WG_THREADS), 0, stream,
+                     reinterpret_cast<const uintx4*>(cols.xp.p),
+                     reinterpret_cast<const floatx4*>(cols.ap.p),
+                     reinterpret_cast<const VSplit*>(vp),
+                     reinterpret_cast<const uintx4*>(rows.xp.p), rows.ar.p, p.nrt,
+                     ceil_div(p.njb, 2), p.jb_per_split / 2, int(diag), scale2, colscale, sl, Y,
+                     ldy, rows.n, b, part, rows.npad);
+  FD_LAUNCH_CHECK();
+}
+
+template <int DC>
+static void product_bf16_ncb(const KVPlan& p, const PointPack& rows, const PointPack& cols,
+                             const float* vp, const float* cs, bool diag, const float* sl,
+                             float* Y, int64_t ldy, int b, float* part, hipStream_t stream) {
+  switch (p.ncb) {
+    case 1: return product_bf16_launch<DC, 1>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
+    case 2: return product_bf16_launch<DC, 2>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
+    case 3: return product_bf16_launch<DC, 3>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
+    case 4: return product_bf16_launch<DC, 4>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
+  }
+  throw Error{FD_ERR_UNSUPPORTED, "block width above 64"};
 }
 
 template <int DP, int NCB, int NIB>
@@ -895,7 +1254,6 @@ void launch_product(const KVPlan& p, const PointPack& rows, const PointPack& col
              FD_ERR_INVALID_ARG, "internal: block width does not match the plan");
   FD_REQUIRE(p.jb_per_split % 2 == 0 && round_up(p.njb, 2) * TILE <= cols.npad,
              FD_ERR_INVALID_ARG, "internal: column pairs do not fit the pack");
-  check_span(vp, size_t(ceil_div(p.njb, 2)) * p.ncb * 64 * 8, "split V pack");
   check_span(vscale, 128, "column scales");
   const float* cs = vscale.p + 64;
   float* pp = nullptr;
@@ -903,6 +1261,16 @@ void launch_product(const KVPlan& p, const PointPack& rows, const PointPack& col
     check_span(part, size_t(p.nsplit) * rows.npad * p.ncb * 16, "partial products");
     pp = part.p;
   }
+  if (rows.bf16 || cols.bf16) {
+    FD_REQUIRE(rows.bf16 && cols.bf16 && rows.dc == cols.dc && p.nib == 4, FD_ERR_INVALID_ARG,
+               "internal: mixed pack kinds");
+    check_span(vp, size_t(ceil_div(p.njb, 2)) * p.ncb * 64 * 8, "split V pack");
+    if (rows.dc == 1)
+      product_bf16_ncb<1>(p, rows, cols, vp.p, cs, diag, sl, Y, ldy, b, pp, stream);
+    else
+      product_bf16_ncb<2>(p, rows, cols, vp.p, cs, diag, sl, Y, ldy, b, pp, stream);
+  } else {
+  check_span(vp, size_t(ceil_div(p.njb, 2)) * p.ncb * 64 * 8, "split V pack");
   switch (p.dp) {
     case 4: product_dispatch_ncb<4>(p, rows, cols, vp.p, cs, diag, sl, Y, ldy, b, pp, stream); break;
     case 8: product_dispatch_ncb<8>(p, rows, cols, vp.p, cs, diag, sl, Y, ldy, b, pp, stream); break;
@@ -913,6 +1281,7 @@ void launch_product(const KVPlan& p, const PointPack& rows, const PointPack& col
     case 48: product_dispatch_ncb<48>(p, rows, cols, vp.p, cs, diag, sl, Y, ldy, b, pp, stream); break;
     case 64: product_dispatch_ncb<64>(p, rows, cols, vp.p, cs, diag, sl, Y, ldy, b, pp, stream); break;
     default: throw Error{FD_ERR_UNSUPPORTED, "feature dimension above 64"};
+  }
   }
   if (p.nsplit > 1) {
     const int64_t total = rows.n * b;
@@ -945,6 +1314,22 @@ static void rowsum_dispatch_u(const KVPlan& p, const PointPack& rows, const Poin
     rowsum_dispatch<DP, false>(p, rows, cols, wp, diag, out, part, stream);
 }
 
+template <int DC, bool UNIT>
+static void rowsum_bf16_launch(const KVPlan& p, const PointPack& rows, const PointPack& cols,
+                               const float* wp, bool diag, float* out, float* part,
+                               hipStream_t stream) {
+  const unsigned grid = unsigned(p.nrt * p.nsplit);
+  const float scale2 = float(2.0 * rows.beta * LOG2E);
+  ProfScope prof(FD_KERNEL_ROWSUM, stream);
+  hipLaunchKernelGGL((rowsum_bf16_kernel<DC, 4, UNIT>), dim3(grid), dim3(WG_THREADS), 0, stream,
+                     reinterpret_cast<const uintx4*>(cols.xp.p),
+                     reinterpret_cast<const floatx4*>(cols.ap.p),
+                     reinterpret_cast<const floatx4*>(wp),
+                     reinterpret_cast<const uintx4*>(rows.xp.p), rows.ar.p, p.nrt, p.njb,
+                     p.jb_per_split, int(diag), scale2, out, rows.n, part, rows.npad);
+  FD_LAUNCH_CHECK();
+}
+
 void launch_rowsum(const KVPlan& p, const PointPack& rows, const PointPack& cols, FSpan wp,
                    bool diag, float* out, FSpan part, hipStream_t stream) {
   check_tiles(p, rows, cols);
@@ -955,6 +1340,17 @@ void launch_rowsum(const KVPlan& p, const PointPack& rows, const PointPack& cols
     check_span(part, size_t(p.nsplit) * rows.npad, "partial row sums");
     pp = part.p;
   }
+  if (rows.bf16 || cols.bf16) {
+    FD_REQUIRE(rows.bf16 && cols.bf16 && rows.dc == cols.dc, FD_ERR_INVALID_ARG,
+               "internal: mixed pack kinds");
+    const bool unit = wp.p == nullptr;
+    if (rows.dc == 1)
+      unit ? rowsum_bf16_launch<1, true>(p, rows, cols, wp.p, diag, out, pp, stream)
+           : rowsum_bf16_launch<1, false>(p, rows, cols, wp.p, diag, out, pp, stream);
+    else
+      unit ? rowsum_bf16_launch<2, true>(p, rows, cols, wp.p, diag, out, pp, stream)
+           : rowsum_bf16_launch<2, false>(p, rows, cols, wp.p, diag, out, pp, stream);
+  } else {
   switch (p.dp) {
     case 4: rowsum_dispatch_u<4>(p, rows, cols, wp.p, diag, out, pp, stream); break;
     case 8: rowsum_dispatch_u<8>(p, rows, cols, wp.p, diag, out, pp, stream); break;
@@ -965,6 +1361,7 @@ void launch_rowsum(const KVPlan& p, const PointPack& rows, const PointPack& cols
     case 48: rowsum_dispatch_u<48>(p, rows, cols, wp.p, diag, out, pp, stream); break;
     case 64: rowsum_dispatch_u<64>(p, rows, cols, wp.p, diag, out, pp, stream); break;
     default: throw Error{FD_ERR_UNSUPPORTED, "feature dimension above 64"};
+  }
   }
   if (p.nsplit > 1) {
     hipLaunchKernelGGL(reduce_rowsum_kernel, dim3(blocks_for(rows.n, 256)), dim3(256), 0, stream,

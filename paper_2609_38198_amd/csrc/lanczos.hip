@@ -448,7 +448,9 @@ fd_status fd_block_lanczos(const void* X, fd_dtype xt, int64_t N, int64_t D, int
       hipStream_t st = static_cast<hipStream_t>(stream);
 
       degree_run(w.deg, X, xt, N, D, ldx, beta, alpha, nullptr, w.d, w.s, w.s_off, true, st);
-      Lanczos L(w, w.prod, st, N, int(b), lay.mm, o.seed);
+      // the product view takes the packs as filled (kind and bandwidth)
+      Lanczos L(w, product_view(w.prod, w.deg.rows, w.deg.cols, int(b)), st, N, int(b), lay.mm,
+                o.seed);
       SolveResult R = lanczos_solve(w, L, lay, int(k), V0, V0 ? k0 : 0, ldv0,
                                     warm_is_psi ? 0.5 : 0.0, o);
       copy_cols(w.Q, lay.mm, evecs, k, N, int(k), nullptr, 0.0, st);

@@ -78,3 +78,16 @@ def test_grid_torus_constant_degree():
     assert np.abs(q / q0 - 1).max() <= 1e-5
     s = to_np(deg.s)
     assert np.abs(s * np.sqrt(q0) - 1).max() <= 1e-5
+
+
+def test_bf16_normalisation():
+    # bfloat16 X: exact bfloat16 products in the distance contraction, float32
+    # sums, so the normalisation meets the float32 tolerance
+    s = inputs.stress(N=4096)
+    dev = device()
+    beta = s.betas[0]
+    case("degree bf16 N=4096 D=64")
+    deg = fd.fd_degree(to_dev(s.X, dev), beta, 0.5)
+    ref = on.normalise(s.X_f64(), beta, 0.5)
+    for name in ("q", "d", "s"):
+        assert rel_fro(to_np(getattr(deg, name)), getattr(ref, name)) <= TOL_F32

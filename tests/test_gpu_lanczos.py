@@ -150,3 +150,16 @@ def test_deterministic(torus2_ref):
     b = fd.fd_block_lanczos(X, 8.0, 16, 8)
     assert a.evals == b.evals
     assert torch.equal(a.evecs, b.evecs)
+
+
+def test_bf16_input_eigenpairs():
+    # the bfloat16 path rounds K to float16 (relative 2^-12): eigenvalues to 2e-3,
+    # the stated bfloat16-input tolerance; the solver itself converges to 1e-5
+    s = inputs.stress(N=2048)
+    beta = s.betas[0]
+    sp = oe.spectrum(s.X_f64(), beta, 0.5, 16)
+    dev = device()
+    case("lanczos bf16 stress N=2048 k=8 b=8")
+    e = fd.fd_block_lanczos(to_dev(s.X, dev), beta, 8, 8)
+    assert np.max(np.abs(np.asarray(e.evals) - sp.evals[:8])) <= 2e-3
+    assert max(e.residuals) <= 1e-5

@@ -11,7 +11,7 @@ import numpy as np
 import pytest
 import torch
 
-from gpu_util import TOL_F32, case, device, rel_fro, to_dev, to_np
+from gpu_util import TOL_BF16, TOL_F32, case, device, rel_fro, to_dev, to_np
 from oracle import kernel as ok
 from oracle import torus_grid as tg
 from paper_2609_38198_amd import _lib as fd
@@ -141,13 +141,34 @@ def test_strided_operands_and_determinism():
 
 
 def test_bf16_input_uses_exact_bf16_values():
+    # bfloat16 X: the oracle takes the exact bfloat16 values; tolerance 2e-3
     s = inputs.stress(N=4096)
-    V = inputs.random_block(4096, 16)
-    beta = s.betas[0]
-    case("bf16 X N=4096 D=64 b=16")
-    Y = _run(s.X, None, beta, V)
-    ref = ok.kernel_matmul(s.X_f64(), None, beta, V)
-    assert rel_fro(Y, ref) <= TOL_F32
+    for b in (16, 64):
+        V = inputs.random_block(4096, b)
+        beta = s.betas[0]
+        case(f"bf16 X N=4096 D=64 b={b}")
+        Y = _run(s.X, None, beta, V)
+        ref = ok.kernel_matmul(s.X_f64(), None, beta, V)
+        err = rel_fro(Y, ref)
+        print(f"bf16 product rel err {err:.2e}")
+        assert err <= TOL_BF16
+
+
+@pytest.mark.parametrize("D,b", [(64, 64), (30, 32), (8, 8)])
+def test_bf16_shapes_sampled_rows(D, b):
+    N = 65536
+    X = inputs.stress_points(N, seed=3, D=D, sub_dim=min(8, D)).astype(np.float32)
+    bits = inputs.f32_to_bf16_bits(X)
+    Xb = inputs.bf16_bits_to_f64(bits)
+    beta = 1.0 / inputs.median_sq_distance(Xb, 1024, 0)
+    V = inputs.random_block(N, b, seed=4)
+    case(f"bf16 shape N={N} D={D} b={b}")
+    Y = _run(bits, None, beta, V)
+    rows = np.random.default_rng(2).choice(N, 64, replace=False)
+    ref = ok.kernel_matmul(Xb, None, beta, V, rows=rows, threads=8)
+    err = rel_fro(Y[rows], ref)
+    print(f"bf16 D={D} b={b} rel err {err:.2e}")
+    assert err <= TOL_BF16
 
 
 def test_invalid_arguments_raise():
