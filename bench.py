@@ -141,6 +141,47 @@ def continuation_leg(fd, torch, dev) -> dict:
                       for n, beta, i in zip(ns, bs, lad.info)]}
 
 
+def stress_leg(fd, torch, dev) -> dict:
+    """bfloat16 X, N = 2^21 in R^64: fused product throughput and 20 block-Lanczos iterations."""
+    from paper_2609_38198_amd import inputs
+    log("stress leg: generating N=2^21 x 64 bf16")
+    w = inputs.stress()
+    X = torch.from_numpy(w.X.view(np.int16)).to(dev).view(torch.bfloat16)
+    N, D, b = w.N, w.D, w.b
+    beta = float(w.betas[0])
+    V = torch.from_numpy(inputs.random_block(N, b)).to(dev)
+    Y = torch.empty((N, b), dtype=torch.float32, device=dev)
+    ws = torch.empty(fd.fd_workspace_size(fd.FD_OP_KERNEL_MATMUL, N, N, D, b), dtype=torch.uint8,
+                     device=dev)
+    fd.fd_kernel_matmul(X, None, beta, V, Y=Y, ws=ws)
+    torch.cuda.synchronize()
+    fd.fd_profile_read(fd.FD_KERNEL_PRODUCT)
+    fd.fd_profile_enable(True)
+    reps = 3
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        fd.fd_kernel_matmul(X, None, beta, V, Y=Y, ws=ws)
+    torch.cuda.synchronize()
+    tp = (time.perf_counter() - t0) / reps
+    fd.fd_profile_enable(False)
+    pms, pn = fd.fd_profile_read(fd.FD_KERNEL_PRODUCT)
+    del ws, Y
+    log(f"stress leg: product {tp:.3f} s; 20 block-Lanczos iterations")
+    o = fd.default_opts(max_matvecs=20, max_basis_blocks=16, keep=64, verbose=1)
+    t0 = time.perf_counter()
+    e = fd.fd_block_lanczos(X, beta, 64, b, opts=o, allow_not_converged=True)
+    torch.cuda.synchronize()
+    tl = time.perf_counter() - t0
+    avg = pms * 1e-3 / max(pn, 1)
+    return {"workload": f"stress bf16 N={N} D={D} b={b} beta={beta:.5f}",
+            "product_s": tp, "product_kernel_s": avg,
+            "pair_cols_per_s": float(N) * N * b / avg,
+            "exp_per_s": float(N) * N / avg,
+            "lanczos_20_iters_s": tl, "block_matvecs": e.info["block_matvecs"],
+            "nconv": e.info["nconv"], "max_residual": e.info["max_residual"],
+            "evals_head": e.evals[:4], "evals_tail": e.evals[-2:]}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -151,6 +192,7 @@ def main() -> int:
     ap.add_argument("--lanczos", action="store_true")
     ap.add_argument("--molecule", action="store_true")
     ap.add_argument("--continuation", action="store_true")
+    ap.add_argument("--stress", action="store_true")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -241,6 +283,8 @@ def main() -> int:
         rec["lanczos_molecule"] = molecule_leg(fd, torch, dev)
     if args.continuation:
         rec["continuation"] = continuation_leg(fd, torch, dev)
+    if args.stress:
+        rec["stress"] = stress_leg(fd, torch, dev)
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(wl.X, 2.0, b, args.cpu_seconds)
     print(json.dumps(rec), flush=True)

@@ -883,6 +883,7 @@ __global__ __launch_bounds__(WG_THREADS) void product_bf16_kernel(
     }
 }
 
+
 // Row sums for bfloat16 inputs: the same half squared distances, K = 2^t
 // clamped to [0, 1], summed (times the weights) on the vector ALUs.
 template <int DC, int NIB, bool UNIT>
@@ -1176,15 +1177,14 @@ void launch_pack_v_for(const PointPack& /*rows*/, const float* V, int64_t n, int
   launch_pack_v_split(V, n, b, ldv, sr, ncb, npad, vp, vscale, stream);
 }
 
-template <int DC, int NCB>
-static void product_bf16_launch(const KVPlan& p, const PointPack& rows, const PointPack& cols,
-                                const float* vp, const float* colscale, bool diag,
-                                const float* sl, float* Y, int64_t ldy, int b, float* part,
-                                hipStream_t stream) {
+template <int DC, int NCB, int NIB>
+static void product_bf16_nib(const KVPlan& p, const PointPack& rows, const PointPack& cols,
+                             const float* vp, const float* colscale, bool diag, const float* sl,
+                             float* Y, int64_t ldy, int b, float* part, hipStream_t stream) {
   const unsigned grid = unsigned(p.nrt * p.nsplit);
   const float scale2 = float(2.0 * rows.beta * LOG2E);
   ProfScope prof(FD_KERNEL_PRODUCT, stream);
-  hipLaunchKernelGGL((product_bf16_kernel<DC, NCB, 4>), dim3(grid), dim3(WG_THREADS), 0, stream,
+  hipLaunchKernelGGL((product_bf16_kernel<DC, NCB, NIB>), dim3(grid), dim3(WG_THREADS), 0, stream,
                      reinterpret_cast<const uintx4*>(cols.xp.p),
                      reinterpret_cast<const floatx4*>(cols.ap.p),
                      reinterpret_cast<const VSplit*>(vp),
@@ -1192,6 +1192,16 @@ static void product_bf16_launch(const KVPlan& p, const PointPack& rows, const Po
                      ceil_div(p.njb, 2), p.jb_per_split / 2, int(diag), scale2, colscale, sl, Y,
                      ldy, rows.n, b, part, rows.npad);
   FD_LAUNCH_CHECK();
+}
+
+template <int DC, int NCB>
+static void product_bf16_launch(const KVPlan& p, const PointPack& rows, const PointPack& cols,
+                                const float* vp, const float* cs, bool diag, const float* sl,
+                                float* Y, int64_t ldy, int b, float* part, hipStream_t stream) {
+  if (p.nib == 2)
+    product_bf16_nib<DC, NCB, 2>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
+  else
+    product_bf16_nib<DC, NCB, 4>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
 }
 
 template <int DC>
@@ -1262,7 +1272,7 @@ void launch_product(const KVPlan& p, const PointPack& rows, const PointPack& col
     pp = part.p;
   }
   if (rows.bf16 || cols.bf16) {
-    FD_REQUIRE(rows.bf16 && cols.bf16 && rows.dc == cols.dc && p.nib == 4, FD_ERR_INVALID_ARG,
+    FD_REQUIRE(rows.bf16 && cols.bf16 && rows.dc == cols.dc, FD_ERR_INVALID_ARG,
                "internal: mixed pack kinds");
     check_span(vp, size_t(ceil_div(p.njb, 2)) * p.ncb * 64 * 8, "split V pack");
     if (rows.dc == 1)
