@@ -80,17 +80,21 @@ int padded_dim(int64_t D);
 constexpr int MAX_D = 64;
 constexpr int MAX_B = 64;
 
-// Packed operands of one point set, produced by pack_points.
-//   xp : [tiles][DP/4][64] contraction operand (scaled by `scale`)
-//   ap : [tiles][64][4]    a_j = -beta*log2(e)*||x_j||^2 in accumulator order
-//   ar : [npad]            a_i in plain order
+// Packed operands of one point set, produced by launch_pack_points.
+// float32 X: xp holds the split float16 exponent chunks ([tiles][chunks][64]
+//   uint4; chunk layout by recipe rid, row or column side).
+// bfloat16 X: xp holds [tiles][dc][64] uint4 of raw bfloat16 features,
+//   ap [tiles][64][4] the column offsets -||x_j||^2/2 in accumulator order,
+//   ar [npad] the row offsets.
 struct PointPack {
   FSpan xp, ap, ar;
   int64_t n = 0;      // real points
   int64_t npad = 0;   // padded points
-  int dp = 0;         // padded contraction width (float32 packs)
-  bool bf16 = false;  // filled from bfloat16 X: 16x16x32 bf16 layout, dc chunks of 32
-  int dc = 0;
+  int dp = 0;         // padded feature width the region was sized for
+  bool bf16 = false;  // filled from bfloat16 X
+  int dc = 0;         // bfloat16: 32-feature chunks
+  int rid = -1;       // float32: split-exponent recipe
+  bool row_side = false;
   double beta = 0.0;  // bandwidth the pack was made for
 };
 
@@ -118,8 +122,6 @@ PointPack carve_pack(Arena& a, int64_t n, int dp, int64_t pad);
 // Launchers (enqueue on stream; throw Error on failure).
 void launch_pack_points(const void* X, fd_dtype xt, int64_t n, int64_t D, int64_t ldx,
                         double beta, bool row_side, PointPack& out, hipStream_t stream);
-void launch_pack_v(const float* V, int64_t n, int64_t b, int64_t ldv, const float* sr,
-                   int ncb, int64_t npad, FSpan vp, hipStream_t stream);
 void launch_pack_w(const float* w, int64_t n, int64_t npad, FSpan wp, hipStream_t stream);
 // Pack sr * V for the product that matches the row pack's kind.
 void launch_pack_v_for(const PointPack& rows, const float* V, int64_t n, int64_t b, int64_t ldv,

@@ -1,0 +1,664 @@
+// Fused Gaussian-kernel products for float32 inputs on gfx950 matrix cores.
+//
+// Operation (FlashDiffusion Sec. 2.1 eq. matmat, Sec. 2.2 eq. tiled_rbf):
+//   Y_I = diag(sl_I) * sum_J K_IJ * (sr_J * V_J),  K_ij = exp(-beta ||x_i - x_j||^2),
+// with the exponent in the Gram form (eq. rbf_gram), in log2 units:
+//   t_ij = a_i + a_j + sum_k x_jk b_ik,  a = -beta log2(e) ||x||^2,  b = 2 beta log2(e) x,
+// and K_ij = 2^t_ij.  The N x N kernel matrix is never stored: each 16 x 16
+// tile lives in four registers of one wave between two matrix-core steps.
+//
+// Exponent contraction in float16 pieces.  Every float32 coordinate x' (and
+// every b', computed in float64) is written as three float16 pieces
+// v = v1 + v2 + v3 (each the round-to-nearest float16 of the remainder), which
+// represents a float32 value exactly (33 >= 24 significant bits) unless a piece
+// underflows.  The contraction keeps the six products whose pieces sum to at
+// most four (x1 b1, x2 b1, x1 b2, x3 b1, x1 b3, x2 b2); the three dropped ones
+// are below 2^-30 of the term.  Products of float16 values are exact in
+// float32, so the exponent carries only the float32 accumulation rounding, as a
+// float32 contraction would.  The offsets a_i and a_j enter the same
+// contraction as three float16 pieces each, multiplied by slots holding 1, and
+// sit in the first instruction next to x1 b1 so the large Gram terms cancel
+// early.  x' = s x and b' = b / s with s = 2^e, e ~ log2(2 beta log2 e) / 2,
+// keep both operands near the same magnitude; s cancels exactly in x' . b'.
+//
+// Why float16: on gfx950 the float16 matrix instructions run concurrently with
+// vector-ALU work of the same wave (the transcendental exp2 and the K split),
+// while the float32 matrix instruction shares the vector datapath.  Moving the
+// contraction to float16 pieces lets it hide under the exponentials.
+//
+// Pack layout (both sides): per 16-point tile and 32-slot chunk c, lane (g, p)
+// holds slots 8g .. 8g+7 of point 16 tile + p as eight float16 values (one
+// uint4): the A operand of v_mfma_f32_16x16x32_f16 for a column tile, the B
+// operand for a row tile.  A recipe (table below, per range of D) says which
+// piece or constant each slot holds and which (column chunk, row chunk) pairs
+// the contraction multiplies.  The accumulator then holds T^T[4g + r][p], the
+// layout the K*V step consumes without data movement (see product_hx_kernel).
+//
+// K*V contraction: float16 two-term split of both factors,
+//   K' = 2^15 K = Kh + Kl,  V' = 2^e_c sr V = Vh + Vl,  K'V' ~= Kh Vh + Kh Vl + Kl Vh,
+// on v_mfma_f32_16x16x32_f16 with float32 accumulation; the result is scaled
+// back by 2^(-15 - e_c).  The shift 15 is folded into the row-side offset
+// pieces (a_i + 15), so both the product and the row sums work with
+// K' = 2^15 K (the row sums scale back by 2^-15, exactly).  Sums over columns
+// are two-level (a fresh accumulator per 64 column tiles added into a running
+// total).  When rows and columns are the same point set the diagonal exponent
+// is set to its exact value (K'_ii = 2^15).
+//
+// Accuracy condition (either contraction form): the Gram form cancels terms of
+// size beta ||x||^2; inputs should be centred so that this stays moderate
+// (float32 resolves t to about 2^-24 beta log2(e) max ||x||^2).  Pieces are
+// saturated to the float16 range, so even beyond that every value is finite.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+
+#include "fd_profile.hpp"
+#include "kv_common.hpp"
+
+namespace fd {
+
+namespace {
+
+// ------------------------------------------------------------------ recipes
+
+enum : int8_t { SEG_END = 0, SEG_X = 1, SEG_ONES = 2, SEG_A = 3 };
+
+// A run of slots: SEG_X holds piece `piece` of features foff .. foff+cap-1
+// (zero past D); SEG_ONES holds three 1s; SEG_A the three pieces of a.
+struct HxSeg {
+  int8_t kind, piece, slot, cap, foff;
+};
+constexpr int HX_SEGS = 8, HX_CHUNKS = 7, HX_MFMAS = 13, HX_RECIPES = 6;
+struct HxChunk {
+  HxSeg s[HX_SEGS];
+};
+struct HxSide {
+  HxChunk ch[HX_CHUNKS];
+};
+// nc / nb: chunks per column / row point; instruction m multiplies column
+// chunk sa[m] by row chunk sb[m].
+struct HxRecipe {
+  int8_t maxd, nc, nb, nm;
+  int8_t sa[HX_MFMAS], sb[HX_MFMAS];
+  HxSide col, row;
+};
+
+constexpr HxSeg X(int piece, int slot, int cap, int foff = 0) {
+  return HxSeg{SEG_X, int8_t(piece), int8_t(slot), int8_t(cap), int8_t(foff)};
+}
+constexpr HxSeg ONES(int slot) { return HxSeg{SEG_ONES, 0, int8_t(slot), 3, 0}; }
+constexpr HxSeg AOF(int slot) { return HxSeg{SEG_A, 0, int8_t(slot), 3, 0}; }
+
+// Column side: x pieces, a_j against row-side 1s; row side: b pieces, a_i
+// against column-side 1s.  Slot by slot the column and row chunks of each
+// instruction pair as (x_p, b_q) with p + q <= 4, (1, a_i) or (a_j, 1); every
+// other slot pairing has a zero on one side.
+constexpr HxRecipe HX_TABLE[HX_RECIPES] = {
+    // D <= 4: one instruction
+    {4, 1, 1, 1, {0}, {0},
+     {{{{X(1, 0, 4), X(2, 4, 4), X(1, 8, 4), X(3, 12, 4), X(1, 16, 4), X(2, 20, 4), ONES(24),
+         AOF(27)}}}},
+     {{{{X(1, 0, 4), X(1, 4, 4), X(2, 8, 4), X(1, 12, 4), X(3, 16, 4), X(2, 20, 4), AOF(24),
+         ONES(27)}}}}},
+    // D <= 8: x1b1 + x2b1 + x3b1 + a_i + a_j, then x1b2 + x1b3 + x2b2
+    {8, 2, 2, 2, {0, 1}, {0, 1},
+     {{{{X(1, 0, 8), X(2, 8, 8), X(3, 16, 8), ONES(24), AOF(27)}},
+       {{X(1, 0, 8), X(1, 8, 8), X(2, 16, 8)}}}},
+     {{{{X(1, 0, 8), X(1, 8, 8), X(1, 16, 8), AOF(24), ONES(27)}},
+       {{X(2, 0, 8), X(3, 8, 8), X(2, 16, 8)}}}}},
+    // D <= 13: column chunk 0 serves two instructions
+    {13, 2, 3, 3, {0, 1, 0}, {0, 1, 2},
+     {{{{X(1, 0, 13), ONES(13), X(2, 16, 13), AOF(29)}},
+       {{X(1, 0, 13), X(3, 16, 13)}}}},
+     {{{{X(1, 0, 13), AOF(13), X(1, 16, 13), ONES(29)}},
+       {{X(2, 0, 13), X(1, 16, 13)}},
+       {{X(3, 0, 13), X(2, 16, 13)}}}}},
+    // D <= 26: one piece per chunk, offsets in the spare slots of chunk pair (0, 0)
+    {26, 3, 3, 6, {0, 1, 0, 2, 0, 1}, {0, 0, 1, 0, 2, 1},
+     {{{{X(1, 0, 26), ONES(26), AOF(29)}}, {{X(2, 0, 26)}}, {{X(3, 0, 26)}}}},
+     {{{{X(1, 0, 26), AOF(26), ONES(29)}}, {{X(2, 0, 26)}}, {{X(3, 0, 26)}}}}},
+    // D <= 32: offsets in a chunk of their own
+    {32, 4, 4, 7, {0, 3, 1, 0, 2, 0, 1}, {0, 3, 0, 1, 0, 2, 1},
+     {{{{X(1, 0, 32)}}, {{X(2, 0, 32)}}, {{X(3, 0, 32)}}, {{ONES(0), AOF(3)}}}},
+     {{{{X(1, 0, 32)}}, {{X(2, 0, 32)}}, {{X(3, 0, 32)}}, {{AOF(0), ONES(3)}}}}},
+    // D <= 64: two chunks per piece
+    {64, 7, 7, 13, {0, 1, 6, 2, 3, 0, 1, 4, 5, 0, 1, 2, 3}, {0, 1, 6, 0, 1, 2, 3, 0, 1, 4, 5, 2, 3},
+     {{{{X(1, 0, 32)}}, {{X(1, 0, 32, 32)}}, {{X(2, 0, 32)}}, {{X(2, 0, 32, 32)}},
+       {{X(3, 0, 32)}}, {{X(3, 0, 32, 32)}}, {{ONES(0), AOF(3)}}}},
+     {{{{X(1, 0, 32)}}, {{X(1, 0, 32, 32)}}, {{X(2, 0, 32)}}, {{X(2, 0, 32, 32)}},
+       {{X(3, 0, 32)}}, {{X(3, 0, 32, 32)}}, {{AOF(0), ONES(3)}}}}},
+};
+
+template <int RID>
+struct Hx {
+  static constexpr int nc = HX_TABLE[RID].nc;
+  static constexpr int nb = HX_TABLE[RID].nb;
+  static constexpr int nm = HX_TABLE[RID].nm;
+};
+
+// Minimum waves per SIMD asked of the compiler.  At 2 a wave has at most 256
+// registers and the matrix instructions then accumulate in ordinary VGPRs, so
+// the vector ALUs read the exponent tiles without copies out of the
+// accumulation registers.  The variants listed take 1 (accumulation
+// registers, up to 512 per wave): their operands and accumulators do not fit
+// in 256 registers (they spill at 2).
+template <int RID, int NCB, int NIB>
+constexpr int hx_waves() {
+  const bool big = (NIB == 4 && ((NCB == 4 && RID >= 1) || (NCB == 3 && RID >= 3) || RID == 5)) ||
+                   (RID == 5 && NCB >= 3);
+  return big ? 1 : 2;
+}
+
+// ------------------------------------------------------------------ packing
+
+// Piece k (1..3) of v: the float16 nearest to what the earlier pieces leave.
+__device__ __forceinline__ float piece_of(double v, int k) {
+  v = fmin(fmax(v, -65504.0), 65504.0);
+  float out = 0.f;
+  for (int q = 1; q <= 3; ++q) {
+    const float h = float(_Float16(float(v)));
+    if (q == k) {
+      out = h;
+      break;
+    }
+    v -= double(h);
+  }
+  return out;
+}
+
+// One thread per (tile, chunk, lane): the lane's eight slots of the chunk.
+// `scale` multiplies the coordinates (s on the column side, 2 beta log2(e) / s
+// on the row side); the offsets are neg_bl ||x||^2 + shift with
+// neg_bl = -beta log2(e).  Padded points have zero coordinates and offset
+// -65504, so their kernel values are exactly 0.
+__global__ void pack_hx_kernel(const float* __restrict__ X, int64_t n, int D, int64_t ldx,
+                               double scale, double neg_bl, double shift, HxSide side, int nch,
+                               int64_t ntiles, uintx4* __restrict__ out) {
+  const int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (idx >= ntiles * nch * 64) return;
+  const int lane = int(idx & 63);
+  const int ch = int((idx >> 6) % nch);
+  const int64_t tile = idx / (64 * nch);
+  const int g = lane >> 4, p = lane & 15;
+  const int64_t i = tile * TILE + p;
+  const bool real = i < n;
+  halfx8 h;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) h[e] = _Float16(0.f);
+  for (int s = 0; s < HX_SEGS; ++s) {
+    const HxSeg sg = side.ch[ch].s[s];
+    if (sg.kind == SEG_END) break;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int off = 8 * g + e - sg.slot;
+      if (off < 0 || off >= sg.cap) continue;
+      float v = 0.f;
+      if (sg.kind == SEG_ONES) {
+        v = 1.f;
+      } else if (sg.kind == SEG_X) {
+        const int f = sg.foff + off;
+        if (real && f < D) v = piece_of(scale * double(X[i * ldx + f]), sg.piece);
+      } else {
+        double a = -65504.0;
+        if (real) {
+          double r = 0.0;
+          for (int k = 0; k < D; ++k) {
+            const double x = double(X[i * ldx + k]);
+            r += x * x;
+          }
+          a = neg_bl * r + shift;
+        }
+        v = piece_of(a, off + 1);
+      }
+      h[e] = _Float16(v);
+    }
+  }
+  out[idx] = __builtin_bit_cast(uintx4, h);
+}
+
+// ------------------------------------------------------------------ exponent
+
+// t += sum over the recipe's instructions M.. of column chunk x row chunk.
+template <int RID, int M = 0>
+__device__ __forceinline__ void hx_chain(floatx4& t, const uintx4* xa, const uintx4* br) {
+  if constexpr (M < HX_TABLE[RID].nm) {
+    constexpr int ca = HX_TABLE[RID].sa[M];
+    constexpr int cb = HX_TABLE[RID].sb[M];
+    t = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(halfx8, xa[ca]),
+                                               __builtin_bit_cast(halfx8, br[cb]), t, 0, 0, 0);
+    hx_chain<RID, M + 1>(t, xa, br);
+  }
+}
+
+// Shift of the exponents: K' = 2^SHIFT K.
+constexpr float SHIFT = 15.f;
+
+// Exponent tile T^T[4g + r][p] of one row tile against one column tile (the
+// shift included); DIAG: the same 16 points on both sides, entry j == i set
+// to its exact value SHIFT.
+template <int RID, bool DIAG>
+__device__ __forceinline__ floatx4 hx_exponent(const uintx4* xa, const uintx4* br, int g, int p) {
+  floatx4 t = floatx4{0.f, 0.f, 0.f, 0.f};
+  hx_chain<RID>(t, xa, br);
+  if (DIAG) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      if (4 * g + r == p) t[r] = SHIFT;
+  }
+  return t;
+}
+
+// ------------------------------------------------------------------ product
+
+template <int RID, int NCB>
+struct HxPair {
+  uintx4 xa[2][Hx<RID>::nc];
+  VSplit v[NCB];
+};
+
+template <int RID, int NCB>
+__device__ __forceinline__ void load_hx_pair(HxPair<RID, NCB>& c, const uintx4* __restrict__ xc,
+                                             const VSplit* __restrict__ vp, int64_t jp,
+                                             int lane) {
+  constexpr int NC = Hx<RID>::nc;
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const int64_t jb = 2 * jp + t;
+#pragma unroll
+    for (int ch = 0; ch < NC; ++ch) c.xa[t][ch] = xc[(jb * NC + ch) * 64 + lane];
+  }
+#pragma unroll
+  for (int cb = 0; cb < NCB; ++cb) c.v[cb] = vp[(jp * NCB + cb) * 64 + lane];
+}
+
+// One pair of column tiles against the wave's NIB row tiles.  From the two
+// exponent tiles lane (g, p) holds K'[p][J0 + 4g + r] and K'[p][J1 + 4g + r],
+// which are its eight A-operand values (k = 8g + e, e = r for J0 and 4 + r for
+// J1) of the K*V instruction; the V pack stores the matching rows per lane.
+template <int RID, int NCB, int NIB, bool DIAG>
+__device__ __forceinline__ void hx_pair(const HxPair<RID, NCB>& c,
+                                        const uintx4 (&br)[NIB][Hx<RID>::nb],
+                                        floatx4 (&acc)[NIB][NCB], int64_t jp, int64_t ib0,
+                                        float m1, int g, int p) {
+#pragma unroll
+  for (int ib = 0; ib < NIB; ++ib) {
+    floatx4 t[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      if (DIAG && 2 * jp + u == ib0 + ib)
+        t[u] = hx_exponent<RID, true>(c.xa[u], br[ib], g, p);
+      else
+        t[u] = hx_exponent<RID, false>(c.xa[u], br[ib], g, p);
+    }
+    uintx4 hw, lw;
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int r = 0; r < 4; r += 2) {
+        // K' = 2^t with the shift in t: K' <= 2^15 (up to rounding)
+        const float k0 = __builtin_amdgcn_exp2f(t[u][r]);
+        const float k1 = __builtin_amdgcn_exp2f(t[u][r + 1]);
+        unsigned hh, ll;
+        split2m(k0, k1, m1, hh, ll);
+        hw[2 * u + r / 2] = hh;
+        lw[2 * u + r / 2] = ll;
+      }
+    const halfx8 khi = __builtin_bit_cast(halfx8, hw);
+    const halfx8 klo = __builtin_bit_cast(halfx8, lw);
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) {
+      acc[ib][cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(khi, c.v[cb].hi, acc[ib][cb], 0, 0, 0);
+      acc[ib][cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(khi, c.v[cb].lo, acc[ib][cb], 0, 0, 0);
+      acc[ib][cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(klo, c.v[cb].hi, acc[ib][cb], 0, 0, 0);
+    }
+  }
+}
+
+// One workgroup = 4 waves; wave w owns row tiles [ib0, ib0 + NIB).  The
+// workgroup's column split is streamed in pairs of tiles through two operand
+// buffers used in turn: a buffer is refilled right after its pair is
+// consumed, so each load has a whole pair's compute to land.  Chunk totals of
+// the two-level sum live in LDS, which keeps registers free for more waves.
+// m1 = -1 (see split2m).
+template <int RID, int NCB, int NIB>
+__global__ __launch_bounds__(WG_THREADS)
+__attribute__((amdgpu_waves_per_eu(hx_waves<RID, NCB, NIB>()))) void product_hx_kernel(
+    const uintx4* __restrict__ xc, const VSplit* __restrict__ vp, const uintx4* __restrict__ xr,
+    int64_t nrt, int64_t njp, int64_t jp_per_split, int diag, float m1,
+    const float* __restrict__ colscale, const float* __restrict__ sl, float* __restrict__ Y,
+    int64_t ldy, int64_t Nr, int b, float* __restrict__ part, int64_t nrpad) {
+  constexpr int NB = Hx<RID>::nb;
+  __shared__ floatx4 tot[4][NIB][NCB][64];
+  const int lane = threadIdx.x & 63;
+  // the wave index is uniform: make the row-tile range (and the diagonal
+  // tests on it) scalar
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wr = xcd_remap(blockIdx.x, gridDim.x);
+  const int64_t split = wr / nrt;
+  const int64_t rt = wr % nrt;
+  const int64_t ib0 = (rt * 4 + wave) * NIB;
+  const int64_t jp_begin = split * jp_per_split;
+  const int64_t jp_end = min(njp, jp_begin + jp_per_split);
+  const int g = lane >> 4, p = lane & 15;
+
+  uintx4 br[NIB][NB];
+#pragma unroll
+  for (int ib = 0; ib < NIB; ++ib)
+#pragma unroll
+    for (int ch = 0; ch < NB; ++ch) br[ib][ch] = xr[((ib0 + ib) * NB + ch) * 64 + lane];
+  floatx4 acc[NIB][NCB];
+#pragma unroll
+  for (int ib = 0; ib < NIB; ++ib)
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) {
+      acc[ib][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
+      tot[wave][ib][cb][lane] = floatx4{0.f, 0.f, 0.f, 0.f};
+    }
+
+  auto step = [&](const HxPair<RID, NCB>& c, int64_t jp) {
+    if (diag && 2 * jp + 1 >= ib0 && 2 * jp < ib0 + NIB)
+      hx_pair<RID, NCB, NIB, true>(c, br, acc, jp, ib0, m1, g, p);
+    else
+      hx_pair<RID, NCB, NIB, false>(c, br, acc, jp, ib0, m1, g, p);
+  };
+  HxPair<RID, NCB> b0, b1;
+  load_hx_pair(b0, xc, vp, jp_begin, lane);
+  // keep b0's loads ahead of b1's, the order the loop keeps them in: the wait
+  // before each step then only covers the buffer it consumes
+  __builtin_amdgcn_sched_barrier(0);
+  load_hx_pair(b1, xc, vp, min(jp_begin + 1, jp_end - 1), lane);
+  int chunk = 0;
+  for (int64_t jp = jp_begin; jp < jp_end; jp += 2) {
+    step(b0, jp);
+    load_hx_pair(b0, xc, vp, min(jp + 2, jp_end - 1), lane);
+    // the refill is unconditional (clamped index) so that the number of loads
+    // in flight at the top of the loop is the same on every path
+    if (jp + 1 < jp_end) step(b1, jp + 1);
+    load_hx_pair(b1, xc, vp, min(jp + 3, jp_end - 1), lane);
+    chunk += 2;
+    if (chunk >= CHUNK_TILES / 2) {
+      chunk = 0;
+#pragma unroll
+      for (int ib = 0; ib < NIB; ++ib)
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb) {
+          tot[wave][ib][cb][lane] += acc[ib][cb];
+          acc[ib][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
+        }
+    }
+  }
+
+#pragma unroll
+  for (int ib = 0; ib < NIB; ++ib)
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) {
+      const floatx4 v = tot[wave][ib][cb][lane] + acc[ib][cb];
+      const int c = cb * 16 + p;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int64_t i = (ib0 + ib) * TILE + 4 * g + e;
+        if (part != nullptr) {
+          part[(split * nrpad + i) * (NCB * 16) + c] = v[e];
+        } else if (i < Nr && c < b) {
+          const float y = v[e] * colscale[c];
+          Y[i * ldy + c] = (sl != nullptr) ? y * sl[i] : y;
+        }
+      }
+    }
+}
+
+// ------------------------------------------------------------------ row sums
+
+template <int RID>
+struct HxCol {
+  uintx4 xa[Hx<RID>::nc];
+  floatx4 w;
+};
+
+template <int RID, bool UNIT>
+__device__ __forceinline__ void load_hx_col(HxCol<RID>& c, const uintx4* __restrict__ xc,
+                                            const floatx4* __restrict__ wp, int64_t jb,
+                                            int lane) {
+  constexpr int NC = Hx<RID>::nc;
+#pragma unroll
+  for (int ch = 0; ch < NC; ++ch) c.xa[ch] = xc[(jb * NC + ch) * 64 + lane];
+  if (!UNIT) c.w = wp[jb * 64 + lane];
+}
+
+// One column tile against the wave's NIB row tiles: all exponent chains
+// first (independent, so the matrix core and the exponentials overlap), then
+// K' = 2^t summed (times the weights) on the vector ALUs.
+template <int RID, int NIB, bool UNIT, bool DIAG>
+__device__ __forceinline__ void hx_rowsum_tile(const HxCol<RID>& c,
+                                               const uintx4 (&br)[NIB][Hx<RID>::nb],
+                                               float (&acc)[NIB], int64_t jb, int64_t ib0, int g,
+                                               int p) {
+  floatx4 t[NIB];
+#pragma unroll
+  for (int ib = 0; ib < NIB; ++ib) {
+    if (DIAG && jb == ib0 + ib)
+      t[ib] = hx_exponent<RID, true>(c.xa, br[ib], g, p);
+    else
+      t[ib] = hx_exponent<RID, false>(c.xa, br[ib], g, p);
+  }
+#pragma unroll
+  for (int ib = 0; ib < NIB; ++ib) {
+    float k[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      k[r] = __builtin_amdgcn_exp2f(t[ib][r]);
+      if (!UNIT) k[r] *= c.w[r];
+    }
+    acc[ib] += (k[0] + k[1]) + (k[2] + k[3]);
+  }
+}
+
+// Row sums sum_j K_ij w_j (b = 1, the normalisation passes): the same
+// exponent tiles, reduced on the vector ALUs instead of a second contraction.
+// Column tiles stream through two operand buffers used in turn.
+template <int RID, int NIB, bool UNIT>
+__global__ __launch_bounds__(WG_THREADS)
+__attribute__((amdgpu_waves_per_eu(hx_waves<RID, 0, NIB>()))) void rowsum_hx_kernel(
+    const uintx4* __restrict__ xc, const floatx4* __restrict__ wp, const uintx4* __restrict__ xr,
+    int64_t nrt, int64_t njb, int64_t jb_per_split, int diag, float* __restrict__ out,
+    int64_t Nr, float* __restrict__ part, int64_t nrpad) {
+  constexpr int NB = Hx<RID>::nb;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wr = xcd_remap(blockIdx.x, gridDim.x);
+  const int64_t split = wr / nrt;
+  const int64_t rt = wr % nrt;
+  const int64_t ib0 = (rt * 4 + wave) * NIB;
+  const int64_t jb_begin = split * jb_per_split;
+  const int64_t jb_end = min(njb, jb_begin + jb_per_split);
+  const int g = lane >> 4, p = lane & 15;
+
+  uintx4 br[NIB][NB];
+#pragma unroll
+  for (int ib = 0; ib < NIB; ++ib)
+#pragma unroll
+    for (int ch = 0; ch < NB; ++ch) br[ib][ch] = xr[((ib0 + ib) * NB + ch) * 64 + lane];
+  float acc[NIB], tot[NIB];
+#pragma unroll
+  for (int ib = 0; ib < NIB; ++ib) acc[ib] = tot[ib] = 0.f;
+
+  auto step = [&](const HxCol<RID>& c, int64_t jb) {
+    if (diag && jb >= ib0 && jb < ib0 + NIB)
+      hx_rowsum_tile<RID, NIB, UNIT, true>(c, br, acc, jb, ib0, g, p);
+    else
+      hx_rowsum_tile<RID, NIB, UNIT, false>(c, br, acc, jb, ib0, g, p);
+  };
+  HxCol<RID> b0, b1;
+  b0.w = b1.w = floatx4{1.f, 1.f, 1.f, 1.f};
+  load_hx_col<RID, UNIT>(b0, xc, wp, jb_begin, lane);
+  __builtin_amdgcn_sched_barrier(0);  // b0's loads ahead of b1's, as in the loop
+  load_hx_col<RID, UNIT>(b1, xc, wp, min(jb_begin + 1, jb_end - 1), lane);
+  int chunk = 0;
+  for (int64_t jb = jb_begin; jb < jb_end; jb += 2) {
+    step(b0, jb);
+    load_hx_col<RID, UNIT>(b0, xc, wp, min(jb + 2, jb_end - 1), lane);
+    if (jb + 1 < jb_end) step(b1, jb + 1);
+    load_hx_col<RID, UNIT>(b1, xc, wp, min(jb + 3, jb_end - 1), lane);
+    chunk += 2;
+    if (chunk >= CHUNK_TILES) {
+      chunk = 0;
+#pragma unroll
+      for (int ib = 0; ib < NIB; ++ib) {
+        tot[ib] += acc[ib];
+        acc[ib] = 0.f;
+      }
+    }
+  }
+#pragma unroll
+  for (int ib = 0; ib < NIB; ++ib) {
+    // undo the shift (exact) and add the four lanes p, p+16, p+32, p+48 of row p
+    float v = (tot[ib] + acc[ib]) * 0x1p-15f;
+    v += __shfl_xor(v, 16);
+    v += __shfl_xor(v, 32);
+    if (g == 0) {
+      const int64_t i = (ib0 + ib) * TILE + p;
+      if (part != nullptr)
+        part[split * nrpad + i] = v;
+      else if (i < Nr)
+        out[i] = v;
+    }
+  }
+}
+
+// ------------------------------------------------------------------ host dispatch
+
+template <int RID, int NCB, int NIB>
+void product_hx_launch(const KVPlan& p, const PointPack& rows, const PointPack& cols,
+                       const float* vp, const float* colscale, bool diag, const float* sl,
+                       float* Y, int64_t ldy, int b, float* part, hipStream_t stream) {
+  const unsigned grid = unsigned(p.nrt * p.nsplit);
+  ProfScope prof(FD_KERNEL_PRODUCT, stream);
+  hipLaunchKernelGGL((product_hx_kernel<RID, NCB, NIB>), dim3(grid), dim3(WG_THREADS), 0, stream,
+                     reinterpret_cast<const uintx4*>(cols.xp.p),
+                     reinterpret_cast<const VSplit*>(vp),
+                     reinterpret_cast<const uintx4*>(rows.xp.p), p.nrt, ceil_div(p.njb, 2),
+                     p.jb_per_split / 2, int(diag), -1.0f, colscale, sl, Y, ldy, rows.n, b, part,
+                     rows.npad);
+  FD_LAUNCH_CHECK();
+}
+
+template <int RID, int NCB>
+void product_hx_nib(const KVPlan& p, const PointPack& rows, const PointPack& cols,
+                    const float* vp, const float* cs, bool diag, const float* sl, float* Y,
+                    int64_t ldy, int b, float* part, hipStream_t stream) {
+  switch (p.nib) {
+    case 2: return product_hx_launch<RID, NCB, 2>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
+    case 4: return product_hx_launch<RID, NCB, 4>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
+  }
+  throw Error{FD_ERR_INVALID_ARG, "internal: unsupported rows per wave"};
+}
+
+template <int RID>
+void product_hx_ncb(const KVPlan& p, const PointPack& rows, const PointPack& cols,
+                    const float* vp, const float* cs, bool diag, const float* sl, float* Y,
+                    int64_t ldy, int b, float* part, hipStream_t stream) {
+  switch (p.ncb) {
+    case 1: return product_hx_nib<RID, 1>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
+    case 2: return product_hx_nib<RID, 2>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
+    case 3: return product_hx_nib<RID, 3>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
+    case 4: return product_hx_nib<RID, 4>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
+  }
+  throw Error{FD_ERR_UNSUPPORTED, "block width above 64"};
+}
+
+template <int RID, bool UNIT>
+void rowsum_hx_launch(const KVPlan& p, const PointPack& rows, const PointPack& cols,
+                      const float* wp, bool diag, float* out, float* part, hipStream_t stream) {
+  const unsigned grid = unsigned(p.nrt * p.nsplit);
+  ProfScope prof(FD_KERNEL_ROWSUM, stream);
+  hipLaunchKernelGGL((rowsum_hx_kernel<RID, 4, UNIT>), dim3(grid), dim3(WG_THREADS), 0, stream,
+                     reinterpret_cast<const uintx4*>(cols.xp.p),
+                     reinterpret_cast<const floatx4*>(wp),
+                     reinterpret_cast<const uintx4*>(rows.xp.p), p.nrt, p.njb, p.jb_per_split,
+                     int(diag), out, rows.n, part, rows.npad);
+  FD_LAUNCH_CHECK();
+}
+
+template <int RID>
+void rowsum_hx_u(const KVPlan& p, const PointPack& rows, const PointPack& cols, const float* wp,
+                 bool diag, float* out, float* part, hipStream_t stream) {
+  if (wp == nullptr)
+    rowsum_hx_launch<RID, true>(p, rows, cols, wp, diag, out, part, stream);
+  else
+    rowsum_hx_launch<RID, false>(p, rows, cols, wp, diag, out, part, stream);
+}
+
+void check_hx(const KVPlan& p, const PointPack& rows, const PointPack& cols) {
+  FD_REQUIRE(rows.rid >= 0 && rows.rid < HX_RECIPES && rows.rid == cols.rid && rows.row_side &&
+                 !cols.row_side,
+             FD_ERR_INVALID_ARG, "internal: split packs do not match");
+  const HxRecipe& R = HX_TABLE[rows.rid];
+  const int64_t row_tiles = p.nrt * 4 * p.nib;
+  check_span(rows.xp, size_t(row_tiles) * R.nb * 64 * 4, "split row pack");
+  check_span(cols.xp, size_t(round_up(p.njb, 2)) * R.nc * 64 * 4, "split column pack");
+}
+
+}  // namespace
+
+int hx_recipe_for(int64_t D) {
+  for (int r = 0; r < HX_RECIPES; ++r)
+    if (D >= 1 && D <= HX_TABLE[r].maxd) return r;
+  return -1;
+}
+int hx_col_chunks(int rid) { return HX_TABLE[rid].nc; }
+int hx_row_chunks(int rid) { return HX_TABLE[rid].nb; }
+
+void launch_pack_points_hx(const float* X, int64_t n, int64_t D, int64_t ldx, double beta,
+                           bool row_side, PointPack& out, hipStream_t stream) {
+  const int rid = hx_recipe_for(D);
+  FD_REQUIRE(rid >= 0, FD_ERR_UNSUPPORTED, "feature dimension above 64");
+  const HxRecipe& R = HX_TABLE[rid];
+  const int nch = row_side ? R.nb : R.nc;
+  FD_REQUIRE(out.npad % (2 * TILE) == 0 && out.npad >= n, FD_ERR_INVALID_ARG,
+             "internal: bad split pack geometry");
+  const int64_t ntiles = out.npad / TILE;
+  check_span(out.xp, size_t(ntiles) * nch * 64 * 4, "split point pack");
+  const double bl = beta * LOG2E;
+  // s = 2^e balances |x'| = s|x| and |b'| = 2 beta log2(e) |x| / s
+  int e = 0;
+  if (beta > 0.0) e = std::clamp(int(std::lround(0.5 * std::log2(2.0 * bl))), -12, 12);
+  const double s = std::ldexp(1.0, e);
+  const double scale = row_side ? 2.0 * bl / s : s;
+  hipLaunchKernelGGL(pack_hx_kernel, dim3(blocks_for(ntiles * nch * 64, 256)), dim3(256), 0,
+                     stream, X, n, int(D), ldx, scale, -bl, row_side ? double(SHIFT) : 0.0,
+                     row_side ? R.row : R.col, nch, ntiles, reinterpret_cast<uintx4*>(out.xp.p));
+  FD_LAUNCH_CHECK();
+  out.rid = rid;
+  out.row_side = row_side;
+}
+
+void launch_product_hx(const KVPlan& p, const PointPack& rows, const PointPack& cols,
+                       const float* vp, const float* cs, bool diag, const float* sl, float* Y,
+                       int64_t ldy, int b, float* part, hipStream_t stream) {
+  check_hx(p, rows, cols);
+  switch (rows.rid) {
+    case 0: return product_hx_ncb<0>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
+    case 1: return product_hx_ncb<1>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
+    case 2: return product_hx_ncb<2>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
+    case 3: return product_hx_ncb<3>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
+    case 4: return product_hx_ncb<4>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
+    case 5: return product_hx_ncb<5>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
+  }
+}
+
+void launch_rowsum_hx(const KVPlan& p, const PointPack& rows, const PointPack& cols,
+                      const float* wp, bool diag, float* out, float* part, hipStream_t stream) {
+  check_hx(p, rows, cols);
+  FD_REQUIRE(p.nib == 4, FD_ERR_INVALID_ARG, "internal: row-sum plan");
+  switch (rows.rid) {
+    case 0: return rowsum_hx_u<0>(p, rows, cols, wp, diag, out, part, stream);
+    case 1: return rowsum_hx_u<1>(p, rows, cols, wp, diag, out, part, stream);
+    case 2: return rowsum_hx_u<2>(p, rows, cols, wp, diag, out, part, stream);
+    case 3: return rowsum_hx_u<3>(p, rows, cols, wp, diag, out, part, stream);
+    case 4: return rowsum_hx_u<4>(p, rows, cols, wp, diag, out, part, stream);
+    case 5: return rowsum_hx_u<5>(p, rows, cols, wp, diag, out, part, stream);
+  }
+}
+
+}  // namespace fd

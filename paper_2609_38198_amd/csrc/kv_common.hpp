@@ -1,0 +1,76 @@
+// Device-side types and helpers shared by the fused-product translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "fd_internal.hpp"
+
+namespace fd {
+
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef _Float16 halfx8 __attribute__((ext_vector_type(8)));
+typedef __fp16 pkhalf2 __attribute__((ext_vector_type(2)));
+typedef unsigned uintx4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+constexpr double LOG2E = 1.4426950408889634073599;
+constexpr int CHUNK_TILES = 64;  // column tiles per partial accumulator
+
+// Workgroups of one dispatch are spread over the eight XCDs round-robin by
+// id.  Re-number them so that each XCD owns a contiguous block of logical
+// work items (same column split, hence a shared working set in its L2).
+__device__ __forceinline__ int xcd_remap(int w, int total) {
+  if ((total & 7) != 0) return w;
+  const int per = total >> 3;
+  return (w & 7) * per + (w >> 3);
+}
+
+// Split float16 pack of V for one pair of 16-point column tiles: lane (g, p)
+// holds rows {4g + r} of the first tile and {16 + 4g + r} of the second
+// (r = 0..3) of column 16 cb + p, as hi and lo halves.
+struct VSplit {
+  halfx8 hi;
+  halfx8 lo;
+};
+
+// Round two floats toward zero to float16 (hi) and the remainders likewise
+// (lo); returns both packed pairs as 32-bit words.
+__device__ __forceinline__ void split2(float a, float b, unsigned& hi, unsigned& lo) {
+  const pkhalf2 h = __builtin_amdgcn_cvt_pkrtz(a, b);
+  const pkhalf2 l = __builtin_amdgcn_cvt_pkrtz(a - float(h[0]), b - float(h[1]));
+  hi = __builtin_bit_cast(unsigned, h);
+  lo = __builtin_bit_cast(unsigned, l);
+}
+
+// The same split with the remainders formed by one mixed-precision FMA each,
+// k - h = fma(h, m1, k) reading h straight from the packed float16 word.
+// m1 must be -1; it is a run-time value (a kernel argument) so that the
+// compiler keeps the FMA form instead of turning it into a subtraction.
+__device__ __forceinline__ void split2m(float a, float b, float m1, unsigned& hi, unsigned& lo) {
+  const pkhalf2 h = __builtin_amdgcn_cvt_pkrtz(a, b);
+  const pkhalf2 l = __builtin_amdgcn_cvt_pkrtz(__builtin_fmaf(float(h[0]), m1, a),
+                                               __builtin_fmaf(float(h[1]), m1, b));
+  hi = __builtin_bit_cast(unsigned, h);
+  lo = __builtin_bit_cast(unsigned, l);
+}
+
+inline unsigned blocks_for(int64_t n, int t) { return unsigned(ceil_div(n, t)); }
+
+// ---------------------------------------------------------------- float32 path
+// (split float16 exponent contraction; hx_kernels.hip)
+
+// Recipe index and chunk counts of the split-exponent pack for a feature
+// dimension D (1 <= D <= 64).
+int hx_recipe_for(int64_t D);
+int hx_col_chunks(int rid);
+int hx_row_chunks(int rid);
+
+void launch_pack_points_hx(const float* X, int64_t n, int64_t D, int64_t ldx, double beta,
+                           bool row_side, PointPack& out, hipStream_t stream);
+void launch_product_hx(const KVPlan& p, const PointPack& rows, const PointPack& cols,
+                       const float* vp, const float* colscale, bool diag, const float* sl,
+                       float* Y, int64_t ldy, int b, float* part, hipStream_t stream);
+void launch_rowsum_hx(const KVPlan& p, const PointPack& rows, const PointPack& cols,
+                      const float* wp, bool diag, float* out, float* part, hipStream_t stream);
+
+}  // namespace fd

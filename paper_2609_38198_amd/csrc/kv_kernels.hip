@@ -1,42 +1,20 @@
-// Fused Gaussian-kernel products on gfx950 matrix cores (float32 path).
+// Shared pieces of the fused Gaussian-kernel products: V and weight packs,
+// the bfloat16-input kernels, partial-sum reductions, the degree epilogues and
+// the host-side planning and dispatch.  The float32-input kernels (split
+// float16 exponent contraction) are in hx_kernels.hip.
 //
 // Operation (FlashDiffusion Sec. 2.1 eq. matmat, Sec. 2.2 eq. tiled_rbf):
-//   Y_I = diag(sl_I) * sum_J exp(-beta * (r_I 1^T + 1 r_J^T - 2 X_I X_J^T)) * (sr_J * V_J)
-// with r the squared row norms (Gram form, eq. rbf_gram).  The N x N kernel
-// matrix is never stored: each 16 x 16 tile of it lives in four registers of
-// one wave and is consumed by the next matrix-core instruction.
-//
-// Register-level fusion.  The exponent tile is computed transposed,
-//   T^T[j][i] = a_i + a_j + sum_k xa[j][k] * xb[i][k],
-//   a = -beta*log2(e)*r,  xa = x,  xb = 2*beta*log2(e)*x,
-// with v_mfma_f32_16x16x4_f32 taking A = point tile J and B = point tile I.
-// Its accumulator gives lane (g = lane/16, p = lane%16) the entries
-// T^T[4g + r][p], r = 0..3.  After k = exp2(min(t, 0)) those four values are,
-// unchanged, the A operands of four further 16x16x4 MFMAs that contract over j
-// (A[m = p][kk = g] = K[i = p][j = 4g + r]); the V tile is pre-packed so that
-// its B operand for instruction r is V[4g + r][c].  No LDS round trip and no
-// cross-lane movement is needed between the two contractions.
-//
-// Operands are pre-packed in HBM in exactly the per-lane order of the MFMA
-// operands, so every load is a fully coalesced 256-byte (or 1-KiB float4)
-// wave load that the L1/L2 serve to all row tiles streaming the same columns.
-//
-// Accuracy: accumulation is float32 with a two-level sum (a fresh accumulator
-// per chunk of 1024 columns, added into a running total), which keeps the
-// rounding growth at about sqrt(chunk) + sqrt(N/chunk) units.  When rows and
-// columns are the same point set the diagonal exponent is set to its exact
-// value 0 (K_ii = 1).
+//   Y_I = diag(sl_I) * sum_J exp(-beta * ||x_i - x_j||^2) * (sr_J * V_J),
+// and the row sums q = K 1, K w of the normalisation (Sec. 2.1).  The N x N
+// kernel matrix is never stored.
 #include <hip/hip_runtime.h>
 
-#include "fd_internal.hpp"
+#include <algorithm>
+
 #include "fd_profile.hpp"
+#include "kv_common.hpp"
 
 namespace fd {
-
-typedef float floatx4 __attribute__((ext_vector_type(4)));
-
-constexpr double LOG2E = 1.4426950408889634073599;
-constexpr int CHUNK_TILES = 64;  // column tiles per partial accumulator
 
 int padded_dim(int64_t D) {
   static const int dims[] = {4, 8, 12, 16, 24, 32, 48, 64};
@@ -45,10 +23,15 @@ int padded_dim(int64_t D) {
   return 0;
 }
 
+// Floats per point of a pack region: large enough for the float32 (split
+// float16 chunks of 16 floats) and the bfloat16 pack of any D with this
+// padded width; chunk counts grow with D, so the largest D decides.
 int pack_floats_per_point(int64_t D) {
   const int dp = padded_dim(D);
-  const int dc16 = int(ceil_div(D, 32)) * 16;
-  return std::max(dp, dc16);
+  const int dc16 = int(ceil_div(dp, 32)) * 16;
+  const int rid = hx_recipe_for(dp);
+  const int hx = 16 * std::max(hx_col_chunks(rid), hx_row_chunks(rid));
+  return std::max({dp, dc16, hx});
 }
 
 PointPack carve_pack(Arena& a, int64_t n, int dp, int64_t pad) {
@@ -56,84 +39,13 @@ PointPack carve_pack(Arena& a, int64_t n, int dp, int64_t pad) {
   p.n = n;
   p.npad = round_up(n, pad);
   p.dp = dp;
-  p.xp = a.fspan(size_t(p.npad) * std::max(dp, int(ceil_div(dp, 32)) * 16));
+  p.xp = a.fspan(size_t(p.npad) * pack_floats_per_point(dp));
   p.ap = a.fspan(size_t(p.npad) * 16);  // [tiles][64][4]: 16 floats per point
   p.ar = a.fspan(size_t(p.npad));
   return p;
 }
 
-// Workgroups of one dispatch are spread over the eight XCDs round-robin by
-// id.  Re-number them so that each XCD owns a contiguous block of logical
-// work items (same column split, hence a shared working set in its L2).
-__device__ __forceinline__ int xcd_remap(int w, int total) {
-  if ((total & 7) != 0) return w;
-  const int per = total >> 3;
-  return (w & 7) * per + (w >> 3);
-}
-
 // ------------------------------------------------------------------ packing
-
-__device__ __forceinline__ float load_x(const float* X, int64_t idx) { return X[idx]; }
-__device__ __forceinline__ float load_x(const uint16_t* X, int64_t idx) {
-  return __uint_as_float(uint32_t(X[idx]) << 16);
-}
-
-template <typename TIn>
-__global__ void pack_points_kernel(const TIn* __restrict__ X, int64_t n, int D, int64_t ldx,
-                                   double beta_log2e, double scale, float* __restrict__ xp,
-                                   float* __restrict__ ap, float* __restrict__ ar, int64_t npad,
-                                   int dp) {
-  const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (i >= npad) return;
-  const int S = dp / 4;
-  const int64_t tile = i / TILE;
-  const int p = int(i % TILE);
-  float* dst = xp + tile * S * 64;
-  double r = 0.0;
-  for (int k = 0; k < dp; ++k) {
-    float v = 0.f;
-    if (i < n && k < D) {
-      const double x = double(load_x(X, i * ldx + k));
-      r += x * x;
-      v = float(x * scale);
-    }
-    dst[(k >> 2) * 64 + (k & 3) * 16 + p] = v;
-  }
-  // padded points get a huge negative offset: their kernel values are exactly 0,
-  // also in the unit-weight row sums where no zero V row masks them
-  const float a = (i < n) ? float(-beta_log2e * r) : -1e30f;
-  ar[i] = a;
-  if (ap != nullptr) {
-    // accumulator order: lane 16g+q holds rows j = 4g + r of the tile
-    const int g = p >> 2, rr = p & 3;
-    float* base = ap + (tile * 64 + 16 * g) * 4 + rr;
-    for (int q = 0; q < 16; ++q) base[q * 4] = a;
-  }
-}
-
-__global__ void pack_v_kernel(const float* __restrict__ V, int64_t n, int b, int64_t ldv,
-                              const float* __restrict__ sr, int ncb, int64_t ntiles,
-                              floatx4* __restrict__ vp) {
-  const int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (idx >= ntiles * ncb * 64) return;
-  const int lane = int(idx & 63);
-  const int cb = int((idx >> 6) % ncb);
-  const int64_t jb = idx / (64 * ncb);
-  const int g = lane >> 4, p = lane & 15;
-  const int c = cb * 16 + p;
-  floatx4 out;
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int64_t j = jb * TILE + 4 * g + r;
-    float v = 0.f;
-    if (j < n && c < b) {
-      v = V[j * ldv + c];
-      if (sr != nullptr) v *= sr[j];
-    }
-    out[r] = v;
-  }
-  vp[idx] = out;
-}
 
 __global__ void pack_w_kernel(const float* __restrict__ w, int64_t n, int64_t ntiles,
                               floatx4* __restrict__ wp) {
@@ -151,8 +63,6 @@ __global__ void pack_w_kernel(const float* __restrict__ w, int64_t n, int64_t nt
   wp[idx] = out;
 }
 
-// ------------------------------------------------------------------ products
-
 // 2^t clamped to [0, 1]: the exponent of a true kernel value is <= 0 and
 // rounding can only push it a few ulps above.  The median-of-three with 0 and 1
 // folds into the output clamp bit of v_exp_f32 (one instruction).  Written with
@@ -163,272 +73,16 @@ __device__ __forceinline__ float exp2_unit(float t) {
 }
 
 // Column-tile operands of one 16-point tile, per lane.
-template <int S, int NW>
-struct ColTile {
-  float xa[S];     // contraction operand (A of the exponent MFMA)
-  floatx4 aj;      // a_j for the four accumulator rows of this lane
-  floatx4 w[NW];   // V (B operand of the product MFMA) or row-sum weights
-};
-
-template <int S, int NW>
-__device__ __forceinline__ void load_cols(ColTile<S, NW>& c, const float* __restrict__ xa,
-                                          const floatx4* __restrict__ aj,
-                                          const floatx4* __restrict__ wv, int64_t jb, int lane) {
-#pragma unroll
-  for (int s = 0; s < S; ++s) c.xa[s] = xa[(jb * S + s) * 64 + lane];
-  c.aj = aj[jb * 64 + lane];
-  if (wv != nullptr) {
-#pragma unroll
-    for (int k = 0; k < NW; ++k) c.w[k] = wv[(jb * NW + k) * 64 + lane];
-  }
-}
-
-// Exponent tile T^T[4g + r][p] for row tile ib against the loaded column tile;
-// DIAG: rows and columns are the same 16 points, so entry j == i is set to 0.
-template <int S, int NW, bool DIAG>
-__device__ __forceinline__ floatx4 exponent_tile(const ColTile<S, NW>& c, const float* xb,
-                                                 float ai, int g, int p) {
-  floatx4 t;
-#pragma unroll
-  for (int r = 0; r < 4; ++r) t[r] = ai + c.aj[r];
-#pragma unroll
-  for (int s = 0; s < S; ++s) t = __builtin_amdgcn_mfma_f32_16x16x4f32(c.xa[s], xb[s], t, 0, 0, 0);
-  if (DIAG) {
-#pragma unroll
-    for (int r = 0; r < 4; ++r)
-      if (4 * g + r == p) t[r] = 0.f;
-  }
-  return t;
-}
-
-template <int DP, int NCB, int NIB, bool DIAG>
-__device__ __forceinline__ void product_tile(const ColTile<DP / 4, NCB>& c,
-                                             const float (&xbr)[NIB][DP / 4],
-                                             const float (&ai)[NIB], floatx4 (&acc)[NIB][NCB],
-                                             int64_t jb, int64_t ib0, int g, int p) {
-#pragma unroll
-  for (int ib = 0; ib < NIB; ++ib) {
-    floatx4 t;
-    if (DIAG && jb == ib0 + ib)
-      t = exponent_tile<DP / 4, NCB, true>(c, xbr[ib], ai[ib], g, p);
-    else
-      t = exponent_tile<DP / 4, NCB, false>(c, xbr[ib], ai[ib], g, p);
-    float kk[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) kk[r] = exp2_unit(t[r]);
-#pragma unroll
-    for (int cb = 0; cb < NCB; ++cb)
-#pragma unroll
-      for (int r = 0; r < 4; ++r)
-        acc[ib][cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(kk[r], c.w[cb][r], acc[ib][cb], 0, 0, 0);
-  }
-}
-
-// One workgroup = 4 waves; wave w owns row tiles [ib0, ib0 + NIB) of 16 rows.
-// Column tiles [jb_begin, jb_end) of the workgroup's split are streamed, the
-// next tile's operands being loaded while the current one is computed.
-template <int DP, int NCB, int NIB>
-__global__ __launch_bounds__(WG_THREADS) void product_f32_kernel(
-    const float* __restrict__ xa, const floatx4* __restrict__ aj, const floatx4* __restrict__ vp,
-    const float* __restrict__ xb, const float* __restrict__ ar, int64_t nrt, int64_t njb,
-    int64_t jb_per_split, int diag, const float* __restrict__ sl, float* __restrict__ Y,
-    int64_t ldy, int64_t Nr, int b, float* __restrict__ part, int64_t nrpad) {
-  constexpr int S = DP / 4;
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int wr = xcd_remap(blockIdx.x, gridDim.x);
-  const int64_t split = wr / nrt;
-  const int64_t rt = wr % nrt;
-  const int64_t ib0 = (rt * 4 + wave) * NIB;
-  const int64_t jb_begin = split * jb_per_split;
-  const int64_t jb_end = min(njb, jb_begin + jb_per_split);
-  const int g = lane >> 4, p = lane & 15;
-
-  float xbr[NIB][S];
-  float ai[NIB];
-#pragma unroll
-  for (int ib = 0; ib < NIB; ++ib) {
-#pragma unroll
-    for (int s = 0; s < S; ++s) xbr[ib][s] = xb[((ib0 + ib) * S + s) * 64 + lane];
-    ai[ib] = ar[(ib0 + ib) * TILE + p];
-  }
-
-  floatx4 acc[NIB][NCB];
-  floatx4 tot[NIB][NCB];
-#pragma unroll
-  for (int ib = 0; ib < NIB; ++ib)
-#pragma unroll
-    for (int cb = 0; cb < NCB; ++cb) {
-      acc[ib][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
-      tot[ib][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
-    }
-
-  ColTile<S, NCB> cur, nxt;
-  load_cols(cur, xa, aj, vp, jb_begin, lane);
-  int chunk = 0;
-  for (int64_t jb = jb_begin; jb < jb_end; ++jb) {
-    load_cols(nxt, xa, aj, vp, min(jb + 1, jb_end - 1), lane);
-    if (diag && jb >= ib0 && jb < ib0 + NIB)
-      product_tile<DP, NCB, NIB, true>(cur, xbr, ai, acc, jb, ib0, g, p);
-    else
-      product_tile<DP, NCB, NIB, false>(cur, xbr, ai, acc, jb, ib0, g, p);
-    if (++chunk == CHUNK_TILES) {
-      chunk = 0;
-#pragma unroll
-      for (int ib = 0; ib < NIB; ++ib)
-#pragma unroll
-        for (int cb = 0; cb < NCB; ++cb) {
-          tot[ib][cb] += acc[ib][cb];
-          acc[ib][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
-        }
-    }
-    cur = nxt;
-  }
-
-#pragma unroll
-  for (int ib = 0; ib < NIB; ++ib)
-#pragma unroll
-    for (int cb = 0; cb < NCB; ++cb) {
-      const floatx4 v = tot[ib][cb] + acc[ib][cb];
-      const int c = cb * 16 + p;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int64_t i = (ib0 + ib) * TILE + 4 * g + e;
-        if (part != nullptr) {
-          part[(split * nrpad + i) * (NCB * 16) + c] = v[e];
-        } else if (i < Nr && c < b) {
-          Y[i * ldy + c] = (sl != nullptr) ? v[e] * sl[i] : v[e];
-        }
-      }
-    }
-}
-
-template <int DP, int NIB, bool UNIT, bool DIAG>
-__device__ __forceinline__ void rowsum_tile(const ColTile<DP / 4, 1>& c,
-                                            const float (&xbr)[NIB][DP / 4],
-                                            const float (&ai)[NIB], float (&acc)[NIB],
-                                            int64_t jb, int64_t ib0, int g, int p) {
-#pragma unroll
-  for (int ib = 0; ib < NIB; ++ib) {
-    floatx4 t;
-    if (DIAG && jb == ib0 + ib)
-      t = exponent_tile<DP / 4, 1, true>(c, xbr[ib], ai[ib], g, p);
-    else
-      t = exponent_tile<DP / 4, 1, false>(c, xbr[ib], ai[ib], g, p);
-    float sum = 0.f;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const float k = exp2_unit(t[r]);
-      sum = UNIT ? sum + k : fmaf(k, c.w[0][r], sum);
-    }
-    acc[ib] += sum;
-  }
-}
-
-// Row sums sum_j K_ij w_j (b = 1, the normalisation passes): the same
-// exponent tiles, reduced on the vector ALUs instead of a second MFMA.
-template <int DP, int NIB, bool UNIT>
-__global__ __launch_bounds__(WG_THREADS) void rowsum_f32_kernel(
-    const float* __restrict__ xa, const floatx4* __restrict__ aj, const floatx4* __restrict__ wp,
-    const float* __restrict__ xb, const float* __restrict__ ar, int64_t nrt, int64_t njb,
-    int64_t jb_per_split, int diag, float* __restrict__ out, int64_t Nr,
-    float* __restrict__ part, int64_t nrpad) {
-  constexpr int S = DP / 4;
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int wr = xcd_remap(blockIdx.x, gridDim.x);
-  const int64_t split = wr / nrt;
-  const int64_t rt = wr % nrt;
-  const int64_t ib0 = (rt * 4 + wave) * NIB;
-  const int64_t jb_begin = split * jb_per_split;
-  const int64_t jb_end = min(njb, jb_begin + jb_per_split);
-  const int g = lane >> 4, p = lane & 15;
-
-  float xbr[NIB][S];
-  float ai[NIB];
-#pragma unroll
-  for (int ib = 0; ib < NIB; ++ib) {
-#pragma unroll
-    for (int s = 0; s < S; ++s) xbr[ib][s] = xb[((ib0 + ib) * S + s) * 64 + lane];
-    ai[ib] = ar[(ib0 + ib) * TILE + p];
-  }
-  float acc[NIB], tot[NIB];
-#pragma unroll
-  for (int ib = 0; ib < NIB; ++ib) acc[ib] = tot[ib] = 0.f;
-
-  const floatx4* wsrc = UNIT ? nullptr : wp;
-  ColTile<S, 1> cur, nxt;
-  cur.w[0] = nxt.w[0] = floatx4{1.f, 1.f, 1.f, 1.f};
-  load_cols(cur, xa, aj, wsrc, jb_begin, lane);
-  int chunk = 0;
-  for (int64_t jb = jb_begin; jb < jb_end; ++jb) {
-    load_cols(nxt, xa, aj, wsrc, min(jb + 1, jb_end - 1), lane);
-    if (diag && jb >= ib0 && jb < ib0 + NIB)
-      rowsum_tile<DP, NIB, UNIT, true>(cur, xbr, ai, acc, jb, ib0, g, p);
-    else
-      rowsum_tile<DP, NIB, UNIT, false>(cur, xbr, ai, acc, jb, ib0, g, p);
-    if (++chunk == CHUNK_TILES) {
-      chunk = 0;
-#pragma unroll
-      for (int ib = 0; ib < NIB; ++ib) {
-        tot[ib] += acc[ib];
-        acc[ib] = 0.f;
-      }
-    }
-    cur = nxt;
-  }
-#pragma unroll
-  for (int ib = 0; ib < NIB; ++ib) {
-    float v = tot[ib] + acc[ib];
-    // lanes p, p+16, p+32, p+48 hold partial sums of row p
-    v += __shfl_xor(v, 16);
-    v += __shfl_xor(v, 32);
-    if (g == 0) {
-      const int64_t i = (ib0 + ib) * TILE + p;
-      if (part != nullptr)
-        part[split * nrpad + i] = v;
-      else if (i < Nr)
-        out[i] = v;
-    }
-  }
-}
-
-
-// ------------------------------------------------------------------ split K*V product
+// ------------------------------------------------------------------ split V pack
 //
-// The K*V contraction in float16 with a two-term split of both factors:
+// The K*V contraction runs in float16 with a two-term split of both factors:
 //   K' = 2^15 K = Kh + Kl,  V' = 2^e_c sr V = Vh + Vl  (Kh, Kl, Vh, Vl float16),
 //   K' V' ~= Kh Vh + Kh Vl + Kl Vh       (the dropped Kl Vl is 2^-22 relative),
-// on v_mfma_f32_16x16x32_f16 with float32 accumulation; the result is scaled
-// back by 2^(-15 - e_c).  K' carries the factor 2^15 (added to the exponent
-// offset, so K' <= 2^15 < 65504 needs no clamp) so that Kl stays a normal
-// float16 down to K ~ 4e-6; e_c puts the largest |V'| of column c just below
-// 2^14.  The representation error of each split is below 2^-21 relative.
-// The exponent contraction stays float32 (its cancellation needs it).
-//
-// Operand layout: two consecutive 16-point column tiles form the 32-wide
-// contraction.  From the two exponent tiles lane (g, p) holds
-// K[p][J0 + 4g + r] and K[p][J1 + 4g + r]; these are its 8 A-operand halves
-// (k = 8g + e with e = r for J0 and e = 4 + r for J1).  The V pack stores, per
-// lane, the 8 matching rows of column 16 cb + p as hi and lo halves.
-
-typedef _Float16 halfx8 __attribute__((ext_vector_type(8)));
-typedef __fp16 pkhalf2 __attribute__((ext_vector_type(2)));
-typedef unsigned uintx4 __attribute__((ext_vector_type(4)));
-
-struct VSplit {
-  halfx8 hi;
-  halfx8 lo;
-};
-
-// Round two floats toward zero to float16 (hi) and the remainders likewise
-// (lo); returns both packed pairs as 32-bit words.
-__device__ __forceinline__ void split2(float a, float b, unsigned& hi, unsigned& lo) {
-  const pkhalf2 h = __builtin_amdgcn_cvt_pkrtz(a, b);
-  const pkhalf2 l = __builtin_amdgcn_cvt_pkrtz(a - float(h[0]), b - float(h[1]));
-  hi = __builtin_bit_cast(unsigned, h);
-  lo = __builtin_bit_cast(unsigned, l);
-}
+// with float32 accumulation; the result is scaled back by 2^(-15 - e_c).  e_c
+// puts the largest |V'| of column c just below 2^14; the representation error
+// of each split is below 2^-21 relative.  Two consecutive 16-point column tiles
+// form the 32-wide contraction; the pack stores, per lane (g, p), the 8 rows
+// {4g + r, 16 + 4g + r} of column 16 cb + p as hi and lo halves.
 
 // max |sr_j V[j][c]| per column as float bits (non-negative floats order like
 // their bit patterns, so an integer max is exact and order independent)
@@ -510,168 +164,6 @@ __global__ void pack_v_split_kernel(const float* __restrict__ V, int64_t n, int 
 
 // Column-pair operands: exponent-contraction inputs of two 16-point tiles and
 // the split V pack of the pair.
-template <int S, int NCB>
-struct ColPair {
-  float xa[2][S];
-  floatx4 aj[2];
-  VSplit v[NCB];
-};
-
-template <int S, int NCB>
-__device__ __forceinline__ void load_pair(ColPair<S, NCB>& c, const float* __restrict__ xa,
-                                          const floatx4* __restrict__ aj,
-                                          const VSplit* __restrict__ vp, int64_t jp, int lane) {
-#pragma unroll
-  for (int t = 0; t < 2; ++t) {
-    const int64_t jb = 2 * jp + t;
-#pragma unroll
-    for (int s = 0; s < S; ++s) c.xa[t][s] = xa[(jb * S + s) * 64 + lane];
-    c.aj[t] = aj[jb * 64 + lane];
-  }
-#pragma unroll
-  for (int cb = 0; cb < NCB; ++cb) c.v[cb] = vp[(jp * NCB + cb) * 64 + lane];
-}
-
-template <int S, bool DIAG>
-__device__ __forceinline__ floatx4 exponent_of(const float* xa, const floatx4& aj, const float* xb,
-                                               float ai, int g, int p) {
-  floatx4 t;
-#pragma unroll
-  for (int r = 0; r < 4; ++r) t[r] = ai + aj[r];
-#pragma unroll
-  for (int s = 0; s < S; ++s) t = __builtin_amdgcn_mfma_f32_16x16x4f32(xa[s], xb[s], t, 0, 0, 0);
-  if (DIAG) {
-#pragma unroll
-    for (int r = 0; r < 4; ++r)
-      if (4 * g + r == p) t[r] = 15.f;  // K_ii = 1, times the 2^15 shift
-  }
-  return t;
-}
-
-template <int DP, int NCB, int NIB, bool DIAG>
-__device__ __forceinline__ void split_pair(const ColPair<DP / 4, NCB>& c,
-                                           const float (&xbr)[NIB][DP / 4],
-                                           const float (&ai)[NIB], floatx4 (&acc)[NIB][NCB],
-                                           int64_t jp, int64_t ib0, int g, int p) {
-  constexpr int S = DP / 4;
-#pragma unroll
-  for (int ib = 0; ib < NIB; ++ib) {
-    floatx4 t[2];
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      if (DIAG && 2 * jp + u == ib0 + ib)
-        t[u] = exponent_of<S, true>(c.xa[u], c.aj[u], xbr[ib], ai[ib], g, p);
-      else
-        t[u] = exponent_of<S, false>(c.xa[u], c.aj[u], xbr[ib], ai[ib], g, p);
-    }
-    uintx4 hw, lw;
-#pragma unroll
-    for (int u = 0; u < 2; ++u)
-#pragma unroll
-      for (int r = 0; r < 4; r += 2) {
-        // K' = 2^t with the shift 15 already in ai: K' <= 2^15 (up to rounding)
-        const float k0 = __builtin_amdgcn_exp2f(t[u][r]);
-        const float k1 = __builtin_amdgcn_exp2f(t[u][r + 1]);
-        unsigned h, l;
-        split2(k0, k1, h, l);
-        hw[2 * u + r / 2] = h;
-        lw[2 * u + r / 2] = l;
-      }
-    const halfx8 khi = __builtin_bit_cast(halfx8, hw);
-    const halfx8 klo = __builtin_bit_cast(halfx8, lw);
-#pragma unroll
-    for (int cb = 0; cb < NCB; ++cb) {
-      acc[ib][cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(khi, c.v[cb].hi, acc[ib][cb], 0, 0, 0);
-      acc[ib][cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(khi, c.v[cb].lo, acc[ib][cb], 0, 0, 0);
-      acc[ib][cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(klo, c.v[cb].hi, acc[ib][cb], 0, 0, 0);
-    }
-  }
-}
-
-// One workgroup = 4 waves; wave w owns row tiles [ib0, ib0 + NIB).  The
-// workgroup's column split is streamed in pairs of tiles, the next pair's
-// operands loading while the current one computes.  Chunk totals of the
-// two-level sum live in LDS (one float4 per lane and accumulator), which keeps
-// registers free for more waves per SIMD: vector-ALU and matrix-core work of
-// different waves then overlap.
-template <int DP, int NCB, int NIB>
-__global__ __launch_bounds__(WG_THREADS) void product_split_kernel(
-    const float* __restrict__ xa, const floatx4* __restrict__ aj, const VSplit* __restrict__ vp,
-    const float* __restrict__ xb, const float* __restrict__ ar, int64_t nrt, int64_t njp,
-    int64_t jp_per_split, int diag, const float* __restrict__ colscale,
-    const float* __restrict__ sl, float* __restrict__ Y, int64_t ldy, int64_t Nr, int b,
-    float* __restrict__ part, int64_t nrpad) {
-  constexpr int S = DP / 4;
-  __shared__ floatx4 tot[4][NIB][NCB][64];
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int wr = xcd_remap(blockIdx.x, gridDim.x);
-  const int64_t split = wr / nrt;
-  const int64_t rt = wr % nrt;
-  const int64_t ib0 = (rt * 4 + wave) * NIB;
-  const int64_t jp_begin = split * jp_per_split;
-  const int64_t jp_end = min(njp, jp_begin + jp_per_split);
-  const int g = lane >> 4, p = lane & 15;
-
-  float xbr[NIB][S];
-  float ai[NIB];
-#pragma unroll
-  for (int ib = 0; ib < NIB; ++ib) {
-#pragma unroll
-    for (int s = 0; s < S; ++s) xbr[ib][s] = xb[((ib0 + ib) * S + s) * 64 + lane];
-    ai[ib] = ar[(ib0 + ib) * TILE + p] + 15.f;  // K' = 2^15 K
-  }
-  floatx4 acc[NIB][NCB];
-#pragma unroll
-  for (int ib = 0; ib < NIB; ++ib)
-#pragma unroll
-    for (int cb = 0; cb < NCB; ++cb) {
-      acc[ib][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
-      tot[wave][ib][cb][lane] = floatx4{0.f, 0.f, 0.f, 0.f};
-    }
-
-  ColPair<S, NCB> cur, nxt;
-  load_pair(cur, xa, aj, vp, jp_begin, lane);
-  int chunk = 0;
-  for (int64_t jp = jp_begin; jp < jp_end; ++jp) {
-    load_pair(nxt, xa, aj, vp, min(jp + 1, jp_end - 1), lane);
-    if (diag && 2 * jp + 1 >= ib0 && 2 * jp < ib0 + NIB)
-      split_pair<DP, NCB, NIB, true>(cur, xbr, ai, acc, jp, ib0, g, p);
-    else
-      split_pair<DP, NCB, NIB, false>(cur, xbr, ai, acc, jp, ib0, g, p);
-    if (++chunk == CHUNK_TILES / 2) {
-      chunk = 0;
-#pragma unroll
-      for (int ib = 0; ib < NIB; ++ib)
-#pragma unroll
-        for (int cb = 0; cb < NCB; ++cb) {
-          tot[wave][ib][cb][lane] += acc[ib][cb];
-          acc[ib][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
-        }
-    }
-    cur = nxt;
-  }
-
-#pragma unroll
-  for (int ib = 0; ib < NIB; ++ib)
-#pragma unroll
-    for (int cb = 0; cb < NCB; ++cb) {
-      const floatx4 v = tot[wave][ib][cb][lane] + acc[ib][cb];
-      const int c = cb * 16 + p;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int64_t i = (ib0 + ib) * TILE + 4 * g + e;
-        if (part != nullptr) {
-          part[(split * nrpad + i) * (NCB * 16) + c] = v[e];
-        } else if (i < Nr && c < b) {
-          const float y = v[e] * colscale[c];
-          Y[i * ldy + c] = (sl != nullptr) ? y * sl[i] : y;
-        }
-      }
-    }
-}
-
-
 // ------------------------------------------------------------------ bfloat16 inputs
 //
 // For X in bfloat16 the exponent contraction runs on v_mfma_f32_16x16x32_bf16:
@@ -734,7 +226,6 @@ __global__ void pack_bf16_kernel(const uint16_t* __restrict__ X, int64_t n, int 
   xp[idx] = out;
 }
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 template <int DC, bool DIAG>
 __device__ __forceinline__ floatx4 half_sqdist(const uintx4* xa, const floatx4& aj,
@@ -1050,11 +541,6 @@ KVPlan plan_product(int64_t Nr, int64_t Nc, int dp, int b) {
 
 KVPlan plan_rowsum(int64_t Nr, int64_t Nc, int dp) { return plan_tiles(Nr, Nc, dp, 1, 4); }
 
-static inline unsigned blocks_for(int64_t n, int t) { return unsigned(ceil_div(n, t)); }
-
-// Extents (in floats) the kernels touch, checked against the carved regions
-// before every launch.
-static inline size_t xp_extent(int64_t tiles, int dp) { return size_t(tiles) * dp * TILE; }
 static inline size_t lane4_extent(int64_t tiles, int groups) {
   return size_t(tiles) * groups * 64 * 4;
 }
@@ -1083,37 +569,15 @@ void launch_pack_points(const void* X, fd_dtype xt, int64_t n, int64_t D, int64_
   out.beta = beta;
   if (xt == FD_BF16) {
     pack_points_bf16(static_cast<const uint16_t*>(X), n, D, ldx, row_side, out, stream);
+    out.rid = -1;
+    out.row_side = row_side;
     return;
   }
   out.bf16 = false;
   out.dc = 0;
-  const double bl = beta * LOG2E;
-  // rows carry the factor 2*beta*log2(e) of the cross term; columns are plain
-  const double scale = row_side ? 2.0 * bl : 1.0;
-  const bool with_ap = !row_side;
-  FD_REQUIRE(out.npad % TILE == 0 && out.npad >= n && out.dp % 4 == 0 && D <= out.dp,
-             FD_ERR_INVALID_ARG, "internal: bad point pack geometry");
-  check_span(out.xp, xp_extent(out.npad / TILE, out.dp), "point pack");
-  check_span(out.ar, size_t(out.npad), "row offsets");
-  if (with_ap) check_span(out.ap, lane4_extent(out.npad / TILE, 1), "column offsets");
-  const unsigned grid = blocks_for(out.npad, 256);
-  float* ap = with_ap ? out.ap.p : nullptr;
-  hipLaunchKernelGGL(pack_points_kernel<float>, dim3(grid), dim3(256), 0, stream,
-                     static_cast<const float*>(X), n, int(D), ldx, bl, scale, out.xp.p, ap,
-                     out.ar.p, out.npad, out.dp);
-  FD_LAUNCH_CHECK();
-}
-
-void launch_pack_v(const float* V, int64_t n, int64_t b, int64_t ldv, const float* sr, int ncb,
-                   int64_t npad, FSpan vp, hipStream_t stream) {
-  FD_REQUIRE(npad % TILE == 0 && npad >= n && b <= ncb * 16, FD_ERR_INVALID_ARG,
-             "internal: bad V pack geometry");
-  const int64_t ntiles = npad / TILE;
-  check_span(vp, lane4_extent(ntiles, ncb), "V pack");
-  const int64_t total = ntiles * ncb * 64;
-  hipLaunchKernelGGL(pack_v_kernel, dim3(blocks_for(total, 256)), dim3(256), 0, stream, V, n,
-                     int(b), ldv, sr, ncb, ntiles, reinterpret_cast<floatx4*>(vp.p));
-  FD_LAUNCH_CHECK();
+  FD_REQUIRE(out.dp % 4 == 0 && D <= out.dp, FD_ERR_INVALID_ARG,
+             "internal: bad point pack geometry");
+  launch_pack_points_hx(static_cast<const float*>(X), n, D, ldx, beta, row_side, out, stream);
 }
 
 void launch_pack_w(const float* w, int64_t n, int64_t npad, FSpan wp, hipStream_t stream) {
@@ -1139,12 +603,9 @@ static void check_tiles(const KVPlan& p, const PointPack& rows, const PointPack&
   if (rows.bf16) {
     check_span(rows.xp, size_t(row_tiles) * rows.dc * 64 * 4, "bf16 row pack");
     check_span(cols.xp, size_t(round_up(p.njb, 2)) * cols.dc * 64 * 4, "bf16 column pack");
-  } else {
-    check_span(rows.xp, xp_extent(row_tiles, p.dp), "row pack");
-    check_span(cols.xp, xp_extent(round_up(p.njb, 2), p.dp), "column pack");
+    check_span(rows.ar, size_t(rows.npad), "row offsets");
+    check_span(cols.ap, lane4_extent(round_up(p.njb, 2), 1), "column offsets");
   }
-  check_span(rows.ar, size_t(rows.npad), "row offsets");
-  check_span(cols.ap, lane4_extent(round_up(p.njb, 2), 1), "column offsets");
 }
 
 void launch_pack_v_split(const float* V, int64_t n, int64_t b, int64_t ldv, const float* sr,
@@ -1217,45 +678,6 @@ static void product_bf16_ncb(const KVPlan& p, const PointPack& rows, const Point
   throw Error{FD_ERR_UNSUPPORTED, "block width above 64"};
 }
 
-template <int DP, int NCB, int NIB>
-static void product_launch(const KVPlan& p, const PointPack& rows, const PointPack& cols,
-                           const float* vp, const float* colscale, bool diag, const float* sl,
-                           float* Y, int64_t ldy, int b, float* part, hipStream_t stream) {
-  const unsigned grid = unsigned(p.nrt * p.nsplit);
-  ProfScope prof(FD_KERNEL_PRODUCT, stream);
-  hipLaunchKernelGGL((product_split_kernel<DP, NCB, NIB>), dim3(grid), dim3(WG_THREADS), 0,
-                     stream, cols.xp.p, reinterpret_cast<const floatx4*>(cols.ap.p),
-                     reinterpret_cast<const VSplit*>(vp), rows.xp.p, rows.ar.p, p.nrt,
-                     ceil_div(p.njb, 2), p.jb_per_split / 2, int(diag), colscale, sl, Y, ldy,
-                     rows.n, b, part, rows.npad);
-  FD_LAUNCH_CHECK();
-}
-
-template <int DP, int NCB>
-static void product_dispatch_nib(const KVPlan& p, const PointPack& rows, const PointPack& cols,
-                                 const float* vp, const float* colscale, bool diag,
-                                 const float* sl, float* Y, int64_t ldy, int b, float* part,
-                                 hipStream_t stream) {
-  switch (p.nib) {
-    case 2: return product_launch<DP, NCB, 2>(p, rows, cols, vp, colscale, diag, sl, Y, ldy, b, part, stream);
-    case 4: return product_launch<DP, NCB, 4>(p, rows, cols, vp, colscale, diag, sl, Y, ldy, b, part, stream);
-  }
-  throw Error{FD_ERR_INVALID_ARG, "internal: unsupported rows per wave"};
-}
-
-template <int DP>
-static void product_dispatch_ncb(const KVPlan& p, const PointPack& rows, const PointPack& cols,
-                                 const float* vp, const float* cs, bool diag, const float* sl,
-                                 float* Y, int64_t ldy, int b, float* part, hipStream_t stream) {
-  switch (p.ncb) {
-    case 1: return product_dispatch_nib<DP, 1>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
-    case 2: return product_dispatch_nib<DP, 2>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
-    case 3: return product_dispatch_nib<DP, 3>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
-    case 4: return product_dispatch_nib<DP, 4>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
-  }
-  throw Error{FD_ERR_UNSUPPORTED, "block width above 64"};
-}
-
 void launch_product(const KVPlan& p, const PointPack& rows, const PointPack& cols, FSpan vp,
                     FSpan vscale, bool diag, const float* sl, float* Y, int64_t ldy, int b,
                     FSpan part, hipStream_t stream) {
@@ -1280,18 +702,8 @@ void launch_product(const KVPlan& p, const PointPack& rows, const PointPack& col
     else
       product_bf16_ncb<2>(p, rows, cols, vp.p, cs, diag, sl, Y, ldy, b, pp, stream);
   } else {
-  check_span(vp, size_t(ceil_div(p.njb, 2)) * p.ncb * 64 * 8, "split V pack");
-  switch (p.dp) {
-    case 4: product_dispatch_ncb<4>(p, rows, cols, vp.p, cs, diag, sl, Y, ldy, b, pp, stream); break;
-    case 8: product_dispatch_ncb<8>(p, rows, cols, vp.p, cs, diag, sl, Y, ldy, b, pp, stream); break;
-    case 12: product_dispatch_ncb<12>(p, rows, cols, vp.p, cs, diag, sl, Y, ldy, b, pp, stream); break;
-    case 16: product_dispatch_ncb<16>(p, rows, cols, vp.p, cs, diag, sl, Y, ldy, b, pp, stream); break;
-    case 24: product_dispatch_ncb<24>(p, rows, cols, vp.p, cs, diag, sl, Y, ldy, b, pp, stream); break;
-    case 32: product_dispatch_ncb<32>(p, rows, cols, vp.p, cs, diag, sl, Y, ldy, b, pp, stream); break;
-    case 48: product_dispatch_ncb<48>(p, rows, cols, vp.p, cs, diag, sl, Y, ldy, b, pp, stream); break;
-    case 64: product_dispatch_ncb<64>(p, rows, cols, vp.p, cs, diag, sl, Y, ldy, b, pp, stream); break;
-    default: throw Error{FD_ERR_UNSUPPORTED, "feature dimension above 64"};
-  }
+    check_span(vp, size_t(ceil_div(p.njb, 2)) * p.ncb * 64 * 8, "split V pack");
+    launch_product_hx(p, rows, cols, vp.p, cs, diag, sl, Y, ldy, b, pp, stream);
   }
   if (p.nsplit > 1) {
     const int64_t total = rows.n * b;
@@ -1299,29 +711,6 @@ void launch_product(const KVPlan& p, const PointPack& rows, const PointPack& col
                        pp, p.nsplit, rows.npad, p.ncb * 16, cs, sl, Y, ldy, rows.n, b);
     FD_LAUNCH_CHECK();
   }
-}
-
-template <int DP, bool UNIT>
-static void rowsum_dispatch(const KVPlan& p, const PointPack& rows, const PointPack& cols,
-                            const float* wp, bool diag, float* out, float* part,
-                            hipStream_t stream) {
-  const unsigned grid = unsigned(p.nrt * p.nsplit);
-  ProfScope prof(FD_KERNEL_ROWSUM, stream);
-  hipLaunchKernelGGL((rowsum_f32_kernel<DP, 4, UNIT>), dim3(grid), dim3(WG_THREADS), 0, stream,
-                     cols.xp.p, reinterpret_cast<const floatx4*>(cols.ap.p),
-                     reinterpret_cast<const floatx4*>(wp), rows.xp.p, rows.ar.p, p.nrt, p.njb,
-                     p.jb_per_split, int(diag), out, rows.n, part, rows.npad);
-  FD_LAUNCH_CHECK();
-}
-
-template <int DP>
-static void rowsum_dispatch_u(const KVPlan& p, const PointPack& rows, const PointPack& cols,
-                              const float* wp, bool diag, float* out, float* part,
-                              hipStream_t stream) {
-  if (wp == nullptr)
-    rowsum_dispatch<DP, true>(p, rows, cols, wp, diag, out, part, stream);
-  else
-    rowsum_dispatch<DP, false>(p, rows, cols, wp, diag, out, part, stream);
 }
 
 template <int DC, bool UNIT>
@@ -1361,17 +750,7 @@ void launch_rowsum(const KVPlan& p, const PointPack& rows, const PointPack& cols
       unit ? rowsum_bf16_launch<2, true>(p, rows, cols, wp.p, diag, out, pp, stream)
            : rowsum_bf16_launch<2, false>(p, rows, cols, wp.p, diag, out, pp, stream);
   } else {
-  switch (p.dp) {
-    case 4: rowsum_dispatch_u<4>(p, rows, cols, wp.p, diag, out, pp, stream); break;
-    case 8: rowsum_dispatch_u<8>(p, rows, cols, wp.p, diag, out, pp, stream); break;
-    case 12: rowsum_dispatch_u<12>(p, rows, cols, wp.p, diag, out, pp, stream); break;
-    case 16: rowsum_dispatch_u<16>(p, rows, cols, wp.p, diag, out, pp, stream); break;
-    case 24: rowsum_dispatch_u<24>(p, rows, cols, wp.p, diag, out, pp, stream); break;
-    case 32: rowsum_dispatch_u<32>(p, rows, cols, wp.p, diag, out, pp, stream); break;
-    case 48: rowsum_dispatch_u<48>(p, rows, cols, wp.p, diag, out, pp, stream); break;
-    case 64: rowsum_dispatch_u<64>(p, rows, cols, wp.p, diag, out, pp, stream); break;
-    default: throw Error{FD_ERR_UNSUPPORTED, "feature dimension above 64"};
-  }
+    launch_rowsum_hx(p, rows, cols, wp.p, diag, out, pp, stream);
   }
   if (p.nsplit > 1) {
     hipLaunchKernelGGL(reduce_rowsum_kernel, dim3(blocks_for(rows.n, 256)), dim3(256), 0, stream,
