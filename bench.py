@@ -9,8 +9,14 @@ Inputs are resident in HBM before the timed region.
 
 Printed value: whole-step throughput in kernel pair-columns per second,
 sum over the sweep of N^2 * b divided by the step time (the normalisation
-passes are inside the step time).  The roofline object is for the fused
-product kernel, timed with HIP events on its launch stream.
+passes are inside the step time).  The roofline object is for the kernel
+with the larger share of the step (the row-sum pass or the fused product),
+timed with HIP events on its launch stream.  Its bound is the transcendental
+rate: every kernel entry costs one v_exp_f32, and the matrix-core work of the
+contractions does not run concurrently with the vector ALUs on gfx950, so the
+exponentials set the floor.  HBM traffic comes from the rocprofv3 counter
+summary under profiles/ when that summary was taken on the current kernel
+sources, else it is null.
 
 ``--lanczos`` adds the time to the top-16 eigenpairs on the 2-torus
 workload (N = 2048, beta = 8, b = 8) as an extra field.
@@ -29,8 +35,40 @@ import numpy as np
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-PEAK_FP32_MFMA_TFLOPS = 157.3
 PEAK_HBM_GBS = 8000.0
+# v_exp_f32 issues a wave64 in 8 cycles (half the plain-VALU rate of 16
+# lanes/cycle): 256 CUs x 4 SIMDs x 8 lanes x 2.4 GHz
+PEAK_EXP_TS = 256 * 4 * 8 * 2.4e9 / 1e12
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_torus6.md")
+KERNEL_SOURCES = ("hx_kernels.hip", "kv_common.hpp", "kv_kernels.hip")
+
+
+def kernel_source_hash() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2609_38198_amd", "csrc", name), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def recorded_traffic(kernel: str):
+    """HBM bytes per launch of `kernel` from the counter summary, if current."""
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            text = fh.read()
+    except OSError:
+        return None
+    fields = {}
+    for line in text.splitlines():
+        line = line.strip().lstrip("-* ")
+        if ":" in line:
+            k, v = line.split(":", 1)
+            fields[k.strip()] = v.strip().strip("`")
+    if fields.get("kernel_source_sha256_16") != kernel_source_hash():
+        return None
+    v = fields.get(f"{kernel}_hbm_bytes_per_launch")
+    return float(v) if v else None
 
 
 def log(msg: str) -> None:
@@ -113,7 +151,8 @@ def molecule_leg(fd, torch, dev) -> dict:
             "restarts": e.info["restarts"], "nconv": e.info["nconv"],
             "max_residual": e.info["max_residual"], "gap_perron": e.info["gap_perron"],
             "product_avg_ms": avg * 1e3, "product_tflops": flops / avg / 1e12,
-            "product_frac_fp32_mfma": flops / avg / 1e12 / PEAK_FP32_MFMA_TFLOPS,
+            "product_texp_per_s": float(N) * N / avg / 1e12,
+            "product_frac_exp_peak": float(N) * N / avg / 1e12 / PEAK_EXP_TS,
             "product_total_s": pms * 1e-3, "rowsum_total_s": rms * 1e-3,
             "evals_head": e.evals[:4], "evals_tail": e.evals[-2:]}
 
@@ -244,8 +283,12 @@ def main() -> int:
     value = pair_cols / (ms_per_step * 1e-3)
     avg_prod_s = prod_ms * 1e-3 / max(prod_n, 1)
     flops = 2.0 * N * N * (D + b)
-    achieved = flops / avg_prod_s / 1e12
     avg_row_s = row_ms * 1e-3 / max(row_n, 1)
+    # one exponential per kernel entry and launch, in both kernels
+    exp_prod = float(N) * N / avg_prod_s / 1e12
+    exp_row = float(N) * N / avg_row_s / 1e12
+    dominant = "rowsum" if row_ms >= prod_ms else "product"
+    achieved = exp_row if dominant == "rowsum" else exp_prod
 
     rec = {
         "metric": "fused K*V pair-cols/sec (N^2*b per sec)",
@@ -264,17 +307,21 @@ def main() -> int:
                                f"alpha={alpha}: per beta 2 normalisation passes + 1 fused "
                                f"normalised product", "N": N, "D": D, "b": b,
                    "betas": list(betas), "alpha": alpha, "parallelism": "single GPU"},
-        "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_FP32_MFMA_TFLOPS,
-                     "unit": "TFLOP/s", "frac": achieved / PEAK_FP32_MFMA_TFLOPS,
-                     "traffic": None},
+        "roofline": {"bound": "alu", "kernel": dominant, "achieved": achieved,
+                     "peak": PEAK_EXP_TS, "unit": "Texp/s", "frac": achieved / PEAK_EXP_TS,
+                     "traffic": recorded_traffic(dominant)},
         "kernels": {
             "product": {"launches": prod_n, "avg_ms": avg_prod_s * 1e3,
+                        "step_ms": prod_ms / args.steps,
                         "pair_cols_per_s": float(N) * N * b / avg_prod_s,
-                        "exp_per_s": float(N) * N / avg_prod_s,
-                        "flops_per_launch": flops},
+                        "texp_per_s": exp_prod, "frac_exp_peak": exp_prod / PEAK_EXP_TS,
+                        "contraction_tflops": flops / avg_prod_s / 1e12,
+                        "hbm_bytes_per_launch": recorded_traffic("product")},
             "rowsum": {"launches": row_n, "avg_ms": avg_row_s * 1e3,
-                       "pairs_per_s": float(N) * N / avg_row_s,
-                       "tflops": 2.0 * N * N * D / avg_row_s / 1e12},
+                       "step_ms": row_ms / args.steps,
+                       "texp_per_s": exp_row, "frac_exp_peak": exp_row / PEAK_EXP_TS,
+                       "contraction_tflops": 2.0 * N * N * D / avg_row_s / 1e12,
+                       "hbm_bytes_per_launch": recorded_traffic("rowsum")},
         },
     }
     if args.lanczos:

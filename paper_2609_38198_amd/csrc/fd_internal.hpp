@@ -68,7 +68,7 @@ struct Arena {
 // ---------------------------------------------------------------- geometry
 constexpr int TILE = 16;          // points per MFMA tile
 constexpr int WG_THREADS = 256;   // four wave64 per workgroup
-constexpr int ROW_PAD = 256;      // row packs are padded to this many points
+constexpr int ROW_PAD = 512;      // row packs: whole workgroups of 4 waves x 8 row tiles
 constexpr int COL_PAD = 32;       // column packs: whole pairs of 16-point tiles
 
 inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }

@@ -65,11 +65,12 @@ namespace {
 enum : int8_t { SEG_END = 0, SEG_X = 1, SEG_ONES = 2, SEG_A = 3 };
 
 // A run of slots: SEG_X holds piece `piece` of features foff .. foff+cap-1
-// (zero past D); SEG_ONES holds three 1s; SEG_A the three pieces of a.
+// (zero past D); SEG_ONES holds cap 1s; SEG_A holds pieces piece .. piece+cap-1
+// of the offset a.
 struct HxSeg {
   int8_t kind, piece, slot, cap, foff;
 };
-constexpr int HX_SEGS = 8, HX_CHUNKS = 7, HX_MFMAS = 13, HX_RECIPES = 6;
+constexpr int HX_SEGS = 8, HX_CHUNKS = 7, HX_MFMAS = 13, HX_RECIPES = 7;
 struct HxChunk {
   HxSeg s[HX_SEGS];
 };
@@ -87,8 +88,12 @@ struct HxRecipe {
 constexpr HxSeg X(int piece, int slot, int cap, int foff = 0) {
   return HxSeg{SEG_X, int8_t(piece), int8_t(slot), int8_t(cap), int8_t(foff)};
 }
-constexpr HxSeg ONES(int slot) { return HxSeg{SEG_ONES, 0, int8_t(slot), 3, 0}; }
-constexpr HxSeg AOF(int slot) { return HxSeg{SEG_A, 0, int8_t(slot), 3, 0}; }
+constexpr HxSeg ONES(int slot, int cap = 3) {
+  return HxSeg{SEG_ONES, 0, int8_t(slot), int8_t(cap), 0};
+}
+constexpr HxSeg AOF(int slot) { return HxSeg{SEG_A, 1, int8_t(slot), 3, 0}; }
+// single piece k of the offset
+constexpr HxSeg APC(int slot, int k) { return HxSeg{SEG_A, int8_t(k), int8_t(slot), 1, 0}; }
 
 // Column side: x pieces, a_j against row-side 1s; row side: b pieces, a_i
 // against column-side 1s.  Slot by slot the column and row chunks of each
@@ -114,15 +119,27 @@ constexpr HxRecipe HX_TABLE[HX_RECIPES] = {
      {{{{X(1, 0, 13), AOF(13), X(1, 16, 13), ONES(29)}},
        {{X(2, 0, 13), X(1, 16, 13)}},
        {{X(3, 0, 13), X(2, 16, 13)}}}}},
-    // D <= 26: one piece per chunk, offsets in the spare slots of chunk pair (0, 0)
-    {26, 3, 3, 6, {0, 1, 0, 2, 0, 1}, {0, 0, 1, 0, 2, 1},
-     {{{{X(1, 0, 26), ONES(26), AOF(29)}}, {{X(2, 0, 26)}}, {{X(3, 0, 26)}}}},
-     {{{{X(1, 0, 26), AOF(26), ONES(29)}}, {{X(2, 0, 26)}}, {{X(3, 0, 26)}}}}},
+    // D <= 30: one piece per chunk; the offsets use the two spare slots of
+    // each chunk.  Slot 30: 1 on x1 against a_i1, a_i2, a_i3 on b1, b2, b3;
+    // slot 31: a_j1, a_j2, a_j3 on x1, x2, x3 against 1 on b1.  The six
+    // instructions meet each offset piece exactly once.
+    {30, 3, 3, 6, {0, 1, 0, 2, 0, 1}, {0, 0, 1, 0, 2, 1},
+     {{{{X(1, 0, 30), ONES(30, 1), APC(31, 1)}}, {{X(2, 0, 30), APC(31, 2)}},
+       {{X(3, 0, 30), APC(31, 3)}}}},
+     {{{{X(1, 0, 30), APC(30, 1), ONES(31, 1)}}, {{X(2, 0, 30), APC(30, 2)}},
+       {{X(3, 0, 30), APC(30, 3)}}}}},
     // D <= 32: offsets in a chunk of their own
     {32, 4, 4, 7, {0, 3, 1, 0, 2, 0, 1}, {0, 3, 0, 1, 0, 2, 1},
      {{{{X(1, 0, 32)}}, {{X(2, 0, 32)}}, {{X(3, 0, 32)}}, {{ONES(0), AOF(3)}}}},
      {{{{X(1, 0, 32)}}, {{X(2, 0, 32)}}, {{X(3, 0, 32)}}, {{AOF(0), ONES(3)}}}}},
-    // D <= 64: two chunks per piece
+    // D <= 62: two chunks per piece; the offsets take the spare slots of the
+    // second chunks, laid out as for D <= 30
+    {62, 6, 6, 12, {0, 1, 2, 3, 0, 1, 4, 5, 0, 1, 2, 3}, {0, 1, 0, 1, 2, 3, 0, 1, 4, 5, 2, 3},
+     {{{{X(1, 0, 32)}}, {{X(1, 0, 30, 32), ONES(30, 1), APC(31, 1)}}, {{X(2, 0, 32)}},
+       {{X(2, 0, 30, 32), APC(31, 2)}}, {{X(3, 0, 32)}}, {{X(3, 0, 30, 32), APC(31, 3)}}}},
+     {{{{X(1, 0, 32)}}, {{X(1, 0, 30, 32), APC(30, 1), ONES(31, 1)}}, {{X(2, 0, 32)}},
+       {{X(2, 0, 30, 32), APC(30, 2)}}, {{X(3, 0, 32)}}, {{X(3, 0, 30, 32), APC(30, 3)}}}}},
+    // D <= 64: two chunks per piece, offsets in a chunk of their own
     {64, 7, 7, 13, {0, 1, 6, 2, 3, 0, 1, 4, 5, 0, 1, 2, 3}, {0, 1, 6, 0, 1, 2, 3, 0, 1, 4, 5, 2, 3},
      {{{{X(1, 0, 32)}}, {{X(1, 0, 32, 32)}}, {{X(2, 0, 32)}}, {{X(2, 0, 32, 32)}},
        {{X(3, 0, 32)}}, {{X(3, 0, 32, 32)}}, {{ONES(0), AOF(3)}}}},
@@ -145,8 +162,8 @@ struct Hx {
 // in 256 registers (they spill at 2).
 template <int RID, int NCB, int NIB>
 constexpr int hx_waves() {
-  const bool big = (NIB == 4 && ((NCB == 4 && RID >= 1) || (NCB == 3 && RID >= 3) || RID == 5)) ||
-                   (RID == 5 && NCB >= 3);
+  const bool big = (NIB == 4 && ((NCB == 4 && RID >= 1) || (NCB == 3 && RID >= 3) || RID >= 5)) ||
+                   (RID >= 5 && NCB >= 3) || (NIB == 8 && (RID >= 3 || NCB >= 2));
   return big ? 1 : 2;
 }
 
@@ -209,7 +226,7 @@ __global__ void pack_hx_kernel(const float* __restrict__ X, int64_t n, int D, in
           }
           a = neg_bl * r + shift;
         }
-        v = piece_of(a, off + 1);
+        v = piece_of(a, sg.piece + off);
       }
       h[e] = _Float16(v);
     }
@@ -550,6 +567,10 @@ void product_hx_nib(const KVPlan& p, const PointPack& rows, const PointPack& col
   switch (p.nib) {
     case 2: return product_hx_launch<RID, NCB, 2>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
     case 4: return product_hx_launch<RID, NCB, 4>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
+    case 8:
+      if constexpr (RID <= 3 && NCB <= 2)
+        return product_hx_launch<RID, NCB, 8>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
+      break;
   }
   throw Error{FD_ERR_INVALID_ARG, "internal: unsupported rows per wave"};
 }
@@ -567,12 +588,12 @@ void product_hx_ncb(const KVPlan& p, const PointPack& rows, const PointPack& col
   throw Error{FD_ERR_UNSUPPORTED, "block width above 64"};
 }
 
-template <int RID, bool UNIT>
+template <int RID, int NIB, bool UNIT>
 void rowsum_hx_launch(const KVPlan& p, const PointPack& rows, const PointPack& cols,
                       const float* wp, bool diag, float* out, float* part, hipStream_t stream) {
   const unsigned grid = unsigned(p.nrt * p.nsplit);
   ProfScope prof(FD_KERNEL_ROWSUM, stream);
-  hipLaunchKernelGGL((rowsum_hx_kernel<RID, 4, UNIT>), dim3(grid), dim3(WG_THREADS), 0, stream,
+  hipLaunchKernelGGL((rowsum_hx_kernel<RID, NIB, UNIT>), dim3(grid), dim3(WG_THREADS), 0, stream,
                      reinterpret_cast<const uintx4*>(cols.xp.p),
                      reinterpret_cast<const floatx4*>(wp),
                      reinterpret_cast<const uintx4*>(rows.xp.p), p.nrt, p.njb, p.jb_per_split,
@@ -583,10 +604,17 @@ void rowsum_hx_launch(const KVPlan& p, const PointPack& rows, const PointPack& c
 template <int RID>
 void rowsum_hx_u(const KVPlan& p, const PointPack& rows, const PointPack& cols, const float* wp,
                  bool diag, float* out, float* part, hipStream_t stream) {
+  if (p.nib == 8) {
+    if (wp == nullptr)
+      rowsum_hx_launch<RID, 8, true>(p, rows, cols, wp, diag, out, part, stream);
+    else
+      rowsum_hx_launch<RID, 8, false>(p, rows, cols, wp, diag, out, part, stream);
+    return;
+  }
   if (wp == nullptr)
-    rowsum_hx_launch<RID, true>(p, rows, cols, wp, diag, out, part, stream);
+    rowsum_hx_launch<RID, 4, true>(p, rows, cols, wp, diag, out, part, stream);
   else
-    rowsum_hx_launch<RID, false>(p, rows, cols, wp, diag, out, part, stream);
+    rowsum_hx_launch<RID, 4, false>(p, rows, cols, wp, diag, out, part, stream);
 }
 
 void check_hx(const KVPlan& p, const PointPack& rows, const PointPack& cols) {
@@ -644,13 +672,14 @@ void launch_product_hx(const KVPlan& p, const PointPack& rows, const PointPack& 
     case 3: return product_hx_ncb<3>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
     case 4: return product_hx_ncb<4>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
     case 5: return product_hx_ncb<5>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
+    case 6: return product_hx_ncb<6>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
   }
 }
 
 void launch_rowsum_hx(const KVPlan& p, const PointPack& rows, const PointPack& cols,
                       const float* wp, bool diag, float* out, float* part, hipStream_t stream) {
   check_hx(p, rows, cols);
-  FD_REQUIRE(p.nib == 4, FD_ERR_INVALID_ARG, "internal: row-sum plan");
+  FD_REQUIRE(p.nib == 4 || p.nib == 8, FD_ERR_INVALID_ARG, "internal: row-sum plan");
   switch (rows.rid) {
     case 0: return rowsum_hx_u<0>(p, rows, cols, wp, diag, out, part, stream);
     case 1: return rowsum_hx_u<1>(p, rows, cols, wp, diag, out, part, stream);
@@ -658,6 +687,7 @@ void launch_rowsum_hx(const KVPlan& p, const PointPack& rows, const PointPack& c
     case 3: return rowsum_hx_u<3>(p, rows, cols, wp, diag, out, part, stream);
     case 4: return rowsum_hx_u<4>(p, rows, cols, wp, diag, out, part, stream);
     case 5: return rowsum_hx_u<5>(p, rows, cols, wp, diag, out, part, stream);
+    case 6: return rowsum_hx_u<6>(p, rows, cols, wp, diag, out, part, stream);
   }
 }
 

@@ -67,6 +67,19 @@ def test_torus6_full_size_markov_rows_sum_to_one(beta):
     assert rel_fro(to_np(q)[rows], qref) <= TOL_F32
 
 
+@pytest.mark.parametrize("D", [1, 5, 9, 14, 27, 31, 33, 63])
+def test_every_feature_width(D):
+    rng = np.random.default_rng(2000 + D)
+    X = (rng.normal(size=(900, D)) * 0.5).astype(np.float32)
+    X -= X.mean(0)
+    dev = device()
+    case(f"degree feature width D={D}")
+    deg = fd.fd_degree(to_dev(X, dev), 2.0 / D, 0.5)
+    ref = on.normalise(X, 2.0 / D, 0.5)
+    for name in ("q", "d", "s"):
+        assert rel_fro(to_np(getattr(deg, name)), getattr(ref, name)) <= TOL_F32
+
+
 def test_grid_torus_constant_degree():
     counts = (8, 8, 8, 8, 4, 4)
     X = inputs.grid_torus_points(counts).astype(np.float32)

@@ -97,6 +97,25 @@ def test_ragged_and_edge_shapes(N, D, b, beta):
     assert rel_fro(Y, ref) <= TOL_F32
 
 
+# every range boundary of the float32 path's contraction layouts (D <= 4, 8,
+# 13, 30, 32, 62, 64) and the widths on either side of it
+RECIPE_DIMS = [1, 4, 5, 8, 9, 13, 14, 26, 27, 30, 31, 32, 33, 48, 62, 63, 64]
+
+
+@pytest.mark.parametrize("D", RECIPE_DIMS)
+def test_every_feature_width(D):
+    rng = np.random.default_rng(1000 + D)
+    N = 700
+    X = (rng.normal(size=(N, D)) * 0.5).astype(np.float32)
+    X -= X.mean(0)
+    V = rng.normal(size=(N, 5)).astype(np.float32)
+    beta = 2.0 / D  # mean exponent about -1
+    case(f"feature width D={D} N={N} b=5")
+    Y = _run(X, None, beta, V)
+    ref = ok.kernel_matmul(X, None, beta, V)
+    assert rel_fro(Y, ref) <= TOL_F32
+
+
 def test_beta_zero_gives_column_sums():
     rng = np.random.default_rng(1)
     X = rng.normal(size=(513, 7)).astype(np.float32)
