@@ -147,6 +147,76 @@ constexpr HxRecipe HX_TABLE[HX_RECIPES] = {
        {{X(3, 0, 32)}}, {{X(3, 0, 32, 32)}}, {{AOF(0), ONES(3)}}}}},
 };
 
+// ------------------------------------------------------------------ recipe check
+//
+// Compile-time proof that every recipe contracts exactly
+//   sum_f sum_{p + q <= 4} x_p[f] b_q[f] + (a_i1 + a_i2 + a_i3) + (a_j1 + a_j2 + a_j3)
+// for all features f < maxd: over the instructions' (column chunk, row chunk)
+// pairs, slot by slot, each such product appears once, features match, and
+// every other pairing has a zero on one side.  Segments may not overlap.
+
+struct HxSlot {
+  int kind = SEG_END, piece = 0, feat = 0;
+  bool clash = false;
+};
+
+constexpr HxSlot hx_slot(const HxChunk& c, int slot) {
+  HxSlot out;
+  for (int k = 0; k < HX_SEGS; ++k) {
+    const HxSeg& g = c.s[k];
+    if (g.kind == SEG_END) break;
+    if (g.slot + g.cap > 32) out.clash = true;
+    if (slot < g.slot || slot >= g.slot + g.cap) continue;
+    if (out.kind != SEG_END) out.clash = true;
+    const int off = slot - g.slot;
+    out.kind = g.kind;
+    out.piece = g.kind == SEG_A ? g.piece + off : g.piece;
+    out.feat = g.foff + off;
+  }
+  return out;
+}
+
+constexpr bool hx_valid(const HxRecipe& R) {
+  int cnt[64][4][4] = {};
+  int ai[4] = {}, aj[4] = {};
+  if (R.nm < 1 || R.nm > HX_MFMAS || R.nc > HX_CHUNKS || R.nb > HX_CHUNKS) return false;
+  for (int m = 0; m < R.nm; ++m) {
+    if (R.sa[m] < 0 || R.sa[m] >= R.nc || R.sb[m] < 0 || R.sb[m] >= R.nb) return false;
+    for (int slot = 0; slot < 32; ++slot) {
+      const HxSlot c = hx_slot(R.col.ch[R.sa[m]], slot);
+      const HxSlot r = hx_slot(R.row.ch[R.sb[m]], slot);
+      if (c.clash || r.clash) return false;
+      if (c.kind == SEG_END || r.kind == SEG_END) continue;
+      if (c.kind == SEG_X && r.kind == SEG_X) {
+        if (c.feat != r.feat || c.feat >= 64 || c.piece + r.piece > 4) return false;
+        ++cnt[c.feat][c.piece][r.piece];
+      } else if (c.kind == SEG_ONES && r.kind == SEG_A) {
+        if (r.piece < 1 || r.piece > 3) return false;
+        ++ai[r.piece];
+      } else if (c.kind == SEG_A && r.kind == SEG_ONES) {
+        if (c.piece < 1 || c.piece > 3) return false;
+        ++aj[c.piece];
+      } else {
+        return false;
+      }
+    }
+  }
+  for (int k = 1; k <= 3; ++k)
+    if (ai[k] != 1 || aj[k] != 1) return false;
+  for (int f = 0; f < 64; ++f)
+    for (int p = 1; p <= 3; ++p)
+      for (int q = 1; q <= 3; ++q) {
+        const int want = (f < R.maxd && p + q <= 4) ? 1 : 0;
+        if (cnt[f][p][q] != want) return false;
+      }
+  return true;
+}
+
+static_assert(hx_valid(HX_TABLE[0]) && hx_valid(HX_TABLE[1]) && hx_valid(HX_TABLE[2]) &&
+                  hx_valid(HX_TABLE[3]) && hx_valid(HX_TABLE[4]) && hx_valid(HX_TABLE[5]) &&
+                  hx_valid(HX_TABLE[6]),
+              "a split-exponent recipe does not contract the intended sum");
+
 template <int RID>
 struct Hx {
   static constexpr int nc = HX_TABLE[RID].nc;
@@ -184,13 +254,20 @@ __device__ __forceinline__ float piece_of(double v, int k) {
   return out;
 }
 
+// Slot map of one side: per chunk and slot, what the slot holds, decoded from
+// the recipe's segments on the host: 0 = zero, SEG_X << 14 | piece << 8 |
+// feature, SEG_ONES << 14, SEG_A << 14 | piece.
+struct HxSlotMap {
+  int16_t code[HX_CHUNKS][32];
+};
+
 // One thread per (tile, chunk, lane): the lane's eight slots of the chunk.
 // `scale` multiplies the coordinates (s on the column side, 2 beta log2(e) / s
-// on the row side); the offsets are neg_bl ||x||^2 + shift with
-// neg_bl = -beta log2(e).  Padded points have zero coordinates and offset
-// -65504, so their kernel values are exactly 0.
+// on the row side); the offset is neg_bl ||x||^2 + shift with
+// neg_bl = -beta log2(e), computed once per thread in float64.  Padded points
+// have zero coordinates and offset -65504, so their kernel values are 0.
 __global__ void pack_hx_kernel(const float* __restrict__ X, int64_t n, int D, int64_t ldx,
-                               double scale, double neg_bl, double shift, HxSide side, int nch,
+                               double scale, double neg_bl, double shift, HxSlotMap map, int nch,
                                int64_t ntiles, uintx4* __restrict__ out) {
   const int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
   if (idx >= ntiles * nch * 64) return;
@@ -200,38 +277,50 @@ __global__ void pack_hx_kernel(const float* __restrict__ X, int64_t n, int D, in
   const int g = lane >> 4, p = lane & 15;
   const int64_t i = tile * TILE + p;
   const bool real = i < n;
+  const float* xi = X + i * ldx;
+  bool have_a = false;
+  double a = -65504.0;
   halfx8 h;
 #pragma unroll
-  for (int e = 0; e < 8; ++e) h[e] = _Float16(0.f);
-  for (int s = 0; s < HX_SEGS; ++s) {
-    const HxSeg sg = side.ch[ch].s[s];
-    if (sg.kind == SEG_END) break;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int off = 8 * g + e - sg.slot;
-      if (off < 0 || off >= sg.cap) continue;
-      float v = 0.f;
-      if (sg.kind == SEG_ONES) {
-        v = 1.f;
-      } else if (sg.kind == SEG_X) {
-        const int f = sg.foff + off;
-        if (real && f < D) v = piece_of(scale * double(X[i * ldx + f]), sg.piece);
-      } else {
-        double a = -65504.0;
-        if (real) {
-          double r = 0.0;
-          for (int k = 0; k < D; ++k) {
-            const double x = double(X[i * ldx + k]);
-            r += x * x;
-          }
-          a = neg_bl * r + shift;
+  for (int e = 0; e < 8; ++e) {
+    const int code = map.code[ch][8 * g + e];
+    const int kind = (code >> 14) & 3;
+    float v = 0.f;
+    if (kind == SEG_X) {
+      const int f = code & 0xff;
+      if (real && f < D) v = piece_of(scale * double(xi[f]), (code >> 8) & 3);
+    } else if (kind == SEG_ONES) {
+      v = 1.f;
+    } else if (kind == SEG_A) {
+      if (!have_a && real) {
+        double r = 0.0;
+        for (int k = 0; k < D; ++k) {
+          const double x = double(xi[k]);
+          r += x * x;
         }
-        v = piece_of(a, sg.piece + off);
+        a = neg_bl * r + shift;
       }
-      h[e] = _Float16(v);
+      have_a = true;
+      v = piece_of(a, code & 3);
     }
+    h[e] = _Float16(v);
   }
   out[idx] = __builtin_bit_cast(uintx4, h);
+}
+
+// Slot map of a recipe side (the segments are checked at compile time).
+HxSlotMap hx_slot_map(const HxSide& side, int nch) {
+  HxSlotMap m{};
+  for (int c = 0; c < nch; ++c)
+    for (int slot = 0; slot < 32; ++slot) {
+      const HxSlot v = hx_slot(side.ch[c], slot);
+      int code = 0;
+      if (v.kind == SEG_X) code = (SEG_X << 14) | (v.piece << 8) | v.feat;
+      if (v.kind == SEG_ONES) code = SEG_ONES << 14;
+      if (v.kind == SEG_A) code = (SEG_A << 14) | v.piece;
+      m.code[c][slot] = int16_t(code);
+    }
+  return m;
 }
 
 // ------------------------------------------------------------------ exponent
@@ -463,11 +552,14 @@ __device__ __forceinline__ void hx_rowsum_tile(const HxCol<RID>& c,
   for (int ib = 0; ib < NIB; ++ib) {
     float k[4];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      k[r] = __builtin_amdgcn_exp2f(t[ib][r]);
-      if (!UNIT) k[r] *= c.w[r];
+    for (int r = 0; r < 4; ++r) k[r] = __builtin_amdgcn_exp2f(t[ib][r]);
+    if (UNIT) {
+      acc[ib] += (k[0] + k[1]) + (k[2] + k[3]);
+    } else {
+      // one FMA per entry: as many vector instructions as the unit-weight sum
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[ib] = fmaf(k[r], c.w[r], acc[ib]);
     }
-    acc[ib] += (k[0] + k[1]) + (k[2] + k[3]);
   }
 }
 
@@ -653,9 +745,10 @@ void launch_pack_points_hx(const float* X, int64_t n, int64_t D, int64_t ldx, do
   if (beta > 0.0) e = std::clamp(int(std::lround(0.5 * std::log2(2.0 * bl))), -12, 12);
   const double s = std::ldexp(1.0, e);
   const double scale = row_side ? 2.0 * bl / s : s;
+  const HxSlotMap map = hx_slot_map(row_side ? R.row : R.col, nch);
   hipLaunchKernelGGL(pack_hx_kernel, dim3(blocks_for(ntiles * nch * 64, 256)), dim3(256), 0,
-                     stream, X, n, int(D), ldx, scale, -bl, row_side ? double(SHIFT) : 0.0,
-                     row_side ? R.row : R.col, nch, ntiles, reinterpret_cast<uintx4*>(out.xp.p));
+                     stream, X, n, int(D), ldx, scale, -bl, row_side ? double(SHIFT) : 0.0, map,
+                     nch, ntiles, reinterpret_cast<uintx4*>(out.xp.p));
   FD_LAUNCH_CHECK();
   out.rid = rid;
   out.row_side = row_side;

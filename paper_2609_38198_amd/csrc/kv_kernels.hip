@@ -499,8 +499,15 @@ __global__ void degree_finish_kernel(const float* __restrict__ q, const float* _
 __global__ __launch_bounds__(1024) void sum_minus_n_kernel(const float* __restrict__ q, int64_t n,
                                                             double* __restrict__ out) {
   __shared__ double red[1024];
-  double s = 0.0;
-  for (int64_t i = threadIdx.x; i < n; i += 1024) s += double(q[i]);
+  // four independent partial sums per thread, each over a fixed index set
+  double s4[4] = {0.0, 0.0, 0.0, 0.0};
+  int64_t i = threadIdx.x;
+  for (; i + 3 * 1024 < n; i += 4 * 1024) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) s4[u] += double(q[i + u * 1024]);
+  }
+  for (; i < n; i += 1024) s4[0] += double(q[i]);
+  double s = (s4[0] + s4[1]) + (s4[2] + s4[3]);
   red[threadIdx.x] = s;
   __syncthreads();
   for (int w = 512; w > 0; w >>= 1) {
@@ -622,7 +629,7 @@ void launch_pack_v_split(const float* V, int64_t n, int64_t b, int64_t ldv, cons
   float* colscale = vscale.p + 64;
   hipLaunchKernelGGL(vmax_zero_kernel, dim3(1), dim3(64), 0, stream, maxbits);
   FD_LAUNCH_CHECK();
-  const int64_t rpb = 1024;
+  const int64_t rpb = 64;  // many small blocks: the pass is bandwidth bound
   hipLaunchKernelGGL(vmax_kernel, dim3(blocks_for(n, int(rpb))), dim3(256), 0, stream, V, n,
                      int(b), ldv, sr, rpb, maxbits);
   FD_LAUNCH_CHECK();

@@ -211,6 +211,7 @@ static SolveResult lanczos_solve(SolverWs& w, Lanczos& L, const SolverLayout& la
   hipStream_t st = L.st;
   const int64_t N = L.N;
   const int b = lay.b, mm = lay.mm;
+  const auto t_start = std::chrono::steady_clock::now();
   SolveResult R;
   int m = 0;
   bool need_rr = false;
@@ -257,11 +258,13 @@ static SolveResult lanczos_solve(SolverWs& w, Lanczos& L, const SolverLayout& la
       if (o.verbose) {
         double worst = 0.0;
         for (int c = 0; c < std::min(k, nkeep); ++c) worst = std::max(worst, rs[c]);
+        const double el =
+            std::chrono::duration<double>(std::chrono::steady_clock::now() - t_start).count();
         std::fprintf(stderr,
                      "[fd_lanczos] N=%lld cycle=%d basis=%d products=%d converged=%d/%d "
-                     "max_residual=%.3e theta0=%.9f theta_k-1=%.6e\n",
+                     "max_residual=%.3e theta0=%.9f theta_k-1=%.6e elapsed=%.3fs\n",
                      (long long)N, R.restarts, m, L.matvecs, nconv, k, worst, th[0],
-                     th[std::min(k, m) - 1]);
+                     th[std::min(k, m) - 1], el);
         std::fflush(stderr);
       }
       R.nconv = nconv;
