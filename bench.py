@@ -232,6 +232,9 @@ def main() -> int:
     ap.add_argument("--molecule", action="store_true")
     ap.add_argument("--continuation", action="store_true")
     ap.add_argument("--stress", action="store_true")
+    ap.add_argument("--calibration-copy", type=int, default=0, metavar="MIB",
+                    help="after the timed steps, copy MIB MiB device to device (a plain copy "
+                         "kernel of known size, read by the HBM counter runs as their scale)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -324,6 +327,13 @@ def main() -> int:
                        "hbm_bytes_per_launch": recorded_traffic("rowsum")},
         },
     }
+    if args.calibration_copy > 0:
+        src = torch.ones(args.calibration_copy << 18, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        rec["calibration_copy_bytes"] = 2 * src.numel() * 4
+        del src, dst
     if args.lanczos:
         rec["lanczos"] = lanczos_leg(fd, torch, dev)
     if args.molecule:
