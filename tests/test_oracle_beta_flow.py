@@ -1,0 +1,132 @@
+"""Pins of the oracle's beta-function flow (Sec. 2.3) against facts that do
+not depend on its own formulas: closed-form initial bandwidths, exact
+spectra, the paper's statement that n_eff equals k for k equally weighted
+interactions per row, the intrinsic dimension of flat grid tori (circulant
+closed form), an exact parabola, and the sweep's three exits on mocked
+probe sequences."""
+import math
+
+import numpy as np
+import pytest
+
+from oracle import beta_flow as bf
+from oracle import normalise as on
+from oracle import torus_grid as tg
+
+
+def circle(N, R, dim=2):
+    t = 2 * np.pi * np.arange(N) / N
+    X = np.zeros((N, dim))
+    X[:, 0] = R * np.cos(t)
+    X[:, 1] = R * np.sin(t)
+    return X + 5.0  # an offset the centring must remove
+
+
+@pytest.mark.parametrize("R,want", [(3.0, 1.0 / 18.0), (1.0, 0.1), (2.0, 0.1)])
+def test_beta0_closed_form(R, want):
+    # centred points on a circle of radius R: mean ||x||^2 = R^2
+    assert bf.beta0(circle(360, R)) == pytest.approx(want, rel=1e-12)
+
+
+def test_v_bias_exact_spectrum():
+    ev = np.exp(-np.array([0.0, 1.0, 2.0, 3.0, 7.0]))
+    assert bf.v_bias(ev) == pytest.approx(2.5, rel=1e-12)  # median of 1, 2, 3, 7
+    assert bf.v_bias(2.0 * ev) == pytest.approx(2.5, rel=1e-12)  # scale invariant
+
+
+@pytest.mark.parametrize("k", [1, 3, 7])
+def test_n_eff_counts_equal_interactions(k):
+    # groups of k + 1 coincident points, groups far apart: every row has k
+    # interactions of weight 1 at any beta, so n_eff = k (text after eq. neff)
+    rng = np.random.default_rng(k)
+    centres = rng.normal(size=(40, 3)) * 100.0
+    X = np.repeat(centres, k + 1, axis=0)
+    N = X.shape[0]
+    s1 = on.normalise(X, 0.5, 0.5).s_off
+    s2 = on.normalise(X, 1.0, 0.5).s_off
+    assert s1 == pytest.approx(N * k, rel=1e-12)
+    assert bf.n_eff(s1, s2, N) == pytest.approx(k, rel=1e-12)
+
+
+def test_v_stat_definition():
+    assert bf.v_stat(25.0, 4.0) == pytest.approx(0.1, rel=1e-15)
+
+
+@pytest.mark.parametrize("counts,d", [((256, 256), 2), ((64, 64, 64), 3)])
+def test_d_hat_recovers_grid_dimension(counts, d):
+    # flat grid torus, kernel wider than the spacing and narrower than the
+    # circles: S_off ~ beta^(-d/2), so d_hat ~ d (eq. dhat)
+    N = int(np.prod(counts))
+    beta = 20.0 if d == 2 else 8.0
+    s1 = N * (tg.degree(counts, beta) - 1.0)
+    s2 = N * (tg.degree(counts, 2 * beta) - 1.0)
+    assert bf.d_hat(s1, s2, beta, 2 * beta) == pytest.approx(d, rel=0.05)
+
+
+def test_parabola_vertex_exact():
+    x = [0.0, 0.5, 1.2]
+    y = [3 * (v - 0.7) ** 2 + 1 for v in x]
+    assert bf.parabola_vertex(x, y) == pytest.approx(0.7, rel=1e-12)
+
+
+def _mock(vb, soff, gaps, beta0=0.1):
+    """Probe callable from per-probe V_bias, S_off and Perron gaps (index by
+    the dyadic step; the vertex probe reuses the nearest step's values)."""
+    def probe(beta):
+        i = int(round(math.log2(beta / beta0)))
+        i = max(0, min(i, len(vb) - 1))
+        # evals with lambda_0 = 1, lambda_1 = 1 - gap and median -log = vb
+        ev = np.array([1.0, 1.0 - gaps[i], math.exp(-vb[i]), math.exp(-vb[i])])
+        return bf.make_probe(beta, ev, soff[i])
+    return probe
+
+
+def test_flow_brackets_known_minimum():
+    N = 1000
+    vb = [4.0, 2.0, 1.0, 0.5, 0.25, 0.12, 0.06]
+    # S_off halving per step until step 3, then falling faster: V_stat grows
+    soff = [N * 400 / 2 ** i for i in range(4)] + [N * 400 / 2 ** 3 / 8 ** j for j in range(1, 4)]
+    gaps = [0.5] * 7
+    F = bf.flow(_mock(vb, soff, gaps), N, 0.1, max_probes=7)
+    assert F.reason == "bracket"
+    Vs = [p.v_total for p in F.probes if p.v_total is not None]
+    m = int(np.argmin(Vs))
+    assert F.bracket == m
+    lo, hi = F.probes[m - 1].beta, F.probes[m + 1].beta
+    assert lo <= F.beta_x <= hi
+
+
+def test_flow_stops_at_the_wall():
+    N = 1000
+    vb = [4.0, 2.0, 1.0, 0.5, 0.25, 0.12]
+    soff = [N * 400 / 2 ** i for i in range(6)]
+    gaps = [0.5, 0.2, 1e-3, 2e-5, 1e-7, 1e-8]  # step 4 is past kappa * eta = 1e-6
+    F = bf.flow(_mock(vb, soff, gaps), N, 0.1, max_probes=6)
+    assert F.reason == "wall"
+    assert len(F.probes) == 4
+    assert F.beta_x == pytest.approx(0.1 * 2 ** 3)
+
+
+def test_flow_budget_takes_smallest_complete_potential():
+    N = 1000
+    vb = [4.0, 2.0, 1.0, 0.5]
+    soff = [N * 400 / 2 ** i for i in range(4)]
+    F = bf.flow(_mock(vb, soff, [0.5] * 4), N, 0.1, max_probes=4)
+    assert F.reason == "budget"
+    done = [p for p in F.probes if p.v_total is not None]
+    assert F.final is min(done, key=lambda p: p.v_total)
+
+
+def test_flow_on_two_torus_heat_regime():
+    # 2048 points of the flat 2-torus, alpha = 1/2, 16 pairs: V_bias ~ 1/beta
+    # and d_hat -> 2 in the heat regime; the sweep brackets a minimum
+    from paper_2609_38198_amd import inputs
+    w = inputs.torus2()
+    F = bf.flow(bf.dense_probe(w.X, 0.5, 16), w.N, bf.beta0(w.X), max_probes=12)
+    assert F.reason == "bracket"
+    heat = [p for p in F.probes if p.v_total is not None and p.beta >= 3.0]
+    assert heat
+    for p in heat:
+        assert p.d_hat == pytest.approx(2.0, rel=0.1)
+    for a, c in zip(heat, heat[1:]):
+        assert a.v_bias / c.v_bias == pytest.approx(2.0, rel=0.15)
