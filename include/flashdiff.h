@@ -57,7 +57,8 @@ typedef enum fd_op {
   FD_OP_KERNEL_MATMUL = 0,
   FD_OP_DEGREE = 1,
   FD_OP_BLOCK_LANCZOS = 2,
-  FD_OP_CONTINUATION = 3
+  FD_OP_CONTINUATION = 3,
+  FD_OP_BETA_FLOW = 4
 } fd_op;
 
 /* Options of the block Lanczos eigensolver (Sec. 2.3, first paragraph: block
@@ -93,6 +94,7 @@ void fd_lanczos_default_opts(fd_lanczos_opts* opts);
  *   op = FD_OP_KERNEL_MATMUL: Nr output rows, Nc columns, D, b; k ignored.
  *   op = FD_OP_DEGREE:        Nr = Nc = N, D; b, k ignored.
  *   op = FD_OP_BLOCK_LANCZOS: Nr = Nc = N, D, b, k, opts (NULL = defaults).
+ *   op = FD_OP_BETA_FLOW:     Nr = Nc = N, D, b, k, opts (NULL = defaults).
  *   op = FD_OP_CONTINUATION:  Nr = largest n of the schedule, Nc = number of steps,
  *                             D, b, k (<= 64), opts.
  * Returns 0 for arguments the entry point would reject. */
@@ -177,6 +179,68 @@ fd_status fd_continuation(const void* X, fd_dtype xt, int64_t N, int64_t D, int6
                           float* evecs, float* psi, fd_lanczos_info* per_step,
                           int32_t stop_at_wall, int64_t* steps_done, void* ws, size_t ws_bytes,
                           void* stream);
+
+/* ---- bandwidth selection by the beta-function flow (Sec. 2.3) ----
+ *
+ * Dyadic probes beta_0, 2 beta_0, 4 beta_0, ... on all N points.  Each probe
+ * runs the normalisation and the top-k eigensolve of M (k includes the Perron
+ * pair), warm-started from the previous probe's Markov eigenvectors, and
+ * records
+ *   S_off = sum_{i != j} K_ij,  g_P = (lambda_0 - lambda_1) / |lambda_0|,
+ *   V_bias = median_j -log(lambda_j / lambda_0) over the k - 1 nontrivial pairs (eq. vbias),
+ *   V_mach = (kappa_P eta / g_P)^p (eq. vmach),
+ * and, once the next dyadic probe has run,
+ *   n_eff = S_off(beta)^2 / (N S_off(2 beta)) (eq. neff),  V_stat = (n_eff V_bias)^-1/2 (eq. vstat),
+ *   V = V_bias + V_stat + V_mach (eq. vtotal),  d_hat = -2 dlog S_off / dlog beta (eq. dhat).
+ * A probe with g_P <= kappa_P eta (eq. perronwall) ends the sweep; the last
+ * admissible probe is then the achieved bandwidth.  When three consecutive
+ * complete probes have V falling then rising, with V_bias falling and V_stat
+ * or V_mach rising between the outer two, a quadratic in log beta through the
+ * three gives a vertex, which one more probe resolves (if that probe is past
+ * the wall, the middle probe is taken).  When max_probes run out first, the
+ * complete probe with the smallest V is taken.  beta_0 defaults to
+ * min(0.1, 1 / (2 mean_i ||x_i - mean||^2)) from the centred data (eq. beta0). */
+typedef struct fd_flow_opts {
+  double beta_start;   /* <= 0: beta_0 of eq. beta0 */
+  double eta;          /* precision scale of the kernel data; <= 0: by dtype (fp32 1e-7, bf16 8e-3) */
+  double kappa;        /* kappa_P, default 10 */
+  double p;            /* barrier exponent, default 6 */
+  int32_t max_probes;  /* dyadic probes at most, default 24 (1..64) */
+  int32_t reserved;
+} fd_flow_opts;
+
+typedef struct fd_flow_probe {
+  double beta, s_off, gap_perron, v_bias, v_mach;
+  double n_eff, v_stat, v_total, d_hat;  /* NaN until the next dyadic probe ran */
+  double seconds;
+  int32_t role;        /* 0 dyadic probe, 1 vertex probe, 2 solve at the selected bandwidth */
+  int32_t admissible;  /* g_P > kappa_P eta */
+  int32_t status;      /* status of the probe's eigensolve (FD_OK or FD_ERR_NOT_CONVERGED) */
+  int32_t block_matvecs, nconv, reserved;
+} fd_flow_probe;
+
+typedef enum fd_flow_exit { FD_FLOW_BRACKET = 0, FD_FLOW_WALL = 1, FD_FLOW_BUDGET = 2 } fd_flow_exit;
+
+void fd_flow_default_opts(fd_flow_opts* o);
+
+/* Runs the flow and returns the eigenpairs at the achieved bandwidth.
+ *   X: N x D (device, dtype xt, ldx).  0 <= alpha <= 1, 1 <= b <= 64, 2 <= k <= N.
+ *   fopts, opts: NULL = defaults.
+ *   probes: host array of at least max_probes + 2 records; *nprobes (host) receives
+ *     how many were written: the dyadic probes in order (a probe past the wall
+ *     included), then the vertex probe and the solve at the selected bandwidth,
+ *     each if it ran.
+ *   beta_x (host): achieved bandwidth.  exit_reason (host): an fd_flow_exit.
+ *   evals (host, k), evecs (device, N x k, ld k), psi (device or NULL): the
+ *     eigenpairs at beta_x as in fd_block_lanczos.
+ * Returns FD_ERR_NOT_CONVERGED (outputs valid) when the solve at beta_x stopped
+ * before k pairs converged, FD_ERR_PERRON_WALL (records valid, nothing else)
+ * when already the first probe is past the wall. */
+fd_status fd_beta_flow(const void* X, fd_dtype xt, int64_t N, int64_t D, int64_t ldx, float alpha,
+                       int64_t b, int64_t k, const fd_flow_opts* fopts,
+                       const fd_lanczos_opts* opts, fd_flow_probe* probes, int64_t* nprobes,
+                       double* beta_x, int32_t* exit_reason, double* evals, float* evecs,
+                       float* psi, void* ws, size_t ws_bytes, void* stream);
 
 /* ---- diagnostics: kernel timing with HIP events ----
  * When enabled, every launch of the fused product kernel (FD_KERNEL_PRODUCT)

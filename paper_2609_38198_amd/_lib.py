@@ -28,11 +28,13 @@ STATUS = {
 }
 FD_F32, FD_BF16 = 0, 1
 FD_OP_KERNEL_MATMUL, FD_OP_DEGREE, FD_OP_BLOCK_LANCZOS, FD_OP_CONTINUATION = 0, 1, 2, 3
+FD_OP_BETA_FLOW = 4
+FLOW_EXIT = {0: "bracket", 1: "wall", 2: "budget"}
 
 EXPORTS = (
     "fd_lanczos_default_opts", "fd_workspace_size", "fd_kernel_matmul", "fd_degree",
     "fd_block_lanczos", "fd_continuation", "fd_last_error", "fd_status_string",
-    "fd_profile_enable", "fd_profile_read",
+    "fd_profile_enable", "fd_profile_read", "fd_flow_default_opts", "fd_beta_flow",
 )
 FD_KERNEL_PRODUCT, FD_KERNEL_ROWSUM = 0, 1
 
@@ -59,6 +61,26 @@ class LanczosInfo(ctypes.Structure):
 
     def as_dict(self) -> dict:
         return {f: getattr(self, f) for f, _ in self._fields_}
+
+
+class FlowOpts(ctypes.Structure):
+    _fields_ = [("beta_start", ctypes.c_double), ("eta", ctypes.c_double),
+                ("kappa", ctypes.c_double), ("p", ctypes.c_double),
+                ("max_probes", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+class FlowProbe(ctypes.Structure):
+    _fields_ = [("beta", ctypes.c_double), ("s_off", ctypes.c_double),
+                ("gap_perron", ctypes.c_double), ("v_bias", ctypes.c_double),
+                ("v_mach", ctypes.c_double), ("n_eff", ctypes.c_double),
+                ("v_stat", ctypes.c_double), ("v_total", ctypes.c_double),
+                ("d_hat", ctypes.c_double), ("seconds", ctypes.c_double),
+                ("role", ctypes.c_int32), ("admissible", ctypes.c_int32),
+                ("status", ctypes.c_int32), ("block_matvecs", ctypes.c_int32),
+                ("nconv", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+    def as_dict(self) -> dict:
+        return {f: getattr(self, f) for f, _ in self._fields_ if f != "reserved"}
 
 
 _c_i64 = ctypes.c_int64
@@ -97,6 +119,14 @@ def load(path: str = LIB_PATH):
         _c_i64, _c_p, _c_i64, _c_i64, ctypes.POINTER(LanczosOpts), _c_p, _c_p, _c_p,
         ctypes.POINTER(LanczosInfo), ctypes.c_int32, _c_p, _c_p, ctypes.c_size_t, _c_p]
     lib.fd_continuation.restype = ctypes.c_int
+    lib.fd_flow_default_opts.argtypes = [ctypes.POINTER(FlowOpts)]
+    lib.fd_flow_default_opts.restype = None
+    lib.fd_beta_flow.argtypes = [
+        _c_p, ctypes.c_int, _c_i64, _c_i64, _c_i64, ctypes.c_float, _c_i64, _c_i64,
+        ctypes.POINTER(FlowOpts), ctypes.POINTER(LanczosOpts), ctypes.POINTER(FlowProbe),
+        ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_double),
+        ctypes.POINTER(ctypes.c_int32), _c_p, _c_p, _c_p, _c_p, ctypes.c_size_t, _c_p]
+    lib.fd_beta_flow.restype = ctypes.c_int
     lib.fd_last_error.argtypes = []
     lib.fd_last_error.restype = ctypes.c_char_p
     lib.fd_status_string.argtypes = [ctypes.c_int]
@@ -329,3 +359,55 @@ def fd_continuation(X: torch.Tensor, n_steps: Sequence[int], beta_steps: Sequenc
                 allow)
     ev = [[evals[t * k + i] for i in range(k)] for t in range(T)]
     return Ladder(ev, evecs, psi, [infos[t].as_dict() for t in range(T)], done.value, st)
+
+
+def flow_default_opts(**kw) -> FlowOpts:
+    o = FlowOpts()
+    load().fd_flow_default_opts(ctypes.byref(o))
+    for key, v in kw.items():
+        setattr(o, key, v)
+    return o
+
+
+@dataclass
+class Flow:
+    probes: list       # per-probe records (dicts), in the order run
+    beta_x: float      # achieved bandwidth
+    reason: str        # "bracket", "wall" or "budget"
+    evals: list
+    evecs: torch.Tensor
+    psi: Optional[torch.Tensor]
+    status: int
+
+
+def fd_beta_flow(X: torch.Tensor, k: int, b: int, alpha: float = 0.5,
+                 fopts: Optional[FlowOpts] = None, opts: Optional[LanczosOpts] = None,
+                 want_psi: bool = True, ws: Optional[torch.Tensor] = None,
+                 allow=(FD_OK,)) -> Flow:
+    """Bandwidth selection by the beta-function flow; eigenpairs at beta_x."""
+    lib = load()
+    _check_dev(X)
+    N, D = X.shape
+    dev = X.device
+    fo = fopts if fopts is not None else flow_default_opts()
+    o = opts if opts is not None else default_opts()
+    cap = int(fo.max_probes) + 2
+    recs = (FlowProbe * cap)()
+    nrec = ctypes.c_int64(0)
+    bx = ctypes.c_double(0.0)
+    why = ctypes.c_int32(0)
+    evals = (ctypes.c_double * k)()
+    evecs = torch.empty((N, k), dtype=torch.float32, device=dev)
+    psi = torch.empty((N, k), dtype=torch.float32, device=dev) if want_psi else None
+    need = fd_workspace_size(FD_OP_BETA_FLOW, N, N, D, b, k, o)
+    if need == 0:
+        raise FdError(1, "unsupported sizes")
+    if ws is None or ws.numel() < need:
+        ws = _workspace(need, dev)
+    st = _check(lib.fd_beta_flow(_ptr(X), _dtype_code(X), N, D, X.stride(0), float(alpha), b, k,
+                                 ctypes.byref(fo), ctypes.byref(o), recs, ctypes.byref(nrec),
+                                 ctypes.byref(bx), ctypes.byref(why), evals, _ptr(evecs),
+                                 _ptr(psi), _ptr(ws), ws.numel(), _stream(dev)), allow)
+    return Flow([recs[i].as_dict() for i in range(nrec.value)], bx.value,
+                FLOW_EXIT.get(why.value, str(why.value)), [evals[i] for i in range(k)], evecs,
+                psi, st)

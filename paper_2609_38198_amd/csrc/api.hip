@@ -202,6 +202,14 @@ size_t fd_workspace_size(fd_op op, int64_t Nr, int64_t Nc, int64_t D, int64_t b,
         carve_continuation_ws(a, Nr, Nc, D, int(b), int(k), o);
         break;
       }
+      case FD_OP_BETA_FLOW: {
+        fd_lanczos_opts o;
+        fd_lanczos_default_opts(&o);
+        if (opts != nullptr) o = *opts;
+        FD_REQUIRE(b >= 1 && b <= MAX_B && k >= 2 && k <= Nr, FD_ERR_INVALID_ARG, "size");
+        carve_flow_ws(a, Nr, D, int(b), int(k), o);
+        break;
+      }
       default:
         throw Error{FD_ERR_INVALID_ARG, "unknown op"};
     }

@@ -49,5 +49,6 @@ ProductWs product_view(const ProductWs& big, const PointPack& rows, const PointP
 void carve_solver(Arena& a, int64_t N, int64_t D, int b, int k, const fd_lanczos_opts& o);
 void carve_continuation_ws(Arena& a, int64_t nmax, int64_t nsteps, int64_t D, int b, int k,
                            const fd_lanczos_opts& o);
+void carve_flow_ws(Arena& a, int64_t N, int64_t D, int b, int k, const fd_lanczos_opts& o);
 
 }  // namespace fd

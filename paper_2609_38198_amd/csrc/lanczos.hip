@@ -410,6 +410,213 @@ void carve_continuation_ws(Arena& a, int64_t nmax, int64_t nsteps, int64_t D, in
   carve_continuation(a, nmax, nsteps, D, b, k, o);
 }
 
+// ----------------------------------------------------------------- bandwidth flow
+//
+// Sec. 2.3 ("beta-function flow"): dyadic probes from beta_0, the empirical
+// potential V = V_bias + V_stat + V_mach over log beta, the bracketing rule
+// with a quadratic vertex probe, and the Perron wall.
+
+struct FlowWs {
+  SolverWs sw;
+  float* psi_keep = nullptr;  // N x k: Markov vectors of the latest admissible probe
+  float* psi_new = nullptr;   // N x k: Markov vectors of the probe being solved
+  double* stats = nullptr;    // centring: nblk x (D + 1) partials, D means, 1 total
+  int nblk = 0;
+};
+
+static int flow_stat_blocks(int64_t N) {
+  return int(std::min<int64_t>(256, std::max<int64_t>(1, (N + 4095) / 4096)));
+}
+
+static FlowWs carve_flow(Arena& a, int64_t N, int64_t D, int b, int k, const fd_lanczos_opts& o) {
+  FlowWs f;
+  const SolverLayout L = solver_layout(N, b, k, o);
+  f.sw = carve_solver_ws(a, N, D, b, L.mm, b);
+  f.psi_keep = a.take<float>(size_t(N) * k);
+  f.psi_new = a.take<float>(size_t(N) * k);
+  f.nblk = flow_stat_blocks(N);
+  f.stats = a.take<double>(size_t(f.nblk) * (D + 1) + size_t(D) + 1);
+  return f;
+}
+
+void carve_flow_ws(Arena& a, int64_t N, int64_t D, int b, int k, const fd_lanczos_opts& o) {
+  carve_flow(a, N, D, b, k, o);
+}
+
+__device__ __forceinline__ double x_at(const float* X, int64_t i) { return double(X[i]); }
+__device__ __forceinline__ double x_at(const uint16_t* X, int64_t i) {
+  return double(__uint_as_float(uint32_t(X[i]) << 16));
+}
+
+// Block partials over rows [blk rpb, (blk + 1) rpb), fixed order: the column
+// sums (mu == NULL) or sum_i ||x_i - mu||^2 (mu given, into slot D).
+template <typename T>
+__global__ __launch_bounds__(256) void centre_partial_kernel(const T* __restrict__ X, int64_t N,
+                                                             int D, int64_t ldx,
+                                                             const double* __restrict__ mu,
+                                                             int64_t rpb,
+                                                             double* __restrict__ part) {
+  __shared__ double red[256];
+  const int t = threadIdx.x;
+  const int64_t r0 = int64_t(blockIdx.x) * rpb;
+  const int64_t r1 = min(N, r0 + rpb);
+  const int nout = mu == nullptr ? D : 1;
+  for (int k = 0; k < nout; ++k) {
+    double acc = 0.0;
+    for (int64_t i = r0 + t; i < r1; i += 256) {
+      if (mu == nullptr) {
+        acc += x_at(X, i * ldx + k);
+      } else {
+        double r = 0.0;
+        for (int f = 0; f < D; ++f) {
+          const double v = x_at(X, i * ldx + f) - mu[f];
+          r += v * v;
+        }
+        acc += r;
+      }
+    }
+    red[t] = acc;
+    __syncthreads();
+    for (int w = 128; w > 0; w >>= 1) {
+      if (t < w) red[t] += red[t + w];
+      __syncthreads();
+    }
+    if (t == 0) part[int64_t(blockIdx.x) * (D + 1) + (mu == nullptr ? k : D)] = red[0];
+    __syncthreads();
+  }
+}
+
+// out[c] = (sum over blocks of part[., slot0 + c]) / N, c < nc, blocks in order
+__global__ void centre_finish_kernel(const double* __restrict__ part, int nblk, int D, int slot0,
+                                     int nc, int64_t N, double* __restrict__ out) {
+  const int c = threadIdx.x;
+  if (c >= nc) return;
+  double acc = 0.0;
+  for (int b = 0; b < nblk; ++b) acc += part[int64_t(b) * (D + 1) + slot0 + c];
+  out[c] = acc / double(N);
+}
+
+// mean_i ||x_i - mean||^2 in float64, two passes (means, then deviations).
+template <typename T>
+static double centred_mean_sq(FlowWs& f, const T* X, int64_t N, int64_t D, int64_t ldx,
+                              hipStream_t st) {
+  const int64_t rpb = (N + f.nblk - 1) / f.nblk;
+  double* part = f.stats;
+  double* mu = f.stats + size_t(f.nblk) * (D + 1);
+  double* tot = mu + D;
+  hipLaunchKernelGGL((centre_partial_kernel<T>), dim3(f.nblk), dim3(256), 0, st, X, N, int(D),
+                     ldx, nullptr, rpb, part);
+  FD_LAUNCH_CHECK();
+  hipLaunchKernelGGL(centre_finish_kernel, dim3(1), dim3(64), 0, st, part, f.nblk, int(D), 0,
+                     int(D), N, mu);
+  FD_LAUNCH_CHECK();
+  hipLaunchKernelGGL((centre_partial_kernel<T>), dim3(f.nblk), dim3(256), 0, st, X, N, int(D),
+                     ldx, mu, rpb, part);
+  FD_LAUNCH_CHECK();
+  hipLaunchKernelGGL(centre_finish_kernel, dim3(1), dim3(64), 0, st, part, f.nblk, int(D),
+                     int(D), 1, N, tot);
+  FD_LAUNCH_CHECK();
+  double ms = 0.0;
+  FD_HIP_CHECK(hipMemcpyAsync(&ms, tot, sizeof(double), hipMemcpyDeviceToHost, st));
+  FD_HIP_CHECK(hipStreamSynchronize(st));
+  return ms;
+}
+
+struct FlowParams {
+  double eta, kappa, p;
+};
+
+struct FlowProbe {
+  double beta = 0.0, s_off = 0.0, gap = 0.0, v_bias = 0.0, v_mach = 0.0;
+  double n_eff = NAN, v_stat = NAN, v_total = NAN, d_hat = NAN, seconds = 0.0;
+  bool admissible = false, converged = false;
+  int role = 0, matvecs = 0, nconv = 0;
+  std::vector<double> evals;
+  bool complete() const { return !std::isnan(v_total); }
+};
+
+// One probe: normalisation and top-k eigensolve at beta (warm: Markov vectors
+// N x k or NULL); the Ritz vectors stay in sw.Q, psi goes to psi_out.
+static FlowProbe flow_probe(FlowWs& f, const void* X, fd_dtype xt, int64_t N, int64_t D,
+                            int64_t ldx, double beta, double alpha, int b, int k,
+                            const float* warm, float* psi_out, const fd_lanczos_opts& o,
+                            const FlowParams& fp, int role, uint64_t seed_offset,
+                            hipStream_t st) {
+  const auto t0 = std::chrono::steady_clock::now();
+  FlowProbe pr;
+  pr.beta = beta;
+  pr.role = role;
+  degree_run(f.sw.deg, X, xt, N, D, ldx, beta, alpha, nullptr, f.sw.d, f.sw.s, f.sw.s_off, true,
+             st);
+  const SolverLayout lay = solver_layout(N, b, k, o);
+  Lanczos L(f.sw, product_view(f.sw.prod, f.sw.deg.rows, f.sw.deg.cols, b), st, N, b, lay.mm,
+            o.seed + seed_offset);
+  SolveResult R = lanczos_solve(f.sw, L, lay, k, warm, warm ? k : 0, k, 0.5, o);
+  copy_cols(f.sw.Q, lay.mm, psi_out, k, N, k, f.sw.d, -0.5, st);
+  FD_HIP_CHECK(hipMemcpyAsync(&pr.s_off, f.sw.s_off, sizeof(double), hipMemcpyDeviceToHost, st));
+  FD_HIP_CHECK(hipStreamSynchronize(st));
+  pr.evals = R.theta;
+  pr.evals.resize(k, 0.0);
+  pr.converged = R.converged;
+  pr.matvecs = R.matvecs;
+  pr.nconv = R.nconv;
+  const double l0 = pr.evals[0];
+  pr.gap = (l0 - pr.evals[1]) / std::fabs(l0);
+  std::vector<double> h;
+  for (int j = 1; j < k; ++j) h.push_back(-std::log(pr.evals[j] / l0));
+  std::sort(h.begin(), h.end());
+  const size_t n = h.size();
+  pr.v_bias = (n % 2 == 1) ? h[n / 2] : 0.5 * (h[n / 2 - 1] + h[n / 2]);
+  pr.v_mach = pr.gap > 0.0 ? std::pow(fp.kappa * fp.eta / pr.gap, fp.p) : INFINITY;
+  pr.admissible = pr.gap > fp.kappa * fp.eta;
+  pr.seconds = std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
+  return pr;
+}
+
+// Quantities of `a` that need S_off at twice its bandwidth (probe c).
+static void flow_complete(FlowProbe& a, const FlowProbe& c, int64_t N) {
+  a.n_eff = a.s_off * a.s_off / (double(N) * c.s_off);
+  a.v_stat = 1.0 / std::sqrt(a.n_eff * a.v_bias);
+  a.v_total = a.v_bias + a.v_stat + a.v_mach;
+  a.d_hat = -2.0 * (std::log(c.s_off) - std::log(a.s_off)) / (std::log(c.beta) - std::log(a.beta));
+}
+
+static bool flow_brackets(const FlowProbe& a, const FlowProbe& m, const FlowProbe& c) {
+  return a.v_total > m.v_total && c.v_total > m.v_total && c.v_bias < a.v_bias &&
+         (c.v_stat > a.v_stat || c.v_mach > a.v_mach);
+}
+
+// Vertex abscissa of the parabola through (x_i, y_i), clamped to [x0, x2].
+static double flow_vertex(const double x[3], const double y[3]) {
+  const double den = (x[0] - x[1]) * (x[0] - x[2]) * (x[1] - x[2]);
+  const double A = (x[2] * (y[1] - y[0]) + x[1] * (y[0] - y[2]) + x[0] * (y[2] - y[1])) / den;
+  const double B =
+      (x[2] * x[2] * (y[0] - y[1]) + x[1] * x[1] * (y[2] - y[0]) + x[0] * x[0] * (y[1] - y[2])) /
+      den;
+  const double v = -B / (2.0 * A);
+  return std::min(std::max(v, x[0]), x[2]);
+}
+
+static fd_flow_probe flow_record(const FlowProbe& p) {
+  fd_flow_probe r{};
+  r.beta = p.beta;
+  r.s_off = p.s_off;
+  r.gap_perron = p.gap;
+  r.v_bias = p.v_bias;
+  r.v_mach = p.v_mach;
+  r.n_eff = p.n_eff;
+  r.v_stat = p.v_stat;
+  r.v_total = p.v_total;
+  r.d_hat = p.d_hat;
+  r.seconds = p.seconds;
+  r.role = p.role;
+  r.admissible = p.admissible ? 1 : 0;
+  r.status = p.converged ? FD_OK : FD_ERR_NOT_CONVERGED;
+  r.block_matvecs = p.matvecs;
+  r.nconv = p.nconv;
+  return r;
+}
+
 }  // namespace fd
 
 using namespace fd;
@@ -607,6 +814,171 @@ fd_status fd_continuation(const void* X, fd_dtype xt, int64_t N, int64_t D, int6
     }
     if (any_unconverged) {
       set_error("at least one step stopped before all k pairs converged");
+      return FD_ERR_NOT_CONVERGED;
+    }
+    set_error("");
+    return FD_OK;
+  } catch (const Error& e) {
+    set_error(e.msg);
+    return e.status;
+  } catch (const std::exception& e) {
+    set_error(std::string("internal error: ") + e.what());
+    return FD_ERR_HIP;
+  }
+}
+
+void fd_flow_default_opts(fd_flow_opts* o) {
+  if (o == nullptr) return;
+  *o = fd_flow_opts{};
+  o->beta_start = 0.0;
+  o->eta = 0.0;
+  o->kappa = 10.0;
+  o->p = 6.0;
+  o->max_probes = 24;
+}
+
+fd_status fd_beta_flow(const void* X, fd_dtype xt, int64_t N, int64_t D, int64_t ldx, float alpha,
+                       int64_t b, int64_t k, const fd_flow_opts* fopts,
+                       const fd_lanczos_opts* opts, fd_flow_probe* probes, int64_t* nprobes,
+                       double* beta_x, int32_t* exit_reason, double* evals, float* evecs,
+                       float* psi, void* ws, size_t ws_bytes, void* stream) {
+  try {
+    check_points(X, xt, N, D, ldx, "X");
+    FD_REQUIRE(alpha >= 0.f && alpha <= 1.f, FD_ERR_INVALID_ARG, "alpha must be in [0, 1]");
+    FD_REQUIRE(b >= 1 && b <= MAX_B, FD_ERR_INVALID_ARG, "b must be in [1, 64]");
+    FD_REQUIRE(k >= 2 && k <= N, FD_ERR_INVALID_ARG, "k must be in [2, N]");
+    FD_REQUIRE(probes != nullptr && nprobes != nullptr && beta_x != nullptr &&
+                   exit_reason != nullptr && evals != nullptr && evecs != nullptr,
+               FD_ERR_INVALID_ARG, "NULL output");
+    fd_flow_opts fo;
+    fd_flow_default_opts(&fo);
+    if (fopts != nullptr) fo = *fopts;
+    FD_REQUIRE(fo.max_probes >= 1 && fo.max_probes <= 64, FD_ERR_INVALID_ARG,
+               "max_probes must be in [1, 64]");
+    FD_REQUIRE(std::isfinite(fo.kappa) && fo.kappa > 0.0 && std::isfinite(fo.p) && fo.p > 0.0,
+               FD_ERR_INVALID_ARG, "kappa and p must be finite and > 0");
+    FD_REQUIRE(std::isfinite(fo.beta_start) && std::isfinite(fo.eta), FD_ERR_INVALID_ARG,
+               "beta_start and eta must be finite");
+    FlowParams fp{fo.eta > 0.0 ? fo.eta : (xt == FD_BF16 ? 8e-3 : 1e-7), fo.kappa, fo.p};
+    fd_lanczos_opts o;
+    fd_lanczos_default_opts(&o);
+    if (opts != nullptr) o = *opts;
+    validate_opts(o);
+    const SolverLayout lay = solver_layout(N, int(b), int(k), o);
+    FD_REQUIRE(lay.dense || k <= lay.kk, FD_ERR_INVALID_ARG, "k too large for the basis");
+    Arena m;
+    m.measuring = true;
+    carve_flow(m, N, D, int(b), int(k), o);
+    check_workspace(ws, ws_bytes, m.used);
+    Arena a;
+    a.base = static_cast<char*>(ws);
+    a.cap = ws_bytes;
+    FlowWs f = carve_flow(a, N, D, int(b), int(k), o);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const int kk = int(k), bb = int(b);
+
+    double beta = fo.beta_start;
+    if (beta <= 0.0) {
+      const double ms = xt == FD_BF16
+                            ? centred_mean_sq(f, static_cast<const uint16_t*>(X), N, D, ldx, st)
+                            : centred_mean_sq(f, static_cast<const float*>(X), N, D, ldx, st);
+      beta = ms > 0.0 ? std::min(0.1, 1.0 / (2.0 * ms)) : 0.1;
+    }
+    std::vector<FlowProbe> pr;       // admissible dyadic probes
+    std::vector<fd_flow_probe> out;  // records in the order run
+    bool have_keep = false;          // psi_keep holds the latest admissible probe
+    double in_q = -1.0;              // bandwidth whose Ritz vectors are in sw.Q
+    int reason = FD_FLOW_BUDGET;
+    FlowProbe fin;
+    bool fin_in_q = false;
+    for (int t = 0; t < fo.max_probes; ++t) {
+      FlowProbe p = flow_probe(f, X, xt, N, D, ldx, beta, alpha, bb, kk,
+                               have_keep ? f.psi_keep : nullptr, f.psi_new, o, fp, 0,
+                               uint64_t(t) * 7919u, st);
+      in_q = beta;
+      if (!p.admissible) {
+        out.push_back(flow_record(p));
+        reason = FD_FLOW_WALL;
+        break;
+      }
+      if (!pr.empty()) {
+        flow_complete(pr.back(), p, N);
+        out.back() = flow_record(pr.back());
+      }
+      pr.push_back(p);
+      out.push_back(flow_record(p));
+      std::swap(f.psi_keep, f.psi_new);
+      have_keep = true;
+      std::vector<int> done;
+      for (int i = 0; i < int(pr.size()); ++i)
+        if (pr[i].complete()) done.push_back(i);
+      const int nd = int(done.size());
+      if (nd >= 3 && flow_brackets(pr[done[nd - 3]], pr[done[nd - 2]], pr[done[nd - 1]])) {
+        const FlowProbe& pa = pr[done[nd - 3]];
+        const FlowProbe& pm = pr[done[nd - 2]];
+        const FlowProbe& pc = pr[done[nd - 1]];
+        const double xs[3] = {std::log(pa.beta), std::log(pm.beta), std::log(pc.beta)};
+        const double ys[3] = {pa.v_total, pm.v_total, pc.v_total};
+        const double bv = std::exp(flow_vertex(xs, ys));
+        FlowProbe v = flow_probe(f, X, xt, N, D, ldx, bv, alpha, bb, kk, f.psi_keep, f.psi_new,
+                                 o, fp, 1, 104729u, st);
+        in_q = bv;
+        out.push_back(flow_record(v));
+        reason = FD_FLOW_BRACKET;
+        if (v.admissible) {
+          fin = v;
+          fin_in_q = true;
+        } else {
+          fin = pm;
+        }
+        break;
+      }
+      beta *= 2.0;
+    }
+    if (pr.empty()) {
+      // the first probe is already past the wall: nothing admissible to return
+      for (size_t i = 0; i < out.size(); ++i) probes[i] = out[i];
+      *nprobes = int64_t(out.size());
+      *beta_x = NAN;
+      *exit_reason = FD_FLOW_WALL;
+      set_error("the first probe is already past the Perron wall (g_P <= kappa_P eta)");
+      return FD_ERR_PERRON_WALL;
+    }
+    if (reason != FD_FLOW_BRACKET) {
+      fin = pr.back();
+      if (reason == FD_FLOW_BUDGET) {
+        for (const FlowProbe& q : pr)
+          if (q.complete() && (!fin.complete() || q.v_total < fin.v_total)) fin = q;
+      }
+      fin_in_q = in_q == fin.beta;
+    }
+    if (!fin_in_q) {
+      // the selected probe's vectors were overwritten: solve again from the
+      // latest admissible probe's Markov vectors
+      FlowProbe r = flow_probe(f, X, xt, N, D, ldx, fin.beta, alpha, bb, kk, f.psi_keep,
+                               f.psi_new, o, fp, 2, 15485863u, st);
+      out.push_back(flow_record(r));
+      fin.evals = r.evals;
+      fin.converged = r.converged;
+      fin.nconv = r.nconv;
+      std::swap(f.psi_keep, f.psi_new);
+    } else if (fin.role == 0) {
+      // the latest dyadic probe: its Markov vectors were moved to psi_keep
+    } else {
+      std::swap(f.psi_keep, f.psi_new);
+    }
+    // the selected solve's eigenvectors are in sw.Q, its Markov vectors in psi_keep
+    const SolverLayout lz = solver_layout(N, bb, kk, o);
+    copy_cols(f.sw.Q, lz.mm, evecs, kk, N, kk, nullptr, 0.0, st);
+    if (psi != nullptr) copy_cols(f.psi_keep, kk, psi, kk, N, kk, nullptr, 0.0, st);
+    FD_HIP_CHECK(hipStreamSynchronize(st));
+    for (int i = 0; i < kk; ++i) evals[i] = fin.evals[i];
+    for (size_t i = 0; i < out.size(); ++i) probes[i] = out[i];
+    *nprobes = int64_t(out.size());
+    *beta_x = fin.beta;
+    *exit_reason = reason;
+    if (!fin.converged) {
+      set_error("the eigensolve at the selected bandwidth stopped before all k pairs converged");
       return FD_ERR_NOT_CONVERGED;
     }
     set_error("");

@@ -73,3 +73,50 @@ def test_host_validation_without_gpu():
     assert lib.fd_degree(fake, 0, 10, 4, 4, 1.0, 1.5, None, None, None, None, None, 0, None) == 1
     assert lib.fd_degree(fake, 0, 10, 4, 4, 0.0, 0.5, None, None, None, None, None, 0, None) == 1
     assert b"alpha" in lib.fd_last_error() or b"beta" in lib.fd_last_error()
+
+
+def test_struct_layouts_match_the_header(tmp_path):
+    # the ctypes mirrors of the ABI structs against a C compiler's view of the header
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    structs = {"fd_lanczos_opts": fd.LanczosOpts, "fd_lanczos_info": fd.LanczosInfo,
+               "fd_flow_opts": fd.FlowOpts, "fd_flow_probe": fd.FlowProbe}
+    lines = ["#include <stdio.h>", "#include <stddef.h>", '#include "flashdiff.h"', "int main(void) {"]
+    for name, cls in structs.items():
+        lines.append(f'printf("{name} size %zu\\n", sizeof({name}));')
+        for field, _ in cls._fields_:
+            lines.append(f'printf("{name} {field} %zu\\n", offsetof({name}, {field}));')
+    lines += ["return 0;", "}"]
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "layout"
+    subprocess.run([cc, "-std=c11", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)],
+                   check=True)
+    out = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split("\n")
+    got = {tuple(l.split()[:2]): int(l.split()[2]) for l in out if l.strip()}
+    for name, cls in structs.items():
+        assert got[(name, "size")] == ctypes.sizeof(cls), name
+        for field, _ in cls._fields_:
+            assert got[(name, field)] == getattr(cls, field).offset, (name, field)
+
+
+def test_flow_workspace_and_validation_without_gpu():
+    assert fd.fd_workspace_size(fd.FD_OP_BETA_FLOW, 2048, 2048, 4, 8, 16) > 0
+    assert fd.fd_workspace_size(fd.FD_OP_BETA_FLOW, 2048, 2048, 4, 8, 1) == 0   # k < 2
+    lib = fd.load()
+    fake = ctypes.c_void_p(256)
+    o = fd.flow_default_opts()
+    assert o.kappa == 10.0 and o.p == 6.0 and o.max_probes == 24
+    recs = (fd.FlowProbe * 26)()
+    n, bx, why = ctypes.c_int64(), ctypes.c_double(), ctypes.c_int32()
+    ev = (ctypes.c_double * 16)()
+    args = lambda k, fo: (fake, 0, 2048, 4, 4, 0.5, 8, k, ctypes.byref(fo), None, recs,
+                          ctypes.byref(n), ctypes.byref(bx), ctypes.byref(why), ev, fake, None,
+                          None, 0, None)
+    assert lib.fd_beta_flow(*args(1, o)) == 1  # k < 2
+    bad = fd.flow_default_opts(max_probes=0)
+    assert lib.fd_beta_flow(*args(16, bad)) == 1
+    assert lib.fd_beta_flow(*args(16, o)) == 3  # no workspace

@@ -1,0 +1,110 @@
+"""Parity of fd_beta_flow (Sec. 2.3 beta-function flow) with the oracle's flow.
+
+The oracle runs the same selection rules on dense float64 probes (LAPACK
+spectra, exact S_off); the library on its own normalisation passes and block
+Lanczos.  Compared per dyadic probe: bandwidth, S_off, Perron gap, V_bias,
+n_eff, V_stat, V, d_hat; then the exit, the bracket and the achieved
+bandwidth, and the eigenvalues returned there against a dense solve at the
+library's beta_x.  Tolerances are propagated from the eigenvalue (1e-5
+relative, 1e-6 floor) and normalisation (1e-5) bars through each formula;
+the vertex to 1e-3.
+"""
+import numpy as np
+import pytest
+
+from gpu_util import case, device, to_dev
+from oracle import beta_flow as bf
+from oracle import eig as oe
+from paper_2609_38198_amd import _lib as fd
+from paper_2609_38198_amd import inputs
+
+pytestmark = pytest.mark.gpu
+
+
+def dyadic(flow):
+    return [p for p in flow.probes if p["role"] == 0 and p["admissible"]]
+
+
+def compare_probes(gpu, ref):
+    # tolerances propagated from the parity bars of the inputs: eigenvalues to
+    # max(1e-5 |lambda|, 1e-6) (so -log(lambda_j / lambda_0) to about 1e-5 absolute
+    # and the gap to 1e-6 absolute), S_off to 1e-5 relative (n_eff to 1e-4)
+    assert len(gpu) == len(ref.probes)
+    for g, r in zip(gpu, ref.probes):
+        assert g["beta"] == pytest.approx(r.beta, rel=1e-12)
+        assert g["s_off"] == pytest.approx(r.s_off, rel=1e-5)
+        gap_tol = max(1e-4 * r.gap, 1e-6)
+        assert abs(g["gap_perron"] - r.gap) <= gap_tol
+        vb_tol = max(1e-4 * r.v_bias, 1e-5)
+        assert abs(g["v_bias"] - r.v_bias) <= vb_tol
+        vm_tol = r.v_mach * 6.0 * gap_tol / r.gap
+        assert abs(g["v_mach"] - r.v_mach) <= vm_tol + 1e-300
+        if r.v_total is None:
+            assert np.isnan(g["v_total"])
+            continue
+        assert g["n_eff"] == pytest.approx(r.n_eff, rel=1e-4)
+        vs_tol = r.v_stat * 0.5 * (1e-4 + vb_tol / r.v_bias)
+        assert abs(g["v_stat"] - r.v_stat) <= vs_tol
+        assert abs(g["v_total"] - r.v_total) <= vb_tol + vs_tol + vm_tol
+        assert g["d_hat"] == pytest.approx(r.d_hat, abs=1e-3)
+
+
+def test_two_torus_flow_brackets_like_the_oracle():
+    w = inputs.torus2()
+    k, b = 16, 8
+    case("beta flow torus2 N=2048 k=16 b=8")
+    got = fd.fd_beta_flow(to_dev(w.X, device()), k, b, alpha=0.5,
+                          fopts=fd.flow_default_opts(max_probes=12))
+    ref = bf.flow(bf.dense_probe(w.X, 0.5, k), w.N, bf.beta0(w.X), max_probes=12)
+    assert got.reason == ref.reason == "bracket"
+    compare_probes(dyadic(got), ref)
+    assert got.beta_x == pytest.approx(ref.beta_x, rel=1e-3)
+    sp = oe.spectrum(w.X, got.beta_x, 0.5, k)
+    tol = np.maximum(1e-5 * np.abs(sp.evals), 1e-6)
+    assert np.all(np.abs(np.asarray(got.evals) - sp.evals) <= tol)
+    # the returned Markov vectors belong to the returned eigenvalues
+    assert abs(got.evals[0] - 1.0) <= 1e-6
+
+
+def clustered_points(seed=3, groups=24, per=6):
+    # tight clusters far apart: the Perron gap closes once the kernel is
+    # narrower than the clusters' spread
+    rng = np.random.default_rng(seed)
+    centres = rng.normal(size=(groups, 3)) * 4.0
+    X = np.repeat(centres, per, axis=0) + rng.normal(size=(groups * per, 3)) * 0.3
+    return (X - X.mean(0)).astype(np.float32)
+
+
+def test_wall_ends_the_sweep_like_the_oracle():
+    X = clustered_points()
+    k, b = 4, 4
+    case("beta flow clustered N=144 wall")
+    fo = fd.flow_default_opts(beta_start=0.02, max_probes=16)
+    got = fd.fd_beta_flow(to_dev(X, device()), k, b, alpha=0.5, fopts=fo)
+    ref = bf.flow(bf.dense_probe(X, 0.5, k), X.shape[0], 0.02, max_probes=16)
+    assert ref.reason == "wall"
+    assert got.reason == "wall"
+    compare_probes(dyadic(got), ref)
+    assert got.beta_x == pytest.approx(ref.beta_x, rel=1e-12)
+    walls = [p for p in got.probes if p["role"] == 0 and not p["admissible"]]
+    assert len(walls) == 1 and walls[0]["gap_perron"] <= 1e-6
+
+
+def test_budget_exit_like_the_oracle():
+    w = inputs.torus2()
+    case("beta flow torus2 budget 3 probes")
+    got = fd.fd_beta_flow(to_dev(w.X, device()), 8, 8, alpha=0.5,
+                          fopts=fd.flow_default_opts(max_probes=3))
+    ref = bf.flow(bf.dense_probe(w.X, 0.5, 8), w.N, bf.beta0(w.X), max_probes=3)
+    assert got.reason == ref.reason == "budget"
+    compare_probes(dyadic(got), ref)
+    assert got.beta_x == pytest.approx(ref.beta_x, rel=1e-12)
+
+
+def test_first_probe_past_the_wall_reports_it():
+    X = clustered_points()
+    case("beta flow first probe past the wall")
+    fo = fd.flow_default_opts(beta_start=1e4, max_probes=4)
+    got = fd.fd_beta_flow(to_dev(X, device()), 4, 4, fopts=fo, allow=(0, 6))
+    assert got.status == 6 and got.reason == "wall"
+    assert len(got.probes) == 1 and not got.probes[0]["admissible"]
