@@ -1,5 +1,6 @@
 // C ABI entry points: argument validation, workspace carving and the
 // composition of the kernels into the operations declared in flashdiff.h.
+#include <algorithm>
 #include <cmath>
 #include <exception>
 #include <string>
@@ -114,7 +115,8 @@ DegreeWs carve_degree(Arena& a, int64_t N, int64_t D) {
   w.q = a.take<float>(size_t(N));
   w.t = a.take<float>(size_t(N));
   w.w = a.take<float>(size_t(N));
-  w.part = a.fspan(part_rows_bound(w.rows.npad));
+  w.part = a.fspan(std::max(part_rows_bound(w.rows.npad), sym_part_rows(w.rows.npad, SYM_NIB)));
+  w.colfix = a.take<unsigned long long>(size_t(w.rows.npad));
   return w;
 }
 
@@ -126,7 +128,7 @@ void degree_run(DegreeWs& w, const void* X, fd_dtype xt, int64_t N, int64_t D, i
     launch_pack_points(X, xt, N, D, ldx, beta, false, w.cols, stream);
   }
   float* qq = q != nullptr ? q : w.q;
-  launch_rowsum(w.plan, w.rows, w.cols, FSpan{}, true, qq, w.part, stream);
+  launch_rowsum(w.plan, w.rows, w.cols, FSpan{}, true, qq, w.part, stream, w.colfix);
   if (s_off != nullptr) launch_sum_minus_n(qq, N, s_off, stream);
   if (alpha == 0.0) {
     launch_degree_finish(qq, qq, N, 0.0, d, s, stream);
@@ -134,7 +136,7 @@ void degree_run(DegreeWs& w, const void* X, fd_dtype xt, int64_t N, int64_t D, i
   }
   launch_pow_neg(qq, N, alpha, w.w, stream);
   launch_pack_w(w.w, N, w.cols.npad, w.wp, stream);
-  launch_rowsum(w.plan, w.rows, w.cols, w.wp, true, w.t, w.part, stream);
+  launch_rowsum(w.plan, w.rows, w.cols, w.wp, true, w.t, w.part, stream, w.colfix);
   launch_degree_finish(qq, w.t, N, alpha, d, s, stream);
 }
 

@@ -135,9 +135,19 @@ void launch_pack_v_split(const float* V, int64_t n, int64_t b, int64_t ldv, cons
 void launch_product(const KVPlan& p, const PointPack& rows, const PointPack& cols, FSpan vp,
                     FSpan vscale, bool diag, const float* sl, float* Y, int64_t ldy, int b,
                     FSpan part, hipStream_t stream);
-// out = K w (wp.p == NULL: w = 1).
+// out = K w (wp.p == NULL: w = 1).  With colfix (npad 64-bit words of
+// scratch) and rows and columns the same float32 point set, the symmetric
+// kernel is used (weights must lie in [0, 1]).
 void launch_rowsum(const KVPlan& p, const PointPack& rows, const PointPack& cols, FSpan wp,
-                   bool diag, float* out, FSpan part, hipStream_t stream);
+                   bool diag, float* out, FSpan part, hipStream_t stream,
+                   unsigned long long* colfix = nullptr);
+KVPlan plan_rowsum_sym(int64_t N, int64_t npad, int dp, int nib);
+// Row tiles per wave of the symmetric row sums, and the fewest column splits
+// of their large-problem plans.
+constexpr int SYM_NIB = 8;
+constexpr int64_t SYM_MIN_SPLITS = 16;
+// Row slots of the partial sums of a symmetric row-sum plan with npad rows.
+size_t sym_part_rows(int64_t npad, int nib);
 void launch_degree_finish(const float* q, const float* t, int64_t n, double alpha, float* d,
                           float* s, hipStream_t stream);
 void launch_pow_neg(const float* q, int64_t n, double alpha, float* w, hipStream_t stream);

@@ -19,6 +19,7 @@ struct DegreeWs {
   float* q = nullptr;
   float* t = nullptr;
   float* w = nullptr;
+  unsigned long long* colfix = nullptr;  // npad words: column sums of the symmetric row sums
   KVPlan plan;
 };
 

@@ -21,10 +21,13 @@
 // early.  x' = s x and b' = b / s with s = 2^e, e ~ log2(2 beta log2 e) / 2,
 // keep both operands near the same magnitude; s cancels exactly in x' . b'.
 //
-// Why float16: on gfx950 the float16 matrix instructions run concurrently with
-// vector-ALU work of the same wave (the transcendental exp2 and the K split),
-// while the float32 matrix instruction shares the vector datapath.  Moving the
-// contraction to float16 pieces lets it hide under the exponentials.
+// Why float16: on gfx950 a v_mfma_f32_16x16x32_f16 (32 slots) issues every 16
+// cycles per SIMD, a v_mfma_f32_16x16x4_f32 (4 slots) every 32.  Measured on
+// the device, a matrix instruction holds off ordinary vector instructions of
+// the SIMD for most of its duration (the exponentials overlap it only in
+// part), so a tile costs about the sum of its instruction times and the
+// cheaper float16 contraction (3 instructions for D <= 13 instead of 4 float32
+// ones at twice the cost each) shortens it directly.
 //
 // Pack layout (both sides): per 16-point tile and 32-slot chunk c, lane (g, p)
 // holds slots 8g .. 8g+7 of point 16 tile + p as eight float16 values (one
@@ -533,8 +536,9 @@ __device__ __forceinline__ void load_hx_col(HxCol<RID>& c, const uintx4* __restr
 }
 
 // One column tile against the wave's NIB row tiles: all exponent chains
-// first (independent, so the matrix core and the exponentials overlap), then
-// K' = 2^t summed (times the weights) on the vector ALUs.
+// first (independent chains issue back to back and the exponentials can
+// overlap their tail), then K' = 2^t summed (times the weights) on the vector
+// ALUs.
 template <int RID, int NIB, bool UNIT, bool DIAG>
 __device__ __forceinline__ void hx_rowsum_tile(const HxCol<RID>& c,
                                                const uintx4 (&br)[NIB][Hx<RID>::nb],
@@ -635,6 +639,225 @@ __attribute__((amdgpu_waves_per_eu(hx_waves<RID, 0, NIB>()))) void rowsum_hx_ker
   }
 }
 
+// ------------------------------------------------------------------ symmetric row sums
+//
+// When rows and columns are the same N points, K is symmetric and each
+// off-diagonal tile K_IJ can serve both sums: q_I += K_IJ w_J along its rows and
+// q_J += K_IJ^T w_I along its columns, so every kernel entry off the diagonal
+// blocks is evaluated (and exponentiated) once instead of twice.
+//
+// Points are grouped in blocks of 512 (one workgroup's 4 waves x 8 row tiles);
+// with B blocks and h = (B - 1) / 2, the workgroup of block P takes its own
+// block (row sums only, exact diagonal) and then the blocks P + 1 .. P + h
+// (mod B), plus P + B/2 when B is even and P < B/2: every unordered pair of
+// distinct blocks is then taken exactly once.  That column range is split over
+// nsplit workgroups.  Row sums go to per-split partials as in the plain kernel.
+// Column sums are reduced over the wave's 128 rows (in-lane over its row
+// tiles, then across the 16 lanes of a DPP row), converted to 64-bit fixed
+// point and added into a per-workgroup LDS array with integer LDS atomics; every
+// SYM_CHUNK column tiles the workgroup adds that array into the global
+// per-point accumulator with integer atomics.  Integer addition is exact and
+// order-free, so the result is bitwise reproducible.  (Global atomics inside
+// the tile loop would make each operand-load wait also wait for an atomic's
+// round trip, since vector memory operations retire in order.)  The
+// fixed-point scale assumes weights in [0, 1] (the normalisation weights
+// q^-alpha with q >= 1 are) and leaves a factor 4 of headroom below 2^63 for
+// the total.
+
+// Column tiles whose fixed-point column sums a workgroup gathers in LDS
+// (SYM_CHUNK x 16 x 8 bytes) before adding them into global memory; even.
+constexpr int SYM_CHUNK = 256;
+
+// Sum of v over the 16 lanes of the lane's DPP row (every lane gets the sum).
+__device__ __forceinline__ float dpp_row_sum(float v) {
+  // xor 1 and xor 2 inside quads, then mirrored quads and mirrored half-rows
+  v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0xB1,
+                                                             0xF, 0xF, false));
+  v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x4E,
+                                                             0xF, 0xF, false));
+  v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x141,
+                                                             0xF, 0xF, false));
+  v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x140,
+                                                             0xF, 0xF, false));
+  return v;
+}
+
+// One off-diagonal column tile J against the wave's NIB own row tiles: row
+// sums into acc, column sums of the tile into the fixed-point accumulator.
+template <int RID, int NIB, bool UNIT>
+__device__ __forceinline__ void hx_rowsum_sym_tile(const HxCol<RID>& c,
+                                                   const uintx4 (&br)[NIB][Hx<RID>::nb],
+                                                   const float (&wi)[NIB], float (&acc)[NIB],
+                                                   int64_t jl, double fix_scale,
+                                                   unsigned long long* lds_col, int g,
+                                                   int p) {
+  floatx4 t[NIB];
+#pragma unroll
+  for (int ib = 0; ib < NIB; ++ib) t[ib] = hx_exponent<RID, false>(c.xa, br[ib], g, p);
+  float cs[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int ib = 0; ib < NIB; ++ib) {
+    float k[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) k[r] = __builtin_amdgcn_exp2f(t[ib][r]);
+    if (UNIT) {
+      acc[ib] += (k[0] + k[1]) + (k[2] + k[3]);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) cs[r] += k[r];
+    } else {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        acc[ib] = fmaf(k[r], c.w[r], acc[ib]);
+        cs[r] = fmaf(k[r], wi[ib], cs[r]);
+      }
+    }
+  }
+  // lane (g, p) holds, for column 4g + r of the tile, the sum over rows p of
+  // the wave's tiles; the 16 lanes of DPP row g hold the wave's other rows
+#pragma unroll
+  for (int r = 0; r < 4; ++r) cs[r] = dpp_row_sum(cs[r]);
+  // lane p < 4 adds column 4g + p (selects, no branches)
+  const float v01 = (p & 1) ? cs[1] : cs[0];
+  const float v23 = (p & 1) ? cs[3] : cs[2];
+  const float v = (p & 2) ? v23 : v01;
+  const long long fx = __double2ll_rn(double(v) * fix_scale);
+  if (p < 4) atomicAdd(lds_col + jl * TILE + 4 * g + p, static_cast<unsigned long long>(fx));
+}
+
+template <int RID, int NIB, bool UNIT>
+__global__ __launch_bounds__(WG_THREADS)
+__attribute__((amdgpu_waves_per_eu(hx_waves<RID, 0, NIB>()))) void rowsum_sym_hx_kernel(
+    const uintx4* __restrict__ xc, const floatx4* __restrict__ wp, const uintx4* __restrict__ xr,
+    int64_t nblk, int64_t njb, int64_t jb_per_split, int64_t nsplit, float* __restrict__ part,
+    int64_t nrpad, unsigned long long* __restrict__ colfix, double fix_scale) {
+  constexpr int NB = Hx<RID>::nb;
+  constexpr int BT = 4 * NIB;  // tiles per block
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wr = xcd_remap(blockIdx.x, gridDim.x);
+  // whole-block splits: number the workgroups by the block c their window
+  // starts at (c = P + split * blocks per split), so that consecutive ids (run
+  // together on one XCD) read the same column tiles
+  const int64_t jbk = jb_per_split / BT;
+  int64_t split, P;
+  if (jb_per_split % BT == 0) {
+    const int64_t c = wr / nsplit;
+    split = wr % nsplit;
+    P = ((c - split * jbk) % nblk + nblk) % nblk;
+  } else {
+    split = wr / nblk;
+    P = wr % nblk;
+  }
+  const int64_t ib0 = P * BT + wave * NIB;
+  const int64_t h = (nblk - 1) / 2;
+  const int64_t span = BT * (1 + h + ((nblk % 2 == 0 && 2 * P < nblk) ? 1 : 0));
+  const int64_t jj_begin = split * jb_per_split;
+  const int64_t jj_end = min(span, jj_begin + jb_per_split);
+  const int64_t ntile = nblk * BT;
+  const int g = lane >> 4, p = lane & 15;
+  // fixed-point column sums of the current chunk of SYM_CHUNK tiles
+  __shared__ unsigned long long lds_col[SYM_CHUNK * TILE];
+  for (int e = threadIdx.x; e < SYM_CHUNK * TILE; e += WG_THREADS) lds_col[e] = 0ull;
+  __syncthreads();
+
+  uintx4 br[NIB][NB];
+  float wi[NIB];
+#pragma unroll
+  for (int ib = 0; ib < NIB; ++ib) {
+#pragma unroll
+    for (int ch = 0; ch < NB; ++ch) br[ib][ch] = xr[((ib0 + ib) * NB + ch) * 64 + lane];
+    // weight of own row 16 (ib0 + ib) + p: pack element (tile, lane 16 (p / 4), p % 4);
+    // own tiles past the column pack are padding rows (their kernel values are 0)
+    wi[ib] = 0.f;
+    if (!UNIT && ib0 + ib < njb)
+      wi[ib] = reinterpret_cast<const float*>(wp)[((ib0 + ib) * 64 + 16 * (p >> 2)) * 4 + (p & 3)];
+  }
+  float acc[NIB], tot[NIB];
+#pragma unroll
+  for (int ib = 0; ib < NIB; ++ib) acc[ib] = tot[ib] = 0.f;
+
+  // column tile of range position jj (0 <= jj < span <= ntile + BT, cyclic over
+  // the blocks); -1 for the padding tiles past the real columns
+  const int base = int(P * BT), nt32 = int(ntile), njb32 = int(njb);
+  auto tile_of = [&](int64_t jj) -> int {
+    int J = base + int(jj);
+    if (J >= nt32) J -= nt32;
+    return J < njb32 ? J : -1;
+  };
+  // loads are unconditional (index clamped into the range, padding tiles read
+  // tile 0) so that every path reaches the loop top with the same loads in
+  // flight and the waits there cover one buffer only
+  auto load = [&](HxCol<RID>& c, int64_t jj) {
+    const int J = tile_of(max(min(jj, jj_end - 1), int64_t(0)));
+    load_hx_col<RID, UNIT>(c, xc, wp, J < 0 ? 0 : J, lane);
+  };
+  auto step = [&](const HxCol<RID>& c, int64_t jj) {
+    const int J = tile_of(jj);
+    if (J < 0) return;
+    if (jj >= BT) {
+      hx_rowsum_sym_tile<RID, NIB, UNIT>(c, br, wi, acc, (jj - jj_begin) % SYM_CHUNK, fix_scale,
+                                         lds_col, g, p);
+    } else if (J >= ib0 && J < ib0 + NIB) {
+      hx_rowsum_tile<RID, NIB, UNIT, true>(c, br, acc, J, ib0, g, p);
+    } else {
+      hx_rowsum_tile<RID, NIB, UNIT, false>(c, br, acc, J, ib0, g, p);
+    }
+  };
+  HxCol<RID> b0, b1;
+  b0.w = b1.w = floatx4{1.f, 1.f, 1.f, 1.f};
+  load(b0, jj_begin);
+  __builtin_amdgcn_sched_barrier(0);  // b0's loads ahead of b1's, as in the loop
+  load(b1, jj_begin + 1);
+  // consume the row operands here (an empty statement reading them): their
+  // loads complete before the loop, whose waits then only ever cover the
+  // column buffer a step consumes (left to itself the compiler sinks these
+  // loads past the loop entry and every iteration waits for all loads)
+#pragma unroll
+  for (int ib = 0; ib < NIB; ++ib)
+#pragma unroll
+    for (int ch = 0; ch < NB; ++ch) asm volatile("" ::"v"(br[ib][ch]));
+  // likewise the scalar kernel argument used in the loop: with its load done
+  // here, the loop's LDS atomics (which share the counter) are never waited on
+  asm volatile("" ::"s"(fix_scale));
+  int chunk = 0;
+  for (int64_t jj = jj_begin; jj < jj_end; jj += 2) {
+    step(b0, jj);
+    load(b0, jj + 2);
+    if (jj + 1 < jj_end) step(b1, jj + 1);
+    load(b1, jj + 3);
+    chunk += 2;
+    if (chunk >= CHUNK_TILES) {
+      chunk = 0;
+#pragma unroll
+      for (int ib = 0; ib < NIB; ++ib) {
+        tot[ib] += acc[ib];
+        acc[ib] = 0.f;
+      }
+    }
+    // end of a chunk of column tiles (the trip count is uniform over the
+    // workgroup): add the chunk's column sums into the global accumulator
+    const int64_t done = jj + 2 - jj_begin;
+    if (done % SYM_CHUNK == 0 || jj + 2 >= jj_end) {
+      const int64_t c0 = jj_begin + (done - 1) / SYM_CHUNK * SYM_CHUNK;
+      __syncthreads();
+      for (int e = threadIdx.x; e < SYM_CHUNK * TILE; e += WG_THREADS) {
+        const unsigned long long v = lds_col[e];
+        const int J = c0 + e / TILE < jj_end ? tile_of(c0 + e / TILE) : -1;
+        if (v != 0ull && J >= 0) atomicAdd(colfix + int64_t(J) * TILE + e % TILE, v);
+        lds_col[e] = 0ull;
+      }
+      __syncthreads();
+    }
+  }
+#pragma unroll
+  for (int ib = 0; ib < NIB; ++ib) {
+    float v = (tot[ib] + acc[ib]) * 0x1p-15f;
+    v += __shfl_xor(v, 16);
+    v += __shfl_xor(v, 32);
+    if (g == 0) part[split * nrpad + (ib0 + ib) * TILE + p] = v;
+  }
+}
+
 // ------------------------------------------------------------------ host dispatch
 
 template <int RID, int NCB, int NIB>
@@ -709,6 +932,37 @@ void rowsum_hx_u(const KVPlan& p, const PointPack& rows, const PointPack& cols, 
     rowsum_hx_launch<RID, 4, false>(p, rows, cols, wp, diag, out, part, stream);
 }
 
+template <int RID, int NIB, bool UNIT>
+void rowsum_sym_hx_launch(const KVPlan& p, const PointPack& rows, const PointPack& cols,
+                          const float* wp, float* part, unsigned long long* colfix,
+                          double fix_scale, hipStream_t stream) {
+  const unsigned grid = unsigned(p.nrt * p.nsplit);
+  ProfScope prof(FD_KERNEL_ROWSUM, stream);
+  hipLaunchKernelGGL((rowsum_sym_hx_kernel<RID, NIB, UNIT>), dim3(grid), dim3(WG_THREADS), 0, stream,
+                     reinterpret_cast<const uintx4*>(cols.xp.p),
+                     reinterpret_cast<const floatx4*>(wp),
+                     reinterpret_cast<const uintx4*>(rows.xp.p), p.nrt, p.njb, p.jb_per_split,
+                     int64_t(p.nsplit), part, rows.npad, colfix, fix_scale);
+  FD_LAUNCH_CHECK();
+}
+
+template <int RID>
+void rowsum_sym_hx_u(const KVPlan& p, const PointPack& rows, const PointPack& cols,
+                     const float* wp, float* part, unsigned long long* colfix, double fix_scale,
+                     hipStream_t stream) {
+  if (p.nib == 4) {
+    if (wp == nullptr)
+      rowsum_sym_hx_launch<RID, 4, true>(p, rows, cols, wp, part, colfix, fix_scale, stream);
+    else
+      rowsum_sym_hx_launch<RID, 4, false>(p, rows, cols, wp, part, colfix, fix_scale, stream);
+    return;
+  }
+  if (wp == nullptr)
+    rowsum_sym_hx_launch<RID, 8, true>(p, rows, cols, wp, part, colfix, fix_scale, stream);
+  else
+    rowsum_sym_hx_launch<RID, 8, false>(p, rows, cols, wp, part, colfix, fix_scale, stream);
+}
+
 void check_hx(const KVPlan& p, const PointPack& rows, const PointPack& cols) {
   FD_REQUIRE(rows.rid >= 0 && rows.rid < HX_RECIPES && rows.rid == cols.rid && rows.row_side &&
                  !cols.row_side,
@@ -766,6 +1020,29 @@ void launch_product_hx(const KVPlan& p, const PointPack& rows, const PointPack& 
     case 4: return product_hx_ncb<4>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
     case 5: return product_hx_ncb<5>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
     case 6: return product_hx_ncb<6>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
+  }
+}
+
+void launch_rowsum_sym_hx(const KVPlan& p, const PointPack& rows, const PointPack& cols,
+                          const float* wp, float* part, unsigned long long* colfix,
+                          double fix_scale, hipStream_t stream) {
+  FD_REQUIRE(rows.rid >= 0 && rows.rid < HX_RECIPES && rows.rid == cols.rid && rows.row_side &&
+                 !cols.row_side && rows.n == cols.n,
+             FD_ERR_INVALID_ARG, "internal: symmetric row sums need one point set");
+  FD_REQUIRE((p.nib == 4 || p.nib == 8) && p.nrt * 4 * p.nib * TILE == rows.npad &&
+                 p.njb == ceil_div(cols.n, TILE),
+             FD_ERR_INVALID_ARG, "internal: symmetric row-sum plan");
+  const HxRecipe& R = HX_TABLE[rows.rid];
+  check_span(rows.xp, size_t(rows.npad / TILE) * R.nb * 64 * 4, "split row pack");
+  check_span(cols.xp, size_t(round_up(p.njb, 2)) * R.nc * 64 * 4, "split column pack");
+  switch (rows.rid) {
+    case 0: return rowsum_sym_hx_u<0>(p, rows, cols, wp, part, colfix, fix_scale, stream);
+    case 1: return rowsum_sym_hx_u<1>(p, rows, cols, wp, part, colfix, fix_scale, stream);
+    case 2: return rowsum_sym_hx_u<2>(p, rows, cols, wp, part, colfix, fix_scale, stream);
+    case 3: return rowsum_sym_hx_u<3>(p, rows, cols, wp, part, colfix, fix_scale, stream);
+    case 4: return rowsum_sym_hx_u<4>(p, rows, cols, wp, part, colfix, fix_scale, stream);
+    case 5: return rowsum_sym_hx_u<5>(p, rows, cols, wp, part, colfix, fix_scale, stream);
+    case 6: return rowsum_sym_hx_u<6>(p, rows, cols, wp, part, colfix, fix_scale, stream);
   }
 }
 

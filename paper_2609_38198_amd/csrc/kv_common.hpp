@@ -72,5 +72,11 @@ void launch_product_hx(const KVPlan& p, const PointPack& rows, const PointPack& 
                        float* Y, int64_t ldy, int b, float* part, hipStream_t stream);
 void launch_rowsum_hx(const KVPlan& p, const PointPack& rows, const PointPack& cols,
                       const float* wp, bool diag, float* out, float* part, hipStream_t stream);
+// Symmetric row sums of one point set (rows.n == cols.n): per-split row partials
+// into part ([nsplit][rows.npad]) and column sums added into colfix (64-bit fixed
+// point, fix_scale per unit of the shifted kernel 2^15 K; weights in [0, 1]).
+void launch_rowsum_sym_hx(const KVPlan& p, const PointPack& rows, const PointPack& cols,
+                          const float* wp, float* part, unsigned long long* colfix,
+                          double fix_scale, hipStream_t stream);
 
 }  // namespace fd

@@ -10,6 +10,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 
 #include "fd_profile.hpp"
 #include "kv_common.hpp"
@@ -476,6 +477,24 @@ __global__ void reduce_rowsum_kernel(const float* __restrict__ part, int nsplit,
   out[i] = float(s);
 }
 
+// Symmetric row sums: out_i = sum over splits of the row partials + the
+// fixed-point column sums (colfix * 2^-F), in double, fixed order.
+__global__ void reduce_rowsum_sym_kernel(const float* __restrict__ part, int nsplit,
+                                         int64_t nrpad, const unsigned long long* __restrict__ colfix,
+                                         double inv_fix, float* __restrict__ out, int64_t Nr) {
+  const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i >= Nr) return;
+  double s = 0.0;
+  for (int k = 0; k < nsplit; ++k) s += double(part[k * nrpad + i]);
+  s += double(static_cast<long long>(colfix[i])) * inv_fix;
+  out[i] = float(s);
+}
+
+__global__ void zero_u64_kernel(unsigned long long* __restrict__ p, int64_t n) {
+  const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0ull;
+}
+
 // w = q^-alpha
 __global__ void pow_neg_kernel(const float* __restrict__ q, int64_t n, double alpha,
                                float* __restrict__ w) {
@@ -549,6 +568,43 @@ KVPlan plan_product(int64_t Nr, int64_t Nc, int dp, int b) {
 // Row sums: eight row tiles per wave (more independent exponent chains per
 // column tile than four; measured faster on every shape).
 KVPlan plan_rowsum(int64_t Nr, int64_t Nc, int dp) { return plan_tiles(Nr, Nc, dp, 1, 8); }
+
+// Symmetric row sums (one point set): workgroups of 4 waves x nib row tiles
+// own blocks of 64 nib points; a block's column range (its own block and about
+// half of the others) is split for >= 2048 workgroups.  nrt holds the number
+// of blocks.  From 64 blocks up, splits are whole blocks (at least
+// SYM_MIN_SPLITS of them): the workgroups whose windows start at the same
+// block then read the same column tiles, and the kernel runs them side by side
+// on one XCD so that they share its L2.
+KVPlan plan_rowsum_sym(int64_t N, int64_t npad, int dp, int nib) {
+  KVPlan p;
+  p.dp = dp;
+  p.ncb = 1;
+  p.nib = nib;
+  p.njb = ceil_div(N, TILE);
+  const int64_t BT = 4 * nib;
+  p.nrt = npad / (BT * TILE);
+  const int64_t span_blocks = 1 + (p.nrt - 1) / 2 + (p.nrt % 2 == 0 ? 1 : 0);  // longest range
+  const int64_t target = 2048;
+  if (p.nrt >= 64) {
+    const int64_t ns = std::max<int64_t>(SYM_MIN_SPLITS, ceil_div(target, p.nrt));
+    const int64_t jbk = std::max<int64_t>(1, span_blocks / ns);
+    p.jb_per_split = jbk * BT;
+    p.nsplit = int(ceil_div(span_blocks, jbk));
+    return p;
+  }
+  const int64_t span = BT * span_blocks;
+  int64_t ns = std::max<int64_t>(1, ceil_div(target, p.nrt));
+  ns = std::min<int64_t>(ns, std::max<int64_t>(1, span / 8));
+  ns = std::min<int64_t>(ns, 64);
+  p.jb_per_split = round_up(ceil_div(span, ns), 2);
+  p.nsplit = int(ceil_div(span, p.jb_per_split));
+  return p;
+}
+
+size_t sym_part_rows(int64_t npad, int nib) {
+  return size_t(plan_rowsum_sym(npad, npad, 4, nib).nsplit) * size_t(npad);
+}
 
 static inline size_t lane4_extent(int64_t tiles, int groups) {
   return size_t(tiles) * groups * 64 * 4;
@@ -749,9 +805,29 @@ static void rowsum_bf16_launch(const KVPlan& p, const PointPack& rows, const Poi
     rowsum_bf16_nib<DC, 4, UNIT>(p, rows, cols, wp, diag, out, part, stream);
 }
 
+
 void launch_rowsum(const KVPlan& p, const PointPack& rows, const PointPack& cols, FSpan wp,
-                   bool diag, float* out, FSpan part, hipStream_t stream) {
+                   bool diag, float* out, FSpan part, hipStream_t stream,
+                   unsigned long long* colfix) {
   check_tiles(p, rows, cols);
+  if (colfix != nullptr && diag && !rows.bf16 && !cols.bf16 && rows.n == cols.n) {
+    // one point set: each off-diagonal tile serves its rows and its columns
+    const KVPlan sp = plan_rowsum_sym(rows.n, rows.npad, p.dp, SYM_NIB);
+    if (wp.p != nullptr) check_span(wp, lane4_extent(sp.njb, 1), "weight pack");
+    check_span(part, size_t(sp.nsplit) * rows.npad, "partial row sums");
+    // fixed point with F fractional bits: the total of weights in [0, 1] over
+    // npad columns stays below 2^62 / 4
+    const int F = 62 - int(std::ceil(std::log2(double(rows.npad)))) - 2;
+    hipLaunchKernelGGL(zero_u64_kernel, dim3(blocks_for(rows.npad, 256)), dim3(256), 0, stream,
+                       colfix, rows.npad);
+    FD_LAUNCH_CHECK();
+    launch_rowsum_sym_hx(sp, rows, cols, wp.p, part.p, colfix, std::ldexp(1.0, F - 15), stream);
+    hipLaunchKernelGGL(reduce_rowsum_sym_kernel, dim3(blocks_for(rows.n, 256)), dim3(256), 0,
+                       stream, part.p, sp.nsplit, rows.npad, colfix, std::ldexp(1.0, -F), out,
+                       rows.n);
+    FD_LAUNCH_CHECK();
+    return;
+  }
   FD_REQUIRE(p.nib == 4 || p.nib == 8, FD_ERR_INVALID_ARG, "internal: row-sum plan");
   if (wp.p != nullptr) check_span(wp, lane4_extent(p.njb, 1), "weight pack");
   float* pp = nullptr;

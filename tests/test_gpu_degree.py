@@ -104,3 +104,43 @@ def test_bf16_normalisation():
     ref = on.normalise(s.X_f64(), beta, 0.5)
     for name in ("q", "d", "s"):
         assert rel_fro(to_np(getattr(deg, name)), getattr(ref, name)) <= TOL_F32
+
+
+# Block counts of the symmetric row sums (blocks of 512 points): one block,
+# even and odd counts (the pairing of blocks differs), ragged last blocks.
+@pytest.mark.parametrize("N", [1, 2, 17, 511, 513, 1536, 2560, 3072, 3583])
+def test_symmetric_block_counts(N):
+    rng = np.random.default_rng(31 + N)
+    X = rng.normal(size=(N, 7)).astype(np.float32)
+    X -= X.mean(0)
+    dev = device()
+    case(f"degree symmetric row sums N={N}")
+    for beta in (0.05, 1.0):
+        deg = fd.fd_degree(to_dev(X, dev), beta, 0.5)
+        ref = on.normalise(X, beta, 0.5)
+        for name in ("q", "d", "s"):
+            assert rel_fro(to_np(getattr(deg, name)), getattr(ref, name)) <= TOL_F32, (beta, name)
+
+
+def test_symmetric_row_sums_match_plain_product_and_repeat_bitwise():
+    # q from the symmetric row sums against K 1 from the fused product (a
+    # separate kernel that evaluates every entry), and two calls bit for bit
+    w = inputs.torus6()
+    dev = device()
+    X = to_dev(w.X, dev)
+    case("degree symmetric vs product K 1, torus6 N=65536")
+    ones = torch.ones((w.N, 1), dtype=torch.float32, device=dev)
+    for beta in (0.5, 8.0):
+        a = fd.fd_degree(X, beta, 0.5)
+        b = fd.fd_degree(X, beta, 0.5)
+        torch.cuda.synchronize()
+        for name in ("q", "d", "s"):
+            assert torch.equal(getattr(a, name), getattr(b, name)), name
+        k1 = to_np(fd.fd_kernel_matmul(X, None, beta, ones))[:, 0]
+        q = to_np(a.q)
+        # both evaluate the exponent in float32 in the Gram form, with a rounding
+        # of about 2^-24 * 2 beta log2(e) max ||x||^2 (in log2 units) that
+        # depends on the evaluation order: entries may differ by twice that
+        bound = 2 * 2.0**-24 * 2 * beta * np.log2(np.e) * float((w.X.astype(np.float64) ** 2).sum(1).max())
+        assert rel_fro(q, k1) <= 1e-6
+        assert np.abs(q / k1 - 1.0).max() <= bound * np.log(2) + 1e-6
