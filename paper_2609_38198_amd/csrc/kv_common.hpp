@@ -12,6 +12,8 @@ typedef _Float16 halfx8 __attribute__((ext_vector_type(8)));
 typedef __fp16 pkhalf2 __attribute__((ext_vector_type(2)));
 typedef unsigned uintx4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx2 __attribute__((ext_vector_type(2)));
+typedef _Float16 halfx2 __attribute__((ext_vector_type(2)));
 
 constexpr double LOG2E = 1.4426950408889634073599;
 constexpr int CHUNK_TILES = 64;  // column tiles per partial accumulator

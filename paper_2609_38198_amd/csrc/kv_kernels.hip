@@ -270,9 +270,16 @@ __device__ __forceinline__ void load_pair_b(ColPairB<DC, NCB>& cp, const uintx4*
   }
 }
 
+// Exponents of one pair of column tiles against row tile ib, in accumulator
+// layout with the column offsets as the initial accumulator:
+//   u_ij = -||x_j||^2 / 2 + x_j . x_i,  K'_ij = 2^(scale2 u_ij + c_i) = 2^15 K_ij,
+// with c_i = 15 - scale2 ||x_i||^2 / 2 per row (one FMA per entry).  K' is
+// rounded to float16 (nearest, two per instruction) and multiplied into the
+// split V on the float16 matrix cores; lane (g, p) holds K'[p][J0 + 4g + r]
+// and K'[p][J1 + 4g + r], its A-operand values k = 8g + 4u + r.
 template <int DC, int NCB, int NIB, bool DIAG>
 __device__ __forceinline__ void bf16_pair(const ColPairB<DC, NCB>& c, const uintx4 (&xbr)[NIB][DC],
-                                          const float (&ai)[NIB], float scale2,
+                                          const float (&ci)[NIB], float scale2,
                                           floatx4 (&acc)[NIB][NCB], int64_t jp, int64_t ib0,
                                           int g, int p) {
 #pragma unroll
@@ -280,17 +287,30 @@ __device__ __forceinline__ void bf16_pair(const ColPairB<DC, NCB>& c, const uint
     floatx4 t[2];
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
-      if (DIAG && 2 * jp + u == ib0 + ib)
-        t[u] = half_sqdist<DC, true>(c.xa[u], c.aj[u], xbr[ib], ai[ib], g, p);
-      else
-        t[u] = half_sqdist<DC, false>(c.xa[u], c.aj[u], xbr[ib], ai[ib], g, p);
+      t[u] = c.aj[u];
+#pragma unroll
+      for (int cc = 0; cc < DC; ++cc)
+        t[u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, c.xa[u][cc]),
+                                                       __builtin_bit_cast(bf16x8, xbr[ib][cc]),
+                                                       t[u], 0, 0, 0);
     }
-    halfx8 k;
+    float e[8];
 #pragma unroll
     for (int u = 0; u < 2; ++u)
 #pragma unroll
-      for (int r = 0; r < 4; ++r)  // K' = 2^(2 beta log2e C + 15) <= 2^15
-        k[4 * u + r] = _Float16(__builtin_amdgcn_exp2f(fmaf(t[u][r], scale2, 15.f)));
+      for (int r = 0; r < 4; ++r) {
+        e[4 * u + r] = fmaf(t[u][r], scale2, ci[ib]);
+        // the diagonal of one point set: K'_ii = 2^15 exactly
+        if (DIAG && 2 * jp + u == ib0 + ib && 4 * g + r == p) e[4 * u + r] = 15.f;
+      }
+    halfx8 k;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const floatx2 kk = floatx2{__builtin_amdgcn_exp2f(e[2 * q]), __builtin_amdgcn_exp2f(e[2 * q + 1])};
+      const halfx2 hk = __builtin_convertvector(kk, halfx2);
+      k[2 * q] = hk[0];
+      k[2 * q + 1] = hk[1];
+    }
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb) {
       acc[ib][cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(k, c.v[cb].hi, acc[ib][cb], 0, 0, 0);
@@ -299,8 +319,20 @@ __device__ __forceinline__ void bf16_pair(const ColPairB<DC, NCB>& c, const uint
   }
 }
 
+// Waves per SIMD asked of the compiler (at 2 a wave has at most 256
+// registers and accumulates in ordinary VGPRs; the widest blocks take 1).
 template <int DC, int NCB, int NIB>
-__global__ __launch_bounds__(WG_THREADS) void product_bf16_kernel(
+constexpr int bf16_waves() {
+  return (NIB * NCB * 4 + NIB * DC * 4 + 2 * (DC * 8 + 8 + NCB * 8) > 200) ? 1 : 2;
+}
+
+// One workgroup = 4 waves; wave w owns row tiles [ib0, ib0 + NIB).  Column
+// tiles stream in pairs through two operand buffers used in turn (each
+// refilled right after its pair is consumed); chunk totals of the two-level
+// column sum live in LDS.
+template <int DC, int NCB, int NIB>
+__global__ __launch_bounds__(WG_THREADS)
+__attribute__((amdgpu_waves_per_eu(bf16_waves<DC, NCB, NIB>()))) void product_bf16_kernel(
     const uintx4* __restrict__ xa, const floatx4* __restrict__ aj, const VSplit* __restrict__ vp,
     const uintx4* __restrict__ xb, const float* __restrict__ ar, int64_t nrt, int64_t njp,
     int64_t jp_per_split, int diag, float scale2, const float* __restrict__ colscale,
@@ -308,7 +340,7 @@ __global__ __launch_bounds__(WG_THREADS) void product_bf16_kernel(
     float* __restrict__ part, int64_t nrpad) {
   __shared__ floatx4 tot[4][NIB][NCB][64];
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wr = xcd_remap(blockIdx.x, gridDim.x);
   const int64_t split = wr / nrt;
   const int64_t rt = wr % nrt;
@@ -318,12 +350,12 @@ __global__ __launch_bounds__(WG_THREADS) void product_bf16_kernel(
   const int g = lane >> 4, p = lane & 15;
 
   uintx4 xbr[NIB][DC];
-  float ai[NIB];
+  float ci[NIB];
 #pragma unroll
   for (int ib = 0; ib < NIB; ++ib) {
 #pragma unroll
-    for (int c = 0; c < DC; ++c) xbr[ib][c] = xb[((ib0 + ib) * DC + c) * 64 + lane];
-    ai[ib] = ar[(ib0 + ib) * TILE + p];
+    for (int cc = 0; cc < DC; ++cc) xbr[ib][cc] = xb[((ib0 + ib) * DC + cc) * 64 + lane];
+    ci[ib] = fmaf(scale2, ar[(ib0 + ib) * TILE + p], 15.f);
   }
   floatx4 acc[NIB][NCB];
 #pragma unroll
@@ -334,16 +366,35 @@ __global__ __launch_bounds__(WG_THREADS) void product_bf16_kernel(
       tot[wave][ib][cb][lane] = floatx4{0.f, 0.f, 0.f, 0.f};
     }
 
-  ColPairB<DC, NCB> cur, nxt;
-  load_pair_b(cur, xa, aj, vp, jp_begin, lane);
-  int chunk = 0;
-  for (int64_t jp = jp_begin; jp < jp_end; ++jp) {
-    load_pair_b(nxt, xa, aj, vp, min(jp + 1, jp_end - 1), lane);
+  auto step = [&](const ColPairB<DC, NCB>& c, int64_t jp) {
     if (diag && 2 * jp + 1 >= ib0 && 2 * jp < ib0 + NIB)
-      bf16_pair<DC, NCB, NIB, true>(cur, xbr, ai, scale2, acc, jp, ib0, g, p);
+      bf16_pair<DC, NCB, NIB, true>(c, xbr, ci, scale2, acc, jp, ib0, g, p);
     else
-      bf16_pair<DC, NCB, NIB, false>(cur, xbr, ai, scale2, acc, jp, ib0, g, p);
-    if (++chunk == CHUNK_TILES / 2) {
+      bf16_pair<DC, NCB, NIB, false>(c, xbr, ci, scale2, acc, jp, ib0, g, p);
+  };
+  ColPairB<DC, NCB> b0, b1;
+  load_pair_b(b0, xa, aj, vp, jp_begin, lane);
+  __builtin_amdgcn_sched_barrier(0);  // b0's loads ahead of b1's, as in the loop
+  load_pair_b(b1, xa, aj, vp, min(jp_begin + 1, jp_end - 1), lane);
+  // consume the row operands before the loop (an empty statement reading
+  // them): their loads then complete here, and the loop's waits only ever
+  // cover the column buffer a step consumes
+#pragma unroll
+  for (int ib = 0; ib < NIB; ++ib) {
+#pragma unroll
+    for (int cc = 0; cc < DC; ++cc) asm volatile("" ::"v"(xbr[ib][cc]));
+    asm volatile("" ::"v"(ci[ib]));
+  }
+  int chunk = 0;
+  for (int64_t jp = jp_begin; jp < jp_end; jp += 2) {
+    step(b0, jp);
+    // the refills are unconditional (clamped index): every path reaches the
+    // loop top with the same loads in flight
+    load_pair_b(b0, xa, aj, vp, min(jp + 2, jp_end - 1), lane);
+    if (jp + 1 < jp_end) step(b1, jp + 1);
+    load_pair_b(b1, xa, aj, vp, min(jp + 3, jp_end - 1), lane);
+    chunk += 2;
+    if (chunk >= CHUNK_TILES / 2) {
       chunk = 0;
 #pragma unroll
       for (int ib = 0; ib < NIB; ++ib)
@@ -353,7 +404,6 @@ __global__ __launch_bounds__(WG_THREADS) void product_bf16_kernel(
           acc[ib][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
         }
     }
-    cur = nxt;
   }
 
 #pragma unroll
