@@ -221,6 +221,46 @@ def stress_leg(fd, torch, dev) -> dict:
             "evals_head": e.evals[:4], "evals_tail": e.evals[-2:]}
 
 
+# The paper's XGEMM timings for one raw kernel application K V on its T^6
+# set-up (App. B, the matvec and matmat tables: fp32, D = 32, beta = 1, one
+# RTX PRO 6000), seconds at N = 2^lg.  Context only: other hardware.
+PAPER_XGEMM_S = {
+    1: {16: 0.010897011, 18: 0.1407541988, 20: 2.08317415},
+    8: {16: 0.012966476, 18: 0.152757719, 20: 2.897318638},
+}
+
+
+def paper_t6_leg(fd, torch, dev) -> dict:
+    """Raw K V (b = 1 and 8) on the paper's T^6 set-up, beside its own timings."""
+    from paper_2609_38198_amd import inputs
+    rows = []
+    for lg in (16, 18, 20):
+        w = inputs.torus6_paper(1 << lg)
+        N, D = w.N, w.D
+        X = torch.from_numpy(w.X).to(dev)
+        for b in (1, 8):
+            V = torch.from_numpy(inputs.random_block(N, b)).to(dev)
+            Y = torch.empty((N, b), dtype=torch.float32, device=dev)
+            ws = torch.empty(fd.fd_workspace_size(fd.FD_OP_KERNEL_MATMUL, N, N, D, b),
+                             dtype=torch.uint8, device=dev)
+            fd.fd_kernel_matmul(X, None, 1.0, V, Y=Y, ws=ws)
+            torch.cuda.synchronize()
+            reps = 3 if lg >= 20 else 10
+            t0 = time.perf_counter()
+            for _ in range(reps):
+                fd.fd_kernel_matmul(X, None, 1.0, V, Y=Y, ws=ws)
+            torch.cuda.synchronize()
+            t = (time.perf_counter() - t0) / reps
+            paper = PAPER_XGEMM_S[b][lg]
+            rows.append({"N": N, "b": b, "seconds": t, "pairs_per_s": float(N) * N / t,
+                         "pair_cols_per_s": float(N) * N * b / t, "paper_xgemm_s": paper,
+                         "paper_over_this": paper / t})
+            del ws, Y, V
+            log(f"paper T6 leg: N=2^{lg} b={b}: {t * 1e3:.2f} ms (paper {paper * 1e3:.2f} ms)")
+    return {"workload": "anisotropic flat 6-torus, radii 1.00..1.50, D=32 zero-padded, beta=1, "
+                        "seed 42, unnormalised K V", "rows": rows}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -232,6 +272,9 @@ def main() -> int:
     ap.add_argument("--molecule", action="store_true")
     ap.add_argument("--continuation", action="store_true")
     ap.add_argument("--stress", action="store_true")
+    ap.add_argument("--paper-t6", action="store_true",
+                    help="raw K V on the paper's T^6 set-up (D=32, beta=1, b=1 and 8) beside "
+                         "the paper's own timings")
     ap.add_argument("--calibration-copy", type=int, default=0, metavar="MIB",
                     help="after the timed steps, copy MIB MiB device to device (a plain copy "
                          "kernel of known size, read by the HBM counter runs as their scale)")
@@ -342,6 +385,8 @@ def main() -> int:
         rec["continuation"] = continuation_leg(fd, torch, dev)
     if args.stress:
         rec["stress"] = stress_leg(fd, torch, dev)
+    if args.paper_t6:
+        rec["paper_t6"] = paper_t6_leg(fd, torch, dev)
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(wl.X, 2.0, b, args.cpu_seconds)
     print(json.dumps(rec), flush=True)

@@ -5,6 +5,13 @@
   eta per data type from the footnote to eq. perronwall.
 * Smooth barrier V_mach = (kappa_P eta / g_P)^p with p = 6 (eq. vmach).
 * Principal angles between subspaces (LAPACK-based, through scipy).
+* Rotation-invariant subspace overlap of Sec. 3 (the T^6 recovery score, in
+  the footnote to the discussion of its figure c): with A and B the column
+  blocks of two subspaces and G_AA, G_BB, G_AB their centred covariance
+  blocks, C = G_AA^-1/2 G_AB G_BB^-1/2 and the score is sum_ij C_ij^2 / 2 for
+  two-dimensional blocks (the squared RV coefficient).  Reading: for blocks
+  of other widths the sum is divided by the smaller width, so that the score
+  is 1 when one span contains the other and 0 when they are orthogonal.
 """
 from __future__ import annotations
 
@@ -34,3 +41,22 @@ def principal_angles(A: np.ndarray, B: np.ndarray) -> np.ndarray:
     """Principal angles (radians, descending) between span(A) and span(B)."""
     return scipy.linalg.subspace_angles(np.asarray(A, dtype=np.float64),
                                         np.asarray(B, dtype=np.float64))
+
+
+def _inv_sqrt_spd(G: np.ndarray) -> np.ndarray:
+    w, U = np.linalg.eigh(G)
+    return (U / np.sqrt(w)) @ U.T
+
+
+def rv_overlap(A: np.ndarray, B: np.ndarray) -> float:
+    """Whitened cross-covariance overlap of span(A) and span(B) in [0, 1]."""
+    A = np.asarray(A, dtype=np.float64)
+    B = np.asarray(B, dtype=np.float64)
+    if A.ndim == 1:
+        A = A[:, None]
+    if B.ndim == 1:
+        B = B[:, None]
+    A = A - A.mean(axis=0)
+    B = B - B.mean(axis=0)
+    C = _inv_sqrt_spd(A.T @ A) @ (A.T @ B) @ _inv_sqrt_spd(B.T @ B)
+    return float((C ** 2).sum() / min(A.shape[1], B.shape[1]))

@@ -65,6 +65,7 @@ ProductWs carve_product(Arena& a, int64_t Nr, int64_t Nc, int64_t D, int b) {
   w.vp = a.fspan(size_t(w.cols.npad) * w.plan.ncb * 16);
   w.vscale = a.fspan(128);
   w.part = a.fspan(part_rows_bound(w.rows.npad) * w.plan.ncb * 16);
+  w.tmp = a.fspan(size_t(Nr));
   return w;
 }
 
@@ -98,6 +99,16 @@ ProductWs product_view(const ProductWs& big, const PointPack& rows, const PointP
 
 void product_apply(ProductWs& w, const float* sl, const float* sr, const float* V, int64_t ldv,
                    int b, float* Y, int64_t ldy, bool diag, hipStream_t stream) {
+  if (b == 1) {
+    // one right-hand side: weighted row sums K (sr v) on the vector ALUs (no
+    // matrix-core contraction padded to 16 columns), then the row scale
+    launch_pack_wv(V, ldv, sr, w.cols.n, w.cols.npad, w.vp, stream);
+    const KVPlan rp = plan_rowsum(w.rows.n, w.cols.n, w.rows.dp);
+    check_span(w.tmp, size_t(w.rows.n), "single-column row sums");
+    launch_rowsum(rp, w.rows, w.cols, w.vp, diag, w.tmp.p, w.part, stream);
+    launch_scale_rows(w.tmp.p, sl, w.rows.n, Y, ldy, stream);
+    return;
+  }
   launch_pack_v_for(w.rows, V, w.cols.n, b, ldv, sr, w.plan.ncb, w.cols.npad, w.vp, w.vscale,
                     stream);
   launch_product(w.plan, w.rows, w.cols, w.vp, w.vscale, diag, sl, Y, ldy, b, w.part, stream);

@@ -123,6 +123,12 @@ PointPack carve_pack(Arena& a, int64_t n, int dp, int64_t pad);
 void launch_pack_points(const void* X, fd_dtype xt, int64_t n, int64_t D, int64_t ldx,
                         double beta, bool row_side, PointPack& out, hipStream_t stream);
 void launch_pack_w(const float* w, int64_t n, int64_t npad, FSpan wp, hipStream_t stream);
+// Weight pack of sr * v for one column v (row stride ldv; sr may be NULL).
+void launch_pack_wv(const float* v, int64_t ldv, const float* sr, int64_t n, int64_t npad,
+                    FSpan wp, hipStream_t stream);
+// Y[i * ldy] = sl[i] * t[i] (sl NULL: t[i]).
+void launch_scale_rows(const float* t, const float* sl, int64_t n, float* Y, int64_t ldy,
+                       hipStream_t stream);
 // Pack sr * V for the product that matches the row pack's kind.
 void launch_pack_v_for(const PointPack& rows, const float* V, int64_t n, int64_t b, int64_t ldv,
                        const float* sr, int ncb, int64_t npad, FSpan vp, FSpan vscale,

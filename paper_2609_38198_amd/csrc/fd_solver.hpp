@@ -9,6 +9,7 @@ namespace fd {
 struct ProductWs {
   PointPack rows, cols;
   FSpan vp, vscale, part;
+  FSpan tmp;  // one float per row: the single-column product's row sums
   KVPlan plan;
 };
 

@@ -64,6 +64,32 @@ __global__ void pack_w_kernel(const float* __restrict__ w, int64_t n, int64_t nt
   wp[idx] = out;
 }
 
+// Weight pack of sr * v for a single right-hand side v (stride ldv): the
+// layout of pack_w_kernel.
+__global__ void pack_wv_kernel(const float* __restrict__ v, int64_t ldv,
+                               const float* __restrict__ sr, int64_t n, int64_t ntiles,
+                               floatx4* __restrict__ wp) {
+  const int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (idx >= ntiles * 64) return;
+  const int lane = int(idx & 63);
+  const int64_t jb = idx >> 6;
+  const int g = lane >> 4;
+  floatx4 out;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int64_t j = jb * TILE + 4 * g + r;
+    out[r] = (j < n) ? (sr != nullptr ? sr[j] * v[j * ldv] : v[j * ldv]) : 0.f;
+  }
+  wp[idx] = out;
+}
+
+// Y[i] = sl[i] * t[i] (sl NULL: copy), Y with row stride ldy.
+__global__ void scale_rows_kernel(const float* __restrict__ t, const float* __restrict__ sl,
+                                  int64_t n, float* __restrict__ Y, int64_t ldy) {
+  const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i < n) Y[i * ldy] = (sl != nullptr) ? sl[i] * t[i] : t[i];
+}
+
 // 2^t clamped to [0, 1]: the exponent of a true kernel value is <= 0 and
 // rounding can only push it a few ulps above.  The median-of-three with 0 and 1
 // folds into the output clamp bit of v_exp_f32 (one instruction).  Written with
@@ -701,6 +727,23 @@ void launch_pack_w(const float* w, int64_t n, int64_t npad, FSpan wp, hipStream_
   check_span(wp, lane4_extent(ntiles, 1), "weight pack");
   hipLaunchKernelGGL(pack_w_kernel, dim3(blocks_for(ntiles * 64, 256)), dim3(256), 0, stream, w,
                      n, ntiles, reinterpret_cast<floatx4*>(wp.p));
+  FD_LAUNCH_CHECK();
+}
+
+void launch_pack_wv(const float* v, int64_t ldv, const float* sr, int64_t n, int64_t npad,
+                    FSpan wp, hipStream_t stream) {
+  FD_REQUIRE(npad % TILE == 0 && npad >= n, FD_ERR_INVALID_ARG, "internal: bad w pack geometry");
+  const int64_t ntiles = npad / TILE;
+  check_span(wp, lane4_extent(ntiles, 1), "weight pack");
+  hipLaunchKernelGGL(pack_wv_kernel, dim3(blocks_for(ntiles * 64, 256)), dim3(256), 0, stream, v,
+                     ldv, sr, n, ntiles, reinterpret_cast<floatx4*>(wp.p));
+  FD_LAUNCH_CHECK();
+}
+
+void launch_scale_rows(const float* t, const float* sl, int64_t n, float* Y, int64_t ldy,
+                       hipStream_t stream) {
+  hipLaunchKernelGGL(scale_rows_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, stream, t, sl, n,
+                     Y, ldy);
   FD_LAUNCH_CHECK();
 }
 

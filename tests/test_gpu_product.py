@@ -198,3 +198,44 @@ def test_invalid_arguments_raise():
         fd.fd_kernel_matmul(X, None, 1.0, V)
     with pytest.raises(fd.FdError):
         fd.fd_kernel_matmul(X, None, -1.0, V[:, :4])
+
+
+# A single right-hand side (b = 1) takes the weighted row sums instead of the
+# matrix-core contraction: cover square / rectangular, scaled, strided, signed
+# weights, beta = 0, both input types, and repeat determinism.
+@pytest.mark.parametrize("N,D,beta", [(1, 3, 1.0), (700, 12, 0.8), (4099, 30, 0.3), (2048, 64, 0.05)])
+def test_single_column_product(N, D, beta):
+    rng = np.random.default_rng(50 + N)
+    X = rng.normal(size=(N, D)).astype(np.float32)
+    X -= X.mean(0)
+    v = rng.normal(size=(N, 1)).astype(np.float32)
+    sl = rng.uniform(0.5, 2, N).astype(np.float32)
+    sr = rng.uniform(0.5, 2, N).astype(np.float32)
+    case(f"b=1 N={N} D={D} beta={beta}")
+    Y = _run(X, None, beta, v, sl, sr)
+    ref = ok.kernel_matmul(X, None, beta, v, sl=sl, sr=sr)
+    assert rel_fro(Y, ref) <= TOL_F32
+    assert np.array_equal(_run(X, None, beta, v, sl, sr), Y)
+
+
+def test_single_column_rectangular_strided_bf16_and_beta_zero():
+    dev = device()
+    rng = np.random.default_rng(61)
+    Xr = rng.normal(size=(777, 9)).astype(np.float32)
+    Xc = rng.normal(size=(1234, 9)).astype(np.float32)
+    Vbig = rng.normal(size=(1234, 5)).astype(np.float32)
+    case("b=1 rectangular strided")
+    Ybig = torch.zeros((777, 3), dtype=torch.float32, device=dev)
+    fd.fd_kernel_matmul(to_dev(Xr, dev), to_dev(Xc, dev), 0.4, to_dev(Vbig, dev)[:, 2:3],
+                        Y=Ybig[:, 1:2])
+    ref = ok.kernel_matmul(Xr, Xc, 0.4, Vbig[:, 2:3])
+    assert rel_fro(to_np(Ybig[:, 1:2]), ref) <= TOL_F32
+    assert np.all(to_np(Ybig[:, 0]) == 0) and np.all(to_np(Ybig[:, 2]) == 0)
+    case("b=1 beta=0")
+    Y0 = _run(Xc, None, 0.0, Vbig[:, :1])
+    assert rel_fro(Y0, np.full((1234, 1), Vbig[:, 0].astype(np.float64).sum())) <= TOL_F32
+    s = inputs.stress(N=4096)
+    v = inputs.random_block(4096, 1)
+    case("b=1 bf16 N=4096 D=64")
+    Yb = _run(s.X, None, s.betas[0], v)
+    assert rel_fro(Yb, ok.kernel_matmul(s.X_f64(), None, s.betas[0], v)) <= TOL_BF16

@@ -63,3 +63,17 @@ def test_median_sq_distance_small():
     X = np.array([[0.0], [1.0], [3.0]])
     # pairwise squared distances 1, 9, 4 -> median 4
     assert inputs.median_sq_distance(X, n_sub=3) == pytest.approx(4.0)
+
+
+def test_torus6_paper_layout():
+    # Sec. 3: radii (1.00 ... 1.50) in R^12, zero-padded to D=32, centred,
+    # angles kept for the recovery score
+    w = inputs.torus6_paper(2000)
+    assert w.X.shape == (2000, 32) and w.X.dtype == np.float32
+    assert np.all(w.X[:, 12:] == 0.0)
+    X = w.X.astype(np.float64)
+    np.testing.assert_allclose(X.mean(0), 0.0, atol=1e-6)
+    th = w.extra["theta"]
+    for a, R in enumerate(inputs.T6_RADII):
+        raw = np.stack([R * np.cos(th[:, a]), R * np.sin(th[:, a])], 1)
+        np.testing.assert_allclose(X[:, 2 * a:2 * a + 2], raw - raw.mean(0), atol=1e-6)
