@@ -64,14 +64,17 @@ ProductWs carve_product(Arena& a, int64_t Nr, int64_t Nc, int64_t D, int b) {
   w.cols = carve_pack(a, Nc, dp, COL_PAD);
   w.vp = a.fspan(size_t(w.cols.npad) * w.plan.ncb * 16);
   w.vscale = a.fspan(128);
-  w.part = a.fspan(part_rows_bound(w.rows.npad) * w.plan.ncb * 16);
+  w.part = a.fspan(part_rows_bound(w.rows.npad, Nc) * w.plan.ncb * 16);
   w.tmp = a.fspan(size_t(Nr));
   return w;
 }
 
-// Every plan has nsplit * (row tiles) <= 2048 + (row tiles), so the partial
-// buffers of any problem with at most npad rows fit in this many row slots.
-size_t part_rows_bound(int64_t npad) { return size_t(2048) * ROW_PAD + size_t(npad); }
+// Every plan has nsplit <= max(ceil(2048 / row blocks), ceil(column tiles /
+// SPLIT_SPAN_TILES)), so the partial buffers of any problem with at most npad
+// rows and nc columns fit in this many row slots.
+size_t part_rows_bound(int64_t npad, int64_t nc) {
+  return size_t(2048) * ROW_PAD + size_t(npad) * size_t(1 + ceil_div(ceil_div(nc, TILE), SPLIT_SPAN_TILES));
+}
 
 PointPack pack_view(const PointPack& big, int64_t n, int64_t pad) {
   PointPack p = big;
@@ -126,7 +129,7 @@ DegreeWs carve_degree(Arena& a, int64_t N, int64_t D) {
   w.q = a.take<float>(size_t(N));
   w.t = a.take<float>(size_t(N));
   w.w = a.take<float>(size_t(N));
-  w.part = a.fspan(std::max(part_rows_bound(w.rows.npad), sym_part_rows(w.rows.npad, SYM_NIB)));
+  w.part = a.fspan(std::max(part_rows_bound(w.rows.npad, N), sym_part_rows(w.rows.npad, SYM_NIB)));
   w.colfix = a.take<unsigned long long>(size_t(w.rows.npad));
   return w;
 }

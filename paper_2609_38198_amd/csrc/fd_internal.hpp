@@ -70,6 +70,9 @@ constexpr int TILE = 16;          // points per MFMA tile
 constexpr int WG_THREADS = 256;   // four wave64 per workgroup
 constexpr int ROW_PAD = 512;      // row packs: whole workgroups of 4 waves x 8 row tiles
 constexpr int COL_PAD = 32;       // column packs: whole pairs of 16-point tiles
+// Longest column range one workgroup of a product or row-sum plan streams
+// (tiles of 16 points); longer ranges are split.
+constexpr int64_t SPLIT_SPAN_TILES = 32768;
 
 inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 inline int64_t ceil_div(int64_t x, int64_t m) { return (x + m - 1) / m; }

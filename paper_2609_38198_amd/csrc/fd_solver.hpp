@@ -39,8 +39,8 @@ void degree_run(DegreeWs& w, const void* X, fd_dtype xt, int64_t N, int64_t D, i
                 bool pack, hipStream_t stream);
 
 // Row slots of a partial-sum buffer large enough for every plan with at most
-// npad rows (see plan_product).
-size_t part_rows_bound(int64_t npad);
+// npad rows and nc columns (see plan_product).
+size_t part_rows_bound(int64_t npad, int64_t nc);
 // Views of workspace carved for a larger problem, for n <= the carved size.
 PointPack pack_view(const PointPack& big, int64_t n, int64_t pad);
 DegreeWs degree_view(const DegreeWs& big, int64_t n);

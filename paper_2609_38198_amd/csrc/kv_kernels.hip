@@ -303,6 +303,50 @@ __device__ __forceinline__ void load_pair_b(ColPairB<DC, NCB>& cp, const uintx4*
 // rounded to float16 (nearest, two per instruction) and multiplied into the
 // split V on the float16 matrix cores; lane (g, p) holds K'[p][J0 + 4g + r]
 // and K'[p][J1 + 4g + r], its A-operand values k = 8g + 4u + r.
+template <int DC, bool DIAG>
+__device__ __forceinline__ halfx8 bf16_kpair(const uintx4 (&xa)[2][DC], const floatx4 (&aj)[2],
+                                             const uintx4 (&xb)[DC], float ci, float scale2,
+                                             int64_t jp, int64_t ib, int g, int p) {
+  floatx4 t[2];
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    t[u] = aj[u];
+#pragma unroll
+    for (int cc = 0; cc < DC; ++cc)
+      t[u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, xa[u][cc]),
+                                                     __builtin_bit_cast(bf16x8, xb[cc]), t[u], 0,
+                                                     0, 0);
+  }
+  float e[8];
+#pragma unroll
+  for (int u = 0; u < 2; ++u)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      e[4 * u + r] = fmaf(t[u][r], scale2, ci);
+      // the diagonal of one point set: K'_ii = 2^15 exactly
+      if (DIAG && 2 * jp + u == ib && 4 * g + r == p) e[4 * u + r] = 15.f;
+    }
+  halfx8 k;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const floatx2 kk = floatx2{__builtin_amdgcn_exp2f(e[2 * q]), __builtin_amdgcn_exp2f(e[2 * q + 1])};
+    const halfx2 hk = __builtin_convertvector(kk, halfx2);
+    k[2 * q] = hk[0];
+    k[2 * q + 1] = hk[1];
+  }
+  return k;
+}
+
+template <int NCB>
+__device__ __forceinline__ void bf16_kv(const halfx8& k, const VSplit (&v)[NCB],
+                                        floatx4 (&acc)[NCB]) {
+#pragma unroll
+  for (int cb = 0; cb < NCB; ++cb) {
+    acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(k, v[cb].hi, acc[cb], 0, 0, 0);
+    acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(k, v[cb].lo, acc[cb], 0, 0, 0);
+  }
+}
+
 template <int DC, int NCB, int NIB, bool DIAG>
 __device__ __forceinline__ void bf16_pair(const ColPairB<DC, NCB>& c, const uintx4 (&xbr)[NIB][DC],
                                           const float (&ci)[NIB], float scale2,
@@ -310,38 +354,8 @@ __device__ __forceinline__ void bf16_pair(const ColPairB<DC, NCB>& c, const uint
                                           int g, int p) {
 #pragma unroll
   for (int ib = 0; ib < NIB; ++ib) {
-    floatx4 t[2];
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      t[u] = c.aj[u];
-#pragma unroll
-      for (int cc = 0; cc < DC; ++cc)
-        t[u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, c.xa[u][cc]),
-                                                       __builtin_bit_cast(bf16x8, xbr[ib][cc]),
-                                                       t[u], 0, 0, 0);
-    }
-    float e[8];
-#pragma unroll
-    for (int u = 0; u < 2; ++u)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        e[4 * u + r] = fmaf(t[u][r], scale2, ci[ib]);
-        // the diagonal of one point set: K'_ii = 2^15 exactly
-        if (DIAG && 2 * jp + u == ib0 + ib && 4 * g + r == p) e[4 * u + r] = 15.f;
-      }
-    halfx8 k;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const floatx2 kk = floatx2{__builtin_amdgcn_exp2f(e[2 * q]), __builtin_amdgcn_exp2f(e[2 * q + 1])};
-      const halfx2 hk = __builtin_convertvector(kk, halfx2);
-      k[2 * q] = hk[0];
-      k[2 * q + 1] = hk[1];
-    }
-#pragma unroll
-    for (int cb = 0; cb < NCB; ++cb) {
-      acc[ib][cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(k, c.v[cb].hi, acc[ib][cb], 0, 0, 0);
-      acc[ib][cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(k, c.v[cb].lo, acc[ib][cb], 0, 0, 0);
-    }
+    const halfx8 k = bf16_kpair<DC, DIAG>(c.xa, c.aj, xbr[ib], ci[ib], scale2, jp, ib0 + ib, g, p);
+    bf16_kv<NCB>(k, c.v, acc[ib]);
   }
 }
 
@@ -349,7 +363,8 @@ __device__ __forceinline__ void bf16_pair(const ColPairB<DC, NCB>& c, const uint
 // registers and accumulates in ordinary VGPRs; the widest blocks take 1).
 template <int DC, int NCB, int NIB>
 constexpr int bf16_waves() {
-  return (NIB * NCB * 4 + NIB * DC * 4 + 2 * (DC * 8 + 8 + NCB * 8) > 200) ? 1 : 2;
+  constexpr int buffers = NCB >= 3 ? 1 : 2;
+  return (NIB * NCB * 4 + NIB * DC * 4 + buffers * (DC * 8 + 8 + NCB * 8) > 200) ? 1 : 2;
 }
 
 // One workgroup = 4 waves; wave w owns row tiles [ib0, ib0 + NIB).  Column
@@ -392,6 +407,56 @@ __attribute__((amdgpu_waves_per_eu(bf16_waves<DC, NCB, NIB>()))) void product_bf
       tot[wave][ib][cb][lane] = floatx4{0.f, 0.f, 0.f, 0.f};
     }
 
+  if constexpr (NCB >= 3) {
+    // Wide blocks: one buffer each for the exponent operands and for V.  A
+    // step first forms K' of all the wave's row tiles (then refills the
+    // exponent operands), then multiplies them into V (then refills V); each
+    // load has the other phase's work to land, and the registers saved by
+    // single buffering keep two waves per SIMD.
+    ColPairB<DC, NCB> c;
+    load_pair_b(c, xa, aj, vp, jp_begin, lane);
+#pragma unroll
+    for (int ib = 0; ib < NIB; ++ib) {
+#pragma unroll
+      for (int cc = 0; cc < DC; ++cc) asm volatile("" ::"v"(xbr[ib][cc]));
+      asm volatile("" ::"v"(ci[ib]));
+    }
+    int chunk = 0;
+    for (int64_t jp = jp_begin; jp < jp_end; ++jp) {
+      const int64_t jn = min(jp + 1, jp_end - 1);
+      halfx8 k[NIB];
+      if (diag && 2 * jp + 1 >= ib0 && 2 * jp < ib0 + NIB) {
+#pragma unroll
+        for (int ib = 0; ib < NIB; ++ib)
+          k[ib] = bf16_kpair<DC, true>(c.xa, c.aj, xbr[ib], ci[ib], scale2, jp, ib0 + ib, g, p);
+      } else {
+#pragma unroll
+        for (int ib = 0; ib < NIB; ++ib)
+          k[ib] = bf16_kpair<DC, false>(c.xa, c.aj, xbr[ib], ci[ib], scale2, jp, ib0 + ib, g, p);
+      }
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const int64_t jb = 2 * jn + t;
+#pragma unroll
+        for (int cc = 0; cc < DC; ++cc) c.xa[t][cc] = xa[(jb * DC + cc) * 64 + lane];
+        c.aj[t] = aj[jb * 64 + lane];
+      }
+#pragma unroll
+      for (int ib = 0; ib < NIB; ++ib) bf16_kv<NCB>(k[ib], c.v, acc[ib]);
+#pragma unroll
+      for (int cb = 0; cb < NCB; ++cb) c.v[cb] = vp[(jn * NCB + cb) * 64 + lane];
+      if (++chunk == CHUNK_TILES / 2) {
+        chunk = 0;
+#pragma unroll
+        for (int ib = 0; ib < NIB; ++ib)
+#pragma unroll
+          for (int cb = 0; cb < NCB; ++cb) {
+            tot[wave][ib][cb][lane] += acc[ib][cb];
+            acc[ib][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
+          }
+      }
+    }
+  } else {
   auto step = [&](const ColPairB<DC, NCB>& c, int64_t jp) {
     if (diag && 2 * jp + 1 >= ib0 && 2 * jp < ib0 + NIB)
       bf16_pair<DC, NCB, NIB, true>(c, xbr, ci, scale2, acc, jp, ib0, g, p);
@@ -430,6 +495,7 @@ __attribute__((amdgpu_waves_per_eu(bf16_waves<DC, NCB, NIB>()))) void product_bf
           acc[ib][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
         }
     }
+  }
   }
 
 #pragma unroll
@@ -626,6 +692,10 @@ KVPlan plan_tiles(int64_t Nr, int64_t Nc, int dp, int b, int nib) {
   const int64_t target = 2048;
   int64_t ns = std::max<int64_t>(1, ceil_div(target, p.nrt));
   ns = std::min<int64_t>(ns, std::max<int64_t>(1, p.njb / 8));
+  // at most SPLIT_SPAN_TILES column tiles per workgroup: the workgroups that
+  // run together on an XCD start a split together and drift apart as they go;
+  // over a shorter span they stay close enough to share column tiles in L2
+  ns = std::max<int64_t>(ns, ceil_div(p.njb, SPLIT_SPAN_TILES));
   ns = std::min<int64_t>(ns, 64);
   // splits hold an even number of column tiles (the split product takes them in pairs)
   p.jb_per_split = round_up(ceil_div(p.njb, ns), 2);

@@ -87,7 +87,8 @@ static SolverWs carve_solver_ws(Arena& a, int64_t N, int64_t D, int b, int mm_ca
   w.prod.cols = w.deg.cols;
   w.prod.vp = a.fspan(size_t(w.prod.cols.npad) * w.prod.plan.ncb * 16);
   w.prod.vscale = a.fspan(128);
-  w.prod.part = a.fspan(part_rows_bound(w.prod.rows.npad) * w.prod.plan.ncb * 16);
+  w.prod.part = a.fspan(part_rows_bound(w.prod.rows.npad, N) * w.prod.plan.ncb * 16);
+  w.prod.tmp = a.fspan(size_t(N));  // single-column products (block width 1)
   w.d = a.take<float>(size_t(N));
   w.s = a.take<float>(size_t(N));
   w.s_off = a.take<double>(1);

@@ -163,3 +163,13 @@ def test_bf16_input_eigenpairs():
     e = fd.fd_block_lanczos(to_dev(s.X, dev), beta, 8, 8)
     assert np.max(np.abs(np.asarray(e.evals) - sp.evals[:8])) <= 2e-3
     assert max(e.residuals) <= 1e-5
+
+
+def test_block_width_one():
+    # b = 1 runs every product through the single-column path
+    w = inputs.torus6_paper(1024)
+    dev = device()
+    case("lanczos T6 paper N=1024 beta=0.5 b=1 k=3")
+    e = fd.fd_block_lanczos(to_dev(w.X, dev), 0.5, 3, 1)
+    ref = oe.spectrum(w.X.astype(np.float64), 0.5, 0.5, 3)
+    assert np.all(np.abs(np.asarray(e.evals) - ref.evals) <= np.maximum(1e-5 * np.abs(ref.evals), 1e-6))
