@@ -94,7 +94,8 @@ void fd_lanczos_default_opts(fd_lanczos_opts* opts);
  *   op = FD_OP_KERNEL_MATMUL: Nr output rows, Nc columns, D, b; k ignored.
  *   op = FD_OP_DEGREE:        Nr = Nc = N, D; b, k ignored.
  *   op = FD_OP_BLOCK_LANCZOS: Nr = Nc = N, D, b, k, opts (NULL = defaults).
- *   op = FD_OP_BETA_FLOW:     Nr = Nc = N, D, b, k, opts (NULL = defaults).
+ *   op = FD_OP_BETA_FLOW:     Nr = Nc = N, D, b, k, opts (NULL = defaults); also the
+ *                             size for fd_beta_flow_cascade.
  *   op = FD_OP_CONTINUATION:  Nr = largest n of the schedule, Nc = number of steps,
  *                             D, b, k (<= 64), opts.
  * Returns 0 for arguments the entry point would reject. */
@@ -216,7 +217,8 @@ typedef struct fd_flow_probe {
   int32_t role;        /* 0 dyadic probe, 1 vertex probe, 2 solve at the selected bandwidth */
   int32_t admissible;  /* g_P > kappa_P eta */
   int32_t status;      /* status of the probe's eigensolve (FD_OK or FD_ERR_NOT_CONVERGED) */
-  int32_t block_matvecs, nconv, reserved;
+  int32_t block_matvecs, nconv;
+  int32_t level;       /* cascade level of the probe (0 for fd_beta_flow) */
 } fd_flow_probe;
 
 typedef enum fd_flow_exit { FD_FLOW_BRACKET = 0, FD_FLOW_WALL = 1, FD_FLOW_BUDGET = 2 } fd_flow_exit;
@@ -241,6 +243,27 @@ fd_status fd_beta_flow(const void* X, fd_dtype xt, int64_t N, int64_t D, int64_t
                        const fd_lanczos_opts* opts, fd_flow_probe* probes, int64_t* nprobes,
                        double* beta_x, int32_t* exit_reason, double* evals, float* evecs,
                        float* psi, void* ws, size_t ws_bytes, void* stream);
+
+/* Precision cascade of the flow (Sec. 2.3, last paragraph): the same points
+ * supplied in several data types, lowest precision first.  Level 0 runs the
+ * flow of fd_beta_flow on Xs[0] (from beta_start, or beta_0 of eq. beta0);
+ * each later level runs it on Xs[l] starting at the previous level's achieved
+ * bandwidth, its first probe warm-started from the previous level's Markov
+ * eigenvectors.  Each level uses the eta of its own data type (fp32 1e-7,
+ * bf16 8e-3) unless fopts->eta > 0 fixes one for all.  The achieved bandwidth
+ * and the eigenpairs are those of the last level.
+ *   Xs, xts, ldxs: nlevels (1..4) device arrays of the same N x D points, their
+ *     dtypes and leading dimensions (host arrays of pointers / values).
+ *   probes: host array of at least nlevels * (max_probes + 2) records, each
+ *     tagged with its level; other arguments and returns as fd_beta_flow
+ *     (FD_ERR_PERRON_WALL when the first probe of any level is past the wall). */
+fd_status fd_beta_flow_cascade(const void* const* Xs, const fd_dtype* xts, const int64_t* ldxs,
+                               int32_t nlevels, int64_t N, int64_t D, float alpha, int64_t b,
+                               int64_t k, const fd_flow_opts* fopts,
+                               const fd_lanczos_opts* opts, fd_flow_probe* probes,
+                               int64_t* nprobes, double* beta_x, int32_t* exit_reason,
+                               double* evals, float* evecs, float* psi, void* ws, size_t ws_bytes,
+                               void* stream);
 
 /* ---- diagnostics: kernel timing with HIP events ----
  * When enabled, every launch of the fused product kernel (FD_KERNEL_PRODUCT)

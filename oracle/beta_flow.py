@@ -21,6 +21,10 @@ Sec. 2.3 ("beta-function flow"), in the paper's order:
   probe is the achieved bandwidth;
 * intrinsic-dimension diagnostic d_hat = -2 dlog S_off / dlog beta over a
   dyadic pair (eq. dhat).
+* precision cascade (last paragraph of Sec. 2.3): with several data types,
+  one sweep per type, lowest precision first; each later sweep starts at the
+  bandwidth the previous one selected, and the last sweep's selection is
+  the result.
 
 Readings where the text leaves a choice:
 * ``k`` counts the Perron pair (k - 1 nontrivial modes enter V_bias);
@@ -171,3 +175,19 @@ def flow(probe: Callable[[float], Probe], N: int, beta_start: float,
         F.final = F.probes[-1]
     F.beta_x = F.final.beta if F.final is not None else float("nan")
     return F
+
+
+def cascade(levels: List[Callable[[float], Probe]], N: int, beta_start: float,
+            max_probes: int = 24) -> List[Flow]:
+    """Precision cascade: one flow per probe callable (one data type each,
+    lowest precision first), each from the previous flow's achieved
+    bandwidth.  Returns the flows run; the last one holds the result."""
+    flows: List[Flow] = []
+    beta = beta_start
+    for probe in levels:
+        F = flow(probe, N, beta, max_probes)
+        flows.append(F)
+        if not F.probes:
+            break
+        beta = F.beta_x
+    return flows

@@ -35,6 +35,7 @@ EXPORTS = (
     "fd_lanczos_default_opts", "fd_workspace_size", "fd_kernel_matmul", "fd_degree",
     "fd_block_lanczos", "fd_continuation", "fd_last_error", "fd_status_string",
     "fd_profile_enable", "fd_profile_read", "fd_flow_default_opts", "fd_beta_flow",
+    "fd_beta_flow_cascade",
 )
 FD_KERNEL_PRODUCT, FD_KERNEL_ROWSUM = 0, 1
 
@@ -77,7 +78,7 @@ class FlowProbe(ctypes.Structure):
                 ("d_hat", ctypes.c_double), ("seconds", ctypes.c_double),
                 ("role", ctypes.c_int32), ("admissible", ctypes.c_int32),
                 ("status", ctypes.c_int32), ("block_matvecs", ctypes.c_int32),
-                ("nconv", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+                ("nconv", ctypes.c_int32), ("level", ctypes.c_int32)]
 
     def as_dict(self) -> dict:
         return {f: getattr(self, f) for f, _ in self._fields_ if f != "reserved"}
@@ -127,6 +128,13 @@ def load(path: str = LIB_PATH):
         ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_double),
         ctypes.POINTER(ctypes.c_int32), _c_p, _c_p, _c_p, _c_p, ctypes.c_size_t, _c_p]
     lib.fd_beta_flow.restype = ctypes.c_int
+    lib.fd_beta_flow_cascade.argtypes = [
+        ctypes.POINTER(_c_p), ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_int64),
+        ctypes.c_int32, _c_i64, _c_i64, ctypes.c_float, _c_i64, _c_i64,
+        ctypes.POINTER(FlowOpts), ctypes.POINTER(LanczosOpts), ctypes.POINTER(FlowProbe),
+        ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_double),
+        ctypes.POINTER(ctypes.c_int32), _c_p, _c_p, _c_p, _c_p, ctypes.c_size_t, _c_p]
+    lib.fd_beta_flow_cascade.restype = ctypes.c_int
     lib.fd_last_error.argtypes = []
     lib.fd_last_error.restype = ctypes.c_char_p
     lib.fd_status_string.argtypes = [ctypes.c_int]
@@ -408,6 +416,49 @@ def fd_beta_flow(X: torch.Tensor, k: int, b: int, alpha: float = 0.5,
                                  ctypes.byref(fo), ctypes.byref(o), recs, ctypes.byref(nrec),
                                  ctypes.byref(bx), ctypes.byref(why), evals, _ptr(evecs),
                                  _ptr(psi), _ptr(ws), ws.numel(), _stream(dev)), allow)
+    return Flow([recs[i].as_dict() for i in range(nrec.value)], bx.value,
+                FLOW_EXIT.get(why.value, str(why.value)), [evals[i] for i in range(k)], evecs,
+                psi, st)
+
+
+def fd_beta_flow_cascade(Xs: Sequence[torch.Tensor], k: int, b: int, alpha: float = 0.5,
+                         fopts: Optional[FlowOpts] = None, opts: Optional[LanczosOpts] = None,
+                         want_psi: bool = True, ws: Optional[torch.Tensor] = None,
+                         allow=(FD_OK,)) -> Flow:
+    """Precision cascade of the flow: the same points in each dtype of Xs, lowest first."""
+    lib = load()
+    Xs = list(Xs)
+    if not 1 <= len(Xs) <= 4:
+        raise ValueError("the cascade takes 1 to 4 levels")
+    for X in Xs:
+        _check_dev(X)
+        if X.dim() != 2 or X.stride(1) != 1 or X.shape != Xs[0].shape:
+            raise ValueError("every level must be the same row-major N x D points")
+    N, D = Xs[0].shape
+    dev = Xs[0].device
+    fo = fopts if fopts is not None else flow_default_opts()
+    o = opts if opts is not None else default_opts()
+    cap = len(Xs) * (int(fo.max_probes) + 2)
+    recs = (FlowProbe * cap)()
+    nrec = ctypes.c_int64(0)
+    bx = ctypes.c_double(0.0)
+    why = ctypes.c_int32(0)
+    evals = (ctypes.c_double * k)()
+    evecs = torch.empty((N, k), dtype=torch.float32, device=dev)
+    psi = torch.empty((N, k), dtype=torch.float32, device=dev) if want_psi else None
+    need = fd_workspace_size(FD_OP_BETA_FLOW, N, N, D, b, k, o)
+    if need == 0:
+        raise FdError(1, "unsupported sizes")
+    if ws is None or ws.numel() < need:
+        ws = _workspace(need, dev)
+    ptrs = (_c_p * len(Xs))(*[X.data_ptr() for X in Xs])
+    codes = (ctypes.c_int * len(Xs))(*[_dtype_code(X) for X in Xs])
+    lds = (ctypes.c_int64 * len(Xs))(*[X.stride(0) for X in Xs])
+    st = _check(lib.fd_beta_flow_cascade(ptrs, codes, lds, len(Xs), N, D, float(alpha), b, k,
+                                         ctypes.byref(fo), ctypes.byref(o), recs,
+                                         ctypes.byref(nrec), ctypes.byref(bx), ctypes.byref(why),
+                                         evals, _ptr(evecs), _ptr(psi), _ptr(ws), ws.numel(),
+                                         _stream(dev)), allow)
     return Flow([recs[i].as_dict() for i in range(nrec.value)], bx.value,
                 FLOW_EXIT.get(why.value, str(why.value)), [evals[i] for i in range(k)], evecs,
                 psi, st)

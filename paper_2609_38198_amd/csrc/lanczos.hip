@@ -598,8 +598,9 @@ static double flow_vertex(const double x[3], const double y[3]) {
   return std::min(std::max(v, x[0]), x[2]);
 }
 
-static fd_flow_probe flow_record(const FlowProbe& p) {
+static fd_flow_probe flow_record(const FlowProbe& p, int level) {
   fd_flow_probe r{};
+  r.level = level;
   r.beta = p.beta;
   r.s_off = p.s_off;
   r.gap_perron = p.gap;
@@ -616,6 +617,112 @@ static fd_flow_probe flow_record(const FlowProbe& p) {
   r.block_matvecs = p.matvecs;
   r.nconv = p.nconv;
   return r;
+}
+
+
+// beta_0 of eq. beta0 from the centred data: min(0.1, 1 / (2 mean ||x - mean||^2)).
+static double flow_beta0(FlowWs& f, const void* X, fd_dtype xt, int64_t N, int64_t D,
+                         int64_t ldx, hipStream_t st) {
+  const double ms = xt == FD_BF16
+                        ? centred_mean_sq(f, static_cast<const uint16_t*>(X), N, D, ldx, st)
+                        : centred_mean_sq(f, static_cast<const float*>(X), N, D, ldx, st);
+  return ms > 0.0 ? std::min(0.1, 1.0 / (2.0 * ms)) : 0.1;
+}
+
+struct FlowOutcome {
+  bool any = false;  // at least one admissible probe
+  int reason = FD_FLOW_BUDGET;
+  FlowProbe fin;     // the probe at the achieved bandwidth
+};
+
+// One sweep of the flow on X from `beta` (Sec. 2.3).  warm: psi_keep already
+// holds Markov vectors to start the first probe from.  Records are appended
+// to `out` with the given level.  On return with any == true, sw.Q holds the
+// eigenvectors of the solve at fin.beta and psi_keep its Markov vectors.
+static FlowOutcome run_flow(FlowWs& f, const void* X, fd_dtype xt, int64_t N, int64_t D,
+                            int64_t ldx, double alpha, int bb, int kk, double beta, bool warm,
+                            const FlowParams& fp, const fd_lanczos_opts& o, int max_probes,
+                            int level, std::vector<fd_flow_probe>& out, hipStream_t st) {
+  FlowOutcome res;
+  std::vector<FlowProbe> pr;  // admissible dyadic probes
+  bool have_keep = warm;      // psi_keep holds the latest admissible probe (or the warm start)
+  double in_q = -1.0;         // bandwidth whose Ritz vectors are in sw.Q
+  int reason = FD_FLOW_BUDGET;
+  FlowProbe fin;
+  bool fin_in_q = false;
+  const uint64_t lseed = uint64_t(level) * 1000003u;
+  for (int t = 0; t < max_probes; ++t) {
+    FlowProbe p = flow_probe(f, X, xt, N, D, ldx, beta, alpha, bb, kk,
+                             have_keep ? f.psi_keep : nullptr, f.psi_new, o, fp, 0,
+                             lseed + uint64_t(t) * 7919u, st);
+    in_q = beta;
+    if (!p.admissible) {
+      out.push_back(flow_record(p, level));
+      reason = FD_FLOW_WALL;
+      break;
+    }
+    if (!pr.empty()) {
+      flow_complete(pr.back(), p, N);
+      out.back() = flow_record(pr.back(), level);
+    }
+    pr.push_back(p);
+    out.push_back(flow_record(p, level));
+    std::swap(f.psi_keep, f.psi_new);
+    have_keep = true;
+    std::vector<int> done;
+    for (int i = 0; i < int(pr.size()); ++i)
+      if (pr[i].complete()) done.push_back(i);
+    const int nd = int(done.size());
+    if (nd >= 3 && flow_brackets(pr[done[nd - 3]], pr[done[nd - 2]], pr[done[nd - 1]])) {
+      const FlowProbe& pa = pr[done[nd - 3]];
+      const FlowProbe& pm = pr[done[nd - 2]];
+      const FlowProbe& pc = pr[done[nd - 1]];
+      const double xs[3] = {std::log(pa.beta), std::log(pm.beta), std::log(pc.beta)};
+      const double ys[3] = {pa.v_total, pm.v_total, pc.v_total};
+      const double bv = std::exp(flow_vertex(xs, ys));
+      FlowProbe v = flow_probe(f, X, xt, N, D, ldx, bv, alpha, bb, kk, f.psi_keep, f.psi_new, o,
+                               fp, 1, lseed + 104729u, st);
+      in_q = bv;
+      out.push_back(flow_record(v, level));
+      reason = FD_FLOW_BRACKET;
+      if (v.admissible) {
+        fin = v;
+        fin_in_q = true;
+      } else {
+        fin = pm;
+      }
+      break;
+    }
+    beta *= 2.0;
+  }
+  res.reason = reason;
+  if (pr.empty()) return res;
+  res.any = true;
+  if (reason != FD_FLOW_BRACKET) {
+    fin = pr.back();
+    if (reason == FD_FLOW_BUDGET) {
+      for (const FlowProbe& q : pr)
+        if (q.complete() && (!fin.complete() || q.v_total < fin.v_total)) fin = q;
+    }
+    fin_in_q = in_q == fin.beta;
+  }
+  if (!fin_in_q) {
+    // the selected probe's vectors were overwritten: solve again from the
+    // latest admissible probe's Markov vectors
+    FlowProbe r = flow_probe(f, X, xt, N, D, ldx, fin.beta, alpha, bb, kk, f.psi_keep,
+                             f.psi_new, o, fp, 2, lseed + 15485863u, st);
+    out.push_back(flow_record(r, level));
+    fin.evals = r.evals;
+    fin.converged = r.converged;
+    fin.nconv = r.nconv;
+    std::swap(f.psi_keep, f.psi_new);
+  } else if (fin.role == 0) {
+    // the latest dyadic probe: its Markov vectors were moved to psi_keep
+  } else {
+    std::swap(f.psi_keep, f.psi_new);
+  }
+  res.fin = fin;
+  return res;
 }
 
 }  // namespace fd
@@ -879,64 +986,11 @@ fd_status fd_beta_flow(const void* X, fd_dtype xt, int64_t N, int64_t D, int64_t
     const int kk = int(k), bb = int(b);
 
     double beta = fo.beta_start;
-    if (beta <= 0.0) {
-      const double ms = xt == FD_BF16
-                            ? centred_mean_sq(f, static_cast<const uint16_t*>(X), N, D, ldx, st)
-                            : centred_mean_sq(f, static_cast<const float*>(X), N, D, ldx, st);
-      beta = ms > 0.0 ? std::min(0.1, 1.0 / (2.0 * ms)) : 0.1;
-    }
-    std::vector<FlowProbe> pr;       // admissible dyadic probes
+    if (beta <= 0.0) beta = flow_beta0(f, X, xt, N, D, ldx, st);
     std::vector<fd_flow_probe> out;  // records in the order run
-    bool have_keep = false;          // psi_keep holds the latest admissible probe
-    double in_q = -1.0;              // bandwidth whose Ritz vectors are in sw.Q
-    int reason = FD_FLOW_BUDGET;
-    FlowProbe fin;
-    bool fin_in_q = false;
-    for (int t = 0; t < fo.max_probes; ++t) {
-      FlowProbe p = flow_probe(f, X, xt, N, D, ldx, beta, alpha, bb, kk,
-                               have_keep ? f.psi_keep : nullptr, f.psi_new, o, fp, 0,
-                               uint64_t(t) * 7919u, st);
-      in_q = beta;
-      if (!p.admissible) {
-        out.push_back(flow_record(p));
-        reason = FD_FLOW_WALL;
-        break;
-      }
-      if (!pr.empty()) {
-        flow_complete(pr.back(), p, N);
-        out.back() = flow_record(pr.back());
-      }
-      pr.push_back(p);
-      out.push_back(flow_record(p));
-      std::swap(f.psi_keep, f.psi_new);
-      have_keep = true;
-      std::vector<int> done;
-      for (int i = 0; i < int(pr.size()); ++i)
-        if (pr[i].complete()) done.push_back(i);
-      const int nd = int(done.size());
-      if (nd >= 3 && flow_brackets(pr[done[nd - 3]], pr[done[nd - 2]], pr[done[nd - 1]])) {
-        const FlowProbe& pa = pr[done[nd - 3]];
-        const FlowProbe& pm = pr[done[nd - 2]];
-        const FlowProbe& pc = pr[done[nd - 1]];
-        const double xs[3] = {std::log(pa.beta), std::log(pm.beta), std::log(pc.beta)};
-        const double ys[3] = {pa.v_total, pm.v_total, pc.v_total};
-        const double bv = std::exp(flow_vertex(xs, ys));
-        FlowProbe v = flow_probe(f, X, xt, N, D, ldx, bv, alpha, bb, kk, f.psi_keep, f.psi_new,
-                                 o, fp, 1, 104729u, st);
-        in_q = bv;
-        out.push_back(flow_record(v));
-        reason = FD_FLOW_BRACKET;
-        if (v.admissible) {
-          fin = v;
-          fin_in_q = true;
-        } else {
-          fin = pm;
-        }
-        break;
-      }
-      beta *= 2.0;
-    }
-    if (pr.empty()) {
+    const FlowOutcome R = run_flow(f, X, xt, N, D, ldx, alpha, bb, kk, beta, false, fp, o,
+                                   fo.max_probes, 0, out, st);
+    if (!R.any) {
       // the first probe is already past the wall: nothing admissible to return
       for (size_t i = 0; i < out.size(); ++i) probes[i] = out[i];
       *nprobes = int64_t(out.size());
@@ -945,29 +999,8 @@ fd_status fd_beta_flow(const void* X, fd_dtype xt, int64_t N, int64_t D, int64_t
       set_error("the first probe is already past the Perron wall (g_P <= kappa_P eta)");
       return FD_ERR_PERRON_WALL;
     }
-    if (reason != FD_FLOW_BRACKET) {
-      fin = pr.back();
-      if (reason == FD_FLOW_BUDGET) {
-        for (const FlowProbe& q : pr)
-          if (q.complete() && (!fin.complete() || q.v_total < fin.v_total)) fin = q;
-      }
-      fin_in_q = in_q == fin.beta;
-    }
-    if (!fin_in_q) {
-      // the selected probe's vectors were overwritten: solve again from the
-      // latest admissible probe's Markov vectors
-      FlowProbe r = flow_probe(f, X, xt, N, D, ldx, fin.beta, alpha, bb, kk, f.psi_keep,
-                               f.psi_new, o, fp, 2, 15485863u, st);
-      out.push_back(flow_record(r));
-      fin.evals = r.evals;
-      fin.converged = r.converged;
-      fin.nconv = r.nconv;
-      std::swap(f.psi_keep, f.psi_new);
-    } else if (fin.role == 0) {
-      // the latest dyadic probe: its Markov vectors were moved to psi_keep
-    } else {
-      std::swap(f.psi_keep, f.psi_new);
-    }
+    const FlowProbe& fin = R.fin;
+    const int reason = R.reason;
     // the selected solve's eigenvectors are in sw.Q, its Markov vectors in psi_keep
     const SolverLayout lz = solver_layout(N, bb, kk, o);
     copy_cols(f.sw.Q, lz.mm, evecs, kk, N, kk, nullptr, 0.0, st);
@@ -978,6 +1011,95 @@ fd_status fd_beta_flow(const void* X, fd_dtype xt, int64_t N, int64_t D, int64_t
     *nprobes = int64_t(out.size());
     *beta_x = fin.beta;
     *exit_reason = reason;
+    if (!fin.converged) {
+      set_error("the eigensolve at the selected bandwidth stopped before all k pairs converged");
+      return FD_ERR_NOT_CONVERGED;
+    }
+    set_error("");
+    return FD_OK;
+  } catch (const Error& e) {
+    set_error(e.msg);
+    return e.status;
+  } catch (const std::exception& e) {
+    set_error(std::string("internal error: ") + e.what());
+    return FD_ERR_HIP;
+  }
+}
+
+fd_status fd_beta_flow_cascade(const void* const* Xs, const fd_dtype* xts, const int64_t* ldxs,
+                               int32_t nlevels, int64_t N, int64_t D, float alpha, int64_t b,
+                               int64_t k, const fd_flow_opts* fopts, const fd_lanczos_opts* opts,
+                               fd_flow_probe* probes, int64_t* nprobes, double* beta_x,
+                               int32_t* exit_reason, double* evals, float* evecs, float* psi,
+                               void* ws, size_t ws_bytes, void* stream) {
+  try {
+    FD_REQUIRE(Xs != nullptr && xts != nullptr && ldxs != nullptr && nlevels >= 1 && nlevels <= 4,
+               FD_ERR_INVALID_ARG, "the cascade needs 1 to 4 levels");
+    for (int l = 0; l < nlevels; ++l) check_points(Xs[l], xts[l], N, D, ldxs[l], "X level");
+    FD_REQUIRE(alpha >= 0.f && alpha <= 1.f, FD_ERR_INVALID_ARG, "alpha must be in [0, 1]");
+    FD_REQUIRE(b >= 1 && b <= MAX_B, FD_ERR_INVALID_ARG, "b must be in [1, 64]");
+    FD_REQUIRE(k >= 2 && k <= N, FD_ERR_INVALID_ARG, "k must be in [2, N]");
+    FD_REQUIRE(probes != nullptr && nprobes != nullptr && beta_x != nullptr &&
+                   exit_reason != nullptr && evals != nullptr && evecs != nullptr,
+               FD_ERR_INVALID_ARG, "NULL output");
+    fd_flow_opts fo;
+    fd_flow_default_opts(&fo);
+    if (fopts != nullptr) fo = *fopts;
+    FD_REQUIRE(fo.max_probes >= 1 && fo.max_probes <= 64, FD_ERR_INVALID_ARG,
+               "max_probes must be in [1, 64]");
+    FD_REQUIRE(std::isfinite(fo.kappa) && fo.kappa > 0.0 && std::isfinite(fo.p) && fo.p > 0.0,
+               FD_ERR_INVALID_ARG, "kappa and p must be finite and > 0");
+    FD_REQUIRE(std::isfinite(fo.beta_start) && std::isfinite(fo.eta), FD_ERR_INVALID_ARG,
+               "beta_start and eta must be finite");
+    fd_lanczos_opts o;
+    fd_lanczos_default_opts(&o);
+    if (opts != nullptr) o = *opts;
+    validate_opts(o);
+    const SolverLayout lay = solver_layout(N, int(b), int(k), o);
+    FD_REQUIRE(lay.dense || k <= lay.kk, FD_ERR_INVALID_ARG, "k too large for the basis");
+    Arena m;
+    m.measuring = true;
+    carve_flow(m, N, D, int(b), int(k), o);
+    check_workspace(ws, ws_bytes, m.used);
+    Arena a;
+    a.base = static_cast<char*>(ws);
+    a.cap = ws_bytes;
+    FlowWs f = carve_flow(a, N, D, int(b), int(k), o);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const int kk = int(k), bb = int(b);
+
+    std::vector<fd_flow_probe> out;
+    FlowOutcome R;
+    double beta = fo.beta_start;
+    for (int l = 0; l < nlevels; ++l) {
+      const void* X = Xs[l];
+      const fd_dtype xt = xts[l];
+      const FlowParams fp{fo.eta > 0.0 ? fo.eta : (xt == FD_BF16 ? 8e-3 : 1e-7), fo.kappa, fo.p};
+      // level 0 starts from beta_0 (or beta_start); every later level from
+      // the previous level's achieved bandwidth and Markov vectors
+      if (l == 0 && beta <= 0.0) beta = flow_beta0(f, X, xt, N, D, ldxs[l], st);
+      R = run_flow(f, X, xt, N, D, ldxs[l], alpha, bb, kk, beta, l > 0, fp, o, fo.max_probes, l,
+                   out, st);
+      if (!R.any) {
+        for (size_t i = 0; i < out.size(); ++i) probes[i] = out[i];
+        *nprobes = int64_t(out.size());
+        *beta_x = NAN;
+        *exit_reason = FD_FLOW_WALL;
+        set_error("the first probe of cascade level " + std::to_string(l) +
+                  " is already past the Perron wall (g_P <= kappa_P eta)");
+        return FD_ERR_PERRON_WALL;
+      }
+      beta = R.fin.beta;
+    }
+    const FlowProbe& fin = R.fin;
+    copy_cols(f.sw.Q, lay.mm, evecs, kk, N, kk, nullptr, 0.0, st);
+    if (psi != nullptr) copy_cols(f.psi_keep, kk, psi, kk, N, kk, nullptr, 0.0, st);
+    FD_HIP_CHECK(hipStreamSynchronize(st));
+    for (int i = 0; i < kk; ++i) evals[i] = fin.evals[i];
+    for (size_t i = 0; i < out.size(); ++i) probes[i] = out[i];
+    *nprobes = int64_t(out.size());
+    *beta_x = fin.beta;
+    *exit_reason = R.reason;
     if (!fin.converged) {
       set_error("the eigensolve at the selected bandwidth stopped before all k pairs converged");
       return FD_ERR_NOT_CONVERGED;

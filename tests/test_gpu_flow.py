@@ -108,3 +108,59 @@ def test_first_probe_past_the_wall_reports_it():
     got = fd.fd_beta_flow(to_dev(X, device()), 4, 4, fopts=fo, allow=(0, 6))
     assert got.status == 6 and got.reason == "wall"
     assert len(got.probes) == 1 and not got.probes[0]["admissible"]
+
+
+def compare_probes_bf16(gpu, ref):
+    # bfloat16 level: the product rounds K' to float16, so eigenvalues carry
+    # the bf16-input bar (2e-3 absolute, as in the bf16 eigensolver test):
+    # the Perron gap to 4e-3, -log(lambda_j / lambda_0) to 2e-3 / lambda_j;
+    # the normalisation passes keep S_off to 1e-5
+    assert len(gpu) == len(ref.probes)
+    for g, r in zip(gpu, ref.probes):
+        assert g["beta"] == pytest.approx(r.beta, rel=1e-12)
+        assert g["s_off"] == pytest.approx(r.s_off, rel=1e-5)
+        assert abs(g["gap_perron"] - r.gap) <= 4e-3
+        lam_min = float(np.min(r.evals[1:]))
+        assert abs(g["v_bias"] - r.v_bias) <= 4e-3 / lam_min
+
+
+def test_precision_cascade_bf16_then_fp32_like_the_oracle():
+    # Sec. 2.3, last paragraph: a bf16 sweep first (eta 8e-3: its wall comes
+    # early), then an fp32 sweep from the bandwidth it selected
+    w = inputs.torus2()
+    bits = inputs.f32_to_bf16_bits(w.X)
+    Xb = inputs.bf16_bits_to_f64(bits)
+    k, b = 16, 8
+    dev = device()
+    case("beta flow cascade bf16 -> fp32 torus2 N=2048 k=16 b=8")
+    got = fd.fd_beta_flow_cascade([to_dev(bits, dev), to_dev(w.X, dev)], k, b, alpha=0.5,
+                                  fopts=fd.flow_default_opts(max_probes=12))
+    lv0 = [p for p in got.probes if p["level"] == 0]
+    lv1 = [p for p in got.probes if p["level"] == 1]
+    ref0 = bf.flow(bf.dense_probe(Xb, 0.5, k, "bf16"), w.N, bf.beta0(Xb), max_probes=12)
+    assert ref0.reason == "wall"
+    compare_probes_bf16([p for p in lv0 if p["role"] == 0 and p["admissible"]], ref0)
+    walls = [p for p in lv0 if p["role"] == 0 and not p["admissible"]]
+    assert len(walls) == 1
+    # level 1 starts at level 0's selection, warm
+    beta_x0 = lv1[0]["beta"]
+    assert beta_x0 == pytest.approx(ref0.beta_x, rel=1e-12)
+    ref1 = bf.flow(bf.dense_probe(w.X, 0.5, k), w.N, beta_x0, max_probes=12)
+    assert got.reason == ref1.reason == "bracket"
+    compare_probes([p for p in lv1 if p["role"] == 0 and p["admissible"]], ref1)
+    assert got.beta_x == pytest.approx(ref1.beta_x, rel=1e-3)
+    sp = oe.spectrum(w.X, got.beta_x, 0.5, k)
+    tol = np.maximum(1e-5 * np.abs(sp.evals), 1e-6)
+    assert np.all(np.abs(np.asarray(got.evals) - sp.evals) <= tol)
+
+
+def test_single_level_cascade_equals_the_flow():
+    w = inputs.torus2()
+    dev = device()
+    case("beta flow cascade one level = flow, torus2 budget 3")
+    fo = fd.flow_default_opts(max_probes=3)
+    a = fd.fd_beta_flow_cascade([to_dev(w.X, dev)], 8, 8, alpha=0.5, fopts=fo)
+    c = fd.fd_beta_flow(to_dev(w.X, dev), 8, 8, alpha=0.5, fopts=fo)
+    assert a.beta_x == c.beta_x and a.reason == c.reason
+    assert [p["beta"] for p in a.probes] == [p["beta"] for p in c.probes]
+    assert a.evals == c.evals

@@ -130,3 +130,36 @@ def test_flow_on_two_torus_heat_regime():
         assert p.d_hat == pytest.approx(2.0, rel=0.1)
     for a, c in zip(heat, heat[1:]):
         assert a.v_bias / c.v_bias == pytest.approx(2.0, rel=0.15)
+
+
+def test_cascade_chains_levels_from_the_previous_selection():
+    # level 0 (bf16: kappa * eta = 0.08) stops at its wall; level 1 (fp32)
+    # starts at level 0's achieved bandwidth and continues to a bracket
+    N = 1000
+    vb = [4.0, 2.0, 1.0, 0.5, 0.25, 0.12, 0.06]
+    soff = [N * 400 / 2 ** i for i in range(4)] + [N * 400 / 2 ** 3 / 8 ** j for j in range(1, 4)]
+    gaps = [0.5, 0.3, 0.05, 0.02, 0.01, 0.01, 0.01]
+
+    def mock(dtype):
+        def probe(beta):
+            i = max(0, min(int(round(math.log2(beta / 0.1))), len(vb) - 1))
+            ev = np.array([1.0, 1.0 - gaps[i], math.exp(-vb[i]), math.exp(-vb[i])])
+            return bf.make_probe(beta, ev, soff[i], dtype)
+        return probe
+
+    flows = bf.cascade([mock("bf16"), mock("fp32")], N, 0.1, max_probes=7)
+    lo, hi = flows
+    assert lo.reason == "wall" and lo.beta_x == pytest.approx(0.2)
+    assert hi.probes[0].beta == pytest.approx(lo.beta_x)
+    alone = bf.flow(mock("fp32"), N, lo.beta_x, max_probes=7)
+    assert hi.beta_x == pytest.approx(alone.beta_x) and hi.reason == alone.reason
+
+
+def test_single_level_cascade_is_the_flow():
+    from paper_2609_38198_amd import inputs
+    w = inputs.torus2()
+    probe = bf.dense_probe(w.X, 0.5, 8)
+    (F,) = bf.cascade([probe], w.N, bf.beta0(w.X), max_probes=4)
+    G = bf.flow(probe, w.N, bf.beta0(w.X), max_probes=4)
+    assert F.beta_x == G.beta_x and F.reason == G.reason
+    assert [p.beta for p in F.probes] == [p.beta for p in G.probes]
