@@ -38,9 +38,11 @@ void fill_normal(float* Z, int64_t ldz, int64_t N, int nb, const int* flags, uin
 // out[c] = ||W[:, c] - theta_c Y[:, c]||_2 for c < nc (Y, W share ld).
 void residual_norms(const float* Y, const float* W, int64_t ld, int nc, const double* theta,
                     int64_t N, FSpanD part, double* out, hipStream_t stream);
-// Symmetric eigensolve of A (m x m, overwritten): theta descending, S columns.
-void jacobi_eig(double* A, int m, int lda, double* Vw, double* theta, double* S, int lds,
-                int* sweeps, hipStream_t stream);
+// Symmetric eigensolve of A (m x m, overwritten; A2 an m x m scratch with the
+// same ld): theta descending, S columns.  Vw: m x m scratch (ld m); norms: 2
+// doubles of scratch.  Synchronises the stream once per sweep.
+void jacobi_eig(double* A, double* A2, int m, int lda, double* Vw, double* theta, double* S,
+                int lds, double* norms, hipStream_t stream);
 void copy_cols(const float* src, int64_t lds, float* dst, int64_t ldd, int64_t N, int nc,
                const float* scale, double power, hipStream_t stream);
 void sub_theta(const float* Y, float* W, int64_t ld, int64_t N, int nc, const double* theta,

@@ -65,7 +65,8 @@ struct SolverWs {
   double* s_off = nullptr;
   float *Q = nullptr, *Qa = nullptr, *W = nullptr, *Wa = nullptr, *Zt = nullptr;
   FSpanD part;
-  double *T = nullptr, *Tw = nullptr, *S = nullptr, *Vw = nullptr, *theta = nullptr;
+  double *T = nullptr, *Tw = nullptr, *Tw2 = nullptr, *S = nullptr, *Vw = nullptr,
+         *theta = nullptr, *norms = nullptr;
   double *C = nullptr, *G = nullptr, *res = nullptr;
   float *C32 = nullptr, *S32 = nullptr, *Rinv = nullptr;
   int *flags = nullptr, *sel = nullptr, *sweeps = nullptr;
@@ -104,6 +105,8 @@ static SolverWs carve_solver_ws(Arena& a, int64_t N, int64_t D, int b, int mm_ca
   const size_t m2 = size_t(mm_cap) * mm_cap;
   w.T = a.take<double>(m2);
   w.Tw = a.take<double>(m2);
+  w.Tw2 = a.take<double>(m2);
+  w.norms = a.take<double>(2);
   w.S = a.take<double>(m2);
   w.Vw = a.take<double>(m2);
   w.theta = a.take<double>(mm_cap);
@@ -185,7 +188,7 @@ struct Lanczos {
   // leading nkeep Ritz vectors / images to Qa / Wa, their residual norms to res.
   void rayleigh_ritz(int m, int nkeep) {
     copy_square(w.T, mm, w.Tw, mm, m, st);
-    jacobi_eig(w.Tw, m, mm, w.Vw, w.theta, w.S, mm, w.sweeps, st);
+    jacobi_eig(w.Tw, w.Tw2, m, mm, w.Vw, w.theta, w.S, mm, w.norms, st);
     for (int c0 = 0; c0 < nkeep; c0 += 64) {
       const int nc = std::min(64, nkeep - c0);
       narrow(w.S + c0, mm, m, nc, w.S32, st);

@@ -6,6 +6,7 @@
 //   * residual norms ||W s - theta Q s|| of Ritz pairs,
 //   * cyclic Jacobi eigensolver for the small symmetric projected matrix.
 // Everything is deterministic: no atomics, fixed reduction orders.
+#include <algorithm>
 #include <cmath>
 
 #include "fd_linalg.hpp"
@@ -269,128 +270,175 @@ void residual_norms(const float* Y, const float* W, int64_t ld, int nc, const do
 }
 
 // ------------------------------------------------------------ Jacobi eigensolver
-// Cyclic two-sided Jacobi (Golub & Van Loan, Alg. 8.5.3, parallel ordering):
-// in each round the indices are split into disjoint pairs by the circle
-// method, every pair (p, q) gets the rotation that annihilates A_pq
-// (Alg. 8.5.2), all row rotations are applied, then all column rotations and
-// the eigenvector updates.  A (m x m, float64, ld lda) is overwritten; on exit
-// theta (m) holds the eigenvalues sorted descending and S (m x m, ld lds) the
-// matching eigenvectors in its columns.  Vw (m x m) is a scratch matrix.
-__global__ __launch_bounds__(1024) void jacobi_kernel(double* __restrict__ A, int m, int lda,
-                                                      double* __restrict__ Vw,
-                                                      double* __restrict__ theta,
-                                                      double* __restrict__ S, int lds,
-                                                      int max_sweeps, double tol,
-                                                      int* __restrict__ sweeps_out) {
-  __shared__ int pp[512], qq[512];
-  __shared__ double cc[512], ss[512];
-  __shared__ double red[1024];
-  __shared__ int stop;
-  const int t = threadIdx.x;
-  const int nt = blockDim.x;
-  const int me = m + (m & 1);  // even number of players (index m is a dummy when m is odd)
-  const int npairs = me / 2;
-  for (int e = t; e < m * m; e += nt) Vw[(e / m) * m + (e % m)] = (e / m == e % m) ? 1.0 : 0.0;
-  if (t == 0) stop = 0;
-  __syncthreads();
-  int sweep = 0;
-  for (; sweep < max_sweeps; ++sweep) {
-    // convergence: off-diagonal Frobenius norm relative to the whole matrix
-    double off = 0.0, all = 0.0;
-    for (int e = t; e < m * m; e += nt) {
-      const int i = e / m, j = e % m;
-      const double v = A[int64_t(i) * lda + j];
-      all += v * v;
-      if (i != j) off += v * v;
-    }
-    red[t] = off;
-    __syncthreads();
-    for (int w = nt / 2; w > 0; w >>= 1) {
-      if (t < w) red[t] += red[t + w];
-      __syncthreads();
-    }
-    const double off_sum = red[0];
-    __syncthreads();
-    red[t] = all;
-    __syncthreads();
-    for (int w = nt / 2; w > 0; w >>= 1) {
-      if (t < w) red[t] += red[t + w];
-      __syncthreads();
-    }
-    if (t == 0) stop = (off_sum <= tol * tol * red[0]) ? 1 : 0;
-    __syncthreads();
-    if (stop) break;
-    for (int round = 0; round < me - 1; ++round) {
-      for (int k = t; k < npairs; k += nt) {
-        // circle method: player 0 fixed, players 1..me-1 rotate
-        const int a = (k == 0) ? 0 : ((round + k - 1) % (me - 1)) + 1;
-        const int bq = ((round + me - 2 - k) % (me - 1)) + 1;
-        int p = min(a, bq), q = max(a, bq);
-        double c = 1.0, s = 0.0;
-        if (q < m) {
-          const double apq = A[int64_t(p) * lda + q];
-          if (apq != 0.0) {
-            const double app = A[int64_t(p) * lda + p], aqq = A[int64_t(q) * lda + q];
-            const double tau = (aqq - app) / (2.0 * apq);
-            const double tt = (tau >= 0.0 ? 1.0 : -1.0) / (fabs(tau) + sqrt(1.0 + tau * tau));
-            c = 1.0 / sqrt(1.0 + tt * tt);
-            s = tt * c;
-          }
-        } else {
-          p = q = -1;
-        }
-        pp[k] = p;
-        qq[k] = q;
-        cc[k] = c;
-        ss[k] = s;
-      }
-      __syncthreads();
-      // rows: A_p <- c A_p - s A_q, A_q <- s A_p + c A_q
-      for (int e = t; e < npairs * m; e += nt) {
-        const int k = e / m, j = e % m;
-        const int p = pp[k], q = qq[k];
-        if (p < 0 || ss[k] == 0.0) continue;
-        const double c = cc[k], s = ss[k];
-        const double ap = A[int64_t(p) * lda + j], aq = A[int64_t(q) * lda + j];
-        A[int64_t(p) * lda + j] = c * ap - s * aq;
-        A[int64_t(q) * lda + j] = s * ap + c * aq;
-      }
-      __syncthreads();
-      // columns of A and of V
-      for (int e = t; e < npairs * m; e += nt) {
-        const int k = e / m, i = e % m;
-        const int p = pp[k], q = qq[k];
-        if (p < 0 || ss[k] == 0.0) continue;
-        const double c = cc[k], s = ss[k];
-        const double ap = A[int64_t(i) * lda + p], aq = A[int64_t(i) * lda + q];
-        A[int64_t(i) * lda + p] = c * ap - s * aq;
-        A[int64_t(i) * lda + q] = s * ap + c * aq;
-        const double vp = Vw[int64_t(i) * m + p], vq = Vw[int64_t(i) * m + q];
-        Vw[int64_t(i) * m + p] = c * vp - s * vq;
-        Vw[int64_t(i) * m + q] = s * vp + c * vq;
-      }
-      __syncthreads();
-    }
+// Cyclic two-sided Jacobi (Golub & Van Loan, Alg. 8.5.3, parallel ordering).
+// In each round the indices are split into disjoint pairs by the circle
+// method and every pair (p, q) gets the rotation that annihilates A_pq
+// (Alg. 8.5.2).  Because the pairs of a round are disjoint, the round's
+// similarity transform acts on A block by block: for row pair i and column
+// pair j the 2 x 2 block (rows p_i, q_i; columns p_j, q_j) becomes
+// R_i^T X R_j.  One launch per round does all blocks (and the matching
+// column rotations of the eigenvector matrix) with as many workgroups as the
+// size needs, reading A and writing its transform to a second buffer; every
+// workgroup recomputes the round's rotations from the (unchanged) input.
+// After each sweep the off-diagonal Frobenius norm is checked on the host
+// (one scalar read back).  On exit theta (m) holds the eigenvalues sorted
+// descending and S (m x m, ld lds) the matching eigenvectors in its columns.
+
+// pair k of round `round` among me (even) players: indices p < q, q = -1 for
+// the dummy player of an odd m; rotation (c, s) annihilating A_pq
+__device__ __forceinline__ void jacobi_pair(const double* __restrict__ A, int lda, int m, int me,
+                                            int round, int k, int& p, int& q, double& c,
+                                            double& s) {
+  const int a = (k == 0) ? 0 : ((round + k - 1) % (me - 1)) + 1;
+  const int bq = ((round + me - 2 - k) % (me - 1)) + 1;
+  p = min(a, bq);
+  q = max(a, bq);
+  c = 1.0;
+  s = 0.0;
+  if (q >= m) {
+    q = -1;  // dummy partner: identity
+    return;
   }
-  // sort descending: rank of i = number of j before it in the order
-  for (int i = t; i < m; i += nt) {
-    const double di = A[int64_t(i) * lda + i];
-    int rank = 0;
-    for (int j = 0; j < m; ++j) {
-      const double dj = A[int64_t(j) * lda + j];
-      rank += (dj > di || (dj == di && j < i)) ? 1 : 0;
-    }
-    theta[rank] = di;
-    for (int r = 0; r < m; ++r) S[int64_t(r) * lds + rank] = Vw[int64_t(r) * m + i];
+  const double apq = A[int64_t(p) * lda + q];
+  if (apq != 0.0) {
+    const double app = A[int64_t(p) * lda + p], aqq = A[int64_t(q) * lda + q];
+    const double tau = (aqq - app) / (2.0 * apq);
+    const double tt = (tau >= 0.0 ? 1.0 : -1.0) / (fabs(tau) + sqrt(1.0 + tau * tau));
+    c = 1.0 / sqrt(1.0 + tt * tt);
+    s = tt * c;
   }
-  if (t == 0 && sweeps_out != nullptr) *sweeps_out = sweep;
 }
 
-void jacobi_eig(double* A, int m, int lda, double* Vw, double* theta, double* S, int lds,
-                int* sweeps, hipStream_t stream) {
+// One round: B = J^T A J block by block, V <- V J (in place).
+__global__ __launch_bounds__(256) void jacobi_round_kernel(const double* __restrict__ A,
+                                                           double* __restrict__ B, int lda,
+                                                           double* __restrict__ V, int m, int me,
+                                                           int round) {
+  __shared__ int pp[512], qq[512];
+  __shared__ double cc[512], ss[512];
+  const int npairs = me / 2;
+  for (int k = threadIdx.x; k < npairs; k += blockDim.x) {
+    int p, q;
+    double c, s;
+    jacobi_pair(A, lda, m, me, round, k, p, q, c, s);
+    pp[k] = p;
+    qq[k] = q;
+    cc[k] = c;
+    ss[k] = s;
+  }
+  __syncthreads();
+  const int64_t nA = int64_t(npairs) * npairs;
+  const int64_t nV = int64_t(m) * npairs;
+  const int64_t stride = int64_t(gridDim.x) * blockDim.x;
+  for (int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; idx < nA + nV; idx += stride) {
+    if (idx < nA) {
+      const int i = int(idx / npairs), j = int(idx % npairs);
+      const int pi = pp[i], qi = qq[i], pj = pp[j], qj = qq[j];
+      const double ci = cc[i], si = ss[i], cj = cc[j], sj = ss[j];
+      const double a = A[int64_t(pi) * lda + pj];
+      const double b = qj >= 0 ? A[int64_t(pi) * lda + qj] : 0.0;
+      const double d = qi >= 0 ? A[int64_t(qi) * lda + pj] : 0.0;
+      const double e = (qi >= 0 && qj >= 0) ? A[int64_t(qi) * lda + qj] : 0.0;
+      // rows: p' = c p - s q, q' = s p + c q; then the same on the columns
+      const double a1 = ci * a - si * d, b1 = ci * b - si * e;
+      const double d1 = si * a + ci * d, e1 = si * b + ci * e;
+      B[int64_t(pi) * lda + pj] = cj * a1 - sj * b1;
+      if (qj >= 0) B[int64_t(pi) * lda + qj] = sj * a1 + cj * b1;
+      if (qi >= 0) B[int64_t(qi) * lda + pj] = cj * d1 - sj * e1;
+      if (qi >= 0 && qj >= 0) B[int64_t(qi) * lda + qj] = sj * d1 + cj * e1;
+    } else {
+      const int64_t v = idx - nA;
+      const int r = int(v / npairs), j = int(v % npairs);
+      const int pj = pp[j], qj = qq[j];
+      if (qj < 0 || ss[j] == 0.0) continue;
+      const double cj = cc[j], sj = ss[j];
+      const double vp = V[int64_t(r) * m + pj], vq = V[int64_t(r) * m + qj];
+      V[int64_t(r) * m + pj] = cj * vp - sj * vq;
+      V[int64_t(r) * m + qj] = sj * vp + cj * vq;
+    }
+  }
+}
+
+__global__ void jacobi_init_kernel(double* __restrict__ V, int m) {
+  const int64_t e = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (e < int64_t(m) * m) V[e] = (e / m == e % m) ? 1.0 : 0.0;
+}
+
+// out[0] = sum of squared off-diagonal entries, out[1] = sum of all (one
+// workgroup, fixed order)
+__global__ __launch_bounds__(1024) void jacobi_offnorm_kernel(const double* __restrict__ A, int m,
+                                                              int lda, double* __restrict__ out) {
+  __shared__ double r0[1024], r1[1024];
+  const int t = threadIdx.x;
+  double off = 0.0, all = 0.0;
+  for (int64_t e = t; e < int64_t(m) * m; e += blockDim.x) {
+    const int i = int(e / m), j = int(e % m);
+    const double v = A[int64_t(i) * lda + j];
+    all += v * v;
+    if (i != j) off += v * v;
+  }
+  r0[t] = off;
+  r1[t] = all;
+  __syncthreads();
+  for (int w = blockDim.x / 2; w > 0; w >>= 1) {
+    if (t < w) {
+      r0[t] += r0[t + w];
+      r1[t] += r1[t + w];
+    }
+    __syncthreads();
+  }
+  if (t == 0) {
+    out[0] = r0[0];
+    out[1] = r1[0];
+  }
+}
+
+// theta = diag(A) sorted descending, S columns = matching columns of V
+__global__ void jacobi_sort_kernel(const double* __restrict__ A, int m, int lda,
+                                   const double* __restrict__ V, double* __restrict__ theta,
+                                   double* __restrict__ S, int lds) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= m) return;
+  const double di = A[int64_t(i) * lda + i];
+  int rank = 0;
+  for (int j = 0; j < m; ++j) {
+    const double dj = A[int64_t(j) * lda + j];
+    rank += (dj > di || (dj == di && j < i)) ? 1 : 0;
+  }
+  theta[rank] = di;
+  for (int r = 0; r < m; ++r) S[int64_t(r) * lds + rank] = V[int64_t(r) * m + i];
+}
+
+void jacobi_eig(double* A, double* A2, int m, int lda, double* Vw, double* theta, double* S,
+                int lds, double* norms, hipStream_t stream) {
   FD_REQUIRE(m >= 1 && m <= 1024, FD_ERR_UNSUPPORTED, "projected matrix larger than 1024");
-  hipLaunchKernelGGL(jacobi_kernel, dim3(1), dim3(1024), 0, stream, A, m, lda, Vw, theta, S, lds,
-                     60, 1e-13, sweeps);
+  constexpr int MAX_SWEEPS = 60;
+  constexpr double TOL = 1e-13;
+  const int me = m + (m & 1);
+  const int npairs = me / 2;
+  const int64_t items = int64_t(npairs) * npairs + int64_t(m) * npairs;
+  const unsigned grid = unsigned(std::min<int64_t>(2048, std::max<int64_t>(1, (items + 255) / 256)));
+  hipLaunchKernelGGL(jacobi_init_kernel, dim3(nblk(int64_t(m) * m, 256)), dim3(256), 0, stream, Vw,
+                     m);
+  FD_LAUNCH_CHECK();
+  double* cur = A;
+  double* nxt = A2;
+  for (int sweep = 0; sweep < MAX_SWEEPS && m > 1; ++sweep) {
+    hipLaunchKernelGGL(jacobi_offnorm_kernel, dim3(1), dim3(1024), 0, stream, cur, m, lda, norms);
+    FD_LAUNCH_CHECK();
+    double h[2] = {0.0, 0.0};
+    FD_HIP_CHECK(hipMemcpyAsync(h, norms, sizeof(h), hipMemcpyDeviceToHost, stream));
+    FD_HIP_CHECK(hipStreamSynchronize(stream));
+    if (h[0] <= TOL * TOL * h[1]) break;
+    for (int round = 0; round < me - 1; ++round) {
+      hipLaunchKernelGGL(jacobi_round_kernel, dim3(grid), dim3(256), 0, stream, cur, nxt, lda, Vw,
+                         m, me, round);
+      FD_LAUNCH_CHECK();
+      std::swap(cur, nxt);
+    }
+  }
+  hipLaunchKernelGGL(jacobi_sort_kernel, dim3(nblk(m, 256)), dim3(256), 0, stream, cur, m, lda, Vw,
+                     theta, S, lds);
   FD_LAUNCH_CHECK();
 }
 
