@@ -17,7 +17,8 @@ static inline unsigned nblk(int64_t n, int t) { return unsigned((n + t - 1) / t)
 
 // ------------------------------------------------------------ C = A^T B
 // Grid (l tiles of 64, row chunks).  Thread (lg, cg) accumulates a 4 x 4
-// block C[l0 + 4 lg + u][4 cg + v] in float64 over its chunk of rows.
+// block C[l0 + 4 lg + u][4 cg + v] in float64 over its chunk of rows, four
+// rows per step with all sixteen loads of a step issued before its FMAs.
 __global__ __launch_bounds__(256) void gemm_tn_partial_kernel(
     const float* __restrict__ A, int64_t lda, int ma, const float* __restrict__ B, int64_t ldb,
     int nb, int64_t N, int64_t rows_per_chunk, double* __restrict__ part) {
@@ -33,16 +34,37 @@ __global__ __launch_bounds__(256) void gemm_tn_partial_kernel(
 #pragma unroll
     for (int v = 0; v < 4; ++v) acc[u][v] = 0.0;
   if (l0 < ma && c0 < nb) {
-    for (int64_t i = r0; i < r1; ++i) {
-      double a[4], bv[4];
+    // columns past the edge read a valid column; their sums are not stored
+    int la[4], cb[4];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) a[u] = (l0 + u < ma) ? double(A[i * lda + l0 + u]) : 0.0;
+    for (int u = 0; u < 4; ++u) {
+      la[u] = min(l0 + u, ma - 1);
+      cb[u] = min(c0 + u, nb - 1);
+    }
+    int64_t i = r0;
+    for (; i + 4 <= r1; i += 4) {
+      float a[4][4], bv[4][4];
 #pragma unroll
-      for (int v = 0; v < 4; ++v) bv[v] = (c0 + v < nb) ? double(B[i * ldb + c0 + v]) : 0.0;
+      for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          a[r][u] = A[(i + r) * lda + la[u]];
+          bv[r][u] = B[(i + r) * ldb + cb[u]];
+        }
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+          for (int v = 0; v < 4; ++v)
+            acc[u][v] = fma(double(a[r][u]), double(bv[r][v]), acc[u][v]);
+    }
+    for (; i < r1; ++i) {
 #pragma unroll
       for (int u = 0; u < 4; ++u)
 #pragma unroll
-        for (int v = 0; v < 4; ++v) acc[u][v] = fma(a[u], bv[v], acc[u][v]);
+        for (int v = 0; v < 4; ++v)
+          acc[u][v] = fma(double(A[i * lda + la[u]]), double(B[i * ldb + cb[v]]), acc[u][v]);
     }
   }
   double* out = part + chunk * int64_t(ma) * nb;
@@ -65,8 +87,9 @@ __global__ void reduce_partials_kernel(const double* __restrict__ part, int64_t 
 }
 
 int64_t gemm_tn_chunks(int64_t N) {
-  // enough chunks to fill the GPU with (l tiles x chunks) workgroups
-  return std::max<int64_t>(1, std::min<int64_t>(512, (N + 1023) / 1024));
+  // enough chunks (of >= 128 rows) to fill the GPU with (l tiles x chunks)
+  // workgroups even when there is a single l tile
+  return std::max<int64_t>(1, std::min<int64_t>(1024, (N + 127) / 128));
 }
 
 void gemm_tn(const float* A, int64_t lda, int ma, const float* B, int64_t ldb, int nb, int64_t N,
