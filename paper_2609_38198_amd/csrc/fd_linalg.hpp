@@ -40,9 +40,13 @@ void residual_norms(const float* Y, const float* W, int64_t ld, int nc, const do
                     int64_t N, FSpanD part, double* out, hipStream_t stream);
 // Symmetric eigensolve of A (m x m, overwritten; A2 an m x m scratch with the
 // same ld): theta descending, S columns.  Vw: m x m scratch (ld m); norms: 2
-// doubles of scratch.  Synchronises the stream once per sweep.
+// doubles of scratch; log: jacobi_log_doubles(m) doubles (enough for every
+// size up to m) and state: 2 ints of scratch (the one-workgroup path for small
+// m).  Synchronises the stream once
+// per sweep (once per few sweeps on the one-workgroup path).
+size_t jacobi_log_doubles(int m);
 void jacobi_eig(double* A, double* A2, int m, int lda, double* Vw, double* theta, double* S,
-                int lds, double* norms, hipStream_t stream);
+                int lds, double* norms, FSpanD log, int* state, hipStream_t stream);
 void copy_cols(const float* src, int64_t lds, float* dst, int64_t ldd, int64_t N, int nc,
                const float* scale, double power, hipStream_t stream);
 void sub_theta(const float* Y, float* W, int64_t ld, int64_t N, int nc, const double* theta,

@@ -55,6 +55,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <type_traits>
 
 #include "fd_profile.hpp"
 #include "kv_common.hpp"
@@ -682,36 +683,64 @@ __device__ __forceinline__ float dpp_row_sum(float v) {
   return v;
 }
 
-// One off-diagonal column tile J against the wave's NIB own row tiles: row
-// sums into acc, column sums of the tile into the fixed-point accumulator.
-template <int RID, int NIB, bool UNIT>
-__device__ __forceinline__ void hx_rowsum_sym_tile(const HxCol<RID>& c,
-                                                   const uintx4 (&br)[NIB][Hx<RID>::nb],
-                                                   const float (&wi)[NIB], float (&acc)[NIB],
-                                                   int64_t jl, double fix_scale,
-                                                   unsigned long long* lds_col, int g,
-                                                   int p) {
-  floatx4 t[NIB];
-#pragma unroll
-  for (int ib = 0; ib < NIB; ++ib) t[ib] = hx_exponent<RID, false>(c.xa, br[ib], g, p);
+// Scheduling pattern for a region holding M matrix instructions and E
+// exponentials: each matrix instruction followed by its share of the
+// exponentials and V other vector instructions.
+template <int M, int E, int V, int m = 0>
+__device__ __forceinline__ void sched_interleave() {
+  if constexpr (m < M) {
+    constexpr int ne = (m + 1) * E / M - m * E / M;
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // matrix
+    if constexpr (ne > 0) __builtin_amdgcn_sched_group_barrier(0x400, ne, 0);  // transcendental
+    __builtin_amdgcn_sched_group_barrier(0x002, V, 0);  // vector
+    sched_interleave<M, E, V, m + 1>();
+  }
+}
+
+// One pipeline step of the symmetric row sums.  t holds the exponent tiles of
+// an off-diagonal column tile J against the wave's NIB row tiles; each is
+// exponentiated and then overwritten with the exponent tile of the next column
+// tile (operands xn), so the matrix-core chain of row tile ib runs alongside
+// the vector work of row tiles ib + 1, ...  SUMS: add J's row sums into acc and
+// its column sums into the fixed-point accumulator (false for padding tiles).
+template <int RID, int NIB, bool UNIT, bool SUMS>
+__device__ __forceinline__ void hx_sym_step(floatx4 (&t)[NIB], const uintx4* xn,
+                                            const uintx4 (&br)[NIB][Hx<RID>::nb],
+                                            const floatx4& w, const float (&wi)[NIB],
+                                            float (&acc)[NIB], int64_t jl, double fix_scale,
+                                            unsigned long long* lds_col, int g, int p) {
   float cs[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int ib = 0; ib < NIB; ++ib) {
     float k[4];
+    if (SUMS) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r) k[r] = __builtin_amdgcn_exp2f(t[ib][r]);
-    if (UNIT) {
-      acc[ib] += (k[0] + k[1]) + (k[2] + k[3]);
+      for (int r = 0; r < 4; ++r) k[r] = __builtin_amdgcn_exp2f(t[ib][r]);
+    }
+    t[ib] = hx_exponent<RID, false>(xn, br[ib], g, p);
+    if (SUMS) {
+      if (UNIT) {
+        acc[ib] += (k[0] + k[1]) + (k[2] + k[3]);
 #pragma unroll
-      for (int r = 0; r < 4; ++r) cs[r] += k[r];
-    } else {
+        for (int r = 0; r < 4; ++r) cs[r] += k[r];
+      } else {
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        acc[ib] = fmaf(k[r], c.w[r], acc[ib]);
-        cs[r] = fmaf(k[r], wi[ib], cs[r]);
+        for (int r = 0; r < 4; ++r) {
+          acc[ib] = fmaf(k[r], w[r], acc[ib]);
+          cs[r] = fmaf(k[r], wi[ib], cs[r]);
+        }
       }
     }
   }
+  if (!SUMS) return;
+  // the row sums are due here (an empty statement reading them), not sunk
+  // past the column-sum atomic below, so that they interleave too
+#pragma unroll
+  for (int ib = 0; ib < NIB; ++ib) asm volatile("" ::"v"(acc[ib]));
+  // Interleave the contraction with the exponentials and sums (left to
+  // itself the scheduler issues the exponentials first, then the matrix
+  // instructions with little vector work between them).
+  sched_interleave<Hx<RID>::nm * NIB, 4 * NIB, 3>();
   // lane (g, p) holds, for column 4g + r of the tile, the sum over rows p of
   // the wave's tiles; the 16 lanes of DPP row g hold the wave's other rows
 #pragma unroll
@@ -731,6 +760,7 @@ __attribute__((amdgpu_waves_per_eu(hx_waves<RID, 0, NIB>()))) void rowsum_sym_hx
     int64_t nblk, int64_t njb, int64_t jb_per_split, int64_t nsplit, float* __restrict__ part,
     int64_t nrpad, unsigned long long* __restrict__ colfix, double fix_scale) {
   constexpr int NB = Hx<RID>::nb;
+  constexpr int NC = Hx<RID>::nc;
   constexpr int BT = 4 * NIB;  // tiles per block
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -784,48 +814,16 @@ __attribute__((amdgpu_waves_per_eu(hx_waves<RID, 0, NIB>()))) void rowsum_sym_hx
     if (J >= nt32) J -= nt32;
     return J < njb32 ? J : -1;
   };
-  // loads are unconditional (index clamped into the range, padding tiles read
-  // tile 0) so that every path reaches the loop top with the same loads in
-  // flight and the waits there cover one buffer only
-  auto load = [&](HxCol<RID>& c, int64_t jj) {
-    const int J = tile_of(max(min(jj, jj_end - 1), int64_t(0)));
-    load_hx_col<RID, UNIT>(c, xc, wp, J < 0 ? 0 : J, lane);
+  // tile loaded for range position jj of [lo, jj_end): clamped into the range,
+  // padding tiles read tile 0, so that loads are unconditional and every path
+  // keeps the same loads in flight
+  auto load_tile = [&](int64_t jj, int64_t lo) -> int64_t {
+    const int J = tile_of(max(min(jj, jj_end - 1), lo));
+    return J < 0 ? 0 : J;
   };
-  auto step = [&](const HxCol<RID>& c, int64_t jj) {
-    const int J = tile_of(jj);
-    if (J < 0) return;
-    if (jj >= BT) {
-      hx_rowsum_sym_tile<RID, NIB, UNIT>(c, br, wi, acc, (jj - jj_begin) % SYM_CHUNK, fix_scale,
-                                         lds_col, g, p);
-    } else if (J >= ib0 && J < ib0 + NIB) {
-      hx_rowsum_tile<RID, NIB, UNIT, true>(c, br, acc, J, ib0, g, p);
-    } else {
-      hx_rowsum_tile<RID, NIB, UNIT, false>(c, br, acc, J, ib0, g, p);
-    }
-  };
-  HxCol<RID> b0, b1;
-  b0.w = b1.w = floatx4{1.f, 1.f, 1.f, 1.f};
-  load(b0, jj_begin);
-  __builtin_amdgcn_sched_barrier(0);  // b0's loads ahead of b1's, as in the loop
-  load(b1, jj_begin + 1);
-  // consume the row operands here (an empty statement reading them): their
-  // loads complete before the loop, whose waits then only ever cover the
-  // column buffer a step consumes (left to itself the compiler sinks these
-  // loads past the loop entry and every iteration waits for all loads)
-#pragma unroll
-  for (int ib = 0; ib < NIB; ++ib)
-#pragma unroll
-    for (int ch = 0; ch < NB; ++ch) asm volatile("" ::"v"(br[ib][ch]));
-  // likewise the scalar kernel argument used in the loop: with its load done
-  // here, the loop's LDS atomics (which share the counter) are never waited on
-  asm volatile("" ::"s"(fix_scale));
   int chunk = 0;
-  for (int64_t jj = jj_begin; jj < jj_end; jj += 2) {
-    step(b0, jj);
-    load(b0, jj + 2);
-    if (jj + 1 < jj_end) step(b1, jj + 1);
-    load(b1, jj + 3);
-    chunk += 2;
+  auto row_chunk = [&](int tiles) {
+    chunk += tiles;
     if (chunk >= CHUNK_TILES) {
       chunk = 0;
 #pragma unroll
@@ -834,19 +832,108 @@ __attribute__((amdgpu_waves_per_eu(hx_waves<RID, 0, NIB>()))) void rowsum_sym_hx
         acc[ib] = 0.f;
       }
     }
-    // end of a chunk of column tiles (the trip count is uniform over the
-    // workgroup): add the chunk's column sums into the global accumulator
-    const int64_t done = jj + 2 - jj_begin;
-    if (done % SYM_CHUNK == 0 || jj + 2 >= jj_end) {
-      const int64_t c0 = jj_begin + (done - 1) / SYM_CHUNK * SYM_CHUNK;
-      __syncthreads();
-      for (int e = threadIdx.x; e < SYM_CHUNK * TILE; e += WG_THREADS) {
-        const unsigned long long v = lds_col[e];
-        const int J = c0 + e / TILE < jj_end ? tile_of(c0 + e / TILE) : -1;
-        if (v != 0ull && J >= 0) atomicAdd(colfix + int64_t(J) * TILE + e % TILE, v);
-        lds_col[e] = 0ull;
+  };
+
+  // The workgroup's own block (range positions below BT, in split 0 only):
+  // plain row sums, exact diagonal.  Column tiles stream through two buffers
+  // used in turn.
+  const int64_t own_end = min(jj_end, int64_t(BT));
+  if (jj_begin < own_end) {
+    auto step = [&](const HxCol<RID>& c, int64_t jj) {
+      const int J = tile_of(jj);
+      if (J < 0) return;
+      if (J >= ib0 && J < ib0 + NIB)
+        hx_rowsum_tile<RID, NIB, UNIT, true>(c, br, acc, J, ib0, g, p);
+      else
+        hx_rowsum_tile<RID, NIB, UNIT, false>(c, br, acc, J, ib0, g, p);
+    };
+    HxCol<RID> b0, b1;
+    b0.w = b1.w = floatx4{1.f, 1.f, 1.f, 1.f};
+    load_hx_col<RID, UNIT>(b0, xc, wp, load_tile(jj_begin, jj_begin), lane);
+    __builtin_amdgcn_sched_barrier(0);  // b0's loads ahead of b1's, as in the loop
+    load_hx_col<RID, UNIT>(b1, xc, wp, load_tile(min(jj_begin + 1, own_end - 1), jj_begin),
+                           lane);
+    for (int64_t jj = jj_begin; jj < own_end; jj += 2) {
+      step(b0, jj);
+      load_hx_col<RID, UNIT>(b0, xc, wp, load_tile(min(jj + 2, own_end - 1), jj_begin), lane);
+      if (jj + 1 < own_end) step(b1, jj + 1);
+      load_hx_col<RID, UNIT>(b1, xc, wp, load_tile(min(jj + 3, own_end - 1), jj_begin), lane);
+      row_chunk(2);
+    }
+  }
+
+  // The other blocks: each tile serves both sums.  Two-stage pipeline over
+  // the tiles u = 0, 1, ... of [s0, jj_end): step u exponentiates and sums
+  // tile u, whose exponents the previous step made, while the matrix cores
+  // make those of tile u + 1 (hx_sym_step).  Tile v's column operands sit in
+  // slot v % 2 and are loaded two steps ahead of their contraction, its
+  // weights one step ahead of its sums.
+  const int64_t s0 = max(jj_begin, int64_t(BT));
+  const int64_t n2 = jj_end - s0;
+  if (n2 > 0) {
+    uintx4 xa[2][NC];
+    floatx4 w[2];
+    floatx4 t[NIB];
+    w[0] = w[1] = floatx4{1.f, 1.f, 1.f, 1.f};
+    auto load_xa = [&](uintx4 (&dst)[NC], int64_t u) {
+      const int64_t J = load_tile(s0 + u, s0);
+#pragma unroll
+      for (int ch = 0; ch < NC; ++ch) dst[ch] = xc[(J * NC + ch) * 64 + lane];
+    };
+    auto load_w = [&](floatx4& dst, int64_t u) {
+      if (!UNIT) dst = wp[load_tile(s0 + u, s0) * 64 + lane];
+    };
+    load_xa(xa[0], 0);
+    load_w(w[0], 0);
+    __builtin_amdgcn_sched_barrier(0);
+    load_xa(xa[1], 1);
+    // consume the row operands here (an empty statement reading them): their
+    // loads complete before the loop, whose waits then only ever cover the
+    // column operands a step consumes (left to itself the compiler sinks these
+    // loads past the loop entry and every iteration waits for all loads)
+#pragma unroll
+    for (int ib = 0; ib < NIB; ++ib)
+#pragma unroll
+      for (int ch = 0; ch < NB; ++ch) asm volatile("" ::"v"(br[ib][ch]));
+    // likewise the scalar kernel argument used in the loop: with its load done
+    // here, the loop's LDS atomics (which share the counter) are never waited on
+    asm volatile("" ::"s"(fix_scale));
+#pragma unroll
+    for (int ib = 0; ib < NIB; ++ib) t[ib] = hx_exponent<RID, false>(xa[0], br[ib], g, p);
+    // step u (slot S = u % 2): operands of tile u + 2 into slot S, weights of
+    // tile u + 1 into slot S ^ 1, sums of tile u with weights from slot S,
+    // contraction of tile u + 1 from slot S ^ 1
+    auto pipe_step = [&](auto S_, int64_t u) {
+      constexpr int S = decltype(S_)::value;
+      load_xa(xa[S], u + 2);
+      load_w(w[S ^ 1], u + 1);
+      const int J = tile_of(s0 + u);
+      const int64_t jl = (s0 + u - jj_begin) % SYM_CHUNK;
+      if (J >= 0)
+        hx_sym_step<RID, NIB, UNIT, true>(t, xa[S ^ 1], br, w[S], wi, acc, jl, fix_scale, lds_col,
+                                          g, p);
+      else
+        hx_sym_step<RID, NIB, UNIT, false>(t, xa[S ^ 1], br, w[S], wi, acc, jl, fix_scale,
+                                           lds_col, g, p);
+      row_chunk(1);
+      // end of a chunk of column tiles (the trip count is uniform over the
+      // workgroup): add the chunk's column sums into the global accumulator
+      const int64_t done = s0 + u + 1 - jj_begin;
+      if (done % SYM_CHUNK == 0 || s0 + u + 1 >= jj_end) {
+        const int64_t c0 = jj_begin + (done - 1) / SYM_CHUNK * SYM_CHUNK;
+        __syncthreads();
+        for (int e = threadIdx.x; e < SYM_CHUNK * TILE; e += WG_THREADS) {
+          const unsigned long long v = lds_col[e];
+          const int Jc = c0 + e / TILE < jj_end ? tile_of(c0 + e / TILE) : -1;
+          if (v != 0ull && Jc >= 0) atomicAdd(colfix + int64_t(Jc) * TILE + e % TILE, v);
+          lds_col[e] = 0ull;
+        }
+        __syncthreads();
       }
-      __syncthreads();
+    };
+    for (int64_t u = 0; u < n2; u += 2) {
+      pipe_step(std::integral_constant<int, 0>{}, u);
+      if (u + 1 < n2) pipe_step(std::integral_constant<int, 1>{}, u + 1);
     }
   }
 #pragma unroll

@@ -67,9 +67,10 @@ struct SolverWs {
   FSpanD part;
   double *T = nullptr, *Tw = nullptr, *Tw2 = nullptr, *S = nullptr, *Vw = nullptr,
          *theta = nullptr, *norms = nullptr;
+  FSpanD jlog;
   double *C = nullptr, *G = nullptr, *res = nullptr;
   float *C32 = nullptr, *S32 = nullptr, *Rinv = nullptr;
-  int *flags = nullptr, *sel = nullptr, *sweeps = nullptr;
+  int *flags = nullptr, *sel = nullptr, *sweeps = nullptr, *jstate = nullptr;
   int64_t N = 0;
   int mm_cap = 0, b = 0;
 };
@@ -109,6 +110,7 @@ static SolverWs carve_solver_ws(Arena& a, int64_t N, int64_t D, int b, int mm_ca
   w.norms = a.take<double>(2);
   w.S = a.take<double>(m2);
   w.Vw = a.take<double>(m2);
+  w.jlog = take_d(a, jacobi_log_doubles(mm_cap));
   w.theta = a.take<double>(mm_cap);
   w.res = a.take<double>(mm_cap);
   w.C = a.take<double>(size_t(mm_cap) * b);
@@ -119,6 +121,7 @@ static SolverWs carve_solver_ws(Arena& a, int64_t N, int64_t D, int b, int mm_ca
   w.flags = a.take<int>(64);
   w.sel = a.take<int>(64);
   w.sweeps = a.take<int>(1);
+  w.jstate = a.take<int>(2);
   return w;
 }
 
@@ -188,7 +191,7 @@ struct Lanczos {
   // leading nkeep Ritz vectors / images to Qa / Wa, their residual norms to res.
   void rayleigh_ritz(int m, int nkeep) {
     copy_square(w.T, mm, w.Tw, mm, m, st);
-    jacobi_eig(w.Tw, w.Tw2, m, mm, w.Vw, w.theta, w.S, mm, w.norms, st);
+    jacobi_eig(w.Tw, w.Tw2, m, mm, w.Vw, w.theta, w.S, mm, w.norms, w.jlog, w.jstate, st);
     for (int c0 = 0; c0 < nkeep; c0 += 64) {
       const int nc = std::min(64, nkeep - c0);
       narrow(w.S + c0, mm, m, nc, w.S32, st);

@@ -16,15 +16,55 @@ namespace fd {
 static inline unsigned nblk(int64_t n, int t) { return unsigned((n + t - 1) / t); }
 
 // ------------------------------------------------------------ C = A^T B
-// Grid (l tiles of 64, row chunks).  Thread (lg, cg) accumulates a 4 x 4
-// block C[l0 + 4 lg + u][4 cg + v] in float64 over its chunk of rows, four
-// rows per step with all sixteen loads of a step issued before its FMAs.
+// Each thread accumulates a 4 x 4 block C[4 lq + u][4 cq + v] in float64
+// (products of float32 values are exact in float64).  The output is split
+// into groups of lqg x tc such blocks (tc = ceil(nb / 4) column quads, lqg
+// row quads, at most 256 threads); a workgroup of 256 threads holds
+// S = 256 / (lqg tc) slices of one group, which walk interleaved 4-row steps
+// of the workgroup's chunk of rows and are added in LDS in slice order.  Grid
+// (groups, chunks); partial sums per chunk are then reduced in a fixed order.
+
+struct GemmTnShape {
+  int tc = 1, lqg = 1, slices = 1, groups = 1;
+  int64_t chunks = 1, rows_per_chunk = 1;
+};
+
+static GemmTnShape gemm_tn_shape(int ma, int nb, int64_t N) {
+  GemmTnShape g;
+  g.tc = (nb + 3) / 4;
+  const int lq = (ma + 3) / 4;
+  g.lqg = std::min(lq, 256 / g.tc);
+  g.groups = (lq + g.lqg - 1) / g.lqg;
+  g.lqg = (lq + g.groups - 1) / g.groups;  // balance the groups
+  g.slices = 256 / (g.lqg * g.tc);
+  // 4 to 16 steps of 4 rows per thread (a multiple of the 4 a loop iteration
+  // takes): as few as keep >= ~512 workgroups busy, but at most
+  // gemm_tn_chunks(N) chunks (the partial buffer's size)
+  const int64_t steps_total = (N + 3) / 4;
+  int64_t spt = steps_total * g.groups / (int64_t(g.slices) * 512);
+  spt = round_up(std::max<int64_t>(4, std::min<int64_t>(16, spt)), 4);
+  g.rows_per_chunk = 4 * spt * g.slices;
+  g.chunks = (N + g.rows_per_chunk - 1) / g.rows_per_chunk;
+  const int64_t cap = gemm_tn_chunks(N);
+  if (g.chunks > cap) {
+    g.chunks = cap;
+    g.rows_per_chunk = round_up((N + cap - 1) / cap, int64_t(4) * g.slices);
+    g.chunks = (N + g.rows_per_chunk - 1) / g.rows_per_chunk;
+  }
+  return g;
+}
+
 __global__ __launch_bounds__(256) void gemm_tn_partial_kernel(
     const float* __restrict__ A, int64_t lda, int ma, const float* __restrict__ B, int64_t ldb,
-    int nb, int64_t N, int64_t rows_per_chunk, double* __restrict__ part) {
-  const int lg = threadIdx.x >> 4, cg = threadIdx.x & 15;
-  const int l0 = blockIdx.x * 64 + 4 * lg;
-  const int c0 = 4 * cg;
+    int nb, int64_t N, int64_t rows_per_chunk, int tc, int lqg, int slices,
+    double* __restrict__ part) {
+  __shared__ double red[256 * 16];
+  const int t = threadIdx.x;
+  const int to = lqg * tc;
+  const int slice = t / to, o = t % to;
+  const int l0 = 4 * (blockIdx.x * lqg + o / tc);
+  const int c0 = 4 * (o % tc);
+  const bool active = slice < slices && l0 < ma;
   const int64_t chunk = blockIdx.y;
   const int64_t r0 = chunk * rows_per_chunk;
   const int64_t r1 = min(N, r0 + rows_per_chunk);
@@ -33,7 +73,7 @@ __global__ __launch_bounds__(256) void gemm_tn_partial_kernel(
   for (int u = 0; u < 4; ++u)
 #pragma unroll
     for (int v = 0; v < 4; ++v) acc[u][v] = 0.0;
-  if (l0 < ma && c0 < nb) {
+  if (active) {
     // columns past the edge read a valid column; their sums are not stored
     int la[4], cb[4];
 #pragma unroll
@@ -41,32 +81,50 @@ __global__ __launch_bounds__(256) void gemm_tn_partial_kernel(
       la[u] = min(l0 + u, ma - 1);
       cb[u] = min(c0 + u, nb - 1);
     }
-    int64_t i = r0;
-    for (; i + 4 <= r1; i += 4) {
-      float a[4][4], bv[4][4];
+    // four steps (of 4 rows) per iteration with all their loads issued first:
+    // the rows are far apart in memory and each step alone would wait a full
+    // load latency; rows past the chunk read its last row with weight 0
+    const int64_t stride = 4 * int64_t(slices);
+    for (int64_t i = r0 + 4 * slice; i < r1; i += 4 * stride) {
+      float a[4][4][4], bv[4][4][4];
 #pragma unroll
-      for (int r = 0; r < 4; ++r)
+      for (int st = 0; st < 4; ++st)
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          a[r][u] = A[(i + r) * lda + la[u]];
-          bv[r][u] = B[(i + r) * ldb + cb[u]];
+        for (int r = 0; r < 4; ++r) {
+          const int64_t ir = i + st * stride + r;
+          const int64_t irc = min(ir, r1 - 1);
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            a[st][r][u] = A[irc * lda + la[u]];
+            bv[st][r][u] = (ir < r1) ? B[irc * ldb + cb[u]] : 0.f;
+          }
         }
 #pragma unroll
-      for (int r = 0; r < 4; ++r)
+      for (int st = 0; st < 4; ++st)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+              acc[u][v] = fma(double(a[st][r][u]), double(bv[st][r][v]), acc[u][v]);
+    }
+  }
+  if (slices > 1) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) red[(4 * u + v) * 256 + t] = acc[u][v];
+    __syncthreads();
+    if (slice == 0) {
+      for (int sl = 1; sl < slices; ++sl)
 #pragma unroll
         for (int u = 0; u < 4; ++u)
 #pragma unroll
-          for (int v = 0; v < 4; ++v)
-            acc[u][v] = fma(double(a[r][u]), double(bv[r][v]), acc[u][v]);
-    }
-    for (; i < r1; ++i) {
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
-#pragma unroll
-        for (int v = 0; v < 4; ++v)
-          acc[u][v] = fma(double(A[i * lda + la[u]]), double(B[i * ldb + cb[v]]), acc[u][v]);
+          for (int v = 0; v < 4; ++v) acc[u][v] += red[(4 * u + v) * 256 + sl * to + o];
     }
   }
+  if (slice != 0 || !active) return;
   double* out = part + chunk * int64_t(ma) * nb;
 #pragma unroll
   for (int u = 0; u < 4; ++u)
@@ -75,36 +133,45 @@ __global__ __launch_bounds__(256) void gemm_tn_partial_kernel(
       if (l0 + u < ma && c0 + v < nb) out[int64_t(l0 + u) * nb + c0 + v] = acc[u][v];
 }
 
-__global__ void reduce_partials_kernel(const double* __restrict__ part, int64_t nparts,
-                                       int64_t count, double* __restrict__ out,
-                                       float* __restrict__ out32) {
-  const int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (idx >= count) return;
+// out[idx] = sum over p of part[p * count + idx]: 8 threads per output, each
+// summing every 8th partial, then added in thread order (fixed).
+__global__ __launch_bounds__(256) void reduce_partials_kernel(const double* __restrict__ part,
+                                                              int64_t nparts, int64_t count,
+                                                              double* __restrict__ out,
+                                                              float* __restrict__ out32) {
+  __shared__ double red[8][32];
+  const int lane = threadIdx.x & 31, team = threadIdx.x >> 5;
+  const int64_t idx = int64_t(blockIdx.x) * 32 + lane;
   double s = 0.0;
-  for (int64_t p = 0; p < nparts; ++p) s += part[p * count + idx];
-  if (out != nullptr) out[idx] = s;
-  if (out32 != nullptr) out32[idx] = float(s);
+  if (idx < count)
+    for (int64_t p = team; p < nparts; p += 8) s += part[p * count + idx];
+  red[team][lane] = s;
+  __syncthreads();
+  if (team != 0 || idx >= count) return;
+  double tot = red[0][lane];
+  for (int k = 1; k < 8; ++k) tot += red[k][lane];
+  if (out != nullptr) out[idx] = tot;
+  if (out32 != nullptr) out32[idx] = float(tot);
 }
 
 int64_t gemm_tn_chunks(int64_t N) {
-  // enough chunks (of >= 128 rows) to fill the GPU with (l tiles x chunks)
-  // workgroups even when there is a single l tile
-  return std::max<int64_t>(1, std::min<int64_t>(1024, (N + 127) / 128));
+  // bound on the row chunks of gemm_tn (its partial buffer holds this many)
+  return std::max<int64_t>(1, std::min<int64_t>(1024, (N + 15) / 16));
 }
 
 void gemm_tn(const float* A, int64_t lda, int ma, const float* B, int64_t ldb, int nb, int64_t N,
              FSpanD part, double* C, float* C32, hipStream_t stream) {
-  FD_REQUIRE(ma >= 1 && nb >= 1 && N >= 1, FD_ERR_INVALID_ARG, "internal: gemm_tn shape");
-  const int64_t chunks = gemm_tn_chunks(N);
-  const int64_t rpc = (N + chunks - 1) / chunks;
-  check_span_d(part, size_t(chunks) * ma * nb, "gemm partials");
-  dim3 grid(nblk(ma, 64), unsigned(chunks));
-  hipLaunchKernelGGL(gemm_tn_partial_kernel, grid, dim3(256), 0, stream, A, lda, ma, B, ldb, nb,
-                     N, rpc, part.p);
+  FD_REQUIRE(ma >= 1 && nb >= 1 && nb <= 64 && N >= 1, FD_ERR_INVALID_ARG,
+             "internal: gemm_tn shape");
+  const GemmTnShape g = gemm_tn_shape(ma, nb, N);
+  check_span_d(part, size_t(g.chunks) * ma * nb, "gemm partials");
+  hipLaunchKernelGGL(gemm_tn_partial_kernel, dim3(unsigned(g.groups), unsigned(g.chunks)),
+                     dim3(256), 0, stream, A, lda, ma, B, ldb, nb, N, g.rows_per_chunk, g.tc,
+                     g.lqg, g.slices, part.p);
   FD_LAUNCH_CHECK();
   const int64_t count = int64_t(ma) * nb;
-  hipLaunchKernelGGL(reduce_partials_kernel, dim3(nblk(count, 256)), dim3(256), 0, stream, part.p,
-                     chunks, count, C, C32);
+  hipLaunchKernelGGL(reduce_partials_kernel, dim3(nblk(count, 32)), dim3(256), 0, stream, part.p,
+                     g.chunks, count, C, C32);
   FD_LAUNCH_CHECK();
 }
 
@@ -432,32 +499,277 @@ __global__ void jacobi_sort_kernel(const double* __restrict__ A, int m, int lda,
   for (int r = 0; r < m; ++r) S[int64_t(r) * lds + rank] = V[int64_t(r) * m + i];
 }
 
+// ---- one-workgroup variant for m <= JL_MAX
+// The upper triangle of A (float64) fits in one workgroup's LDS, so a single
+// workgroup runs whole sweeps with a barrier between rounds instead of a
+// launch per round; blocks whose two rotations are both the identity are
+// skipped (most of them in the last sweeps).  The rotations (c, s) of every
+// round are logged in order; a second kernel replays them on the rows of V
+// (rows are independent under column rotations), one workgroup per group of
+// rows held in LDS.
+
+constexpr int JL_MAX = 192;   // largest m on the one-workgroup path
+constexpr int JL_SWEEPS = 4;  // sweeps per launch (the log holds this many)
+constexpr int JL_BATCH = 16;  // rounds of the log staged in LDS at a time by the replay
+
+// log capacity that every size up to m needs
+size_t jacobi_log_doubles(int m) {
+  const int mc = std::min(m, JL_MAX);
+  const int me = mc + (mc & 1);
+  return size_t(JL_SWEEPS) * me * std::max(me - 1, 1);
+}
+
+// circle-method pair k of round `round` among me players (p < q, q >= m for
+// the dummy player of an odd m)
+__device__ __forceinline__ void circle_pair(int me, int round, int k, int& p, int& q) {
+  const int a = (k == 0) ? 0 : ((round + k - 1) % (me - 1)) + 1;
+  const int bq = ((round + me - 2 - k) % (me - 1)) + 1;
+  p = min(a, bq);
+  q = max(a, bq);
+}
+
+// Up to max_sweeps sweeps on A (m x m, ld lda, symmetric; read at the start,
+// written back in full at the end).  Stops at the start of a sweep whose
+// off-diagonal norm is <= tol * the Frobenius norm.  state[0] = rounds done
+// (their rotations in log, me doubles per round: c, s per pair), state[1] = 1
+// if converged.  sweep0: sweeps done by earlier launches.  An odd m gets a
+// zero row and column m (the circle method's dummy player: its rotations are
+// the identity and it stays zero).  From the fifth sweep on, an A_pq
+// negligible next to both A_pp and A_qq in float64 (100 |A_pq| vanishes when
+// added to either) is set to zero instead of rotated (Rutishauser's rule), so
+// late sweeps leave most blocks untouched.
+__global__ __launch_bounds__(1024) void jacobi_lds_kernel(double* __restrict__ A, int m, int lda,
+                                                          double* __restrict__ log,
+                                                          int* __restrict__ state, double tol2,
+                                                          int max_sweeps, int sweep0) {
+  __shared__ double tri[JL_MAX * (JL_MAX + 1) / 2];
+  __shared__ int4 pr[JL_MAX / 2];      // p, q, row offsets of p and q
+  __shared__ double2 rot[JL_MAX / 2];  // c, s
+  __shared__ double red[2][16];
+  const int t = threadIdx.x;
+  const int nt = blockDim.x;
+  const int me = m + (m & 1), n = me / 2;
+  // upper-triangle position of (r, c), r <= c, in the me x me matrix
+  auto roff = [me](int r) { return r * me - r * (r + 1) / 2; };
+  for (int e = t; e < me * me; e += nt) {
+    const int r = e / me, c = e % me;
+    if (c >= r) tri[roff(r) + c] = (c < m) ? A[int64_t(r) * lda + c] : 0.0;
+  }
+  __syncthreads();
+  // blocks (i, j), i <= j, folded into groups of n + 1: group g holds the
+  // blocks of column pairs g and n - 1 - g (only g for the middle one of an
+  // odd n), TPG threads per group
+  const int ng = (n + 1) / 2;
+  const int tpg = nt / ng;
+  const int grp = t / tpg, gl = t % tpg;
+  const int gcnt = grp < ng ? (2 * grp + 1 == n ? grp + 1 : n + 1) : 0;
+  int rounds = 0, converged = 0;
+  for (int sweep = 0; sweep < max_sweeps; ++sweep) {
+    // squared off-diagonal and total Frobenius norms (fixed reduction order)
+    double off = 0.0, all = 0.0;
+    for (int e = t; e < me * me; e += nt) {
+      const int r = e / me, c = e % me;
+      if (c < r) continue;
+      const double v = tri[roff(r) + c];
+      if (c == r) {
+        all += v * v;
+      } else {
+        off += 2.0 * v * v;
+        all += 2.0 * v * v;
+      }
+    }
+    for (int o = 32; o > 0; o >>= 1) {
+      off += __shfl_down(off, o);
+      all += __shfl_down(all, o);
+    }
+    if ((t & 63) == 0) {
+      red[0][t >> 6] = off;
+      red[1][t >> 6] = all;
+    }
+    __syncthreads();
+    double offs = 0.0, alls = 0.0;
+    for (int w = 0; w < nt / 64; ++w) {
+      offs += red[0][w];
+      alls += red[1][w];
+    }
+    __syncthreads();  // red is rewritten next sweep
+    if (offs <= tol2 * alls) {
+      converged = 1;
+      break;
+    }
+    const bool late = sweep0 + sweep >= 4;
+    for (int round = 0; round < me - 1; ++round) {
+      for (int k = t; k < n; k += nt) {
+        int p, q;
+        circle_pair(me, round, k, p, q);
+        const int rp = roff(p), rq = roff(q);
+        const double apq = tri[rp + q], app = tri[rp + p], aqq = tri[rq + q];
+        double c = 1.0, s = 0.0;
+        const double g = 100.0 * fabs(apq);
+        if (late && fabs(app) + g == fabs(app) && fabs(aqq) + g == fabs(aqq)) {
+          tri[rp + q] = 0.0;
+        } else if (apq != 0.0) {
+          const double tau = (aqq - app) / (2.0 * apq);
+          const double tt = (tau >= 0.0 ? 1.0 : -1.0) / (fabs(tau) + sqrt(1.0 + tau * tau));
+          c = 1.0 / sqrt(1.0 + tt * tt);
+          s = tt * c;
+        }
+        pr[k] = make_int4(p, q, rp, rq);
+        rot[k] = make_double2(c, s);
+        log[(int64_t(rounds) * n + k) * 2] = c;
+        log[(int64_t(rounds) * n + k) * 2 + 1] = s;
+      }
+      __syncthreads();
+      // block (i, j): rows p_i, q_i and columns p_j, q_j become R_i^T X R_j;
+      // each upper-triangle entry belongs to exactly one block with i <= j
+      for (int bk = gl; bk < gcnt; bk += tpg) {
+        const int i = bk <= grp ? bk : bk - grp - 1;
+        const int j = bk <= grp ? grp : n - 1 - grp;
+        const double2 ri = rot[i], rj = rot[j];
+        if (ri.y == 0.0 && rj.y == 0.0) continue;
+        const int4 Pi = pr[i], Pj = pr[j];
+        // position of (r, c) given both row offsets
+        auto pos = [](int r, int ro_r, int c, int ro_c) { return r <= c ? ro_r + c : ro_c + r; };
+        const int xa = pos(Pi.x, Pi.z, Pj.x, Pj.z), xb = pos(Pi.x, Pi.z, Pj.y, Pj.w);
+        const int xd = pos(Pi.y, Pi.w, Pj.x, Pj.z), xe = pos(Pi.y, Pi.w, Pj.y, Pj.w);
+        const double a = tri[xa], b = tri[xb], d = tri[xd], e = tri[xe];
+        const double ci = ri.x, si = ri.y, cj = rj.x, sj = rj.y;
+        const double a1 = ci * a - si * d, b1 = ci * b - si * e;
+        const double d1 = si * a + ci * d, e1 = si * b + ci * e;
+        tri[xa] = cj * a1 - sj * b1;
+        tri[xb] = sj * a1 + cj * b1;
+        if (i != j) tri[xd] = cj * d1 - sj * e1;
+        tri[xe] = sj * d1 + cj * e1;
+      }
+      __syncthreads();
+      ++rounds;
+    }
+  }
+  for (int e = t; e < m * m; e += nt) {
+    const int r = e / m, c = e % m;
+    A[int64_t(r) * lda + c] = r <= c ? tri[roff(r) + c] : tri[roff(c) + r];
+  }
+  if (t == 0) {
+    state[0] = rounds;
+    state[1] = converged;
+  }
+}
+
+// V (m x m, ld m) <- V J_1 J_2 ... for the state[0] logged rounds.  Workgroup
+// w owns rows [w R, w R + R), R = blockDim.x / npairs, thread (row, pair k).
+// Rounds of the log are staged in LDS JL_BATCH at a time, the next batch
+// loaded into registers while the current one is applied.
+__global__ __launch_bounds__(1024) void jacobi_replay_kernel(double* __restrict__ V, int m,
+                                                             const double* __restrict__ log,
+                                                             const int* __restrict__ state) {
+  __shared__ double vs[2048];  // R rows x m <= 2 * blockDim.x (m <= 2 npairs)
+  __shared__ double stage[2][JL_BATCH * JL_MAX];
+  const int t = threadIdx.x;
+  const int nt = blockDim.x;
+  const int me = m + (m & 1), npairs = me / 2;
+  const int R = nt / npairs;
+  const int row0 = blockIdx.x * R;
+  const int nrow = min(R, m - row0);
+  const int rounds = state[0];
+  if (nrow <= 0 || rounds <= 0) return;
+  const int lr = t / npairs, k = t % npairs;
+  const bool active = lr < nrow;
+  for (int e = t; e < nrow * m; e += nt) vs[e] = V[int64_t(row0 + e / m) * m + e % m];
+  const int per_batch = JL_BATCH * me;  // doubles of the log per batch
+  constexpr int PF = (JL_BATCH * JL_MAX + 1023) / 1024;  // loads per thread per batch
+  const int nbatch = (rounds + JL_BATCH - 1) / JL_BATCH;
+  auto fetch = [&](int bt, double (&reg)[PF]) {
+#pragma unroll
+    for (int u = 0; u < PF; ++u) {
+      const int e = t + u * nt;
+      const int64_t g = int64_t(bt) * per_batch + e;
+      reg[u] = (e < per_batch && g < int64_t(rounds) * me) ? log[g] : 0.0;
+    }
+  };
+  auto put = [&](int slot, const double (&reg)[PF]) {
+#pragma unroll
+    for (int u = 0; u < PF; ++u) {
+      const int e = t + u * nt;
+      if (e < per_batch) stage[slot][e] = reg[u];
+    }
+  };
+  double reg[PF];
+  fetch(0, reg);
+  put(0, reg);
+  __syncthreads();
+  for (int bt = 0; bt < nbatch; ++bt) {
+    if (bt + 1 < nbatch) fetch(bt + 1, reg);
+    const int r1 = min(rounds, (bt + 1) * JL_BATCH);
+    for (int r = bt * JL_BATCH; r < r1; ++r) {
+      if (active) {
+        int p, q;
+        circle_pair(me, r % (me - 1), k, p, q);
+        const int o = ((r - bt * JL_BATCH) * npairs + k) * 2;
+        const double c = stage[bt & 1][o], s = stage[bt & 1][o + 1];
+        if (q < m && s != 0.0) {
+          double* v = vs + lr * m;
+          const double vp = v[p], vq = v[q];
+          v[p] = c * vp - s * vq;
+          v[q] = s * vp + c * vq;
+        }
+      }
+      __syncthreads();
+    }
+    if (bt + 1 < nbatch) {
+      put((bt + 1) & 1, reg);
+      __syncthreads();
+    }
+  }
+  for (int e = t; e < nrow * m; e += nt) V[int64_t(row0 + e / m) * m + e % m] = vs[e];
+}
+
 void jacobi_eig(double* A, double* A2, int m, int lda, double* Vw, double* theta, double* S,
-                int lds, double* norms, hipStream_t stream) {
+                int lds, double* norms, FSpanD log, int* state, hipStream_t stream) {
   FD_REQUIRE(m >= 1 && m <= 1024, FD_ERR_UNSUPPORTED, "projected matrix larger than 1024");
   constexpr int MAX_SWEEPS = 60;
   constexpr double TOL = 1e-13;
   const int me = m + (m & 1);
   const int npairs = me / 2;
-  const int64_t items = int64_t(npairs) * npairs + int64_t(m) * npairs;
-  const unsigned grid = unsigned(std::min<int64_t>(2048, std::max<int64_t>(1, (items + 255) / 256)));
   hipLaunchKernelGGL(jacobi_init_kernel, dim3(nblk(int64_t(m) * m, 256)), dim3(256), 0, stream, Vw,
                      m);
   FD_LAUNCH_CHECK();
   double* cur = A;
-  double* nxt = A2;
-  for (int sweep = 0; sweep < MAX_SWEEPS && m > 1; ++sweep) {
-    hipLaunchKernelGGL(jacobi_offnorm_kernel, dim3(1), dim3(1024), 0, stream, cur, m, lda, norms);
-    FD_LAUNCH_CHECK();
-    double h[2] = {0.0, 0.0};
-    FD_HIP_CHECK(hipMemcpyAsync(h, norms, sizeof(h), hipMemcpyDeviceToHost, stream));
-    FD_HIP_CHECK(hipStreamSynchronize(stream));
-    if (h[0] <= TOL * TOL * h[1]) break;
-    for (int round = 0; round < me - 1; ++round) {
-      hipLaunchKernelGGL(jacobi_round_kernel, dim3(grid), dim3(256), 0, stream, cur, nxt, lda, Vw,
-                         m, me, round);
+  if (m > 1 && m <= JL_MAX) {
+    check_span_d(log, jacobi_log_doubles(m), "jacobi rotation log");
+    FD_REQUIRE(lda >= m && state != nullptr, FD_ERR_INVALID_ARG, "internal: jacobi state");
+    const int R = 1024 / npairs;
+    const unsigned rgrid = unsigned((m + R - 1) / R);
+    for (int done = 0; done < MAX_SWEEPS; done += JL_SWEEPS) {
+      hipLaunchKernelGGL(jacobi_lds_kernel, dim3(1), dim3(1024), 0, stream, A, m, lda, log.p,
+                         state, TOL * TOL, std::min(JL_SWEEPS, MAX_SWEEPS - done), done);
       FD_LAUNCH_CHECK();
-      std::swap(cur, nxt);
+      hipLaunchKernelGGL(jacobi_replay_kernel, dim3(rgrid), dim3(1024), 0, stream, Vw, m, log.p,
+                         state);
+      FD_LAUNCH_CHECK();
+      int h[2] = {0, 0};
+      FD_HIP_CHECK(hipMemcpyAsync(h, state, sizeof(h), hipMemcpyDeviceToHost, stream));
+      FD_HIP_CHECK(hipStreamSynchronize(stream));
+      if (h[1]) break;
+    }
+  } else {
+    const int64_t items = int64_t(npairs) * npairs + int64_t(m) * npairs;
+    const unsigned grid =
+        unsigned(std::min<int64_t>(2048, std::max<int64_t>(1, (items + 255) / 256)));
+    double* nxt = A2;
+    for (int sweep = 0; sweep < MAX_SWEEPS && m > 1; ++sweep) {
+      hipLaunchKernelGGL(jacobi_offnorm_kernel, dim3(1), dim3(1024), 0, stream, cur, m, lda,
+                         norms);
+      FD_LAUNCH_CHECK();
+      double h[2] = {0.0, 0.0};
+      FD_HIP_CHECK(hipMemcpyAsync(h, norms, sizeof(h), hipMemcpyDeviceToHost, stream));
+      FD_HIP_CHECK(hipStreamSynchronize(stream));
+      if (h[0] <= TOL * TOL * h[1]) break;
+      for (int round = 0; round < me - 1; ++round) {
+        hipLaunchKernelGGL(jacobi_round_kernel, dim3(grid), dim3(256), 0, stream, cur, nxt, lda,
+                           Vw, m, me, round);
+        FD_LAUNCH_CHECK();
+        std::swap(cur, nxt);
+      }
     }
   }
   hipLaunchKernelGGL(jacobi_sort_kernel, dim3(nblk(m, 256)), dim3(256), 0, stream, cur, m, lda, Vw,
