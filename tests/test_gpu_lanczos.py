@@ -173,3 +173,25 @@ def test_block_width_one():
     e = fd.fd_block_lanczos(to_dev(w.X, dev), 0.5, 3, 1)
     ref = oe.spectrum(w.X.astype(np.float64), 0.5, 0.5, 3)
     assert np.all(np.abs(np.asarray(e.evals) - ref.evals) <= np.maximum(1e-5 * np.abs(ref.evals), 1e-6))
+
+
+@pytest.mark.parametrize("N,k,b", [(191, 40, 32), (255, 40, 64)])
+def test_dense_mode_both_jacobi_paths(N, k, b):
+    # N <= basis width: the eigensolve runs on the whole (odd-sized) projected
+    # matrix; 191 takes the one-workgroup Jacobi (padded with a dummy index),
+    # 255 the launch-per-round one
+    rng = np.random.default_rng(N)
+    X = rng.normal(size=(N, 3)).astype(np.float32)
+    X -= X.mean(0)
+    beta = 1.5
+    sp = oe.spectrum(X.astype(np.float64), beta, 0.5, k + 4)
+    dev = device()
+    case(f"lanczos dense N={N} k={k} b={b}")
+    e = fd.fd_block_lanczos(to_dev(X, dev), beta, k, b)
+    ok_, worst = eval_ok(e.evals, sp.evals[:k])
+    assert ok_, (worst, e.info)
+    phi = to_np(e.evecs)
+    assert np.abs(phi.T @ phi - np.eye(k)).max() <= 1e-5
+    assert max(e.residuals) <= 1e-5
+    for c in clean_cuts(sp.evals, k):
+        assert od.principal_angles(phi[:, :c], sp.phi[:, :c]).max() < 1e-3
