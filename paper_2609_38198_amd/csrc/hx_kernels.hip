@@ -243,12 +243,18 @@ constexpr int hx_waves() {
 
 // ------------------------------------------------------------------ packing
 
-// Piece k (1..3) of v: the float16 nearest to what the earlier pieces leave.
+// Piece k (1..3) of v: the float16 nearest to (the float32 rounding of) what
+// the earlier pieces leave; each remainder is exact in float64.  The float32
+// step is kept explicit (an empty statement on the value): folded into one
+// float64 -> float16 rounding, the conversion has no instruction on gfx950 and
+// becomes a long integer sequence.
 __device__ __forceinline__ float piece_of(double v, int k) {
   v = fmin(fmax(v, -65504.0), 65504.0);
   float out = 0.f;
   for (int q = 1; q <= 3; ++q) {
-    const float h = float(_Float16(float(v)));
+    float vf = float(v);
+    asm volatile("" : "+v"(vf));
+    const float h = float(_Float16(vf));
     if (q == k) {
       out = h;
       break;
@@ -270,6 +276,9 @@ struct HxSlotMap {
 // on the row side); the offset is neg_bl ||x||^2 + shift with
 // neg_bl = -beta log2(e), computed once per thread in float64.  Padded points
 // have zero coordinates and offset -65504, so their kernel values are 0.
+// Every load is issued before any arithmetic (unconditionally, from a valid
+// row and feature, the unused values masked afterwards): one load latency per
+// thread instead of one per slot and per norm term.
 __global__ void pack_hx_kernel(const float* __restrict__ X, int64_t n, int D, int64_t ldx,
                                double scale, double neg_bl, double shift, HxSlotMap map, int nch,
                                int64_t ntiles, uintx4* __restrict__ out) {
@@ -281,31 +290,44 @@ __global__ void pack_hx_kernel(const float* __restrict__ X, int64_t n, int D, in
   const int g = lane >> 4, p = lane & 15;
   const int64_t i = tile * TILE + p;
   const bool real = i < n;
-  const float* xi = X + i * ldx;
-  bool have_a = false;
+  const float* xi = X + min(i, n - 1) * ldx;
+  int code[8];
+  float xv[8];
+  bool need_a = false;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    code[e] = map.code[ch][8 * g + e];
+    const int kind = (code[e] >> 14) & 3;
+    const int f = code[e] & 0xff;
+    need_a = need_a || kind == SEG_A;
+    xv[e] = xi[(kind == SEG_X && f < D) ? f : 0];
+  }
   double a = -65504.0;
+  if (need_a && real) {
+    // ||x||^2 in float64, eight independent loads at a time
+    double r = 0.0;
+    for (int k0 = 0; k0 < D; k0 += 8) {
+      float xk[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) xk[u] = xi[min(k0 + u, D - 1)];
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (k0 + u < D) r += double(xk[u]) * double(xk[u]);
+    }
+    a = neg_bl * r + shift;
+  }
   halfx8 h;
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
-    const int code = map.code[ch][8 * g + e];
-    const int kind = (code >> 14) & 3;
+    const int kind = (code[e] >> 14) & 3;
     float v = 0.f;
     if (kind == SEG_X) {
-      const int f = code & 0xff;
-      if (real && f < D) v = piece_of(scale * double(xi[f]), (code >> 8) & 3);
+      const int f = code[e] & 0xff;
+      if (real && f < D) v = piece_of(scale * double(xv[e]), (code[e] >> 8) & 3);
     } else if (kind == SEG_ONES) {
       v = 1.f;
     } else if (kind == SEG_A) {
-      if (!have_a && real) {
-        double r = 0.0;
-        for (int k = 0; k < D; ++k) {
-          const double x = double(xi[k]);
-          r += x * x;
-        }
-        a = neg_bl * r + shift;
-      }
-      have_a = true;
-      v = piece_of(a, code & 3);
+      v = piece_of(a, code[e] & 3);
     }
     h[e] = _Float16(v);
   }

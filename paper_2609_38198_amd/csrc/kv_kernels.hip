@@ -117,27 +117,41 @@ __global__ void vmax_zero_kernel(unsigned* __restrict__ maxbits) {
   if (threadIdx.x < 64) maxbits[threadIdx.x] = 0u;
 }
 
+// Thread (row lane rl, column c): tc = power of two >= b columns side by side
+// (consecutive addresses of a row), 256 / tc row lanes; the grid strides over
+// the rows, four at a time with their loads issued together; one integer
+// atomicMax per column and workgroup.
 __global__ __launch_bounds__(256) void vmax_kernel(const float* __restrict__ V, int64_t n, int b,
                                                    int64_t ldv, const float* __restrict__ sr,
-                                                   int64_t rows_per_block,
-                                                   unsigned* __restrict__ maxbits) {
+                                                   int tc, unsigned* __restrict__ maxbits) {
   __shared__ float red[256];
-  const int c = threadIdx.x & 63;
-  const int r0 = threadIdx.x >> 6;
-  const int64_t i0 = int64_t(blockIdx.x) * rows_per_block;
-  const int64_t i1 = min(n, i0 + rows_per_block);
+  const int c = threadIdx.x % tc;
+  const int rl = threadIdx.x / tc;
+  const int nrl = 256 / tc;
+  const int64_t stride = int64_t(gridDim.x) * nrl;
   float m = 0.f;
   if (c < b) {
-    for (int64_t i = i0 + r0; i < i1; i += 4) {
-      float v = V[i * ldv + c];
-      if (sr != nullptr) v *= sr[i];
-      m = fmaxf(m, fabsf(v));
+    for (int64_t i = int64_t(blockIdx.x) * nrl + rl; i < n; i += 4 * stride) {
+      float v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int64_t r = min(i + u * stride, n - 1);
+        v[u] = V[r * ldv + c];
+        if (sr != nullptr) v[u] *= sr[r];
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (i + u * stride < n) m = fmaxf(m, fabsf(v[u]));
     }
   }
   red[threadIdx.x] = m;
   __syncthreads();
-  if (threadIdx.x < 64) {
-    m = fmaxf(fmaxf(red[c], red[c + 64]), fmaxf(red[c + 128], red[c + 192]));
+  for (int w = 128; w >= tc; w >>= 1) {
+    if (threadIdx.x < w) red[threadIdx.x] = fmaxf(red[threadIdx.x], red[threadIdx.x + w]);
+    __syncthreads();
+  }
+  if (threadIdx.x < tc) {
+    m = red[threadIdx.x];
     if (c < b && m > 0.f) atomicMax(&maxbits[c], __float_as_uint(m));
   }
 }
@@ -848,9 +862,12 @@ void launch_pack_v_split(const float* V, int64_t n, int64_t b, int64_t ldv, cons
   float* colscale = vscale.p + 64;
   hipLaunchKernelGGL(vmax_zero_kernel, dim3(1), dim3(64), 0, stream, maxbits);
   FD_LAUNCH_CHECK();
-  const int64_t rpb = 64;  // many small blocks: the pass is bandwidth bound
-  hipLaunchKernelGGL(vmax_kernel, dim3(blocks_for(n, int(rpb))), dim3(256), 0, stream, V, n,
-                     int(b), ldv, sr, rpb, maxbits);
+  int tc = 1;
+  while (tc < b) tc *= 2;
+  const int64_t nrl = 256 / tc;
+  const unsigned vgrid = unsigned(std::min<int64_t>(256, std::max<int64_t>(1, (n + 4 * nrl - 1) / (4 * nrl))));
+  hipLaunchKernelGGL(vmax_kernel, dim3(vgrid), dim3(256), 0, stream, V, n, int(b), ldv, sr, tc,
+                     maxbits);
   FD_LAUNCH_CHECK();
   const int64_t total = npairs * ncb * 64;
   hipLaunchKernelGGL(pack_v_split_kernel, dim3(blocks_for(total, 256)), dim3(256), 0, stream, V,

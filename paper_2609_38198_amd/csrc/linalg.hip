@@ -4,7 +4,8 @@
 //   * Cholesky of a small Gram matrix with detection of dependent columns,
 //   * refill of such columns from a counter-based normal generator,
 //   * residual norms ||W s - theta Q s|| of Ritz pairs,
-//   * cyclic Jacobi eigensolver for the small symmetric projected matrix.
+//   * parallel cyclic Jacobi eigensolver for the small symmetric projected
+//     matrix.
 // Everything is deterministic: no atomics, fixed reduction orders.
 #include <algorithm>
 #include <cmath>
@@ -366,13 +367,19 @@ void residual_norms(const float* Y, const float* W, int64_t ld, int nc, const do
 // (Alg. 8.5.2).  Because the pairs of a round are disjoint, the round's
 // similarity transform acts on A block by block: for row pair i and column
 // pair j the 2 x 2 block (rows p_i, q_i; columns p_j, q_j) becomes
-// R_i^T X R_j.  One launch per round does all blocks (and the matching
-// column rotations of the eigenvector matrix) with as many workgroups as the
-// size needs, reading A and writing its transform to a second buffer; every
-// workgroup recomputes the round's rotations from the (unchanged) input.
-// After each sweep the off-diagonal Frobenius norm is checked on the host
-// (one scalar read back).  On exit theta (m) holds the eigenvalues sorted
-// descending and S (m x m, ld lds) the matching eigenvectors in its columns.
+// R_i^T X R_j.  Two ways to run the rounds:
+//   * m <= JL_MAX: one workgroup holds the upper triangle in LDS and runs
+//     whole sweeps with a barrier between rounds (jacobi_lds_kernel); the
+//     rotations are logged and replayed on the eigenvector matrix by a
+//     second kernel (jacobi_replay_kernel);
+//   * larger m: one launch per round does all blocks (and the matching
+//     column rotations of the eigenvector matrix) with as many workgroups as
+//     the size needs, reading A and writing its transform to a second buffer;
+//     every workgroup recomputes the round's rotations from the (unchanged)
+//     input, and after each sweep the off-diagonal Frobenius norm is checked
+//     on the host (one scalar read back).
+// On exit theta (m) holds the eigenvalues sorted descending and S (m x m,
+// ld lds) the matching eigenvectors in its columns.
 
 // pair k of round `round` among me (even) players: indices p < q, q = -1 for
 // the dummy player of an odd m; rotation (c, s) annihilating A_pq
