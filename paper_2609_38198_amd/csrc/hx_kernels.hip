@@ -242,111 +242,96 @@ constexpr int hx_waves() {
 }
 
 // ------------------------------------------------------------------ packing
+//
+// One thread per (padded) point computes the three float16 pieces of each
+// coordinate (scaled) and of the offset once, and writes all of the point's
+// slots, whose contents are resolved at compile time from the recipe.
+// `scale` multiplies the coordinates (s on the column side, 2 beta log2(e) / s
+// on the row side); the offset is neg_bl ||x||^2 + shift with
+// neg_bl = -beta log2(e), in float64.  Padded points have zero coordinates and
+// offset -65504, so their kernel values are 0.
+template <int RID, bool ROW>
+constexpr const HxSide& hx_side() {
+  return ROW ? HX_TABLE[RID].row : HX_TABLE[RID].col;
+}
 
-// Piece k (1..3) of v: the float16 nearest to (the float32 rounding of) what
-// the earlier pieces leave; each remainder is exact in float64.  The float32
+// The pieces of v: each the float16 nearest to (the float32 rounding of) what
+// the earlier ones leave; each remainder is exact in float64.  The float32
 // step is kept explicit (an empty statement on the value): folded into one
 // float64 -> float16 rounding, the conversion has no instruction on gfx950 and
 // becomes a long integer sequence.
-__device__ __forceinline__ float piece_of(double v, int k) {
+__device__ __forceinline__ void pieces3(double v, float (&out)[3]) {
   v = fmin(fmax(v, -65504.0), 65504.0);
-  float out = 0.f;
-  for (int q = 1; q <= 3; ++q) {
+#pragma unroll
+  for (int q = 0; q < 3; ++q) {
     float vf = float(v);
     asm volatile("" : "+v"(vf));
     const float h = float(_Float16(vf));
-    if (q == k) {
-      out = h;
-      break;
-    }
+    out[q] = h;
     v -= double(h);
   }
-  return out;
 }
 
-// Slot map of one side: per chunk and slot, what the slot holds, decoded from
-// the recipe's segments on the host: 0 = zero, SEG_X << 14 | piece << 8 |
-// feature, SEG_ONES << 14, SEG_A << 14 | piece.
-struct HxSlotMap {
-  int16_t code[HX_CHUNKS][32];
-};
+// value of slot S = 32 ch + 8 g + e of the point
+template <int RID, bool ROW, int S, int M>
+__device__ __forceinline__ _Float16 hx_slot_value(const float (&px)[M][3], const float (&pa)[3]) {
+  constexpr HxSlot v = hx_slot(hx_side<RID, ROW>().ch[S / 32], S % 32);
+  if constexpr (v.kind == SEG_X && v.feat < M && v.piece >= 1 && v.piece <= 3)
+    return _Float16(px[v.feat][v.piece - 1]);
+  else if constexpr (v.kind == SEG_ONES)
+    return _Float16(1.f);
+  else if constexpr (v.kind == SEG_A && v.piece >= 1 && v.piece <= 3)
+    return _Float16(pa[v.piece - 1]);
+  else
+    return _Float16(0.f);
+}
 
-// One thread per (tile, chunk, lane): the lane's eight slots of the chunk.
-// `scale` multiplies the coordinates (s on the column side, 2 beta log2(e) / s
-// on the row side); the offset is neg_bl ||x||^2 + shift with
-// neg_bl = -beta log2(e), computed once per thread in float64.  Padded points
-// have zero coordinates and offset -65504, so their kernel values are 0.
-// Every load is issued before any arithmetic (unconditionally, from a valid
-// row and feature, the unused values masked afterwards): one load latency per
-// thread instead of one per slot and per norm term.
-__global__ void pack_hx_kernel(const float* __restrict__ X, int64_t n, int D, int64_t ldx,
-                               double scale, double neg_bl, double shift, HxSlotMap map, int nch,
-                               int64_t ntiles, uintx4* __restrict__ out) {
-  const int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (idx >= ntiles * nch * 64) return;
-  const int lane = int(idx & 63);
-  const int ch = int((idx >> 6) % nch);
-  const int64_t tile = idx / (64 * nch);
-  const int g = lane >> 4, p = lane & 15;
-  const int64_t i = tile * TILE + p;
+// lane (g, p) word of chunk ch, for CG = 4 ch + g = 0 .. 4 nch - 1
+template <int RID, bool ROW, int NCH, int M, int CG = 0>
+__device__ __forceinline__ void hx_emit(const float (&px)[M][3], const float (&pa)[3],
+                                        uintx4* __restrict__ out, int64_t tile, int p) {
+  if constexpr (CG < 4 * NCH) {
+    constexpr int CH = CG / 4, G = CG % 4, S = 32 * CH + 8 * G;
+    halfx8 h;
+    h[0] = hx_slot_value<RID, ROW, S + 0, M>(px, pa);
+    h[1] = hx_slot_value<RID, ROW, S + 1, M>(px, pa);
+    h[2] = hx_slot_value<RID, ROW, S + 2, M>(px, pa);
+    h[3] = hx_slot_value<RID, ROW, S + 3, M>(px, pa);
+    h[4] = hx_slot_value<RID, ROW, S + 4, M>(px, pa);
+    h[5] = hx_slot_value<RID, ROW, S + 5, M>(px, pa);
+    h[6] = hx_slot_value<RID, ROW, S + 6, M>(px, pa);
+    h[7] = hx_slot_value<RID, ROW, S + 7, M>(px, pa);
+    out[(tile * NCH + CH) * 64 + 16 * G + p] = __builtin_bit_cast(uintx4, h);
+    hx_emit<RID, ROW, NCH, M, CG + 1>(px, pa, out, tile, p);
+  }
+}
+
+template <int RID, bool ROW>
+__global__ __launch_bounds__(256) void pack_hx_point_kernel(const float* __restrict__ X, int64_t n,
+                                                            int D, int64_t ldx, double scale,
+                                                            double neg_bl, double shift,
+                                                            int64_t npad,
+                                                            uintx4* __restrict__ out) {
+  constexpr int M = HX_TABLE[RID].maxd;
+  constexpr int NCH = ROW ? HX_TABLE[RID].nb : HX_TABLE[RID].nc;
+  const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i >= npad) return;
   const bool real = i < n;
   const float* xi = X + min(i, n - 1) * ldx;
-  int code[8];
-  float xv[8];
-  bool need_a = false;
+  float xv[M];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    code[e] = map.code[ch][8 * g + e];
-    const int kind = (code[e] >> 14) & 3;
-    const int f = code[e] & 0xff;
-    need_a = need_a || kind == SEG_A;
-    xv[e] = xi[(kind == SEG_X && f < D) ? f : 0];
+  for (int f = 0; f < M; ++f) xv[f] = xi[min(f, D - 1)];
+  float px[M][3];
+  double r = 0.0;
+#pragma unroll
+  for (int f = 0; f < M; ++f) {
+    const bool use = real && f < D;
+    if (use) r += double(xv[f]) * double(xv[f]);
+    pieces3(use ? scale * double(xv[f]) : 0.0, px[f]);
   }
-  double a = -65504.0;
-  if (need_a && real) {
-    // ||x||^2 in float64, eight independent loads at a time
-    double r = 0.0;
-    for (int k0 = 0; k0 < D; k0 += 8) {
-      float xk[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) xk[u] = xi[min(k0 + u, D - 1)];
-#pragma unroll
-      for (int u = 0; u < 8; ++u)
-        if (k0 + u < D) r += double(xk[u]) * double(xk[u]);
-    }
-    a = neg_bl * r + shift;
-  }
-  halfx8 h;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const int kind = (code[e] >> 14) & 3;
-    float v = 0.f;
-    if (kind == SEG_X) {
-      const int f = code[e] & 0xff;
-      if (real && f < D) v = piece_of(scale * double(xv[e]), (code[e] >> 8) & 3);
-    } else if (kind == SEG_ONES) {
-      v = 1.f;
-    } else if (kind == SEG_A) {
-      v = piece_of(a, code[e] & 3);
-    }
-    h[e] = _Float16(v);
-  }
-  out[idx] = __builtin_bit_cast(uintx4, h);
-}
-
-// Slot map of a recipe side (the segments are checked at compile time).
-HxSlotMap hx_slot_map(const HxSide& side, int nch) {
-  HxSlotMap m{};
-  for (int c = 0; c < nch; ++c)
-    for (int slot = 0; slot < 32; ++slot) {
-      const HxSlot v = hx_slot(side.ch[c], slot);
-      int code = 0;
-      if (v.kind == SEG_X) code = (SEG_X << 14) | (v.piece << 8) | v.feat;
-      if (v.kind == SEG_ONES) code = SEG_ONES << 14;
-      if (v.kind == SEG_A) code = (SEG_A << 14) | v.piece;
-      m.code[c][slot] = int16_t(code);
-    }
-  return m;
+  float pa[3];
+  pieces3(real ? neg_bl * r + shift : -65504.0, pa);
+  hx_emit<RID, ROW, NCH, M>(px, pa, out, i / TILE, int(i % TILE));
 }
 
 // ------------------------------------------------------------------ exponent
@@ -1108,10 +1093,30 @@ void launch_pack_points_hx(const float* X, int64_t n, int64_t D, int64_t ldx, do
   if (beta > 0.0) e = std::clamp(int(std::lround(0.5 * std::log2(2.0 * bl))), -12, 12);
   const double s = std::ldexp(1.0, e);
   const double scale = row_side ? 2.0 * bl / s : s;
-  const HxSlotMap map = hx_slot_map(row_side ? R.row : R.col, nch);
-  hipLaunchKernelGGL(pack_hx_kernel, dim3(blocks_for(ntiles * nch * 64, 256)), dim3(256), 0,
-                     stream, X, n, int(D), ldx, scale, -bl, row_side ? double(SHIFT) : 0.0, map,
-                     nch, ntiles, reinterpret_cast<uintx4*>(out.xp.p));
+  const double shift = row_side ? double(SHIFT) : 0.0;
+  uintx4* xp = reinterpret_cast<uintx4*>(out.xp.p);
+  const dim3 grid(blocks_for(out.npad, 256));
+  auto go = [&](auto rid_, auto row_) {
+    constexpr int RID = decltype(rid_)::value;
+    constexpr bool ROW = decltype(row_)::value;
+    hipLaunchKernelGGL((pack_hx_point_kernel<RID, ROW>), grid, dim3(256), 0, stream, X, n, int(D),
+                       ldx, scale, -bl, shift, out.npad, xp);
+  };
+  auto side = [&](auto rid_) {
+    if (row_side)
+      go(rid_, std::true_type{});
+    else
+      go(rid_, std::false_type{});
+  };
+  switch (rid) {
+    case 0: side(std::integral_constant<int, 0>{}); break;
+    case 1: side(std::integral_constant<int, 1>{}); break;
+    case 2: side(std::integral_constant<int, 2>{}); break;
+    case 3: side(std::integral_constant<int, 3>{}); break;
+    case 4: side(std::integral_constant<int, 4>{}); break;
+    case 5: side(std::integral_constant<int, 5>{}); break;
+    default: side(std::integral_constant<int, 6>{}); break;
+  }
   FD_LAUNCH_CHECK();
   out.rid = rid;
   out.row_side = row_side;
