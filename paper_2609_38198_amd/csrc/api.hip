@@ -142,6 +142,23 @@ void degree_run(DegreeWs& w, const void* X, fd_dtype xt, int64_t N, int64_t D, i
     launch_pack_points(X, xt, N, D, ldx, beta, false, w.cols, stream);
   }
   float* qq = q != nullptr ? q : w.q;
+  if (rowsum_sym_applies(w.rows, w.cols, true, w.colfix)) {
+    // symmetric row sums with the epilogues fused into their reductions; the
+    // first reduction leaves the column-sum words zeroed for the second pass
+    const SymPass p1 = launch_rowsum_sym_pass(w.plan, w.rows, w.cols, FSpan{}, w.part, w.colfix,
+                                              true, stream);
+    launch_degree_reduce_q(p1, w.rows, w.cols, w.part, w.colfix, qq, alpha,
+                           alpha == 0.0 ? FSpan{} : w.wp, stream);
+    if (s_off != nullptr) launch_sum_minus_n(qq, N, s_off, stream);
+    if (alpha == 0.0) {
+      launch_degree_finish(qq, qq, N, 0.0, d, s, stream);
+      return;
+    }
+    const SymPass p2 = launch_rowsum_sym_pass(w.plan, w.rows, w.cols, w.wp, w.part, w.colfix,
+                                              false, stream);
+    launch_degree_reduce_ds(p2, w.rows, w.part, w.colfix, qq, alpha, d, s, stream);
+    return;
+  }
   launch_rowsum(w.plan, w.rows, w.cols, FSpan{}, true, qq, w.part, stream, w.colfix);
   if (s_off != nullptr) launch_sum_minus_n(qq, N, s_off, stream);
   if (alpha == 0.0) {

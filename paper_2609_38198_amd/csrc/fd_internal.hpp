@@ -151,6 +151,28 @@ void launch_rowsum(const KVPlan& p, const PointPack& rows, const PointPack& cols
                    bool diag, float* out, FSpan part, hipStream_t stream,
                    unsigned long long* colfix = nullptr);
 KVPlan plan_rowsum_sym(int64_t N, int64_t npad, int dp, int nib);
+// The symmetric path piece by piece (the two normalisation passes fuse their
+// epilogues into its reduction): whether it applies, one pass of the kernel
+// (row partials in part, fixed-point column sums added into colfix, which is
+// zeroed first if asked), and the fused reductions.  Each reduction leaves
+// colfix zeroed.  launch_degree_reduce_q: q, and w = q^-alpha into the weight
+// pack (the column pack's extent) when wp.p is set; launch_degree_reduce_ds: d = w t and s = w d^-1/2
+// (either may be NULL).
+struct SymPass {
+  int nsplit = 0;
+  double inv_fix = 0.0;
+};
+bool rowsum_sym_applies(const PointPack& rows, const PointPack& cols, bool diag,
+                        const unsigned long long* colfix);
+SymPass launch_rowsum_sym_pass(const KVPlan& p, const PointPack& rows, const PointPack& cols,
+                               FSpan wp, FSpan part, unsigned long long* colfix, bool zero_colfix,
+                               hipStream_t stream);
+void launch_degree_reduce_q(const SymPass& sp, const PointPack& rows, const PointPack& cols,
+                            FSpan part, unsigned long long* colfix, float* q, double alpha,
+                            FSpan wp, hipStream_t stream);
+void launch_degree_reduce_ds(const SymPass& sp, const PointPack& rows, FSpan part,
+                             unsigned long long* colfix, const float* q, double alpha, float* d,
+                             float* s, hipStream_t stream);
 // Row tiles per wave of the symmetric row sums, and the fewest column splits
 // of their large-problem plans.
 constexpr int SYM_NIB = 8;

@@ -670,6 +670,61 @@ __global__ void degree_finish_kernel(const float* __restrict__ q, const float* _
   if (s != nullptr) s[i] = float(w / sqrt(dd));
 }
 
+// The two normalisation passes on the symmetric path with their epilogues in
+// the reductions (same arithmetic, in the same order, as reduce_rowsum_sym +
+// pow_neg + pack_w and reduce_rowsum_sym + degree_finish).  One thread per
+// padded point; each clears its fixed-point column sum for the next pass.
+// Pass 1: q_i, and if wpk is set w_i = q_i^-alpha written to the weight pack
+// (pack_w_kernel's layout: w_j in lanes 16 g + p, p = 0..15, component r of
+// tile j / 16, j % 16 = 4 g + r; 0 for padding points) for the wnpad points
+// of the column pack.
+__global__ void degree_reduce_q_kernel(const float* __restrict__ part, int nsplit, int64_t nrpad,
+                                       unsigned long long* __restrict__ colfix, double inv_fix,
+                                       float* __restrict__ q, int64_t n, int64_t npad,
+                                       double alpha, float* __restrict__ wpk, int64_t wnpad) {
+  const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i >= npad) return;
+  float w = 0.f;
+  if (i < n) {
+    double sum = 0.0;
+    for (int k = 0; k < nsplit; ++k) sum += double(part[k * nrpad + i]);
+    sum += double(static_cast<long long>(colfix[i])) * inv_fix;
+    const float qi = float(sum);
+    q[i] = qi;
+    w = float(pow(double(qi), -alpha));
+  }
+  colfix[i] = 0ull;
+  if (wpk != nullptr && i < wnpad) {
+    const int64_t jb = i / TILE;
+    const int jj = int(i % TILE), g = jj / 4, r = jj % 4;
+    float* base = wpk + (jb * 64 + 16 * g) * 4 + r;
+#pragma unroll
+    for (int p = 0; p < 16; ++p) base[4 * p] = w;
+  }
+}
+
+// Pass 2: t_i (the weighted row sums), then d_i = w_i t_i and
+// s_i = w_i d_i^-1/2 with w_i = q_i^-alpha in double.
+__global__ void degree_reduce_ds_kernel(const float* __restrict__ part, int nsplit, int64_t nrpad,
+                                        unsigned long long* __restrict__ colfix, double inv_fix,
+                                        const float* __restrict__ q, int64_t n, int64_t npad,
+                                        double alpha, float* __restrict__ d,
+                                        float* __restrict__ s) {
+  const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i >= npad) return;
+  if (i < n) {
+    double sum = 0.0;
+    for (int k = 0; k < nsplit; ++k) sum += double(part[k * nrpad + i]);
+    sum += double(static_cast<long long>(colfix[i])) * inv_fix;
+    const float ti = float(sum);
+    const double w = pow(double(q[i]), -alpha);
+    const double dd = w * double(ti);
+    if (d != nullptr) d[i] = float(dd);
+    if (s != nullptr) s[i] = float(w / sqrt(dd));
+  }
+  colfix[i] = 0ull;
+}
+
 // sum(q) - n in double, one workgroup, fixed order (deterministic)
 __global__ __launch_bounds__(1024) void sum_minus_n_kernel(const float* __restrict__ q, int64_t n,
                                                             double* __restrict__ out) {
@@ -986,25 +1041,62 @@ static void rowsum_bf16_launch(const KVPlan& p, const PointPack& rows, const Poi
 }
 
 
+bool rowsum_sym_applies(const PointPack& rows, const PointPack& cols, bool diag,
+                        const unsigned long long* colfix) {
+  return colfix != nullptr && diag && !rows.bf16 && !cols.bf16 && rows.n == cols.n;
+}
+
+SymPass launch_rowsum_sym_pass(const KVPlan& p, const PointPack& rows, const PointPack& cols,
+                               FSpan wp, FSpan part, unsigned long long* colfix, bool zero_colfix,
+                               hipStream_t stream) {
+  check_tiles(p, rows, cols);
+  FD_REQUIRE(rowsum_sym_applies(rows, cols, true, colfix), FD_ERR_INVALID_ARG,
+             "internal: symmetric row sums need one float32 point set");
+  const KVPlan sp = plan_rowsum_sym(rows.n, rows.npad, p.dp, SYM_NIB);
+  if (wp.p != nullptr) check_span(wp, lane4_extent(sp.njb, 1), "weight pack");
+  check_span(part, size_t(sp.nsplit) * rows.npad, "partial row sums");
+  // fixed point with F fractional bits: the total of weights in [0, 1] over
+  // npad columns stays below 2^62 / 4
+  const int F = 62 - int(std::ceil(std::log2(double(rows.npad)))) - 2;
+  if (zero_colfix) {
+    hipLaunchKernelGGL(zero_u64_kernel, dim3(blocks_for(rows.npad, 256)), dim3(256), 0, stream,
+                       colfix, rows.npad);
+    FD_LAUNCH_CHECK();
+  }
+  launch_rowsum_sym_hx(sp, rows, cols, wp.p, part.p, colfix, std::ldexp(1.0, F - 15), stream);
+  return SymPass{int(sp.nsplit), std::ldexp(1.0, -F)};
+}
+
+void launch_degree_reduce_q(const SymPass& sp, const PointPack& rows, const PointPack& cols,
+                            FSpan part, unsigned long long* colfix, float* q, double alpha,
+                            FSpan wp, hipStream_t stream) {
+  FD_REQUIRE(cols.npad % TILE == 0 && cols.npad <= rows.npad && cols.n == rows.n,
+             FD_ERR_INVALID_ARG, "internal: bad weight pack geometry");
+  if (wp.p != nullptr) check_span(wp, lane4_extent(cols.npad / TILE, 1), "weight pack");
+  hipLaunchKernelGGL(degree_reduce_q_kernel, dim3(blocks_for(rows.npad, 256)), dim3(256), 0,
+                     stream, part.p, sp.nsplit, rows.npad, colfix, sp.inv_fix, q, rows.n,
+                     rows.npad, alpha, wp.p, cols.npad);
+  FD_LAUNCH_CHECK();
+}
+
+void launch_degree_reduce_ds(const SymPass& sp, const PointPack& rows, FSpan part,
+                             unsigned long long* colfix, const float* q, double alpha, float* d,
+                             float* s, hipStream_t stream) {
+  hipLaunchKernelGGL(degree_reduce_ds_kernel, dim3(blocks_for(rows.npad, 256)), dim3(256), 0,
+                     stream, part.p, sp.nsplit, rows.npad, colfix, sp.inv_fix, q, rows.n,
+                     rows.npad, alpha, d, s);
+  FD_LAUNCH_CHECK();
+}
+
 void launch_rowsum(const KVPlan& p, const PointPack& rows, const PointPack& cols, FSpan wp,
                    bool diag, float* out, FSpan part, hipStream_t stream,
                    unsigned long long* colfix) {
   check_tiles(p, rows, cols);
-  if (colfix != nullptr && diag && !rows.bf16 && !cols.bf16 && rows.n == cols.n) {
+  if (rowsum_sym_applies(rows, cols, diag, colfix)) {
     // one point set: each off-diagonal tile serves its rows and its columns
-    const KVPlan sp = plan_rowsum_sym(rows.n, rows.npad, p.dp, SYM_NIB);
-    if (wp.p != nullptr) check_span(wp, lane4_extent(sp.njb, 1), "weight pack");
-    check_span(part, size_t(sp.nsplit) * rows.npad, "partial row sums");
-    // fixed point with F fractional bits: the total of weights in [0, 1] over
-    // npad columns stays below 2^62 / 4
-    const int F = 62 - int(std::ceil(std::log2(double(rows.npad)))) - 2;
-    hipLaunchKernelGGL(zero_u64_kernel, dim3(blocks_for(rows.npad, 256)), dim3(256), 0, stream,
-                       colfix, rows.npad);
-    FD_LAUNCH_CHECK();
-    launch_rowsum_sym_hx(sp, rows, cols, wp.p, part.p, colfix, std::ldexp(1.0, F - 15), stream);
+    const SymPass sp = launch_rowsum_sym_pass(p, rows, cols, wp, part, colfix, true, stream);
     hipLaunchKernelGGL(reduce_rowsum_sym_kernel, dim3(blocks_for(rows.n, 256)), dim3(256), 0,
-                       stream, part.p, sp.nsplit, rows.npad, colfix, std::ldexp(1.0, -F), out,
-                       rows.n);
+                       stream, part.p, sp.nsplit, rows.npad, colfix, sp.inv_fix, out, rows.n);
     FD_LAUNCH_CHECK();
     return;
   }
