@@ -381,15 +381,32 @@ void residual_norms(const float* Y, const float* W, int64_t ld, int nc, const do
 // On exit theta (m) holds the eigenvalues sorted descending and S (m x m,
 // ld lds) the matching eigenvectors in its columns.
 
+// circle-method pair k of round `round` among me players (p < q, q >= m for
+// the dummy player of an odd m)
+__device__ __forceinline__ void circle_pair(int me, int round, int k, int& p, int& q) {
+  const int a = (k == 0) ? 0 : ((round + k - 1) % (me - 1)) + 1;
+  const int bq = ((round + me - 2 - k) % (me - 1)) + 1;
+  p = min(a, bq);
+  q = max(a, bq);
+}
+
+// rotation (c, s) annihilating A_pq (apq != 0): t = tan of the angle, the
+// smaller root of t^2 + 2 tau t - 1 = 0 (the 2 x 2 symmetric Schur
+// decomposition of Golub & Van Loan)
+__device__ __forceinline__ void jacobi_rotation(double app, double aqq, double apq, double& c,
+                                                double& s) {
+  const double tau = (aqq - app) / (2.0 * apq);
+  const double tt = (tau >= 0.0 ? 1.0 : -1.0) / (fabs(tau) + sqrt(1.0 + tau * tau));
+  c = 1.0 / sqrt(1.0 + tt * tt);
+  s = tt * c;
+}
+
 // pair k of round `round` among me (even) players: indices p < q, q = -1 for
 // the dummy player of an odd m; rotation (c, s) annihilating A_pq
 __device__ __forceinline__ void jacobi_pair(const double* __restrict__ A, int lda, int m, int me,
                                             int round, int k, int& p, int& q, double& c,
                                             double& s) {
-  const int a = (k == 0) ? 0 : ((round + k - 1) % (me - 1)) + 1;
-  const int bq = ((round + me - 2 - k) % (me - 1)) + 1;
-  p = min(a, bq);
-  q = max(a, bq);
+  circle_pair(me, round, k, p, q);
   c = 1.0;
   s = 0.0;
   if (q >= m) {
@@ -397,13 +414,7 @@ __device__ __forceinline__ void jacobi_pair(const double* __restrict__ A, int ld
     return;
   }
   const double apq = A[int64_t(p) * lda + q];
-  if (apq != 0.0) {
-    const double app = A[int64_t(p) * lda + p], aqq = A[int64_t(q) * lda + q];
-    const double tau = (aqq - app) / (2.0 * apq);
-    const double tt = (tau >= 0.0 ? 1.0 : -1.0) / (fabs(tau) + sqrt(1.0 + tau * tau));
-    c = 1.0 / sqrt(1.0 + tt * tt);
-    s = tt * c;
-  }
+  if (apq != 0.0) jacobi_rotation(A[int64_t(p) * lda + p], A[int64_t(q) * lda + q], apq, c, s);
 }
 
 // One round: B = J^T A J block by block, V <- V J (in place).
@@ -526,14 +537,6 @@ size_t jacobi_log_doubles(int m) {
   return size_t(JL_SWEEPS) * me * std::max(me - 1, 1);
 }
 
-// circle-method pair k of round `round` among me players (p < q, q >= m for
-// the dummy player of an odd m)
-__device__ __forceinline__ void circle_pair(int me, int round, int k, int& p, int& q) {
-  const int a = (k == 0) ? 0 : ((round + k - 1) % (me - 1)) + 1;
-  const int bq = ((round + me - 2 - k) % (me - 1)) + 1;
-  p = min(a, bq);
-  q = max(a, bq);
-}
 
 // Up to max_sweeps sweeps on A (m x m, ld lda, symmetric; read at the start,
 // written back in full at the end).  Stops at the start of a sweep whose
@@ -615,12 +618,9 @@ __global__ __launch_bounds__(1024) void jacobi_lds_kernel(double* __restrict__ A
         const double g = 100.0 * fabs(apq);
         if (late && fabs(app) + g == fabs(app) && fabs(aqq) + g == fabs(aqq)) {
           tri[rp + q] = 0.0;
-        } else if (apq != 0.0) {
-          const double tau = (aqq - app) / (2.0 * apq);
-          const double tt = (tau >= 0.0 ? 1.0 : -1.0) / (fabs(tau) + sqrt(1.0 + tau * tau));
-          c = 1.0 / sqrt(1.0 + tt * tt);
-          s = tt * c;
-        }
+          } else if (apq != 0.0) {
+            jacobi_rotation(app, aqq, apq, c, s);
+          }
         pr[k] = make_int4(p, q, rp, rq);
         rot[k] = make_double2(c, s);
         log[(int64_t(rounds) * n + k) * 2] = c;
