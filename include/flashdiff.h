@@ -67,7 +67,9 @@ typedef enum fd_op {
 typedef struct fd_lanczos_opts {
   double tol;               /* converged when ||M phi - theta phi||_2 <= tol (||M||_2 = 1). Default 1e-5 */
   int32_t max_restarts;     /* restart cycles before FD_ERR_NOT_CONVERGED. Default 200 */
-  int32_t max_basis_blocks; /* basis capacity in blocks of b (0 = automatic: k + keep + 4b, rounded) */
+  int32_t max_basis_blocks; /* basis capacity in blocks of b (0 = automatic: k + keep rounded up to
+                               whole blocks, plus as many again but at least 2 blocks; at most
+                               1024 columns) */
   int32_t keep;             /* Ritz vectors kept at restart beyond k (-1 = automatic: b) */
   int32_t max_matvecs;      /* stop after this many block products (0 = no limit). A run that
                                stops this way returns FD_ERR_NOT_CONVERGED with valid Ritz pairs */
