@@ -1,0 +1,93 @@
+"""Parity at the full sizes of the larger workloads, on sampled rows.
+
+The noisy 6-torus at n = 262,144 (D = 12, b = 32), the molecule-like set at
+N = 2^20 (D = 30, b = 32) and the bfloat16 stress set at N = 2^21 (D = 64,
+b = 64), each through the kernels and launch configurations the bench legs
+time.  The oracle evaluates the float64 difference-form definition on a
+seeded subset of output rows against all N columns: row sums q_S, raw K V,
+s on those rows (from the device's q for the other points), the normalised
+product diag(s) K diag(s) V with the device's s, and for the molecule set
+the true residuals (M phi - theta phi)_S of the top-64 Ritz pairs.
+"""
+import numpy as np
+import pytest
+
+from gpu_util import TOL_BF16, TOL_F32, case, device, rel_fro, to_dev, to_np
+from oracle import kernel as ok
+from paper_2609_38198_amd import _lib as fd
+from paper_2609_38198_amd import inputs
+
+pytestmark = pytest.mark.gpu
+
+ALPHA = 0.5
+
+
+def _degree_and_products(X_dev, X64, beta, V, rows, tol):
+    dev = device()
+    deg = fd.fd_degree(X_dev, beta, ALPHA)
+    q = to_np(deg.q)
+    s = to_np(deg.s)
+    Vd = to_dev(V, dev)
+    Y0 = to_np(fd.fd_kernel_matmul(X_dev, None, beta, Vd))
+    Y = to_np(fd.fd_kernel_matmul(X_dev, None, beta, Vd, sl=deg.s, sr=deg.s))
+    ones = np.ones((X64.shape[0], 1))
+    q_ref = ok.kernel_matmul(X64, None, beta, ones, rows=rows, threads=8)[:, 0]
+    assert rel_fro(q[rows], q_ref) <= tol
+    # s on the sampled rows from w = q^-alpha of every point (device q, checked above on S)
+    w = q ** -ALPHA
+    t_ref = ok.kernel_matmul(X64, None, beta, w[:, None], rows=rows, threads=8)[:, 0]
+    s_ref = w[rows] / np.sqrt(w[rows] * t_ref)
+    assert rel_fro(s[rows], s_ref) <= tol
+    y0_ref = ok.kernel_matmul(X64, None, beta, V, rows=rows, threads=8)
+    assert rel_fro(Y0[rows], y0_ref) <= tol
+    y_ref = ok.kernel_matmul(X64, None, beta, V, sl=s, sr=s, rows=rows, threads=8)
+    assert rel_fro(Y[rows], y_ref) <= tol
+    return deg, s
+
+
+@pytest.mark.parametrize("beta", [0.5, 8.0])
+def test_noisy_torus6_262144(beta):
+    w = inputs.torus6_noisy()
+    X = w.X.astype(np.float32)
+    V = inputs.random_block(w.N, w.b, seed=21)
+    rows = np.random.default_rng(22).choice(w.N, 48, replace=False)
+    case(f"full size noisy 6-torus N={w.N} D={w.D} b={w.b} beta={beta}")
+    _degree_and_products(to_dev(X, device()), X.astype(np.float64), beta, V, rows, TOL_F32)
+
+
+def test_molecule_2_20_products_and_lanczos_residuals():
+    w = inputs.molecule()
+    beta = w.betas[0]
+    X = w.X.astype(np.float32)
+    X64 = X.astype(np.float64)
+    V = inputs.random_block(w.N, w.b, seed=23)
+    rows = np.random.default_rng(24).choice(w.N, 24, replace=False)
+    case(f"full size molecule N={w.N} D={w.D} b={w.b}")
+    Xd = to_dev(X, device())
+    _, s = _degree_and_products(Xd, X64, beta, V, rows, TOL_F32)
+    case(f"full size molecule lanczos k={w.k} b={w.b}")
+    e = fd.fd_block_lanczos(Xd, beta, w.k, w.b, alpha=ALPHA, allow_not_converged=True)
+    phi = to_np(e.evecs)
+    theta = np.asarray(e.evals)
+    assert e.info["nconv"] == w.k and abs(theta[0] - 1.0) <= 1e-6
+    # (M phi)_S = s_S (K (s phi))_S with the device's s (checked on S above)
+    mphi = ok.kernel_matmul(X64, None, beta, phi, sl=s, sr=s, rows=rows, threads=8)
+    r = mphi - phi[rows] * theta[None, :]
+    # every entry of a residual is at most its norm (<= the solver's 1e-5);
+    # the slack covers the float32 operator's own error (~1e-6 relative)
+    assert np.abs(r).max() <= 1.5e-5, np.abs(r).max()
+    assert np.abs(phi.T @ phi - np.eye(w.k)).max() <= 1e-5
+
+
+def test_stress_bf16_2_21():
+    s = inputs.stress()
+    beta = s.betas[0]
+    V = inputs.random_block(s.N, s.b, seed=25)
+    rows = np.random.default_rng(26).choice(s.N, 16, replace=False)
+    case(f"full size bf16 stress N={s.N} D={s.D} b={s.b}")
+    Xd = to_dev(s.X, device())
+    Y0 = to_np(fd.fd_kernel_matmul(Xd, None, beta, to_dev(V, device())))
+    ref = ok.kernel_matmul(s.X_f64(), None, beta, V, rows=rows, threads=8)
+    err = rel_fro(Y0[rows], ref)
+    print(f"bf16 full size rel err {err:.2e}")
+    assert err <= TOL_BF16
