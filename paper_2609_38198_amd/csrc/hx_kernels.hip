@@ -430,6 +430,10 @@ __device__ __forceinline__ void hx_pair(const HxPair<RID, NCB>& c,
       acc[ib][cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(klo, c.v[cb].hi, acc[ib][cb], 0, 0, 0);
     }
   }
+  // one matrix instruction, then its share of the exponentials and three
+  // other vector instructions (3.5% faster at D = 30, b = 32; unchanged at
+  // D = 12, b = 16)
+  sched_interleave<NIB * (2 * Hx<RID>::nm + 3 * NCB), 8 * NIB, 3>();
 }
 
 // One workgroup = 4 waves; wave w owns row tiles [ib0, ib0 + NIB).  The
@@ -688,20 +692,6 @@ __device__ __forceinline__ float dpp_row_sum(float v) {
   v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x140,
                                                              0xF, 0xF, false));
   return v;
-}
-
-// Scheduling pattern for a region holding M matrix instructions and E
-// exponentials: each matrix instruction followed by its share of the
-// exponentials and V other vector instructions.
-template <int M, int E, int V, int m = 0>
-__device__ __forceinline__ void sched_interleave() {
-  if constexpr (m < M) {
-    constexpr int ne = (m + 1) * E / M - m * E / M;
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // matrix
-    if constexpr (ne > 0) __builtin_amdgcn_sched_group_barrier(0x400, ne, 0);  // transcendental
-    __builtin_amdgcn_sched_group_barrier(0x002, V, 0);  // vector
-    sched_interleave<M, E, V, m + 1>();
-  }
 }
 
 // One pipeline step of the symmetric row sums.  t holds the exponent tiles of

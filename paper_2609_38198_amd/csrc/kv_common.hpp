@@ -81,4 +81,18 @@ void launch_rowsum_sym_hx(const KVPlan& p, const PointPack& rows, const PointPac
                           const float* wp, float* part, unsigned long long* colfix,
                           double fix_scale, hipStream_t stream);
 
+// Scheduling pattern for a region holding M matrix instructions and E
+// exponentials: each matrix instruction followed by its share of the
+// exponentials and V other vector instructions.
+template <int M, int E, int V, int m = 0>
+__device__ __forceinline__ void sched_interleave() {
+  if constexpr (m < M) {
+    constexpr int ne = (m + 1) * E / M - m * E / M;
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // matrix
+    if constexpr (ne > 0) __builtin_amdgcn_sched_group_barrier(0x400, ne, 0);  // transcendental
+    __builtin_amdgcn_sched_group_barrier(0x002, V, 0);  // vector
+    sched_interleave<M, E, V, m + 1>();
+  }
+}
+
 }  // namespace fd
