@@ -55,6 +55,11 @@ static GemmTnShape gemm_tn_shape(int ma, int nb, int64_t N) {
   return g;
 }
 
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// VEC: ma, nb, lda, ldb multiples of 4 and A, B 16-byte aligned; each step
+// then reads its 4 + 4 values per row as two 16-byte loads (same sums).
+template <bool VEC>
 __global__ __launch_bounds__(256) void gemm_tn_partial_kernel(
     const float* __restrict__ A, int64_t lda, int ma, const float* __restrict__ B, int64_t ldb,
     int nb, int64_t N, int64_t rows_per_chunk, int tc, int lqg, int slices,
@@ -94,10 +99,20 @@ __global__ __launch_bounds__(256) void gemm_tn_partial_kernel(
         for (int r = 0; r < 4; ++r) {
           const int64_t ir = i + st * stride + r;
           const int64_t irc = min(ir, r1 - 1);
+          if constexpr (VEC) {
+            const f32x4 av = *reinterpret_cast<const f32x4*>(A + irc * lda + l0);
+            const f32x4 bw = *reinterpret_cast<const f32x4*>(B + irc * ldb + c0);
 #pragma unroll
-          for (int u = 0; u < 4; ++u) {
-            a[st][r][u] = A[irc * lda + la[u]];
-            bv[st][r][u] = (ir < r1) ? B[irc * ldb + cb[u]] : 0.f;
+            for (int u = 0; u < 4; ++u) {
+              a[st][r][u] = av[u];
+              bv[st][r][u] = (ir < r1) ? bw[u] : 0.f;
+            }
+          } else {
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+              a[st][r][u] = A[irc * lda + la[u]];
+              bv[st][r][u] = (ir < r1) ? B[irc * ldb + cb[u]] : 0.f;
+            }
           }
         }
 #pragma unroll
@@ -166,9 +181,16 @@ void gemm_tn(const float* A, int64_t lda, int ma, const float* B, int64_t ldb, i
              "internal: gemm_tn shape");
   const GemmTnShape g = gemm_tn_shape(ma, nb, N);
   check_span_d(part, size_t(g.chunks) * ma * nb, "gemm partials");
-  hipLaunchKernelGGL(gemm_tn_partial_kernel, dim3(unsigned(g.groups), unsigned(g.chunks)),
-                     dim3(256), 0, stream, A, lda, ma, B, ldb, nb, N, g.rows_per_chunk, g.tc,
-                     g.lqg, g.slices, part.p);
+  const bool vec = ma % 4 == 0 && nb % 4 == 0 && lda % 4 == 0 && ldb % 4 == 0 &&
+                   reinterpret_cast<uintptr_t>(A) % 16 == 0 &&
+                   reinterpret_cast<uintptr_t>(B) % 16 == 0;
+  const dim3 grid(unsigned(g.groups), unsigned(g.chunks));
+  if (vec)
+    hipLaunchKernelGGL(gemm_tn_partial_kernel<true>, grid, dim3(256), 0, stream, A, lda, ma, B, ldb,
+                       nb, N, g.rows_per_chunk, g.tc, g.lqg, g.slices, part.p);
+  else
+    hipLaunchKernelGGL(gemm_tn_partial_kernel<false>, grid, dim3(256), 0, stream, A, lda, ma, B,
+                       ldb, nb, N, g.rows_per_chunk, g.tc, g.lqg, g.slices, part.p);
   FD_LAUNCH_CHECK();
   const int64_t count = int64_t(ma) * nb;
   hipLaunchKernelGGL(reduce_partials_kernel, dim3(nblk(count, 32)), dim3(256), 0, stream, part.p,
@@ -205,9 +227,65 @@ __global__ __launch_bounds__(256) void gemm_nn_kernel(const float* __restrict__ 
   }
 }
 
+// Same product with ma, nb, ldq, ldz multiples of 4 and Q, Z 16-byte aligned:
+// thread (row, column quad) reads its row of Q four values at a time and
+// writes four outputs at once; every output is the same fmaf chain over l in
+// order as in gemm_nn_kernel.
+__global__ __launch_bounds__(256) void gemm_nn4_kernel(const float* __restrict__ Q, int64_t ldq,
+                                                       int ma, const float* __restrict__ C, int nb,
+                                                       int nqp, float* __restrict__ Z, int64_t ldz,
+                                                       int64_t N, float alpha, float beta) {
+  __shared__ float cs[128 * 64];
+  const int rows_per_wg = 256 / nqp;
+  const int tr = threadIdx.x / nqp, tq = threadIdx.x % nqp;
+  const int64_t i = int64_t(blockIdx.x) * rows_per_wg + tr;
+  const bool active = i < N && 4 * tq < nb;
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  for (int l0 = 0; l0 < ma; l0 += 128) {
+    const int len = min(128, ma - l0);
+    __syncthreads();
+    for (int e = threadIdx.x; e < len * nb; e += 256) cs[e] = C[int64_t(l0) * nb + e];
+    __syncthreads();
+    if (active) {
+      const float* q = Q + i * ldq + l0;
+      for (int l = 0; l < len; l += 4) {
+        const f32x4 q4 = *reinterpret_cast<const f32x4*>(q + l);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const f32x4 c4 = *reinterpret_cast<const f32x4*>(cs + (l + u) * nb + 4 * tq);
+#pragma unroll
+          for (int v = 0; v < 4; ++v) acc[v] = fmaf(q4[u], c4[v], acc[v]);
+        }
+      }
+    }
+  }
+  if (active) {
+    f32x4* z = reinterpret_cast<f32x4*>(Z + i * ldz + 4 * tq);
+    f32x4 out;
+    if (beta == 0.f) {
+#pragma unroll
+      for (int v = 0; v < 4; ++v) out[v] = alpha * acc[v];
+    } else {
+      const f32x4 zo = *z;
+#pragma unroll
+      for (int v = 0; v < 4; ++v) out[v] = fmaf(beta, zo[v], alpha * acc[v]);
+    }
+    *z = out;
+  }
+}
+
 void gemm_nn(const float* Q, int64_t ldq, int ma, const float* C, int nb, float* Z, int64_t ldz,
              int64_t N, float alpha, float beta, hipStream_t stream) {
   FD_REQUIRE(ma >= 1 && nb >= 1 && nb <= 64, FD_ERR_INVALID_ARG, "internal: gemm_nn shape");
+  if (ma % 4 == 0 && nb % 4 == 0 && ldq % 4 == 0 && ldz % 4 == 0 &&
+      reinterpret_cast<uintptr_t>(Q) % 16 == 0 && reinterpret_cast<uintptr_t>(Z) % 16 == 0) {
+    int nqp = 1;
+    while (nqp < nb / 4) nqp <<= 1;
+    hipLaunchKernelGGL(gemm_nn4_kernel, dim3(nblk(N, 256 / nqp)), dim3(256), 0, stream, Q, ldq,
+                       ma, C, nb, nqp, Z, ldz, N, alpha, beta);
+    FD_LAUNCH_CHECK();
+    return;
+  }
   int nbp = 1;
   while (nbp < nb) nbp <<= 1;
   const int rows_per_wg = 256 / nbp;
