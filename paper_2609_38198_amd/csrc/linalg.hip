@@ -606,7 +606,7 @@ __global__ void jacobi_sort_kernel(const double* __restrict__ A, int m, int lda,
 
 constexpr int JL_MAX = 192;   // largest m on the one-workgroup path
 constexpr int JL_SWEEPS = 4;  // sweeps per launch (the log holds this many)
-constexpr int JL_BATCH = 16;  // rounds of the log staged in LDS at a time by the replay
+constexpr int JL_BATCH = 32;  // rounds of the log staged in LDS at a time by the replay
 
 // log capacity that every size up to m needs
 size_t jacobi_log_doubles(int m) {
@@ -740,33 +740,44 @@ __global__ __launch_bounds__(1024) void jacobi_lds_kernel(double* __restrict__ A
   }
 }
 
-// V (m x m, ld m) <- V J_1 J_2 ... for the state[0] logged rounds.  Workgroup
-// w owns rows [w R, w R + R), R = blockDim.x / npairs, thread (row, pair k).
-// Rounds of the log are staged in LDS JL_BATCH at a time, the next batch
-// loaded into registers while the current one is applied.
-__global__ __launch_bounds__(1024) void jacobi_replay_kernel(double* __restrict__ V, int m,
-                                                             const double* __restrict__ log,
-                                                             const int* __restrict__ state) {
-  __shared__ double vs[2048];  // R rows x m <= 2 * blockDim.x (m <= 2 npairs)
+// V (m x m, ld m) <- V J_1 J_2 ... for the state[0] logged rounds.  Rows are
+// independent under column rotations, so each wave owns one row of V (held
+// in LDS) and applies the rounds to it in order with no barrier: lane l takes
+// pairs l and l + 64, whose indices it advances from round to round (the
+// circle method moves every player but 0 one place per round); within a
+// wave LDS accesses complete in order.  The four waves of a workgroup share
+// the log, staged in LDS JL_BATCH rounds at a time, the next batch loaded
+// into registers while the current one is applied.
+__global__ __launch_bounds__(256) void jacobi_replay_kernel(double* __restrict__ V, int m,
+                                                            const double* __restrict__ log,
+                                                            const int* __restrict__ state) {
+  __shared__ double vs[4][JL_MAX];
   __shared__ double stage[2][JL_BATCH * JL_MAX];
   const int t = threadIdx.x;
-  const int nt = blockDim.x;
-  const int me = m + (m & 1), npairs = me / 2;
-  const int R = nt / npairs;
-  const int row0 = blockIdx.x * R;
-  const int nrow = min(R, m - row0);
+  const int lane = t & 63, wv = t >> 6;
+  const int me = m + (m & 1), n = me / 2;
+  const int row = blockIdx.x * 4 + wv;
+  const bool active = row < m;
   const int rounds = state[0];
-  if (nrow <= 0 || rounds <= 0) return;
-  const int lr = t / npairs, k = t % npairs;
-  const bool active = lr < nrow;
-  for (int e = t; e < nrow * m; e += nt) vs[e] = V[int64_t(row0 + e / m) * m + e % m];
+  if (rounds <= 0) return;
+  double* v = vs[wv];
+  if (active)
+    for (int c = lane; c < m; c += 64) v[c] = V[int64_t(row) * m + c];
+  // pair indices of round 0 for pairs lane and lane + 64
+  int pa[2], pb[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int k = lane + 64 * h;
+    pa[h] = k;            // 0 for k = 0 (player 0 never moves)
+    pb[h] = me - 1 - k;
+  }
   const int per_batch = JL_BATCH * me;  // doubles of the log per batch
-  constexpr int PF = (JL_BATCH * JL_MAX + 1023) / 1024;  // loads per thread per batch
+  constexpr int PF = (JL_BATCH * JL_MAX + 255) / 256;  // loads per thread per batch
   const int nbatch = (rounds + JL_BATCH - 1) / JL_BATCH;
   auto fetch = [&](int bt, double (&reg)[PF]) {
 #pragma unroll
     for (int u = 0; u < PF; ++u) {
-      const int e = t + u * nt;
+      const int e = t + u * 256;
       const int64_t g = int64_t(bt) * per_batch + e;
       reg[u] = (e < per_batch && g < int64_t(rounds) * me) ? log[g] : 0.0;
     }
@@ -774,7 +785,7 @@ __global__ __launch_bounds__(1024) void jacobi_replay_kernel(double* __restrict_
   auto put = [&](int slot, const double (&reg)[PF]) {
 #pragma unroll
     for (int u = 0; u < PF; ++u) {
-      const int e = t + u * nt;
+      const int e = t + u * 256;
       if (e < per_batch) stage[slot][e] = reg[u];
     }
   };
@@ -785,27 +796,43 @@ __global__ __launch_bounds__(1024) void jacobi_replay_kernel(double* __restrict_
   for (int bt = 0; bt < nbatch; ++bt) {
     if (bt + 1 < nbatch) fetch(bt + 1, reg);
     const int r1 = min(rounds, (bt + 1) * JL_BATCH);
+    const double* sb = stage[bt & 1];
     for (int r = bt * JL_BATCH; r < r1; ++r) {
-      if (active) {
-        int p, q;
-        circle_pair(me, r % (me - 1), k, p, q);
-        const int o = ((r - bt * JL_BATCH) * npairs + k) * 2;
-        const double c = stage[bt & 1][o], s = stage[bt & 1][o + 1];
-        if (q < m && s != 0.0) {
-          double* v = vs + lr * m;
-          const double vp = v[p], vq = v[q];
-          v[p] = c * vp - s * vq;
-          v[q] = s * vp + c * vq;
-        }
+      // both pairs' reads first (one LDS latency per round), then the writes;
+      // the pairs of a round are disjoint, so the two never touch one entry
+      int p[2], q[2];
+      bool on[2];
+      double c[2], sn[2], vp[2], vq[2];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int k = lane + 64 * h;
+        p[h] = min(pa[h], pb[h]);
+        q[h] = max(pa[h], pb[h]);
+        on[h] = active && k < n && q[h] < m;
+        const int o = ((r - bt * JL_BATCH) * n + min(k, n - 1)) * 2;
+        c[h] = sb[o];
+        sn[h] = sb[o + 1];
+        vp[h] = v[on[h] ? p[h] : 0];
+        vq[h] = v[on[h] ? q[h] : 0];
       }
-      __syncthreads();
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        if (on[h] && sn[h] != 0.0) {
+          v[p[h]] = c[h] * vp[h] - sn[h] * vq[h];
+          v[q[h]] = sn[h] * vp[h] + c[h] * vq[h];
+        }
+        if (lane + 64 * h != 0) pa[h] = pa[h] == me - 1 ? 1 : pa[h] + 1;
+        pb[h] = pb[h] == me - 1 ? 1 : pb[h] + 1;
+      }
     }
     if (bt + 1 < nbatch) {
+      __syncthreads();  // every wave is done with the slot about to be refilled
       put((bt + 1) & 1, reg);
       __syncthreads();
     }
   }
-  for (int e = t; e < nrow * m; e += nt) V[int64_t(row0 + e / m) * m + e % m] = vs[e];
+  if (active)
+    for (int c = lane; c < m; c += 64) V[int64_t(row) * m + c] = v[c];
 }
 
 void jacobi_eig(double* A, double* A2, int m, int lda, double* Vw, double* theta, double* S,
@@ -822,13 +849,12 @@ void jacobi_eig(double* A, double* A2, int m, int lda, double* Vw, double* theta
   if (m > 1 && m <= JL_MAX) {
     check_span_d(log, jacobi_log_doubles(m), "jacobi rotation log");
     FD_REQUIRE(lda >= m && state != nullptr, FD_ERR_INVALID_ARG, "internal: jacobi state");
-    const int R = 1024 / npairs;
-    const unsigned rgrid = unsigned((m + R - 1) / R);
+    const unsigned rgrid = unsigned((m + 3) / 4);
     for (int done = 0; done < MAX_SWEEPS; done += JL_SWEEPS) {
       hipLaunchKernelGGL(jacobi_lds_kernel, dim3(1), dim3(1024), 0, stream, A, m, lda, log.p,
                          state, TOL * TOL, std::min(JL_SWEEPS, MAX_SWEEPS - done), done);
       FD_LAUNCH_CHECK();
-      hipLaunchKernelGGL(jacobi_replay_kernel, dim3(rgrid), dim3(1024), 0, stream, Vw, m, log.p,
+      hipLaunchKernelGGL(jacobi_replay_kernel, dim3(rgrid), dim3(256), 0, stream, Vw, m, log.p,
                          state);
       FD_LAUNCH_CHECK();
       int h[2] = {0, 0};
