@@ -471,11 +471,13 @@ __device__ __forceinline__ void circle_pair(int me, int round, int k, int& p, in
 // rotation (c, s) annihilating A_pq (apq != 0): t = tan of the angle, the
 // smaller root of t^2 + 2 tau t - 1 = 0 (the 2 x 2 symmetric Schur
 // decomposition of Golub & Van Loan)
+// (with tau = (aqq - app) / (2 apq) multiplied through by 2 |apq|: one square
+// root and one division fewer on the dependent chain)
 __device__ __forceinline__ void jacobi_rotation(double app, double aqq, double apq, double& c,
                                                 double& s) {
-  const double tau = (aqq - app) / (2.0 * apq);
-  const double tt = (tau >= 0.0 ? 1.0 : -1.0) / (fabs(tau) + sqrt(1.0 + tau * tau));
-  c = 1.0 / sqrt(1.0 + tt * tt);
+  const double d = aqq - app;
+  const double tt = (d >= 0.0 ? 2.0 * apq : -2.0 * apq) / (fabs(d) + sqrt(d * d + 4.0 * apq * apq));
+  c = rsqrt(1.0 + tt * tt);
   s = tt * c;
 }
 
@@ -710,13 +712,16 @@ __global__ __launch_bounds__(1024) void jacobi_lds_kernel(double* __restrict__ A
       for (int bk = gl; bk < gcnt; bk += tpg) {
         const int i = bk <= grp ? bk : bk - grp - 1;
         const int j = bk <= grp ? grp : n - 1 - grp;
+        // the pair data of both blocks in one go (one LDS wait, not two): the
+        // positions are formed before the skip test
         const double2 ri = rot[i], rj = rot[j];
-        if (ri.y == 0.0 && rj.y == 0.0) continue;
         const int4 Pi = pr[i], Pj = pr[j];
         // position of (r, c) given both row offsets
         auto pos = [](int r, int ro_r, int c, int ro_c) { return r <= c ? ro_r + c : ro_c + r; };
         const int xa = pos(Pi.x, Pi.z, Pj.x, Pj.z), xb = pos(Pi.x, Pi.z, Pj.y, Pj.w);
         const int xd = pos(Pi.y, Pi.w, Pj.x, Pj.z), xe = pos(Pi.y, Pi.w, Pj.y, Pj.w);
+        asm volatile("" ::"v"(xa), "v"(xb), "v"(xd), "v"(xe));
+        if (ri.y == 0.0 && rj.y == 0.0) continue;
         const double a = tri[xa], b = tri[xb], d = tri[xd], e = tri[xe];
         const double ci = ri.x, si = ri.y, cj = rj.x, sj = rj.y;
         const double a1 = ci * a - si * d, b1 = ci * b - si * e;
