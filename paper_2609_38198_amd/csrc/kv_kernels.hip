@@ -304,10 +304,11 @@ __device__ __forceinline__ void load_pair_b(ColPairB<DC, NCB>& cp, const uintx4*
     for (int c = 0; c < DC; ++c) cp.xa[t][c] = xa[(jb * DC + c) * 64 + lane];
     cp.aj[t] = aj[jb * 64 + lane];
   }
-  if (vp != nullptr) {
+  // unconditional: a branch here would leave the compiler unsure whether the
+  // V loads were issued, and its merged load counts would then make every
+  // exponent contraction wait for the V loads as well
 #pragma unroll
-    for (int cb = 0; cb < NCB; ++cb) cp.v[cb] = vp[(jp * NCB + cb) * 64 + lane];
-  }
+  for (int cb = 0; cb < NCB; ++cb) cp.v[cb] = vp[(jp * NCB + cb) * 64 + lane];
 }
 
 // Exponents of one pair of column tiles against row tile ib, in accumulator

@@ -173,7 +173,7 @@ def test_bf16_input_uses_exact_bf16_values():
         assert err <= TOL_BF16
 
 
-@pytest.mark.parametrize("D,b", [(64, 64), (30, 32), (8, 8)])
+@pytest.mark.parametrize("D,b", [(64, 64), (30, 32), (8, 8), (30, 48), (64, 40)])
 def test_bf16_shapes_sampled_rows(D, b):
     N = 65536
     X = inputs.stress_points(N, seed=3, D=D, sub_dim=min(8, D)).astype(np.float32)
