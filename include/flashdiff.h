@@ -58,7 +58,8 @@ typedef enum fd_op {
   FD_OP_DEGREE = 1,
   FD_OP_BLOCK_LANCZOS = 2,
   FD_OP_CONTINUATION = 3,
-  FD_OP_BETA_FLOW = 4
+  FD_OP_BETA_FLOW = 4,
+  FD_OP_DEGREE_DYADIC = 5
 } fd_op;
 
 /* Options of the block Lanczos eigensolver (Sec. 2.3, first paragraph: block
@@ -95,6 +96,7 @@ void fd_lanczos_default_opts(fd_lanczos_opts* opts);
 /* Bytes of workspace an entry point needs.
  *   op = FD_OP_KERNEL_MATMUL: Nr output rows, Nc columns, D, b; k ignored.
  *   op = FD_OP_DEGREE:        Nr = Nc = N, D; b, k ignored.
+ *   op = FD_OP_DEGREE_DYADIC: Nr = Nc = N, D; b, k ignored.
  *   op = FD_OP_BLOCK_LANCZOS: Nr = Nc = N, D, b, k, opts (NULL = defaults).
  *   op = FD_OP_BETA_FLOW:     Nr = Nc = N, D, b, k, opts (NULL = defaults); also the
  *                             size for fd_beta_flow_cascade.
@@ -133,6 +135,24 @@ fd_status fd_kernel_matmul(const void* Xr, int64_t Nr, const void* Xc, int64_t N
 fd_status fd_degree(const void* X, fd_dtype xt, int64_t N, int64_t D, int64_t ldx, float beta,
                     float alpha, float* q, float* d, float* s, double* s_off, void* ws,
                     size_t ws_bytes, void* stream);
+
+/* Normalisation vectors of a dyadic bandwidth ladder beta_l = beta0 2^l,
+ * l = 0 .. nbeta - 1 (Sec. 2.3, dyadic continuation): level l holds what
+ * fd_degree returns at beta_l, up to rounding.  The kernel at 2 beta is the
+ * entrywise square of the kernel at beta (eq. kernel), so on float32 inputs
+ * with alpha > 0 the second pass of level l also sums K(beta_l)^2 along rows
+ * and columns, which is level l + 1's q = K(beta_{l+1}) 1: every level after
+ * the first takes one pass over the kernel instead of two.  Other inputs run
+ * fd_degree's passes level by level.
+ *   X: N x D (device).  beta0 > 0 with beta0 2^(nbeta-1) finite; 1 <= nbeta <= 32;
+ *   0 <= alpha <= 1.
+ *   q, d, s: nbeta x N floats each (device; level l at offset l N), or NULL each.
+ *   s_off: nbeta doubles (device), sum(q_l) - N per level, or NULL.
+ *   Workspace: fd_workspace_size(FD_OP_DEGREE_DYADIC, N, N, D, 0, 0, NULL).
+ * Asynchronous on `stream`. */
+fd_status fd_degree_dyadic(const void* X, fd_dtype xt, int64_t N, int64_t D, int64_t ldx,
+                           float beta0, int32_t nbeta, float alpha, float* q, float* d, float* s,
+                           double* s_off, void* ws, size_t ws_bytes, void* stream);
 
 /* Top-k eigenpairs of M = diag(s) K diag(s) by thick-restart block Lanczos
  * (Sec. 2.3, first paragraph; Sec. 2.1 eq. symmetric), including the Perron

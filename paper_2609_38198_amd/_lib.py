@@ -29,13 +29,14 @@ STATUS = {
 FD_F32, FD_BF16 = 0, 1
 FD_OP_KERNEL_MATMUL, FD_OP_DEGREE, FD_OP_BLOCK_LANCZOS, FD_OP_CONTINUATION = 0, 1, 2, 3
 FD_OP_BETA_FLOW = 4
+FD_OP_DEGREE_DYADIC = 5
 FLOW_EXIT = {0: "bracket", 1: "wall", 2: "budget"}
 
 EXPORTS = (
     "fd_lanczos_default_opts", "fd_workspace_size", "fd_kernel_matmul", "fd_degree",
     "fd_block_lanczos", "fd_continuation", "fd_last_error", "fd_status_string",
     "fd_profile_enable", "fd_profile_read", "fd_flow_default_opts", "fd_beta_flow",
-    "fd_beta_flow_cascade",
+    "fd_beta_flow_cascade", "fd_degree_dyadic",
 )
 FD_KERNEL_PRODUCT, FD_KERNEL_ROWSUM = 0, 1
 
@@ -110,6 +111,10 @@ def load(path: str = LIB_PATH):
     lib.fd_degree.argtypes = [_c_p, ctypes.c_int, _c_i64, _c_i64, _c_i64, ctypes.c_float,
                               ctypes.c_float, _c_p, _c_p, _c_p, _c_p, _c_p, ctypes.c_size_t, _c_p]
     lib.fd_degree.restype = ctypes.c_int
+    lib.fd_degree_dyadic.argtypes = [_c_p, ctypes.c_int, _c_i64, _c_i64, _c_i64, ctypes.c_float,
+                                     ctypes.c_int32, ctypes.c_float, _c_p, _c_p, _c_p, _c_p, _c_p,
+                                     ctypes.c_size_t, _c_p]
+    lib.fd_degree_dyadic.restype = ctypes.c_int
     lib.fd_block_lanczos.argtypes = [
         _c_p, ctypes.c_int, _c_i64, _c_i64, _c_i64, ctypes.c_float, ctypes.c_float, _c_i64, _c_i64,
         _c_p, _c_i64, _c_i64, ctypes.c_int32, ctypes.POINTER(LanczosOpts), _c_p, _c_p, _c_p, _c_p,
@@ -277,6 +282,30 @@ def fd_degree(X: torch.Tensor, beta: float, alpha: float = 0.5,
     _check(lib.fd_degree(_ptr(X), _dtype_code(X), N, D, X.stride(0), float(beta), float(alpha),
                          _ptr(q), _ptr(d), _ptr(s), _ptr(s_off), _ptr(ws), ws.numel(),
                          _stream(dev)))
+    return Degree(q, d, s, s_off)
+
+
+def fd_degree_dyadic(X: torch.Tensor, beta0: float, nbeta: int, alpha: float = 0.5,
+                     ws: Optional[torch.Tensor] = None) -> Degree:
+    """fd_degree at beta0 * 2^l for l < nbeta: q, d, s are nbeta x N, s_off nbeta."""
+    lib = load()
+    _check_dev(X)
+    if X.dim() != 2 or X.stride(1) != 1:
+        raise ValueError("X must be row-major N x D")
+    N, D = X.shape
+    dev = X.device
+    q = torch.empty((nbeta, N), dtype=torch.float32, device=dev)
+    d = torch.empty_like(q)
+    s = torch.empty_like(q)
+    s_off = torch.empty(nbeta, dtype=torch.float64, device=dev)
+    need = fd_workspace_size(FD_OP_DEGREE_DYADIC, N, N, D)
+    if need == 0:
+        raise FdError(1, "unsupported sizes")
+    if ws is None or ws.numel() < need:
+        ws = _workspace(need, dev)
+    _check(lib.fd_degree_dyadic(_ptr(X), _dtype_code(X), N, D, X.stride(0), float(beta0),
+                                int(nbeta), float(alpha), _ptr(q), _ptr(d), _ptr(s),
+                                _ptr(s_off), _ptr(ws), ws.numel(), _stream(dev)))
     return Degree(q, d, s, s_off)
 
 

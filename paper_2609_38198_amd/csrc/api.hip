@@ -1,6 +1,7 @@
 // C ABI entry points: argument validation, workspace carving and the
 // composition of the kernels into the operations declared in flashdiff.h.
 #include <algorithm>
+#include <cfloat>
 #include <cmath>
 #include <exception>
 #include <string>
@@ -171,6 +172,57 @@ void degree_run(DegreeWs& w, const void* X, fd_dtype xt, int64_t N, int64_t D, i
   launch_degree_finish(qq, w.t, N, alpha, d, s, stream);
 }
 
+DegreeWs carve_degree_dyadic(Arena& a, int64_t N, int64_t D) {
+  DegreeWs w = carve_degree(a, N, D);
+  w.sq_part = a.fspan(sym_part_rows(w.rows.npad, SYM_NIB));
+  w.sq_colfix = a.take<unsigned long long>(size_t(w.rows.npad));
+  return w;
+}
+
+void degree_run_dyadic(DegreeWs& w, const void* X, fd_dtype xt, int64_t N, int64_t D,
+                       int64_t ldx, double beta0, int nb, double alpha, float* q, float* d,
+                       float* s, double* s_off, hipStream_t stream) {
+  auto at = [N](float* v, int l) { return v != nullptr ? v + int64_t(l) * N : nullptr; };
+  auto beta_of = [beta0](int l) { return std::ldexp(beta0, l); };
+  launch_pack_points(X, xt, N, D, ldx, beta_of(0), true, w.rows, stream);
+  launch_pack_points(X, xt, N, D, ldx, beta_of(0), false, w.cols, stream);
+  if (alpha == 0.0 || !rowsum_sym_applies(w.rows, w.cols, true, w.colfix)) {
+    // no weighted pass to carry the squares (alpha = 0), or not the symmetric
+    // path: fd_degree's passes, level by level
+    for (int l = 0; l < nb; ++l)
+      degree_run(w, X, xt, N, D, ldx, beta_of(l), alpha, at(q, l), at(d, l), at(s, l),
+                 s_off != nullptr ? s_off + l : nullptr, l > 0, stream);
+    return;
+  }
+  // q of the current level and of the next, in the caller's arrays or in two
+  // workspace vectors used in turn
+  auto q_of = [&](int l) { return q != nullptr ? q + int64_t(l) * N : (l % 2 ? w.w : w.q); };
+  const SymPass p1 = launch_rowsum_sym_pass(w.plan, w.rows, w.cols, FSpan{}, w.part, w.colfix,
+                                            true, stream);
+  launch_degree_reduce_q(p1, w.rows, w.cols, w.part, w.colfix, q_of(0), alpha, w.wp, stream);
+  if (s_off != nullptr) launch_sum_minus_n(q_of(0), N, s_off, stream);
+  launch_zero_u64(w.sq_colfix, w.rows.npad, stream);
+  for (int l = 0; l < nb; ++l) {
+    if (l > 0) {
+      launch_pack_points(X, xt, N, D, ldx, beta_of(l), true, w.rows, stream);
+      launch_pack_points(X, xt, N, D, ldx, beta_of(l), false, w.cols, stream);
+    }
+    if (l + 1 == nb) {
+      const SymPass p2 = launch_rowsum_sym_pass(w.plan, w.rows, w.cols, w.wp, w.part, w.colfix,
+                                                false, stream);
+      launch_degree_reduce_ds(p2, w.rows, w.part, w.colfix, q_of(l), alpha, at(d, l), at(s, l),
+                              stream);
+      break;
+    }
+    // weighted pass of level l with the squared sums: t_l and q_{l+1}
+    const SymPass p2 = launch_rowsum_sym_pass(w.plan, w.rows, w.cols, w.wp, w.part, w.colfix,
+                                              false, stream, w.sq_part, w.sq_colfix);
+    launch_degree_reduce_dsq(p2, w.rows, w.cols, w.part, w.colfix, q_of(l), alpha, at(d, l),
+                             at(s, l), w.sq_part, w.sq_colfix, q_of(l + 1), w.wp, stream);
+    if (s_off != nullptr) launch_sum_minus_n(q_of(l + 1), N, s_off + l + 1, stream);
+  }
+}
+
 }  // namespace fd
 
 using namespace fd;
@@ -217,6 +269,9 @@ size_t fd_workspace_size(fd_op op, int64_t Nr, int64_t Nc, int64_t D, int64_t b,
         break;
       case FD_OP_DEGREE:
         carve_degree(a, Nr, D);
+        break;
+      case FD_OP_DEGREE_DYADIC:
+        carve_degree_dyadic(a, Nr, D);
         break;
       case FD_OP_BLOCK_LANCZOS: {
         fd_lanczos_opts o;
@@ -296,6 +351,30 @@ fd_status fd_degree(const void* X, fd_dtype xt, int64_t N, int64_t D, int64_t ld
     DegreeWs w = carve_degree(a, N, D);
     degree_run(w, X, xt, N, D, ldx, beta, alpha, q, d, s, s_off, true,
                static_cast<hipStream_t>(stream));
+  });
+}
+
+fd_status fd_degree_dyadic(const void* X, fd_dtype xt, int64_t N, int64_t D, int64_t ldx,
+                           float beta0, int32_t nbeta, float alpha, float* q, float* d, float* s,
+                           double* s_off, void* ws, size_t ws_bytes, void* stream) {
+  return guarded([&] {
+    check_points(X, xt, N, D, ldx, "X");
+    FD_REQUIRE(nbeta >= 1 && nbeta <= 32, FD_ERR_INVALID_ARG, "nbeta must be in [1, 32]");
+    FD_REQUIRE(std::isfinite(beta0) && beta0 > 0.f &&
+                   std::isfinite(std::ldexp(double(beta0), nbeta - 1)) &&
+                   std::ldexp(double(beta0), nbeta - 1) <= double(FLT_MAX),
+               FD_ERR_INVALID_ARG, "beta0 must be > 0 with beta0 2^(nbeta-1) finite");
+    FD_REQUIRE(alpha >= 0.f && alpha <= 1.f, FD_ERR_INVALID_ARG, "alpha must be in [0, 1]");
+    Arena m;
+    m.measuring = true;
+    carve_degree_dyadic(m, N, D);
+    check_workspace(ws, ws_bytes, m.used);
+    Arena a;
+    a.base = static_cast<char*>(ws);
+    a.cap = ws_bytes;
+    DegreeWs w = carve_degree_dyadic(a, N, D);
+    degree_run_dyadic(w, X, xt, N, D, ldx, beta0, int(nbeta), alpha, q, d, s, s_off,
+                      static_cast<hipStream_t>(stream));
   });
 }
 

@@ -162,17 +162,36 @@ struct SymPass {
   int nsplit = 0;
   double inv_fix = 0.0;
 };
+// Second output of a weighted symmetric pass: the unit-weight row sums (per
+// split, part) and fixed-point column sums (colfix) of the squared kernel.
+struct SymSquares {
+  float* part = nullptr;
+  unsigned long long* colfix = nullptr;
+  double fix_scale = 0.0;
+};
 bool rowsum_sym_applies(const PointPack& rows, const PointPack& cols, bool diag,
                         const unsigned long long* colfix);
+// sq_part / sq_colfix (weighted passes only): also the squared-kernel sums, whose
+// reduction uses the returned inv_fix as well.
 SymPass launch_rowsum_sym_pass(const KVPlan& p, const PointPack& rows, const PointPack& cols,
                                FSpan wp, FSpan part, unsigned long long* colfix, bool zero_colfix,
-                               hipStream_t stream);
+                               hipStream_t stream, FSpan sq_part = FSpan{},
+                               unsigned long long* sq_colfix = nullptr);
 void launch_degree_reduce_q(const SymPass& sp, const PointPack& rows, const PointPack& cols,
                             FSpan part, unsigned long long* colfix, float* q, double alpha,
                             FSpan wp, hipStream_t stream);
 void launch_degree_reduce_ds(const SymPass& sp, const PointPack& rows, FSpan part,
                              unsigned long long* colfix, const float* q, double alpha, float* d,
                              float* s, hipStream_t stream);
+// launch_degree_reduce_ds plus the squared-kernel sums of the same pass: the
+// next dyadic level's q_next = K(2 beta) 1 and its w = q_next^-alpha into the
+// weight pack wp (the column pack's extent); leaves both colfix arrays zeroed.
+void launch_degree_reduce_dsq(const SymPass& sp, const PointPack& rows, const PointPack& cols,
+                              FSpan part, unsigned long long* colfix, const float* q,
+                              double alpha, float* d, float* s, FSpan sq_part,
+                              unsigned long long* sq_colfix, float* q_next, FSpan wp,
+                              hipStream_t stream);
+void launch_zero_u64(unsigned long long* p, int64_t n, hipStream_t stream);
 // Row tiles per wave of the symmetric row sums, and the fewest column splits
 // of their large-problem plans.
 constexpr int SYM_NIB = 8;

@@ -21,6 +21,8 @@ struct DegreeWs {
   float* t = nullptr;
   float* w = nullptr;
   unsigned long long* colfix = nullptr;  // npad words: column sums of the symmetric row sums
+  FSpan sq_part;                          // squared-kernel row partials (dyadic levels)
+  unsigned long long* sq_colfix = nullptr;
   KVPlan plan;
 };
 
@@ -37,6 +39,14 @@ DegreeWs carve_degree(Arena& a, int64_t N, int64_t D);
 void degree_run(DegreeWs& w, const void* X, fd_dtype xt, int64_t N, int64_t D, int64_t ldx,
                 double beta, double alpha, float* q, float* d, float* s, double* s_off,
                 bool pack, hipStream_t stream);
+
+// carve_degree plus the squared-kernel buffers of the dyadic ladder.
+DegreeWs carve_degree_dyadic(Arena& a, int64_t N, int64_t D);
+// Levels l = 0 .. nb - 1 at beta0 2^l: q, d, s at offset l N (each may be NULL),
+// s_off[l] (or NULL).
+void degree_run_dyadic(DegreeWs& w, const void* X, fd_dtype xt, int64_t N, int64_t D,
+                       int64_t ldx, double beta0, int nb, double alpha, float* q, float* d,
+                       float* s, double* s_off, hipStream_t stream);
 
 // Row slots of a partial-sum buffer large enough for every plan with at most
 // npad rows and nc columns (see plan_product).

@@ -551,11 +551,11 @@ __device__ __forceinline__ void load_hx_col(HxCol<RID>& c, const uintx4* __restr
 // first (independent chains issue back to back and the exponentials can
 // overlap their tail), then K' = 2^t summed (times the weights) on the vector
 // ALUs.
-template <int RID, int NIB, bool UNIT, bool DIAG>
+template <int RID, int NIB, bool UNIT, bool DIAG, bool SQ = false>
 __device__ __forceinline__ void hx_rowsum_tile(const HxCol<RID>& c,
                                                const uintx4 (&br)[NIB][Hx<RID>::nb],
                                                float (&acc)[NIB], int64_t jb, int64_t ib0, int g,
-                                               int p) {
+                                               int p, float (*acc2)[NIB] = nullptr) {
   floatx4 t[NIB];
 #pragma unroll
   for (int ib = 0; ib < NIB; ++ib) {
@@ -575,6 +575,11 @@ __device__ __forceinline__ void hx_rowsum_tile(const HxCol<RID>& c,
       // one FMA per entry: as many vector instructions as the unit-weight sum
 #pragma unroll
       for (int r = 0; r < 4; ++r) acc[ib] = fmaf(k[r], c.w[r], acc[ib]);
+    }
+    if constexpr (SQ) {
+      // (K')^2 = 2^30 K^2: the kernel at twice the bandwidth, unit weights
+#pragma unroll
+      for (int r = 0; r < 4; ++r) (*acc2)[ib] = fmaf(k[r], k[r], (*acc2)[ib]);
     }
   }
 }
@@ -700,13 +705,16 @@ __device__ __forceinline__ float dpp_row_sum(float v) {
 // tile (operands xn), so the matrix-core chain of row tile ib runs alongside
 // the vector work of row tiles ib + 1, ...  SUMS: add J's row sums into acc and
 // its column sums into the fixed-point accumulator (false for padding tiles).
-template <int RID, int NIB, bool UNIT, bool SUMS>
+template <int RID, int NIB, bool UNIT, bool SUMS, bool SQ>
 __device__ __forceinline__ void hx_sym_step(floatx4 (&t)[NIB], const uintx4* xn,
                                             const uintx4 (&br)[NIB][Hx<RID>::nb],
                                             const floatx4& w, const float (&wi)[NIB],
-                                            float (&acc)[NIB], int64_t jl, double fix_scale,
-                                            unsigned long long* lds_col, int g, int p) {
+                                            float (&acc)[NIB], float (&acc2)[NIB], int64_t jl,
+                                            double fix_scale, double fix_scale2,
+                                            unsigned long long* lds_col,
+                                            unsigned long long* lds_col2, int g, int p) {
   float cs[4] = {0.f, 0.f, 0.f, 0.f};
+  float cs2[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int ib = 0; ib < NIB; ++ib) {
     float k[4];
@@ -726,6 +734,15 @@ __device__ __forceinline__ void hx_sym_step(floatx4 (&t)[NIB], const uintx4* xn,
           acc[ib] = fmaf(k[r], w[r], acc[ib]);
           cs[r] = fmaf(k[r], wi[ib], cs[r]);
         }
+        if constexpr (SQ) {
+          // the squared kernel (K at twice the bandwidth) with unit weights,
+          // along the rows and along the columns of the tile
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            acc2[ib] = fmaf(k[r], k[r], acc2[ib]);
+            cs2[r] = fmaf(k[r], k[r], cs2[r]);
+          }
+        }
       }
     }
   }
@@ -733,11 +750,14 @@ __device__ __forceinline__ void hx_sym_step(floatx4 (&t)[NIB], const uintx4* xn,
   // the row sums are due here (an empty statement reading them), not sunk
   // past the column-sum atomic below, so that they interleave too
 #pragma unroll
-  for (int ib = 0; ib < NIB; ++ib) asm volatile("" ::"v"(acc[ib]));
+  for (int ib = 0; ib < NIB; ++ib) {
+    asm volatile("" ::"v"(acc[ib]));
+    if constexpr (SQ) asm volatile("" ::"v"(acc2[ib]));
+  }
   // Interleave the contraction with the exponentials and sums (left to
   // itself the scheduler issues the exponentials first, then the matrix
   // instructions with little vector work between them).
-  sched_interleave<Hx<RID>::nm * NIB, 4 * NIB, 3>();
+  sched_interleave<Hx<RID>::nm * NIB, 4 * NIB, SQ ? 5 : 3>();
   // lane (g, p) holds, for column 4g + r of the tile, the sum over rows p of
   // the wave's tiles; the 16 lanes of DPP row g hold the wave's other rows
 #pragma unroll
@@ -748,14 +768,28 @@ __device__ __forceinline__ void hx_sym_step(floatx4 (&t)[NIB], const uintx4* xn,
   const float v = (p & 2) ? v23 : v01;
   const long long fx = __double2ll_rn(double(v) * fix_scale);
   if (p < 4) atomicAdd(lds_col + jl * TILE + 4 * g + p, static_cast<unsigned long long>(fx));
+  if constexpr (SQ) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) cs2[r] = dpp_row_sum(cs2[r]);
+    const float u01 = (p & 1) ? cs2[1] : cs2[0];
+    const float u23 = (p & 1) ? cs2[3] : cs2[2];
+    const float u = (p & 2) ? u23 : u01;
+    const long long fx2 = __double2ll_rn(double(u) * fix_scale2);
+    if (p < 4) atomicAdd(lds_col2 + jl * TILE + 4 * g + p, static_cast<unsigned long long>(fx2));
+  }
 }
 
-template <int RID, int NIB, bool UNIT>
+// SQ (weighted passes only): also the row and column sums of the squared
+// kernel, K^2 1 = K(2 beta) 1 (eq. kernel), into part2 / colfix2 with the scale
+// fix_scale2 per unit of (2^15 K)^2.
+template <int RID, int NIB, bool UNIT, bool SQ = false>
 __global__ __launch_bounds__(WG_THREADS)
 __attribute__((amdgpu_waves_per_eu(hx_waves<RID, 0, NIB>()))) void rowsum_sym_hx_kernel(
     const uintx4* __restrict__ xc, const floatx4* __restrict__ wp, const uintx4* __restrict__ xr,
     int64_t nblk, int64_t njb, int64_t jb_per_split, int64_t nsplit, float* __restrict__ part,
-    int64_t nrpad, unsigned long long* __restrict__ colfix, double fix_scale) {
+    int64_t nrpad, unsigned long long* __restrict__ colfix, double fix_scale,
+    float* __restrict__ part2, unsigned long long* __restrict__ colfix2, double fix_scale2) {
+  static_assert(!(SQ && UNIT), "squared sums ride on a weighted pass");
   constexpr int NB = Hx<RID>::nb;
   constexpr int NC = Hx<RID>::nc;
   constexpr int BT = 4 * NIB;  // tiles per block
@@ -784,7 +818,11 @@ __attribute__((amdgpu_waves_per_eu(hx_waves<RID, 0, NIB>()))) void rowsum_sym_hx
   const int g = lane >> 4, p = lane & 15;
   // fixed-point column sums of the current chunk of SYM_CHUNK tiles
   __shared__ unsigned long long lds_col[SYM_CHUNK * TILE];
-  for (int e = threadIdx.x; e < SYM_CHUNK * TILE; e += WG_THREADS) lds_col[e] = 0ull;
+  __shared__ unsigned long long lds_col2[SQ ? SYM_CHUNK * TILE : 1];
+  for (int e = threadIdx.x; e < SYM_CHUNK * TILE; e += WG_THREADS) {
+    lds_col[e] = 0ull;
+    if constexpr (SQ) lds_col2[e] = 0ull;
+  }
   __syncthreads();
 
   uintx4 br[NIB][NB];
@@ -799,9 +837,9 @@ __attribute__((amdgpu_waves_per_eu(hx_waves<RID, 0, NIB>()))) void rowsum_sym_hx
     if (!UNIT && ib0 + ib < njb)
       wi[ib] = reinterpret_cast<const float*>(wp)[((ib0 + ib) * 64 + 16 * (p >> 2)) * 4 + (p & 3)];
   }
-  float acc[NIB], tot[NIB];
+  float acc[NIB], tot[NIB], acc2[NIB], tot2[NIB];
 #pragma unroll
-  for (int ib = 0; ib < NIB; ++ib) acc[ib] = tot[ib] = 0.f;
+  for (int ib = 0; ib < NIB; ++ib) acc[ib] = tot[ib] = acc2[ib] = tot2[ib] = 0.f;
 
   // column tile of range position jj (0 <= jj < span <= ntile + BT, cyclic over
   // the blocks); -1 for the padding tiles past the real columns
@@ -827,6 +865,10 @@ __attribute__((amdgpu_waves_per_eu(hx_waves<RID, 0, NIB>()))) void rowsum_sym_hx
       for (int ib = 0; ib < NIB; ++ib) {
         tot[ib] += acc[ib];
         acc[ib] = 0.f;
+        if constexpr (SQ) {
+          tot2[ib] += acc2[ib];
+          acc2[ib] = 0.f;
+        }
       }
     }
   };
@@ -840,9 +882,9 @@ __attribute__((amdgpu_waves_per_eu(hx_waves<RID, 0, NIB>()))) void rowsum_sym_hx
       const int J = tile_of(jj);
       if (J < 0) return;
       if (J >= ib0 && J < ib0 + NIB)
-        hx_rowsum_tile<RID, NIB, UNIT, true>(c, br, acc, J, ib0, g, p);
+        hx_rowsum_tile<RID, NIB, UNIT, true, SQ>(c, br, acc, J, ib0, g, p, &acc2);
       else
-        hx_rowsum_tile<RID, NIB, UNIT, false>(c, br, acc, J, ib0, g, p);
+        hx_rowsum_tile<RID, NIB, UNIT, false, SQ>(c, br, acc, J, ib0, g, p, &acc2);
     };
     HxCol<RID> b0, b1;
     b0.w = b1.w = floatx4{1.f, 1.f, 1.f, 1.f};
@@ -907,11 +949,11 @@ __attribute__((amdgpu_waves_per_eu(hx_waves<RID, 0, NIB>()))) void rowsum_sym_hx
       const int J = tile_of(s0 + u);
       const int64_t jl = (s0 + u - jj_begin) % SYM_CHUNK;
       if (J >= 0)
-        hx_sym_step<RID, NIB, UNIT, true>(t, xa[S ^ 1], br, w[S], wi, acc, jl, fix_scale, lds_col,
-                                          g, p);
+        hx_sym_step<RID, NIB, UNIT, true, SQ>(t, xa[S ^ 1], br, w[S], wi, acc, acc2, jl,
+                                              fix_scale, fix_scale2, lds_col, lds_col2, g, p);
       else
-        hx_sym_step<RID, NIB, UNIT, false>(t, xa[S ^ 1], br, w[S], wi, acc, jl, fix_scale,
-                                           lds_col, g, p);
+        hx_sym_step<RID, NIB, UNIT, false, SQ>(t, xa[S ^ 1], br, w[S], wi, acc, acc2, jl,
+                                               fix_scale, fix_scale2, lds_col, lds_col2, g, p);
       row_chunk(1);
       // end of a chunk of column tiles (the trip count is uniform over the
       // workgroup): add the chunk's column sums into the global accumulator
@@ -924,6 +966,11 @@ __attribute__((amdgpu_waves_per_eu(hx_waves<RID, 0, NIB>()))) void rowsum_sym_hx
           const int Jc = c0 + e / TILE < jj_end ? tile_of(c0 + e / TILE) : -1;
           if (v != 0ull && Jc >= 0) atomicAdd(colfix + int64_t(Jc) * TILE + e % TILE, v);
           lds_col[e] = 0ull;
+          if constexpr (SQ) {
+            const unsigned long long v2 = lds_col2[e];
+            if (v2 != 0ull && Jc >= 0) atomicAdd(colfix2 + int64_t(Jc) * TILE + e % TILE, v2);
+            lds_col2[e] = 0ull;
+          }
         }
         __syncthreads();
       }
@@ -939,6 +986,12 @@ __attribute__((amdgpu_waves_per_eu(hx_waves<RID, 0, NIB>()))) void rowsum_sym_hx
     v += __shfl_xor(v, 16);
     v += __shfl_xor(v, 32);
     if (g == 0) part[split * nrpad + (ib0 + ib) * TILE + p] = v;
+    if constexpr (SQ) {
+      float v2 = (tot2[ib] + acc2[ib]) * 0x1p-30f;
+      v2 += __shfl_xor(v2, 16);
+      v2 += __shfl_xor(v2, 32);
+      if (g == 0) part2[split * nrpad + (ib0 + ib) * TILE + p] = v2;
+    }
   }
 }
 
@@ -1016,35 +1069,48 @@ void rowsum_hx_u(const KVPlan& p, const PointPack& rows, const PointPack& cols, 
     rowsum_hx_launch<RID, 4, false>(p, rows, cols, wp, diag, out, part, stream);
 }
 
-template <int RID, int NIB, bool UNIT>
+template <int RID, int NIB, bool UNIT, bool SQ>
 void rowsum_sym_hx_launch(const KVPlan& p, const PointPack& rows, const PointPack& cols,
                           const float* wp, float* part, unsigned long long* colfix,
-                          double fix_scale, hipStream_t stream) {
+                          double fix_scale, const SymSquares& sq, hipStream_t stream) {
   const unsigned grid = unsigned(p.nrt * p.nsplit);
   ProfScope prof(FD_KERNEL_ROWSUM, stream);
-  hipLaunchKernelGGL((rowsum_sym_hx_kernel<RID, NIB, UNIT>), dim3(grid), dim3(WG_THREADS), 0, stream,
-                     reinterpret_cast<const uintx4*>(cols.xp.p),
+  hipLaunchKernelGGL((rowsum_sym_hx_kernel<RID, NIB, UNIT, SQ>), dim3(grid), dim3(WG_THREADS), 0,
+                     stream, reinterpret_cast<const uintx4*>(cols.xp.p),
                      reinterpret_cast<const floatx4*>(wp),
                      reinterpret_cast<const uintx4*>(rows.xp.p), p.nrt, p.njb, p.jb_per_split,
-                     int64_t(p.nsplit), part, rows.npad, colfix, fix_scale);
+                     int64_t(p.nsplit), part, rows.npad, colfix, fix_scale, sq.part, sq.colfix,
+                     sq.fix_scale);
   FD_LAUNCH_CHECK();
 }
 
 template <int RID>
 void rowsum_sym_hx_u(const KVPlan& p, const PointPack& rows, const PointPack& cols,
                      const float* wp, float* part, unsigned long long* colfix, double fix_scale,
-                     hipStream_t stream) {
+                     const SymSquares& sq, hipStream_t stream) {
+  if (sq.part != nullptr) {
+    // squared sums: weighted passes of the eight-tile plan only
+    FD_REQUIRE(p.nib == 8 && wp != nullptr, FD_ERR_INVALID_ARG,
+               "internal: squared sums need a weighted eight-tile pass");
+    rowsum_sym_hx_launch<RID, 8, false, true>(p, rows, cols, wp, part, colfix, fix_scale, sq,
+                                              stream);
+    return;
+  }
   if (p.nib == 4) {
     if (wp == nullptr)
-      rowsum_sym_hx_launch<RID, 4, true>(p, rows, cols, wp, part, colfix, fix_scale, stream);
+      rowsum_sym_hx_launch<RID, 4, true, false>(p, rows, cols, wp, part, colfix, fix_scale, sq,
+                                                stream);
     else
-      rowsum_sym_hx_launch<RID, 4, false>(p, rows, cols, wp, part, colfix, fix_scale, stream);
+      rowsum_sym_hx_launch<RID, 4, false, false>(p, rows, cols, wp, part, colfix, fix_scale, sq,
+                                                 stream);
     return;
   }
   if (wp == nullptr)
-    rowsum_sym_hx_launch<RID, 8, true>(p, rows, cols, wp, part, colfix, fix_scale, stream);
+    rowsum_sym_hx_launch<RID, 8, true, false>(p, rows, cols, wp, part, colfix, fix_scale, sq,
+                                              stream);
   else
-    rowsum_sym_hx_launch<RID, 8, false>(p, rows, cols, wp, part, colfix, fix_scale, stream);
+    rowsum_sym_hx_launch<RID, 8, false, false>(p, rows, cols, wp, part, colfix, fix_scale, sq,
+                                               stream);
 }
 
 void check_hx(const KVPlan& p, const PointPack& rows, const PointPack& cols) {
@@ -1129,7 +1195,7 @@ void launch_product_hx(const KVPlan& p, const PointPack& rows, const PointPack& 
 
 void launch_rowsum_sym_hx(const KVPlan& p, const PointPack& rows, const PointPack& cols,
                           const float* wp, float* part, unsigned long long* colfix,
-                          double fix_scale, hipStream_t stream) {
+                          double fix_scale, const SymSquares& sq, hipStream_t stream) {
   FD_REQUIRE(rows.rid >= 0 && rows.rid < HX_RECIPES && rows.rid == cols.rid && rows.row_side &&
                  !cols.row_side && rows.n == cols.n,
              FD_ERR_INVALID_ARG, "internal: symmetric row sums need one point set");
@@ -1140,13 +1206,13 @@ void launch_rowsum_sym_hx(const KVPlan& p, const PointPack& rows, const PointPac
   check_span(rows.xp, size_t(rows.npad / TILE) * R.nb * 64 * 4, "split row pack");
   check_span(cols.xp, size_t(round_up(p.njb, 2)) * R.nc * 64 * 4, "split column pack");
   switch (rows.rid) {
-    case 0: return rowsum_sym_hx_u<0>(p, rows, cols, wp, part, colfix, fix_scale, stream);
-    case 1: return rowsum_sym_hx_u<1>(p, rows, cols, wp, part, colfix, fix_scale, stream);
-    case 2: return rowsum_sym_hx_u<2>(p, rows, cols, wp, part, colfix, fix_scale, stream);
-    case 3: return rowsum_sym_hx_u<3>(p, rows, cols, wp, part, colfix, fix_scale, stream);
-    case 4: return rowsum_sym_hx_u<4>(p, rows, cols, wp, part, colfix, fix_scale, stream);
-    case 5: return rowsum_sym_hx_u<5>(p, rows, cols, wp, part, colfix, fix_scale, stream);
-    case 6: return rowsum_sym_hx_u<6>(p, rows, cols, wp, part, colfix, fix_scale, stream);
+    case 0: return rowsum_sym_hx_u<0>(p, rows, cols, wp, part, colfix, fix_scale, sq, stream);
+    case 1: return rowsum_sym_hx_u<1>(p, rows, cols, wp, part, colfix, fix_scale, sq, stream);
+    case 2: return rowsum_sym_hx_u<2>(p, rows, cols, wp, part, colfix, fix_scale, sq, stream);
+    case 3: return rowsum_sym_hx_u<3>(p, rows, cols, wp, part, colfix, fix_scale, sq, stream);
+    case 4: return rowsum_sym_hx_u<4>(p, rows, cols, wp, part, colfix, fix_scale, sq, stream);
+    case 5: return rowsum_sym_hx_u<5>(p, rows, cols, wp, part, colfix, fix_scale, sq, stream);
+    case 6: return rowsum_sym_hx_u<6>(p, rows, cols, wp, part, colfix, fix_scale, sq, stream);
   }
 }
 

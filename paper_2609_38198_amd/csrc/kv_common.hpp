@@ -77,9 +77,12 @@ void launch_rowsum_hx(const KVPlan& p, const PointPack& rows, const PointPack& c
 // Symmetric row sums of one point set (rows.n == cols.n): per-split row partials
 // into part ([nsplit][rows.npad]) and column sums added into colfix (64-bit fixed
 // point, fix_scale per unit of the shifted kernel 2^15 K; weights in [0, 1]).
+// With sq.part set (weighted passes only), the unit-weight sums of the squared
+// kernel K^2 (the kernel at twice the bandwidth) go the same way into sq.part
+// and sq.colfix, sq.fix_scale per unit of (2^15 K)^2.
 void launch_rowsum_sym_hx(const KVPlan& p, const PointPack& rows, const PointPack& cols,
                           const float* wp, float* part, unsigned long long* colfix,
-                          double fix_scale, hipStream_t stream);
+                          double fix_scale, const SymSquares& sq, hipStream_t stream);
 
 // Scheduling pattern for a region holding M matrix instructions and E
 // exponentials: each matrix instruction followed by its share of the

@@ -726,6 +726,48 @@ __global__ void degree_reduce_ds_kernel(const float* __restrict__ part, int nspl
   colfix[i] = 0ull;
 }
 
+// Pass 2 of a dyadic level: degree_reduce_ds_kernel's outputs, and from the
+// squared-kernel sums of the same pass the next level's q (K(2 beta) 1, the
+// reduction in the same order as degree_reduce_q_kernel's) with its
+// w = q^-alpha written to the weight pack as degree_reduce_q_kernel writes it.
+__global__ void degree_reduce_dsq_kernel(const float* __restrict__ part, int nsplit,
+                                         int64_t nrpad, unsigned long long* __restrict__ colfix,
+                                         double inv_fix, const float* __restrict__ q, int64_t n,
+                                         int64_t npad, double alpha, float* __restrict__ d,
+                                         float* __restrict__ s, const float* __restrict__ part2,
+                                         unsigned long long* __restrict__ colfix2,
+                                         float* __restrict__ q_next, float* __restrict__ wpk,
+                                         int64_t wnpad) {
+  const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i >= npad) return;
+  float wn = 0.f;
+  if (i < n) {
+    double sum = 0.0;
+    for (int k = 0; k < nsplit; ++k) sum += double(part[k * nrpad + i]);
+    sum += double(static_cast<long long>(colfix[i])) * inv_fix;
+    const float ti = float(sum);
+    const double w = pow(double(q[i]), -alpha);
+    const double dd = w * double(ti);
+    if (d != nullptr) d[i] = float(dd);
+    if (s != nullptr) s[i] = float(w / sqrt(dd));
+    double sum2 = 0.0;
+    for (int k = 0; k < nsplit; ++k) sum2 += double(part2[k * nrpad + i]);
+    sum2 += double(static_cast<long long>(colfix2[i])) * inv_fix;
+    const float qn = float(sum2);
+    q_next[i] = qn;
+    wn = float(pow(double(qn), -alpha));
+  }
+  colfix[i] = 0ull;
+  colfix2[i] = 0ull;
+  if (i < wnpad) {
+    const int64_t jb = i / TILE;
+    const int jj = int(i % TILE), g = jj / 4, r = jj % 4;
+    float* base = wpk + (jb * 64 + 16 * g) * 4 + r;
+#pragma unroll
+    for (int p = 0; p < 16; ++p) base[4 * p] = wn;
+  }
+}
+
 // sum(q) - n in double, one workgroup, fixed order (deterministic)
 __global__ __launch_bounds__(1024) void sum_minus_n_kernel(const float* __restrict__ q, int64_t n,
                                                             double* __restrict__ out) {
@@ -1049,7 +1091,7 @@ bool rowsum_sym_applies(const PointPack& rows, const PointPack& cols, bool diag,
 
 SymPass launch_rowsum_sym_pass(const KVPlan& p, const PointPack& rows, const PointPack& cols,
                                FSpan wp, FSpan part, unsigned long long* colfix, bool zero_colfix,
-                               hipStream_t stream) {
+                               hipStream_t stream, FSpan sq_part, unsigned long long* sq_colfix) {
   check_tiles(p, rows, cols);
   FD_REQUIRE(rowsum_sym_applies(rows, cols, true, colfix), FD_ERR_INVALID_ARG,
              "internal: symmetric row sums need one float32 point set");
@@ -1064,7 +1106,15 @@ SymPass launch_rowsum_sym_pass(const KVPlan& p, const PointPack& rows, const Poi
                        colfix, rows.npad);
     FD_LAUNCH_CHECK();
   }
-  launch_rowsum_sym_hx(sp, rows, cols, wp.p, part.p, colfix, std::ldexp(1.0, F - 15), stream);
+  SymSquares sq;
+  if (sq_part.p != nullptr) {
+    FD_REQUIRE(wp.p != nullptr && sq_colfix != nullptr, FD_ERR_INVALID_ARG,
+               "internal: squared sums ride on a weighted pass");
+    check_span(sq_part, size_t(sp.nsplit) * rows.npad, "partial squared row sums");
+    // (2^15 K)^2 per unit: K^2 <= 1 keeps the same headroom as the weights
+    sq = SymSquares{sq_part.p, sq_colfix, std::ldexp(1.0, F - 30)};
+  }
+  launch_rowsum_sym_hx(sp, rows, cols, wp.p, part.p, colfix, std::ldexp(1.0, F - 15), sq, stream);
   return SymPass{int(sp.nsplit), std::ldexp(1.0, -F)};
 }
 
@@ -1086,6 +1136,28 @@ void launch_degree_reduce_ds(const SymPass& sp, const PointPack& rows, FSpan par
   hipLaunchKernelGGL(degree_reduce_ds_kernel, dim3(blocks_for(rows.npad, 256)), dim3(256), 0,
                      stream, part.p, sp.nsplit, rows.npad, colfix, sp.inv_fix, q, rows.n,
                      rows.npad, alpha, d, s);
+  FD_LAUNCH_CHECK();
+}
+
+void launch_degree_reduce_dsq(const SymPass& sp, const PointPack& rows, const PointPack& cols,
+                              FSpan part, unsigned long long* colfix, const float* q,
+                              double alpha, float* d, float* s, FSpan sq_part,
+                              unsigned long long* sq_colfix, float* q_next, FSpan wp,
+                              hipStream_t stream) {
+  FD_REQUIRE(cols.npad % TILE == 0 && cols.npad <= rows.npad && cols.n == rows.n,
+             FD_ERR_INVALID_ARG, "internal: bad weight pack geometry");
+  check_span(wp, lane4_extent(cols.npad / TILE, 1), "weight pack");
+  check_span(sq_part, size_t(sp.nsplit) * rows.npad, "partial squared row sums");
+  FD_REQUIRE(q_next != nullptr && sq_colfix != nullptr, FD_ERR_INVALID_ARG,
+             "internal: dyadic reduction outputs");
+  hipLaunchKernelGGL(degree_reduce_dsq_kernel, dim3(blocks_for(rows.npad, 256)), dim3(256), 0,
+                     stream, part.p, sp.nsplit, rows.npad, colfix, sp.inv_fix, q, rows.n,
+                     rows.npad, alpha, d, s, sq_part.p, sq_colfix, q_next, wp.p, cols.npad);
+  FD_LAUNCH_CHECK();
+}
+
+void launch_zero_u64(unsigned long long* p, int64_t n, hipStream_t stream) {
+  hipLaunchKernelGGL(zero_u64_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, stream, p, n);
   FD_LAUNCH_CHECK();
 }
 

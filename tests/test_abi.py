@@ -46,6 +46,9 @@ def test_workspace_sizes():
     assert fd.fd_workspace_size(fd.FD_OP_KERNEL_MATMUL, 10, 10, 65, 4) == 0   # D > 64
     assert fd.fd_workspace_size(fd.FD_OP_KERNEL_MATMUL, 10, 10, 4, 65) == 0   # b > 64
     assert fd.fd_workspace_size(fd.FD_OP_DEGREE, 1 << 20, 1 << 20, 30) > 0
+    # the dyadic ladder adds the squared-kernel partial sums to the degree workspace
+    assert (fd.fd_workspace_size(fd.FD_OP_DEGREE_DYADIC, 65536, 65536, 12)
+            > fd.fd_workspace_size(fd.FD_OP_DEGREE, 65536, 65536, 12) > 0)
     assert fd.fd_workspace_size(fd.FD_OP_BLOCK_LANCZOS, 2048, 2048, 4, 8, 16) > 0
     assert fd.fd_workspace_size(fd.FD_OP_BLOCK_LANCZOS, 10, 10, 4, 8, 11) == 0  # k > N
 
@@ -73,6 +76,14 @@ def test_host_validation_without_gpu():
     assert lib.fd_degree(fake, 0, 10, 4, 4, 1.0, 1.5, None, None, None, None, None, 0, None) == 1
     assert lib.fd_degree(fake, 0, 10, 4, 4, 0.0, 0.5, None, None, None, None, None, 0, None) == 1
     assert b"alpha" in lib.fd_last_error() or b"beta" in lib.fd_last_error()
+    # dyadic ladder: levels outside [1, 32], beta0 <= 0, beta0 2^(nbeta-1) not finite
+    # in float, alpha out of range, missing workspace
+    for beta0, nb, alpha in ((1.0, 0, 0.5), (1.0, 33, 0.5), (0.0, 2, 0.5), (3e38, 3, 0.5),
+                             (1.0, 2, -0.1)):
+        assert lib.fd_degree_dyadic(fake, 0, 10, 4, 4, beta0, nb, alpha, None, None, None, None,
+                                    None, 0, None) == 1
+    assert lib.fd_degree_dyadic(fake, 0, 10, 4, 4, 1.0, 3, 0.5, None, None, None, None, None, 0,
+                                None) == 3
 
 
 def test_struct_layouts_match_the_header(tmp_path):

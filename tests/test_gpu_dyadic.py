@@ -1,0 +1,139 @@
+"""Parity of fd_degree_dyadic (normalisation vectors of a dyadic beta ladder).
+
+Level l at beta_l = beta0 2^l must equal fd_degree at beta_l: q = K 1,
+d = w (K w), s = w d^-1/2 with w = q^-alpha (Sec. 2.1), S_off = sum(q) - N
+(Sec. 2.3).  On the float32 symmetric path the degree of level l + 1 is the
+row sum of the squared kernel of level l (K(2 beta) = K(beta)^2 entrywise,
+eq. kernel), accumulated in level l's second pass; other inputs run the
+levels one by one.  Checked against the float64 oracle (relative 2-norm
+<= 1e-5 per vector), against fd_degree at the full 6-torus size, through the
+Markov rows P 1 = 1 built from the ladder's own w and d, and on a grid torus
+against the circulant closed form of q at every level.
+"""
+import numpy as np
+import pytest
+import torch
+
+from gpu_util import TOL_F32, case, device, rel_fro, to_dev, to_np
+from oracle import normalise as on
+from oracle import torus_grid as tg
+from paper_2609_38198_amd import _lib as fd
+from paper_2609_38198_amd import inputs
+
+pytestmark = pytest.mark.gpu
+
+
+def _check_against_oracle(X, beta0, nbeta, alpha, dev):
+    lad = fd.fd_degree_dyadic(to_dev(X, dev), beta0, nbeta, alpha)
+    s_off = to_np(lad.s_off)
+    for l in range(nbeta):
+        beta = beta0 * 2.0 ** l
+        ref = on.normalise(X, beta, alpha)
+        for name in ("q", "d", "s"):
+            err = rel_fro(to_np(getattr(lad, name)[l]), getattr(ref, name))
+            assert err <= TOL_F32, (l, name, err)
+        assert abs(s_off[l] - ref.s_off) <= TOL_F32 * float(ref.q.sum()), l
+
+
+@pytest.mark.parametrize("alpha", [0.5, 1.0, 0.0])
+def test_torus2_ladder_matches_oracle(alpha):
+    w = inputs.torus2()
+    dev = device()
+    case(f"dyadic degree torus2 beta 0.5..8 alpha={alpha}")
+    _check_against_oracle(w.X, 0.5, 5, alpha, dev)
+
+
+@pytest.mark.parametrize("N", [1, 2, 513, 1001, 3583])
+def test_ragged_and_block_counts(N):
+    # one block, even and odd block counts, ragged last blocks
+    rng = np.random.default_rng(400 + N)
+    X = rng.normal(size=(N, 7)).astype(np.float32)
+    X -= X.mean(0)
+    dev = device()
+    case(f"dyadic degree N={N} D=7 beta 0.05..0.8")
+    _check_against_oracle(X, 0.05, 5, 0.5, dev)
+
+
+def test_one_level_equals_fd_degree_bitwise():
+    w = inputs.torus2()
+    dev = device()
+    X = to_dev(w.X, dev)
+    case("dyadic degree one level vs fd_degree")
+    lad = fd.fd_degree_dyadic(X, 2.0, 1, 0.5)
+    ref = fd.fd_degree(X, 2.0, 0.5)
+    torch.cuda.synchronize()
+    for name in ("q", "d", "s"):
+        assert torch.equal(getattr(lad, name)[0], getattr(ref, name)), name
+
+
+def test_torus6_full_size_against_fd_degree_and_markov_rows():
+    # the bench's sweep: beta in {0.5, 1, 2, 4, 8} at N = 65,536 (many blocks,
+    # whole-block column splits); levels 1..4 take q from the squared sums
+    w = inputs.torus6()
+    dev = device()
+    X = to_dev(w.X, dev)
+    case("dyadic degree torus6 N=65536 beta 0.5..8")
+    lad = fd.fd_degree_dyadic(X, 0.5, 5, 0.5)
+    again = fd.fd_degree_dyadic(X, 0.5, 5, 0.5)
+    torch.cuda.synchronize()
+    for name in ("q", "d", "s", "s_off"):
+        assert torch.equal(getattr(lad, name), getattr(again, name)), name
+    ones = torch.ones((w.N, 1), dtype=torch.float32, device=dev)
+    for l, beta in enumerate((0.5, 1.0, 2.0, 4.0, 8.0)):
+        ref = fd.fd_degree(X, beta, 0.5)
+        for name in ("q", "d", "s"):
+            err = rel_fro(to_np(getattr(lad, name)[l]), to_np(getattr(ref, name)))
+            assert err <= TOL_F32, (beta, name, err)
+        if l == 0:
+            assert torch.equal(lad.q[0], ref.q)
+        # P 1 = diag(d)^-1 diag(w) K diag(w) 1 from the ladder's own vectors
+        wv = lad.q[l].double().pow(-0.5).float()
+        sl = (wv.double() / lad.d[l].double()).float()
+        P1 = to_np(fd.fd_kernel_matmul(X, None, beta, ones, sl=sl, sr=wv))[:, 0]
+        assert np.abs(P1 - 1.0).max() <= 1e-5, beta
+    # sampled rows of the squared-sum degrees against the oracle
+    from oracle import kernel as ok
+    rows = np.random.default_rng(5).choice(w.N, 128, replace=False)
+    for l in (1, 4):
+        beta = 0.5 * 2.0 ** l
+        qref = ok.kernel_matmul(w.X, None, beta, np.ones(w.N), rows=rows, threads=8)
+        assert rel_fro(to_np(lad.q[l])[rows], qref) <= TOL_F32, beta
+
+
+def test_grid_torus_every_level_constant_degree():
+    counts = (8, 8, 8, 8, 4, 4)
+    X = inputs.grid_torus_points(counts).astype(np.float32)
+    dev = device()
+    case("dyadic degree grid torus 65536 beta 0.25..4")
+    lad = fd.fd_degree_dyadic(to_dev(X, dev), 0.25, 5, 0.5)
+    for l in range(5):
+        beta = 0.25 * 2.0 ** l
+        q0 = tg.degree(counts, beta)
+        q = to_np(lad.q[l])
+        assert np.abs(q / q0 - 1).max() <= 1e-5, beta
+        s = to_np(lad.s[l])
+        assert np.abs(s * np.sqrt(q0) - 1).max() <= 1e-5, beta
+
+
+def test_bf16_runs_level_by_level():
+    s = inputs.stress(N=4096)
+    dev = device()
+    X = to_dev(s.X, dev)
+    beta0 = s.betas[0]
+    case("dyadic degree bf16 N=4096 D=64")
+    lad = fd.fd_degree_dyadic(X, beta0, 3, 0.5)
+    torch.cuda.synchronize()
+    for l in range(3):
+        ref = fd.fd_degree(X, beta0 * 2.0 ** l, 0.5)
+        torch.cuda.synchronize()
+        for name in ("q", "d", "s"):
+            assert torch.equal(getattr(lad, name)[l], getattr(ref, name)), (l, name)
+
+
+def test_invalid_arguments_raise():
+    dev = device()
+    X = torch.zeros((10, 4), device=dev)
+    for beta0, nb, alpha in ((0.0, 2, 0.5), (1.0, 0, 0.5), (1.0, 33, 0.5), (3e38, 3, 0.5),
+                             (1.0, 2, 1.5)):
+        with pytest.raises(fd.FdError):
+            fd.fd_degree_dyadic(X, beta0, nb, alpha)
