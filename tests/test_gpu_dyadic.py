@@ -137,3 +137,31 @@ def test_invalid_arguments_raise():
                              (1.0, 2, 1.5)):
         with pytest.raises(fd.FdError):
             fd.fd_degree_dyadic(X, beta0, nb, alpha)
+
+
+@pytest.mark.parametrize("which", ["torus6_noisy", "molecule_2_18"])
+def test_large_sets_against_fd_degree(which):
+    # the layouts for D <= 13 and D <= 30 at 2^18 points (whole-block column
+    # splits, 512 blocks); each level against fd_degree, sampled rows of a
+    # squared-sum degree against the oracle
+    dev = device()
+    if which == "torus6_noisy":
+        w = inputs.torus6_noisy()
+        Xh, beta0 = w.X, 0.5
+    else:
+        Xh = inputs.molecule_points(1 << 18).astype(np.float32)
+        beta0 = 0.25 / inputs.median_sq_distance(Xh)
+    X = to_dev(Xh, dev)
+    N = Xh.shape[0]
+    case(f"dyadic degree {which} N={N} D={Xh.shape[1]} beta0={beta0:.4g} x 2^0..3")
+    lad = fd.fd_degree_dyadic(X, beta0, 4, 0.5)
+    for l in range(4):
+        beta = beta0 * 2.0 ** l
+        ref = fd.fd_degree(X, beta, 0.5)
+        for name in ("q", "d", "s"):
+            err = rel_fro(to_np(getattr(lad, name)[l]), to_np(getattr(ref, name)))
+            assert err <= TOL_F32, (l, name, err)
+    from oracle import kernel as ok
+    rows = np.random.default_rng(9).choice(N, 64, replace=False)
+    qref = ok.kernel_matmul(Xh, None, beta0 * 8.0, np.ones(N), rows=rows, threads=8)
+    assert rel_fro(to_np(lad.q[3])[rows], qref) <= TOL_F32
