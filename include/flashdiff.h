@@ -41,7 +41,7 @@ extern "C" {
 typedef enum fd_status {
   FD_OK = 0,
   FD_ERR_INVALID_ARG = 1,    /* bad size, pointer, or parameter value */
-  FD_ERR_UNSUPPORTED = 2,    /* valid request this build does not implement */
+  FD_ERR_UNSUPPORTED = 2,    /* valid request the library does not implement */
   FD_ERR_WORKSPACE = 3,      /* workspace missing, too small or misaligned */
   FD_ERR_HIP = 4,            /* a HIP runtime or launch error (message has it) */
   FD_ERR_NOT_CONVERGED = 5,  /* eigensolver stopped early; outputs hold best Ritz pairs */

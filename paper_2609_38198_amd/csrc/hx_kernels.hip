@@ -11,22 +11,26 @@
 // every b', computed in float64) is written as three float16 pieces
 // v = v1 + v2 + v3 (each the round-to-nearest float16 of the remainder), which
 // represents a float32 value exactly (33 >= 24 significant bits) unless a piece
-// underflows.  The contraction keeps the six products whose pieces sum to at
-// most four (x1 b1, x2 b1, x1 b2, x3 b1, x1 b3, x2 b2); the three dropped ones
-// are below 2^-30 of the term.  Products of float16 values are exact in
-// float32, so the exponent carries only the float32 accumulation rounding, as a
-// float32 contraction would.  The offsets a_i and a_j enter the same
-// contraction as three float16 pieces each, multiplied by slots holding 1, and
-// sit in the first instruction next to x1 b1 so the large Gram terms cancel
-// early.  x' = s x and b' = b / s with s = 2^e, e ~ log2(2 beta log2 e) / 2,
-// keep both operands near the same magnitude; s cancels exactly in x' . b'.
+// underflows.  Products of float16 values are exact in float32.  For D <= 4
+// the contraction keeps the six products whose pieces sum to at most four
+// (x1 b1, x2 b1, x1 b2, x3 b1, x1 b3, x2 b2; the dropped ones are below 2^-30
+// of the term), so the exponent carries only the float32 accumulation rounding.
+// For larger D it keeps x1 b1, x2 b1 and x1 b2 (and x3 b1 where it fits for
+// free): the dropped products are at most 3 * 2^-22 of |x_jk b_ik| each, the
+// order of the float32 rounding of the Gram-form sum itself, for half the
+// matrix instructions.  The offsets a_i and a_j enter the same contraction as
+// float16 pieces (three, or two where the third does not fit), multiplied by
+// slots holding 1, and sit in the first instruction next to x1 b1 so the large
+// Gram terms cancel early.  x' = s x and b' = b / s with s = 2^e,
+// e ~ log2(2 beta log2 e) / 2, keep both operands near the same magnitude; s
+// cancels exactly in x' . b'.
 //
 // Why float16: on gfx950 a v_mfma_f32_16x16x32_f16 (32 slots) issues every 16
 // cycles per SIMD, a v_mfma_f32_16x16x4_f32 (4 slots) every 32.  Measured on
 // the device, a matrix instruction holds off ordinary vector instructions of
 // the SIMD for most of its duration (the exponentials overlap it only in
 // part), so a tile costs about the sum of its instruction times and the
-// cheaper float16 contraction (3 instructions for D <= 13 instead of 4 float32
+// cheaper float16 contraction (2 instructions for D <= 13 instead of 4 float32
 // ones at twice the cost each) shortens it directly.
 //
 // Pack layout (both sides): per 16-point tile and 32-slot chunk c, lane (g, p)
@@ -49,7 +53,8 @@
 //
 // Accuracy condition (either contraction form): the Gram form cancels terms of
 // size beta ||x||^2; inputs should be centred so that this stays moderate
-// (float32 resolves t to about 2^-24 beta log2(e) max ||x||^2).  Pieces are
+// (float32 resolves t to about 2^-24 beta log2(e) max ||x||^2, the short split
+// to a small multiple of 2^-22 of it).  Pieces are
 // saturated to the float16 range, so even beyond that every value is finite.
 #include <hip/hip_runtime.h>
 
@@ -74,7 +79,7 @@ enum : int8_t { SEG_END = 0, SEG_X = 1, SEG_ONES = 2, SEG_A = 3 };
 struct HxSeg {
   int8_t kind, piece, slot, cap, foff;
 };
-constexpr int HX_SEGS = 8, HX_CHUNKS = 7, HX_MFMAS = 13, HX_RECIPES = 7;
+constexpr int HX_SEGS = 8, HX_CHUNKS = 5, HX_MFMAS = 7, HX_RECIPES = 7;
 struct HxChunk {
   HxSeg s[HX_SEGS];
 };
@@ -82,9 +87,10 @@ struct HxSide {
   HxChunk ch[HX_CHUNKS];
 };
 // nc / nb: chunks per column / row point; instruction m multiplies column
-// chunk sa[m] by row chunk sb[m].
+// chunk sa[m] by row chunk sb[m].  order: the recipe holds every piece product
+// x_p b_q with p + q <= order (4: the exact split, 3: the short split).
 struct HxRecipe {
-  int8_t maxd, nc, nb, nm;
+  int8_t maxd, nc, nb, nm, order;
   int8_t sa[HX_MFMAS], sb[HX_MFMAS];
   HxSide col, row;
 };
@@ -101,63 +107,70 @@ constexpr HxSeg APC(int slot, int k) { return HxSeg{SEG_A, int8_t(k), int8_t(slo
 
 // Column side: x pieces, a_j against row-side 1s; row side: b pieces, a_i
 // against column-side 1s.  Slot by slot the column and row chunks of each
-// instruction pair as (x_p, b_q) with p + q <= 4, (1, a_i) or (a_j, 1); every
-// other slot pairing has a zero on one side.
+// instruction pair as (x_p, b_q), (1, a_i) or (a_j, 1); every other slot
+// pairing has a zero on one side.
+//
+// D <= 4 fits the exact split in one instruction.  Above that the recipes
+// keep the products of order p + q <= 3 (x1 b1, x2 b1, x1 b2) and the offset
+// pieces 1 and 2, plus what fits in the same instructions for free (x3 b1 and
+// the third offset pieces for some D).  The dropped terms are at most
+// 3 * 2^-22 |x_jk b_ik| per feature and 2^-22 |a| per offset, the order of the
+// float32 rounding of the Gram-form sum itself, and the contraction needs
+// about half the instructions of the exact split.
 constexpr HxRecipe HX_TABLE[HX_RECIPES] = {
-    // D <= 4: one instruction
-    {4, 1, 1, 1, {0}, {0},
+    // D <= 4: one instruction, exact split
+    {4, 1, 1, 1, 4, {0}, {0},
      {{{{X(1, 0, 4), X(2, 4, 4), X(1, 8, 4), X(3, 12, 4), X(1, 16, 4), X(2, 20, 4), ONES(24),
          AOF(27)}}}},
      {{{{X(1, 0, 4), X(1, 4, 4), X(2, 8, 4), X(1, 12, 4), X(3, 16, 4), X(2, 20, 4), AOF(24),
          ONES(27)}}}}},
-    // D <= 8: x1b1 + x2b1 + x3b1 + a_i + a_j, then x1b2 + x1b3 + x2b2
-    {8, 2, 2, 2, {0, 1}, {0, 1},
-     {{{{X(1, 0, 8), X(2, 8, 8), X(3, 16, 8), ONES(24), AOF(27)}},
-       {{X(1, 0, 8), X(1, 8, 8), X(2, 16, 8)}}}},
-     {{{{X(1, 0, 8), X(1, 8, 8), X(1, 16, 8), AOF(24), ONES(27)}},
-       {{X(2, 0, 8), X(3, 8, 8), X(2, 16, 8)}}}}},
-    // D <= 13: column chunk 0 serves two instructions
-    {13, 2, 3, 3, {0, 1, 0}, {0, 1, 2},
+    // D <= 8: x1b1 + x2b1 + x1b2 + a_i + a_j in one instruction
+    {8, 1, 1, 1, 3, {0}, {0},
+     {{{{X(1, 0, 8), X(2, 8, 8), X(1, 16, 8), ONES(24), AOF(27)}}}},
+     {{{{X(1, 0, 8), X(1, 8, 8), X(2, 16, 8), AOF(24), ONES(27)}}}}},
+    // D <= 13: x1b1 + a_i + x2b1 + a_j, then x1b2 + x3b1 (column chunk 0
+    // pairs with row chunk 0, column chunk 1 with row chunk 1)
+    {13, 2, 2, 2, 3, {0, 1}, {0, 1},
      {{{{X(1, 0, 13), ONES(13), X(2, 16, 13), AOF(29)}},
        {{X(1, 0, 13), X(3, 16, 13)}}}},
      {{{{X(1, 0, 13), AOF(13), X(1, 16, 13), ONES(29)}},
-       {{X(2, 0, 13), X(1, 16, 13)}},
-       {{X(3, 0, 13), X(2, 16, 13)}}}}},
+       {{X(2, 0, 13), X(1, 16, 13)}}}}},
     // D <= 30: one piece per chunk; the offsets use the two spare slots of
-    // each chunk.  Slot 30: 1 on x1 against a_i1, a_i2, a_i3 on b1, b2, b3;
-    // slot 31: a_j1, a_j2, a_j3 on x1, x2, x3 against 1 on b1.  The six
-    // instructions meet each offset piece exactly once.
-    {30, 3, 3, 6, {0, 1, 0, 2, 0, 1}, {0, 0, 1, 0, 2, 1},
-     {{{{X(1, 0, 30), ONES(30, 1), APC(31, 1)}}, {{X(2, 0, 30), APC(31, 2)}},
-       {{X(3, 0, 30), APC(31, 3)}}}},
-     {{{{X(1, 0, 30), APC(30, 1), ONES(31, 1)}}, {{X(2, 0, 30), APC(30, 2)}},
-       {{X(3, 0, 30), APC(30, 3)}}}}},
+    // each chunk.  Slot 30: 1 on x1 against a_i1, a_i2 on b1, b2; slot 31:
+    // a_j1, a_j2 on x1, x2 against 1 on b1.  The three instructions meet each
+    // of these offset pieces exactly once.
+    {30, 2, 2, 3, 3, {0, 1, 0}, {0, 0, 1},
+     {{{{X(1, 0, 30), ONES(30, 1), APC(31, 1)}}, {{X(2, 0, 30), APC(31, 2)}}}},
+     {{{{X(1, 0, 30), APC(30, 1), ONES(31, 1)}}, {{X(2, 0, 30), APC(30, 2)}}}}},
     // D <= 32: offsets in a chunk of their own
-    {32, 4, 4, 7, {0, 3, 1, 0, 2, 0, 1}, {0, 3, 0, 1, 0, 2, 1},
-     {{{{X(1, 0, 32)}}, {{X(2, 0, 32)}}, {{X(3, 0, 32)}}, {{ONES(0), AOF(3)}}}},
-     {{{{X(1, 0, 32)}}, {{X(2, 0, 32)}}, {{X(3, 0, 32)}}, {{AOF(0), ONES(3)}}}}},
+    {32, 3, 3, 4, 3, {0, 2, 1, 0}, {0, 2, 0, 1},
+     {{{{X(1, 0, 32)}}, {{X(2, 0, 32)}}, {{ONES(0), AOF(3)}}}},
+     {{{{X(1, 0, 32)}}, {{X(2, 0, 32)}}, {{AOF(0), ONES(3)}}}}},
     // D <= 62: two chunks per piece; the offsets take the spare slots of the
     // second chunks, laid out as for D <= 30
-    {62, 6, 6, 12, {0, 1, 2, 3, 0, 1, 4, 5, 0, 1, 2, 3}, {0, 1, 0, 1, 2, 3, 0, 1, 4, 5, 2, 3},
+    {62, 4, 4, 6, 3, {0, 1, 2, 3, 0, 1}, {0, 1, 0, 1, 2, 3},
      {{{{X(1, 0, 32)}}, {{X(1, 0, 30, 32), ONES(30, 1), APC(31, 1)}}, {{X(2, 0, 32)}},
-       {{X(2, 0, 30, 32), APC(31, 2)}}, {{X(3, 0, 32)}}, {{X(3, 0, 30, 32), APC(31, 3)}}}},
+       {{X(2, 0, 30, 32), APC(31, 2)}}}},
      {{{{X(1, 0, 32)}}, {{X(1, 0, 30, 32), APC(30, 1), ONES(31, 1)}}, {{X(2, 0, 32)}},
-       {{X(2, 0, 30, 32), APC(30, 2)}}, {{X(3, 0, 32)}}, {{X(3, 0, 30, 32), APC(30, 3)}}}}},
+       {{X(2, 0, 30, 32), APC(30, 2)}}}}},
     // D <= 64: two chunks per piece, offsets in a chunk of their own
-    {64, 7, 7, 13, {0, 1, 6, 2, 3, 0, 1, 4, 5, 0, 1, 2, 3}, {0, 1, 6, 0, 1, 2, 3, 0, 1, 4, 5, 2, 3},
+    {64, 5, 5, 7, 3, {0, 1, 4, 2, 3, 0, 1}, {0, 1, 4, 0, 1, 2, 3},
      {{{{X(1, 0, 32)}}, {{X(1, 0, 32, 32)}}, {{X(2, 0, 32)}}, {{X(2, 0, 32, 32)}},
-       {{X(3, 0, 32)}}, {{X(3, 0, 32, 32)}}, {{ONES(0), AOF(3)}}}},
+       {{ONES(0), AOF(3)}}}},
      {{{{X(1, 0, 32)}}, {{X(1, 0, 32, 32)}}, {{X(2, 0, 32)}}, {{X(2, 0, 32, 32)}},
-       {{X(3, 0, 32)}}, {{X(3, 0, 32, 32)}}, {{AOF(0), ONES(3)}}}}},
+       {{AOF(0), ONES(3)}}}}},
 };
 
 // ------------------------------------------------------------------ recipe check
 //
-// Compile-time proof that every recipe contracts exactly
-//   sum_f sum_{p + q <= 4} x_p[f] b_q[f] + (a_i1 + a_i2 + a_i3) + (a_j1 + a_j2 + a_j3)
-// for all features f < maxd: over the instructions' (column chunk, row chunk)
-// pairs, slot by slot, each such product appears once, features match, and
-// every other pairing has a zero on one side.  Segments may not overlap.
+// Compile-time proof that every recipe contracts
+//   sum_f sum_{p + q <= order} x_p[f] b_q[f] + (a_i1 + a_i2 [+ a_i3]) + (a_j1 + a_j2 [+ a_j3])
+// plus possibly some of the higher products (p + q = 4) and third offset
+// pieces, for all features f < maxd: over the instructions' (column chunk,
+// row chunk) pairs, slot by slot, each wanted product appears exactly once,
+// each optional one at most once, features match, and every other pairing has
+// a zero on one side.  The exact split (order 4) must hold all three offset
+// pieces.  Segments may not overlap.
 
 struct HxSlot {
   int kind = SEG_END, piece = 0, feat = 0;
@@ -184,6 +197,7 @@ constexpr bool hx_valid(const HxRecipe& R) {
   int cnt[64][4][4] = {};
   int ai[4] = {}, aj[4] = {};
   if (R.nm < 1 || R.nm > HX_MFMAS || R.nc > HX_CHUNKS || R.nb > HX_CHUNKS) return false;
+  if (R.order != 3 && R.order != 4) return false;
   for (int m = 0; m < R.nm; ++m) {
     if (R.sa[m] < 0 || R.sa[m] >= R.nc || R.sb[m] < 0 || R.sb[m] >= R.nb) return false;
     for (int slot = 0; slot < 32; ++slot) {
@@ -205,13 +219,16 @@ constexpr bool hx_valid(const HxRecipe& R) {
       }
     }
   }
-  for (int k = 1; k <= 3; ++k)
-    if (ai[k] != 1 || aj[k] != 1) return false;
+  for (int k = 1; k <= 3; ++k) {
+    const bool need = k <= 2 || R.order == 4;
+    if (ai[k] > 1 || aj[k] > 1 || (need && (ai[k] != 1 || aj[k] != 1))) return false;
+  }
   for (int f = 0; f < 64; ++f)
     for (int p = 1; p <= 3; ++p)
       for (int q = 1; q <= 3; ++q) {
-        const int want = (f < R.maxd && p + q <= 4) ? 1 : 0;
-        if (cnt[f][p][q] != want) return false;
+        const bool real = f < R.maxd && p + q <= 4;
+        const bool need = f < R.maxd && p + q <= R.order;
+        if (cnt[f][p][q] > (real ? 1 : 0) || (need && cnt[f][p][q] != 1)) return false;
       }
   return true;
 }
