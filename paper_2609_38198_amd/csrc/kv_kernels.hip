@@ -815,9 +815,12 @@ KVPlan plan_tiles(int64_t Nr, int64_t Nc, int dp, int b, int nib) {
   return p;
 }
 
-// Row tiles per wave of the fused product.  Four was the fastest or tied on
-// every workload shape measured (D in {4, 12, 30, 64}, b in {8 .. 64}).
-int product_nib(int /*dp*/, int /*ncb*/) { return 4; }
+// Row tiles per wave of the fused product.  Eight for one 16-column block at
+// D <= 12 (5% faster than four on the 6-torus, b = 16: two instructions per
+// exponent tile leave room for more independent chains); four everywhere else
+// (the fastest or tied on every other shape measured: D in {4, 12, 30, 64},
+// b in {8 .. 64}; two and eight are 11-17% slower at D = 30, b = 32).
+int product_nib(int dp, int ncb) { return (ncb == 1 && dp <= 12) ? 8 : 4; }
 
 KVPlan plan_product(int64_t Nr, int64_t Nc, int dp, int b) {
   return plan_tiles(Nr, Nc, dp, b, product_nib(dp, int(ceil_div(b, 16))));
@@ -1002,6 +1005,12 @@ template <int DC, int NCB>
 static void product_bf16_launch(const KVPlan& p, const PointPack& rows, const PointPack& cols,
                                 const float* vp, const float* cs, bool diag, const float* sl,
                                 float* Y, int64_t ldy, int b, float* part, hipStream_t stream) {
+  // eight row tiles per wave only for the shapes product_nib gives them to
+  if constexpr (DC == 1 && NCB == 1) {
+    if (p.nib == 8)
+      return product_bf16_nib<DC, NCB, 8>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part,
+                                          stream);
+  }
   FD_REQUIRE(p.nib == 2 || p.nib == 4, FD_ERR_INVALID_ARG, "internal: bf16 rows per wave");
   if (p.nib == 2)
     product_bf16_nib<DC, NCB, 2>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
