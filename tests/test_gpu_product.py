@@ -57,6 +57,33 @@ def test_torus6_full_size_sampled_rows(beta):
     assert rel_fro(Y[rows], ref) <= TOL_F32
 
 
+# Error budget of the short split exponent (D > 4): the dropped piece
+# products are at most 3 * 2^-22 of each |x_jk b_ik|, which at the largest
+# beta log2(e) max ||x||^2 of the workloads (about 70: the tori at beta = 8)
+# stays within a third of the 1e-5 bar.  Measured 3e-7 to 1.2e-6.
+SHORT_SPLIT_BUDGET = 3e-6
+
+
+@pytest.mark.parametrize("which", ["torus6 beta=8", "noisy6 n=65536 beta=8", "molecule n=65536"])
+def test_short_split_error_budget(which):
+    if which.startswith("torus6"):
+        X, beta, b = inputs.torus6().X, 8.0, 16
+    elif which.startswith("noisy6"):
+        X, beta, b = inputs.torus6_noisy(65536).X, 8.0, 32
+    else:
+        w = inputs.molecule(65536)
+        X, beta, b = w.X, w.betas[0], 32
+    N = X.shape[0]
+    V = inputs.random_block(N, b)
+    case(f"short split budget: {which} D={X.shape[1]} b={b}")
+    Y = _run(X, None, beta, V)
+    rows = np.random.default_rng(12).choice(N, 256, replace=False)
+    ref = ok.kernel_matmul(X, None, beta, V, rows=rows, threads=8)
+    err = rel_fro(Y[rows], ref)
+    print(f"{which}: rel err {err:.2e}")
+    assert err <= SHORT_SPLIT_BUDGET
+
+
 @pytest.mark.parametrize("D,b", [(4, 8), (12, 32), (30, 32), (64, 64), (30, 16), (12, 64)])
 def test_shapes_sampled_rows(D, b):
     # every (feature width, block width) family of the kernel at 65,536 points
