@@ -1,28 +1,30 @@
 #!/usr/bin/env python3
 """Benchmark of the diffusion-map hot path on one MI355X.
 
-One step = one pass of the path over the flat 6-torus workload (65,536
-points in R^12, block width 16, bandwidth sweep beta in {0.5, 1, 2, 4, 8},
-alpha = 1/2): for every beta the normalisation vectors (q = K 1,
-d = q^-a K q^-a, s) and one fused normalised product Y = diag(s) K diag(s) V.
-The sweep is a dyadic ladder, so the normalisation runs as one
-fd_degree_dyadic call: q of each beta after the first is the row sum of the
-previous beta's squared kernel, summed in that beta's second pass.
-Inputs are resident in HBM before the timed region.
+One step = one pass of the path over the molecule-like workload (N = 2^20
+points in R^30, float32, block width b = 32, alpha = 1/2, beta = 1 / median
+squared distance of a 4,096-point subsample): the normalisation vectors
+(q = K 1, w = q^-a, d = w (K w), s = w d^-1/2: two passes over the kernel,
+`fd_degree`) and one fused normalised product Y = diag(s) K diag(s) V
+(`fd_kernel_matmul`).  Inputs are resident in HBM before the timed region.
 
 Printed value: whole-step throughput in kernel pair-columns per second,
-sum over the sweep of N^2 * b divided by the step time (the normalisation
-passes are inside the step time).  The roofline object is for the kernel
-with the larger share of the step (the row-sum pass or the fused product),
-timed with HIP events on its launch stream.  Its bound is the transcendental
-rate: every kernel entry costs one v_exp_f32, and the matrix-core work of the
-contractions does not run concurrently with the vector ALUs on gfx950, so the
-exponentials set the floor.  HBM traffic comes from the rocprofv3 counter
-summary under profiles/ when that summary was taken on the current kernel
-sources, else it is null.
+N^2 * b divided by the step time (the normalisation passes are inside the
+step time).  The roofline object is for the fused product, the kernel with
+the larger share of the step, timed with HIP events on its launch stream.
+Its bound is the transcendental rate: every kernel entry costs one
+v_exp_f32, and the matrix-core work of the contractions does not run
+concurrently with the vector ALUs on gfx950, so the exponentials set the
+floor.  HBM traffic comes from the rocprofv3 counter summary under
+profiles/ when that summary was taken on the current kernel sources, else
+it is null.
 
-``--lanczos`` adds the time to the top-16 eigenpairs on the 2-torus
-workload (N = 2048, beta = 8, b = 8) as an extra field.
+Extra fields: `lanczos_top64_s`, the wall time of `fd_block_lanczos` to
+the top 64 eigenpairs on the same workload (both normalisation passes
+included), and `torus6_sweep`, the flat 6-torus sweep (N = 65,536, D = 12,
+b = 16, beta in {0.5, 1, 2, 4, 8}: the dyadic normalisation ladder and one
+normalised product per beta).  Optional legs add other workloads
+(see --help).
 """
 from __future__ import annotations
 
@@ -42,7 +44,13 @@ PEAK_HBM_GBS = 8000.0
 # v_exp_f32 issues a wave64 in 8 cycles (half the plain-VALU rate of 16
 # lanes/cycle): 256 CUs x 4 SIMDs x 8 lanes x 2.4 GHz
 PEAK_EXP_TS = 256 * 4 * 8 * 2.4e9 / 1e12
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_torus6.md")
+PEAK_F16_MFMA_TFS = 2516.6
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_molecule.md")
+TRAFFIC_FILE_TORUS6 = os.path.join(ROOT, "profiles", "hbm_traffic_torus6.md")
+CONTRACTION = ("exponent: float16 matrix instructions over three-piece float16 splits of the "
+               "float32 coordinates (short split for D > 4 within its tested exponent budget, "
+               "exact split otherwise), float32 accumulate; K V: float16 two-term splits of K "
+               "and V, three float16 matrix instructions per 16 columns, float32 accumulate")
 KERNEL_SOURCES = ("hx_kernels.hip", "kv_common.hpp", "kv_kernels.hip")
 
 
@@ -55,10 +63,10 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def recorded_traffic(kernel: str):
-    """HBM bytes per launch of `kernel` from the counter summary, if current."""
+def recorded_traffic(kernel: str, path: str = TRAFFIC_FILE):
+    """HBM bytes per launch of `kernel` from a counter summary, if current."""
     try:
-        with open(TRAFFIC_FILE) as fh:
+        with open(path) as fh:
             text = fh.read()
     except OSError:
         return None
@@ -89,7 +97,7 @@ def cpu_model() -> str:
     return platform.processor() or "unknown"
 
 
-def cpu_baseline(X: np.ndarray, beta: float, b: int, seconds: float) -> dict:
+def cpu_baseline(X: np.ndarray, beta: float, b: int, seconds: float, label: str) -> dict:
     """Time the oracle's product on a bounded sample of rows (float64, CPU)."""
     from oracle import kernel as ok
     from paper_2609_38198_amd import inputs
@@ -98,18 +106,24 @@ def cpu_baseline(X: np.ndarray, beta: float, b: int, seconds: float) -> dict:
     N = X.shape[0]
     V = inputs.random_block(N, b, seed=2)
     rng = np.random.default_rng(0)
-    probe_rows = rng.choice(N, 64 * cores, replace=False)
+    # row blocks of 16 keep a thread's float64 temporaries near 256 MB at
+    # N = 2^20; rounds of one block per thread run until the time is spent
+    blk = 16 if N > (1 << 18) else 64
+    order = rng.permutation(N)
+    per_round = blk * cores
+    nrows = 0
     t0 = time.perf_counter()
-    ok.kernel_matmul(X, None, beta, V, rows=probe_rows, block=64, threads=cores)
-    t_probe = time.perf_counter() - t0
-    nrows = int(min(N, max(64 * cores, len(probe_rows) * seconds / max(t_probe, 1e-3))))
-    rows = rng.choice(N, nrows, replace=False)
-    t0 = time.perf_counter()
-    ok.kernel_matmul(X, None, beta, V, rows=rows, block=64, threads=cores)
+    while nrows + per_round <= N:
+        rows = order[nrows:nrows + per_round]
+        ok.kernel_matmul(X, None, beta, V, rows=rows, block=blk, threads=cores)
+        nrows += per_round
+        if time.perf_counter() - t0 >= seconds:
+            break
     t = time.perf_counter() - t0
     return {"value": nrows * N * b / t, "unit": "pair-cols/s", "cores": cores, "kind": "oracle",
-            "sample": f"float64 difference-form product K V on {nrows} seeded rows x all {N} "
-                      f"columns, b={b}, beta={beta}, {t:.1f} s on {cores} threads of {cpu_model()}"}
+            "sample": f"{label}: float64 difference-form product K V on {nrows} seeded rows x "
+                      f"all {N} columns, b={b}, beta={beta:.5g}, {t:.1f} s on {cores} threads "
+                      f"of {cpu_model()}"}
 
 
 def lanczos_leg(fd, torch, dev) -> dict:
@@ -127,18 +141,15 @@ def lanczos_leg(fd, torch, dev) -> dict:
             "max_residual": e.info["max_residual"]}
 
 
-def molecule_leg(fd, torch, dev) -> dict:
-    """Top-64 eigenpairs at N = 2^20 (molecule-like manifold, D = 30, b = 32)."""
-    from paper_2609_38198_amd import inputs
-    w = inputs.molecule()
-    X = torch.from_numpy(w.X).to(dev)
+def lanczos_top64_leg(fd, torch, w, X) -> dict:
+    """Top-64 eigenpairs of the step's workload (molecule-like, N = 2^20, D = 30, b = 32)."""
     beta = float(w.betas[0])
     torch.cuda.synchronize()
     fd.fd_profile_read(fd.FD_KERNEL_PRODUCT)
     fd.fd_profile_read(fd.FD_KERNEL_ROWSUM)
     fd.fd_profile_enable(True)
+    log(f"top-64 leg: N={w.N} beta={beta:.5f} start")
     t0 = time.perf_counter()
-    log(f"molecule leg: N={w.N} beta={beta:.5f} start")
     e = fd.fd_block_lanczos(X, beta, w.k, w.b, allow_not_converged=True,
                             opts=fd.default_opts(verbose=1))
     torch.cuda.synchronize()
@@ -146,18 +157,58 @@ def molecule_leg(fd, torch, dev) -> dict:
     fd.fd_profile_enable(False)
     pms, pn = fd.fd_profile_read(fd.FD_KERNEL_PRODUCT)
     rms, rn = fd.fd_profile_read(fd.FD_KERNEL_ROWSUM)
-    N, D, b = w.N, w.D, w.b
-    avg = pms * 1e-3 / max(pn, 1)
-    flops = 2.0 * N * N * (D + b)
-    return {"workload": f"molecule-like N={N} D={D} beta={beta:.5f} b={b} k={w.k} alpha=0.5",
-            "seconds": t, "status": e.status, "block_matvecs": e.info["block_matvecs"],
+    log(f"top-64 leg: {t:.3f} s, {e.info['block_matvecs']} block products, "
+        f"{e.info['nconv']}/{w.k} converged")
+    return {"seconds": t, "status": e.status, "block_matvecs": e.info["block_matvecs"],
             "restarts": e.info["restarts"], "nconv": e.info["nconv"],
             "max_residual": e.info["max_residual"], "gap_perron": e.info["gap_perron"],
-            "product_avg_ms": avg * 1e3, "product_tflops": flops / avg / 1e12,
-            "product_texp_per_s": float(N) * N / avg / 1e12,
-            "product_frac_exp_peak": float(N) * N / avg / 1e12 / PEAK_EXP_TS,
-            "product_total_s": pms * 1e-3, "rowsum_total_s": rms * 1e-3,
+            "product_total_s": pms * 1e-3, "product_launches": pn,
+            "rowsum_total_s": rms * 1e-3, "rowsum_launches": rn,
             "evals_head": e.evals[:4], "evals_tail": e.evals[-2:]}
+
+
+def torus6_sweep_leg(fd, torch, dev, steps: int, warmup: int = 2) -> dict:
+    """The flat 6-torus sweep: dyadic normalisation ladder + one normalised product per beta."""
+    from paper_2609_38198_amd import inputs
+    wl = inputs.torus6()
+    N, D, b = wl.N, wl.D, wl.b
+    betas, alpha = wl.betas, wl.alpha
+    X = torch.from_numpy(wl.X).to(dev)
+    V = torch.from_numpy(inputs.random_block(N, b)).to(dev)
+    Y = torch.empty((N, b), dtype=torch.float32, device=dev)
+    ws_p = torch.empty(fd.fd_workspace_size(fd.FD_OP_KERNEL_MATMUL, N, N, D, b),
+                       dtype=torch.uint8, device=dev)
+    ws_d = torch.empty(fd.fd_workspace_size(fd.FD_OP_DEGREE_DYADIC, N, N, D),
+                       dtype=torch.uint8, device=dev)
+    nb = len(betas)
+    # K at 2 beta is K at beta squared entrywise: each level's q comes from
+    # the previous level's second pass
+    assert all(betas[i + 1] == 2.0 * betas[i] for i in range(nb - 1))
+
+    def step():
+        lad = fd.fd_degree_dyadic(X, betas[0], nb, alpha, ws=ws_d)
+        for l, beta in enumerate(betas):
+            fd.fd_kernel_matmul(X, None, beta, V, sl=lad.s[l], sr=lad.s[l], Y=Y, ws=ws_p)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    fd.fd_profile_read(fd.FD_KERNEL_PRODUCT)
+    fd.fd_profile_enable(True)
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    t = (time.perf_counter() - t0) / steps
+    fd.fd_profile_enable(False)
+    pms, pn = fd.fd_profile_read(fd.FD_KERNEL_PRODUCT)
+    avg = pms * 1e-3 / max(pn, 1)
+    return {"workload": f"flat 6-torus N={N} D={D} b={b} beta sweep {list(betas)} "
+                        f"alpha={alpha}", "steps": steps, "ms_per_step": t * 1e3,
+            "pair_cols_per_s": nb * float(N) * N * b / t,
+            "product_avg_ms": avg * 1e3, "product_texp_per_s": float(N) * N / avg / 1e12,
+            "product_frac_exp_peak": float(N) * N / avg / 1e12 / PEAK_EXP_TS,
+            "product_hbm_bytes_per_launch": recorded_traffic("product", TRAFFIC_FILE_TORUS6)}
 
 
 def continuation_leg(fd, torch, dev) -> dict:
@@ -273,12 +324,18 @@ def paper_t6_leg(fd, torch, dev) -> dict:
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
-    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--lanczos", action="store_true")
-    ap.add_argument("--molecule", action="store_true")
+    ap.add_argument("--no-top64", action="store_true",
+                    help="skip the top-64 eigensolve on the step's workload")
+    ap.add_argument("--no-torus6", action="store_true", help="skip the flat 6-torus sweep")
+    ap.add_argument("--only-torus6", action="store_true",
+                    help="run only the flat 6-torus sweep (--steps / --warmup apply to it) and "
+                         "print its record (for the counter runs of its kernels)")
+    ap.add_argument("--lanczos", action="store_true",
+                    help="time to the top 16 eigenpairs on the 2-torus (N = 2048)")
     ap.add_argument("--continuation", action="store_true")
     ap.add_argument("--stress", action="store_true")
     ap.add_argument("--paper-t6", action="store_true",
@@ -300,26 +357,31 @@ def main() -> int:
     from paper_2609_38198_amd import inputs
 
     dev = torch.device("cuda:0")
-    wl = inputs.torus6()
+    if args.only_torus6:
+        rec = {"torus6_sweep": torus6_sweep_leg(fd, torch, dev, args.steps, args.warmup)}
+        if args.calibration_copy > 0:
+            src = torch.ones(args.calibration_copy << 18, dtype=torch.float32, device=dev)
+            dst = torch.empty_like(src)
+            dst.copy_(src)
+            torch.cuda.synchronize()
+            rec["calibration_copy_bytes"] = 2 * src.numel() * 4
+        print(json.dumps(rec), flush=True)
+        return 0
+    log("generating the molecule-like workload (N = 2^20, D = 30)")
+    wl = inputs.molecule()
     N, D, b = wl.N, wl.D, wl.b
-    betas = wl.betas
-    alpha = wl.alpha
+    beta, alpha = float(wl.betas[0]), wl.alpha
     X = torch.from_numpy(wl.X).to(dev)
     V = torch.from_numpy(inputs.random_block(N, b)).to(dev)
     Y = torch.empty((N, b), dtype=torch.float32, device=dev)
     ws_p = torch.empty(fd.fd_workspace_size(fd.FD_OP_KERNEL_MATMUL, N, N, D, b),
                        dtype=torch.uint8, device=dev)
-    ws_d = torch.empty(fd.fd_workspace_size(fd.FD_OP_DEGREE_DYADIC, N, N, D),
+    ws_d = torch.empty(fd.fd_workspace_size(fd.FD_OP_DEGREE, N, N, D),
                        dtype=torch.uint8, device=dev)
-    nb = len(betas)
-    # the sweep is a dyadic ladder: K at 2 beta is K at beta squared entrywise,
-    # so each level's degree q comes from the previous level's second pass
-    assert all(betas[i + 1] == 2.0 * betas[i] for i in range(nb - 1))
 
     def step():
-        lad = fd.fd_degree_dyadic(X, betas[0], nb, alpha, ws=ws_d)
-        for l, beta in enumerate(betas):
-            fd.fd_kernel_matmul(X, None, beta, V, sl=lad.s[l], sr=lad.s[l], Y=Y, ws=ws_p)
+        deg = fd.fd_degree(X, beta, alpha, ws=ws_d)
+        fd.fd_kernel_matmul(X, None, beta, V, sl=deg.s, sr=deg.s, Y=Y, ws=ws_p)
 
     for _ in range(args.warmup):
         step()
@@ -327,6 +389,7 @@ def main() -> int:
     fd.fd_profile_read(fd.FD_KERNEL_PRODUCT)
     fd.fd_profile_read(fd.FD_KERNEL_ROWSUM)
     fd.fd_profile_enable(True)
+    log(f"timing {args.steps} steps")
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
@@ -338,22 +401,18 @@ def main() -> int:
     row_ms, row_n = fd.fd_profile_read(fd.FD_KERNEL_ROWSUM)
 
     ms_per_step = (t1 - t0) * 1e3 / args.steps
-    pair_cols = len(betas) * float(N) * N * b
-    value = pair_cols / (ms_per_step * 1e-3)
+    value = float(N) * N * b / (ms_per_step * 1e-3)
     avg_prod_s = prod_ms * 1e-3 / max(prod_n, 1)
-    flops = 2.0 * N * N * (D + b)
     avg_row_s = row_ms * 1e-3 / max(row_n, 1)
-    # algorithmic exponentials: one per kernel entry of each kernel application
-    # the definition makes.  The product applies K once per launch.  The row
-    # sums make the 2 normalisation applications of every bandwidth (q = K 1
-    # and K w) in 1 + nb launches per step (the squared sums of a weighted
-    # launch are the next bandwidth's q), so their rate is taken over the
-    # kernel's whole time in the step.
+    # algorithmic work of one product launch: N^2 kernel entries (one
+    # exponential each) and 2 N^2 (D + b) flops of the two contractions
     exp_prod = float(N) * N / avg_prod_s / 1e12
-    row_apps = 2.0 * nb * args.steps
-    exp_row = row_apps * float(N) * N / (row_ms * 1e-3) / 1e12
-    dominant = "rowsum" if row_ms >= prod_ms else "product"
-    achieved = exp_row if dominant == "rowsum" else exp_prod
+    flops = 2.0 * N * N * (D + b)
+    # the row sums make the two normalisation applications (q = K 1, K w) in
+    # two launches per step
+    exp_row = float(N) * N / avg_row_s / 1e12
+    log(f"step {ms_per_step:.1f} ms: product {avg_prod_s * 1e3:.1f} ms, "
+        f"row-sum pass {avg_row_s * 1e3:.1f} ms")
 
     rec = {
         "metric": "fused K*V pair-cols/sec (N^2*b per sec)",
@@ -367,31 +426,31 @@ def main() -> int:
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "f32",
+        "contraction": CONTRACTION,
         "data": "synthetic",
-        "config": {"workload": f"flat 6-torus N={N} D={D} b={b} beta sweep {list(betas)} "
-                               f"alpha={alpha}: per beta the normalisation vectors (q = K 1 "
-                               f"from the previous beta's squared kernel sums) + 1 fused "
-                               f"normalised product", "N": N, "D": D, "b": b,
-                   "betas": list(betas), "alpha": alpha, "parallelism": "single GPU"},
-        "roofline": {"bound": "alu", "kernel": dominant, "achieved": achieved,
-                     "peak": PEAK_EXP_TS, "unit": "Texp/s", "frac": achieved / PEAK_EXP_TS,
-                     "traffic": recorded_traffic(dominant)},
+        "config": {"workload": f"molecule-like manifold N={N} D={D} b={b} beta={beta:.5f} "
+                               f"alpha={alpha}: normalisation vectors (2 passes) + 1 fused "
+                               f"normalised product diag(s) K diag(s) V", "N": N, "D": D,
+                   "b": b, "beta": beta, "alpha": alpha, "parallelism": "single GPU"},
+        "roofline": {"bound": "alu", "kernel": "product", "achieved": exp_prod,
+                     "peak": PEAK_EXP_TS, "unit": "Texp/s", "frac": exp_prod / PEAK_EXP_TS,
+                     "traffic": recorded_traffic("product")},
+        "roofline_mfma_f16": {"kernel": "product", "achieved": flops / avg_prod_s / 1e12,
+                              "peak": PEAK_F16_MFMA_TFS, "unit": "TFLOP/s",
+                              "frac": flops / avg_prod_s / 1e12 / PEAK_F16_MFMA_TFS,
+                              "flops_per_launch": flops},
         "kernels": {
             "product": {"launches": prod_n, "avg_ms": avg_prod_s * 1e3,
-                        "step_ms": prod_ms / args.steps,
                         "pair_cols_per_s": float(N) * N * b / avg_prod_s,
                         "texp_per_s": exp_prod, "frac_exp_peak": exp_prod / PEAK_EXP_TS,
                         "contraction_tflops": flops / avg_prod_s / 1e12,
                         "hbm_bytes_per_launch": recorded_traffic("product")},
             "rowsum": {"launches": row_n, "avg_ms": avg_row_s * 1e3,
-                       "step_ms": row_ms / args.steps,
-                       "normalisation_applications": row_apps,
                        "texp_per_s": exp_row, "frac_exp_peak": exp_row / PEAK_EXP_TS,
-                       "contraction_tflops": row_apps * 2.0 * N * N * D / (row_ms * 1e-3)
-                       / 1e12,
                        "hbm_bytes_per_launch": recorded_traffic("rowsum")},
         },
     }
+    del ws_p, ws_d, Y, V
     if args.calibration_copy > 0:
         src = torch.ones(args.calibration_copy << 18, dtype=torch.float32, device=dev)
         dst = torch.empty_like(src)
@@ -399,10 +458,17 @@ def main() -> int:
         torch.cuda.synchronize()
         rec["calibration_copy_bytes"] = 2 * src.numel() * 4
         del src, dst
+    if not args.no_top64:
+        top = lanczos_top64_leg(fd, torch, wl, X)
+        rec["lanczos_top64_s"] = top["seconds"]
+        rec["lanczos_top64"] = top
+    if not args.no_torus6:
+        log("flat 6-torus sweep")
+        rec["torus6_sweep"] = torus6_sweep_leg(fd, torch, dev, 10)
+    del X
+    torch.cuda.empty_cache()
     if args.lanczos:
         rec["lanczos"] = lanczos_leg(fd, torch, dev)
-    if args.molecule:
-        rec["lanczos_molecule"] = molecule_leg(fd, torch, dev)
     if args.continuation:
         rec["continuation"] = continuation_leg(fd, torch, dev)
     if args.stress:
@@ -410,7 +476,9 @@ def main() -> int:
     if args.paper_t6:
         rec["paper_t6"] = paper_t6_leg(fd, torch, dev)
     if not args.no_cpu_baseline:
-        rec["cpu_baseline"] = cpu_baseline(wl.X, 2.0, b, args.cpu_seconds)
+        log("CPU oracle baseline")
+        rec["cpu_baseline"] = cpu_baseline(wl.X, beta, b, args.cpu_seconds,
+                                           "molecule-like N=2^20 D=30")
     print(json.dumps(rec), flush=True)
     return 0
 

@@ -48,6 +48,49 @@ def test_n_eff_counts_equal_interactions(k):
     assert bf.n_eff(s1, s2, N) == pytest.approx(k, rel=1e-12)
 
 
+def simplex_clusters(k, h, groups=40):
+    """Groups of k + 1 points at the vertices of a regular simplex of edge h
+    (scaled unit vectors of R^(k+1)), group centres 100 apart on a line."""
+    centres = np.zeros((groups, k + 1))
+    centres[:, 0] = 100.0 * np.arange(groups)
+    verts = np.eye(k + 1) * (h / math.sqrt(2.0))
+    return (centres[:, None, :] + verts[None, :, :]).reshape(-1, k + 1)
+
+
+@pytest.mark.parametrize("k", [1, 3, 7])
+def test_n_eff_orientation_on_equidistant_neighbours(k):
+    # every row has k neighbours at squared distance h^2 and nothing else in
+    # reach: S_off(beta) = N k exp(-beta h^2), S_off(2 beta) = N k
+    # exp(-2 beta h^2), and n_eff = k at any beta (text after eq. neff).  The
+    # arguments taken the other way round give k exp(-3 beta h^2).
+    h2, beta = 2.0, 0.5
+    X = simplex_clusters(k, math.sqrt(h2))
+    N = X.shape[0]
+    s1 = on.normalise(X, beta, 0.5).s_off
+    s2 = on.normalise(X, 2 * beta, 0.5).s_off
+    assert s1 == pytest.approx(N * k * math.exp(-beta * h2), rel=1e-10)
+    assert s2 == pytest.approx(N * k * math.exp(-2 * beta * h2), rel=1e-10)
+    assert bf.n_eff(s1, s2, N) == pytest.approx(k, rel=1e-10)
+    assert abs(bf.n_eff(s2, s1, N) - k) > 0.5 * k
+
+
+@pytest.mark.parametrize("counts", [(256, 256), (512, 256)])
+def test_n_eff_heat_regime_closed_form(counts):
+    # flat grid torus of unit circles in the heat regime (kernel much wider
+    # than the grid spacing, much narrower than the circles): the row sums
+    # are a Riemann sum of a Gaussian, q - 1 ~ rho (pi / beta)^(d/2) with
+    # rho = N / (2 pi)^d, so n_eff ~ rho (2 pi / beta)^(d/2) = N beta^(-d/2)
+    # (2 pi)^(-d/2).  The circulant closed form gives q exactly.  The
+    # swapped orientation is 2^(3d/2) = 8 times smaller at d = 2.
+    d, beta = 2, 20.0
+    N = int(np.prod(counts))
+    s1 = N * (tg.degree(counts, beta) - 1.0)
+    s2 = N * (tg.degree(counts, 2 * beta) - 1.0)
+    want = N / (2 * np.pi) ** d * (2 * np.pi / beta) ** (d / 2)
+    assert bf.n_eff(s1, s2, N) == pytest.approx(want, rel=0.02)
+    assert bf.n_eff(s2, s1, N) < want / 4
+
+
 def test_v_stat_definition():
     assert bf.v_stat(25.0, 4.0) == pytest.approx(0.1, rel=1e-15)
 
@@ -79,6 +122,22 @@ def _mock(vb, soff, gaps, beta0=0.1):
         ev = np.array([1.0, 1.0 - gaps[i], math.exp(-vb[i]), math.exp(-vb[i])])
         return bf.make_probe(beta, ev, soff[i])
     return probe
+
+
+def test_flow_probes_carry_n_eff_of_equidistant_neighbours():
+    # the flow's own bookkeeping (each probe completed by the next dyadic
+    # probe) must give n_eff = k on every complete probe when S_off follows
+    # the equidistant-neighbour law N k exp(-beta h^2) of the simplex set
+    # (that set itself is disconnected, so its Perron gap is 0: the probes
+    # take an admissible mocked spectrum and this S_off)
+    k, h2, N = 3, 1.0, 120
+    vb = [4.0, 2.0, 1.0, 0.5]
+    soff = [N * k * math.exp(-0.1 * 2 ** i * h2) for i in range(4)]
+    F = bf.flow(_mock(vb, soff, [0.5] * 4), N, 0.1, max_probes=4)
+    done = [p for p in F.probes if p.n_eff is not None]
+    assert len(done) == 3
+    for p in done:
+        assert p.n_eff == pytest.approx(k, rel=1e-12)
 
 
 def test_flow_brackets_known_minimum():
