@@ -83,7 +83,8 @@ typedef struct fd_lanczos_info {
   int32_t restarts;         /* restart cycles run */
   int32_t block_matvecs;    /* applications of M to a block of b vectors */
   int32_t nconv;            /* leading Ritz pairs with residual <= tol */
-  int32_t wall;             /* 1 when g_P <= kappa_P * eta_fp32 (Sec. 2.3, eq. perronwall) */
+  int32_t wall;             /* 1 when g_P <= kappa_P * eta, kappa_P = 10 and eta of X's dtype
+                               (fp32 1e-7, bf16 8e-3) (Sec. 2.3, eq. perronwall and its footnote) */
   double gap_perron;        /* g_P = (theta_0 - theta_1) / |theta_0| */
   double s_off;             /* S_off = sum_{i != j} K_ij = sum(q) - N (Sec. 2.3) */
   double max_residual;      /* largest residual among the k returned pairs */
@@ -192,7 +193,7 @@ fd_status fd_block_lanczos(const void* X, fd_dtype xt, int64_t N, int64_t D, int
  *   eigenvectors (same layout) or NULL.
  *   per_step: nsteps reports (host) or NULL.
  *   stop_at_wall: when non-zero, stop after the first step whose Perron gap is at or
- *   below kappa_P * eta_fp32 and return FD_ERR_PERRON_WALL; evals of the steps run
+ *   below kappa_P * eta (eta of X's dtype, as in info->wall) and return FD_ERR_PERRON_WALL; evals of the steps run
  *   so far are valid and *steps_done tells how many ran.
  *   steps_done: host int64 or NULL. */
 fd_status fd_continuation(const void* X, fd_dtype xt, int64_t N, int64_t D, int64_t ldx,

@@ -29,7 +29,11 @@
 namespace fd {
 
 constexpr double KAPPA_P = 10.0;   // safety factor of the Perron wall (eq. perronwall)
-constexpr double ETA_FP32 = 1e-7;  // precision scale of float32 kernels
+constexpr double ETA_FP32 = 1e-7;  // precision scale of float32 kernel data
+constexpr double ETA_BF16 = 8e-3;  // precision scale of bfloat16 kernel data
+
+// eta of the data type the kernel is evaluated from (footnote to eq. perronwall)
+static double eta_of(fd_dtype xt) { return xt == FD_BF16 ? ETA_BF16 : ETA_FP32; }
 
 struct SolverLayout {
   int b = 0, k = 0, keep = 0, kk = 0, mm = 0;
@@ -313,7 +317,7 @@ static SolveResult lanczos_solve(SolverWs& w, Lanczos& L, const SolverLayout& la
 }
 
 static void fill_info(fd_lanczos_info* info, const SolveResult& R, double s_off, double secs,
-                      int k) {
+                      int k, double eta) {
   if (info == nullptr) return;
   info->restarts = R.restarts;
   info->block_matvecs = R.matvecs;
@@ -321,7 +325,7 @@ static void fill_info(fd_lanczos_info* info, const SolveResult& R, double s_off,
   double gap = 0.0;
   if (R.theta.size() >= 2 && R.theta[0] != 0.0) gap = (R.theta[0] - R.theta[1]) / std::fabs(R.theta[0]);
   info->gap_perron = gap;
-  info->wall = gap <= KAPPA_P * ETA_FP32 ? 1 : 0;
+  info->wall = gap <= KAPPA_P * eta ? 1 : 0;
   info->s_off = s_off;
   double mx = 0.0;
   for (int i = 0; i < k && i < int(R.res.size()); ++i) mx = std::max(mx, R.res[i]);
@@ -382,8 +386,14 @@ __global__ void nystrom_finish_kernel(const float* __restrict__ num, int ldn,
 }
 
 // Extend Markov vectors psi (n_old x k, ld k) of the step solved at beta on the
-// prefix n_old to the prefix n_new (formula of the oracle's Nystrom module):
-// one row-sum pass for the denominators and ceil(k / 64) fused products.
+// prefix n_old to the prefix n_new by the Nystrom extension the paper uses to
+// warm-start a larger nested sample (Sec. 1, last paragraph; Sec. 2.3, dyadic
+// continuation).  The paper names the extension without a formula; the one
+// here is the eigen-relation P psi = lambda psi evaluated at a new point:
+//   psi(x) = (1 / lambda) sum_j K(x, x_j) w_j psi_j / sum_j K(x, x_j) w_j,
+// w = q^-alpha of the old sample (the new point's own q^-alpha cancels).
+// One row-sum pass gives the denominators, ceil(k / 64) fused products the
+// numerators.
 static void nystrom_extend(ContWs& c, const void* X, fd_dtype xt, int64_t D, int64_t ldx,
                            int64_t n_old, int64_t n_new, double beta, double alpha,
                            const float* psi, const float* q_old, const std::vector<double>& lam,
@@ -787,7 +797,7 @@ fd_status fd_block_lanczos(const void* X, fd_dtype xt, int64_t N, int64_t D, int
         for (int i = 0; i < k; ++i) residuals[i] = i < int(R.res.size()) ? R.res[i] : 0.0;
       const double secs =
           std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
-      fill_info(info, R, s_off, secs, int(k));
+      fill_info(info, R, s_off, secs, int(k), eta_of(xt));
       if (!R.converged) {
         set_error("block Lanczos stopped before all k pairs converged (" +
                   std::to_string(R.nconv) + " of " + std::to_string(k) + ")");
@@ -903,7 +913,7 @@ fd_status fd_continuation(const void* X, fd_dtype xt, int64_t N, int64_t D, int6
       const double secs =
           std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
       fd_lanczos_info info{};
-      fill_info(&info, R, s_off, secs, kk);
+      fill_info(&info, R, s_off, secs, kk, eta_of(xt));
       if (per_step != nullptr) per_step[t] = info;
       any_unconverged = any_unconverged || !R.converged;
       level_beta.push_back(beta_steps[t]);
@@ -973,7 +983,7 @@ fd_status fd_beta_flow(const void* X, fd_dtype xt, int64_t N, int64_t D, int64_t
                FD_ERR_INVALID_ARG, "kappa and p must be finite and > 0");
     FD_REQUIRE(std::isfinite(fo.beta_start) && std::isfinite(fo.eta), FD_ERR_INVALID_ARG,
                "beta_start and eta must be finite");
-    FlowParams fp{fo.eta > 0.0 ? fo.eta : (xt == FD_BF16 ? 8e-3 : 1e-7), fo.kappa, fo.p};
+    FlowParams fp{fo.eta > 0.0 ? fo.eta : eta_of(xt), fo.kappa, fo.p};
     fd_lanczos_opts o;
     fd_lanczos_default_opts(&o);
     if (opts != nullptr) o = *opts;
@@ -1080,7 +1090,7 @@ fd_status fd_beta_flow_cascade(const void* const* Xs, const fd_dtype* xts, const
     for (int l = 0; l < nlevels; ++l) {
       const void* X = Xs[l];
       const fd_dtype xt = xts[l];
-      const FlowParams fp{fo.eta > 0.0 ? fo.eta : (xt == FD_BF16 ? 8e-3 : 1e-7), fo.kappa, fo.p};
+      const FlowParams fp{fo.eta > 0.0 ? fo.eta : eta_of(xt), fo.kappa, fo.p};
       // level 0 starts from beta_0 (or beta_start); every later level from
       // the previous level's achieved bandwidth and Markov vectors
       if (l == 0 && beta <= 0.0) beta = flow_beta0(f, X, xt, N, D, ldxs[l], st);
