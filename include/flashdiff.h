@@ -126,6 +126,27 @@ fd_status fd_kernel_matmul(const void* Xr, int64_t Nr, const void* Xc, int64_t N
                            const float* V, int64_t b, int64_t ldv, float* Y, int64_t ldy,
                            void* ws, size_t ws_bytes, void* stream);
 
+/* Allocation-free variant of fd_kernel_matmul, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  Same arguments and result as
+ * fd_kernel_matmul (the same kernels, bit for bit), without the workspace: the
+ * temporaries live in a scratch array built into the library,
+ * fd_kernel_matmul_noalloc_limit() bytes (256 MiB) per device, which each
+ * device holds from the library's load until the process ends.  A problem
+ * whose temporaries do not fit returns FD_ERR_WORKSPACE (for example, b = 16
+ * fits up to about 2^18 points with D <= 12).  The call allocates nothing.
+ * Every call on one device shares that device's scratch, and a call only
+ * relies on what it writes there itself: calls that overlap in time on one
+ * device (several streams or threads) race and give wrong results, so
+ * serialise them.  Asynchronous on `stream`, like fd_kernel_matmul. */
+fd_status fd_kernel_matmul_noalloc(const void* Xr, int64_t Nr, const void* Xc, int64_t Nc,
+                                   int64_t D, int64_t ldx, fd_dtype xt, float beta,
+                                   const float* sl, const float* sr, const float* V, int64_t b,
+                                   int64_t ldv, float* Y, int64_t ldy, void* stream);
+
+/* Bytes of the built-in scratch of fd_kernel_matmul_noalloc. */
+size_t fd_kernel_matmul_noalloc_limit(void);
+
 /* Normalisation passes (Sec. 2.1, the two "entry fee" applications):
  *     q = K 1;  w = q^-alpha;  d = w * (K w);  s = w * d^-1/2,
  * so that M = diag(s) K diag(s) and P = diag(d)^-1 diag(w) K diag(w).

@@ -36,7 +36,8 @@ EXPORTS = (
     "fd_lanczos_default_opts", "fd_workspace_size", "fd_kernel_matmul", "fd_degree",
     "fd_block_lanczos", "fd_continuation", "fd_last_error", "fd_status_string",
     "fd_profile_enable", "fd_profile_read", "fd_flow_default_opts", "fd_beta_flow",
-    "fd_beta_flow_cascade", "fd_degree_dyadic",
+    "fd_beta_flow_cascade", "fd_degree_dyadic", "fd_kernel_matmul_noalloc",
+    "fd_kernel_matmul_noalloc_limit",
 )
 FD_KERNEL_PRODUCT, FD_KERNEL_ROWSUM = 0, 1
 
@@ -108,6 +109,12 @@ def load(path: str = LIB_PATH):
                                      ctypes.c_float, _c_p, _c_p, _c_p, _c_i64, _c_i64, _c_p,
                                      _c_i64, _c_p, ctypes.c_size_t, _c_p]
     lib.fd_kernel_matmul.restype = ctypes.c_int
+    lib.fd_kernel_matmul_noalloc.argtypes = [_c_p, _c_i64, _c_p, _c_i64, _c_i64, _c_i64,
+                                             ctypes.c_int, ctypes.c_float, _c_p, _c_p, _c_p,
+                                             _c_i64, _c_i64, _c_p, _c_i64, _c_p]
+    lib.fd_kernel_matmul_noalloc.restype = ctypes.c_int
+    lib.fd_kernel_matmul_noalloc_limit.argtypes = []
+    lib.fd_kernel_matmul_noalloc_limit.restype = ctypes.c_size_t
     lib.fd_degree.argtypes = [_c_p, ctypes.c_int, _c_i64, _c_i64, _c_i64, ctypes.c_float,
                               ctypes.c_float, _c_p, _c_p, _c_p, _c_p, _c_p, ctypes.c_size_t, _c_p]
     lib.fd_degree.restype = ctypes.c_int
@@ -251,6 +258,42 @@ def fd_kernel_matmul(Xr: torch.Tensor, Xc: Optional[torch.Tensor], beta: float, 
                                 _ptr(Y2), Y2.stride(0), _ptr(ws), ws.numel(),
                                 _stream(Xr.device)))
     return Y
+
+
+def fd_kernel_matmul_noalloc(Xr: torch.Tensor, Xc: Optional[torch.Tensor], beta: float,
+                             V: torch.Tensor, Y: torch.Tensor,
+                             sl: Optional[torch.Tensor] = None,
+                             sr: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """fd_kernel_matmul into a caller-provided Y, using the library's built-in
+    scratch instead of a workspace (the call allocates nothing)."""
+    lib = load()
+    if Xc is None:
+        Xc = Xr
+    _check_dev(Xr, Xc, V, sl, sr, Y)
+    if Xr.dim() != 2 or Xc.dim() != 2 or Xr.shape[1] != Xc.shape[1]:
+        raise ValueError("Xr and Xc must be N x D with the same D")
+    if Xr.stride(1) != 1 or Xc.stride(1) != 1 or Xr.stride(0) != Xc.stride(0):
+        raise ValueError("Xr and Xc must be row-major with the same leading dimension")
+    if V.dim() != 2 or Y.dim() != 2 or V.stride(1) != 1 or Y.stride(1) != 1:
+        raise ValueError("V and Y must be row-major N x b")
+    if V.dtype != torch.float32 or Y.dtype != torch.float32:
+        raise ValueError("V and Y must be float32")
+    Nr, D = Xr.shape
+    Nc, b = Xc.shape[0], V.shape[1]
+    if V.shape[0] != Nc or Y.shape[0] != Nr or Y.shape[1] != b:
+        raise ValueError("V must be Nc x b and Y Nr x b")
+    for t, n in ((sl, Nr), (sr, Nc)):
+        if t is not None and (t.dtype != torch.float32 or t.numel() != n or not t.is_contiguous()):
+            raise ValueError("sl / sr must be contiguous float32 vectors of matching length")
+    _check(lib.fd_kernel_matmul_noalloc(_ptr(Xr), Nr, _ptr(Xc), Nc, D, Xr.stride(0),
+                                        _dtype_code(Xr), float(beta), _ptr(sl), _ptr(sr),
+                                        _ptr(V), b, V.stride(0), _ptr(Y), Y.stride(0),
+                                        _stream(Xr.device)))
+    return Y
+
+
+def fd_kernel_matmul_noalloc_limit() -> int:
+    return int(load().fd_kernel_matmul_noalloc_limit())
 
 
 @dataclass

@@ -4,7 +4,9 @@
 #include <cfloat>
 #include <cmath>
 #include <exception>
+#include <mutex>
 #include <string>
+#include <vector>
 
 #include "fd_internal.hpp"
 #include "fd_solver.hpp"
@@ -68,6 +70,52 @@ ProductWs carve_product(Arena& a, int64_t Nr, int64_t Nc, int64_t D, int b) {
   w.part = a.fspan(part_rows_bound(w.rows.npad, Nc) * w.plan.ncb * 16);
   w.tmp = a.fspan(size_t(Nr));
   return w;
+}
+
+// The same regions sized for exactly the plan the call will run (the bound
+// above covers every plan up to the given sizes).
+static ProductWs carve_product_exact(Arena& a, int64_t Nr, int64_t Nc, int64_t D, int b) {
+  ProductWs w;
+  const int dp = padded_dim(D);
+  w.plan = plan_product(Nr, Nc, dp, b);
+  w.rows = carve_pack(a, Nr, dp, ROW_PAD);
+  w.cols = carve_pack(a, Nc, dp, COL_PAD);
+  w.vp = a.fspan(size_t(w.cols.npad) * w.plan.ncb * 16);
+  w.vscale = a.fspan(128);
+  const KVPlan rp = plan_rowsum(Nr, Nc, dp);
+  const size_t part_prod = size_t(w.plan.nsplit) * w.rows.npad * w.plan.ncb * 16;
+  const size_t part_row = size_t(rp.nsplit) * w.rows.npad;
+  w.part = a.fspan(b == 1 ? part_row : part_prod);
+  w.tmp = a.fspan(size_t(Nr));
+  return w;
+}
+
+// Scratch of the allocation-free product: one array per device, held until
+// the process ends.  Host code never passes the array's name to a kernel or a
+// copy (on the host it is a stand-in, not a device address); it uses the
+// device address that hipGetSymbolAddress returns, looked up once per device
+// with that device current.
+constexpr size_t SCRATCH_BYTES = size_t(256) << 20;
+static __device__ __align__(256) unsigned char scratch[SCRATCH_BYTES];
+
+static char* scratch_on_current_device() {
+  static std::mutex mu;
+  static std::vector<char*> ptrs;
+  int dev = -1;
+  FD_HIP_CHECK(hipGetDevice(&dev));
+  FD_REQUIRE(dev >= 0, FD_ERR_HIP, "no current device");
+  std::lock_guard<std::mutex> lock(mu);
+  if (size_t(dev) >= ptrs.size()) ptrs.resize(size_t(dev) + 1, nullptr);
+  if (ptrs[size_t(dev)] == nullptr) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    FD_REQUIRE(e == hipSuccess && p != nullptr, FD_ERR_HIP,
+               std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(e));
+    FD_REQUIRE((reinterpret_cast<uintptr_t>(p) & 255) == 0, FD_ERR_HIP,
+               "scratch array is not 256-byte aligned");
+    ptrs[size_t(dev)] = static_cast<char*>(p);
+  }
+  return ptrs[size_t(dev)];
 }
 
 // Every plan has nsplit <= max(ceil(2048 / row blocks), ceil(column tiles /
@@ -333,6 +381,38 @@ fd_status fd_kernel_matmul(const void* Xr, int64_t Nr, const void* Xc, int64_t N
     product_apply(w, sl, sr, V, ldv, int(b), Y, ldy, diag, st);
   });
 }
+
+fd_status fd_kernel_matmul_noalloc(const void* Xr, int64_t Nr, const void* Xc, int64_t Nc,
+                                   int64_t D, int64_t ldx, fd_dtype xt, float beta,
+                                   const float* sl, const float* sr, const float* V, int64_t b,
+                                   int64_t ldv, float* Y, int64_t ldy, void* stream) {
+  return guarded([&] {
+    check_points(Xr, xt, Nr, D, ldx, "Xr");
+    check_points(Xc, xt, Nc, D, ldx, "Xc");
+    FD_REQUIRE(std::isfinite(beta) && beta >= 0.f, FD_ERR_INVALID_ARG, "beta must be finite and >= 0");
+    FD_REQUIRE(V != nullptr && Y != nullptr, FD_ERR_INVALID_ARG, "V and Y must not be NULL");
+    FD_REQUIRE(b >= 1 && b <= MAX_B, FD_ERR_INVALID_ARG, "b must be in [1, 64]");
+    FD_REQUIRE(ldv >= b && ldy >= b, FD_ERR_INVALID_ARG, "ldv and ldy must be >= b");
+    Arena m;
+    m.measuring = true;
+    carve_product_exact(m, Nr, Nc, D, int(b));
+    FD_REQUIRE(m.used <= SCRATCH_BYTES, FD_ERR_WORKSPACE,
+               "problem too large for the built-in scratch: needs " + std::to_string(m.used) +
+                   " bytes, the scratch holds " + std::to_string(SCRATCH_BYTES) +
+                   " (use fd_kernel_matmul with a workspace)");
+    Arena a;
+    a.base = scratch_on_current_device();
+    a.cap = SCRATCH_BYTES;
+    ProductWs w = carve_product_exact(a, Nr, Nc, D, int(b));
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    launch_pack_points(Xr, xt, Nr, D, ldx, beta, true, w.rows, st);
+    launch_pack_points(Xc, xt, Nc, D, ldx, beta, false, w.cols, st);
+    const bool diag = (Xr == Xc);
+    product_apply(w, sl, sr, V, ldv, int(b), Y, ldy, diag, st);
+  });
+}
+
+size_t fd_kernel_matmul_noalloc_limit(void) { return SCRATCH_BYTES; }
 
 fd_status fd_degree(const void* X, fd_dtype xt, int64_t N, int64_t D, int64_t ldx, float beta,
                     float alpha, float* q, float* d, float* s, double* s_off, void* ws,
