@@ -224,17 +224,15 @@ def continuation_leg(fd, torch, dev) -> dict:
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     log("continuation leg: start")
-    # the high-beta steps have the top-64 eigenvalues within 1e-2 of 1: a basis
-    # of 12 blocks (384 columns) converges in fewer products than the default
-    # 6, and the product cap keeps the steps at the precision wall (which never
-    # converge) at the cost the default restart cap gives them
-    opts = fd.default_opts(verbose=1, max_basis_blocks=12, max_matvecs=606)
+    # default options: the steps at the Perron wall stop there and are
+    # reported (wall = 1), every other step converges all 64 pairs
+    opts = fd.default_opts(verbose=1)
     lad = fd.fd_continuation(X, ns, bs, w.k, w.b, allow=(0, 5), opts=opts)
     torch.cuda.synchronize()
     t = time.perf_counter() - t0
     return {"workload": "noisy 6-torus N=262144 D=12 k=64 b=32, n in {16384, 65536, 262144} x "
-                        "beta in {0.5, 1, 2, 4, 8}; basis 12 blocks, at most 606 block "
-                        "products per step", "seconds": t, "status": lad.status,
+                        "beta in {0.5, 1, 2, 4, 8}; default options", "seconds": t,
+            "status": lad.status,
             "steps": [{"n": n, "beta": beta, "matvecs": i["block_matvecs"], "nconv": i["nconv"],
                        "gap": i["gap_perron"], "wall": i["wall"], "s": i["seconds"]}
                       for n, beta, i in zip(ns, bs, lad.info)]}
@@ -321,6 +319,82 @@ def paper_t6_leg(fd, torch, dev) -> dict:
                         "seed 42, unnormalised K V", "rows": rows}
 
 
+# The paper's one-GPU T^6 runs (Sec. 3, the data of figure t6scaling: fp32,
+# k = 3 nontrivial modes, alpha = 1/2, one RTX PRO 6000): N -> (mean wall time
+# s, its std, beta_x, its std, overlap score of the leading doublet).  Context
+# only: other hardware, and the paper's timings include its own solver stack.
+PAPER_T6_ONE_GPU = {
+    1024: (6.0325, 4.5185, 0.36936, 0.03992, 0.92903),
+    2048: (5.8926, 4.3790, 0.42356, 0.06325, 0.96819),
+    4096: (5.8238, 4.4080, 0.49509, 0.08424, 0.98477),
+    8192: (5.9655, 4.4799, 0.58220, 0.10710, 0.98515),
+    16384: (6.3727, 4.9327, 0.68935, 0.13137, 0.99437),
+    32768: (11.5528, 9.5942, 0.80013, 0.18802, 0.99428),
+    65536: (15.9784, 10.9733, 0.91729, 0.27512, 0.99720),
+    131072: (61.5799, 7.1353, 0.70902, 0.0, 0.99918),
+    262144: (147.8957, 2.1209, 0.78405, 0.0, 0.99954),
+    524288: (464.2531, 2.5314, 0.87415, 0.0, 0.99968),
+    1048576: (2225.0375, 3.8461, 0.97949, 0.0, 0.99980),
+}
+
+
+def doublet_overlap(psi2: np.ndarray, theta_s: np.ndarray) -> float:
+    """Recovery score of Sec. 3: overlap of the span of the leading two
+    nontrivial Markov modes with span(cos theta_s, sin theta_s), both centred,
+    in [0, 1]: the mean squared canonical correlation of the two planes
+    (orthonormal bases by QR, float64)."""
+    A = np.asarray(psi2, dtype=np.float64)
+    B = np.stack([np.cos(theta_s), np.sin(theta_s)], 1)
+    qa, _ = np.linalg.qr(A - A.mean(0))
+    qb, _ = np.linalg.qr(B - B.mean(0))
+    return float(np.sum((qa.T @ qb) ** 2) / 2.0)
+
+
+def paper_t6_flow_leg(fd, torch, dev, max_lg: int) -> dict:
+    """Sec. 3's solve on the paper's T^6 set-up: the beta flow with k = 3
+    nontrivial modes (k = 4 with the Perron pair), alpha = 1/2, b = 8, from
+    beta_0 of eq. beta0, at N = 2^10 .. 2^max_lg; time, beta_x and the
+    doublet score beside the paper's one-GPU rows.  Repeats follow the
+    paper's n_rep = clip(ceil(64^((22 - log2 N) / 12)), 1, 64), at most 8."""
+    import math
+    from paper_2609_38198_amd import inputs
+    rows = []
+    warm = inputs.torus6_paper(1024)
+    fd.fd_beta_flow(torch.from_numpy(warm.X).to(dev), 4, 8, alpha=0.5)  # code objects
+    torch.cuda.synchronize()
+    for lg in range(10, max_lg + 1):
+        N = 1 << lg
+        w = inputs.torus6_paper(N)
+        X = torch.from_numpy(w.X).to(dev)
+        nrep = min(8, max(1, min(64, math.ceil(64 ** ((22 - lg) / 12)))))
+        times, flow = [], None
+        for _ in range(nrep):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            flow = fd.fd_beta_flow(X, 4, 8, alpha=0.5, allow=(0, 5))
+            torch.cuda.synchronize()
+            times.append(time.perf_counter() - t0)
+        psi = flow.psi.double().cpu().numpy()
+        score = doublet_overlap(psi[:, 1:3], w.extra["theta"][:, 5])
+        p = PAPER_T6_ONE_GPU.get(N)
+        row = {"N": N, "reps": nrep, "seconds": float(np.mean(times)),
+               "seconds_std": float(np.std(times)), "beta_x": flow.beta_x,
+               "exit": flow.reason, "probes": len(flow.probes), "status": flow.status,
+               "evals": flow.evals, "overlap": score, "one_minus_overlap": 1.0 - score}
+        if p is not None:
+            row.update({"paper_seconds": p[0], "paper_seconds_std": p[1], "paper_beta_x": p[2],
+                        "paper_beta_x_std": p[3], "paper_overlap": p[4],
+                        "paper_over_this_time": p[0] / row["seconds"]})
+        rows.append(row)
+        log(f"paper T6 flow: N=2^{lg}: {row['seconds']:.3f} s x {nrep}, beta_x "
+            f"{flow.beta_x:.4f} ({flow.reason}), 1 - overlap {1.0 - score:.2e}"
+            + (f"; paper {p[0]:.1f} s, beta_x {p[2]:.3f}, 1 - overlap {1.0 - p[4]:.2e}"
+               if p else ""))
+        del X
+    return {"workload": "paper T^6 (radii 1.00 .. 1.50, D = 32 zero-padded, seed 42): beta flow, "
+                        "k = 3 nontrivial + Perron, alpha = 1/2, b = 8, fp32", "rows": rows}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -341,6 +415,9 @@ def main() -> int:
     ap.add_argument("--paper-t6", action="store_true",
                     help="raw K V on the paper's T^6 set-up (D=32, beta=1, b=1 and 8) beside "
                          "the paper's own timings")
+    ap.add_argument("--paper-t6-flow", type=int, default=0, metavar="LOG2N",
+                    help="Sec. 3's beta-flow solve on the paper's T^6 set-up at N = 2^10 .. "
+                         "2^LOG2N beside the paper's one-GPU rows")
     ap.add_argument("--calibration-copy", type=int, default=0, metavar="MIB",
                     help="after the timed steps, copy MIB MiB device to device (a plain copy "
                          "kernel of known size, read by the HBM counter runs as their scale)")
@@ -475,6 +552,8 @@ def main() -> int:
         rec["stress"] = stress_leg(fd, torch, dev)
     if args.paper_t6:
         rec["paper_t6"] = paper_t6_leg(fd, torch, dev)
+    if args.paper_t6_flow:
+        rec["paper_t6_flow"] = paper_t6_flow_leg(fd, torch, dev, args.paper_t6_flow)
     if not args.no_cpu_baseline:
         log("CPU oracle baseline")
         rec["cpu_baseline"] = cpu_baseline(wl.X, beta, b, args.cpu_seconds,

@@ -27,6 +27,11 @@
  *  - X should be centred (subtract the column mean): the method is stated for
  *    centred observations (Sec. 2.1, eq. rbf_gram) and the Gram-form
  *    evaluation loses accuracy on data far from the origin.  Not enforced.
+ *  - Non-finite X: every entry point scans X on the device first.  The
+ *    asynchronous ones (fd_kernel_matmul, fd_kernel_matmul_noalloc, fd_degree,
+ *    fd_degree_dyadic) then fill all their outputs with NaN; the eigensolver,
+ *    continuation and flow entry points return FD_ERR_INVALID_ARG before any
+ *    other work.
  */
 #ifndef FLASHDIFF_H
 #define FLASHDIFF_H
@@ -68,9 +73,13 @@ typedef enum fd_op {
 typedef struct fd_lanczos_opts {
   double tol;               /* converged when ||M phi - theta phi||_2 <= tol (||M||_2 = 1). Default 1e-5 */
   int32_t max_restarts;     /* restart cycles before FD_ERR_NOT_CONVERGED. Default 200 */
-  int32_t max_basis_blocks; /* basis capacity in blocks of b (0 = automatic: k + keep rounded up to
-                               whole blocks, plus as many again but at least 2 blocks; at most
-                               1024 columns) */
+  int32_t max_basis_blocks; /* basis capacity in blocks of b (0 = automatic: four times the first
+                               checkpoint, at most 1024 columns).  The first convergence check
+                               (Rayleigh-Ritz without restart) comes when the basis reaches k + keep
+                               rounded up to whole blocks plus as many again (at least 2 blocks);
+                               later checks come when the block products added since the last one
+                               cost about as much as a check (a fixed cost model of N, D, b and the
+                               basis width, so runs are reproducible); a full basis restarts */
   int32_t keep;             /* Ritz vectors kept at restart beyond k (-1 = automatic: b) */
   int32_t max_matvecs;      /* stop after this many block products (0 = no limit). A run that
                                stops this way returns FD_ERR_NOT_CONVERGED with valid Ritz pairs */
@@ -180,6 +189,11 @@ fd_status fd_degree_dyadic(const void* X, fd_dtype xt, int64_t N, int64_t D, int
  * (Sec. 2.3, first paragraph; Sec. 2.1 eq. symmetric), including the Perron
  * pair theta_0 = 1.  Computes the normalisation itself (fd_degree) and then
  * applies M to blocks of b vectors, one fused product per block.
+ * A solve stops early at the Perron wall (eq. perronwall): when the Perron pair
+ * has converged and the Ritz gap (theta_0 - theta_1) / theta_0, an upper bound
+ * of the true gap, is at or below kappa_P eta (eta of X's dtype), the leading
+ * eigenspace is not resolvable in that precision; info->wall is then 1 and
+ * the status FD_ERR_NOT_CONVERGED unless all k pairs had converged.
  *   X: N x D (device).  beta > 0, 0 <= alpha <= 1, 1 <= b <= 64, 1 <= k <= N.
  *   V0: optional warm start, N x k0 (device, ldv0 >= k0); NULL or k0 = 0 for a
  *       seeded random start.  Interpreted as Markov right eigenvectors psi
@@ -216,7 +230,10 @@ fd_status fd_block_lanczos(const void* X, fd_dtype xt, int64_t N, int64_t D, int
  *   stop_at_wall: when non-zero, stop after the first step whose Perron gap is at or
  *   below kappa_P * eta (eta of X's dtype, as in info->wall) and return FD_ERR_PERRON_WALL; evals of the steps run
  *   so far are valid and *steps_done tells how many ran.
- *   steps_done: host int64 or NULL. */
+ *   steps_done: host int64 or NULL.
+ * Returns FD_ERR_NOT_CONVERGED when a step short of the Perron wall stopped
+ * before its k pairs converged; a step at the wall (per_step[t].wall = 1, its
+ * solve stopped as fd_block_lanczos describes) is reported, not failed. */
 fd_status fd_continuation(const void* X, fd_dtype xt, int64_t N, int64_t D, int64_t ldx,
                           float alpha, const int64_t* n_steps, const float* beta_steps,
                           int64_t nsteps, int64_t b, int64_t k, const float* V0, int64_t k0,

@@ -57,6 +57,82 @@ void check_workspace(const void* ws, size_t ws_bytes, size_t need) {
              "workspace must be 256-byte aligned");
 }
 
+// ---------------------------------------------------------------- non-finite inputs
+
+__global__ void clear_flag_kernel(int* flag) { *flag = 0; }
+
+__global__ void scan_nonfinite_kernel(const void* __restrict__ X, int bf16, int64_t n, int D,
+                                      int64_t ldx, int* __restrict__ flag) {
+  const int64_t total = n * D;
+  bool bad = false;
+  for (int64_t e = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; e < total;
+       e += int64_t(gridDim.x) * blockDim.x) {
+    const int64_t i = e / D, f = e % D;
+    if (bf16) {
+      const uint16_t v = static_cast<const uint16_t*>(X)[i * ldx + f];
+      bad = bad || (v & 0x7F80u) == 0x7F80u;
+    } else {
+      bad = bad || !isfinite(static_cast<const float*>(X)[i * ldx + f]);
+    }
+  }
+  if (bad) atomicOr(flag, 1);
+}
+
+__global__ void poison_f32_kernel(const int* __restrict__ flag, float* __restrict__ v,
+                                  int64_t rows, int64_t cols, int64_t ld) {
+  if (*flag == 0) return;
+  for (int64_t e = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; e < rows * cols;
+       e += int64_t(gridDim.x) * blockDim.x)
+    v[(e / cols) * ld + e % cols] = __builtin_nanf("");
+}
+
+__global__ void poison_f64_kernel(const int* __restrict__ flag, double* __restrict__ v,
+                                  int64_t n) {
+  if (*flag == 0) return;
+  for (int64_t e = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; e < n;
+       e += int64_t(gridDim.x) * blockDim.x)
+    v[e] = __builtin_nan("");
+}
+
+static unsigned stride_grid(int64_t n) {
+  return unsigned(std::min<int64_t>(1024, std::max<int64_t>(1, (n + 255) / 256)));
+}
+
+void launch_scan_nonfinite(const void* X, fd_dtype xt, int64_t N, int64_t D, int64_t ldx,
+                           int* flag, bool clear, hipStream_t stream) {
+  FD_REQUIRE(flag != nullptr, FD_ERR_INVALID_ARG, "internal: no flag word");
+  if (clear) {
+    hipLaunchKernelGGL(clear_flag_kernel, dim3(1), dim3(1), 0, stream, flag);
+    FD_LAUNCH_CHECK();
+  }
+  hipLaunchKernelGGL(scan_nonfinite_kernel, dim3(stride_grid(N * D)), dim3(256), 0, stream, X,
+                     xt == FD_BF16 ? 1 : 0, N, int(D), ldx, flag);
+  FD_LAUNCH_CHECK();
+}
+
+void launch_poison(const int* flag, float* v, int64_t rows, int64_t cols, int64_t ld,
+                   hipStream_t stream) {
+  if (v == nullptr || rows * cols == 0) return;
+  hipLaunchKernelGGL(poison_f32_kernel, dim3(stride_grid(rows * cols)), dim3(256), 0, stream,
+                     flag, v, rows, cols, ld);
+  FD_LAUNCH_CHECK();
+}
+
+void launch_poison(const int* flag, double* v, int64_t n, hipStream_t stream) {
+  if (v == nullptr || n == 0) return;
+  hipLaunchKernelGGL(poison_f64_kernel, dim3(stride_grid(n)), dim3(256), 0, stream, flag, v, n);
+  FD_LAUNCH_CHECK();
+}
+
+void require_finite(const void* X, fd_dtype xt, int64_t N, int64_t D, int64_t ldx, int* flag,
+                    hipStream_t stream) {
+  launch_scan_nonfinite(X, xt, N, D, ldx, flag, true, stream);
+  int h = 0;
+  FD_HIP_CHECK(hipMemcpyAsync(&h, flag, sizeof(int), hipMemcpyDeviceToHost, stream));
+  FD_HIP_CHECK(hipStreamSynchronize(stream));
+  FD_REQUIRE(h == 0, FD_ERR_INVALID_ARG, "X holds a NaN or infinite value");
+}
+
 // ---------------------------------------------------------------- products
 
 ProductWs carve_product(Arena& a, int64_t Nr, int64_t Nc, int64_t D, int b) {
@@ -69,6 +145,7 @@ ProductWs carve_product(Arena& a, int64_t Nr, int64_t Nc, int64_t D, int b) {
   w.vscale = a.fspan(128);
   w.part = a.fspan(part_rows_bound(w.rows.npad, Nc) * w.plan.ncb * 16);
   w.tmp = a.fspan(size_t(Nr));
+  w.flag = a.take<int>(1);
   return w;
 }
 
@@ -87,6 +164,7 @@ static ProductWs carve_product_exact(Arena& a, int64_t Nr, int64_t Nc, int64_t D
   const size_t part_row = size_t(rp.nsplit) * w.rows.npad;
   w.part = a.fspan(b == 1 ? part_row : part_prod);
   w.tmp = a.fspan(size_t(Nr));
+  w.flag = a.take<int>(1);
   return w;
 }
 
@@ -180,6 +258,7 @@ DegreeWs carve_degree(Arena& a, int64_t N, int64_t D) {
   w.w = a.take<float>(size_t(N));
   w.part = a.fspan(std::max(part_rows_bound(w.rows.npad, N), sym_part_rows(w.rows.npad, SYM_NIB)));
   w.colfix = a.take<unsigned long long>(size_t(w.rows.npad));
+  w.flag = a.take<int>(1);
   return w;
 }
 
@@ -374,11 +453,14 @@ fd_status fd_kernel_matmul(const void* Xr, int64_t Nr, const void* Xc, int64_t N
     a.cap = ws_bytes;
     ProductWs w = carve_product(a, Nr, Nc, D, int(b));
     hipStream_t st = static_cast<hipStream_t>(stream);
+    launch_scan_nonfinite(Xr, xt, Nr, D, ldx, w.flag, true, st);
+    if (Xc != Xr) launch_scan_nonfinite(Xc, xt, Nc, D, ldx, w.flag, false, st);
     launch_pack_points(Xr, xt, Nr, D, ldx, beta, true, w.rows, st);
     launch_pack_points(Xc, xt, Nc, D, ldx, beta, false, w.cols, st);
     // same base pointer and ldx: index i names the same point in both sets
     const bool diag = (Xr == Xc);
     product_apply(w, sl, sr, V, ldv, int(b), Y, ldy, diag, st);
+    launch_poison(w.flag, Y, Nr, b, ldy, st);
   });
 }
 
@@ -405,10 +487,13 @@ fd_status fd_kernel_matmul_noalloc(const void* Xr, int64_t Nr, const void* Xc, i
     a.cap = SCRATCH_BYTES;
     ProductWs w = carve_product_exact(a, Nr, Nc, D, int(b));
     hipStream_t st = static_cast<hipStream_t>(stream);
+    launch_scan_nonfinite(Xr, xt, Nr, D, ldx, w.flag, true, st);
+    if (Xc != Xr) launch_scan_nonfinite(Xc, xt, Nc, D, ldx, w.flag, false, st);
     launch_pack_points(Xr, xt, Nr, D, ldx, beta, true, w.rows, st);
     launch_pack_points(Xc, xt, Nc, D, ldx, beta, false, w.cols, st);
     const bool diag = (Xr == Xc);
     product_apply(w, sl, sr, V, ldv, int(b), Y, ldy, diag, st);
+    launch_poison(w.flag, Y, Nr, b, ldy, st);
   });
 }
 
@@ -429,8 +514,11 @@ fd_status fd_degree(const void* X, fd_dtype xt, int64_t N, int64_t D, int64_t ld
     a.base = static_cast<char*>(ws);
     a.cap = ws_bytes;
     DegreeWs w = carve_degree(a, N, D);
-    degree_run(w, X, xt, N, D, ldx, beta, alpha, q, d, s, s_off, true,
-               static_cast<hipStream_t>(stream));
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    launch_scan_nonfinite(X, xt, N, D, ldx, w.flag, true, st);
+    degree_run(w, X, xt, N, D, ldx, beta, alpha, q, d, s, s_off, true, st);
+    for (float* v : {q, d, s}) launch_poison(w.flag, v, N, 1, 1, st);
+    launch_poison(w.flag, s_off, 1, st);
   });
 }
 
@@ -453,8 +541,11 @@ fd_status fd_degree_dyadic(const void* X, fd_dtype xt, int64_t N, int64_t D, int
     a.base = static_cast<char*>(ws);
     a.cap = ws_bytes;
     DegreeWs w = carve_degree_dyadic(a, N, D);
-    degree_run_dyadic(w, X, xt, N, D, ldx, beta0, int(nbeta), alpha, q, d, s, s_off,
-                      static_cast<hipStream_t>(stream));
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    launch_scan_nonfinite(X, xt, N, D, ldx, w.flag, true, st);
+    degree_run_dyadic(w, X, xt, N, D, ldx, beta0, int(nbeta), alpha, q, d, s, s_off, st);
+    for (float* v : {q, d, s}) launch_poison(w.flag, v, int64_t(nbeta) * N, 1, 1, st);
+    launch_poison(w.flag, s_off, nbeta, st);
   });
 }
 

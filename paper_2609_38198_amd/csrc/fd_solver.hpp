@@ -10,6 +10,7 @@ struct ProductWs {
   PointPack rows, cols;
   FSpan vp, vscale, part;
   FSpan tmp;  // one float per row: the single-column product's row sums
+  int* flag = nullptr;  // set when a point set holds a non-finite value
   KVPlan plan;
 };
 
@@ -23,6 +24,7 @@ struct DegreeWs {
   unsigned long long* colfix = nullptr;  // npad words: column sums of the symmetric row sums
   FSpan sq_part;                          // squared-kernel row partials (dyadic levels)
   unsigned long long* sq_colfix = nullptr;
+  int* flag = nullptr;  // set when X holds a non-finite value
   KVPlan plan;
 };
 
@@ -47,6 +49,19 @@ DegreeWs carve_degree_dyadic(Arena& a, int64_t N, int64_t D);
 void degree_run_dyadic(DegreeWs& w, const void* X, fd_dtype xt, int64_t N, int64_t D,
                        int64_t ldx, double beta0, int nb, double alpha, float* q, float* d,
                        float* s, double* s_off, hipStream_t stream);
+
+// Non-finite inputs.  scan: clear *flag, then set it if any of the N x D
+// values of X is NaN or infinite.  poison: when *flag is set, fill rows x cols
+// floats of v (leading dimension ld) with NaN.  Both asynchronous.
+void launch_scan_nonfinite(const void* X, fd_dtype xt, int64_t N, int64_t D, int64_t ldx,
+                           int* flag, bool clear, hipStream_t stream);
+void launch_poison(const int* flag, float* v, int64_t rows, int64_t cols, int64_t ld,
+                   hipStream_t stream);
+void launch_poison(const int* flag, double* v, int64_t n, hipStream_t stream);
+// Synchronous check for the eigensolver entry points: FD_ERR_INVALID_ARG when
+// X holds a non-finite value.
+void require_finite(const void* X, fd_dtype xt, int64_t N, int64_t D, int64_t ldx, int* flag,
+                    hipStream_t stream);
 
 // Row slots of a partial-sum buffer large enough for every plan with at most
 // npad rows and nc columns (see plan_product).

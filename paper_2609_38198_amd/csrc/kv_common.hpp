@@ -44,14 +44,19 @@ __device__ __forceinline__ void split2(float a, float b, unsigned& hi, unsigned&
   lo = __builtin_bit_cast(unsigned, l);
 }
 
-// The same split with the remainders formed by one mixed-precision FMA each,
-// k - h = fma(h, m1, k) reading h straight from the packed float16 word.
+// The same split with each remainder formed by one mixed-precision FMA,
+// k - h = fma(h, m1, k) reading h straight from the packed float16 word (exact
+// in float32) and rounded to nearest float16.
 // m1 must be -1; it is a run-time value (a kernel argument) so that the
 // compiler keeps the FMA form instead of turning it into a subtraction.
 __device__ __forceinline__ void split2m(float a, float b, float m1, unsigned& hi, unsigned& lo) {
   const pkhalf2 h = __builtin_amdgcn_cvt_pkrtz(a, b);
-  const pkhalf2 l = __builtin_amdgcn_cvt_pkrtz(__builtin_fmaf(float(h[0]), m1, a),
-                                               __builtin_fmaf(float(h[1]), m1, b));
+  // each remainder rounded straight into its half of the packed word
+  // (v_fma_mixlo_f16 / v_fma_mixhi_f16: two instructions instead of two
+  // float32 FMAs and a conversion)
+  pkhalf2 l;
+  l[0] = (_Float16)__builtin_fmaf(float(h[0]), m1, a);
+  l[1] = (_Float16)__builtin_fmaf(float(h[1]), m1, b);
   hi = __builtin_bit_cast(unsigned, h);
   lo = __builtin_bit_cast(unsigned, l);
 }

@@ -23,41 +23,24 @@
 #include <cstdio>
 #include <vector>
 
+#include "fd_host_logic.hpp"
 #include "fd_linalg.hpp"
 #include "fd_solver.hpp"
 
 namespace fd {
 
-constexpr double KAPPA_P = 10.0;   // safety factor of the Perron wall (eq. perronwall)
-constexpr double ETA_FP32 = 1e-7;  // precision scale of float32 kernel data
-constexpr double ETA_BF16 = 8e-3;  // precision scale of bfloat16 kernel data
-
-// eta of the data type the kernel is evaluated from (footnote to eq. perronwall)
-static double eta_of(fd_dtype xt) { return xt == FD_BF16 ? ETA_BF16 : ETA_FP32; }
-
-struct SolverLayout {
-  int b = 0, k = 0, keep = 0, kk = 0, mm = 0;
-  bool dense = false;
-};
+using logic::at_perron_wall;
+using logic::count_converged;
+using logic::eta_of;
+using logic::KAPPA_P;
+using logic::next_cycle_width;
+using logic::restart_columns;
+using logic::SolverLayout;
 
 static SolverLayout solver_layout(int64_t N, int b, int k, const fd_lanczos_opts& o) {
   SolverLayout L;
-  L.b = b;
-  L.k = k;
-  L.keep = o.keep >= 0 ? o.keep : b;
-  L.kk = k + L.keep;
-  int mm = o.max_basis_blocks > 0 ? o.max_basis_blocks * b
-                                  : int(round_up(L.kk, b) + std::max<int64_t>(2 * b, round_up(L.kk, b)));
-  mm = std::min(mm, (1024 / b) * b);  // projected eigensolve limit
-  if (N <= mm) {
-    L.dense = true;
-    L.mm = int(N);
-    L.kk = int(N);
-    return L;
-  }
-  L.mm = mm;
-  FD_REQUIRE(L.kk + b <= mm, FD_ERR_INVALID_ARG,
-             "basis too small: need k + keep + b <= max_basis_blocks * b (and <= 1024)");
+  const std::string why = logic::solver_layout(N, b, k, o.keep, o.max_basis_blocks, L);
+  FD_REQUIRE(why.empty(), FD_ERR_INVALID_ARG, why);
   return L;
 }
 
@@ -218,7 +201,7 @@ struct SolveResult {
 // scaled by d^scale_pow (0.5 turns Markov vectors into M's).
 static SolveResult lanczos_solve(SolverWs& w, Lanczos& L, const SolverLayout& lay, int k,
                                  const float* V0, int64_t k0, int64_t ldv0, double scale_pow,
-                                 const fd_lanczos_opts& o) {
+                                 const fd_lanczos_opts& o, double eta) {
   hipStream_t st = L.st;
   const int64_t N = L.N;
   const int b = lay.b, mm = lay.mm;
@@ -253,8 +236,10 @@ static SolveResult lanczos_solve(SolverWs& w, Lanczos& L, const SolverLayout& la
   std::vector<double> th(mm), rs(mm);
   std::vector<int> sel(b);
   const int budget = o.max_matvecs > 0 ? o.max_matvecs : INT32_MAX;
+  int width = lay.m_first;  // basis width of the current restart cycle
+  int nconv_cycle = 0;      // leading converged pairs at the last restart
   while (true) {
-    const bool full = lay.dense || m + b > mm;
+    const bool full = lay.dense || m + b > width;
     const bool out_of_budget = L.matvecs >= budget;
     if (full || need_rr || out_of_budget) {
       const int nkeep = lay.dense ? std::min(mm, std::max(k, 1)) : std::min(lay.kk, m);
@@ -262,10 +247,7 @@ static SolveResult lanczos_solve(SolverWs& w, Lanczos& L, const SolverLayout& la
       FD_HIP_CHECK(hipMemcpyAsync(th.data(), w.theta, sizeof(double) * m, hipMemcpyDeviceToHost, st));
       FD_HIP_CHECK(hipMemcpyAsync(rs.data(), w.res, sizeof(double) * nkeep, hipMemcpyDeviceToHost, st));
       FD_HIP_CHECK(hipStreamSynchronize(st));
-      std::swap(w.Q, w.Qa);
-      std::swap(w.W, w.Wa);
-      int nconv = 0;
-      while (nconv < k && rs[nconv] <= o.tol) ++nconv;
+      const int nconv = count_converged(rs.data(), k, o.tol);
       if (o.verbose) {
         double worst = 0.0;
         for (int c = 0; c < std::min(k, nkeep); ++c) worst = std::max(worst, rs[c]);
@@ -273,27 +255,37 @@ static SolveResult lanczos_solve(SolverWs& w, Lanczos& L, const SolverLayout& la
             std::chrono::duration<double>(std::chrono::steady_clock::now() - t_start).count();
         std::fprintf(stderr,
                      "[fd_lanczos] N=%lld cycle=%d basis=%d products=%d converged=%d/%d "
-                     "max_residual=%.3e theta0=%.9f theta_k-1=%.6e elapsed=%.3fs\n",
+                     "max_residual=%.3e theta0=%.9f theta_k-1=%.6e elapsed=%.3fs%s\n",
                      (long long)N, R.restarts, m, L.matvecs, nconv, k, worst, th[0],
-                     th[std::min(k, m) - 1], el);
+                     th[std::min(k, m) - 1], el, "");
         std::fflush(stderr);
       }
       R.nconv = nconv;
       R.theta.assign(th.begin(), th.begin() + std::min(m, std::max(k, 2)));
       R.res.assign(rs.begin(), rs.begin() + std::min(nkeep, k));
-      if (nconv >= k || lay.dense) {
+      const bool done = nconv >= k || lay.dense;
+      const bool at_wall = at_perron_wall(m, th[0], m >= 2 ? th[1] : 0.0, rs[0], o.tol, eta);
+      const bool stop = out_of_budget || R.restarts >= o.max_restarts || at_wall;
+      // the leading Ritz vectors and their images become the basis
+      std::swap(w.Q, w.Qa);
+      std::swap(w.W, w.Wa);
+      if (done) {
         R.converged = nconv >= k;
         break;
       }
-      if (out_of_budget || R.restarts >= o.max_restarts) break;
-      if (!need_rr) ++R.restarts;
+      if (stop) break;
+      if (!need_rr) {
+        ++R.restarts;
+        width = next_cycle_width(lay, width, nconv_cycle, nconv);
+      } else {
+        width = logic::warm_cycle_width(lay, nkeep);
+      }
+      nconv_cycle = nconv;
       need_rr = false;
       // restart: keep the Ritz pairs, next block from the leading unconverged residuals
       m = nkeep;
       set_diag(w.T, mm, mm, w.theta, m, st);
-      int ns = 0;
-      for (int c = 0; c < nkeep && ns < b; ++c)
-        if (rs[c] > o.tol) sel[ns++] = c;
+      const int ns = restart_columns(rs.data(), nkeep, b, o.tol, sel.data());
       FD_HIP_CHECK(hipMemcpyAsync(w.sel, sel.data(), sizeof(int) * ns, hipMemcpyHostToDevice, st));
       float* Z = w.Q + m;
       gather_residuals(w.Q, w.W, mm, w.theta, w.sel, ns, Z, mm, N, st);
@@ -322,8 +314,7 @@ static void fill_info(fd_lanczos_info* info, const SolveResult& R, double s_off,
   info->restarts = R.restarts;
   info->block_matvecs = R.matvecs;
   info->nconv = R.nconv;
-  double gap = 0.0;
-  if (R.theta.size() >= 2 && R.theta[0] != 0.0) gap = (R.theta[0] - R.theta[1]) / std::fabs(R.theta[0]);
+  const double gap = R.theta.size() >= 2 ? logic::perron_gap(R.theta[0], R.theta[1]) : 0.0;
   info->gap_perron = gap;
   info->wall = gap <= KAPPA_P * eta ? 1 : 0;
   info->s_off = s_off;
@@ -539,18 +530,9 @@ static double centred_mean_sq(FlowWs& f, const T* X, int64_t N, int64_t D, int64
   return ms;
 }
 
-struct FlowParams {
-  double eta, kappa, p;
-};
-
-struct FlowProbe {
-  double beta = 0.0, s_off = 0.0, gap = 0.0, v_bias = 0.0, v_mach = 0.0;
-  double n_eff = NAN, v_stat = NAN, v_total = NAN, d_hat = NAN, seconds = 0.0;
-  bool admissible = false, converged = false;
-  int role = 0, matvecs = 0, nconv = 0;
-  std::vector<double> evals;
-  bool complete() const { return !std::isnan(v_total); }
-};
+using logic::FlowOutcome;
+using logic::FlowParams;
+using logic::FlowProbe;
 
 // One probe: normalisation and top-k eigensolve at beta (warm: Markov vectors
 // N x k or NULL); the Ritz vectors stay in sw.Q, psi goes to psi_out.
@@ -568,50 +550,17 @@ static FlowProbe flow_probe(FlowWs& f, const void* X, fd_dtype xt, int64_t N, in
   const SolverLayout lay = solver_layout(N, b, k, o);
   Lanczos L(f.sw, product_view(f.sw.prod, f.sw.deg.rows, f.sw.deg.cols, b), st, N, b, lay.mm,
             o.seed + seed_offset);
-  SolveResult R = lanczos_solve(f.sw, L, lay, k, warm, warm ? k : 0, k, 0.5, o);
+  SolveResult R = lanczos_solve(f.sw, L, lay, k, warm, warm ? k : 0, k, 0.5, o, eta_of(xt));
   copy_cols(f.sw.Q, lay.mm, psi_out, k, N, k, f.sw.d, -0.5, st);
   FD_HIP_CHECK(hipMemcpyAsync(&pr.s_off, f.sw.s_off, sizeof(double), hipMemcpyDeviceToHost, st));
   FD_HIP_CHECK(hipStreamSynchronize(st));
   pr.evals = R.theta;
-  pr.evals.resize(k, 0.0);
   pr.converged = R.converged;
   pr.matvecs = R.matvecs;
   pr.nconv = R.nconv;
-  const double l0 = pr.evals[0];
-  pr.gap = (l0 - pr.evals[1]) / std::fabs(l0);
-  std::vector<double> h;
-  for (int j = 1; j < k; ++j) h.push_back(-std::log(pr.evals[j] / l0));
-  std::sort(h.begin(), h.end());
-  const size_t n = h.size();
-  pr.v_bias = (n % 2 == 1) ? h[n / 2] : 0.5 * (h[n / 2 - 1] + h[n / 2]);
-  pr.v_mach = pr.gap > 0.0 ? std::pow(fp.kappa * fp.eta / pr.gap, fp.p) : INFINITY;
-  pr.admissible = pr.gap > fp.kappa * fp.eta;
+  logic::probe_stats(pr, k, fp);
   pr.seconds = std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
   return pr;
-}
-
-// Quantities of `a` that need S_off at twice its bandwidth (probe c).
-static void flow_complete(FlowProbe& a, const FlowProbe& c, int64_t N) {
-  a.n_eff = a.s_off * a.s_off / (double(N) * c.s_off);
-  a.v_stat = 1.0 / std::sqrt(a.n_eff * a.v_bias);
-  a.v_total = a.v_bias + a.v_stat + a.v_mach;
-  a.d_hat = -2.0 * (std::log(c.s_off) - std::log(a.s_off)) / (std::log(c.beta) - std::log(a.beta));
-}
-
-static bool flow_brackets(const FlowProbe& a, const FlowProbe& m, const FlowProbe& c) {
-  return a.v_total > m.v_total && c.v_total > m.v_total && c.v_bias < a.v_bias &&
-         (c.v_stat > a.v_stat || c.v_mach > a.v_mach);
-}
-
-// Vertex abscissa of the parabola through (x_i, y_i), clamped to [x0, x2].
-static double flow_vertex(const double x[3], const double y[3]) {
-  const double den = (x[0] - x[1]) * (x[0] - x[2]) * (x[1] - x[2]);
-  const double A = (x[2] * (y[1] - y[0]) + x[1] * (y[0] - y[2]) + x[0] * (y[2] - y[1])) / den;
-  const double B =
-      (x[2] * x[2] * (y[0] - y[1]) + x[1] * x[1] * (y[2] - y[0]) + x[0] * x[0] * (y[1] - y[2])) /
-      den;
-  const double v = -B / (2.0 * A);
-  return std::min(std::max(v, x[0]), x[2]);
 }
 
 static fd_flow_probe flow_record(const FlowProbe& p, int level) {
@@ -645,100 +594,47 @@ static double flow_beta0(FlowWs& f, const void* X, fd_dtype xt, int64_t N, int64
   return ms > 0.0 ? std::min(0.1, 1.0 / (2.0 * ms)) : 0.1;
 }
 
-struct FlowOutcome {
-  bool any = false;  // at least one admissible probe
-  int reason = FD_FLOW_BUDGET;
-  FlowProbe fin;     // the probe at the achieved bandwidth
+// One sweep of the flow on X from `beta` (Sec. 2.3; the decisions are
+// logic::run_flow_logic).  warm: psi_keep already holds Markov vectors to
+// start the first probe from.  Records are appended to `out` with the given
+// level.  On return with any == true, sw.Q holds the eigenvectors of the solve
+// at fin.beta and psi_keep its Markov vectors.
+struct DeviceFlowDriver {
+  FlowWs& f;
+  const void* X;
+  fd_dtype xt;
+  int64_t N, D, ldx;
+  double alpha;
+  int bb, kk;
+  const FlowParams& fp;
+  const fd_lanczos_opts& o;
+  int level;
+  std::vector<fd_flow_probe>& out;
+  hipStream_t st;
+
+  FlowProbe probe(double beta, int role, int t, bool from_keep) {
+    const uint64_t lseed = uint64_t(level) * 1000003u;
+    const uint64_t off = role == 0   ? lseed + uint64_t(t) * 7919u
+                         : role == 1 ? lseed + 104729u
+                                     : lseed + 15485863u;
+    return flow_probe(f, X, xt, N, D, ldx, beta, alpha, bb, kk, from_keep ? f.psi_keep : nullptr,
+                      f.psi_new, o, fp, role, off, st);
+  }
+  void accept() { std::swap(f.psi_keep, f.psi_new); }
+  void record(const FlowProbe& p, bool replace_last) {
+    if (replace_last)
+      out.back() = flow_record(p, level);
+    else
+      out.push_back(flow_record(p, level));
+  }
 };
 
-// One sweep of the flow on X from `beta` (Sec. 2.3).  warm: psi_keep already
-// holds Markov vectors to start the first probe from.  Records are appended
-// to `out` with the given level.  On return with any == true, sw.Q holds the
-// eigenvectors of the solve at fin.beta and psi_keep its Markov vectors.
 static FlowOutcome run_flow(FlowWs& f, const void* X, fd_dtype xt, int64_t N, int64_t D,
                             int64_t ldx, double alpha, int bb, int kk, double beta, bool warm,
                             const FlowParams& fp, const fd_lanczos_opts& o, int max_probes,
                             int level, std::vector<fd_flow_probe>& out, hipStream_t st) {
-  FlowOutcome res;
-  std::vector<FlowProbe> pr;  // admissible dyadic probes
-  bool have_keep = warm;      // psi_keep holds the latest admissible probe (or the warm start)
-  double in_q = -1.0;         // bandwidth whose Ritz vectors are in sw.Q
-  int reason = FD_FLOW_BUDGET;
-  FlowProbe fin;
-  bool fin_in_q = false;
-  const uint64_t lseed = uint64_t(level) * 1000003u;
-  for (int t = 0; t < max_probes; ++t) {
-    FlowProbe p = flow_probe(f, X, xt, N, D, ldx, beta, alpha, bb, kk,
-                             have_keep ? f.psi_keep : nullptr, f.psi_new, o, fp, 0,
-                             lseed + uint64_t(t) * 7919u, st);
-    in_q = beta;
-    if (!p.admissible) {
-      out.push_back(flow_record(p, level));
-      reason = FD_FLOW_WALL;
-      break;
-    }
-    if (!pr.empty()) {
-      flow_complete(pr.back(), p, N);
-      out.back() = flow_record(pr.back(), level);
-    }
-    pr.push_back(p);
-    out.push_back(flow_record(p, level));
-    std::swap(f.psi_keep, f.psi_new);
-    have_keep = true;
-    std::vector<int> done;
-    for (int i = 0; i < int(pr.size()); ++i)
-      if (pr[i].complete()) done.push_back(i);
-    const int nd = int(done.size());
-    if (nd >= 3 && flow_brackets(pr[done[nd - 3]], pr[done[nd - 2]], pr[done[nd - 1]])) {
-      const FlowProbe& pa = pr[done[nd - 3]];
-      const FlowProbe& pm = pr[done[nd - 2]];
-      const FlowProbe& pc = pr[done[nd - 1]];
-      const double xs[3] = {std::log(pa.beta), std::log(pm.beta), std::log(pc.beta)};
-      const double ys[3] = {pa.v_total, pm.v_total, pc.v_total};
-      const double bv = std::exp(flow_vertex(xs, ys));
-      FlowProbe v = flow_probe(f, X, xt, N, D, ldx, bv, alpha, bb, kk, f.psi_keep, f.psi_new, o,
-                               fp, 1, lseed + 104729u, st);
-      in_q = bv;
-      out.push_back(flow_record(v, level));
-      reason = FD_FLOW_BRACKET;
-      if (v.admissible) {
-        fin = v;
-        fin_in_q = true;
-      } else {
-        fin = pm;
-      }
-      break;
-    }
-    beta *= 2.0;
-  }
-  res.reason = reason;
-  if (pr.empty()) return res;
-  res.any = true;
-  if (reason != FD_FLOW_BRACKET) {
-    fin = pr.back();
-    if (reason == FD_FLOW_BUDGET) {
-      for (const FlowProbe& q : pr)
-        if (q.complete() && (!fin.complete() || q.v_total < fin.v_total)) fin = q;
-    }
-    fin_in_q = in_q == fin.beta;
-  }
-  if (!fin_in_q) {
-    // the selected probe's vectors were overwritten: solve again from the
-    // latest admissible probe's Markov vectors
-    FlowProbe r = flow_probe(f, X, xt, N, D, ldx, fin.beta, alpha, bb, kk, f.psi_keep,
-                             f.psi_new, o, fp, 2, lseed + 15485863u, st);
-    out.push_back(flow_record(r, level));
-    fin.evals = r.evals;
-    fin.converged = r.converged;
-    fin.nconv = r.nconv;
-    std::swap(f.psi_keep, f.psi_new);
-  } else if (fin.role == 0) {
-    // the latest dyadic probe: its Markov vectors were moved to psi_keep
-  } else {
-    std::swap(f.psi_keep, f.psi_new);
-  }
-  res.fin = fin;
-  return res;
+  DeviceFlowDriver drv{f, X, xt, N, D, ldx, alpha, bb, kk, fp, o, level, out, st};
+  return logic::run_flow_logic(drv, N, beta, warm, max_probes);
 }
 
 }  // namespace fd
@@ -780,13 +676,14 @@ fd_status fd_block_lanczos(const void* X, fd_dtype xt, int64_t N, int64_t D, int
       a.cap = ws_bytes;
       SolverWs w = carve_solver_ws(a, N, D, int(b), lay.mm, int(b));
       hipStream_t st = static_cast<hipStream_t>(stream);
+      require_finite(X, xt, N, D, ldx, w.deg.flag, st);
 
       degree_run(w.deg, X, xt, N, D, ldx, beta, alpha, nullptr, w.d, w.s, w.s_off, true, st);
       // the product view takes the packs as filled (kind and bandwidth)
       Lanczos L(w, product_view(w.prod, w.deg.rows, w.deg.cols, int(b)), st, N, int(b), lay.mm,
                 o.seed);
       SolveResult R = lanczos_solve(w, L, lay, int(k), V0, V0 ? k0 : 0, ldv0,
-                                    warm_is_psi ? 0.5 : 0.0, o);
+                                    warm_is_psi ? 0.5 : 0.0, o, eta_of(xt));
       copy_cols(w.Q, lay.mm, evecs, k, N, int(k), nullptr, 0.0, st);
       if (psi != nullptr) copy_cols(w.Q, lay.mm, psi, k, N, int(k), w.d, -0.5, st);
       double s_off = 0.0;
@@ -857,6 +754,7 @@ fd_status fd_continuation(const void* X, fd_dtype xt, int64_t N, int64_t D, int6
     a.cap = ws_bytes;
     ContWs c = carve_continuation(a, nmax, nsteps, D, int(b), int(k), o);
     hipStream_t st = static_cast<hipStream_t>(stream);
+    require_finite(X, xt, nmax, D, ldx, c.sw.deg.flag, st);
     const int kk = int(k);
     std::vector<std::vector<double>> lam(nsteps);
     std::vector<float> level_beta;
@@ -884,9 +782,7 @@ fd_status fd_continuation(const void* X, fd_dtype xt, int64_t N, int64_t D, int6
         warm_k = kk;
       } else {
         // Nystrom extension of the matching-beta step of the previous prefix
-        int64_t src = last;
-        for (size_t e = 0; e < level_beta.size(); ++e)
-          if (level_beta[e] == beta_steps[t]) src = level_slot[e];
+        const int64_t src = logic::nystrom_source(level_beta, level_slot, beta_steps[t], last);
         nystrom_extend(c, X, xt, D, ldx, n_prev, n, beta_steps[src], alpha, c.psi(src), c.q(src),
                        lam[src], kk, st);
         warm = c.ext;
@@ -902,7 +798,7 @@ fd_status fd_continuation(const void* X, fd_dtype xt, int64_t N, int64_t D, int6
       FD_REQUIRE(lay.mm <= c.sw.mm_cap, FD_ERR_INVALID_ARG, "internal: basis wider than carved");
       ProductWs pv = product_view(c.sw.prod, dv.rows, dv.cols, int(b));
       Lanczos L(c.sw, pv, st, n, int(b), lay.mm, o.seed + uint64_t(t) * 7919u);
-      SolveResult R = lanczos_solve(c.sw, L, lay, kk, warm, warm_k, warm_ld, 0.5, o);
+      SolveResult R = lanczos_solve(c.sw, L, lay, kk, warm, warm_k, warm_ld, 0.5, o, eta_of(xt));
       copy_cols(c.sw.Q, lay.mm, c.psi(t), kk, n, kk, c.sw.d, -0.5, st);
       double s_off = 0.0;
       FD_HIP_CHECK(hipMemcpyAsync(&s_off, c.sw.s_off, sizeof(double), hipMemcpyDeviceToHost, st));
@@ -915,7 +811,9 @@ fd_status fd_continuation(const void* X, fd_dtype xt, int64_t N, int64_t D, int6
       fd_lanczos_info info{};
       fill_info(&info, R, s_off, secs, kk, eta_of(xt));
       if (per_step != nullptr) per_step[t] = info;
-      any_unconverged = any_unconverged || !R.converged;
+      // a step at the Perron wall is reported (info.wall), not failed: its
+      // leading eigenspace is not resolvable in X's precision
+      any_unconverged = any_unconverged || (!R.converged && !info.wall);
       level_beta.push_back(beta_steps[t]);
       level_slot.push_back(t);
       n_prev = n;
@@ -937,7 +835,7 @@ fd_status fd_continuation(const void* X, fd_dtype xt, int64_t N, int64_t D, int6
       return status;
     }
     if (any_unconverged) {
-      set_error("at least one step stopped before all k pairs converged");
+      set_error("at least one step short of the Perron wall stopped before all k pairs converged");
       return FD_ERR_NOT_CONVERGED;
     }
     set_error("");
@@ -1000,6 +898,7 @@ fd_status fd_beta_flow(const void* X, fd_dtype xt, int64_t N, int64_t D, int64_t
     FlowWs f = carve_flow(a, N, D, int(b), int(k), o);
     hipStream_t st = static_cast<hipStream_t>(stream);
     const int kk = int(k), bb = int(b);
+    require_finite(X, xt, N, D, ldx, f.sw.deg.flag, st);
 
     double beta = fo.beta_start;
     if (beta <= 0.0) beta = flow_beta0(f, X, xt, N, D, ldx, st);
@@ -1083,6 +982,8 @@ fd_status fd_beta_flow_cascade(const void* const* Xs, const fd_dtype* xts, const
     FlowWs f = carve_flow(a, N, D, int(b), int(k), o);
     hipStream_t st = static_cast<hipStream_t>(stream);
     const int kk = int(k), bb = int(b);
+    for (int l = 0; l < nlevels; ++l)
+      require_finite(Xs[l], xts[l], N, D, ldxs[l], f.sw.deg.flag, st);
 
     std::vector<fd_flow_probe> out;
     FlowOutcome R;

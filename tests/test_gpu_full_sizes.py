@@ -86,18 +86,52 @@ def test_molecule_2_20_products_and_lanczos_residuals():
     assert np.abs(phi.T @ phi - np.eye(w.k)).max() <= 1e-5
 
 
-def test_stress_bf16_2_21():
-    s = inputs.stress()
-    beta = s.betas[0]
-    V = inputs.random_block(s.N, s.b, seed=25)
-    rows = np.random.default_rng(26).choice(s.N, 16, replace=False)
-    case(f"full size bf16 stress N={s.N} D={s.D} b={s.b}")
-    Xd = to_dev(s.X, device())
+def test_stress_bf16_2_21_product_and_20_iterations():
+    # the bfloat16 stress set at its full size: the raw product on 64 sampled
+    # rows, then the 20 block iterations of the bench leg (b = 64, basis of 16
+    # blocks, 64 kept) and the true residuals (M phi - theta phi)_S of all 64
+    # Ritz pairs with the exact operator on 32 sampled rows
+    st = inputs.stress()
+    beta = st.betas[0]
+    X64 = st.X_f64()
+    V = inputs.random_block(st.N, st.b, seed=25)
+    rows = np.random.default_rng(26).choice(st.N, 64, replace=False)
+    case(f"full size bf16 stress N={st.N} D={st.D} b={st.b}")
+    Xd = to_dev(st.X, device())
     Y0 = to_np(fd.fd_kernel_matmul(Xd, None, beta, to_dev(V, device())))
-    ref = ok.kernel_matmul(s.X_f64(), None, beta, V, rows=rows, threads=8)
+    ref = ok.kernel_matmul(X64, None, beta, V, rows=rows, threads=8)
     err = rel_fro(Y0[rows], ref)
-    print(f"bf16 full size rel err {err:.2e}")
+    print(f"bf16 full size product rel err {err:.2e}")
     assert err <= TOL_BF16
+
+    case(f"full size bf16 stress: 20 block iterations k=64 b={st.b}")
+    o = fd.default_opts(max_matvecs=20, max_basis_blocks=16, keep=64)
+    e = fd.fd_block_lanczos(Xd, beta, 64, st.b, alpha=ALPHA, opts=o, allow_not_converged=True)
+    assert e.info["block_matvecs"] <= 20
+    phi = to_np(e.evecs)
+    theta = np.asarray(e.evals)
+    deg = fd.fd_degree(Xd, beta, ALPHA)
+    q, s = to_np(deg.q), to_np(deg.s)
+    rs = rows[:32]
+    # s on the sampled rows from the device's q elsewhere (bfloat16 bar)
+    ones = np.ones((st.N, 1))
+    q_ref = ok.kernel_matmul(X64, None, beta, ones, rows=rs, threads=8)[:, 0]
+    assert rel_fro(q[rs], q_ref) <= TOL_BF16
+    w = q ** -ALPHA
+    t_ref = ok.kernel_matmul(X64, None, beta, w[:, None], rows=rs, threads=8)[:, 0]
+    assert rel_fro(s[rs], w[rs] / np.sqrt(w[rs] * t_ref)) <= TOL_BF16
+    mphi = ok.kernel_matmul(X64, None, beta, phi, sl=s, sr=s, rows=rs, threads=8)
+    lhs = phi[rs] * theta[None, :]
+    dev_r = rel_fro(lhs, mphi)
+    print(f"bf16 20 iterations: nconv {e.info['nconv']}, solver max residual "
+          f"{e.info['max_residual']:.2e}, exact-operator residual on 32 rows "
+          f"{dev_r:.2e} (relative), theta0 {theta[0]:.8f}")
+    # the Ritz pairs are eigenpairs of the bfloat16 operator to the solver's
+    # tolerance; against the exact operator they hold to the bfloat16 product bar
+    assert e.info["nconv"] == 64 and e.info["max_residual"] <= 1e-5
+    assert dev_r <= TOL_BF16
+    assert abs(theta[0] - 1.0) <= TOL_BF16
+    assert np.abs(phi.T @ phi - np.eye(64)).max() <= 1e-5
 
 
 @pytest.mark.parametrize("counts", [(8,) * 6, (4,) * 10])

@@ -153,15 +153,20 @@ def test_deterministic(torus2_ref):
 
 
 def test_bf16_input_eigenpairs():
-    # the bfloat16 path rounds K to float16 (relative 2^-12): eigenvalues to 2e-3,
-    # the stated bfloat16-input tolerance; the solver itself converges to 1e-5
+    # the bfloat16 path rounds K to float16 (relative 2^-12), a fixed linear
+    # operator the solver converges on to its 1e-5 residual; against the dense
+    # float64 spectrum of the exact bfloat16 values the eigenvalues hold to the
+    # float32 eigenvalue bar, max(1e-5 |lambda|, 1e-6) (measured: 3e-7)
     s = inputs.stress(N=2048)
     beta = s.betas[0]
     sp = oe.spectrum(s.X_f64(), beta, 0.5, 16)
     dev = device()
     case("lanczos bf16 stress N=2048 k=8 b=8")
     e = fd.fd_block_lanczos(to_dev(s.X, dev), beta, 8, 8)
-    assert np.max(np.abs(np.asarray(e.evals) - sp.evals[:8])) <= 2e-3
+    dev_abs = np.abs(np.asarray(e.evals) - sp.evals[:8])
+    print(f"bf16 eigenvalue deviation: max abs {dev_abs.max():.2e}, max relative "
+          f"{(dev_abs / np.abs(sp.evals[:8])).max():.2e}")
+    assert np.all(dev_abs <= np.maximum(1e-5 * np.abs(sp.evals[:8]), 1e-6))
     assert max(e.residuals) <= 1e-5
 
 

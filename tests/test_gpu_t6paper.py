@@ -8,12 +8,16 @@ library's eigenpairs are compared with a dense float64 solve (eigenvalues
 one by one, the overlap score to 1e-4: the doublet is separated from the
 next pair by 0.037, so its span is stable to ~1e-4 rad under the operator's
 float32 error); at N = 65536 the score must exceed the N = 4096 value
-(recovery improves with sampling density, Sec. 3, figure c).
+(recovery improves with sampling density, Sec. 3, figure c).  The beta flow
+of Sec. 3 (k = 3 nontrivial modes, alpha = 1/2) is compared with the
+oracle's flow at N = 4096.
 """
 import numpy as np
 import pytest
 
+from flow_util import compare_probes, dyadic
 from gpu_util import case, device, to_dev, to_np
+from oracle import beta_flow as bf
 from oracle import diagnostics as od
 from oracle import eig as oe
 from paper_2609_38198_amd import _lib as fd
@@ -54,3 +58,29 @@ def test_t6_doublet_recovery_improves_with_n():
                             small.extra["theta"])
     assert s > s_small
     assert s > 0.99
+
+
+def test_t6_flow_like_the_oracle():
+    # Sec. 3's solve at N = 4096: the beta flow with k = 3 nontrivial modes
+    # (k = 4 with the Perron pair), alpha = 1/2, from beta_0 of eq. beta0; the
+    # library's probes, exit and achieved bandwidth against the oracle's flow
+    # on dense float64 probes, and the doublet score at beta_x against a dense
+    # solve there
+    w = inputs.torus6_paper(4096)
+    X64 = w.X.astype(np.float64)
+    k, b = 4, 8
+    case("t6 paper beta flow N=4096 k=4 b=8")
+    got = fd.fd_beta_flow(to_dev(w.X, device()), k, b, alpha=0.5,
+                          fopts=fd.flow_default_opts(max_probes=12))
+    ref = bf.flow(bf.dense_probe(X64, 0.5, k), w.N, bf.beta0(X64), max_probes=12)
+    assert got.reason == ref.reason
+    compare_probes(dyadic(got), ref)
+    assert got.beta_x == pytest.approx(ref.beta_x, rel=1e-3)
+    dense = oe.spectrum(X64, got.beta_x, 0.5, k)
+    ev = np.asarray(got.evals)
+    assert np.all(np.abs(ev - dense.evals) <= np.maximum(1e-5 * np.abs(dense.evals), 1e-6))
+    s_gpu = doublet_score(to_np(got.psi), w.extra["theta"])
+    s_ref = doublet_score(dense.psi, w.extra["theta"])
+    print(f"t6 flow N=4096: beta_x {got.beta_x:.5f} ({got.reason}), score {s_gpu:.5f} "
+          f"(dense {s_ref:.5f}); the paper's one-GPU run: beta_x 0.495, score 0.985")
+    assert abs(s_gpu - s_ref) <= 1e-4
