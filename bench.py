@@ -238,7 +238,7 @@ def continuation_leg(fd, torch, dev) -> dict:
                       for n, beta, i in zip(ns, bs, lad.info)]}
 
 
-def stress_leg(fd, torch, dev) -> dict:
+def stress_leg(fd, torch, dev, iterations: int = 20) -> dict:
     """bfloat16 X, N = 2^21 in R^64: fused product throughput and 20 block-Lanczos iterations."""
     from paper_2609_38198_amd import inputs
     log("stress leg: generating N=2^21 x 64 bf16")
@@ -263,20 +263,24 @@ def stress_leg(fd, torch, dev) -> dict:
     fd.fd_profile_enable(False)
     pms, pn = fd.fd_profile_read(fd.FD_KERNEL_PRODUCT)
     del ws, Y
-    log(f"stress leg: product {tp:.3f} s; 20 block-Lanczos iterations")
-    o = fd.default_opts(max_matvecs=20, max_basis_blocks=16, keep=64, verbose=1)
+    avg = pms * 1e-3 / max(pn, 1)
+    rec = {"workload": f"stress bf16 N={N} D={D} b={b} beta={beta:.5f}",
+           "product_s": tp, "product_kernel_s": avg,
+           "pair_cols_per_s": float(N) * N * b / avg,
+           "exp_per_s": float(N) * N / avg}
+    if iterations <= 0:
+        return rec
+    log(f"stress leg: product {tp:.3f} s; {iterations} block-Lanczos iterations")
+    o = fd.default_opts(max_matvecs=iterations, max_basis_blocks=16, keep=64, verbose=1)
     t0 = time.perf_counter()
     e = fd.fd_block_lanczos(X, beta, 64, b, opts=o, allow_not_converged=True)
     torch.cuda.synchronize()
     tl = time.perf_counter() - t0
-    avg = pms * 1e-3 / max(pn, 1)
-    return {"workload": f"stress bf16 N={N} D={D} b={b} beta={beta:.5f}",
-            "product_s": tp, "product_kernel_s": avg,
-            "pair_cols_per_s": float(N) * N * b / avg,
-            "exp_per_s": float(N) * N / avg,
-            "lanczos_20_iters_s": tl, "block_matvecs": e.info["block_matvecs"],
-            "nconv": e.info["nconv"], "max_residual": e.info["max_residual"],
-            "evals_head": e.evals[:4], "evals_tail": e.evals[-2:]}
+    rec.update({"lanczos_iters_s": tl, "iterations_cap": iterations,
+                "block_matvecs": e.info["block_matvecs"], "nconv": e.info["nconv"],
+                "max_residual": e.info["max_residual"], "evals_head": e.evals[:4],
+                "evals_tail": e.evals[-2:]})
+    return rec
 
 
 # The paper's XGEMM timings for one raw kernel application K V on its T^6
@@ -411,7 +415,11 @@ def main() -> int:
     ap.add_argument("--lanczos", action="store_true",
                     help="time to the top 16 eigenpairs on the 2-torus (N = 2048)")
     ap.add_argument("--continuation", action="store_true")
-    ap.add_argument("--stress", action="store_true")
+    ap.add_argument("--stress", action="store_true",
+                    help="bfloat16 stress set (N = 2^21, D = 64, b = 64): product throughput and "
+                         "block-Lanczos iterations")
+    ap.add_argument("--stress-iters", type=int, default=20,
+                    help="block-Lanczos iterations of the stress leg (0: the product only)")
     ap.add_argument("--paper-t6", action="store_true",
                     help="raw K V on the paper's T^6 set-up (D=32, beta=1, b=1 and 8) beside "
                          "the paper's own timings")
@@ -549,7 +557,7 @@ def main() -> int:
     if args.continuation:
         rec["continuation"] = continuation_leg(fd, torch, dev)
     if args.stress:
-        rec["stress"] = stress_leg(fd, torch, dev)
+        rec["stress"] = stress_leg(fd, torch, dev, args.stress_iters)
     if args.paper_t6:
         rec["paper_t6"] = paper_t6_leg(fd, torch, dev)
     if args.paper_t6_flow:

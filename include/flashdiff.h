@@ -24,9 +24,18 @@
  *  - Every function returns an fd_status and never throws.  On a non-OK status
  *    fd_last_error() returns a thread-local message; output contents are then
  *    unspecified unless the status says otherwise.
- *  - X should be centred (subtract the column mean): the method is stated for
- *    centred observations (Sec. 2.1, eq. rbf_gram) and the Gram-form
- *    evaluation loses accuracy on data far from the origin.  Not enforced.
+ *  - Centring: the method is stated for centred observations (Sec. 2.1, eq.
+ *    rbf_gram), and the Gram-form evaluation loses accuracy far from the
+ *    origin.  For float32 X the library centres on the device (column means
+ *    in float64, subtracted before the exponent contraction; the kernel is
+ *    translation invariant, so results are unchanged up to rounding);
+ *    bfloat16 X is used as given and should be centred by the caller.
+ *  - Accuracy envelope (float32 X): K V to 1e-5 relative (measured 1e-7 to
+ *    4e-6) while B = beta log2(e) max_i ||x_i - mean||^2 <= 200; above 64 the
+ *    feature widths whose fast exponent layout drops the third offset piece
+ *    (13 < D <= 30, 32 < D <= 62) switch to one that keeps it.  Beyond
+ *    B = 200 the dropped fourth-order piece products can reach the 1e-5 bar
+ *    (1.1e-5 measured at B = 400, D = 30).
  *  - Non-finite X: every entry point scans X on the device first.  The
  *    asynchronous ones (fd_kernel_matmul, fd_kernel_matmul_noalloc, fd_degree,
  *    fd_degree_dyadic) then fill all their outputs with NaN; the eigensolver,

@@ -146,6 +146,7 @@ ProductWs carve_product(Arena& a, int64_t Nr, int64_t Nc, int64_t D, int b) {
   w.part = a.fspan(part_rows_bound(w.rows.npad, Nc) * w.plan.ncb * 16);
   w.tmp = a.fspan(size_t(Nr));
   w.flag = a.take<int>(1);
+  w.centre = carve_centre(a, Nc);
   return w;
 }
 
@@ -165,6 +166,7 @@ static ProductWs carve_product_exact(Arena& a, int64_t Nr, int64_t Nc, int64_t D
   w.part = a.fspan(b == 1 ? part_row : part_prod);
   w.tmp = a.fspan(size_t(Nr));
   w.flag = a.take<int>(1);
+  w.centre = carve_centre(a, Nc);
   return w;
 }
 
@@ -259,6 +261,7 @@ DegreeWs carve_degree(Arena& a, int64_t N, int64_t D) {
   w.part = a.fspan(std::max(part_rows_bound(w.rows.npad, N), sym_part_rows(w.rows.npad, SYM_NIB)));
   w.colfix = a.take<unsigned long long>(size_t(w.rows.npad));
   w.flag = a.take<int>(1);
+  w.centre = carve_centre(a, N);
   return w;
 }
 
@@ -266,8 +269,9 @@ void degree_run(DegreeWs& w, const void* X, fd_dtype xt, int64_t N, int64_t D, i
                 double beta, double alpha, float* q, float* d, float* s, double* s_off,
                 bool pack, hipStream_t stream) {
   if (pack) {
-    launch_pack_points(X, xt, N, D, ldx, beta, true, w.rows, stream);
-    launch_pack_points(X, xt, N, D, ldx, beta, false, w.cols, stream);
+    launch_centre(X, xt, N, D, ldx, w.centre, stream);
+    launch_pack_points(X, xt, N, D, ldx, beta, true, w.rows, &w.centre, stream);
+    launch_pack_points(X, xt, N, D, ldx, beta, false, w.cols, &w.centre, stream);
   }
   float* qq = q != nullptr ? q : w.q;
   if (rowsum_sym_applies(w.rows, w.cols, true, w.colfix)) {
@@ -311,8 +315,9 @@ void degree_run_dyadic(DegreeWs& w, const void* X, fd_dtype xt, int64_t N, int64
                        float* s, double* s_off, hipStream_t stream) {
   auto at = [N](float* v, int l) { return v != nullptr ? v + int64_t(l) * N : nullptr; };
   auto beta_of = [beta0](int l) { return std::ldexp(beta0, l); };
-  launch_pack_points(X, xt, N, D, ldx, beta_of(0), true, w.rows, stream);
-  launch_pack_points(X, xt, N, D, ldx, beta_of(0), false, w.cols, stream);
+  launch_centre(X, xt, N, D, ldx, w.centre, stream);
+  launch_pack_points(X, xt, N, D, ldx, beta_of(0), true, w.rows, &w.centre, stream);
+  launch_pack_points(X, xt, N, D, ldx, beta_of(0), false, w.cols, &w.centre, stream);
   if (alpha == 0.0 || !rowsum_sym_applies(w.rows, w.cols, true, w.colfix)) {
     // no weighted pass to carry the squares (alpha = 0), or not the symmetric
     // path: fd_degree's passes, level by level
@@ -331,8 +336,8 @@ void degree_run_dyadic(DegreeWs& w, const void* X, fd_dtype xt, int64_t N, int64
   launch_zero_u64(w.sq_colfix, w.rows.npad, stream);
   for (int l = 0; l < nb; ++l) {
     if (l > 0) {
-      launch_pack_points(X, xt, N, D, ldx, beta_of(l), true, w.rows, stream);
-      launch_pack_points(X, xt, N, D, ldx, beta_of(l), false, w.cols, stream);
+      launch_pack_points(X, xt, N, D, ldx, beta_of(l), true, w.rows, &w.centre, stream);
+      launch_pack_points(X, xt, N, D, ldx, beta_of(l), false, w.cols, &w.centre, stream);
     }
     if (l + 1 == nb) {
       const SymPass p2 = launch_rowsum_sym_pass(w.plan, w.rows, w.cols, w.wp, w.part, w.colfix,
@@ -455,8 +460,11 @@ fd_status fd_kernel_matmul(const void* Xr, int64_t Nr, const void* Xc, int64_t N
     hipStream_t st = static_cast<hipStream_t>(stream);
     launch_scan_nonfinite(Xr, xt, Nr, D, ldx, w.flag, true, st);
     if (Xc != Xr) launch_scan_nonfinite(Xc, xt, Nc, D, ldx, w.flag, false, st);
-    launch_pack_points(Xr, xt, Nr, D, ldx, beta, true, w.rows, st);
-    launch_pack_points(Xc, xt, Nc, D, ldx, beta, false, w.cols, st);
+    // one centre for both sets: the column set's mean, the radius over both
+    launch_centre(Xc, xt, Nc, D, ldx, w.centre, st);
+    if (Xr != Xc || Nr > Nc) launch_radius_more(Xr, xt, Nr, D, ldx, w.centre, st);
+    launch_pack_points(Xr, xt, Nr, D, ldx, beta, true, w.rows, &w.centre, st);
+    launch_pack_points(Xc, xt, Nc, D, ldx, beta, false, w.cols, &w.centre, st);
     // same base pointer and ldx: index i names the same point in both sets
     const bool diag = (Xr == Xc);
     product_apply(w, sl, sr, V, ldv, int(b), Y, ldy, diag, st);
@@ -489,8 +497,11 @@ fd_status fd_kernel_matmul_noalloc(const void* Xr, int64_t Nr, const void* Xc, i
     hipStream_t st = static_cast<hipStream_t>(stream);
     launch_scan_nonfinite(Xr, xt, Nr, D, ldx, w.flag, true, st);
     if (Xc != Xr) launch_scan_nonfinite(Xc, xt, Nc, D, ldx, w.flag, false, st);
-    launch_pack_points(Xr, xt, Nr, D, ldx, beta, true, w.rows, st);
-    launch_pack_points(Xc, xt, Nc, D, ldx, beta, false, w.cols, st);
+    // one centre for both sets: the column set's mean, the radius over both
+    launch_centre(Xc, xt, Nc, D, ldx, w.centre, st);
+    if (Xr != Xc || Nr > Nc) launch_radius_more(Xr, xt, Nr, D, ldx, w.centre, st);
+    launch_pack_points(Xr, xt, Nr, D, ldx, beta, true, w.rows, &w.centre, st);
+    launch_pack_points(Xc, xt, Nc, D, ldx, beta, false, w.cols, &w.centre, st);
     const bool diag = (Xr == Xc);
     product_apply(w, sl, sr, V, ldv, int(b), Y, ldy, diag, st);
     launch_poison(w.flag, Y, Nr, b, ldy, st);

@@ -99,7 +99,40 @@ struct PointPack {
   int rid = -1;       // float32: split-exponent recipe
   bool row_side = false;
   double beta = 0.0;  // bandwidth the pack was made for
+  // float32 packs of a D whose short layout drops the third offset piece
+  // (13 < D <= 30, 32 < D <= 62): the layout with all three pieces too (xp2,
+  // recipe rid2), and the device word the kernels choose between them by
+  // (max ||x - mu||^2 as float64 bits); variant 1 / 2 = this pack is the
+  // short / the full-offset one, 0 = no choice.
+  FSpan xp2;
+  int rid2 = -1;
+  const unsigned long long* r2max = nullptr;
+  int variant = 0;
 };
+
+// Centring of a float32 point set (the kernel is translation invariant, and
+// the Gram-form exponent is most accurate around the mean): column means mu
+// (float64) and the largest squared distance of a point from them.
+struct CentreWs {
+  double* part = nullptr;             // nblk x D column partial sums
+  double* mu = nullptr;               // D
+  unsigned long long* r2max = nullptr;  // float64 bits of max ||x - mu||^2
+  int nblk = 0;
+};
+CentreWs carve_centre(Arena& a, int64_t n);
+// mu of X[0:n] and r2max over it (float32 X; a no-op for bfloat16).
+void launch_centre(const void* X, fd_dtype xt, int64_t n, int64_t D, int64_t ldx,
+                   const CentreWs& c, hipStream_t stream);
+// r2max also over X2[0:n2], centred on the same mu.
+void launch_radius_more(const void* X2, fd_dtype xt, int64_t n2, int64_t D, int64_t ldx,
+                        const CentreWs& c, hipStream_t stream);
+
+// Exponent budget of the short split layouts: above beta log2(e) max ||x - mu||^2
+// = 64 the kernels take the layout that keeps all three offset pieces (the
+// dropped third piece is a coherent row / column scale error of up to
+// 2^-22 ln 2 times that, 3.7e-6 relative at 64, against measured K V errors of
+// 2.8e-6 at 50 and 5.4e-6 at 100 on the molecule-like set).
+constexpr double EXP_BUDGET = 64.0;
 
 // Floats per point of a pack region (large enough for either pack kind).
 int pack_floats_per_point(int64_t D);
@@ -124,7 +157,8 @@ PointPack carve_pack(Arena& a, int64_t n, int dp, int64_t pad);
 
 // Launchers (enqueue on stream; throw Error on failure).
 void launch_pack_points(const void* X, fd_dtype xt, int64_t n, int64_t D, int64_t ldx,
-                        double beta, bool row_side, PointPack& out, hipStream_t stream);
+                        double beta, bool row_side, PointPack& out, const CentreWs* centre,
+                        hipStream_t stream);
 void launch_pack_w(const float* w, int64_t n, int64_t npad, FSpan wp, hipStream_t stream);
 // Weight pack of sr * v for one column v (row stride ldv; sr may be NULL).
 void launch_pack_wv(const float* v, int64_t ldv, const float* sr, int64_t n, int64_t npad,

@@ -11,6 +11,7 @@ struct ProductWs {
   FSpan vp, vscale, part;
   FSpan tmp;  // one float per row: the single-column product's row sums
   int* flag = nullptr;  // set when a point set holds a non-finite value
+  CentreWs centre;      // common centre of the row and column sets
   KVPlan plan;
 };
 
@@ -25,6 +26,7 @@ struct DegreeWs {
   FSpan sq_part;                          // squared-kernel row partials (dyadic levels)
   unsigned long long* sq_colfix = nullptr;
   int* flag = nullptr;  // set when X holds a non-finite value
+  CentreWs centre;      // centre of X
   KVPlan plan;
 };
 

@@ -328,9 +328,12 @@ __global__ __launch_bounds__(256) void pack_hx_point_kernel(const float* __restr
                                                             int D, int64_t ldx, double scale,
                                                             double neg_bl, double shift,
                                                             int64_t npad,
-                                                            uintx4* __restrict__ out) {
+                                                            uintx4* __restrict__ out,
+                                                            const double* __restrict__ mu,
+                                                            HxGate gate) {
   constexpr int M = HX_TABLE[RID].maxd;
   constexpr int NCH = ROW ? HX_TABLE[RID].nb : HX_TABLE[RID].nc;
+  if (hx_gate_closed(gate)) return;
   const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
   if (i >= npad) return;
   const bool real = i < n;
@@ -343,8 +346,10 @@ __global__ __launch_bounds__(256) void pack_hx_point_kernel(const float* __restr
 #pragma unroll
   for (int f = 0; f < M; ++f) {
     const bool use = real && f < D;
-    if (use) r += double(xv[f]) * double(xv[f]);
-    pieces3(use ? scale * double(xv[f]) : 0.0, px[f]);
+    // centred on mu in float64 (translation invariance of the kernel)
+    const double v = use ? double(xv[f]) - (mu != nullptr ? mu[min(f, D - 1)] : 0.0) : 0.0;
+    r += v * v;
+    pieces3(scale * v, px[f]);
   }
   float pa[3];
   pieces3(real ? neg_bl * r + shift : -65504.0, pa);
@@ -465,9 +470,10 @@ __attribute__((amdgpu_waves_per_eu(hx_waves<RID, NCB, NIB>()))) void product_hx_
     const uintx4* __restrict__ xc, const VSplit* __restrict__ vp, const uintx4* __restrict__ xr,
     int64_t nrt, int64_t njp, int64_t jp_per_split, int diag, float m1,
     const float* __restrict__ colscale, const float* __restrict__ sl, float* __restrict__ Y,
-    int64_t ldy, int64_t Nr, int b, float* __restrict__ part, int64_t nrpad) {
+    int64_t ldy, int64_t Nr, int b, float* __restrict__ part, int64_t nrpad, HxGate gate) {
   constexpr int NB = Hx<RID>::nb;
   __shared__ floatx4 tot[4][NIB][NCB][64];
+  if (hx_gate_closed(gate)) return;
   const int lane = threadIdx.x & 63;
   // the wave index is uniform: make the row-tile range (and the diagonal
   // tests on it) scalar
@@ -609,8 +615,9 @@ __global__ __launch_bounds__(WG_THREADS)
 __attribute__((amdgpu_waves_per_eu(hx_waves<RID, 0, NIB>()))) void rowsum_hx_kernel(
     const uintx4* __restrict__ xc, const floatx4* __restrict__ wp, const uintx4* __restrict__ xr,
     int64_t nrt, int64_t njb, int64_t jb_per_split, int diag, float* __restrict__ out,
-    int64_t Nr, float* __restrict__ part, int64_t nrpad) {
+    int64_t Nr, float* __restrict__ part, int64_t nrpad, HxGate gate) {
   constexpr int NB = Hx<RID>::nb;
+  if (hx_gate_closed(gate)) return;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wr = xcd_remap(blockIdx.x, gridDim.x);
@@ -805,8 +812,10 @@ __attribute__((amdgpu_waves_per_eu(hx_waves<RID, 0, NIB>()))) void rowsum_sym_hx
     const uintx4* __restrict__ xc, const floatx4* __restrict__ wp, const uintx4* __restrict__ xr,
     int64_t nblk, int64_t njb, int64_t jb_per_split, int64_t nsplit, float* __restrict__ part,
     int64_t nrpad, unsigned long long* __restrict__ colfix, double fix_scale,
-    float* __restrict__ part2, unsigned long long* __restrict__ colfix2, double fix_scale2) {
+    float* __restrict__ part2, unsigned long long* __restrict__ colfix2, double fix_scale2,
+    HxGate gate) {
   static_assert(!(SQ && UNIT), "squared sums ride on a weighted pass");
+  if (hx_gate_closed(gate)) return;
   constexpr int NB = Hx<RID>::nb;
   constexpr int NC = Hx<RID>::nc;
   constexpr int BT = 4 * NIB;  // tiles per block
@@ -1019,13 +1028,12 @@ void product_hx_launch(const KVPlan& p, const PointPack& rows, const PointPack& 
                        const float* vp, const float* colscale, bool diag, const float* sl,
                        float* Y, int64_t ldy, int b, float* part, hipStream_t stream) {
   const unsigned grid = unsigned(p.nrt * p.nsplit);
-  ProfScope prof(FD_KERNEL_PRODUCT, stream);
   hipLaunchKernelGGL((product_hx_kernel<RID, NCB, NIB>), dim3(grid), dim3(WG_THREADS), 0, stream,
                      reinterpret_cast<const uintx4*>(cols.xp.p),
                      reinterpret_cast<const VSplit*>(vp),
                      reinterpret_cast<const uintx4*>(rows.xp.p), p.nrt, ceil_div(p.njb, 2),
                      p.jb_per_split / 2, int(diag), -1.0f, colscale, sl, Y, ldy, rows.n, b, part,
-                     rows.npad);
+                     rows.npad, gate_of(rows));
   FD_LAUNCH_CHECK();
 }
 
@@ -1061,12 +1069,11 @@ template <int RID, int NIB, bool UNIT>
 void rowsum_hx_launch(const KVPlan& p, const PointPack& rows, const PointPack& cols,
                       const float* wp, bool diag, float* out, float* part, hipStream_t stream) {
   const unsigned grid = unsigned(p.nrt * p.nsplit);
-  ProfScope prof(FD_KERNEL_ROWSUM, stream);
   hipLaunchKernelGGL((rowsum_hx_kernel<RID, NIB, UNIT>), dim3(grid), dim3(WG_THREADS), 0, stream,
                      reinterpret_cast<const uintx4*>(cols.xp.p),
                      reinterpret_cast<const floatx4*>(wp),
                      reinterpret_cast<const uintx4*>(rows.xp.p), p.nrt, p.njb, p.jb_per_split,
-                     int(diag), out, rows.n, part, rows.npad);
+                     int(diag), out, rows.n, part, rows.npad, gate_of(rows));
   FD_LAUNCH_CHECK();
 }
 
@@ -1091,13 +1098,12 @@ void rowsum_sym_hx_launch(const KVPlan& p, const PointPack& rows, const PointPac
                           const float* wp, float* part, unsigned long long* colfix,
                           double fix_scale, const SymSquares& sq, hipStream_t stream) {
   const unsigned grid = unsigned(p.nrt * p.nsplit);
-  ProfScope prof(FD_KERNEL_ROWSUM, stream);
   hipLaunchKernelGGL((rowsum_sym_hx_kernel<RID, NIB, UNIT, SQ>), dim3(grid), dim3(WG_THREADS), 0,
                      stream, reinterpret_cast<const uintx4*>(cols.xp.p),
                      reinterpret_cast<const floatx4*>(wp),
                      reinterpret_cast<const uintx4*>(rows.xp.p), p.nrt, p.njb, p.jb_per_split,
                      int64_t(p.nsplit), part, rows.npad, colfix, fix_scale, sq.part, sq.colfix,
-                     sq.fix_scale);
+                     sq.fix_scale, gate_of(rows));
   FD_LAUNCH_CHECK();
 }
 
@@ -1142,6 +1148,10 @@ void check_hx(const KVPlan& p, const PointPack& rows, const PointPack& cols) {
 
 }  // namespace
 
+static_assert(HX_TABLE[4].order == 3 && HX_TABLE[6].order == 3 && HX_TABLE[4].maxd >= 30 &&
+                  HX_TABLE[6].maxd >= 62,
+              "full-offset recipes must serve the short recipes' feature widths");
+
 int hx_recipe_for(int64_t D) {
   for (int r = 0; r < HX_RECIPES; ++r)
     if (D >= 1 && D <= HX_TABLE[r].maxd) return r;
@@ -1150,64 +1160,116 @@ int hx_recipe_for(int64_t D) {
 int hx_col_chunks(int rid) { return HX_TABLE[rid].nc; }
 int hx_row_chunks(int rid) { return HX_TABLE[rid].nb; }
 
-void launch_pack_points_hx(const float* X, int64_t n, int64_t D, int64_t ldx, double beta,
-                           bool row_side, PointPack& out, hipStream_t stream) {
-  const int rid = hx_recipe_for(D);
-  FD_REQUIRE(rid >= 0, FD_ERR_UNSUPPORTED, "feature dimension above 64");
-  const HxRecipe& R = HX_TABLE[rid];
-  const int nch = row_side ? R.nb : R.nc;
-  FD_REQUIRE(out.npad % (2 * TILE) == 0 && out.npad >= n, FD_ERR_INVALID_ARG,
-             "internal: bad split pack geometry");
-  const int64_t ntiles = out.npad / TILE;
-  check_span(out.xp, size_t(ntiles) * nch * 64 * 4, "split point pack");
+int hx_full_offset_recipe(int rid) {
+  // short recipes that drop the third offset piece -> the next recipe up,
+  // which keeps all three (checked at compile time below)
+  return rid == 3 ? 4 : rid == 5 ? 6 : -1;
+}
+
+template <int RID, bool ROW>
+static void pack_hx_launch(const float* X, int64_t n, int64_t D, int64_t ldx, double beta,
+                           FSpan xp, int64_t npad, const double* mu, HxGate gate,
+                           hipStream_t stream) {
+  const HxRecipe& R = HX_TABLE[RID];
+  const int nch = ROW ? R.nb : R.nc;
+  check_span(xp, size_t(npad / TILE) * nch * 64 * 4, "split point pack");
+  FD_REQUIRE(D <= R.maxd, FD_ERR_INVALID_ARG, "internal: recipe too narrow for D");
   const double bl = beta * LOG2E;
   // s = 2^e balances |x'| = s|x| and |b'| = 2 beta log2(e) |x| / s
   int e = 0;
   if (beta > 0.0) e = std::clamp(int(std::lround(0.5 * std::log2(2.0 * bl))), -12, 12);
   const double s = std::ldexp(1.0, e);
-  const double scale = row_side ? 2.0 * bl / s : s;
-  const double shift = row_side ? double(SHIFT) : 0.0;
-  uintx4* xp = reinterpret_cast<uintx4*>(out.xp.p);
-  const dim3 grid(blocks_for(out.npad, 256));
-  auto go = [&](auto rid_, auto row_) {
-    constexpr int RID = decltype(rid_)::value;
-    constexpr bool ROW = decltype(row_)::value;
-    hipLaunchKernelGGL((pack_hx_point_kernel<RID, ROW>), grid, dim3(256), 0, stream, X, n, int(D),
-                       ldx, scale, -bl, shift, out.npad, xp);
-  };
-  auto side = [&](auto rid_) {
-    if (row_side)
-      go(rid_, std::true_type{});
-    else
-      go(rid_, std::false_type{});
-  };
-  switch (rid) {
-    case 0: side(std::integral_constant<int, 0>{}); break;
-    case 1: side(std::integral_constant<int, 1>{}); break;
-    case 2: side(std::integral_constant<int, 2>{}); break;
-    case 3: side(std::integral_constant<int, 3>{}); break;
-    case 4: side(std::integral_constant<int, 4>{}); break;
-    case 5: side(std::integral_constant<int, 5>{}); break;
-    default: side(std::integral_constant<int, 6>{}); break;
-  }
+  const double scale = ROW ? 2.0 * bl / s : s;
+  const double shift = ROW ? double(SHIFT) : 0.0;
+  hipLaunchKernelGGL((pack_hx_point_kernel<RID, ROW>), dim3(blocks_for(npad, 256)), dim3(256), 0,
+                     stream, X, n, int(D), ldx, scale, -bl, shift, npad,
+                     reinterpret_cast<uintx4*>(xp.p), mu, gate);
   FD_LAUNCH_CHECK();
+}
+
+template <bool ROW>
+static void pack_hx_rid(int rid, const float* X, int64_t n, int64_t D, int64_t ldx, double beta,
+                        FSpan xp, int64_t npad, const double* mu, HxGate gate,
+                        hipStream_t stream) {
+  switch (rid) {
+    case 0: return pack_hx_launch<0, ROW>(X, n, D, ldx, beta, xp, npad, mu, gate, stream);
+    case 1: return pack_hx_launch<1, ROW>(X, n, D, ldx, beta, xp, npad, mu, gate, stream);
+    case 2: return pack_hx_launch<2, ROW>(X, n, D, ldx, beta, xp, npad, mu, gate, stream);
+    case 3: return pack_hx_launch<3, ROW>(X, n, D, ldx, beta, xp, npad, mu, gate, stream);
+    case 4: return pack_hx_launch<4, ROW>(X, n, D, ldx, beta, xp, npad, mu, gate, stream);
+    case 5: return pack_hx_launch<5, ROW>(X, n, D, ldx, beta, xp, npad, mu, gate, stream);
+    case 6: return pack_hx_launch<6, ROW>(X, n, D, ldx, beta, xp, npad, mu, gate, stream);
+  }
+  throw Error{FD_ERR_UNSUPPORTED, "feature dimension above 64"};
+}
+
+void launch_pack_points_hx(const float* X, int64_t n, int64_t D, int64_t ldx, double beta,
+                           bool row_side, PointPack& out, const CentreWs* centre,
+                           hipStream_t stream) {
+  const int rid = hx_recipe_for(D);
+  FD_REQUIRE(rid >= 0, FD_ERR_UNSUPPORTED, "feature dimension above 64");
+  FD_REQUIRE(out.npad % (2 * TILE) == 0 && out.npad >= n, FD_ERR_INVALID_ARG,
+             "internal: bad split pack geometry");
+  const double* mu = centre != nullptr ? centre->mu : nullptr;
+  const int wide = centre != nullptr ? hx_full_offset_recipe(rid) : -1;
   out.rid = rid;
   out.row_side = row_side;
+  out.rid2 = wide;
+  out.variant = wide >= 0 ? 1 : 0;
+  out.r2max = wide >= 0 ? centre->r2max : nullptr;
+  const HxGate g1{out.r2max, beta * LOG2E, out.variant};
+  if (row_side)
+    pack_hx_rid<true>(rid, X, n, D, ldx, beta, out.xp, out.npad, mu, g1, stream);
+  else
+    pack_hx_rid<false>(rid, X, n, D, ldx, beta, out.xp, out.npad, mu, g1, stream);
+  if (wide >= 0) {
+    const HxGate g2{out.r2max, beta * LOG2E, 2};
+    if (row_side)
+      pack_hx_rid<true>(wide, X, n, D, ldx, beta, out.xp2, out.npad, mu, g2, stream);
+    else
+      pack_hx_rid<false>(wide, X, n, D, ldx, beta, out.xp2, out.npad, mu, g2, stream);
+  }
+}
+
+// The second layout of a pack pair (see PointPack): same geometry, the
+// full-offset recipe's chunks.
+static PointPack full_offset_view(const PointPack& pk) {
+  PointPack q = pk;
+  q.xp = pk.xp2;
+  q.rid = pk.rid2;
+  q.variant = 2;
+  return q;
+}
+
+// Runs `go` on the packs as filled and, when they hold both layouts, again on
+// the full-offset one: each launch reads the exponent-budget word and only
+// the matching one works.  The pair counts as one launch for the timing hooks.
+template <class Go>
+static void dual_dispatch(const PointPack& rows, const PointPack& cols, fd_kernel_kind kind,
+                          hipStream_t stream, Go&& go) {
+  FD_REQUIRE((rows.rid2 >= 0) == (cols.rid2 >= 0) && rows.rid2 == cols.rid2 &&
+                 rows.variant == cols.variant && rows.r2max == cols.r2max,
+             FD_ERR_INVALID_ARG, "internal: pack layouts do not match");
+  ProfScope prof(kind, stream);
+  go(rows, cols);
+  if (rows.rid2 >= 0) go(full_offset_view(rows), full_offset_view(cols));
 }
 
 void launch_product_hx(const KVPlan& p, const PointPack& rows, const PointPack& cols,
                        const float* vp, const float* cs, bool diag, const float* sl, float* Y,
                        int64_t ldy, int b, float* part, hipStream_t stream) {
-  check_hx(p, rows, cols);
-  switch (rows.rid) {
-    case 0: return product_hx_ncb<0>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
-    case 1: return product_hx_ncb<1>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
-    case 2: return product_hx_ncb<2>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
-    case 3: return product_hx_ncb<3>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
-    case 4: return product_hx_ncb<4>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
-    case 5: return product_hx_ncb<5>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
-    case 6: return product_hx_ncb<6>(p, rows, cols, vp, cs, diag, sl, Y, ldy, b, part, stream);
-  }
+  dual_dispatch(rows, cols, FD_KERNEL_PRODUCT, stream, [&](const PointPack& r, const PointPack& c) {
+    check_hx(p, r, c);
+    switch (r.rid) {
+      case 0: return product_hx_ncb<0>(p, r, c, vp, cs, diag, sl, Y, ldy, b, part, stream);
+      case 1: return product_hx_ncb<1>(p, r, c, vp, cs, diag, sl, Y, ldy, b, part, stream);
+      case 2: return product_hx_ncb<2>(p, r, c, vp, cs, diag, sl, Y, ldy, b, part, stream);
+      case 3: return product_hx_ncb<3>(p, r, c, vp, cs, diag, sl, Y, ldy, b, part, stream);
+      case 4: return product_hx_ncb<4>(p, r, c, vp, cs, diag, sl, Y, ldy, b, part, stream);
+      case 5: return product_hx_ncb<5>(p, r, c, vp, cs, diag, sl, Y, ldy, b, part, stream);
+      case 6: return product_hx_ncb<6>(p, r, c, vp, cs, diag, sl, Y, ldy, b, part, stream);
+    }
+  });
 }
 
 void launch_rowsum_sym_hx(const KVPlan& p, const PointPack& rows, const PointPack& cols,
@@ -1219,33 +1281,37 @@ void launch_rowsum_sym_hx(const KVPlan& p, const PointPack& rows, const PointPac
   FD_REQUIRE((p.nib == 4 || p.nib == 8) && p.nrt * 4 * p.nib * TILE == rows.npad &&
                  p.njb == ceil_div(cols.n, TILE),
              FD_ERR_INVALID_ARG, "internal: symmetric row-sum plan");
-  const HxRecipe& R = HX_TABLE[rows.rid];
-  check_span(rows.xp, size_t(rows.npad / TILE) * R.nb * 64 * 4, "split row pack");
-  check_span(cols.xp, size_t(round_up(p.njb, 2)) * R.nc * 64 * 4, "split column pack");
-  switch (rows.rid) {
-    case 0: return rowsum_sym_hx_u<0>(p, rows, cols, wp, part, colfix, fix_scale, sq, stream);
-    case 1: return rowsum_sym_hx_u<1>(p, rows, cols, wp, part, colfix, fix_scale, sq, stream);
-    case 2: return rowsum_sym_hx_u<2>(p, rows, cols, wp, part, colfix, fix_scale, sq, stream);
-    case 3: return rowsum_sym_hx_u<3>(p, rows, cols, wp, part, colfix, fix_scale, sq, stream);
-    case 4: return rowsum_sym_hx_u<4>(p, rows, cols, wp, part, colfix, fix_scale, sq, stream);
-    case 5: return rowsum_sym_hx_u<5>(p, rows, cols, wp, part, colfix, fix_scale, sq, stream);
-    case 6: return rowsum_sym_hx_u<6>(p, rows, cols, wp, part, colfix, fix_scale, sq, stream);
-  }
+  dual_dispatch(rows, cols, FD_KERNEL_ROWSUM, stream, [&](const PointPack& r, const PointPack& c) {
+    const HxRecipe& R = HX_TABLE[r.rid];
+    check_span(r.xp, size_t(r.npad / TILE) * R.nb * 64 * 4, "split row pack");
+    check_span(c.xp, size_t(round_up(p.njb, 2)) * R.nc * 64 * 4, "split column pack");
+    switch (r.rid) {
+      case 0: return rowsum_sym_hx_u<0>(p, r, c, wp, part, colfix, fix_scale, sq, stream);
+      case 1: return rowsum_sym_hx_u<1>(p, r, c, wp, part, colfix, fix_scale, sq, stream);
+      case 2: return rowsum_sym_hx_u<2>(p, r, c, wp, part, colfix, fix_scale, sq, stream);
+      case 3: return rowsum_sym_hx_u<3>(p, r, c, wp, part, colfix, fix_scale, sq, stream);
+      case 4: return rowsum_sym_hx_u<4>(p, r, c, wp, part, colfix, fix_scale, sq, stream);
+      case 5: return rowsum_sym_hx_u<5>(p, r, c, wp, part, colfix, fix_scale, sq, stream);
+      case 6: return rowsum_sym_hx_u<6>(p, r, c, wp, part, colfix, fix_scale, sq, stream);
+    }
+  });
 }
 
 void launch_rowsum_hx(const KVPlan& p, const PointPack& rows, const PointPack& cols,
                       const float* wp, bool diag, float* out, float* part, hipStream_t stream) {
-  check_hx(p, rows, cols);
   FD_REQUIRE(p.nib == 4 || p.nib == 8, FD_ERR_INVALID_ARG, "internal: row-sum plan");
-  switch (rows.rid) {
-    case 0: return rowsum_hx_u<0>(p, rows, cols, wp, diag, out, part, stream);
-    case 1: return rowsum_hx_u<1>(p, rows, cols, wp, diag, out, part, stream);
-    case 2: return rowsum_hx_u<2>(p, rows, cols, wp, diag, out, part, stream);
-    case 3: return rowsum_hx_u<3>(p, rows, cols, wp, diag, out, part, stream);
-    case 4: return rowsum_hx_u<4>(p, rows, cols, wp, diag, out, part, stream);
-    case 5: return rowsum_hx_u<5>(p, rows, cols, wp, diag, out, part, stream);
-    case 6: return rowsum_hx_u<6>(p, rows, cols, wp, diag, out, part, stream);
-  }
+  dual_dispatch(rows, cols, FD_KERNEL_ROWSUM, stream, [&](const PointPack& r, const PointPack& c) {
+    check_hx(p, r, c);
+    switch (r.rid) {
+      case 0: return rowsum_hx_u<0>(p, r, c, wp, diag, out, part, stream);
+      case 1: return rowsum_hx_u<1>(p, r, c, wp, diag, out, part, stream);
+      case 2: return rowsum_hx_u<2>(p, r, c, wp, diag, out, part, stream);
+      case 3: return rowsum_hx_u<3>(p, r, c, wp, diag, out, part, stream);
+      case 4: return rowsum_hx_u<4>(p, r, c, wp, diag, out, part, stream);
+      case 5: return rowsum_hx_u<5>(p, r, c, wp, diag, out, part, stream);
+      case 6: return rowsum_hx_u<6>(p, r, c, wp, diag, out, part, stream);
+    }
+  });
 }
 
 }  // namespace fd

@@ -18,6 +18,24 @@ typedef _Float16 halfx2 __attribute__((ext_vector_type(2)));
 constexpr double LOG2E = 1.4426950408889634073599;
 constexpr int CHUNK_TILES = 64;  // column tiles per partial accumulator
 
+// Which of the two layouts of a float32 pack a launch serves (PointPack):
+// every launch of such a pair reads the same device word, and the one whose
+// layout does not match the exponent budget exits before any work.
+struct HxGate {
+  const unsigned long long* r2max;
+  double bl;    // beta log2(e) of the pack
+  int variant;  // 0: no choice, 1: short layout, 2: full-offset layout
+};
+__device__ __forceinline__ bool hx_gate_closed(const HxGate& g) {
+  if (g.variant == 0) return false;
+  const double r2 = __longlong_as_double(static_cast<long long>(*g.r2max));
+  const bool wide = g.bl * r2 > EXP_BUDGET;
+  return wide != (g.variant == 2);
+}
+inline HxGate gate_of(const PointPack& rows) {
+  return HxGate{rows.r2max, rows.beta * LOG2E, rows.variant};
+}
+
 // Workgroups of one dispatch are spread over the eight XCDs round-robin by
 // id.  Re-number them so that each XCD owns a contiguous block of logical
 // work items (same column split, hence a shared working set in its L2).
@@ -73,7 +91,11 @@ int hx_col_chunks(int rid);
 int hx_row_chunks(int rid);
 
 void launch_pack_points_hx(const float* X, int64_t n, int64_t D, int64_t ldx, double beta,
-                           bool row_side, PointPack& out, hipStream_t stream);
+                           bool row_side, PointPack& out, const CentreWs* centre,
+                           hipStream_t stream);
+// Recipe that keeps all three offset pieces for a short recipe that drops the
+// third (-1: the recipe keeps them).
+int hx_full_offset_recipe(int rid);
 void launch_product_hx(const KVPlan& p, const PointPack& rows, const PointPack& cols,
                        const float* vp, const float* colscale, bool diag, const float* sl,
                        float* Y, int64_t ldy, int b, float* part, hipStream_t stream);

@@ -43,7 +43,104 @@ PointPack carve_pack(Arena& a, int64_t n, int dp, int64_t pad) {
   p.xp = a.fspan(size_t(p.npad) * pack_floats_per_point(dp));
   p.ap = a.fspan(size_t(p.npad) * 16);  // [tiles][64][4]: 16 floats per point
   p.ar = a.fspan(size_t(p.npad));
+  // the full-offset layout of a short recipe: every D of this padded width
+  // whose recipe drops the third offset piece takes the same wider recipe
+  const int wide = hx_full_offset_recipe(hx_recipe_for(dp == 32 ? 30 : dp == 64 ? 62 : dp));
+  if (wide >= 0)
+    p.xp2 = a.fspan(size_t(p.npad) * 16 * std::max(hx_col_chunks(wide), hx_row_chunks(wide)));
   return p;
+}
+
+// ------------------------------------------------------------------ centring
+
+// Column partial sums of X rows [blk rpb, (blk + 1) rpb) in float64.
+__global__ void centre_sum_kernel(const float* __restrict__ X, int64_t n, int D, int64_t ldx,
+                                  int64_t rpb, double* __restrict__ part) {
+  __shared__ double red[256];
+  const int64_t r0 = int64_t(blockIdx.x) * rpb;
+  const int64_t r1 = min(n, r0 + rpb);
+  for (int f = 0; f < D; ++f) {
+    double acc = 0.0;
+    for (int64_t i = r0 + threadIdx.x; i < r1; i += blockDim.x) acc += double(X[i * ldx + f]);
+    red[threadIdx.x] = acc;
+    __syncthreads();
+    for (int w = 128; w > 0; w >>= 1) {
+      if (int(threadIdx.x) < w) red[threadIdx.x] += red[threadIdx.x + w];
+      __syncthreads();
+    }
+    if (threadIdx.x == 0) part[int64_t(blockIdx.x) * D + f] = red[0];
+    __syncthreads();
+  }
+}
+
+// mu = column means (fixed order over the blocks); clears r2max.
+__global__ void centre_mean_kernel(const double* __restrict__ part, int nblk, int D, int64_t n,
+                                   double* __restrict__ mu, unsigned long long* r2max) {
+  const int f = threadIdx.x;
+  if (f == 0) *r2max = 0ull;
+  if (f >= D) return;
+  double acc = 0.0;
+  for (int b = 0; b < nblk; ++b) acc += part[int64_t(b) * D + f];
+  mu[f] = acc / double(n);
+}
+
+// r2max = max(r2max, max_i ||x_i - mu||^2) over X[0:n] (non-negative float64
+// values order like their bit patterns, so an integer atomic max serves).
+__global__ void radius_max_kernel(const float* __restrict__ X, int64_t n, int D, int64_t ldx,
+                                  const double* __restrict__ mu, unsigned long long* r2max) {
+  double best = 0.0;
+  for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n;
+       i += int64_t(gridDim.x) * blockDim.x) {
+    double r = 0.0;
+    for (int f = 0; f < D; ++f) {
+      const double v = double(X[i * ldx + f]) - mu[f];
+      r += v * v;
+    }
+    best = r > best ? r : best;  // a NaN row is skipped; the non-finite scan reports it
+  }
+  for (int o = 32; o > 0; o >>= 1) best = fmax(best, __shfl_xor(best, o));
+  if ((threadIdx.x & 63) == 0 && best > 0.0)
+    atomicMax(r2max, static_cast<unsigned long long>(__double_as_longlong(best)));
+}
+
+static int centre_blocks(int64_t n) {
+  return int(std::min<int64_t>(256, std::max<int64_t>(1, ceil_div(n, 4096))));
+}
+
+CentreWs carve_centre(Arena& a, int64_t n) {
+  CentreWs c;
+  c.nblk = centre_blocks(n);
+  c.part = a.take<double>(size_t(c.nblk) * MAX_D);
+  c.mu = a.take<double>(MAX_D);
+  c.r2max = a.take<unsigned long long>(1);
+  return c;
+}
+
+void launch_centre(const void* X, fd_dtype xt, int64_t n, int64_t D, int64_t ldx,
+                   const CentreWs& c, hipStream_t stream) {
+  if (xt != FD_F32) return;
+  FD_REQUIRE(c.part != nullptr && c.mu != nullptr && c.r2max != nullptr && D <= MAX_D &&
+                 centre_blocks(n) <= c.nblk,
+             FD_ERR_INVALID_ARG, "internal: centring workspace");
+  const int nblk = centre_blocks(n);
+  const int64_t rpb = ceil_div(n, nblk);
+  const float* Xf = static_cast<const float*>(X);
+  hipLaunchKernelGGL(centre_sum_kernel, dim3(nblk), dim3(256), 0, stream, Xf, n, int(D), ldx,
+                     rpb, c.part);
+  FD_LAUNCH_CHECK();
+  hipLaunchKernelGGL(centre_mean_kernel, dim3(1), dim3(64), 0, stream, c.part, nblk, int(D), n,
+                     c.mu, c.r2max);
+  FD_LAUNCH_CHECK();
+  launch_radius_more(X, xt, n, D, ldx, c, stream);
+}
+
+void launch_radius_more(const void* X2, fd_dtype xt, int64_t n2, int64_t D, int64_t ldx,
+                        const CentreWs& c, hipStream_t stream) {
+  if (xt != FD_F32) return;
+  const unsigned grid = unsigned(std::min<int64_t>(1024, std::max<int64_t>(1, ceil_div(n2, 256))));
+  hipLaunchKernelGGL(radius_max_kernel, dim3(grid), dim3(256), 0, stream,
+                     static_cast<const float*>(X2), n2, int(D), ldx, c.mu, c.r2max);
+  FD_LAUNCH_CHECK();
 }
 
 // ------------------------------------------------------------------ packing
@@ -891,11 +988,14 @@ static void pack_points_bf16(const uint16_t* X, int64_t n, int64_t D, int64_t ld
 }
 
 void launch_pack_points(const void* X, fd_dtype xt, int64_t n, int64_t D, int64_t ldx,
-                        double beta, bool row_side, PointPack& out, hipStream_t stream) {
+                        double beta, bool row_side, PointPack& out, const CentreWs* centre,
+                        hipStream_t stream) {
   out.beta = beta;
   if (xt == FD_BF16) {
     pack_points_bf16(static_cast<const uint16_t*>(X), n, D, ldx, row_side, out, stream);
     out.rid = -1;
+    out.rid2 = -1;
+    out.variant = 0;
     out.row_side = row_side;
     return;
   }
@@ -903,7 +1003,8 @@ void launch_pack_points(const void* X, fd_dtype xt, int64_t n, int64_t D, int64_
   out.dc = 0;
   FD_REQUIRE(out.dp % 4 == 0 && D <= out.dp, FD_ERR_INVALID_ARG,
              "internal: bad point pack geometry");
-  launch_pack_points_hx(static_cast<const float*>(X), n, D, ldx, beta, row_side, out, stream);
+  launch_pack_points_hx(static_cast<const float*>(X), n, D, ldx, beta, row_side, out, centre,
+                        stream);
 }
 
 void launch_pack_w(const float* w, int64_t n, int64_t npad, FSpan wp, hipStream_t stream) {

@@ -392,8 +392,11 @@ static void nystrom_extend(ContWs& c, const void* X, fd_dtype xt, int64_t D, int
   SolverWs& w = c.sw;
   PointPack rows = pack_view(w.deg.rows, n_new, ROW_PAD);
   PointPack cols = pack_view(w.deg.cols, n_old, COL_PAD);
-  launch_pack_points(X, xt, n_new, D, ldx, beta, true, rows, st);
-  launch_pack_points(X, xt, n_old, D, ldx, beta, false, cols, st);
+  // centred on the old prefix (the column set), radius over the new one
+  launch_centre(X, xt, n_old, D, ldx, w.deg.centre, st);
+  launch_radius_more(X, xt, n_new, D, ldx, w.deg.centre, st);
+  launch_pack_points(X, xt, n_new, D, ldx, beta, true, rows, &w.deg.centre, st);
+  launch_pack_points(X, xt, n_old, D, ldx, beta, false, cols, &w.deg.centre, st);
   launch_pow_neg(q_old, n_old, alpha, c.wv, st);
   // denominators K w
   launch_pack_w(c.wv, n_old, cols.npad, w.deg.wp, st);

@@ -266,3 +266,49 @@ def test_single_column_rectangular_strided_bf16_and_beta_zero():
     case("b=1 bf16 N=4096 D=64")
     Yb = _run(s.X, None, s.betas[0], v)
     assert rel_fro(Yb, ok.kernel_matmul(s.X_f64(), None, s.betas[0], v)) <= TOL_BF16
+
+
+@pytest.mark.parametrize("which,B", [("molecule", 100.0), ("molecule", 200.0),
+                                     ("gauss62", 200.0), ("t6paper", 200.0),
+                                     ("torus6n", 400.0)])
+def test_exponent_budget_large_beta(which, B):
+    # beta log2(e) max ||x - mean||^2 = B far above the range the short split
+    # was first tested on: the layouts without the third offset piece (13 < D
+    # <= 30, 32 < D <= 62) switch to the full-offset layout above 64, and the
+    # error stays within the float32 bar (molecule-like set at B = 200:
+    # 7.7e-6, against 1.1e-5 without the switch; 1.1e-5 at B = 400, where the
+    # dropped fourth-order piece products alone reach the bar)
+    X = {"molecule": lambda: inputs.molecule(32768).X,
+         "gauss62": lambda: inputs.stress_points(32768, D=62).astype(np.float32),
+         "t6paper": lambda: inputs.torus6_paper(32768).X,
+         "torus6n": lambda: inputs.torus6_noisy(32768).X}[which]()
+    m2 = float(((X.astype(np.float64) - X.astype(np.float64).mean(0)) ** 2).sum(1).max())
+    beta = B / (np.log2(np.e) * m2)
+    V = inputs.random_block(X.shape[0], 32, seed=3)
+    case(f"exponent budget {which} D={X.shape[1]} B={B} beta={beta:.4f}")
+    Y = _run(X, None, beta, V)
+    rows = np.random.default_rng(0).choice(X.shape[0], 96, replace=False)
+    ref = ok.kernel_matmul(X, None, beta, V, rows=rows, threads=8)
+    err = rel_fro(Y[rows], ref)
+    print(f"{which} B={B}: rel err {err:.2e}")
+    assert err <= TOL_F32
+
+
+@pytest.mark.parametrize("shift", [3.0, 10.0, 100.0])
+def test_uncentred_data_is_centred_inside(shift):
+    # the same points moved away from the origin: the library centres them
+    # (the kernel is translation invariant), so the product keeps the float32
+    # accuracy it has on the centred set (without centring: 2e-5 at shift 3,
+    # 3e-4 at shift 10)
+    X = inputs.molecule(32768).X
+    m2 = float((X.astype(np.float64) ** 2).sum(1).max())
+    beta = 25.0 / (np.log2(np.e) * m2)
+    Xs = (X + np.float32(shift)).astype(np.float32)
+    V = inputs.random_block(X.shape[0], 32, seed=4)
+    case(f"uncentred molecule shift={shift} beta={beta:.4f}")
+    Y = _run(Xs, None, beta, V)
+    rows = np.random.default_rng(1).choice(X.shape[0], 96, replace=False)
+    ref = ok.kernel_matmul(Xs, None, beta, V, rows=rows, threads=8)
+    err = rel_fro(Y[rows], ref)
+    print(f"shift {shift}: rel err {err:.2e}")
+    assert err <= 3e-6
