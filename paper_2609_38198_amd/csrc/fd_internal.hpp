@@ -71,8 +71,12 @@ constexpr int WG_THREADS = 256;   // four wave64 per workgroup
 constexpr int ROW_PAD = 512;      // row packs: whole workgroups of 4 waves x 8 row tiles
 constexpr int COL_PAD = 32;       // column packs: whole pairs of 16-point tiles
 // Longest column range one workgroup of a product or row-sum plan streams
-// (tiles of 16 points); longer ranges are split.
-constexpr int64_t SPLIT_SPAN_TILES = 32768;
+// (tiles of 16 points); longer ranges are split.  The workgroups that run
+// together on an XCD start a split together and drift apart; over 4,096
+// tiles (a few tens of MB of column operands) their working set stays
+// cache-resident, over 32,768 it did not always (the bfloat16 product at
+// N = 2^21, b = 64 then ran 1.5 to 2.2 s against 1.43 s).
+constexpr int64_t SPLIT_SPAN_TILES = 4096;
 
 inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 inline int64_t ceil_div(int64_t x, int64_t m) { return (x + m - 1) / m; }
