@@ -51,7 +51,7 @@ CONTRACTION = ("exponent: float16 matrix instructions over three-piece float16 s
                "float32 coordinates (short split for D > 4 within its tested exponent budget, "
                "exact split otherwise), float32 accumulate; K V: float16 two-term splits of K "
                "and V, three float16 matrix instructions per 16 columns, float32 accumulate")
-KERNEL_SOURCES = ("hx_kernels.hip", "kv_common.hpp", "kv_kernels.hip")
+KERNEL_SOURCES = ("hx_kernels.hip", "kv_common.hpp", "kv_kernels.hip", "fd_internal.hpp")
 
 
 def kernel_source_hash() -> str:
