@@ -38,15 +38,17 @@ void fill_normal(float* Z, int64_t ldz, int64_t N, int nb, const int* flags, uin
 // out[c] = ||W[:, c] - theta_c Y[:, c]||_2 for c < nc (Y, W share ld).
 void residual_norms(const float* Y, const float* W, int64_t ld, int nc, const double* theta,
                     int64_t N, FSpanD part, double* out, hipStream_t stream);
-// Symmetric eigensolve of A (m x m, overwritten; A2 an m x m scratch with the
-// same ld): theta descending, S columns.  Vw: m x m scratch (ld m); norms: 2
-// doubles of scratch; log: jacobi_log_doubles(m) doubles (enough for every
-// size up to m) and state: 2 ints of scratch (the one-workgroup path for small
-// m).  Synchronises the stream once
-// per sweep (once per few sweeps on the one-workgroup path).
+// Symmetric eigensolve of A (m x m, m <= 1024, overwritten; A2 an m x m
+// scratch with the same ld): theta descending, S columns.  Vw: m x m scratch
+// (ld m); norms: 2 doubles of
+// scratch; log: jacobi_log_doubles(m) doubles (enough for every size up to m;
+// the rotation log of the one-workgroup path for m <= 192, the block
+// rotations of the block path above) and state: 2 ints of scratch.
+// Synchronises the stream once per sweep (once per few sweeps on the
+// one-workgroup path).  Returns the number of sweeps run.
 size_t jacobi_log_doubles(int m);
-void jacobi_eig(double* A, double* A2, int m, int lda, double* Vw, double* theta, double* S,
-                int lds, double* norms, FSpanD log, int* state, hipStream_t stream);
+int jacobi_eig(double* A, double* A2, int m, int lda, double* Vw, double* theta, double* S,
+               int lds, double* norms, FSpanD log, int* state, hipStream_t stream);
 void copy_cols(const float* src, int64_t lds, float* dst, int64_t ldd, int64_t N, int nc,
                const float* scale, double power, hipStream_t stream);
 void sub_theta(const float* Y, float* W, int64_t ld, int64_t N, int nc, const double* theta,
@@ -54,6 +56,9 @@ void sub_theta(const float* Y, float* W, int64_t ld, int64_t N, int nc, const do
 void put_block(double* T, int ldt, const double* C, int m, int c0, int nb, hipStream_t stream);
 void set_diag(double* T, int ldt, int mm, const double* theta, int kk, hipStream_t stream);
 void narrow(const double* S, int lds, int m, int nc, float* S32, hipStream_t stream);
+// L = (3 I - G) / 2 (float32, column chunks of width nc: chunk c0 at L + kk c0
+// with ld min(nc, kk - c0)) for a Gram matrix G (kk x kk, ld ldg); dev = max |G - I|.
+void loewdin(const double* G, int ldg, int kk, int nc, float* L, double* dev, hipStream_t stream);
 void copy_square(const double* src, int lds, double* dst, int ldd, int m, hipStream_t stream);
 
 }  // namespace fd

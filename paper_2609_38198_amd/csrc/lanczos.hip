@@ -56,7 +56,8 @@ struct SolverWs {
          *theta = nullptr, *norms = nullptr;
   FSpanD jlog;
   double *C = nullptr, *G = nullptr, *res = nullptr;
-  float *C32 = nullptr, *S32 = nullptr, *Rinv = nullptr;
+  float *C32 = nullptr, *S32 = nullptr, *Rinv = nullptr, *L32 = nullptr;
+  double* orth = nullptr;
   int *flags = nullptr, *sel = nullptr, *sweeps = nullptr, *jstate = nullptr;
   int64_t N = 0;
   int mm_cap = 0, b = 0;
@@ -103,6 +104,8 @@ static SolverWs carve_solver_ws(Arena& a, int64_t N, int64_t D, int b, int mm_ca
   w.C = a.take<double>(size_t(mm_cap) * b);
   w.C32 = a.take<float>(size_t(mm_cap) * std::max(b, 64));
   w.S32 = a.take<float>(size_t(mm_cap) * 64);
+  w.L32 = a.take<float>(size_t(mm_cap) * mm_cap);
+  w.orth = a.take<double>(1);
   w.G = a.take<double>(size_t(b) * b);
   w.Rinv = a.take<float>(size_t(b) * b);
   w.flags = a.take<int>(64);
@@ -172,6 +175,35 @@ struct Lanczos {
     const int m = c0 + nb;
     gemm_tn(w.Q, mm, m, w.W + c0, mm, nb, N, w.part, w.C, nullptr, st);
     put_block(w.T, mm, w.C, m, c0, nb, st);
+  }
+
+  // Thick restart on the kept Ritz pairs Q[:, 0:kk], W[:, 0:kk]: they are
+  // re-orthonormalised (first-order Loewdin: Q <- Q (3 I - G) / 2 with
+  // G = Q^T Q, W by the same factor) and their block of T is the projection
+  // Q^T W itself.  Without this the float32 products Q S of every restart
+  // let Q^T Q drift from I over many restarts, and T = diag(theta) (which
+  // assumes it) then stalls the residuals near the tolerance.  Qa, Wa are
+  // scratch here.
+  void refresh_kept(int kk) {
+    for (int c0 = 0; c0 < kk; c0 += b) {
+      const int nc = std::min(b, kk - c0);
+      gemm_tn(w.Q, mm, kk, w.Q + c0, mm, nc, N, w.part, w.C, nullptr, st);
+      put_block(w.Tw, mm, w.C, kk, c0, nc, st);
+    }
+    loewdin(w.Tw, mm, kk, 64, w.L32, w.orth, st);
+    for (int c0 = 0; c0 < kk; c0 += 64) {
+      const int nc = std::min(64, kk - c0);
+      gemm_nn(w.Q, mm, kk, w.L32 + int64_t(kk) * c0, nc, w.Qa + c0, mm, N, 1.f, 0.f, st);
+      gemm_nn(w.W, mm, kk, w.L32 + int64_t(kk) * c0, nc, w.Wa + c0, mm, N, 1.f, 0.f, st);
+    }
+    std::swap(w.Q, w.Qa);
+    std::swap(w.W, w.Wa);
+    set_diag(w.T, mm, mm, nullptr, 0, st);
+    for (int c0 = 0; c0 < kk; c0 += b) {
+      const int nc = std::min(b, kk - c0);
+      gemm_tn(w.Q, mm, kk, w.W + c0, mm, nc, N, w.part, w.C, nullptr, st);
+      put_block(w.T, mm, w.C, kk, c0, nc, st);
+    }
   }
 
   // Rayleigh-Ritz on T[0:m, 0:m]: Ritz values (descending) to theta, the
@@ -284,7 +316,15 @@ static SolveResult lanczos_solve(SolverWs& w, Lanczos& L, const SolverLayout& la
       need_rr = false;
       // restart: keep the Ritz pairs, next block from the leading unconverged residuals
       m = nkeep;
-      set_diag(w.T, mm, mm, w.theta, m, st);
+      L.refresh_kept(m);
+      if (o.verbose) {
+        double dev = 0.0;
+        FD_HIP_CHECK(hipMemcpyAsync(&dev, w.orth, sizeof(dev), hipMemcpyDeviceToHost, st));
+        FD_HIP_CHECK(hipStreamSynchronize(st));
+        std::fprintf(stderr, "[fd_lanczos] N=%lld restart: kept basis max|Q^T Q - I| = %.3e\n",
+                     (long long)N, dev);
+        std::fflush(stderr);
+      }
       const int ns = restart_columns(rs.data(), nkeep, b, o.tol, sel.data());
       FD_HIP_CHECK(hipMemcpyAsync(w.sel, sel.data(), sizeof(int) * ns, hipMemcpyHostToDevice, st));
       float* Z = w.Q + m;

@@ -445,17 +445,24 @@ void residual_norms(const float* Y, const float* W, int64_t ld, int nc, const do
 // (Alg. 8.5.2).  Because the pairs of a round are disjoint, the round's
 // similarity transform acts on A block by block: for row pair i and column
 // pair j the 2 x 2 block (rows p_i, q_i; columns p_j, q_j) becomes
-// R_i^T X R_j.  Two ways to run the rounds:
+// R_i^T X R_j.  Two ways to run the sweeps:
 //   * m <= JL_MAX: one workgroup holds the upper triangle in LDS and runs
 //     whole sweeps with a barrier between rounds (jacobi_lds_kernel); the
 //     rotations are logged and replayed on the eigenvector matrix by a
 //     second kernel (jacobi_replay_kernel);
-//   * larger m: one launch per round does all blocks (and the matching
-//     column rotations of the eigenvector matrix) with as many workgroups as
-//     the size needs, reading A and writing its transform to a second buffer;
-//     every workgroup recomputes the round's rotations from the (unchanged)
-//     input, and after each sweep the off-diagonal Frobenius norm is checked
-//     on the host (one scalar read back).
+//   * larger m: block Jacobi (the block-cyclic orderings of Golub & Van Loan,
+//     Sec. 8.5.5).  The indices form blocks of BJ_S; a round pairs the blocks
+//     by the circle method, each pair of blocks (2 BJ_S indices) gets
+//     rotations on its principal submatrix in LDS, and their product U_u
+//     then acts on A tile by tile, A_uv <- U_u^T A_uv U_v, and on the
+//     eigenvector matrix, V_:v <- V_:v U_v.  On the first round of a sweep
+//     the submatrix gets one cyclic sweep (the pairs inside each block), on
+//     the others only its cross-block pairs: every pair of indices meets once
+//     per sweep.  One launch per round (bj_round_kernel) applies round r and
+//     solves round r + 1 side by side (A double-buffered); a sweep takes
+//     m / BJ_S - 1 launches instead of m - 1.  After each sweep the
+//     off-diagonal Frobenius norm is checked on the host (one pair of
+//     scalars read back).
 // On exit theta (m) holds the eigenvalues sorted descending and S (m x m,
 // ld lds) the matching eigenvectors in its columns.
 
@@ -497,88 +504,9 @@ __device__ __forceinline__ void jacobi_pair(const double* __restrict__ A, int ld
   if (apq != 0.0) jacobi_rotation(A[int64_t(p) * lda + p], A[int64_t(q) * lda + q], apq, c, s);
 }
 
-// One round: B = J^T A J block by block, V <- V J (in place).
-__global__ __launch_bounds__(256) void jacobi_round_kernel(const double* __restrict__ A,
-                                                           double* __restrict__ B, int lda,
-                                                           double* __restrict__ V, int m, int me,
-                                                           int round) {
-  __shared__ int pp[512], qq[512];
-  __shared__ double cc[512], ss[512];
-  const int npairs = me / 2;
-  for (int k = threadIdx.x; k < npairs; k += blockDim.x) {
-    int p, q;
-    double c, s;
-    jacobi_pair(A, lda, m, me, round, k, p, q, c, s);
-    pp[k] = p;
-    qq[k] = q;
-    cc[k] = c;
-    ss[k] = s;
-  }
-  __syncthreads();
-  const int64_t nA = int64_t(npairs) * npairs;
-  const int64_t nV = int64_t(m) * npairs;
-  const int64_t stride = int64_t(gridDim.x) * blockDim.x;
-  for (int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; idx < nA + nV; idx += stride) {
-    if (idx < nA) {
-      const int i = int(idx / npairs), j = int(idx % npairs);
-      const int pi = pp[i], qi = qq[i], pj = pp[j], qj = qq[j];
-      const double ci = cc[i], si = ss[i], cj = cc[j], sj = ss[j];
-      const double a = A[int64_t(pi) * lda + pj];
-      const double b = qj >= 0 ? A[int64_t(pi) * lda + qj] : 0.0;
-      const double d = qi >= 0 ? A[int64_t(qi) * lda + pj] : 0.0;
-      const double e = (qi >= 0 && qj >= 0) ? A[int64_t(qi) * lda + qj] : 0.0;
-      // rows: p' = c p - s q, q' = s p + c q; then the same on the columns
-      const double a1 = ci * a - si * d, b1 = ci * b - si * e;
-      const double d1 = si * a + ci * d, e1 = si * b + ci * e;
-      B[int64_t(pi) * lda + pj] = cj * a1 - sj * b1;
-      if (qj >= 0) B[int64_t(pi) * lda + qj] = sj * a1 + cj * b1;
-      if (qi >= 0) B[int64_t(qi) * lda + pj] = cj * d1 - sj * e1;
-      if (qi >= 0 && qj >= 0) B[int64_t(qi) * lda + qj] = sj * d1 + cj * e1;
-    } else {
-      const int64_t v = idx - nA;
-      const int r = int(v / npairs), j = int(v % npairs);
-      const int pj = pp[j], qj = qq[j];
-      if (qj < 0 || ss[j] == 0.0) continue;
-      const double cj = cc[j], sj = ss[j];
-      const double vp = V[int64_t(r) * m + pj], vq = V[int64_t(r) * m + qj];
-      V[int64_t(r) * m + pj] = cj * vp - sj * vq;
-      V[int64_t(r) * m + qj] = sj * vp + cj * vq;
-    }
-  }
-}
-
 __global__ void jacobi_init_kernel(double* __restrict__ V, int m) {
   const int64_t e = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
   if (e < int64_t(m) * m) V[e] = (e / m == e % m) ? 1.0 : 0.0;
-}
-
-// out[0] = sum of squared off-diagonal entries, out[1] = sum of all (one
-// workgroup, fixed order)
-__global__ __launch_bounds__(1024) void jacobi_offnorm_kernel(const double* __restrict__ A, int m,
-                                                              int lda, double* __restrict__ out) {
-  __shared__ double r0[1024], r1[1024];
-  const int t = threadIdx.x;
-  double off = 0.0, all = 0.0;
-  for (int64_t e = t; e < int64_t(m) * m; e += blockDim.x) {
-    const int i = int(e / m), j = int(e % m);
-    const double v = A[int64_t(i) * lda + j];
-    all += v * v;
-    if (i != j) off += v * v;
-  }
-  r0[t] = off;
-  r1[t] = all;
-  __syncthreads();
-  for (int w = blockDim.x / 2; w > 0; w >>= 1) {
-    if (t < w) {
-      r0[t] += r0[t + w];
-      r1[t] += r1[t + w];
-    }
-    __syncthreads();
-  }
-  if (t == 0) {
-    out[0] = r0[0];
-    out[1] = r1[0];
-  }
 }
 
 // theta = diag(A) sorted descending, S columns = matching columns of V
@@ -611,10 +539,32 @@ constexpr int JL_SWEEPS = 4;  // sweeps per launch (the log holds this many)
 constexpr int JL_BATCH = 32;  // rounds of the log staged in LDS at a time by the replay
 
 // log capacity that every size up to m needs
+// ---- block Jacobi for JL_MAX < m <= 1024 (the scheme in the header above)
+constexpr int BJ_S = 16;          // indices per block
+constexpr int BJ_W = 2 * BJ_S;    // indices per pair of blocks
+constexpr int BJ_LD = BJ_W + 1;   // LDS row stride of a BJ_W x BJ_W matrix
+constexpr int BJ_PART = 64;       // workgroups of the off-diagonal norm
+
+// blocks (an even count: a padding block when needed) for an m x m matrix
+static inline int bj_blocks(int m) {
+  const int nb = (m + BJ_S - 1) / BJ_S;
+  return nb + (nb & 1);
+}
+
+// scratch of the block path: the U_u (BJ_W^2 each) and moved flags of two
+// consecutive rounds, and the partial norms (per workgroup of the first
+// check, per tile of A after)
+static inline size_t bj_doubles(int m) {
+  const int P = bj_blocks(m) / 2;
+  return 2 * (size_t(P) * BJ_W * BJ_W + P) + 2 * std::max(BJ_PART, P * (P + 1) / 2);
+}
+
+// scratch that every size up to m needs
 size_t jacobi_log_doubles(int m) {
   const int mc = std::min(m, JL_MAX);
   const int me = mc + (mc & 1);
-  return size_t(JL_SWEEPS) * me * std::max(me - 1, 1);
+  const size_t lds_path = size_t(JL_SWEEPS) * me * std::max(me - 1, 1);
+  return m > JL_MAX ? std::max(lds_path, bj_doubles(m)) : lds_path;
 }
 
 
@@ -840,16 +790,420 @@ __global__ __launch_bounds__(256) void jacobi_replay_kernel(double* __restrict__
     for (int c = lane; c < m; c += 64) V[int64_t(row) * m + c] = v[c];
 }
 
-void jacobi_eig(double* A, double* A2, int m, int lda, double* Vw, double* theta, double* S,
-                int lds, double* norms, FSpanD log, int* state, hipStream_t stream) {
+
+// global index of local index l of the pair of blocks (bp, bq); >= m marks
+// padding (a zero row and column: its rotations are the identity)
+__device__ __forceinline__ int bj_global(int bp, int bq, int l) {
+  return l < BJ_S ? bp * BJ_S + l : bq * BJ_S + (l - BJ_S);
+}
+
+// pair k of inner round r on the BJ_W local indices: a cyclic sweep over all
+// pairs (full: circle method, BJ_W - 1 rounds) or the pairs across the two
+// blocks (BJ_S rounds: local index k meets BJ_S + (k + r) mod BJ_S)
+__device__ __forceinline__ void bj_inner_pair(bool full, int r, int k, int& p, int& q) {
+  if (full) {
+    circle_pair(BJ_W, r, k, p, q);
+  } else {
+    p = k;
+    q = BJ_S + ((k + r) & (BJ_S - 1));
+  }
+}
+
+// rotation (c, s) annihilating S_pq of a BJ_W x BJ_W matrix (row stride
+// BJ_LD); the identity when S_pq is zero or negligible next to both S_pp and
+// S_qq in float64 (100 |S_pq| vanishes when added to either, Rutishauser's
+// rule)
+__device__ __forceinline__ double2 bj_rotation(const double* S, int p, int q) {
+  const double apq = S[p * BJ_LD + q], app = S[p * BJ_LD + p], aqq = S[q * BJ_LD + q];
+  double c = 1.0, sn = 0.0;
+  const double g = 100.0 * fabs(apq);
+  if (apq != 0.0 && !(fabs(app) + g == fabs(app) && fabs(aqq) + g == fabs(aqq)))
+    jacobi_rotation(app, aqq, apq, c, sn);
+  return make_double2(c, sn);
+}
+
+constexpr int BJ_TILE = BJ_W * BJ_LD;  // doubles of one padded BJ_W x BJ_W matrix in LDS
+constexpr int BJ_YLD = BJ_S + 1;       // row stride of a BJ_W x BJ_S product
+
+// One launch per round of the block Jacobi.  Workgroups [0, nsolve) take the
+// pairs of blocks of round rs: each builds its BJ_W x BJ_W principal
+// submatrix of the current A, runs its rotations (one cyclic sweep on round 0
+// of a sweep, the cross-block pairs otherwise; one barrier per inner round,
+// the submatrix double-buffered in LDS and every thread forming the two
+// rotations it needs), and writes their product U_u and a moved flag to
+// Us, fs.  The others apply round ra (rotations Ua, flags fa): tiles (u, v),
+// u <= v, of A0 become U_u^T A0_uv U_v in A1 (mirrored: A1 is exactly
+// symmetric), and the tiles of V (BJ_W rows x the columns of pair v) become
+// V_:v U_v in place.
+//
+// The current A is A1 of this launch's apply, which is not written yet: a
+// solve of round rs = ra + 1 forms its submatrix from A0 and Ua itself (its
+// two blocks sat in two different pairs of round ra; each quadrant is
+// U_ui[:, half]^T A0_{ui uj} U_uj[:, half]).  With ra < 0 (the first launch)
+// A0 is the current matrix.  With part != null the apply workgroups of A
+// write the squared off-diagonal and total norms of their tiles of A1 to
+// part[2 w], part[2 w + 1] (w = tile index).  Workgroups of 256 threads;
+// thread (i, j) = (t / 16, t % 16).
+__global__ __launch_bounds__(256) void bj_round_kernel(
+    const double* __restrict__ A0, double* __restrict__ A1, double* __restrict__ V, int lda,
+    int m, int nbk, int ra, const double* __restrict__ Ua, const double* __restrict__ fa, int rs,
+    double* __restrict__ Us, double* __restrict__ fs, int nsolve, int ntile_a,
+    double* __restrict__ part) {
+  __shared__ double L[4 * BJ_TILE + BJ_W * BJ_YLD];
+  __shared__ int2 owner[64];  // block -> (pair, half) in round ra
+  __shared__ int2 pairs[32];  // pair -> its two blocks in round ra
+  __shared__ int moved;
+  const int P = nbk / 2;
+  const int t = threadIdx.x;
+  const int ti = t >> 4, tj = t & 15;
+  static_assert(BJ_S == 16 && BJ_W == 32, "thread (i, j) owns one 2 x 2 block per inner round");
+
+  if (int(blockIdx.x) < nsolve) {
+    // ------------------------------------------------------------ solve
+    const int u = blockIdx.x;
+    int bp, bq;
+    circle_pair(nbk, rs, u, bp, bq);
+    double* S0 = L;
+    double* S1 = L + BJ_TILE;
+    double* Jm = L + 2 * BJ_TILE;
+    if (ra < 0) {
+      constexpr int NL = BJ_W * BJ_W / 256;
+      double sr[NL];
+#pragma unroll
+      for (int k = 0; k < NL; ++k) {
+        const int e = t + 256 * k;
+        const int gi = bj_global(bp, bq, e / BJ_W), gj = bj_global(bp, bq, e % BJ_W);
+        sr[k] = (gi < m && gj < m) ? A0[int64_t(gi) * lda + gj] : 0.0;
+      }
+#pragma unroll
+      for (int k = 0; k < NL; ++k) {
+        const int e = t + 256 * k;
+        S0[(e / BJ_W) * BJ_LD + e % BJ_W] = sr[k];
+      }
+    } else {
+      if (t < P) {
+        int p, q;
+        circle_pair(nbk, ra, t, p, q);
+        owner[p] = make_int2(t, 0);
+        owner[q] = make_int2(t, 1);
+        pairs[t] = make_int2(p, q);
+      }
+      __syncthreads();
+      const int2 o1 = owner[bp], o2 = owner[bq];
+      const int2 pr1 = pairs[o1.x], pr2 = pairs[o2.x];
+      // the three tiles (pair 1, pair 1), (pair 1, pair 2), (pair 2, pair 2)
+      // of A0 and the two rotation products, all loads in flight at once
+      constexpr int NL = BJ_W * BJ_W / 256;
+      double xr[3][NL], jr[2][NL];
+#pragma unroll
+      for (int k = 0; k < NL; ++k) {
+        const int e = t + 256 * k;
+        const int i = e / BJ_W, j = e % BJ_W;
+        const int g1i = bj_global(pr1.x, pr1.y, i), g1j = bj_global(pr1.x, pr1.y, j);
+        const int g2i = bj_global(pr2.x, pr2.y, i), g2j = bj_global(pr2.x, pr2.y, j);
+        xr[0][k] = (g1i < m && g1j < m) ? A0[int64_t(g1i) * lda + g1j] : 0.0;
+        xr[1][k] = (g1i < m && g2j < m) ? A0[int64_t(g1i) * lda + g2j] : 0.0;
+        xr[2][k] = (g2i < m && g2j < m) ? A0[int64_t(g2i) * lda + g2j] : 0.0;
+        jr[0][k] = Ua[int64_t(o1.x) * BJ_W * BJ_W + e];
+        jr[1][k] = Ua[int64_t(o2.x) * BJ_W * BJ_W + e];
+      }
+      double* X = L + BJ_TILE;
+      double* J1 = L + 2 * BJ_TILE;
+      double* J2 = L + 3 * BJ_TILE;
+      double* Y = L + 4 * BJ_TILE;
+#pragma unroll
+      for (int k = 0; k < NL; ++k) {
+        const int e = t + 256 * k;
+        J1[(e / BJ_W) * BJ_LD + e % BJ_W] = jr[0][k];
+        J2[(e / BJ_W) * BJ_LD + e % BJ_W] = jr[1][k];
+      }
+#pragma unroll
+      for (int qd = 0; qd < 3; ++qd) {
+        // quadrant (qa, qb) of the new submatrix: blocks (qa ? bq : bp, qb ? bq : bp)
+        const int qa = qd == 2 ? 1 : 0, qb = qd == 0 ? 0 : 1;
+        const double* Ji = qa ? J2 : J1;
+        const double* Jj = qb ? J2 : J1;
+        const int ci = 16 * (qa ? o2.y : o1.y), cj = 16 * (qb ? o2.y : o1.y);
+#pragma unroll
+        for (int k = 0; k < NL; ++k) {
+          const int e = t + 256 * k;
+          X[(e / BJ_W) * BJ_LD + e % BJ_W] = xr[qd][k];
+        }
+        __syncthreads();
+        // Y = X Jj[:, cj .. cj + 15]: rows 2 ti, 2 ti + 1 of column tj
+        double y0 = 0.0, y1 = 0.0;
+#pragma unroll 8
+        for (int x = 0; x < BJ_W; ++x) {
+          const double jv = Jj[x * BJ_LD + cj + tj];
+          y0 = fma(X[(2 * ti) * BJ_LD + x], jv, y0);
+          y1 = fma(X[(2 * ti + 1) * BJ_LD + x], jv, y1);
+        }
+        Y[(2 * ti) * BJ_YLD + tj] = y0;
+        Y[(2 * ti + 1) * BJ_YLD + tj] = y1;
+        __syncthreads();
+        // Z = Ji[:, ci .. ci + 15]^T Y: entry (ti, tj)
+        double z = 0.0;
+#pragma unroll 8
+        for (int x = 0; x < BJ_W; ++x) z = fma(Ji[x * BJ_LD + ci + ti], Y[x * BJ_YLD + tj], z);
+        S0[(16 * qa + ti) * BJ_LD + 16 * qb + tj] = z;
+        if (qa != qb) S0[(16 * qb + tj) * BJ_LD + 16 * qa + ti] = z;
+        __syncthreads();  // X, Y are rewritten by the next quadrant
+      }
+    }
+    for (int e = t; e < BJ_W * BJ_W; e += 256)
+      Jm[(e / BJ_W) * BJ_LD + e % BJ_W] = (e / BJ_W == e % BJ_W) ? 1.0 : 0.0;
+    if (t == 0) moved = 0;
+    __syncthreads();
+    const bool full = rs == 0;
+    const int inner = full ? BJ_W - 1 : BJ_S;
+    double* Sc = S0;
+    double* Sn = S1;
+    for (int r = 0; r < inner; ++r) {
+      int pi, qi, pj, qj;
+      bj_inner_pair(full, r, ti, pi, qi);
+      bj_inner_pair(full, r, tj, pj, qj);
+      // rotation k is formed on lanes k, k + 16, ... of each wave (tj = lane
+      // mod 16) and fetched by the lanes that need it (ti lies in 0 .. 15):
+      // one rotation per lane, and no barrier for the exchange
+      const double2 rl = bj_rotation(Sc, pj, qj);
+      const double2 rj = rl;
+      const double2 ri = make_double2(__shfl(rl.x, ti), __shfl(rl.y, ti));
+      if (ti == tj && ri.y != 0.0) moved = 1;  // every writer stores the same value
+      // block (ti, tj): rows pi, qi and columns pj, qj become R_i^T X R_j
+      const double a = Sc[pi * BJ_LD + pj], b = Sc[pi * BJ_LD + qj];
+      const double d = Sc[qi * BJ_LD + pj], e = Sc[qi * BJ_LD + qj];
+      const double a1 = ri.x * a - ri.y * d, b1 = ri.x * b - ri.y * e;
+      const double d1 = ri.y * a + ri.x * d, e1 = ri.y * b + ri.x * e;
+      Sn[pi * BJ_LD + pj] = rj.x * a1 - rj.y * b1;
+      Sn[pi * BJ_LD + qj] = rj.y * a1 + rj.x * b1;
+      Sn[qi * BJ_LD + pj] = rj.x * d1 - rj.y * e1;
+      Sn[qi * BJ_LD + qj] = rj.y * d1 + rj.x * e1;
+      // columns pj, qj of J on rows ti and ti + 16
+      if (rj.y != 0.0) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int x = ti + 16 * h;
+          const double jp = Jm[x * BJ_LD + pj], jq = Jm[x * BJ_LD + qj];
+          Jm[x * BJ_LD + pj] = rj.x * jp - rj.y * jq;
+          Jm[x * BJ_LD + qj] = rj.y * jp + rj.x * jq;
+        }
+      }
+      __syncthreads();
+      double* tmp = Sc;
+      Sc = Sn;
+      Sn = tmp;
+    }
+    double* Uo = Us + int64_t(u) * BJ_W * BJ_W;
+    for (int e = t; e < BJ_W * BJ_W; e += 256) Uo[e] = Jm[(e / BJ_W) * BJ_LD + e % BJ_W];
+    if (t == 0) fs[u] = moved ? 1.0 : 0.0;
+    return;
+  }
+
+  // -------------------------------------------------------------- apply
+  const int w = blockIdx.x - nsolve;
+  const bool on_a = w < ntile_a;
+  int u = 0, v = 0, rc = 0;
+  if (on_a) {
+    int rem = w;
+    while (rem >= P - u) {
+      rem -= P - u;
+      ++u;
+    }
+    v = u + rem;
+  } else {
+    rc = (w - ntile_a) / P;
+    v = (w - ntile_a) % P;
+  }
+  const bool moved_u = on_a && fa[u] != 0.0, moved_v = fa[v] != 0.0;
+  // V tiles in place: nothing to do for an unrotated pair (uniform per workgroup)
+  if (!on_a && !moved_v) return;
+  int bpu = 0, bqu = 0, bpv, bqv;
+  circle_pair(nbk, ra, v, bpv, bqv);
+  if (on_a) circle_pair(nbk, ra, u, bpu, bqu);
+  double* X = L;
+  double* Uu = L + BJ_TILE;
+  double* Uv = L + 2 * BJ_TILE;
+  double* Y = L + 3 * BJ_TILE;
+  constexpr int NL = BJ_W * BJ_W / 256;
+  double xr[NL], ur[NL], vr[NL];
+#pragma unroll
+  for (int k = 0; k < NL; ++k) {
+    const int e = t + 256 * k;
+    const int i = e / BJ_W, j = e % BJ_W;
+    const int gj = bj_global(bpv, bqv, j);
+    xr[k] = 0.0;
+    if (on_a) {
+      const int gi = bj_global(bpu, bqu, i);
+      if (gi < m && gj < m) xr[k] = A0[int64_t(gi) * lda + gj];
+    } else {
+      const int row = rc * BJ_W + i;
+      if (row < m && gj < m) xr[k] = V[int64_t(row) * m + gj];
+    }
+    ur[k] = on_a ? Ua[int64_t(u) * BJ_W * BJ_W + e] : 0.0;
+    vr[k] = Ua[int64_t(v) * BJ_W * BJ_W + e];
+  }
+#pragma unroll
+  for (int k = 0; k < NL; ++k) {
+    const int e = t + 256 * k;
+    const int o = (e / BJ_W) * BJ_LD + e % BJ_W;
+    X[o] = xr[k];
+    Uu[o] = ur[k];
+    Uv[o] = vr[k];
+  }
+  __syncthreads();
+  // thread (ti, tj): rows ti, ti + 16 and columns tj, tj + 16 (16 lanes of
+  // one row group read 16 consecutive doubles: no LDS bank conflicts)
+  double z[2][2];
+  const double* Z = X;
+  if (on_a && moved_u) {
+    double y[2][2] = {{0.0, 0.0}, {0.0, 0.0}};
+#pragma unroll 8
+    for (int x = 0; x < BJ_W; ++x) {
+      const double u0 = Uu[x * BJ_LD + ti], u1 = Uu[x * BJ_LD + ti + 16];
+      const double x0 = X[x * BJ_LD + tj], x1 = X[x * BJ_LD + tj + 16];
+      y[0][0] = fma(u0, x0, y[0][0]);
+      y[0][1] = fma(u0, x1, y[0][1]);
+      y[1][0] = fma(u1, x0, y[1][0]);
+      y[1][1] = fma(u1, x1, y[1][1]);
+    }
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+      for (int c = 0; c < 2; ++c) Y[(ti + 16 * a) * BJ_LD + tj + 16 * c] = y[a][c];
+    __syncthreads();
+    Z = Y;
+  }
+  if (moved_v) {
+    z[0][0] = z[0][1] = z[1][0] = z[1][1] = 0.0;
+#pragma unroll 8
+    for (int y = 0; y < BJ_W; ++y) {
+      const double a0 = Z[ti * BJ_LD + y], a1 = Z[(ti + 16) * BJ_LD + y];
+      const double u0 = Uv[y * BJ_LD + tj], u1 = Uv[y * BJ_LD + tj + 16];
+      z[0][0] = fma(a0, u0, z[0][0]);
+      z[0][1] = fma(a0, u1, z[0][1]);
+      z[1][0] = fma(a1, u0, z[1][0]);
+      z[1][1] = fma(a1, u1, z[1][1]);
+    }
+  } else {
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+      for (int c = 0; c < 2; ++c) z[a][c] = Z[(ti + 16 * a) * BJ_LD + tj + 16 * c];
+  }
+  double off = 0.0, all = 0.0;
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
+    const int j = tj + 16 * c;
+    const int gj = bj_global(bpv, bqv, j);
+    if (gj >= m) continue;
+#pragma unroll
+    for (int a = 0; a < 2; ++a) {
+      const int i = ti + 16 * a;
+      const double val = z[a][c];
+      if (on_a) {
+        const int gi = bj_global(bpu, bqu, i);
+        if (gi >= m || (u == v && i > j)) continue;
+        A1[int64_t(gi) * lda + gj] = val;
+        A1[int64_t(gj) * lda + gi] = val;
+        const double sq = val * val;
+        if (gi == gj) {
+          all += sq;
+        } else {
+          off += 2.0 * sq;
+          all += 2.0 * sq;
+        }
+      } else {
+        const int row = rc * BJ_W + i;
+        if (row < m) V[int64_t(row) * m + gj] = val;
+      }
+    }
+  }
+  if (part != nullptr && on_a) {
+    // fixed-order tree over the workgroup, in LDS no thread reads any more
+    __syncthreads();
+    double* r0 = L;
+    double* r1 = L + 256;
+    r0[t] = off;
+    r1[t] = all;
+    __syncthreads();
+    for (int s2 = 128; s2 > 0; s2 >>= 1) {
+      if (t < s2) {
+        r0[t] += r0[t + s2];
+        r1[t] += r1[t + s2];
+      }
+      __syncthreads();
+    }
+    if (t == 0) {
+      part[2 * w] = r0[0];
+      part[2 * w + 1] = r1[0];
+    }
+  }
+}
+
+// part[2 b], part[2 b + 1] = squared off-diagonal and total Frobenius norms of
+// rows b, b + BJ_PART, ... (fixed order); out = the sums of the parts in order
+__global__ __launch_bounds__(256) void offnorm_partial_kernel(const double* __restrict__ A, int m,
+                                                              int lda, double* __restrict__ part) {
+  __shared__ double r0[256], r1[256];
+  const int t = threadIdx.x;
+  double off = 0.0, all = 0.0;
+  for (int i = blockIdx.x; i < m; i += gridDim.x)
+    for (int j = t; j < m; j += blockDim.x) {
+      const double v = A[int64_t(i) * lda + j];
+      all += v * v;
+      if (i != j) off += v * v;
+    }
+  r0[t] = off;
+  r1[t] = all;
+  __syncthreads();
+  for (int w = blockDim.x / 2; w > 0; w >>= 1) {
+    if (t < w) {
+      r0[t] += r0[t + w];
+      r1[t] += r1[t + w];
+    }
+    __syncthreads();
+  }
+  if (t == 0) {
+    part[2 * blockIdx.x] = r0[0];
+    part[2 * blockIdx.x + 1] = r1[0];
+  }
+}
+
+__global__ __launch_bounds__(256) void offnorm_finish_kernel(const double* __restrict__ part,
+                                                             int nparts,
+                                                             double* __restrict__ out) {
+  __shared__ double r0[256], r1[256];
+  const int t = threadIdx.x;
+  double off = 0.0, all = 0.0;
+  for (int b = t; b < nparts; b += blockDim.x) {
+    off += part[2 * b];
+    all += part[2 * b + 1];
+  }
+  r0[t] = off;
+  r1[t] = all;
+  __syncthreads();
+  for (int w = blockDim.x / 2; w > 0; w >>= 1) {
+    if (t < w) {
+      r0[t] += r0[t + w];
+      r1[t] += r1[t + w];
+    }
+    __syncthreads();
+  }
+  if (t == 0) {
+    out[0] = r0[0];
+    out[1] = r1[0];
+  }
+}
+
+int jacobi_eig(double* A, double* A2, int m, int lda, double* Vw, double* theta, double* S,
+               int lds, double* norms, FSpanD log, int* state, hipStream_t stream) {
   FD_REQUIRE(m >= 1 && m <= 1024, FD_ERR_UNSUPPORTED, "projected matrix larger than 1024");
   constexpr int MAX_SWEEPS = 60;
   constexpr double TOL = 1e-13;
-  const int me = m + (m & 1);
-  const int npairs = me / 2;
   hipLaunchKernelGGL(jacobi_init_kernel, dim3(nblk(int64_t(m) * m, 256)), dim3(256), 0, stream, Vw,
                      m);
   FD_LAUNCH_CHECK();
+  int sweeps = 0;
   double* cur = A;
   if (m > 1 && m <= JL_MAX) {
     check_span_d(log, jacobi_log_doubles(m), "jacobi rotation log");
@@ -865,32 +1219,61 @@ void jacobi_eig(double* A, double* A2, int m, int lda, double* Vw, double* theta
       int h[2] = {0, 0};
       FD_HIP_CHECK(hipMemcpyAsync(h, state, sizeof(h), hipMemcpyDeviceToHost, stream));
       FD_HIP_CHECK(hipStreamSynchronize(stream));
+      sweeps += h[0] / std::max(m + (m & 1) - 1, 1);
       if (h[1]) break;
     }
-  } else {
-    const int64_t items = int64_t(npairs) * npairs + int64_t(m) * npairs;
-    const unsigned grid =
-        unsigned(std::min<int64_t>(2048, std::max<int64_t>(1, (items + 255) / 256)));
+  } else if (m > 1) {
+    FD_REQUIRE(lda >= m && A2 != nullptr, FD_ERR_INVALID_ARG, "internal: block jacobi buffers");
+    check_span_d(log, bj_doubles(m), "block jacobi scratch");
+    const int nbk = bj_blocks(m), P = nbk / 2;
+    // a solve of round r + 1 sits in another pair than in round r only when a
+    // sweep has more than one round
+    FD_REQUIRE(nbk >= 4, FD_ERR_INVALID_ARG, "internal: block jacobi needs two rounds per sweep");
+    const int ntile_a = P * (P + 1) / 2;
+    const int ntile_v = ((m + BJ_W - 1) / BJ_W) * P;
+    double* U[2] = {log.p, log.p + size_t(P) * BJ_W * BJ_W};
+    double* F[2] = {U[1] + size_t(P) * BJ_W * BJ_W, U[1] + size_t(P) * BJ_W * BJ_W + P};
+    double* part = F[1] + P;
     double* nxt = A2;
-    for (int sweep = 0; sweep < MAX_SWEEPS && m > 1; ++sweep) {
-      hipLaunchKernelGGL(jacobi_offnorm_kernel, dim3(1), dim3(1024), 0, stream, cur, m, lda,
+    auto check = [&](int nparts) {
+      hipLaunchKernelGGL(offnorm_finish_kernel, dim3(1), dim3(256), 0, stream, part, nparts,
                          norms);
       FD_LAUNCH_CHECK();
       double h[2] = {0.0, 0.0};
       FD_HIP_CHECK(hipMemcpyAsync(h, norms, sizeof(h), hipMemcpyDeviceToHost, stream));
       FD_HIP_CHECK(hipStreamSynchronize(stream));
-      if (h[0] <= TOL * TOL * h[1]) break;
-      for (int round = 0; round < me - 1; ++round) {
-        hipLaunchKernelGGL(jacobi_round_kernel, dim3(grid), dim3(256), 0, stream, cur, nxt, lda,
-                           Vw, m, me, round);
-        FD_LAUNCH_CHECK();
-        std::swap(cur, nxt);
+      return h[0] <= TOL * TOL * h[1];
+    };
+    hipLaunchKernelGGL(offnorm_partial_kernel, dim3(BJ_PART), dim3(256), 0, stream, cur, m, lda,
+                       part);
+    FD_LAUNCH_CHECK();
+    if (!check(BJ_PART)) {
+      // round 0 solved alone, then per launch: apply round r, solve round r + 1
+      // (round 0 of the next sweep after the last round)
+      int slot = 0;
+      hipLaunchKernelGGL(bj_round_kernel, dim3(P), dim3(256), 0, stream, cur, nxt, Vw, lda, m,
+                         nbk, -1, nullptr, nullptr, 0, U[0], F[0], P, 0, nullptr);
+      FD_LAUNCH_CHECK();
+      for (; sweeps < MAX_SWEEPS;) {
+        for (int r = 0; r < nbk - 1; ++r) {
+          const bool last = r == nbk - 2;
+          const int rn = last ? 0 : r + 1;
+          hipLaunchKernelGGL(bj_round_kernel, dim3(P + ntile_a + ntile_v), dim3(256), 0, stream,
+                             cur, nxt, Vw, lda, m, nbk, r, U[slot], F[slot], rn, U[slot ^ 1],
+                             F[slot ^ 1], P, ntile_a, last ? part : nullptr);
+          FD_LAUNCH_CHECK();
+          std::swap(cur, nxt);
+          slot ^= 1;
+        }
+        ++sweeps;
+        if (check(ntile_a)) break;
       }
     }
   }
   hipLaunchKernelGGL(jacobi_sort_kernel, dim3(nblk(m, 256)), dim3(256), 0, stream, cur, m, lda, Vw,
                      theta, S, lds);
   FD_LAUNCH_CHECK();
+  return sweeps;
 }
 
 // ------------------------------------------------------------ small helpers
@@ -967,6 +1350,37 @@ __global__ void set_diag_kernel(double* __restrict__ T, int ldt, int mm,
 void set_diag(double* T, int ldt, int mm, const double* theta, int kk, hipStream_t stream) {
   hipLaunchKernelGGL(set_diag_kernel, dim3(nblk(int64_t(mm) * mm, 256)), dim3(256), 0, stream, T,
                      ldt, mm, theta, kk);
+  FD_LAUNCH_CHECK();
+}
+
+// First-order Loewdin factor of a Gram matrix G (kk x kk, ld ldg) of nearly
+// orthonormal columns: L = (3 I - G) / 2, so that (Q L)^T (Q L) = I + O(|G - I|^2).
+// Stored in float32 column chunks of width nc (chunk c0 at L + kk c0, element
+// (r, c) at r * width + (c - c0)); dev = max |G - I| (one workgroup, fixed order).
+__global__ __launch_bounds__(256) void loewdin_kernel(const double* __restrict__ G, int ldg,
+                                                      int kk, int nc, float* __restrict__ L,
+                                                      double* __restrict__ dev) {
+  __shared__ double red[256];
+  double mx = 0.0;
+  for (int idx = threadIdx.x; idx < kk * kk; idx += blockDim.x) {
+    const int r = idx / kk, c = idx % kk;
+    const double e = G[int64_t(r) * ldg + c] - (r == c ? 1.0 : 0.0);
+    mx = fmax(mx, fabs(e));
+    const int c0 = c / nc * nc;
+    const int width = min(nc, kk - c0);
+    L[int64_t(kk) * c0 + r * width + (c - c0)] = float((r == c ? 1.0 : 0.0) - 0.5 * e);
+  }
+  red[threadIdx.x] = mx;
+  __syncthreads();
+  for (int w = blockDim.x / 2; w > 0; w >>= 1) {
+    if (threadIdx.x < w) red[threadIdx.x] = fmax(red[threadIdx.x], red[threadIdx.x + w]);
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) *dev = red[0];
+}
+
+void loewdin(const double* G, int ldg, int kk, int nc, float* L, double* dev, hipStream_t stream) {
+  hipLaunchKernelGGL(loewdin_kernel, dim3(1), dim3(256), 0, stream, G, ldg, kk, nc, L, dev);
   FD_LAUNCH_CHECK();
 }
 

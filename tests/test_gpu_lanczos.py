@@ -180,11 +180,12 @@ def test_block_width_one():
     assert np.all(np.abs(np.asarray(e.evals) - ref.evals) <= np.maximum(1e-5 * np.abs(ref.evals), 1e-6))
 
 
-@pytest.mark.parametrize("N,k,b", [(191, 40, 32), (255, 40, 64)])
+@pytest.mark.parametrize("N,k,b", [(191, 40, 32), (255, 40, 64), (384, 40, 64), (1000, 40, 64)])
 def test_dense_mode_both_jacobi_paths(N, k, b):
-    # N <= basis width: the eigensolve runs on the whole (odd-sized) projected
-    # matrix; 191 takes the one-workgroup Jacobi (padded with a dummy index),
-    # 255 the launch-per-round one
+    # N <= basis width: the eigensolve runs on the whole projected matrix; 191
+    # takes the one-workgroup Jacobi (odd: padded with a dummy index), 255,
+    # 384 and 1000 the block Jacobi (255 and 1000 with a partly padded block,
+    # 1000 near the 1024 limit)
     rng = np.random.default_rng(N)
     X = rng.normal(size=(N, 3)).astype(np.float32)
     X -= X.mean(0)
