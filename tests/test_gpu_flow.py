@@ -137,3 +137,28 @@ def test_single_level_cascade_equals_the_flow():
     assert a.beta_x == c.beta_x and a.reason == c.reason
     assert [p["beta"] for p in a.probes] == [p["beta"] for p in c.probes]
     assert a.evals == c.evals
+
+
+@pytest.mark.parametrize("which,B0", [("molecule D=30", 25.0), ("t6paper D=32", 6.0)])
+def test_flow_probes_at_large_beta_on_wide_data(which, B0):
+    # the flow on data wide enough for the float16 layouts whose offsets are
+    # gated (13 < D <= 30) or kept whole (D = 32), started where
+    # B = beta log2(e) max ||x - mean||^2 is B0 and doubled from there: on the
+    # molecule-like set to B = 200, the edge of the tested accuracy envelope
+    # (the layout switch at B = 64 falls between two probes; budget exit); on
+    # the paper's T^6 set to its wall at B = 24.  Every probe against the
+    # oracle's flow on dense float64 probes.
+    N = 2048
+    X = (inputs.molecule(N).X if which.startswith("molecule") else inputs.torus6_paper(N).X)
+    X = np.ascontiguousarray(X, dtype=np.float32)
+    X64 = X.astype(np.float64)
+    r = float(np.max(np.sum((X64 - X64.mean(0)) ** 2, axis=1)))
+    b0 = B0 / (np.log2(np.e) * r)
+    case(f"beta flow at large beta: {which} N={N} from B={B0}")
+    got = fd.fd_beta_flow(to_dev(X, device()), 4, 8, alpha=0.5,
+                          fopts=fd.flow_default_opts(max_probes=4, beta_start=b0))
+    ref = bf.flow(bf.dense_probe(X64, 0.5, 4), N, b0, max_probes=4)
+    print(f"{which}: {ref.reason}, B of the probes "
+          f"{[round(np.log2(np.e) * p.beta * r, 1) for p in ref.probes]}")
+    assert got.reason == ref.reason
+    compare_probes(dyadic(got), ref)
