@@ -72,6 +72,15 @@ def test_host_validation_without_gpu():
     # missing workspace
     assert lib.fd_kernel_matmul(fake, 10, fake, 10, 4, 4, 0, 1.0, None, None, fake, 8, 8, fake, 8,
                                 None, 0, None) == 3
+    # empty and degenerate sizes: no rows, no columns, no features, D > 64
+    for N, Nc, D in ((0, 10, 4), (10, 0, 4), (10, 10, 0)):
+        assert lib.fd_kernel_matmul(fake, N, fake, Nc, D, 4, 0, 1.0, None, None, fake, 8, 8,
+                                    fake, 8, None, 0, None) == 1
+    assert lib.fd_kernel_matmul(fake, 10, None, 0, 65, 65, 0, 1.0, None, None, fake, 8, 8, fake,
+                                8, None, 0, None) == 2
+    assert b"D above 64" in lib.fd_last_error()
+    assert lib.fd_degree(fake, 0, 0, 4, 4, 1.0, 0.5, None, None, None, None, None, 0, None) == 1
+    assert lib.fd_degree(fake, 0, 10, 0, 4, 1.0, 0.5, None, None, None, None, None, 0, None) == 1
     # degree: alpha out of range, beta = 0
     assert lib.fd_degree(fake, 0, 10, 4, 4, 1.0, 1.5, None, None, None, None, None, 0, None) == 1
     assert lib.fd_degree(fake, 0, 10, 4, 4, 0.0, 0.5, None, None, None, None, None, 0, None) == 1
