@@ -211,8 +211,12 @@ def torus6_sweep_leg(fd, torch, dev, steps: int, warmup: int = 2) -> dict:
             "product_hbm_bytes_per_launch": recorded_traffic("product", TRAFFIC_FILE_TORUS6)}
 
 
-def continuation_leg(fd, torch, dev) -> dict:
-    """Noisy 6-torus ladder: n in {16K, 65K, 262K} x beta doubling 0.5 -> 8, k = 64, b = 32."""
+def continuation_leg(fd, torch, dev, cold: bool = False) -> dict:
+    """Noisy 6-torus ladder: n in {16K, 65K, 262K} x beta doubling 0.5 -> 8, k = 64, b = 32.
+
+    cold: also solve every step from a random start (fd_block_lanczos on the
+    prefix) and report its block products beside the warm-started ones.
+    """
     from paper_2609_38198_amd import inputs
     w = inputs.torus6_noisy()
     X = torch.from_numpy(w.X).to(dev)
@@ -230,12 +234,23 @@ def continuation_leg(fd, torch, dev) -> dict:
     lad = fd.fd_continuation(X, ns, bs, w.k, w.b, allow=(0, 5), opts=opts)
     torch.cuda.synchronize()
     t = time.perf_counter() - t0
+    steps = [{"n": n, "beta": beta, "matvecs": i["block_matvecs"], "nconv": i["nconv"],
+              "gap": i["gap_perron"], "wall": i["wall"], "s": i["seconds"]}
+             for n, beta, i in zip(ns, bs, lad.info)]
+    if cold:
+        log("continuation leg: cold solves of every step")
+        for st in steps:
+            t1 = time.perf_counter()
+            e = fd.fd_block_lanczos(X[: st["n"]], st["beta"], w.k, w.b, alpha=0.5,
+                                    opts=fd.default_opts(), allow_not_converged=True)
+            torch.cuda.synchronize()
+            st.update({"cold_matvecs": e.info["block_matvecs"], "cold_nconv": e.info["nconv"],
+                       "cold_s": time.perf_counter() - t1})
+            log(f"  n={st['n']} beta={st['beta']:g}: warm {st['matvecs']} / cold "
+                f"{st['cold_matvecs']} block products")
     return {"workload": "noisy 6-torus N=262144 D=12 k=64 b=32, n in {16384, 65536, 262144} x "
                         "beta in {0.5, 1, 2, 4, 8}; default options", "seconds": t,
-            "status": lad.status,
-            "steps": [{"n": n, "beta": beta, "matvecs": i["block_matvecs"], "nconv": i["nconv"],
-                       "gap": i["gap_perron"], "wall": i["wall"], "s": i["seconds"]}
-                      for n, beta, i in zip(ns, bs, lad.info)]}
+            "status": lad.status, "steps": steps}
 
 
 def stress_leg(fd, torch, dev, iterations: int = 20) -> dict:
@@ -415,6 +430,8 @@ def main() -> int:
     ap.add_argument("--lanczos", action="store_true",
                     help="time to the top 16 eigenpairs on the 2-torus (N = 2048)")
     ap.add_argument("--continuation", action="store_true")
+    ap.add_argument("--continuation-cold", action="store_true",
+                    help="with --continuation: also solve every ladder step from a random start")
     ap.add_argument("--stress", action="store_true",
                     help="bfloat16 stress set (N = 2^21, D = 64, b = 64): product throughput and "
                          "block-Lanczos iterations")
@@ -555,7 +572,7 @@ def main() -> int:
     if args.lanczos:
         rec["lanczos"] = lanczos_leg(fd, torch, dev)
     if args.continuation:
-        rec["continuation"] = continuation_leg(fd, torch, dev)
+        rec["continuation"] = continuation_leg(fd, torch, dev, cold=args.continuation_cold)
     if args.stress:
         rec["stress"] = stress_leg(fd, torch, dev, args.stress_iters)
     if args.paper_t6:

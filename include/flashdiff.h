@@ -83,13 +83,14 @@ typedef struct fd_lanczos_opts {
   double tol;               /* converged when ||M phi - theta phi||_2 <= tol (||M||_2 = 1). Default 1e-5 */
   int32_t max_restarts;     /* restart cycles before FD_ERR_NOT_CONVERGED. Default 200 */
   int32_t max_basis_blocks; /* basis capacity in blocks of b (0 = automatic: four times the first
-                               checkpoint, at most 1024 columns).  The first convergence check
-                               (Rayleigh-Ritz without restart) comes when the basis reaches k + keep
-                               rounded up to whole blocks plus as many again (at least 2 blocks);
-                               later checks come when the block products added since the last one
-                               cost about as much as a check (a fixed cost model of N, D, b and the
-                               basis width, so runs are reproducible); a full basis restarts */
-  int32_t keep;             /* Ritz vectors kept at restart beyond k (-1 = automatic: b) */
+                               cycle's width, at most 1024 columns).  The first restart cycle
+                               grows the basis to k + keep rounded up to whole blocks plus as
+                               many again (at least 2 blocks), then runs Rayleigh-Ritz and a
+                               thick restart; a cycle that converged few new leading pairs
+                               doubles the next cycle's width, up to the capacity.  After a warm
+                               start the first cycle is a single block */
+  int32_t keep;             /* Ritz vectors kept at restart beyond k (-1 = automatic: k, at least
+                               b, as far as k + keep + b fits the capacity) */
   int32_t max_matvecs;      /* stop after this many block products (0 = no limit). A run that
                                stops this way returns FD_ERR_NOT_CONVERGED with valid Ritz pairs */
   int32_t verbose;          /* non-zero: one progress line per restart cycle on stderr */

@@ -27,12 +27,12 @@ static int failures = 0;
 
 static int units() {
   SolverLayout L;
-  // k = 64, b = 32, default keep: first check at 192, capacity 768
+  // k = 64, b = 32, default keep (k): first cycle 256, capacity 1024
   CHECK(solver_layout(262144, 32, 64, -1, 0, L).empty());
-  CHECK(!L.dense && L.kk == 96 && L.m_first == 192 && L.mm == 768);
-  // k = 16, b = 8: first check at 48, capacity 192
+  CHECK(!L.dense && L.kk == 128 && L.m_first == 256 && L.mm == 1024);
+  // k = 16, b = 8: first cycle 64, capacity 256
   CHECK(solver_layout(2048, 8, 16, -1, 0, L).empty());
-  CHECK(L.m_first == 48 && L.mm == 192);
+  CHECK(L.m_first == 64 && L.mm == 256);
   // the capacity never passes 1024 columns
   CHECK(solver_layout(1 << 21, 64, 64, 64, 0, L).empty());
   CHECK(L.mm == 1024 && L.m_first == 256);
@@ -45,24 +45,33 @@ static int units() {
   // a basis too small for k + keep + b is refused
   CHECK(!solver_layout(1 << 20, 32, 64, -1, 3, L).empty());
 
+  // default keep: k (at least b) as far as k + keep + b fits the capacity
+  CHECK(default_keep(32, 64, 1024) == 64 && default_keep(8, 4, 1024) == 8);
+  CHECK(default_keep(32, 500, 1024) == 492 && default_keep(32, 64, 192) == 64);
+  CHECK(default_keep(32, 64, 160) == 64 && default_keep(32, 64, 128) == 32);
   // restart cycles: the width doubles (up to the capacity) after a cycle that
   // converged fewer new leading pairs than min(b, half of those missing)
   CHECK(solver_layout(1 << 20, 32, 64, -1, 0, L).empty());
-  CHECK(next_cycle_width(L, 192, 0, 59) == 192);
-  CHECK(next_cycle_width(L, 192, 0, 31) == 384);
-  CHECK(next_cycle_width(L, 384, 31, 40) == 768);
-  CHECK(next_cycle_width(L, 768, 40, 41) == 768);
-  CHECK(next_cycle_width(L, 192, 10, 42) == 192);
-  CHECK(next_cycle_width(L, 192, 56, 60) == 192);   // 4 of the 8 missing
-  CHECK(next_cycle_width(L, 192, 56, 59) == 384);
+  CHECK(L.keep == 64 && L.kk == 128 && L.m_first == 256 && L.mm == 1024);
+  CHECK(next_cycle_width(L, 256, 0, 59) == 256);
+  CHECK(next_cycle_width(L, 256, 0, 31) == 512);
+  CHECK(next_cycle_width(L, 512, 31, 40) == 1024);
+  CHECK(next_cycle_width(L, 1024, 40, 41) == 1024);
+  CHECK(next_cycle_width(L, 256, 10, 42) == 256);
+  CHECK(next_cycle_width(L, 256, 56, 60) == 256);   // 4 of the 8 missing
+  CHECK(next_cycle_width(L, 256, 56, 59) == 512);
   CHECK(solver_layout(1 << 20, 32, 64, -1, 8, L).empty());  // explicit capacity 256
-  CHECK(next_cycle_width(L, 192, 0, 0) == 256);
+  CHECK(L.keep == 64 && L.m_first == 256 && next_cycle_width(L, 256, 0, 0) == 256);
+  CHECK(solver_layout(1 << 20, 32, 64, 32, 0, L).empty());  // explicit keep = b
+  CHECK(L.kk == 96 && L.m_first == 192 && L.mm == 768);
   CHECK(solver_layout(4096, 8, 8, -1, 0, L).empty());  // k = 8, b = 8
   CHECK(L.m_first == 32 && next_cycle_width(L, 32, 3, 7) == 32);
   // after a warm start the first cycle is one block
   CHECK(warm_cycle_width(L, 8) == 16);
   CHECK(solver_layout(262144, 32, 64, -1, 0, L).empty());
-  CHECK(warm_cycle_width(L, 64) == 96 && warm_cycle_width(L, 192) == 192);
+  CHECK(warm_cycle_width(L, 64) == 96 && warm_cycle_width(L, 128) == 160);
+  // after the one-block check the cycles take the first width, progress or not
+  CHECK(next_cycle_width(L, 96, 0, 64) == 256 && next_cycle_width(L, 96, 0, 0) == 256);
 
   // convergence count stops at the first unconverged pair
   const double res[6] = {1e-7, 2e-6, 5e-5, 1e-8, 1e-9, 3e-4};
