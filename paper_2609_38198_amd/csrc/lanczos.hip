@@ -208,9 +208,9 @@ struct Lanczos {
 
   // Rayleigh-Ritz on T[0:m, 0:m]: Ritz values (descending) to theta, the
   // leading nkeep Ritz vectors / images to Qa / Wa, their residual norms to res.
-  void rayleigh_ritz(int m, int nkeep) {
+  int rayleigh_ritz(int m, int nkeep) {
     copy_square(w.T, mm, w.Tw, mm, m, st);
-    jacobi_eig(w.Tw, w.Tw2, m, mm, w.Vw, w.theta, w.S, mm, w.norms, w.jlog, w.jstate, st);
+    const int sweeps = jacobi_eig(w.Tw, w.Tw2, m, mm, w.Vw, w.theta, w.S, mm, w.norms, w.jlog, w.jstate, st);
     for (int c0 = 0; c0 < nkeep; c0 += 64) {
       const int nc = std::min(64, nkeep - c0);
       narrow(w.S + c0, mm, m, nc, w.S32, st);
@@ -218,6 +218,7 @@ struct Lanczos {
       gemm_nn(w.W, mm, m, w.S32, nc, w.Wa + c0, mm, N, 1.f, 0.f, st);
     }
     residual_norms(w.Qa, w.Wa, mm, nkeep, w.theta, N, w.part, w.res, st);
+    return sweeps;
   }
 };
 
@@ -275,7 +276,7 @@ static SolveResult lanczos_solve(SolverWs& w, Lanczos& L, const SolverLayout& la
     const bool out_of_budget = L.matvecs >= budget;
     if (full || need_rr || out_of_budget) {
       const int nkeep = lay.dense ? std::min(mm, std::max(k, 1)) : std::min(lay.kk, m);
-      L.rayleigh_ritz(m, nkeep);
+      const int sweeps = L.rayleigh_ritz(m, nkeep);
       FD_HIP_CHECK(hipMemcpyAsync(th.data(), w.theta, sizeof(double) * m, hipMemcpyDeviceToHost, st));
       FD_HIP_CHECK(hipMemcpyAsync(rs.data(), w.res, sizeof(double) * nkeep, hipMemcpyDeviceToHost, st));
       FD_HIP_CHECK(hipStreamSynchronize(st));
@@ -287,9 +288,10 @@ static SolveResult lanczos_solve(SolverWs& w, Lanczos& L, const SolverLayout& la
             std::chrono::duration<double>(std::chrono::steady_clock::now() - t_start).count();
         std::fprintf(stderr,
                      "[fd_lanczos] N=%lld cycle=%d basis=%d products=%d converged=%d/%d "
-                     "max_residual=%.3e theta0=%.9f theta_k-1=%.6e elapsed=%.3fs%s\n",
+                     "max_residual=%.3e theta0=%.9f theta_k-1=%.6e jacobi_sweeps=%d "
+                     "elapsed=%.3fs\n",
                      (long long)N, R.restarts, m, L.matvecs, nconv, k, worst, th[0],
-                     th[std::min(k, m) - 1], el, "");
+                     th[std::min(k, m) - 1], sweeps, el);
         std::fflush(stderr);
       }
       R.nconv = nconv;

@@ -475,17 +475,23 @@ __device__ __forceinline__ void circle_pair(int me, int round, int k, int& p, in
   q = max(a, bq);
 }
 
-// rotation (c, s) annihilating A_pq (apq != 0): t = tan of the angle, the
-// smaller root of t^2 + 2 tau t - 1 = 0 (the 2 x 2 symmetric Schur
-// decomposition of Golub & Van Loan)
-// (with tau = (aqq - app) / (2 apq) multiplied through by 2 |apq|: one square
-// root and one division fewer on the dependent chain)
+// rotation (c, s) annihilating A_pq: t = tan of the angle is the smaller
+// root of t^2 + 2 tau t - 1 = 0, tau = (aqq - app) / (2 apq) (the 2 x 2
+// symmetric Schur decomposition of Golub & Van Loan).  With d = aqq - app, r = sqrt(d^2 + 4 apq^2) and e = |d| + r, the tangent of
+// the rotation angle is t = sign(d) 2 apq / e, so (c, s) is the unit vector
+// along (e, sign(d) 2 apq).  r only sets the angle: it is taken in single
+// precision, and the normalisation 1 / |(e, 2 apq)| in float64 keeps
+// c^2 + s^2 = 1 to float64 rounding whatever r's error (about 1e-7 of r,
+// which leaves about 1e-7 of apq unannihilated; the next sweep takes it).
 __device__ __forceinline__ void jacobi_rotation(double app, double aqq, double apq, double& c,
                                                 double& s) {
   const double d = aqq - app;
-  const double tt = (d >= 0.0 ? 2.0 * apq : -2.0 * apq) / (fabs(d) + sqrt(d * d + 4.0 * apq * apq));
-  c = rsqrt(1.0 + tt * tt);
-  s = tt * c;
+  const double a2 = 2.0 * apq;
+  const double r = double(sqrtf(float(fma(d, d, a2 * a2))));
+  const double e = fabs(d) + r;
+  const double q = rsqrt(fma(e, e, a2 * a2));
+  c = e * q;
+  s = (d >= 0.0 ? a2 : -a2) * q;
 }
 
 // pair k of round `round` among me (even) players: indices p < q, q = -1 for
@@ -509,20 +515,34 @@ __global__ void jacobi_init_kernel(double* __restrict__ V, int m) {
   if (e < int64_t(m) * m) V[e] = (e / m == e % m) ? 1.0 : 0.0;
 }
 
-// theta = diag(A) sorted descending, S columns = matching columns of V
-__global__ void jacobi_sort_kernel(const double* __restrict__ A, int m, int lda,
-                                   const double* __restrict__ V, double* __restrict__ theta,
-                                   double* __restrict__ S, int lds) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+// theta = diag(A) sorted descending (ties by index), perm[rank] = the index
+// of that rank; every workgroup stages the diagonal (m <= 1024) in LDS
+__global__ __launch_bounds__(256) void jacobi_rank_kernel(const double* __restrict__ A, int m,
+                                                          int lda, double* __restrict__ theta,
+                                                          int* __restrict__ perm) {
+  __shared__ double dg[1024];
+  for (int j = threadIdx.x; j < m; j += 256) dg[j] = A[int64_t(j) * lda + j];
+  __syncthreads();
+  const int i = blockIdx.x * 256 + threadIdx.x;
   if (i >= m) return;
-  const double di = A[int64_t(i) * lda + i];
+  const double di = dg[i];
   int rank = 0;
   for (int j = 0; j < m; ++j) {
-    const double dj = A[int64_t(j) * lda + j];
+    const double dj = dg[j];
     rank += (dj > di || (dj == di && j < i)) ? 1 : 0;
   }
   theta[rank] = di;
-  for (int r = 0; r < m; ++r) S[int64_t(r) * lds + rank] = V[int64_t(r) * m + i];
+  perm[rank] = i;
+}
+
+// S[r][k] = V[r][perm[k]]: the columns of V in rank order
+__global__ __launch_bounds__(256) void jacobi_permute_kernel(const double* __restrict__ V, int m,
+                                                             const int* __restrict__ perm,
+                                                             double* __restrict__ S, int lds) {
+  const int64_t e = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  if (e >= int64_t(m) * m) return;
+  const int r = int(e / m), k = int(e % m);
+  S[int64_t(r) * lds + k] = V[int64_t(r) * m + perm[k]];
 }
 
 // ---- one-workgroup variant for m <= JL_MAX
@@ -797,33 +817,62 @@ __device__ __forceinline__ int bj_global(int bp, int bq, int l) {
   return l < BJ_S ? bp * BJ_S + l : bq * BJ_S + (l - BJ_S);
 }
 
-// pair k of inner round r on the BJ_W local indices: a cyclic sweep over all
-// pairs (full: circle method, BJ_W - 1 rounds) or the pairs across the two
-// blocks (BJ_S rounds: local index k meets BJ_S + (k + r) mod BJ_S)
-__device__ __forceinline__ void bj_inner_pair(bool full, int r, int k, int& p, int& q) {
-  if (full) {
-    circle_pair(BJ_W, r, k, p, q);
-  } else {
-    p = k;
-    q = BJ_S + ((k + r) & (BJ_S - 1));
-  }
+// rotation (c, s) annihilating the entry apq of a symmetric matrix with
+// diagonal entries app, aqq; the identity when apq is zero or negligible next
+// to both in float64 (100 |apq| vanishes when added to either, Rutishauser's
+// rule).  Branch-free: the rotation is always formed (a zero d and apq give
+// NaNs there) and the identity selected.
+__device__ __forceinline__ double2 bj_rotation(double app, double aqq, double apq) {
+  double c, sn;
+  jacobi_rotation(app, aqq, apq, c, sn);
+  const double g = 100.0 * fabs(apq);
+  const bool skip = fabs(app) + g == fabs(app) && fabs(aqq) + g == fabs(aqq);  // also apq = 0
+  return skip ? make_double2(1.0, 0.0) : make_double2(c, sn);
 }
 
-// rotation (c, s) annihilating S_pq of a BJ_W x BJ_W matrix (row stride
-// BJ_LD); the identity when S_pq is zero or negligible next to both S_pp and
-// S_qq in float64 (100 |S_pq| vanishes when added to either, Rutishauser's
-// rule)
-__device__ __forceinline__ double2 bj_rotation(const double* S, int p, int q) {
-  const double apq = S[p * BJ_LD + q], app = S[p * BJ_LD + p], aqq = S[q * BJ_LD + q];
-  double c = 1.0, sn = 0.0;
-  const double g = 100.0 * fabs(apq);
-  if (apq != 0.0 && !(fabs(app) + g == fabs(app) && fabs(aqq) + g == fabs(aqq)))
-    jacobi_rotation(app, aqq, apq, c, sn);
-  return make_double2(c, sn);
+// One inner round on the BJ_W x BJ_W submatrix Sc -> Sn and the rotation
+// product Jm, for thread (ti, tj) with pairs (pi, qi) = pair ti and
+// (pj, qj) = pair tj of the round.  Every LDS read comes first (the entries of
+// rotation tj, the 2 x 2 block rows pi, qi x columns pj, qj, the entries of J
+// on rows ti, ti + 16 and columns pj, qj); rotation tj is formed on this lane
+// and rotation ti fetched from lane ti of the 16-lane row (whose tj is ti).
+// Returns whether rotation tj is not the identity.
+__device__ __forceinline__ bool bj_inner_round(const double* __restrict__ Sc,
+                                               double* __restrict__ Sn, double* __restrict__ Jm,
+                                               int ti, int pi, int qi, int pj, int qj) {
+  const double jpp = Sc[pj * BJ_LD + pj], jqq = Sc[qj * BJ_LD + qj], jpq = Sc[pj * BJ_LD + qj];
+  const double a = Sc[pi * BJ_LD + pj], b = Sc[pi * BJ_LD + qj];
+  const double d = Sc[qi * BJ_LD + pj], e = Sc[qi * BJ_LD + qj];
+  double jp[2], jq[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    jp[h] = Jm[(ti + 16 * h) * BJ_LD + pj];
+    jq[h] = Jm[(ti + 16 * h) * BJ_LD + qj];
+  }
+  const double2 rj = bj_rotation(jpp, jqq, jpq);
+  const double2 ri = make_double2(__shfl(rj.x, ti, 16), __shfl(rj.y, ti, 16));
+  // block (ti, tj) becomes R_i^T X R_j
+  const double a1 = ri.x * a - ri.y * d, b1 = ri.x * b - ri.y * e;
+  const double d1 = ri.y * a + ri.x * d, e1 = ri.y * b + ri.x * e;
+  Sn[pi * BJ_LD + pj] = rj.x * a1 - rj.y * b1;
+  Sn[pi * BJ_LD + qj] = rj.y * a1 + rj.x * b1;
+  Sn[qi * BJ_LD + pj] = rj.x * d1 - rj.y * e1;
+  Sn[qi * BJ_LD + qj] = rj.y * d1 + rj.x * e1;
+  // columns pj, qj of J (the identity rotation rewrites them unchanged)
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    Jm[(ti + 16 * h) * BJ_LD + pj] = rj.x * jp[h] - rj.y * jq[h];
+    Jm[(ti + 16 * h) * BJ_LD + qj] = rj.y * jp[h] + rj.x * jq[h];
+  }
+  return rj.y != 0.0;
 }
 
 constexpr int BJ_TILE = BJ_W * BJ_LD;  // doubles of one padded BJ_W x BJ_W matrix in LDS
-constexpr int BJ_YLD = BJ_S + 1;       // row stride of a BJ_W x BJ_S product
+
+// float64 matrix instruction v_mfma_f64_16x16x4f64: operand A[i][k] on lane
+// i + 16 k, B[k][j] on lane j + 16 k, result D[i][j] on lane j + 16 (i mod 4),
+// register i / 4 (i, j < 16, k < 4)
+typedef double dbl4 __attribute__((ext_vector_type(4)));
 
 // One launch per round of the block Jacobi.  Workgroups [0, nsolve) take the
 // pairs of blocks of round rs: each builds its BJ_W x BJ_W principal
@@ -842,14 +891,15 @@ constexpr int BJ_YLD = BJ_S + 1;       // row stride of a BJ_W x BJ_S product
 // U_ui[:, half]^T A0_{ui uj} U_uj[:, half]).  With ra < 0 (the first launch)
 // A0 is the current matrix.  With part != null the apply workgroups of A
 // write the squared off-diagonal and total norms of their tiles of A1 to
-// part[2 w], part[2 w + 1] (w = tile index).  Workgroups of 256 threads;
-// thread (i, j) = (t / 16, t % 16).
+// part[2 w], part[2 w + 1] (w = tile index).  Workgroups of 256 threads: in
+// the inner rounds thread (i, j) = (t / 16, t % 16); the submatrix build and
+// the apply run on float64 matrix instructions, one 16 x 16 block per wave.
 __global__ __launch_bounds__(256) void bj_round_kernel(
     const double* __restrict__ A0, double* __restrict__ A1, double* __restrict__ V, int lda,
     int m, int nbk, int ra, const double* __restrict__ Ua, const double* __restrict__ fa, int rs,
     double* __restrict__ Us, double* __restrict__ fs, int nsolve, int ntile_a,
     double* __restrict__ part) {
-  __shared__ double L[4 * BJ_TILE + BJ_W * BJ_YLD];
+  __shared__ double L[3 * BJ_TILE];
   __shared__ int2 owner[64];  // block -> (pair, half) in round ra
   __shared__ int2 pairs[32];  // pair -> its two blocks in round ra
   __shared__ int moved;
@@ -890,109 +940,86 @@ __global__ __launch_bounds__(256) void bj_round_kernel(
       }
       __syncthreads();
       const int2 o1 = owner[bp], o2 = owner[bq];
-      const int2 pr1 = pairs[o1.x], pr2 = pairs[o2.x];
-      // the three tiles (pair 1, pair 1), (pair 1, pair 2), (pair 2, pair 2)
-      // of A0 and the two rotation products, all loads in flight at once
-      constexpr int NL = BJ_W * BJ_W / 256;
-      double xr[3][NL], jr[2][NL];
+      const int wv = t >> 6, l = t & 63, li = l & 15, lk = l >> 4;
+      if (wv < 3) {
+        // quadrant (qa, qb) of the new submatrix (blocks qa ? bq : bp and
+        // qb ? bq : bp), one wave each: Y = X Jj[:, cj .. cj + 15] with X the
+        // old tile of the two pairs, then Z = Ji[:, ci .. ci + 15]^T Y, on
+        // float64 matrix instructions
+        const int qa = wv == 2 ? 1 : 0, qb = wv == 0 ? 0 : 1;
+        const int2 oa = qa ? o2 : o1, ob = qb ? o2 : o1;
+        const int2 pa = pairs[oa.x], pb = pairs[ob.x];
+        const double* Ji = Ua + int64_t(oa.x) * BJ_W * BJ_W + 16 * oa.y;
+        const double* Jj = Ua + int64_t(ob.x) * BJ_W * BJ_W + 16 * ob.y;
+        // every operand load in flight at once
+        double xa[2][8], jb[8], ja[8];
 #pragma unroll
-      for (int k = 0; k < NL; ++k) {
-        const int e = t + 256 * k;
-        const int i = e / BJ_W, j = e % BJ_W;
-        const int g1i = bj_global(pr1.x, pr1.y, i), g1j = bj_global(pr1.x, pr1.y, j);
-        const int g2i = bj_global(pr2.x, pr2.y, i), g2j = bj_global(pr2.x, pr2.y, j);
-        xr[0][k] = (g1i < m && g1j < m) ? A0[int64_t(g1i) * lda + g1j] : 0.0;
-        xr[1][k] = (g1i < m && g2j < m) ? A0[int64_t(g1i) * lda + g2j] : 0.0;
-        xr[2][k] = (g2i < m && g2j < m) ? A0[int64_t(g2i) * lda + g2j] : 0.0;
-        jr[0][k] = Ua[int64_t(o1.x) * BJ_W * BJ_W + e];
-        jr[1][k] = Ua[int64_t(o2.x) * BJ_W * BJ_W + e];
-      }
-      double* X = L + BJ_TILE;
-      double* J1 = L + 2 * BJ_TILE;
-      double* J2 = L + 3 * BJ_TILE;
-      double* Y = L + 4 * BJ_TILE;
+        for (int s = 0; s < 8; ++s) {
+          const int gc = bj_global(pb.x, pb.y, 4 * s + lk);
 #pragma unroll
-      for (int k = 0; k < NL; ++k) {
-        const int e = t + 256 * k;
-        J1[(e / BJ_W) * BJ_LD + e % BJ_W] = jr[0][k];
-        J2[(e / BJ_W) * BJ_LD + e % BJ_W] = jr[1][k];
-      }
-#pragma unroll
-      for (int qd = 0; qd < 3; ++qd) {
-        // quadrant (qa, qb) of the new submatrix: blocks (qa ? bq : bp, qb ? bq : bp)
-        const int qa = qd == 2 ? 1 : 0, qb = qd == 0 ? 0 : 1;
-        const double* Ji = qa ? J2 : J1;
-        const double* Jj = qb ? J2 : J1;
-        const int ci = 16 * (qa ? o2.y : o1.y), cj = 16 * (qb ? o2.y : o1.y);
-#pragma unroll
-        for (int k = 0; k < NL; ++k) {
-          const int e = t + 256 * k;
-          X[(e / BJ_W) * BJ_LD + e % BJ_W] = xr[qd][k];
+          for (int h = 0; h < 2; ++h) {
+            const int gr = bj_global(pa.x, pa.y, 16 * h + li);
+            xa[h][s] = (gr < m && gc < m) ? A0[int64_t(gr) * lda + gc] : 0.0;
+          }
+          jb[s] = Jj[(4 * s + lk) * BJ_W + li];
+          ja[s] = Ji[(4 * s + lk) * BJ_W + li];
         }
-        __syncthreads();
-        // Y = X Jj[:, cj .. cj + 15]: rows 2 ti, 2 ti + 1 of column tj
-        double y0 = 0.0, y1 = 0.0;
-#pragma unroll 8
-        for (int x = 0; x < BJ_W; ++x) {
-          const double jv = Jj[x * BJ_LD + cj + tj];
-          y0 = fma(X[(2 * ti) * BJ_LD + x], jv, y0);
-          y1 = fma(X[(2 * ti + 1) * BJ_LD + x], jv, y1);
+        dbl4 y0 = {0.0, 0.0, 0.0, 0.0}, y1 = y0;
+#pragma unroll
+        for (int s = 0; s < 8; ++s) {
+          y0 = __builtin_amdgcn_mfma_f64_16x16x4f64(xa[0][s], jb[s], y0, 0, 0, 0);
+          y1 = __builtin_amdgcn_mfma_f64_16x16x4f64(xa[1][s], jb[s], y1, 0, 0, 0);
         }
-        Y[(2 * ti) * BJ_YLD + tj] = y0;
-        Y[(2 * ti + 1) * BJ_YLD + tj] = y1;
-        __syncthreads();
-        // Z = Ji[:, ci .. ci + 15]^T Y: entry (ti, tj)
-        double z = 0.0;
-#pragma unroll 8
-        for (int x = 0; x < BJ_W; ++x) z = fma(Ji[x * BJ_LD + ci + ti], Y[x * BJ_YLD + tj], z);
-        S0[(16 * qa + ti) * BJ_LD + 16 * qb + tj] = z;
-        if (qa != qb) S0[(16 * qb + tj) * BJ_LD + 16 * qa + ti] = z;
-        __syncthreads();  // X, Y are rewritten by the next quadrant
+        // the result layout is the B operand layout of the next product: lane
+        // j + 16 k holds Y[4 s + k][j] in register s of y0 (s < 4), y1 (s >= 4)
+        dbl4 z0 = {0.0, 0.0, 0.0, 0.0}, z1 = z0;
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+          z0 = __builtin_amdgcn_mfma_f64_16x16x4f64(ja[s], y0[s], z0, 0, 0, 0);
+          z1 = __builtin_amdgcn_mfma_f64_16x16x4f64(ja[s + 4], y1[s], z1, 0, 0, 0);
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const double z = z0[r] + z1[r];
+          const int i = lk + 4 * r;
+          S0[(16 * qa + i) * BJ_LD + 16 * qb + li] = z;
+          if (qa != qb) S0[(16 * qb + li) * BJ_LD + 16 * qa + i] = z;
+        }
       }
     }
     for (int e = t; e < BJ_W * BJ_W; e += 256)
       Jm[(e / BJ_W) * BJ_LD + e % BJ_W] = (e / BJ_W == e % BJ_W) ? 1.0 : 0.0;
     if (t == 0) moved = 0;
     __syncthreads();
-    const bool full = rs == 0;
-    const int inner = full ? BJ_W - 1 : BJ_S;
-    double* Sc = S0;
-    double* Sn = S1;
-    for (int r = 0; r < inner; ++r) {
-      int pi, qi, pj, qj;
-      bj_inner_pair(full, r, ti, pi, qi);
-      bj_inner_pair(full, r, tj, pj, qj);
-      // rotation k is formed on lanes k, k + 16, ... of each wave (tj = lane
-      // mod 16) and fetched by the lanes that need it (ti lies in 0 .. 15):
-      // one rotation per lane, and no barrier for the exchange
-      const double2 rl = bj_rotation(Sc, pj, qj);
-      const double2 rj = rl;
-      const double2 ri = make_double2(__shfl(rl.x, ti), __shfl(rl.y, ti));
-      if (ti == tj && ri.y != 0.0) moved = 1;  // every writer stores the same value
-      // block (ti, tj): rows pi, qi and columns pj, qj become R_i^T X R_j
-      const double a = Sc[pi * BJ_LD + pj], b = Sc[pi * BJ_LD + qj];
-      const double d = Sc[qi * BJ_LD + pj], e = Sc[qi * BJ_LD + qj];
-      const double a1 = ri.x * a - ri.y * d, b1 = ri.x * b - ri.y * e;
-      const double d1 = ri.y * a + ri.x * d, e1 = ri.y * b + ri.x * e;
-      Sn[pi * BJ_LD + pj] = rj.x * a1 - rj.y * b1;
-      Sn[pi * BJ_LD + qj] = rj.y * a1 + rj.x * b1;
-      Sn[qi * BJ_LD + pj] = rj.x * d1 - rj.y * e1;
-      Sn[qi * BJ_LD + qj] = rj.y * d1 + rj.x * e1;
-      // columns pj, qj of J on rows ti and ti + 16
-      if (rj.y != 0.0) {
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const int x = ti + 16 * h;
-          const double jp = Jm[x * BJ_LD + pj], jq = Jm[x * BJ_LD + qj];
-          Jm[x * BJ_LD + pj] = rj.x * jp - rj.y * jq;
-          Jm[x * BJ_LD + qj] = rj.y * jp + rj.x * jq;
-        }
+    bool mv = false;
+    if (rs == 0) {
+      // one cyclic sweep over all pairs of the submatrix
+      double* Sc = S0;
+      double* Sn = S1;
+      for (int r = 0; r < BJ_W - 1; ++r) {
+        int pi, qi, pj, qj;
+        circle_pair(BJ_W, r, ti, pi, qi);
+        circle_pair(BJ_W, r, tj, pj, qj);
+        mv |= bj_inner_round(Sc, Sn, Jm, ti, pi, qi, pj, qj);
+        __syncthreads();
+        double* tmp = Sc;
+        Sc = Sn;
+        Sn = tmp;
       }
-      __syncthreads();
-      double* tmp = Sc;
-      Sc = Sn;
-      Sn = tmp;
+    } else {
+      // the pairs across the two blocks: local index k meets
+      // BJ_S + (k + r) mod BJ_S in inner round r
+      for (int r = 0; r < BJ_S; r += 2) {
+        mv |= bj_inner_round(S0, S1, Jm, ti, ti, BJ_S + ((ti + r) & (BJ_S - 1)), tj,
+                             BJ_S + ((tj + r) & (BJ_S - 1)));
+        __syncthreads();
+        mv |= bj_inner_round(S1, S0, Jm, ti, ti, BJ_S + ((ti + r + 1) & (BJ_S - 1)), tj,
+                             BJ_S + ((tj + r + 1) & (BJ_S - 1)));
+        __syncthreads();
+      }
     }
+    if (ti == tj && mv) moved = 1;  // every writer stores the same value
+    __syncthreads();
     double* Uo = Us + int64_t(u) * BJ_W * BJ_W;
     for (int e = t; e < BJ_W * BJ_W; e += 256) Uo[e] = Jm[(e / BJ_W) * BJ_LD + e % BJ_W];
     if (t == 0) fs[u] = moved ? 1.0 : 0.0;
@@ -1020,86 +1047,70 @@ __global__ __launch_bounds__(256) void bj_round_kernel(
   int bpu = 0, bqu = 0, bpv, bqv;
   circle_pair(nbk, ra, v, bpv, bqv);
   if (on_a) circle_pair(nbk, ra, u, bpu, bqu);
-  double* X = L;
-  double* Uu = L + BJ_TILE;
-  double* Uv = L + 2 * BJ_TILE;
-  double* Y = L + 3 * BJ_TILE;
-  constexpr int NL = BJ_W * BJ_W / 256;
-  double xr[NL], ur[NL], vr[NL];
-#pragma unroll
-  for (int k = 0; k < NL; ++k) {
-    const int e = t + 256 * k;
-    const int i = e / BJ_W, j = e % BJ_W;
+  // wave (a, c) of the workgroup forms the 16 x 16 block (rows 16 a .., columns
+  // 16 c ..) of each stage on float64 matrix instructions; stage 1 puts
+  // Y = U_u^T X (a tile of A whose row pair u rotated) or Y = X into LDS, stage
+  // 2 takes Z = Y U_v (column pair v rotated) or Z = Y
+  const int wv = t >> 6, l = t & 63, li = l & 15, lk = l >> 4;
+  const int a = wv >> 1, c = wv & 1;
+  auto xval = [&](int i, int j) -> double {
     const int gj = bj_global(bpv, bqv, j);
-    xr[k] = 0.0;
     if (on_a) {
       const int gi = bj_global(bpu, bqu, i);
-      if (gi < m && gj < m) xr[k] = A0[int64_t(gi) * lda + gj];
-    } else {
-      const int row = rc * BJ_W + i;
-      if (row < m && gj < m) xr[k] = V[int64_t(row) * m + gj];
+      return (gi < m && gj < m) ? A0[int64_t(gi) * lda + gj] : 0.0;
     }
-    ur[k] = on_a ? Ua[int64_t(u) * BJ_W * BJ_W + e] : 0.0;
-    vr[k] = Ua[int64_t(v) * BJ_W * BJ_W + e];
-  }
+    const int row = rc * BJ_W + i;
+    return (row < m && gj < m) ? V[int64_t(row) * m + gj] : 0.0;
+  };
+  double* Y = L;
+  {
+    dbl4 y = {0.0, 0.0, 0.0, 0.0};
+    if (on_a && moved_u) {
+      const double* Uu = Ua + int64_t(u) * BJ_W * BJ_W;
+      double ua[8], xb[8];
 #pragma unroll
-  for (int k = 0; k < NL; ++k) {
-    const int e = t + 256 * k;
-    const int o = (e / BJ_W) * BJ_LD + e % BJ_W;
-    X[o] = xr[k];
-    Uu[o] = ur[k];
-    Uv[o] = vr[k];
+      for (int s = 0; s < 8; ++s) {
+        ua[s] = Uu[(4 * s + lk) * BJ_W + 16 * a + li];  // A[i][k] = U_u[4 s + k][16 a + i]
+        xb[s] = xval(4 * s + lk, 16 * c + li);          // B[k][j] = X[4 s + k][16 c + j]
+      }
+#pragma unroll
+      for (int s = 0; s < 8; ++s) y = __builtin_amdgcn_mfma_f64_16x16x4f64(ua[s], xb[s], y, 0, 0, 0);
+    } else {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) y[r] = xval(16 * a + lk + 4 * r, 16 * c + li);
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) Y[(16 * a + lk + 4 * r) * BJ_LD + 16 * c + li] = y[r];
   }
   __syncthreads();
-  // thread (ti, tj): rows ti, ti + 16 and columns tj, tj + 16 (16 lanes of
-  // one row group read 16 consecutive doubles: no LDS bank conflicts)
-  double z[2][2];
-  const double* Z = X;
-  if (on_a && moved_u) {
-    double y[2][2] = {{0.0, 0.0}, {0.0, 0.0}};
-#pragma unroll 8
-    for (int x = 0; x < BJ_W; ++x) {
-      const double u0 = Uu[x * BJ_LD + ti], u1 = Uu[x * BJ_LD + ti + 16];
-      const double x0 = X[x * BJ_LD + tj], x1 = X[x * BJ_LD + tj + 16];
-      y[0][0] = fma(u0, x0, y[0][0]);
-      y[0][1] = fma(u0, x1, y[0][1]);
-      y[1][0] = fma(u1, x0, y[1][0]);
-      y[1][1] = fma(u1, x1, y[1][1]);
-    }
-#pragma unroll
-    for (int a = 0; a < 2; ++a)
-#pragma unroll
-      for (int c = 0; c < 2; ++c) Y[(ti + 16 * a) * BJ_LD + tj + 16 * c] = y[a][c];
-    __syncthreads();
-    Z = Y;
-  }
+  dbl4 z;
   if (moved_v) {
-    z[0][0] = z[0][1] = z[1][0] = z[1][1] = 0.0;
-#pragma unroll 8
-    for (int y = 0; y < BJ_W; ++y) {
-      const double a0 = Z[ti * BJ_LD + y], a1 = Z[(ti + 16) * BJ_LD + y];
-      const double u0 = Uv[y * BJ_LD + tj], u1 = Uv[y * BJ_LD + tj + 16];
-      z[0][0] = fma(a0, u0, z[0][0]);
-      z[0][1] = fma(a0, u1, z[0][1]);
-      z[1][0] = fma(a1, u0, z[1][0]);
-      z[1][1] = fma(a1, u1, z[1][1]);
+    const double* Uv = Ua + int64_t(v) * BJ_W * BJ_W;
+    double ya[8], vb[8];
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+      ya[s] = Y[(16 * a + li) * BJ_LD + 4 * s + lk];  // A[i][k] = Y[16 a + i][4 s + k]
+      vb[s] = Uv[(4 * s + lk) * BJ_W + 16 * c + li];  // B[k][j] = U_v[4 s + k][16 c + j]
     }
+    dbl4 z0 = {0.0, 0.0, 0.0, 0.0}, z1 = z0;
+#pragma unroll
+    for (int s = 0; s < 8; s += 2) {
+      z0 = __builtin_amdgcn_mfma_f64_16x16x4f64(ya[s], vb[s], z0, 0, 0, 0);
+      z1 = __builtin_amdgcn_mfma_f64_16x16x4f64(ya[s + 1], vb[s + 1], z1, 0, 0, 0);
+    }
+    z = z0 + z1;
   } else {
 #pragma unroll
-    for (int a = 0; a < 2; ++a)
-#pragma unroll
-      for (int c = 0; c < 2; ++c) z[a][c] = Z[(ti + 16 * a) * BJ_LD + tj + 16 * c];
+    for (int r = 0; r < 4; ++r) z[r] = Y[(16 * a + lk + 4 * r) * BJ_LD + 16 * c + li];
   }
   double off = 0.0, all = 0.0;
+  const int j = 16 * c + li;
+  const int gj = bj_global(bpv, bqv, j);
+  if (gj < m) {
 #pragma unroll
-  for (int c = 0; c < 2; ++c) {
-    const int j = tj + 16 * c;
-    const int gj = bj_global(bpv, bqv, j);
-    if (gj >= m) continue;
-#pragma unroll
-    for (int a = 0; a < 2; ++a) {
-      const int i = ti + 16 * a;
-      const double val = z[a][c];
+    for (int r = 0; r < 4; ++r) {
+      const int i = 16 * a + lk + 4 * r;
+      const double val = z[r];
       if (on_a) {
         const int gi = bj_global(bpu, bqu, i);
         if (gi >= m || (u == v && i > j)) continue;
@@ -1278,8 +1289,14 @@ int jacobi_eig(double* A, double* A2, int m, int lda, double* Vw, double* theta,
       }
     }
   }
-  hipLaunchKernelGGL(jacobi_sort_kernel, dim3(nblk(m, 256)), dim3(256), 0, stream, cur, m, lda, Vw,
-                     theta, S, lds);
+  // the rotation log / block scratch is free again: it holds the permutation
+  check_span_d(log, size_t(m + 1) / 2, "jacobi permutation");
+  int* perm = reinterpret_cast<int*>(log.p);
+  hipLaunchKernelGGL(jacobi_rank_kernel, dim3(nblk(m, 256)), dim3(256), 0, stream, cur, m, lda,
+                     theta, perm);
+  FD_LAUNCH_CHECK();
+  hipLaunchKernelGGL(jacobi_permute_kernel, dim3(nblk(int64_t(m) * m, 256)), dim3(256), 0, stream,
+                     Vw, m, perm, S, lds);
   FD_LAUNCH_CHECK();
   return sweeps;
 }
