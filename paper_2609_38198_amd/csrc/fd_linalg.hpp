@@ -38,8 +38,9 @@ void fill_normal(float* Z, int64_t ldz, int64_t N, int nb, const int* flags, uin
 // out[c] = ||W[:, c] - theta_c Y[:, c]||_2 for c < nc (Y, W share ld).
 void residual_norms(const float* Y, const float* W, int64_t ld, int nc, const double* theta,
                     int64_t N, FSpanD part, double* out, hipStream_t stream);
-// Symmetric eigensolve of A (m x m, m <= 1024, overwritten; A2 an m x m
-// scratch with the same ld): theta descending, S columns.  Vw: m x m scratch
+// Symmetric eigensolve of A (m x m, m <= 1024, overwritten; only its upper
+// triangle is read; A2 an m x m scratch with the same ld): theta descending,
+// S columns.  Vw: m x m scratch
 // (ld m); norms: 2 doubles of
 // scratch; log: jacobi_log_doubles(m) doubles (enough for every size up to m;
 // the rotation log of the one-workgroup path for m <= 192, the block

@@ -460,7 +460,9 @@ void residual_norms(const float* Y, const float* W, int64_t ld, int nc, const do
 //     the others only its cross-block pairs: every pair of indices meets once
 //     per sweep.  One launch per round (bj_round_kernel) applies round r and
 //     solves round r + 1 side by side (A double-buffered); a sweep takes
-//     m / BJ_S - 1 launches instead of m - 1.  After each sweep the
+//     m / BJ_S - 1 launches instead of m - 1; A is first made exactly
+//     symmetric from its upper triangle (the submatrix builds read tiles
+//     through their transposes).  After each sweep the
 //     off-diagonal Frobenius norm is checked on the host (one pair of
 //     scalars read back).
 // On exit theta (m) holds the eigenvalues sorted descending and S (m x m,
@@ -477,17 +479,17 @@ __device__ __forceinline__ void circle_pair(int me, int round, int k, int& p, in
 
 // rotation (c, s) annihilating A_pq: t = tan of the angle is the smaller
 // root of t^2 + 2 tau t - 1 = 0, tau = (aqq - app) / (2 apq) (the 2 x 2
-// symmetric Schur decomposition of Golub & Van Loan).  With d = aqq - app, r = sqrt(d^2 + 4 apq^2) and e = |d| + r, the tangent of
-// the rotation angle is t = sign(d) 2 apq / e, so (c, s) is the unit vector
-// along (e, sign(d) 2 apq).  r only sets the angle: it is taken in single
-// precision, and the normalisation 1 / |(e, 2 apq)| in float64 keeps
-// c^2 + s^2 = 1 to float64 rounding whatever r's error (about 1e-7 of r,
-// which leaves about 1e-7 of apq unannihilated; the next sweep takes it).
+// symmetric Schur decomposition of Golub & Van Loan).  With d = aqq - app,
+// r = sqrt(d^2 + 4 apq^2) and e = |d| + r, t = sign(d) 2 apq / e, so (c, s)
+// is the unit vector along (e, sign(d) 2 apq), normalised as a vector
+// (1 / |(e, 2 apq)|, which keeps c^2 + s^2 = 1 to float64 rounding): one
+// square root and one reciprocal square root on the dependent path, no
+// division.
 __device__ __forceinline__ void jacobi_rotation(double app, double aqq, double apq, double& c,
                                                 double& s) {
   const double d = aqq - app;
   const double a2 = 2.0 * apq;
-  const double r = double(sqrtf(float(fma(d, d, a2 * a2))));
+  const double r = sqrt(fma(d, d, a2 * a2));
   const double e = fabs(d) + r;
   const double q = rsqrt(fma(e, e, a2 * a2));
   c = e * q;
@@ -515,8 +517,17 @@ __global__ void jacobi_init_kernel(double* __restrict__ V, int m) {
   if (e < int64_t(m) * m) V[e] = (e / m == e % m) ? 1.0 : 0.0;
 }
 
-// theta = diag(A) sorted descending (ties by index), perm[rank] = the index
-// of that rank; every workgroup stages the diagonal (m <= 1024) in LDS
+// whether diagonal entry (dj, j) sorts before (di, i): descending, ties by
+// index, NaN after every number (ties among NaNs by index).  A strict total
+// order for any input, so the ranks below always form a permutation.
+__device__ __forceinline__ bool sorts_before(double dj, int j, double di, int i) {
+  const bool nj = dj != dj, ni = di != di;
+  if (nj || ni) return !nj || (ni && j < i);
+  return dj > di || (dj == di && j < i);
+}
+
+// theta = diag(A) sorted descending, perm[rank] = the index of that rank;
+// every workgroup stages the diagonal (m <= 1024) in LDS
 __global__ __launch_bounds__(256) void jacobi_rank_kernel(const double* __restrict__ A, int m,
                                                           int lda, double* __restrict__ theta,
                                                           int* __restrict__ perm) {
@@ -527,22 +538,22 @@ __global__ __launch_bounds__(256) void jacobi_rank_kernel(const double* __restri
   if (i >= m) return;
   const double di = dg[i];
   int rank = 0;
-  for (int j = 0; j < m; ++j) {
-    const double dj = dg[j];
-    rank += (dj > di || (dj == di && j < i)) ? 1 : 0;
-  }
+  for (int j = 0; j < m; ++j) rank += (j != i && sorts_before(dg[j], j, di, i)) ? 1 : 0;
   theta[rank] = di;
   perm[rank] = i;
 }
 
-// S[r][k] = V[r][perm[k]]: the columns of V in rank order
+// S[r][k] = V[r][perm[k]]: the columns of V in rank order (perm is a
+// permutation of 0 .. m - 1 by construction; the clamp keeps the gather in
+// range whatever it holds)
 __global__ __launch_bounds__(256) void jacobi_permute_kernel(const double* __restrict__ V, int m,
                                                              const int* __restrict__ perm,
                                                              double* __restrict__ S, int lds) {
   const int64_t e = int64_t(blockIdx.x) * 256 + threadIdx.x;
   if (e >= int64_t(m) * m) return;
   const int r = int(e / m), k = int(e % m);
-  S[int64_t(r) * lds + k] = V[int64_t(r) * m + perm[k]];
+  const int src = int(min(unsigned(perm[k]), unsigned(m - 1)));
+  S[int64_t(r) * lds + k] = V[int64_t(r) * m + src];
 }
 
 // ---- one-workgroup variant for m <= JL_MAX
@@ -830,6 +841,20 @@ __device__ __forceinline__ double2 bj_rotation(double app, double aqq, double ap
   return skip ? make_double2(1.0, 0.0) : make_double2(c, sn);
 }
 
+// x if keep, else +0.0, by a bit mask: no select, so the load that produced x
+// is not moved behind a branch
+__device__ __forceinline__ double masked(double x, bool keep) {
+  return __longlong_as_double(__double_as_longlong(x) & (keep ? -1LL : 0LL));
+}
+
+// x of lane (l + 1) mod 16 of this lane's 16-lane row (DPP row rotate)
+__device__ __forceinline__ double row_next(double x) {
+  constexpr int ROW_ROR_15 = 0x12F;
+  const int lo = __builtin_amdgcn_mov_dpp(__double2loint(x), ROW_ROR_15, 0xF, 0xF, false);
+  const int hi = __builtin_amdgcn_mov_dpp(__double2hiint(x), ROW_ROR_15, 0xF, 0xF, false);
+  return __hiloint2double(hi, lo);
+}
+
 // One inner round on the BJ_W x BJ_W submatrix Sc -> Sn and the rotation
 // product Jm, for thread (ti, tj) with pairs (pi, qi) = pair ti and
 // (pj, qj) = pair tj of the round.  Every LDS read comes first (the entries of
@@ -951,19 +976,31 @@ __global__ __launch_bounds__(256) void bj_round_kernel(
         const int2 pa = pairs[oa.x], pb = pairs[ob.x];
         const double* Ji = Ua + int64_t(oa.x) * BJ_W * BJ_W + 16 * oa.y;
         const double* Jj = Ua + int64_t(ob.x) * BJ_W * BJ_W + 16 * ob.y;
-        // every operand load in flight at once
+        // every operand load in flight at once, none behind a branch: padding
+        // rows and columns (index >= m) read a clamped in-range entry and are
+        // zeroed (32-bit offsets: m, lda <= 1024).  A0 is exactly symmetric,
+        // so X[16 h + i][4 s + k] is read as A0[col 4 s + k][row 16 h + i]:
+        // the 16 lanes of a k read 16 consecutive doubles, and a load touches
+        // four 128-byte lines instead of sixteen partly used ones
         double xa[2][8], jb[8], ja[8];
+        int co[2];
+        bool cv[2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int gr = bj_global(pa.x, pa.y, 16 * h + li);
+          cv[h] = gr < m;
+          co[h] = min(gr, m - 1);
+        }
 #pragma unroll
         for (int s = 0; s < 8; ++s) {
           const int gc = bj_global(pb.x, pb.y, 4 * s + lk);
+          const int ro = int(__umul24(unsigned(min(gc, m - 1)), unsigned(lda)));
 #pragma unroll
-          for (int h = 0; h < 2; ++h) {
-            const int gr = bj_global(pa.x, pa.y, 16 * h + li);
-            xa[h][s] = (gr < m && gc < m) ? A0[int64_t(gr) * lda + gc] : 0.0;
-          }
+          for (int h = 0; h < 2; ++h) xa[h][s] = masked(A0[ro + co[h]], cv[h] && gc < m);
           jb[s] = Jj[(4 * s + lk) * BJ_W + li];
           ja[s] = Ji[(4 * s + lk) * BJ_W + li];
         }
+        __builtin_amdgcn_sched_barrier(0);  // all loads issued before the first wait
         dbl4 y0 = {0.0, 0.0, 0.0, 0.0}, y1 = y0;
 #pragma unroll
         for (int s = 0; s < 8; ++s) {
@@ -1007,15 +1044,49 @@ __global__ __launch_bounds__(256) void bj_round_kernel(
         Sn = tmp;
       }
     } else {
-      // the pairs across the two blocks: local index k meets
-      // BJ_S + (k + r) mod BJ_S in inner round r
-      for (int r = 0; r < BJ_S; r += 2) {
-        mv |= bj_inner_round(S0, S1, Jm, ti, ti, BJ_S + ((ti + r) & (BJ_S - 1)), tj,
-                             BJ_S + ((tj + r) & (BJ_S - 1)));
+      // the pairs across the two blocks: local index k meets q(k) =
+      // BJ_S + (k + r) mod BJ_S in inner round r.  Thread (ti, tj) keeps
+      // a = S[ti][tj], b = S[ti][q(tj)] and J[ti + 16 h][tj], J[ti + 16 h][q(tj)]
+      // in registers (J = I at the start); as q(tj) of the next round is
+      // q(tj + 1) of this one, b and the q-column of J pass to the next lane of
+      // the 16-lane row after each round.  LDS keeps the whole submatrix for
+      // the rotations' entries and the entries d = S[q(ti)][tj], e =
+      // S[q(ti)][q(tj)] (written by other rows).
+      double a = S0[ti * BJ_LD + tj], b = S0[ti * BJ_LD + BJ_S + tj];
+      double jp[2] = {ti == tj ? 1.0 : 0.0, 0.0}, jq[2] = {0.0, ti == tj ? 1.0 : 0.0};
+#pragma unroll 2
+      for (int r = 0; r < BJ_S; ++r) {
+        const double* Sc = (r & 1) ? S1 : S0;
+        double* Sn = (r & 1) ? S0 : S1;
+        const int qi = BJ_S + ((ti + r) & (BJ_S - 1)), qj = BJ_S + ((tj + r) & (BJ_S - 1));
+        const double app = Sc[tj * BJ_LD + tj], aqq = Sc[qj * BJ_LD + qj];
+        const double apq = Sc[tj * BJ_LD + qj];
+        const double d = Sc[qi * BJ_LD + tj], e = Sc[qi * BJ_LD + qj];
+        const double2 rj = bj_rotation(app, aqq, apq);
+        const double2 ri = make_double2(__shfl(rj.x, ti, 16), __shfl(rj.y, ti, 16));
+        const double a1 = ri.x * a - ri.y * d, b1 = ri.x * b - ri.y * e;
+        const double d1 = ri.y * a + ri.x * d, e1 = ri.y * b + ri.x * e;
+        a = rj.x * a1 - rj.y * b1;
+        b = rj.y * a1 + rj.x * b1;
+        Sn[ti * BJ_LD + tj] = a;
+        Sn[ti * BJ_LD + qj] = b;
+        Sn[qi * BJ_LD + tj] = rj.x * d1 - rj.y * e1;
+        Sn[qi * BJ_LD + qj] = rj.y * d1 + rj.x * e1;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const double jn = rj.x * jp[h] - rj.y * jq[h];
+          jq[h] = row_next(rj.y * jp[h] + rj.x * jq[h]);
+          jp[h] = jn;
+        }
+        b = row_next(b);
+        mv |= rj.y != 0.0;
         __syncthreads();
-        mv |= bj_inner_round(S1, S0, Jm, ti, ti, BJ_S + ((ti + r + 1) & (BJ_S - 1)), tj,
-                             BJ_S + ((tj + r + 1) & (BJ_S - 1)));
-        __syncthreads();
+      }
+      // after BJ_S rounds q(tj) = BJ_S + tj again
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        Jm[(ti + 16 * h) * BJ_LD + tj] = jp[h];
+        Jm[(ti + 16 * h) * BJ_LD + BJ_S + tj] = jq[h];
       }
     }
     if (ti == tj && mv) moved = 1;  // every writer stores the same value
@@ -1053,14 +1124,15 @@ __global__ __launch_bounds__(256) void bj_round_kernel(
   // 2 takes Z = Y U_v (column pair v rotated) or Z = Y
   const int wv = t >> 6, l = t & 63, li = l & 15, lk = l >> 4;
   const int a = wv >> 1, c = wv & 1;
-  auto xval = [&](int i, int j) -> double {
-    const int gj = bj_global(bpv, bqv, j);
-    if (on_a) {
-      const int gi = bj_global(bpu, bqu, i);
-      return (gi < m && gj < m) ? A0[int64_t(gi) * lda + gj] : 0.0;
-    }
-    const int row = rc * BJ_W + i;
-    return (row < m && gj < m) ? V[int64_t(row) * m + gj] : 0.0;
+  // this lane's column of X in both stages is 16 c + li; loads are clamped
+  // into the matrix and padding zeroed, so none sits behind a branch
+  const int gjl = bj_global(bpv, bqv, 16 * c + li);
+  const int gjc = min(gjl, m - 1);
+  const double* xb_ = on_a ? A0 : V;
+  const unsigned xld = unsigned(on_a ? lda : m);
+  auto xval = [&](int i) -> double {
+    const int row = on_a ? bj_global(bpu, bqu, i) : rc * BJ_W + i;
+    return masked(xb_[int(__umul24(unsigned(min(row, m - 1)), xld)) + gjc], row < m && gjl < m);
   };
   double* Y = L;
   {
@@ -1071,13 +1143,14 @@ __global__ __launch_bounds__(256) void bj_round_kernel(
 #pragma unroll
       for (int s = 0; s < 8; ++s) {
         ua[s] = Uu[(4 * s + lk) * BJ_W + 16 * a + li];  // A[i][k] = U_u[4 s + k][16 a + i]
-        xb[s] = xval(4 * s + lk, 16 * c + li);          // B[k][j] = X[4 s + k][16 c + j]
+        xb[s] = xval(4 * s + lk);                       // B[k][j] = X[4 s + k][16 c + j]
       }
+      __builtin_amdgcn_sched_barrier(0);  // all loads issued before the first wait
 #pragma unroll
       for (int s = 0; s < 8; ++s) y = __builtin_amdgcn_mfma_f64_16x16x4f64(ua[s], xb[s], y, 0, 0, 0);
     } else {
 #pragma unroll
-      for (int r = 0; r < 4; ++r) y[r] = xval(16 * a + lk + 4 * r, 16 * c + li);
+      for (int r = 0; r < 4; ++r) y[r] = xval(16 * a + lk + 4 * r);
     }
 #pragma unroll
     for (int r = 0; r < 4; ++r) Y[(16 * a + lk + 4 * r) * BJ_LD + 16 * c + li] = y[r];
@@ -1092,6 +1165,7 @@ __global__ __launch_bounds__(256) void bj_round_kernel(
       ya[s] = Y[(16 * a + li) * BJ_LD + 4 * s + lk];  // A[i][k] = Y[16 a + i][4 s + k]
       vb[s] = Uv[(4 * s + lk) * BJ_W + 16 * c + li];  // B[k][j] = U_v[4 s + k][16 c + j]
     }
+    __builtin_amdgcn_sched_barrier(0);  // all loads issued before the first wait
     dbl4 z0 = {0.0, 0.0, 0.0, 0.0}, z1 = z0;
 #pragma unroll
     for (int s = 0; s < 8; s += 2) {
@@ -1149,6 +1223,14 @@ __global__ __launch_bounds__(256) void bj_round_kernel(
       part[2 * w + 1] = r1[0];
     }
   }
+}
+
+// A[r][c] = A[c][r] for r > c: A exactly symmetric, from its upper triangle
+__global__ void symmetrize_kernel(double* __restrict__ A, int m, int lda) {
+  const int64_t e = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (e >= int64_t(m) * m) return;
+  const int r = int(e / m), c = int(e % m);
+  if (r > c) A[int64_t(r) * lda + c] = A[int64_t(c) * lda + r];
 }
 
 // part[2 b], part[2 b + 1] = squared off-diagonal and total Frobenius norms of
@@ -1254,6 +1336,10 @@ int jacobi_eig(double* A, double* A2, int m, int lda, double* Vw, double* theta,
     double* F[2] = {U[1] + size_t(P) * BJ_W * BJ_W, U[1] + size_t(P) * BJ_W * BJ_W + P};
     double* part = F[1] + P;
     double* nxt = A2;
+    // the submatrix builds read A through its transpose
+    hipLaunchKernelGGL(symmetrize_kernel, dim3(nblk(int64_t(m) * m, 256)), dim3(256), 0, stream, A,
+                       m, lda);
+    FD_LAUNCH_CHECK();
     auto check = [&](int nparts) {
       hipLaunchKernelGGL(offnorm_finish_kernel, dim3(1), dim3(256), 0, stream, part, nparts,
                          norms);
