@@ -36,6 +36,12 @@
  *    (13 < D <= 30, 32 < D <= 62) switch to one that keeps it.  Beyond
  *    B = 200 the dropped fourth-order piece products can reach the 1e-5 bar
  *    (1.1e-5 measured at B = 400, D = 30).
+ *  - Exponent range (float32 X): the offsets enter the contraction as float16
+ *    pieces, so B above 65488 cannot be formed at all.  There the
+ *    asynchronous entry points fill their outputs with NaN (fd_degree_dyadic:
+ *    when its largest bandwidth is beyond), fd_block_lanczos and
+ *    fd_continuation return FD_ERR_UNSUPPORTED (the continuation's earlier
+ *    steps stay valid), and the flow ends its sweep before such a probe.
  *  - Non-finite X: every entry point scans X on the device first.  The
  *    asynchronous ones (fd_kernel_matmul, fd_kernel_matmul_noalloc, fd_degree,
  *    fd_degree_dyadic) then fill all their outputs with NaN; the eigensolver,
@@ -292,7 +298,16 @@ typedef struct fd_flow_probe {
   int32_t level;       /* cascade level of the probe (0 for fd_beta_flow) */
 } fd_flow_probe;
 
-typedef enum fd_flow_exit { FD_FLOW_BRACKET = 0, FD_FLOW_WALL = 1, FD_FLOW_BUDGET = 2 } fd_flow_exit;
+/* Why a sweep ended: a bracket of V_total (then the vertex probe), the Perron
+ * wall, the probe budget, or the next dyadic bandwidth lies beyond the float32
+ * path's exponent range (beta log2(e) max ||x - mean||^2 > 65488; not probed;
+ * the bandwidth is chosen as on the budget). */
+typedef enum fd_flow_exit {
+  FD_FLOW_BRACKET = 0,
+  FD_FLOW_WALL = 1,
+  FD_FLOW_BUDGET = 2,
+  FD_FLOW_RANGE = 3
+} fd_flow_exit;
 
 void fd_flow_default_opts(fd_flow_opts* o);
 
@@ -308,7 +323,9 @@ void fd_flow_default_opts(fd_flow_opts* o);
  *     eigenpairs at beta_x as in fd_block_lanczos.
  * Returns FD_ERR_NOT_CONVERGED (outputs valid) when the solve at beta_x stopped
  * before k pairs converged, FD_ERR_PERRON_WALL (records valid, nothing else)
- * when already the first probe is past the wall. */
+ * when already the first probe is past the wall, FD_ERR_UNSUPPORTED
+ * (exit_reason FD_FLOW_RANGE, nothing else) when already the first bandwidth
+ * is beyond the exponent range. */
 fd_status fd_beta_flow(const void* X, fd_dtype xt, int64_t N, int64_t D, int64_t ldx, float alpha,
                        int64_t b, int64_t k, const fd_flow_opts* fopts,
                        const fd_lanczos_opts* opts, fd_flow_probe* probes, int64_t* nprobes,

@@ -30,7 +30,7 @@ FD_F32, FD_BF16 = 0, 1
 FD_OP_KERNEL_MATMUL, FD_OP_DEGREE, FD_OP_BLOCK_LANCZOS, FD_OP_CONTINUATION = 0, 1, 2, 3
 FD_OP_BETA_FLOW = 4
 FD_OP_DEGREE_DYADIC = 5
-FLOW_EXIT = {0: "bracket", 1: "wall", 2: "budget"}
+FLOW_EXIT = {0: "bracket", 1: "wall", 2: "budget", 3: "range"}
 
 EXPORTS = (
     "fd_lanczos_default_opts", "fd_workspace_size", "fd_kernel_matmul", "fd_degree",
@@ -453,7 +453,7 @@ def flow_default_opts(**kw) -> FlowOpts:
 class Flow:
     probes: list       # per-probe records (dicts), in the order run
     beta_x: float      # achieved bandwidth
-    reason: str        # "bracket", "wall" or "budget"
+    reason: str        # "bracket", "wall", "budget" or "range"
     evals: list
     evecs: torch.Tensor
     psi: Optional[torch.Tensor]

@@ -468,6 +468,7 @@ fd_status fd_kernel_matmul(const void* Xr, int64_t Nr, const void* Xc, int64_t N
     // same base pointer and ldx: index i names the same point in both sets
     const bool diag = (Xr == Xc);
     product_apply(w, sl, sr, V, ldv, int(b), Y, ldy, diag, st);
+    launch_range_check(xt, w.centre, beta, w.flag, st);
     launch_poison(w.flag, Y, Nr, b, ldy, st);
   });
 }
@@ -504,6 +505,7 @@ fd_status fd_kernel_matmul_noalloc(const void* Xr, int64_t Nr, const void* Xc, i
     launch_pack_points(Xc, xt, Nc, D, ldx, beta, false, w.cols, &w.centre, st);
     const bool diag = (Xr == Xc);
     product_apply(w, sl, sr, V, ldv, int(b), Y, ldy, diag, st);
+    launch_range_check(xt, w.centre, beta, w.flag, st);
     launch_poison(w.flag, Y, Nr, b, ldy, st);
   });
 }
@@ -528,6 +530,7 @@ fd_status fd_degree(const void* X, fd_dtype xt, int64_t N, int64_t D, int64_t ld
     hipStream_t st = static_cast<hipStream_t>(stream);
     launch_scan_nonfinite(X, xt, N, D, ldx, w.flag, true, st);
     degree_run(w, X, xt, N, D, ldx, beta, alpha, q, d, s, s_off, true, st);
+    launch_range_check(xt, w.centre, beta, w.flag, st);
     for (float* v : {q, d, s}) launch_poison(w.flag, v, N, 1, 1, st);
     launch_poison(w.flag, s_off, 1, st);
   });
@@ -555,6 +558,8 @@ fd_status fd_degree_dyadic(const void* X, fd_dtype xt, int64_t N, int64_t D, int
     hipStream_t st = static_cast<hipStream_t>(stream);
     launch_scan_nonfinite(X, xt, N, D, ldx, w.flag, true, st);
     degree_run_dyadic(w, X, xt, N, D, ldx, beta0, int(nbeta), alpha, q, d, s, s_off, st);
+    // the largest bandwidth decides (every level's outputs are poisoned)
+    launch_range_check(xt, w.centre, std::ldexp(double(beta0), nbeta - 1), w.flag, st);
     for (float* v : {q, d, s}) launch_poison(w.flag, v, int64_t(nbeta) * N, 1, 1, st);
     launch_poison(w.flag, s_off, nbeta, st);
   });

@@ -214,8 +214,10 @@ struct FlowOutcome {
 };
 
 // One sweep of the flow from `beta`: dyadic probes until a bracket (then one
-// vertex probe), the wall or max_probes.  The driver runs the probes and owns
-// their vectors:
+// vertex probe), the wall, max_probes or a bandwidth outside the driver's
+// exponent range (not probed; the sweep ends as on the probe budget).  The
+// driver runs the probes and owns their vectors:
+//   bool drv.in_range(double beta)   whether a probe at beta can be run;
 //   FlowProbe drv.probe(double beta, int role, int t, bool from_keep)
 //       solve at beta (role 0 dyadic, 1 vertex, 2 final re-solve), its Markov
 //       vectors into the driver's "new" slot, started from the "keep" slot
@@ -234,6 +236,10 @@ FlowOutcome run_flow_logic(Driver& drv, int64_t N, double beta, bool warm, int m
   FlowProbe fin;
   bool fin_in_q = false;
   for (int t = 0; t < max_probes; ++t) {
+    if (!drv.in_range(beta)) {
+      reason = FD_FLOW_RANGE;
+      break;
+    }
     FlowProbe p = drv.probe(beta, 0, t, have_keep);
     in_q = beta;
     if (!p.admissible) {
@@ -279,7 +285,7 @@ FlowOutcome run_flow_logic(Driver& drv, int64_t N, double beta, bool warm, int m
   res.any = true;
   if (reason != FD_FLOW_BRACKET) {
     fin = pr.back();
-    if (reason == FD_FLOW_BUDGET) {
+    if (reason == FD_FLOW_BUDGET || reason == FD_FLOW_RANGE) {
       for (const FlowProbe& q : pr)
         if (q.complete() && (!fin.complete() || q.v_total < fin.v_total)) fin = q;
     }

@@ -138,6 +138,26 @@ void launch_radius_more(const void* X2, fd_dtype xt, int64_t n2, int64_t D, int6
 // 2.8e-6 at 50 and 5.4e-6 at 100 on the molecule-like set).
 constexpr double EXP_BUDGET = 64.0;
 
+// Exponent range of the float32 path: the row and column offsets
+// -beta log2(e) ||x - mu||^2 (+15 on the row side) enter the contraction as
+// float16 pieces, which hold magnitudes up to 65504.  Above
+// beta log2(e) max ||x - mu||^2 = HX_EXP_RANGE the exponent cannot be formed:
+// the asynchronous entry points fill their outputs with NaN, the synchronous
+// ones refuse (FD_ERR_UNSUPPORTED) and the flow stops before such a probe.
+// (bfloat16 X forms its exponent in float32 and has no such limit.)
+constexpr double HX_EXP_RANGE = 65504.0 - 16.0;
+// Whether bandwidth beta is inside the exponent range for points of squared
+// centred radius r2max (always for bfloat16 X).
+bool exponent_in_range(fd_dtype xt, double beta, double r2max);
+// r2max of a centring (host copy; synchronises the stream; 0 for bfloat16).
+double exponent_radius(fd_dtype xt, const CentreWs& c, hipStream_t stream);
+// Synchronous check: FD_ERR_UNSUPPORTED when beta is outside the range.
+void require_exponent_range(fd_dtype xt, const CentreWs& c, double beta, hipStream_t stream);
+// Asynchronous check: sets bit 2 of *flag (the non-finite-input flag, whose
+// poison fills the outputs with NaN) when beta is outside the range.
+void launch_range_check(fd_dtype xt, const CentreWs& c, double beta, int* flag,
+                        hipStream_t stream);
+
 // Floats per point of a pack region (large enough for either pack kind).
 int pack_floats_per_point(int64_t D);
 

@@ -9,6 +9,8 @@
 // kernel matrix is never stored.
 #include <hip/hip_runtime.h>
 
+#include <cstring>
+
 #include <algorithm>
 #include <cmath>
 
@@ -140,6 +142,47 @@ void launch_radius_more(const void* X2, fd_dtype xt, int64_t n2, int64_t D, int6
   const unsigned grid = unsigned(std::min<int64_t>(1024, std::max<int64_t>(1, ceil_div(n2, 256))));
   hipLaunchKernelGGL(radius_max_kernel, dim3(grid), dim3(256), 0, stream,
                      static_cast<const float*>(X2), n2, int(D), ldx, c.mu, c.r2max);
+  FD_LAUNCH_CHECK();
+}
+
+// ------------------------------------------------------------------ exponent range
+
+__global__ void range_check_kernel(const unsigned long long* __restrict__ r2max, double bl,
+                                   int* __restrict__ flag) {
+  const double r2 = __longlong_as_double(static_cast<long long>(*r2max));
+  if (!(bl * r2 <= HX_EXP_RANGE)) atomicOr(flag, 2);
+}
+
+bool exponent_in_range(fd_dtype xt, double beta, double r2max) {
+  return xt != FD_F32 || beta * LOG2E * r2max <= HX_EXP_RANGE;
+}
+
+double exponent_radius(fd_dtype xt, const CentreWs& c, hipStream_t stream) {
+  if (xt != FD_F32) return 0.0;
+  unsigned long long bits = 0;
+  FD_HIP_CHECK(hipMemcpyAsync(&bits, c.r2max, sizeof(bits), hipMemcpyDeviceToHost, stream));
+  FD_HIP_CHECK(hipStreamSynchronize(stream));
+  double r2 = 0.0;
+  std::memcpy(&r2, &bits, sizeof(r2));
+  return r2;
+}
+
+void require_exponent_range(fd_dtype xt, const CentreWs& c, double beta, hipStream_t stream) {
+  if (xt != FD_F32) return;
+  const double r2 = exponent_radius(xt, c, stream);
+  if (!exponent_in_range(xt, beta, r2))
+    throw Error{FD_ERR_UNSUPPORTED,
+                "beta log2(e) max ||x - mean||^2 = " + std::to_string(beta * LOG2E * r2) +
+                    " is beyond the float32 path's exponent range (" +
+                    std::to_string(HX_EXP_RANGE) + ")"};
+}
+
+void launch_range_check(fd_dtype xt, const CentreWs& c, double beta, int* flag,
+                        hipStream_t stream) {
+  if (xt != FD_F32) return;
+  FD_REQUIRE(c.r2max != nullptr && flag != nullptr, FD_ERR_INVALID_ARG,
+             "internal: range check words");
+  hipLaunchKernelGGL(range_check_kernel, dim3(1), dim3(1), 0, stream, c.r2max, beta * LOG2E, flag);
   FD_LAUNCH_CHECK();
 }
 

@@ -656,7 +656,9 @@ struct DeviceFlowDriver {
   int level;
   std::vector<fd_flow_probe>& out;
   hipStream_t st;
+  double r2max;  // max ||x - mean||^2 of X (host copy)
 
+  bool in_range(double beta) const { return exponent_in_range(xt, beta, r2max); }
   FlowProbe probe(double beta, int role, int t, bool from_keep) {
     const uint64_t lseed = uint64_t(level) * 1000003u;
     const uint64_t off = role == 0   ? lseed + uint64_t(t) * 7919u
@@ -678,8 +680,26 @@ static FlowOutcome run_flow(FlowWs& f, const void* X, fd_dtype xt, int64_t N, in
                             int64_t ldx, double alpha, int bb, int kk, double beta, bool warm,
                             const FlowParams& fp, const fd_lanczos_opts& o, int max_probes,
                             int level, std::vector<fd_flow_probe>& out, hipStream_t st) {
-  DeviceFlowDriver drv{f, X, xt, N, D, ldx, alpha, bb, kk, fp, o, level, out, st};
+  // the radius that bounds the exponent range: X's centring is the same for
+  // every probe
+  launch_centre(X, xt, N, D, ldx, f.sw.deg.centre, st);
+  const double r2 = exponent_radius(xt, f.sw.deg.centre, st);
+  DeviceFlowDriver drv{f, X, xt, N, D, ldx, alpha, bb, kk, fp, o, level, out, st, r2};
   return logic::run_flow_logic(drv, N, beta, warm, max_probes);
+}
+
+// Status and message of a sweep that produced nothing admissible.
+static fd_status flow_nothing_admissible(const FlowOutcome& R, int level, int32_t* exit_reason) {
+  const std::string of = level < 0 ? std::string() : " of cascade level " + std::to_string(level);
+  if (R.reason == FD_FLOW_RANGE) {
+    *exit_reason = FD_FLOW_RANGE;
+    set_error("the first bandwidth" + of + " is beyond the float32 exponent range " +
+              "(beta log2(e) max ||x - mean||^2 > " + std::to_string(HX_EXP_RANGE) + ")");
+    return FD_ERR_UNSUPPORTED;
+  }
+  *exit_reason = FD_FLOW_WALL;
+  set_error("the first probe" + of + " is already past the Perron wall (g_P <= kappa_P eta)");
+  return FD_ERR_PERRON_WALL;
 }
 
 }  // namespace fd
@@ -724,6 +744,7 @@ fd_status fd_block_lanczos(const void* X, fd_dtype xt, int64_t N, int64_t D, int
       require_finite(X, xt, N, D, ldx, w.deg.flag, st);
 
       degree_run(w.deg, X, xt, N, D, ldx, beta, alpha, nullptr, w.d, w.s, w.s_off, true, st);
+      require_exponent_range(xt, w.deg.centre, beta, st);
       // the product view takes the packs as filled (kind and bandwidth)
       Lanczos L(w, product_view(w.prod, w.deg.rows, w.deg.cols, int(b)), st, N, int(b), lay.mm,
                 o.seed);
@@ -839,6 +860,7 @@ fd_status fd_continuation(const void* X, fd_dtype xt, int64_t N, int64_t D, int6
       // normalisation and eigensolve on the prefix
       DegreeWs dv = degree_view(c.sw.deg, n);
       degree_run(dv, X, xt, n, D, ldx, beta, alpha, c.q(t), c.sw.d, c.sw.s, c.sw.s_off, true, st);
+      require_exponent_range(xt, dv.centre, beta, st);
       const SolverLayout lay = solver_layout(n, int(b), kk, o);
       FD_REQUIRE(lay.mm <= c.sw.mm_cap, FD_ERR_INVALID_ARG, "internal: basis wider than carved");
       ProductWs pv = product_view(c.sw.prod, dv.rows, dv.cols, int(b));
@@ -951,13 +973,12 @@ fd_status fd_beta_flow(const void* X, fd_dtype xt, int64_t N, int64_t D, int64_t
     const FlowOutcome R = run_flow(f, X, xt, N, D, ldx, alpha, bb, kk, beta, false, fp, o,
                                    fo.max_probes, 0, out, st);
     if (!R.any) {
-      // the first probe is already past the wall: nothing admissible to return
+      // the first probe is already past the wall or out of range: nothing
+      // admissible to return
       for (size_t i = 0; i < out.size(); ++i) probes[i] = out[i];
       *nprobes = int64_t(out.size());
       *beta_x = NAN;
-      *exit_reason = FD_FLOW_WALL;
-      set_error("the first probe is already past the Perron wall (g_P <= kappa_P eta)");
-      return FD_ERR_PERRON_WALL;
+      return flow_nothing_admissible(R, -1, exit_reason);
     }
     const FlowProbe& fin = R.fin;
     const int reason = R.reason;
@@ -1046,10 +1067,7 @@ fd_status fd_beta_flow_cascade(const void* const* Xs, const fd_dtype* xts, const
         for (size_t i = 0; i < out.size(); ++i) probes[i] = out[i];
         *nprobes = int64_t(out.size());
         *beta_x = NAN;
-        *exit_reason = FD_FLOW_WALL;
-        set_error("the first probe of cascade level " + std::to_string(l) +
-                  " is already past the Perron wall (g_P <= kappa_P eta)");
-        return FD_ERR_PERRON_WALL;
+        return flow_nothing_admissible(R, l, exit_reason);
       }
       beta = R.fin.beta;
     }

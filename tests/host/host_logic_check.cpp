@@ -127,6 +127,8 @@ struct MockDriver {
   FlowParams fp;
   std::vector<double> vb, soff, gap;
   int accepts = 0;
+  double beta_max = INFINITY;  // exponent range of the mock
+  bool in_range(double beta) const { return beta <= beta_max; }
   FlowProbe probe(double beta, int role, int t, bool from_keep) {
     (void)t;
     (void)from_keep;
@@ -152,6 +154,23 @@ struct MockDriver {
   }
 };
 
+// The sweep stops before a bandwidth outside the exponent range and chooses
+// as on the probe budget: V_bias falls and S_off does not, so no bracket; the
+// probe at 8 beta0 would be out of range
+static int flow_range_units() {
+  int fails = 0;
+  const std::vector<double> vb = {4.0, 3.0, 2.2, 1.6, 1.2, 0.9}, so = {1, 1, 1, 1, 1, 1},
+                            gap = {0.5, 0.4, 0.3, 0.2, 0.1, 0.05};
+  MockDriver drv{1.0, 8, FlowParams{1e-7, 10.0, 6.0}, vb, so, gap, 0, 5.0};
+  const FlowOutcome R = run_flow_logic(drv, 1000, 1.0, false, 6);
+  if (!(R.any && R.reason == FD_FLOW_RANGE && R.fin.beta <= 4.0 && drv.accepts >= 3)) ++fails;
+  MockDriver first{1.0, 8, FlowParams{1e-7, 10.0, 6.0}, vb, so, gap, 0, 0.5};
+  const FlowOutcome R0 = run_flow_logic(first, 1000, 1.0, false, 6);
+  if (!(!R0.any && R0.reason == FD_FLOW_RANGE && first.accepts == 0)) ++fails;
+  std::fprintf(stderr, "flow range units: %d failures\n", fails);
+  return fails;
+}
+
 static int flow() {
   long long N = 0;
   int max_probes = 0, k = 0, warm = 0, n = 0;
@@ -161,7 +180,7 @@ static int flow() {
     std::fprintf(stderr, "bad spec\n");
     return 2;
   }
-  MockDriver drv{beta0, k, FlowParams{eta, kappa, p}, {}, {}, {}};
+  MockDriver drv{beta0, k, FlowParams{eta, kappa, p}, {}, {}, {}, 0, INFINITY};
   for (int i = 0; i < n; ++i) {
     double a, b, c;
     if (std::scanf("%lf %lf %lf", &a, &b, &c) != 3) {
@@ -179,7 +198,10 @@ static int flow() {
 }
 
 int main(int argc, char** argv) {
-  if (argc == 2 && std::strcmp(argv[1], "units") == 0) return units();
+  if (argc == 2 && std::strcmp(argv[1], "units") == 0) {
+    const int u = units();
+    return flow_range_units() == 0 ? u : 1;
+  }
   if (argc == 2 && std::strcmp(argv[1], "flow") == 0) return flow();
   std::fprintf(stderr, "usage: host_logic_check units|flow\n");
   return 2;

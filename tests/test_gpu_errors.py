@@ -1,11 +1,16 @@
-"""Error paths on the GPU: non-finite inputs and rank-deficient warm starts.
+"""Error paths on the GPU: non-finite inputs, the float32 exponent range and
+rank-deficient warm starts.
 
 A NaN or infinite coordinate makes every output of the asynchronous entry
 points NaN (fd_kernel_matmul, fd_degree, fd_degree_dyadic) and makes the
 eigensolver entry points return FD_ERR_INVALID_ARG before any other work; a
-later call on clean data through the same workspace is unaffected.  A warm
-start whose columns repeat (rank-deficient) or vanish is completed by the
-solver's orthonormalisation, and the eigenvalues equal a cold solve's.
+later call on clean data through the same workspace is unaffected.  The same
+holds for float32 X whose beta log2(e) max ||x - mean||^2 is beyond 65488,
+where the float16 offset pieces cannot hold the exponent: NaN outputs, or
+FD_ERR_UNSUPPORTED from the eigensolver and continuation, and the flow stops
+its sweep there (exit reason "range").  A warm start whose columns repeat
+(rank-deficient) or vanish is completed by the solver's orthonormalisation,
+and the eigenvalues equal a cold solve's.
 """
 import numpy as np
 import pytest
@@ -78,6 +83,77 @@ def test_eigensolvers_refuse_non_finite_x():
     with pytest.raises(fd.FdError) as e:
         fd.fd_beta_flow(to_dev(bits, dev), 4, 8)
     assert e.value.status == 1
+
+
+def clustered_points(seed=3, groups=24, per=6):
+    # 144 points in tight clusters far apart: max ||x - mean||^2 = 210, so
+    # beta = 100 is inside the exponent range (B = 3.0e4) and 1e4 beyond it
+    rng = np.random.default_rng(seed)
+    centres = rng.normal(size=(groups, 3)) * 4.0
+    X = np.repeat(centres, per, axis=0) + rng.normal(size=(groups * per, 3)) * 0.3
+    return (X - X.mean(0)).astype(np.float32)
+
+
+def chain_points(n=200):
+    # unit spacing on a line: max ||x - mean||^2 = 9900, so beta = 3 is inside
+    # the range (B = 4.3e4, neighbours still coupled by e^-3) and 6 beyond it
+    X = np.zeros((n, 3), dtype=np.float32)
+    X[:, 0] = np.arange(n) - (n - 1) / 2
+    return X
+
+
+def test_exponent_range_async_entry_points_give_nan():
+    X = clustered_points()
+    dev = device()
+    tX = to_dev(X, dev)
+    V = to_dev(inputs.random_block(X.shape[0], 4), dev)
+    case("exponent range: product inside (beta 100) is finite, beyond (1e4) NaN")
+    assert np.isfinite(to_np(fd.fd_kernel_matmul(tX, None, 100.0, V))).all()
+    assert np.isnan(to_np(fd.fd_kernel_matmul(tX, None, 1e4, V))).all()
+    case("exponent range: rectangular product beyond the range")
+    assert np.isnan(to_np(fd.fd_kernel_matmul(to_dev(X[:50], dev), tX, 1e4, V))).all()
+    case("exponent range: fd_degree inside and beyond")
+    deg = fd.fd_degree(tX, 100.0, 0.5)
+    assert all(np.isfinite(to_np(t)).all() for t in (deg.q, deg.d, deg.s, deg.s_off))
+    deg = fd.fd_degree(tX, 1e4, 0.5)
+    for t in (deg.q, deg.d, deg.s, deg.s_off):
+        assert np.isnan(to_np(t)).all()
+    case("exponent range: fd_degree_dyadic whose last level is beyond")
+    lad = fd.fd_degree_dyadic(tX, 100.0, 2, 0.5)
+    assert np.isfinite(to_np(lad.q)).all()
+    lad = fd.fd_degree_dyadic(tX, 100.0, 8, 0.5)
+    for t in (lad.q, lad.d, lad.s, lad.s_off):
+        assert np.isnan(to_np(t)).all()
+    case("exponent range: bfloat16 X has no such limit")
+    Xb = to_dev(inputs.f32_to_bf16_bits(X), dev)
+    assert np.isfinite(to_np(fd.fd_kernel_matmul(Xb, None, 1e4, V))).all()
+
+
+def test_exponent_range_sync_entry_points_refuse():
+    X = clustered_points()
+    tX = to_dev(X, device())
+    case("exponent range: fd_block_lanczos refuses beyond the range")
+    with pytest.raises(fd.FdError) as e:
+        fd.fd_block_lanczos(tX, 1e4, 4, 4)
+    assert e.value.status == 2 and "exponent range" in e.value.msg
+    case("exponent range: fd_continuation refuses at the first step beyond")
+    with pytest.raises(fd.FdError) as e:
+        fd.fd_continuation(tX, [144, 144], [100.0, 1e4], 4, 4, allow=(0, 5))
+    assert e.value.status == 2 and "exponent range" in e.value.msg
+    case("exponent range: fd_beta_flow whose first bandwidth is beyond")
+    got = fd.fd_beta_flow(tX, 4, 4, fopts=fd.flow_default_opts(beta_start=1e4, max_probes=4),
+                          allow=(2,))
+    assert got.status == 2 and got.reason == "range" and len(got.probes) == 0
+
+
+def test_flow_stops_at_the_exponent_range():
+    X = chain_points()
+    case("exponent range: flow on a 200-point chain from beta 3 (6 is beyond)")
+    got = fd.fd_beta_flow(to_dev(X, device()), 4, 4,
+                          fopts=fd.flow_default_opts(beta_start=3.0, max_probes=4), allow=(0, 5))
+    assert got.reason == "range"
+    assert [p["beta"] for p in got.probes] == [3.0]
+    assert got.beta_x == 3.0 and got.probes[0]["admissible"]
 
 
 @pytest.mark.parametrize("kind", ["duplicate", "zero"])

@@ -77,7 +77,10 @@ def test_budget_exit_like_the_oracle():
 def test_first_probe_past_the_wall_reports_it():
     X = clustered_points()
     case("beta flow first probe past the wall")
-    fo = fd.flow_default_opts(beta_start=1e4, max_probes=4)
+    # beta 100: every cluster is already split into single points (K = I to
+    # float32), and B = beta log2(e) max ||x||^2 = 3.0e4 is inside the float32
+    # path's exponent range
+    fo = fd.flow_default_opts(beta_start=100.0, max_probes=4)
     got = fd.fd_beta_flow(to_dev(X, device()), 4, 4, fopts=fo, allow=(0, 6))
     assert got.status == 6 and got.reason == "wall"
     assert len(got.probes) == 1 and not got.probes[0]["admissible"]
