@@ -36,8 +36,10 @@
  *    (13 < D <= 30, 32 < D <= 62) switch to one that keeps it.  Beyond
  *    B = 200 the dropped fourth-order piece products can reach the 1e-5 bar
  *    (1.1e-5 measured at B = 400, D = 30).
- *  - Exponent range (float32 X): the offsets enter the contraction as float16
- *    pieces, so B above 65488 cannot be formed at all.  There the
+ *  - Exponent range (float32 X): the offsets and the scaled coordinates enter
+ *    the contraction as float16 pieces, so B above 65488 cannot be formed at
+ *    all, nor (when beta is so small that the coordinate scale stops at
+ *    2^-12) coordinates whose scaled pieces pass 65504.  There the
  *    asynchronous entry points fill their outputs with NaN (fd_degree_dyadic:
  *    when its largest bandwidth is beyond), fd_block_lanczos and
  *    fd_continuation return FD_ERR_UNSUPPORTED (the continuation's earlier

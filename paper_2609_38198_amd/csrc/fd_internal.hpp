@@ -146,8 +146,16 @@ constexpr double EXP_BUDGET = 64.0;
 // ones refuse (FD_ERR_UNSUPPORTED) and the flow stops before such a probe.
 // (bfloat16 X forms its exponent in float32 and has no such limit.)
 constexpr double HX_EXP_RANGE = 65504.0 - 16.0;
-// Whether bandwidth beta is inside the exponent range for points of squared
-// centred radius r2max (always for bfloat16 X).
+// The coordinates enter as float16 pieces of s (x - mu) (column side) and
+// 2 beta log2(e) (x - mu) / s (row side): both must stay within 65504 too.
+// The balanced s keeps them below 512 inside the offset range; only its clamp
+// at the float32 extremes of beta (below about 1e-39) could break that.
+constexpr double HX_PIECE_MAX = 65504.0;
+// s of the float32 packs for bandwidth beta (a power of two).
+double hx_coord_scale(double beta);
+// Whether bandwidth beta is inside the exponent range (offsets and
+// coordinate pieces) for points of squared centred radius r2max (always for
+// bfloat16 X).
 bool exponent_in_range(fd_dtype xt, double beta, double r2max);
 // r2max of a centring (host copy; synchronises the stream; 0 for bfloat16).
 double exponent_radius(fd_dtype xt, const CentreWs& c, hipStream_t stream);

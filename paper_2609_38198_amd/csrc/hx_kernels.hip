@@ -1157,6 +1157,18 @@ int hx_recipe_for(int64_t D) {
     if (D >= 1 && D <= HX_TABLE[r].maxd) return r;
   return -1;
 }
+// s = 2^e balances |x'| = s|x| and |b'| = 2 beta log2(e) |x| / s: both are
+// then within a factor sqrt(2) of sqrt(2 beta log2(e)) |x|, at most 512 inside
+// the exponent range, and neither falls towards float16's subnormals before
+// the cross term itself is negligible.  (A clamp of e at +-12 made b' lose
+// bits at beta < 2e-8 with large coordinates: 1.8e-5 K V error at B = 0.3.)
+// |e| <= 64 only guards the float32 extremes of beta.
+double hx_coord_scale(double beta) {
+  int e = 0;
+  if (beta > 0.0) e = std::clamp(int(std::lround(0.5 * std::log2(2.0 * beta * LOG2E))), -64, 64);
+  return std::ldexp(1.0, e);
+}
+
 int hx_col_chunks(int rid) { return HX_TABLE[rid].nc; }
 int hx_row_chunks(int rid) { return HX_TABLE[rid].nb; }
 
@@ -1175,10 +1187,7 @@ static void pack_hx_launch(const float* X, int64_t n, int64_t D, int64_t ldx, do
   check_span(xp, size_t(npad / TILE) * nch * 64 * 4, "split point pack");
   FD_REQUIRE(D <= R.maxd, FD_ERR_INVALID_ARG, "internal: recipe too narrow for D");
   const double bl = beta * LOG2E;
-  // s = 2^e balances |x'| = s|x| and |b'| = 2 beta log2(e) |x| / s
-  int e = 0;
-  if (beta > 0.0) e = std::clamp(int(std::lround(0.5 * std::log2(2.0 * bl))), -12, 12);
-  const double s = std::ldexp(1.0, e);
+  const double s = hx_coord_scale(beta);
   const double scale = ROW ? 2.0 * bl / s : s;
   const double shift = ROW ? double(SHIFT) : 0.0;
   hipLaunchKernelGGL((pack_hx_point_kernel<RID, ROW>), dim3(blocks_for(npad, 256)), dim3(256), 0,

@@ -147,14 +147,22 @@ void launch_radius_more(const void* X2, fd_dtype xt, int64_t n2, int64_t D, int6
 
 // ------------------------------------------------------------------ exponent range
 
+// f2: the square of the larger coordinate scale (s or 2 beta log2(e) / s)
 __global__ void range_check_kernel(const unsigned long long* __restrict__ r2max, double bl,
-                                   int* __restrict__ flag) {
+                                   double f2, int* __restrict__ flag) {
   const double r2 = __longlong_as_double(static_cast<long long>(*r2max));
-  if (!(bl * r2 <= HX_EXP_RANGE)) atomicOr(flag, 2);
+  if (!(bl * r2 <= HX_EXP_RANGE && f2 * r2 <= HX_PIECE_MAX * HX_PIECE_MAX)) atomicOr(flag, 2);
+}
+
+static double coord_scale_sq(double beta) {
+  const double s = hx_coord_scale(beta);
+  const double f = std::max(s, 2.0 * beta * LOG2E / s);
+  return f * f;
 }
 
 bool exponent_in_range(fd_dtype xt, double beta, double r2max) {
-  return xt != FD_F32 || beta * LOG2E * r2max <= HX_EXP_RANGE;
+  return xt != FD_F32 || (beta * LOG2E * r2max <= HX_EXP_RANGE &&
+                          coord_scale_sq(beta) * r2max <= HX_PIECE_MAX * HX_PIECE_MAX);
 }
 
 double exponent_radius(fd_dtype xt, const CentreWs& c, hipStream_t stream) {
@@ -173,8 +181,9 @@ void require_exponent_range(fd_dtype xt, const CentreWs& c, double beta, hipStre
   if (!exponent_in_range(xt, beta, r2))
     throw Error{FD_ERR_UNSUPPORTED,
                 "beta log2(e) max ||x - mean||^2 = " + std::to_string(beta * LOG2E * r2) +
-                    " is beyond the float32 path's exponent range (" +
-                    std::to_string(HX_EXP_RANGE) + ")"};
+                    " with max ||x - mean|| = " + std::to_string(std::sqrt(r2)) +
+                    " is beyond the float32 path's exponent range (offsets up to " +
+                    std::to_string(HX_EXP_RANGE) + ", coordinate pieces up to 65504)"};
 }
 
 void launch_range_check(fd_dtype xt, const CentreWs& c, double beta, int* flag,
@@ -182,7 +191,8 @@ void launch_range_check(fd_dtype xt, const CentreWs& c, double beta, int* flag,
   if (xt != FD_F32) return;
   FD_REQUIRE(c.r2max != nullptr && flag != nullptr, FD_ERR_INVALID_ARG,
              "internal: range check words");
-  hipLaunchKernelGGL(range_check_kernel, dim3(1), dim3(1), 0, stream, c.r2max, beta * LOG2E, flag);
+  hipLaunchKernelGGL(range_check_kernel, dim3(1), dim3(1), 0, stream, c.r2max, beta * LOG2E,
+                     coord_scale_sq(beta), flag);
   FD_LAUNCH_CHECK();
 }
 

@@ -124,6 +124,13 @@ def test_exponent_range_async_entry_points_give_nan():
     lad = fd.fd_degree_dyadic(tX, 100.0, 8, 0.5)
     for t in (lad.q, lad.d, lad.s, lad.s_off):
         assert np.isnan(to_np(t)).all()
+    case("coordinate scale: huge coordinates at tiny bandwidths match the oracle")
+    # B = 0.3 in both; the coordinate scale stays balanced (2^-24, 2^-34), so
+    # neither side's float16 pieces lose bits
+    for scale, beta in ((1e6, 1e-15), (1e9, 1e-21)):
+        Xs = (X.astype(np.float64) * scale).astype(np.float32)
+        Ys = to_np(fd.fd_kernel_matmul(to_dev(Xs, dev), None, beta, V))
+        assert rel_fro(Ys, ok.kernel_matmul(Xs, None, beta, to_np(V))) <= TOL_F32
     case("exponent range: bfloat16 X has no such limit")
     Xb = to_dev(inputs.f32_to_bf16_bits(X), dev)
     assert np.isfinite(to_np(fd.fd_kernel_matmul(Xb, None, 1e4, V))).all()
