@@ -258,6 +258,16 @@ constexpr int hx_waves() {
   return big ? 1 : 2;
 }
 
+// Waves per SIMD for the symmetric row sums: two wherever the variant fits
+// 256 registers, so its matrix instructions accumulate in VGPRs and the
+// exponent tiles reach the vector ALUs without v_accvgpr_read copies (one per
+// value: about a seventh of the pass's instructions at D <= 30, 8 row tiles).
+// The widest layouts with 8 row tiles would spill there and keep one wave.
+template <int RID, int NIB, bool SQ>
+constexpr int hx_sym_waves() {
+  return (NIB == 8 && (RID >= 5 || (RID == 4 && SQ))) ? 1 : 2;
+}
+
 // ------------------------------------------------------------------ packing
 //
 // One thread per (padded) point computes the three float16 pieces of each
@@ -808,7 +818,7 @@ __device__ __forceinline__ void hx_sym_step(floatx4 (&t)[NIB], const uintx4* xn,
 // fix_scale2 per unit of (2^15 K)^2.
 template <int RID, int NIB, bool UNIT, bool SQ = false>
 __global__ __launch_bounds__(WG_THREADS)
-__attribute__((amdgpu_waves_per_eu(hx_waves<RID, 0, NIB>()))) void rowsum_sym_hx_kernel(
+__attribute__((amdgpu_waves_per_eu(hx_sym_waves<RID, NIB, SQ>()))) void rowsum_sym_hx_kernel(
     const uintx4* __restrict__ xc, const floatx4* __restrict__ wp, const uintx4* __restrict__ xr,
     int64_t nblk, int64_t njb, int64_t jb_per_split, int64_t nsplit, float* __restrict__ part,
     int64_t nrpad, unsigned long long* __restrict__ colfix, double fix_scale,
