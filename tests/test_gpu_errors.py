@@ -12,6 +12,9 @@ its sweep there (exit reason "range").  A warm start whose columns repeat
 (rank-deficient) or vanish is completed by the solver's orthonormalisation,
 and the eigenvalues equal a cold solve's.
 """
+import os
+import subprocess
+
 import numpy as np
 import pytest
 import torch
@@ -161,6 +164,20 @@ def test_flow_stops_at_the_exponent_range():
     assert got.reason == "range"
     assert [p["beta"] for p in got.probes] == [3.0]
     assert got.beta_x == 3.0 and got.probes[0]["admissible"]
+
+
+JACOBI_CHECK = os.path.join(os.path.dirname(os.path.abspath(__file__)), "capi", "jacobi_check")
+
+
+def test_dense_eigensolve_sorts_nan_last():
+    # the Rayleigh-Ritz eigensolve on matrices with NaN on the diagonal (one
+    # workgroup at m = 100, block Jacobi at m = 300): it finishes and returns
+    # every number, descending, before the NaNs (tests/capi/jacobi_check.cpp)
+    case("jacobi_eig with NaN diagonals, m = 100 and 300")
+    assert os.path.exists(JACOBI_CHECK), "jacobi_check is not built (run __graft_entry__.build())"
+    res = subprocess.run([JACOBI_CHECK], capture_output=True, text=True, timeout=120)
+    assert res.returncode == 0, res.stdout + res.stderr
+    assert res.stdout.count("order ok") == 2, res.stdout
 
 
 @pytest.mark.parametrize("kind", ["duplicate", "zero"])
