@@ -267,6 +267,12 @@ template <int RID, int NIB, bool SQ>
 constexpr int hx_sym_waves() {
   return (NIB == 8 && (RID >= 5 || (RID == 4 && SQ))) ? 1 : 2;
 }
+// The same for the plain row sums (rectangular sums, one right-hand side):
+// only the widest layout with 8 row tiles would spill.
+template <int RID, int NIB>
+constexpr int hx_plain_waves() {
+  return (NIB == 8 && RID >= 6) ? 1 : 2;
+}
 
 // ------------------------------------------------------------------ packing
 //
@@ -622,7 +628,7 @@ __device__ __forceinline__ void hx_rowsum_tile(const HxCol<RID>& c,
 // Column tiles stream through two operand buffers used in turn.
 template <int RID, int NIB, bool UNIT>
 __global__ __launch_bounds__(WG_THREADS)
-__attribute__((amdgpu_waves_per_eu(hx_waves<RID, 0, NIB>()))) void rowsum_hx_kernel(
+__attribute__((amdgpu_waves_per_eu(hx_plain_waves<RID, NIB>()))) void rowsum_hx_kernel(
     const uintx4* __restrict__ xc, const floatx4* __restrict__ wp, const uintx4* __restrict__ xr,
     int64_t nrt, int64_t njb, int64_t jb_per_split, int diag, float* __restrict__ out,
     int64_t Nr, float* __restrict__ part, int64_t nrpad, HxGate gate) {
