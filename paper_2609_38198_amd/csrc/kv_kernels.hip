@@ -684,9 +684,13 @@ __attribute__((amdgpu_waves_per_eu(bf16_waves<DC, NCB, NIB>()))) void product_bf
 
 
 // Row sums for bfloat16 inputs: the same half squared distances, K = 2^t
-// clamped to [0, 1], summed (times the weights) on the vector ALUs.
+// clamped to [0, 1], summed (times the weights) on the vector ALUs.  Two waves
+// per SIMD (every variant fits 256 registers): the matrix instructions then
+// accumulate in VGPRs, with no copies out of accumulation registers (bitwise
+// equal results, 13-17% faster bfloat16 degree passes at D = 30 and 64).
 template <int DC, int NIB, bool UNIT>
-__global__ __launch_bounds__(WG_THREADS) void rowsum_bf16_kernel(
+__global__ __launch_bounds__(WG_THREADS) __attribute__((amdgpu_waves_per_eu(2))) void
+rowsum_bf16_kernel(
     const uintx4* __restrict__ xa, const floatx4* __restrict__ aj, const floatx4* __restrict__ wp,
     const uintx4* __restrict__ xb, const float* __restrict__ ar, int64_t nrt, int64_t njb,
     int64_t jb_per_split, int diag, float scale2, float* __restrict__ out, int64_t Nr,
