@@ -17,136 +17,190 @@ namespace fd {
 static inline unsigned nblk(int64_t n, int t) { return unsigned((n + t - 1) / t); }
 
 // ------------------------------------------------------------ C = A^T B
-// Each thread accumulates a 4 x 4 block C[4 lq + u][4 cq + v] in float64
-// (products of float32 values are exact in float64).  The output is split
-// into groups of lqg x tc such blocks (tc = ceil(nb / 4) column quads, lqg
-// row quads, at most 256 threads); a workgroup of 256 threads holds
-// S = 256 / (lqg tc) slices of one group, which walk interleaved 4-row steps
-// of the workgroup's chunk of rows and are added in LDS in slice order.  Grid
-// (groups, chunks); partial sums per chunk are then reduced in a fixed order.
+// On the float64 matrix instruction v_mfma_f64_16x16x4f64 (operand A[i][k] on
+// lane i + 16 k, B[k][j] on lane j + 16 k, result D[i][j] on lane
+// j + 16 (i mod 4), register i / 4; i, j < 16, k < 4).  A wave owns a
+// 64 x 16 NCB tile of C; its l-block q (q < 4) holds the rows l0 + 4 i + q of
+// C and its c-block h (h < NCB) the columns c0 + NCB j + h, so that lane
+// i + 16 k reads the four A values it needs from row k of a 4-row step with
+// one 16-byte load and its NCB B values with one 4 NCB-byte load.  Products
+// of float32 values are exact in float64 and the matrix unit sums them in
+// float64.  The four waves of a workgroup take consecutive 16-row quarters of
+// each 64 rows of the workgroup's chunk of rows and are added in LDS in a
+// fixed order; the chunks' partial sums are then reduced in a fixed order.
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef double dbl4 __attribute__((ext_vector_type(4)));
+
+constexpr int TN_ROWS = 64;   // rows of one workgroup iteration (4 waves x 4 steps x 4 rows)
+constexpr int TN_WGS = 2048;  // workgroups aimed at (8 waves per SIMD)
 
 struct GemmTnShape {
-  int tc = 1, lqg = 1, slices = 1, groups = 1;
-  int64_t chunks = 1, rows_per_chunk = 1;
+  int ncb = 1, tiles_l = 1, tiles_c = 1;
+  int64_t chunks = 1, rows_per_chunk = TN_ROWS;
 };
 
 static GemmTnShape gemm_tn_shape(int ma, int nb, int64_t N) {
   GemmTnShape g;
-  g.tc = (nb + 3) / 4;
-  const int lq = (ma + 3) / 4;
-  g.lqg = std::min(lq, 256 / g.tc);
-  g.groups = (lq + g.lqg - 1) / g.lqg;
-  g.lqg = (lq + g.groups - 1) / g.groups;  // balance the groups
-  g.slices = 256 / (g.lqg * g.tc);
-  // 4 to 16 steps of 4 rows per thread (a multiple of the 4 a loop iteration
-  // takes): as few as keep >= ~512 workgroups busy, but at most
+  g.ncb = nb <= 16 ? 1 : 2;
+  g.tiles_l = (ma + 63) / 64;
+  g.tiles_c = (nb + 16 * g.ncb - 1) / (16 * g.ncb);
+  const int64_t tiles = int64_t(g.tiles_l) * g.tiles_c;
+  // about TN_WGS workgroups of at least TN_ROWS rows each, and at most
   // gemm_tn_chunks(N) chunks (the partial buffer's size)
-  const int64_t steps_total = (N + 3) / 4;
-  int64_t spt = steps_total * g.groups / (int64_t(g.slices) * 512);
-  spt = round_up(std::max<int64_t>(4, std::min<int64_t>(16, spt)), 4);
-  g.rows_per_chunk = 4 * spt * g.slices;
+  const int64_t want = std::min<int64_t>(gemm_tn_chunks(N), (TN_WGS + tiles - 1) / tiles);
+  g.rows_per_chunk = round_up((N + want - 1) / want, TN_ROWS);
   g.chunks = (N + g.rows_per_chunk - 1) / g.rows_per_chunk;
-  const int64_t cap = gemm_tn_chunks(N);
-  if (g.chunks > cap) {
-    g.chunks = cap;
-    g.rows_per_chunk = round_up((N + cap - 1) / cap, int64_t(4) * g.slices);
-    g.chunks = (N + g.rows_per_chunk - 1) / g.rows_per_chunk;
-  }
   return g;
 }
 
-typedef float f32x4 __attribute__((ext_vector_type(4)));
+// Loads of one 4-row step: row `row` of A (4 values) and of B (NCB values);
+// with CLAMP rows at or past r1 read row r1 - 1 and give B the weight 0.
+template <int NCB, bool VEC, bool CLAMP>
+__device__ __forceinline__ void tn_load(const float* __restrict__ A, int64_t lda,
+                                        const float* __restrict__ B, int64_t ldb, int64_t row,
+                                        int64_t r1, const int (&lc)[4], const int (&cc)[NCB],
+                                        float (&a)[4], float (&b)[NCB]) {
+  const bool ok = !CLAMP || row < r1;
+  const int64_t rc = CLAMP ? (ok ? row : r1 - 1) : row;
+  const float* pa = A + rc * lda;
+  const float* pb = B + rc * ldb;
+  if constexpr (VEC) {
+    const f32x4 v = *reinterpret_cast<const f32x4*>(pa + lc[0]);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) a[u] = v[u];
+    if constexpr (NCB == 2) {
+      const f32x2 w = *reinterpret_cast<const f32x2*>(pb + cc[0]);
+      b[0] = ok ? w[0] : 0.f;
+      b[1] = ok ? w[1] : 0.f;
+    } else {
+      b[0] = ok ? pb[cc[0]] : 0.f;
+    }
+  } else {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) a[u] = pa[lc[u]];
+#pragma unroll
+    for (int h = 0; h < NCB; ++h) b[h] = ok ? pb[cc[h]] : 0.f;
+  }
+}
 
-// VEC: ma, nb, lda, ldb multiples of 4 and A, B 16-byte aligned; each step
-// then reads its 4 + 4 values per row as two 16-byte loads (same sums).
-template <bool VEC>
-__global__ __launch_bounds__(256) void gemm_tn_partial_kernel(
+template <int NCB>
+__device__ __forceinline__ void tn_mfma(const float (&a)[4], const float (&b)[NCB],
+                                        dbl4 (&acc)[4][NCB]) {
+  double bd[NCB];
+#pragma unroll
+  for (int h = 0; h < NCB; ++h) bd[h] = double(b[h]);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const double ad = double(a[q]);
+#pragma unroll
+    for (int h = 0; h < NCB; ++h)
+      acc[q][h] = __builtin_amdgcn_mfma_f64_16x16x4f64(ad, bd[h], acc[q][h], 0, 0, 0);
+  }
+}
+
+// VEC: ma, lda multiples of 4, A 16-byte aligned and, for NCB = 2, nb, ldb
+// even and B 8-byte aligned (the loads above are then vector loads).  Grid:
+// tiles x chunks workgroups, numbered so that the workgroups on one XCD
+// (blockIdx.x mod 8) take all tiles of consecutive chunks (B's rows stay in
+// that XCD's L2).
+template <int NCB, bool VEC>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void gemm_tn_partial_kernel(
     const float* __restrict__ A, int64_t lda, int ma, const float* __restrict__ B, int64_t ldb,
-    int nb, int64_t N, int64_t rows_per_chunk, int tc, int lqg, int slices,
+    int nb, int64_t N, int64_t rows_per_chunk, int tiles_l, int tiles_c, int64_t total,
     double* __restrict__ part) {
-  __shared__ double red[256 * 16];
-  const int t = threadIdx.x;
-  const int to = lqg * tc;
-  const int slice = t / to, o = t % to;
-  const int l0 = 4 * (blockIdx.x * lqg + o / tc);
-  const int c0 = 4 * (o % tc);
-  const bool active = slice < slices && l0 < ma;
-  const int64_t chunk = blockIdx.y;
+  constexpr int E = 16 * NCB;  // result doubles per lane
+  __shared__ double red[2][E * 64];
+  const int64_t gid = blockIdx.x, per = total / 8, rem = total % 8, x = gid % 8;
+  const int64_t lin = x * per + min(x, rem) + gid / 8;
+  const int64_t tiles = int64_t(tiles_l) * tiles_c;
+  const int64_t chunk = lin / tiles;
+  const int tile = int(lin - chunk * tiles);
+  const int l0 = 64 * (tile % tiles_l), c0 = 16 * NCB * (tile / tiles_l);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int i = lane & 15, k = lane >> 4;
+  // columns past the edge read a valid column; their sums are not stored
+  int lc[4], cc[NCB];
+  if constexpr (VEC) {
+    lc[0] = min(l0 + 4 * i, ma - 4);
+    cc[0] = min(c0 + NCB * i, nb - NCB);
+#pragma unroll
+    for (int u = 1; u < 4; ++u) lc[u] = lc[0] + u;
+#pragma unroll
+    for (int h = 1; h < NCB; ++h) cc[h] = cc[0] + h;
+  } else {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) lc[u] = min(l0 + 4 * i + u, ma - 1);
+#pragma unroll
+    for (int h = 0; h < NCB; ++h) cc[h] = min(c0 + NCB * i + h, nb - 1);
+  }
   const int64_t r0 = chunk * rows_per_chunk;
   const int64_t r1 = min(N, r0 + rows_per_chunk);
-  double acc[4][4];
+  dbl4 acc[4][NCB];
 #pragma unroll
-  for (int u = 0; u < 4; ++u)
+  for (int q = 0; q < 4; ++q)
 #pragma unroll
-    for (int v = 0; v < 4; ++v) acc[u][v] = 0.0;
-  if (active) {
-    // columns past the edge read a valid column; their sums are not stored
-    int la[4], cb[4];
+    for (int h = 0; h < NCB; ++h) acc[q][h] = dbl4{0.0, 0.0, 0.0, 0.0};
+  // this lane's row of step s of an iteration at r: r + 16 wave + 4 s + k
+  const int64_t off = 16 * wave + k;
+  int64_t r = r0;
+  for (; r + TN_ROWS <= r1; r += TN_ROWS) {
+    float a[4][4], b[4][NCB];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      la[u] = min(l0 + u, ma - 1);
-      cb[u] = min(c0 + u, nb - 1);
-    }
-    // four steps (of 4 rows) per iteration with all their loads issued first:
-    // the rows are far apart in memory and each step alone would wait a full
-    // load latency; rows past the chunk read its last row with weight 0
-    const int64_t stride = 4 * int64_t(slices);
-    for (int64_t i = r0 + 4 * slice; i < r1; i += 4 * stride) {
-      float a[4][4][4], bv[4][4][4];
+    for (int s = 0; s < 4; ++s)
+      tn_load<NCB, VEC, false>(A, lda, B, ldb, r + off + 4 * s, r1, lc, cc, a[s], b[s]);
 #pragma unroll
-      for (int st = 0; st < 4; ++st)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int64_t ir = i + st * stride + r;
-          const int64_t irc = min(ir, r1 - 1);
-          if constexpr (VEC) {
-            const f32x4 av = *reinterpret_cast<const f32x4*>(A + irc * lda + l0);
-            const f32x4 bw = *reinterpret_cast<const f32x4*>(B + irc * ldb + c0);
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-              a[st][r][u] = av[u];
-              bv[st][r][u] = (ir < r1) ? bw[u] : 0.f;
-            }
-          } else {
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-              a[st][r][u] = A[irc * lda + la[u]];
-              bv[st][r][u] = (ir < r1) ? B[irc * ldb + cb[u]] : 0.f;
-            }
-          }
-        }
-#pragma unroll
-      for (int st = 0; st < 4; ++st)
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-#pragma unroll
-          for (int u = 0; u < 4; ++u)
-#pragma unroll
-            for (int v = 0; v < 4; ++v)
-              acc[u][v] = fma(double(a[st][r][u]), double(bv[st][r][v]), acc[u][v]);
-    }
+    for (int s = 0; s < 4; ++s) tn_mfma<NCB>(a[s], b[s], acc);
   }
-  if (slices > 1) {
+  if (r < r1) {  // the ragged end of the last chunk
+    float a[4][4], b[4][NCB];
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
+    for (int s = 0; s < 4; ++s)
+      tn_load<NCB, VEC, true>(A, lda, B, ldb, r + off + 4 * s, r1, lc, cc, a[s], b[s]);
 #pragma unroll
-      for (int v = 0; v < 4; ++v) red[(4 * u + v) * 256 + t] = acc[u][v];
-    __syncthreads();
-    if (slice == 0) {
-      for (int sl = 1; sl < slices; ++sl)
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-#pragma unroll
-          for (int v = 0; v < 4; ++v) acc[u][v] += red[(4 * u + v) * 256 + sl * to + o];
-    }
+    for (int s = 0; s < 4; ++s) tn_mfma<NCB>(a[s], b[s], acc);
   }
-  if (slice != 0 || !active) return;
+  // (wave 0 + wave 2) + (wave 1 + wave 3)
+  if (wave >= 2) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int h = 0; h < NCB; ++h)
+#pragma unroll
+        for (int s = 0; s < 4; ++s) red[wave - 2][((q * NCB + h) * 4 + s) * 64 + lane] = acc[q][h][s];
+  }
+  __syncthreads();
+  if (wave < 2) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int h = 0; h < NCB; ++h)
+#pragma unroll
+        for (int s = 0; s < 4; ++s) acc[q][h][s] += red[wave][((q * NCB + h) * 4 + s) * 64 + lane];
+  }
+  __syncthreads();
+  if (wave == 1) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int h = 0; h < NCB; ++h)
+#pragma unroll
+        for (int s = 0; s < 4; ++s) red[0][((q * NCB + h) * 4 + s) * 64 + lane] = acc[q][h][s];
+  }
+  __syncthreads();
+  if (wave != 0) return;
   double* out = part + chunk * int64_t(ma) * nb;
 #pragma unroll
-  for (int u = 0; u < 4; ++u)
+  for (int q = 0; q < 4; ++q)
 #pragma unroll
-    for (int v = 0; v < 4; ++v)
-      if (l0 + u < ma && c0 + v < nb) out[int64_t(l0 + u) * nb + c0 + v] = acc[u][v];
+    for (int h = 0; h < NCB; ++h)
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        const int l = l0 + 4 * (4 * s + k) + q, c = c0 + NCB * i + h;
+        const double v = acc[q][h][s] + red[0][((q * NCB + h) * 4 + s) * 64 + lane];
+        if (l < ma && c < nb) out[int64_t(l) * nb + c] = v;
+      }
 }
 
 // out[idx] = sum over p of part[p * count + idx]: 8 threads per output, each
@@ -181,16 +235,22 @@ void gemm_tn(const float* A, int64_t lda, int ma, const float* B, int64_t ldb, i
              "internal: gemm_tn shape");
   const GemmTnShape g = gemm_tn_shape(ma, nb, N);
   check_span_d(part, size_t(g.chunks) * ma * nb, "gemm partials");
-  const bool vec = ma % 4 == 0 && nb % 4 == 0 && lda % 4 == 0 && ldb % 4 == 0 &&
-                   reinterpret_cast<uintptr_t>(A) % 16 == 0 &&
-                   reinterpret_cast<uintptr_t>(B) % 16 == 0;
-  const dim3 grid(unsigned(g.groups), unsigned(g.chunks));
-  if (vec)
-    hipLaunchKernelGGL(gemm_tn_partial_kernel<true>, grid, dim3(256), 0, stream, A, lda, ma, B, ldb,
-                       nb, N, g.rows_per_chunk, g.tc, g.lqg, g.slices, part.p);
-  else
-    hipLaunchKernelGGL(gemm_tn_partial_kernel<false>, grid, dim3(256), 0, stream, A, lda, ma, B,
-                       ldb, nb, N, g.rows_per_chunk, g.tc, g.lqg, g.slices, part.p);
+  const bool veca = ma % 4 == 0 && lda % 4 == 0 && reinterpret_cast<uintptr_t>(A) % 16 == 0;
+  const bool vecb = g.ncb == 1 || (nb % 2 == 0 && ldb % 2 == 0 &&
+                                   reinterpret_cast<uintptr_t>(B) % 8 == 0);
+  const int64_t total = int64_t(g.tiles_l) * g.tiles_c * g.chunks;
+  const dim3 grid{unsigned(total)};
+#define FD_TN_LAUNCH(NCB, VEC)                                                                 \
+  hipLaunchKernelGGL((gemm_tn_partial_kernel<NCB, VEC>), grid, dim3(256), 0, stream, A, lda, ma, B, \
+                     ldb, nb, N, g.rows_per_chunk, g.tiles_l, g.tiles_c, total, part.p)
+  if (g.ncb == 2) {
+    if (veca && vecb) FD_TN_LAUNCH(2, true);
+    else FD_TN_LAUNCH(2, false);
+  } else {
+    if (veca) FD_TN_LAUNCH(1, true);
+    else FD_TN_LAUNCH(1, false);
+  }
+#undef FD_TN_LAUNCH
   FD_LAUNCH_CHECK();
   const int64_t count = int64_t(ma) * nb;
   hipLaunchKernelGGL(reduce_partials_kernel, dim3(nblk(count, 32)), dim3(256), 0, stream, part.p,
@@ -894,10 +954,7 @@ __device__ __forceinline__ bool bj_inner_round(const double* __restrict__ Sc,
 
 constexpr int BJ_TILE = BJ_W * BJ_LD;  // doubles of one padded BJ_W x BJ_W matrix in LDS
 
-// float64 matrix instruction v_mfma_f64_16x16x4f64: operand A[i][k] on lane
-// i + 16 k, B[k][j] on lane j + 16 k, result D[i][j] on lane j + 16 (i mod 4),
-// register i / 4 (i, j < 16, k < 4)
-typedef double dbl4 __attribute__((ext_vector_type(4)));
+// float64 matrix instruction v_mfma_f64_16x16x4f64 (lane layouts as in C = A^T B above)
 
 // One launch per round of the block Jacobi.  Workgroups [0, nsolve) take the
 // pairs of blocks of round rs: each builds its BJ_W x BJ_W principal

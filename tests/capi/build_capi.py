@@ -1,5 +1,5 @@
-"""Build the C-ABI driver tests/capi/capi_check and the internal check
-tests/capi/jacobi_check against the in-tree library."""
+"""Build the C-ABI driver tests/capi/capi_check and the internal checks
+tests/capi/jacobi_check and tests/capi/gemm_check against the in-tree library."""
 import os
 import subprocess
 
@@ -34,6 +34,7 @@ def _build_one(name: str, extra_includes=(), verbose: bool = True) -> str:
 
 def build(verbose: bool = True) -> str:
     _build_one("jacobi_check", (os.path.join(PKG, "csrc"),), verbose)
+    _build_one("gemm_check", (os.path.join(PKG, "csrc"),), verbose)
     return _build_one("capi_check", (), verbose)
 
 
