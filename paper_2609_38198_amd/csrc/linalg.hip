@@ -35,6 +35,8 @@ typedef double dbl4 __attribute__((ext_vector_type(4)));
 
 constexpr int TN_ROWS = 64;   // rows of one workgroup iteration (4 waves x 4 steps x 4 rows)
 constexpr int TN_WGS = 2048;  // workgroups aimed at (8 waves per SIMD)
+constexpr int TN_CHUNKS_MIN = 32;
+constexpr int TN_CHUNK_ROWS = 1024;
 
 struct GemmTnShape {
   int ncb = 1, tiles_l = 1, tiles_c = 1;
@@ -47,9 +49,12 @@ static GemmTnShape gemm_tn_shape(int ma, int nb, int64_t N) {
   g.tiles_l = (ma + 63) / 64;
   g.tiles_c = (nb + 16 * g.ncb - 1) / (16 * g.ncb);
   const int64_t tiles = int64_t(g.tiles_l) * g.tiles_c;
-  // about TN_WGS workgroups of at least TN_ROWS rows each, and at most
-  // gemm_tn_chunks(N) chunks (the partial buffer's size)
-  const int64_t want = std::min<int64_t>(gemm_tn_chunks(N), (TN_WGS + tiles - 1) / tiles);
+  // about TN_WGS workgroups of at least TN_ROWS rows each, but no more than
+  // max(TN_CHUNKS_MIN, N / TN_CHUNK_ROWS) chunks (each chunk writes ma x nb
+  // partial sums that the reduction reads back) and at most gemm_tn_chunks(N)
+  // (the partial buffer's size)
+  const int64_t want = std::min({gemm_tn_chunks(N), (TN_WGS + tiles - 1) / tiles,
+                                 std::max<int64_t>(TN_CHUNKS_MIN, N / TN_CHUNK_ROWS)});
   g.rows_per_chunk = round_up((N + want - 1) / want, TN_ROWS);
   g.chunks = (N + g.rows_per_chunk - 1) / g.rows_per_chunk;
   return g;
@@ -259,98 +264,147 @@ void gemm_tn(const float* A, int64_t lda, int ma, const float* B, int64_t ldb, i
 }
 
 // ------------------------------------------------------------ Z = beta Z + alpha Q C
-// C: ma x nb float32 row-major (ld nb).  Each workgroup owns 256 / nbp rows,
-// thread (row, c) loops over l with C staged in LDS in slices of 128 rows.
-__global__ __launch_bounds__(256) void gemm_nn_kernel(const float* __restrict__ Q, int64_t ldq,
-                                                      int ma, const float* __restrict__ C, int nb,
-                                                      int nbp, float* __restrict__ Z,
-                                                      int64_t ldz, int64_t N, float alpha,
-                                                      float beta) {
-  __shared__ float cs[128 * 64];
-  const int rows_per_wg = 256 / nbp;
-  const int tr = threadIdx.x / nbp, tc = threadIdx.x % nbp;
-  const int64_t i = int64_t(blockIdx.x) * rows_per_wg + tr;
-  float acc = 0.f;
-  for (int l0 = 0; l0 < ma; l0 += 128) {
-    const int len = min(128, ma - l0);
-    __syncthreads();
-    for (int e = threadIdx.x; e < len * nb; e += 256) cs[e] = C[int64_t(l0) * nb + e];
-    __syncthreads();
-    if (i < N && tc < nb) {
-      const float* q = Q + i * ldq + l0;
-      for (int l = 0; l < len; ++l) acc = fmaf(q[l], cs[l * nb + tc], acc);
-    }
-  }
-  if (i < N && tc < nb) {
-    float* z = Z + i * ldz + tc;
-    *z = (beta == 0.f) ? alpha * acc : fmaf(beta, *z, alpha * acc);
-  }
-}
+// On the float32 matrix instruction v_mfma_f32_16x16x4f32 as Z^T = C^T Q^T:
+// operand A = C^T[c][l] on lane c + 16 k, B = Q^T[l][row] on lane row + 16 k,
+// result D[c][row] on lane row + 16 (c / 4), register c mod 4 (c, row < 16,
+// k < 4).  A wave owns 16 MB rows x 16 NCB columns of Z.  In a group of 32
+// values of l, lane x + 16 k takes l = L + 8 k + s at step s (s < 8): it reads
+// its Q values of a row with two 16-byte loads and its C values with two
+// 16-byte reads per column block from an LDS copy of C^T (staged NN_SL values
+// of l at a time), and ends up holding 4 consecutive columns of each of its
+// rows (one 16-byte store).  Sums are float32 in the matrix unit's order,
+// the same on every run.
 
-// Same product with ma, nb, ldq, ldz multiples of 4 and Q, Z 16-byte aligned:
-// thread (row, column quad) reads its row of Q four values at a time and
-// writes four outputs at once; every output is the same fmaf chain over l in
-// order as in gemm_nn_kernel.
-__global__ __launch_bounds__(256) void gemm_nn4_kernel(const float* __restrict__ Q, int64_t ldq,
-                                                       int ma, const float* __restrict__ C, int nb,
-                                                       int nqp, float* __restrict__ Z, int64_t ldz,
-                                                       int64_t N, float alpha, float beta) {
-  __shared__ float cs[128 * 64];
-  const int rows_per_wg = 256 / nqp;
-  const int tr = threadIdx.x / nqp, tq = threadIdx.x % nqp;
-  const int64_t i = int64_t(blockIdx.x) * rows_per_wg + tr;
-  const bool active = i < N && 4 * tq < nb;
-  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-  for (int l0 = 0; l0 < ma; l0 += 128) {
-    const int len = min(128, ma - l0);
-    __syncthreads();
-    for (int e = threadIdx.x; e < len * nb; e += 256) cs[e] = C[int64_t(l0) * nb + e];
-    __syncthreads();
-    if (active) {
-      const float* q = Q + i * ldq + l0;
-      for (int l = 0; l < len; l += 4) {
-        const f32x4 q4 = *reinterpret_cast<const f32x4*>(q + l);
+constexpr int NN_SL = 128;        // values of l per LDS slice of C
+constexpr int NN_LD = NN_SL + 4;  // padded row of the LDS copy of C^T
+
+// VEC: ma, ldq, nb, ldz multiples of 4 and Q, Z 16-byte aligned (vector loads
+// of Q, vector loads and stores of Z).
+template <int MB, int NCB, bool VEC>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void gemm_nn_kernel(
+    const float* __restrict__ Q, int64_t ldq, int ma, const float* __restrict__ C, int nb,
+    float* __restrict__ Z, int64_t ldz, int64_t N, float alpha, float beta) {
+  __shared__ __attribute__((aligned(16))) float ct[16 * NCB * NN_LD];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int x = lane & 15, k = lane >> 4;
+  const int64_t rbase = (int64_t(blockIdx.x) * 4 + wave) * 16 * MB;
+  // rows past N compute on row N - 1 and are not stored
+  const float* qrow[MB];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const f32x4 c4 = *reinterpret_cast<const f32x4*>(cs + (l + u) * nb + 4 * tq);
+  for (int mb = 0; mb < MB; ++mb) qrow[mb] = Q + min(rbase + 16 * mb + x, N - 1) * ldq;
+  f32x4 acc[MB][NCB];
 #pragma unroll
-          for (int v = 0; v < 4; ++v) acc[v] = fmaf(q4[u], c4[v], acc[v]);
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int h = 0; h < NCB; ++h) acc[mb][h] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int l0 = 0; l0 < ma; l0 += NN_SL) {
+    const int len = min(NN_SL, ma - l0);
+    __syncthreads();  // the previous slice is no longer read
+    // C^T slice; l past ma and columns past nb hold 0 (so the clamped Q
+    // values they meet add nothing)
+    for (int e = threadIdx.x; e < NN_SL * 16 * NCB; e += 256) {
+      const int l = e / (16 * NCB), c = e % (16 * NCB);
+      ct[c * NN_LD + l] = (l < len && c < nb) ? C[int64_t(l0 + l) * nb + c] : 0.f;
+    }
+    __syncthreads();
+    for (int L = 0; L < len; L += 32) {
+      const int lq = l0 + L + 8 * k;  // this lane's first l of the group
+      float a[MB][8], b[NCB][8];
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        if constexpr (VEC) {
+#pragma unroll
+          for (int hf = 0; hf < 2; ++hf) {
+            const int cs = lq + 4 * hf;
+            const f32x4 v = *reinterpret_cast<const f32x4*>(qrow[mb] + (cs < ma ? cs : ma - 4));
+#pragma unroll
+            for (int u = 0; u < 4; ++u) a[mb][4 * hf + u] = v[u];
+          }
+        } else {
+#pragma unroll
+          for (int st = 0; st < 8; ++st) a[mb][st] = qrow[mb][min(lq + st, ma - 1)];
         }
       }
+#pragma unroll
+      for (int h = 0; h < NCB; ++h)
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) {
+          const f32x4 v =
+              *reinterpret_cast<const f32x4*>(ct + (16 * h + x) * NN_LD + L + 8 * k + 4 * hf);
+#pragma unroll
+          for (int u = 0; u < 4; ++u) b[h][4 * hf + u] = v[u];
+        }
+#pragma unroll
+      for (int st = 0; st < 8; ++st)
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+          for (int h = 0; h < NCB; ++h)
+            acc[mb][h] = __builtin_amdgcn_mfma_f32_16x16x4f32(b[h][st], a[mb][st], acc[mb][h], 0, 0, 0);
     }
   }
-  if (active) {
-    f32x4* z = reinterpret_cast<f32x4*>(Z + i * ldz + 4 * tq);
-    f32x4 out;
-    if (beta == 0.f) {
 #pragma unroll
-      for (int v = 0; v < 4; ++v) out[v] = alpha * acc[v];
-    } else {
-      const f32x4 zo = *z;
+  for (int mb = 0; mb < MB; ++mb) {
+    const int64_t row = rbase + 16 * mb + x;
+    if (row >= N) continue;
+    float* zr = Z + row * ldz;
 #pragma unroll
-      for (int v = 0; v < 4; ++v) out[v] = fmaf(beta, zo[v], alpha * acc[v]);
+    for (int h = 0; h < NCB; ++h) {
+      const int c0 = 16 * h + 4 * k;
+      if constexpr (VEC) {
+        if (c0 >= nb) continue;
+        f32x4* z = reinterpret_cast<f32x4*>(zr + c0);
+        f32x4 out;
+        if (beta == 0.f) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) out[r] = alpha * acc[mb][h][r];
+        } else {
+          const f32x4 zo = *z;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) out[r] = fmaf(beta, zo[r], alpha * acc[mb][h][r]);
+        }
+        *z = out;
+      } else {
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (c0 + r < nb)
+            zr[c0 + r] = (beta == 0.f) ? alpha * acc[mb][h][r]
+                                       : fmaf(beta, zr[c0 + r], alpha * acc[mb][h][r]);
+      }
     }
-    *z = out;
   }
 }
 
 void gemm_nn(const float* Q, int64_t ldq, int ma, const float* C, int nb, float* Z, int64_t ldz,
              int64_t N, float alpha, float beta, hipStream_t stream) {
-  FD_REQUIRE(ma >= 1 && nb >= 1 && nb <= 64, FD_ERR_INVALID_ARG, "internal: gemm_nn shape");
-  if (ma % 4 == 0 && nb % 4 == 0 && ldq % 4 == 0 && ldz % 4 == 0 &&
-      reinterpret_cast<uintptr_t>(Q) % 16 == 0 && reinterpret_cast<uintptr_t>(Z) % 16 == 0) {
-    int nqp = 1;
-    while (nqp < nb / 4) nqp <<= 1;
-    hipLaunchKernelGGL(gemm_nn4_kernel, dim3(nblk(N, 256 / nqp)), dim3(256), 0, stream, Q, ldq,
-                       ma, C, nb, nqp, Z, ldz, N, alpha, beta);
-    FD_LAUNCH_CHECK();
-    return;
-  }
-  int nbp = 1;
-  while (nbp < nb) nbp <<= 1;
-  const int rows_per_wg = 256 / nbp;
-  hipLaunchKernelGGL(gemm_nn_kernel, dim3(nblk(N, rows_per_wg)), dim3(256), 0, stream, Q, ldq, ma,
-                     C, nb, nbp, Z, ldz, N, alpha, beta);
+  FD_REQUIRE(ma >= 1 && nb >= 1 && nb <= 64 && N >= 1, FD_ERR_INVALID_ARG,
+             "internal: gemm_nn shape");
+  const bool vec = ma % 4 == 0 && nb % 4 == 0 && ldq % 4 == 0 && ldz % 4 == 0 &&
+                   reinterpret_cast<uintptr_t>(Q) % 16 == 0 &&
+                   reinterpret_cast<uintptr_t>(Z) % 16 == 0;
+  // 64 MB rows per workgroup: the most that still gives >= 1024 workgroups
+  const int ncb = nb <= 16 ? 1 : nb <= 32 ? 2 : 4;
+  const int mb = N >= 1024 * 256 ? 4 : N >= 1024 * 128 ? 2 : 1;
+  const dim3 grid{nblk(N, 64 * mb)};
+#define FD_NN_LAUNCH(MB, NCB)                                                                 \
+  do {                                                                                        \
+    if (vec)                                                                                  \
+      hipLaunchKernelGGL((gemm_nn_kernel<MB, NCB, true>), grid, dim3(256), 0, stream, Q, ldq, \
+                         ma, C, nb, Z, ldz, N, alpha, beta);                                  \
+    else                                                                                      \
+      hipLaunchKernelGGL((gemm_nn_kernel<MB, NCB, false>), grid, dim3(256), 0, stream, Q,     \
+                         ldq, ma, C, nb, Z, ldz, N, alpha, beta);                             \
+  } while (0)
+  if (mb == 4 && ncb == 1) FD_NN_LAUNCH(4, 1);
+  else if (mb == 4 && ncb == 2) FD_NN_LAUNCH(4, 2);
+  else if (mb == 4) FD_NN_LAUNCH(4, 4);
+  else if (mb == 2 && ncb == 1) FD_NN_LAUNCH(2, 1);
+  else if (mb == 2 && ncb == 2) FD_NN_LAUNCH(2, 2);
+  else if (mb == 2) FD_NN_LAUNCH(2, 4);
+  else if (ncb == 1) FD_NN_LAUNCH(1, 1);
+  else if (ncb == 2) FD_NN_LAUNCH(1, 2);
+  else FD_NN_LAUNCH(1, 4);
+#undef FD_NN_LAUNCH
   FD_LAUNCH_CHECK();
 }
 
@@ -360,57 +414,138 @@ void gemm_nn(const float* Q, int64_t ldq, int ma, const float* C, int nb, float*
 // columns), or whose norm is not positive, is flagged; it gets an identity
 // row in R and is excluded from the later eliminations.  Output: Rinv
 // (float32, upper triangular, ld b) and flags[b] (1 = replace this column).
+// b <= B: one wave, lane t holds column t of the working matrix in
+// registers (right-looking: step k turns entry k of every column into
+// R[k][t] and updates the entries below it).  The pivot comes from lane k
+// through v_readlane; row k of R is broadcast through LDS, and the reads of
+// it are independent of each other.  Loops keep compile-time trip counts
+// (steps k >= b see a zero column: flagged, unit pivot, no update) so the
+// columns stay in registers.
+__device__ __forceinline__ double readlane_d(double x, int lane) {
+  const unsigned long long u = __double_as_longlong(x);
+  const unsigned lo = unsigned(__builtin_amdgcn_readlane(int(unsigned(u)), lane));
+  const unsigned hi = unsigned(__builtin_amdgcn_readlane(int(unsigned(u >> 32)), lane));
+  return __longlong_as_double(static_cast<long long>((static_cast<unsigned long long>(hi) << 32) | lo));
+}
+
+template <int B>
+__global__ __launch_bounds__(64) void chol_rinv_reg_kernel(const double* __restrict__ G, int b,
+                                                           double rel_tol, float* __restrict__ Rinv,
+                                                           int* __restrict__ flags) {
+  constexpr int LD = B + 1;
+  __shared__ double dgs[B], row[B], Rm[B * LD];
+  const int t = threadIdx.x;
+  const bool live = t < b;
+  double a[B];
+#pragma unroll
+  for (int i = 0; i < B; ++i) a[i] = (live && i < b) ? G[i * b + t] : 0.0;
+  if (t < B) dgs[t] = live ? G[t * b + t] : 0.0;
+  __syncthreads();
+  int fl = 0;
+#pragma unroll
+  for (int k = 0; k < B; ++k) {
+    const double piv = readlane_d(a[k], k);
+    const double d0 = dgs[k];
+    const bool bad = !(d0 > 0.0) || !(piv > rel_tol * rel_tol * d0) || !isfinite(piv);
+    const double rkk = bad ? 1.0 : sqrt(piv);
+    if (t == k) fl = bad ? 1 : 0;
+    // R[k][t]: the pivot on lane k, 0 left of it and in a flagged row
+    const double r = t == k ? rkk : (t > k && !bad) ? a[k] / rkk : 0.0;
+    a[k] = r;
+    if (t < B) row[t] = r;
+    __syncthreads();
+#pragma unroll
+    for (int i = k + 1; i < B; ++i) {
+      const double rki = row[i];
+      if (i <= t) a[i] = fma(-rki, r, a[i]);
+    }
+    __syncthreads();  // row is rewritten by the next step
+  }
+  if (t < B) {
+#pragma unroll
+    for (int i = 0; i < B; ++i) Rm[i * LD + t] = a[i];
+  }
+  __syncthreads();
+  // Rinv: R X = I, lane t solves for column t (each solved entry removed
+  // from the rows above it)
+  double x[B];
+#pragma unroll
+  for (int i = 0; i < B; ++i) x[i] = i == t ? 1.0 : 0.0;
+#pragma unroll
+  for (int l = B - 1; l >= 0; --l) {
+    x[l] = x[l] / Rm[l * LD + l];
+#pragma unroll
+    for (int i = 0; i < l; ++i) x[i] = fma(-Rm[i * LD + l], x[l], x[i]);
+  }
+  if (live) {
+#pragma unroll
+    for (int i = 0; i < B; ++i)
+      if (i < b) Rinv[i * b + t] = float(x[i]);
+    flags[t] = fl;
+  }
+}
+
+// 32 < b <= 64: the same steps with the working matrix in LDS (thread t owns
+// column t; step k writes row k of R, then every thread updates its column).
 __global__ __launch_bounds__(64) void chol_rinv_kernel(const double* __restrict__ G, int b,
                                                        double rel_tol, float* __restrict__ Rinv,
                                                        int* __restrict__ flags) {
-  __shared__ double R[64 * 64];
-  __shared__ double Ri[64 * 64];
+  constexpr int LD = 65;  // padded rows: a column of the matrix sits in 64 banks
+  __shared__ double A[64 * LD];
+  __shared__ double R[64 * LD];
+  __shared__ double X[64 * LD];
+  __shared__ double dg[64];
   __shared__ int flag[64];
   const int t = threadIdx.x;
-  for (int e = t; e < b * b; e += 64) {
+  for (int e = t; e < 64 * LD; e += 64) {
+    const int i = e / LD, j = e % LD;
+    A[e] = (i < b && j < b) ? G[i * b + j] : 0.0;
     R[e] = 0.0;
-    Ri[e] = 0.0;
+    X[e] = 0.0;
   }
+  dg[t] = t < b ? G[t * b + t] : 0.0;
   __syncthreads();
-  // right-looking Cholesky, one column per step (thread t owns column t)
   for (int k = 0; k < b; ++k) {
-    if (t == 0) {
-      double diag = G[k * b + k];
-      double s = diag;
-      for (int l = 0; l < k; ++l) s -= R[l * b + k] * R[l * b + k];
-      const bool bad = !(diag > 0.0) || !(s > rel_tol * rel_tol * diag) || !isfinite(s);
+    const double diag = dg[k];
+    const double piv = A[k * LD + k];
+    const bool bad = !(diag > 0.0) || !(piv > rel_tol * rel_tol * diag) || !isfinite(piv);
+    const double rkk = bad ? 1.0 : sqrt(piv);
+    const bool mine = t > k && t < b;
+    const double r = (mine && !bad) ? A[k * LD + t] / rkk : 0.0;
+    if (mine) R[k * LD + t] = r;
+    if (t == k) {
+      R[k * LD + k] = rkk;
       flag[k] = bad ? 1 : 0;
-      R[k * b + k] = bad ? 1.0 : sqrt(s);
     }
     __syncthreads();
-    if (t > k && t < b) {
-      double v = 0.0;
-      if (!flag[k]) {
-        v = G[k * b + t];
-        for (int l = 0; l < k; ++l) v -= R[l * b + k] * R[l * b + t];
-        v /= R[k * b + k];
-      }
-      R[k * b + t] = v;
-    }
+    if (mine)
+      for (int i = k + 1; i <= t; ++i) A[i * LD + t] -= R[k * LD + i] * r;
     __syncthreads();
   }
-  // Rinv: solve R X = I column by column (thread t owns column t of X)
   if (t < b) {
-    for (int i = t; i >= 0; --i) {
-      double v = (i == t) ? 1.0 : 0.0;
-      for (int l = i + 1; l <= t; ++l) v -= R[i * b + l] * Ri[l * b + t];
-      Ri[i * b + t] = v / R[i * b + i];
+    X[t * LD + t] = 1.0;
+    for (int l = t; l >= 0; --l) {
+      const double xl = X[l * LD + t] / R[l * LD + l];
+      X[l * LD + t] = xl;
+      for (int i = 0; i < l; ++i) X[i * LD + t] -= R[i * LD + l] * xl;
     }
   }
   __syncthreads();
-  for (int e = t; e < b * b; e += 64) Rinv[e] = float(Ri[e]);
+  for (int e = t; e < b * b; e += 64) Rinv[e] = float(X[(e / b) * LD + e % b]);
   if (t < b) flags[t] = flag[t];
 }
 
 void chol_rinv(const double* G, int b, double rel_tol, float* Rinv, int* flags,
                hipStream_t stream) {
   FD_REQUIRE(b >= 1 && b <= 64, FD_ERR_INVALID_ARG, "internal: chol size");
-  hipLaunchKernelGGL(chol_rinv_kernel, dim3(1), dim3(64), 0, stream, G, b, rel_tol, Rinv, flags);
+  if (b <= 16)
+    hipLaunchKernelGGL(chol_rinv_reg_kernel<16>, dim3(1), dim3(64), 0, stream, G, b, rel_tol,
+                       Rinv, flags);
+  else if (b <= 32)
+    hipLaunchKernelGGL(chol_rinv_reg_kernel<32>, dim3(1), dim3(64), 0, stream, G, b, rel_tol,
+                       Rinv, flags);
+  else
+    hipLaunchKernelGGL(chol_rinv_kernel, dim3(1), dim3(64), 0, stream, G, b, rel_tol, Rinv, flags);
   FD_LAUNCH_CHECK();
 }
 

@@ -1,6 +1,7 @@
-// Internal check of the tall-skinny products of the eigensolver's
-// reorthogonalisation and restarts (fd::gemm_tn, fd::gemm_nn in
-// libflashdiff.so) against float64 sums on the host, on shapes that take
+// Internal check of the dense helpers of the eigensolver's
+// reorthogonalisation and restarts in libflashdiff.so against the host.
+// The tall-skinny products (fd::gemm_tn, fd::gemm_nn) are compared with
+// float64 sums on the host on shapes that take
 // every load path: vector and scalar loads, one and two 16-column blocks per
 // wave, one and several column tiles, ragged row counts (not a multiple of the
 // 64 rows a workgroup takes per step), offset and odd leading dimensions, and
@@ -9,14 +10,22 @@
 //     float32 values is exact in float64, so C differs from the host's
 //     sequential float64 sum only by the two summation orders: the bound is
 //     2 N eps sum |a b|.
-//   gemm_nn: Z = beta Z + alpha Q C in float32 (fmaf chains over l); against
-//     the float64 value the bound is (ma + 2) 2^-24 (|beta z| + |alpha| sum |q c|).
+//   gemm_nn: Z = beta Z + alpha Q C in float32 (sums in the float32 matrix
+//     unit); against the float64 value the bound is
+//     (ma + 2) 2^-24 (|beta z| + |alpha| sum |q c|).
+//   chol_rinv: G = R^T R of a Gram matrix G = Y^T Y and Rinv = R^-1 (float32).
+//     Checked: Rinv is upper triangular and Rinv^T G Rinv = I on the
+//     unflagged columns to float32 rounding (1e-5); no flags on a full-rank
+//     G; on a G whose listed columns repeat the column before them (and one
+//     column is zero) exactly those columns are flagged and their rows of
+//     Rinv are unit rows.
 // Prints one line per case; exit status 0 when every check holds.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
 #include <cstdint>
 #include <cstdio>
+#include <random>
 #include <vector>
 
 #include "fd_linalg.hpp"
@@ -156,6 +165,79 @@ bool check_nn(const NnCase& c) {
   return pass;
 }
 
+// Gram matrix Y^T Y of an nr x b matrix Y (float64); columns listed in dup
+// copy the column before them, column `zero` (if >= 0) is 0
+std::vector<double> gram(int b, int nr, const std::vector<int>& dup, int zero, unsigned seed) {
+  // normal entries (the linear index hash of the product checks would give
+  // a Gram matrix of rank about 2)
+  std::mt19937_64 g(seed);
+  std::normal_distribution<double> nd;
+  std::vector<double> Y(size_t(nr) * b);
+  for (double& y : Y) y = nd(g);
+  for (int j : dup)
+    for (int i = 0; i < nr; ++i) Y[size_t(i) * b + j] = Y[size_t(i) * b + j - 1];
+  if (zero >= 0)
+    for (int i = 0; i < nr; ++i) Y[size_t(i) * b + zero] = 0.0;
+  std::vector<double> G(size_t(b) * b, 0.0);
+  for (int i = 0; i < nr; ++i)
+    for (int p = 0; p < b; ++p)
+      for (int q = 0; q < b; ++q) G[size_t(p) * b + q] += Y[size_t(i) * b + p] * Y[size_t(i) * b + q];
+  return G;
+}
+
+bool check_chol(int b, const std::vector<int>& dup, int zero) {
+  const std::vector<double> G = gram(b, 3 * b + 5, dup, zero, 1234u * b);
+  double* dG = dev(G);
+  float* dR = nullptr;
+  int* dF = nullptr;
+  bool ok = dG && hipMalloc(&dR, size_t(b) * b * 4) == hipSuccess &&
+            hipMalloc(&dF, size_t(b) * 4) == hipSuccess;
+  std::vector<float> Ri(size_t(b) * b);
+  std::vector<int> fl(b);
+  if (ok) {
+    fd::chol_rinv(dG, b, 1e-4, dR, dF, nullptr);
+    ok = hipDeviceSynchronize() == hipSuccess &&
+         hipMemcpy(Ri.data(), dR, Ri.size() * 4, hipMemcpyDeviceToHost) == hipSuccess &&
+         hipMemcpy(fl.data(), dF, fl.size() * 4, hipMemcpyDeviceToHost) == hipSuccess;
+  }
+  // expected flags
+  std::vector<int> want(b, 0);
+  for (int j : dup) want[j] = 1;
+  if (zero >= 0) want[zero] = 1;
+  bool flags_ok = ok;
+  for (int j = 0; ok && j < b; ++j) flags_ok = flags_ok && fl[j] == want[j];
+  // R from Rinv (float64 inverse of the float32 triangle) would mix two
+  // roundings; check Rinv directly: lower part zero, and on the unflagged
+  // columns (Rinv^T G Rinv)[p][q] = delta_pq to float32 rounding
+  double lower = 0.0, orth = 0.0;
+  for (int p = 0; ok && p < b; ++p)
+    for (int q = 0; q < p; ++q) lower = std::fmax(lower, std::fabs(double(Ri[size_t(p) * b + q])));
+  for (int p = 0; ok && p < b; ++p) {
+    if (want[p]) continue;
+    for (int q = 0; q < b; ++q) {
+      if (want[q]) continue;
+      double s = 0.0;
+      for (int u = 0; u < b; ++u)
+        for (int v = 0; v < b; ++v)
+          s += double(Ri[size_t(u) * b + p]) * G[size_t(u) * b + v] * double(Ri[size_t(v) * b + q]);
+      orth = std::fmax(orth, std::fabs(s - (p == q ? 1.0 : 0.0)));
+    }
+  }
+  // the unit rows of flagged columns: Rinv row j = e_j
+  bool unit_ok = true;
+  for (int j = 0; ok && j < b; ++j)
+    if (want[j])
+      for (int q = 0; q < b; ++q)
+        if (q > j && Ri[size_t(j) * b + q] != 0.f) unit_ok = false;
+  const bool pass = ok && flags_ok && unit_ok && lower == 0.0 && orth <= 1e-5;
+  std::printf("chol_rinv b %2d, %zu repeated + %s zero column: flags %s, unit rows %s, "
+              "lower part %.1e, max |Rinv^T G Rinv - I| %.2e: %s\n",
+              b, dup.size(), zero >= 0 ? "one" : "no", flags_ok ? "ok" : "WRONG",
+              unit_ok ? "ok" : "WRONG", lower, orth, pass ? "ok" : "FAILED");
+  for (void* p : {(void*)dG, (void*)dR, (void*)dF}) (void)hipFree(p);
+  return pass;
+}
+
 }  // namespace
 
 int main() {
@@ -180,6 +262,12 @@ int main() {
   bool all = true;
   for (const TnCase& c : tn) all = check_tn(c) && all;
   for (const NnCase& c : nn) all = check_nn(c) && all;
+  all = check_chol(1, {}, -1) && all;
+  all = check_chol(7, {}, -1) && all;
+  all = check_chol(32, {}, -1) && all;
+  all = check_chol(64, {}, -1) && all;
+  all = check_chol(32, {5, 17}, 9) && all;
+  all = check_chol(64, {5, 17, 63}, 40) && all;
   std::printf("%s\n", all ? "all ok" : "FAILED");
   return all ? 0 : 1;
 }
