@@ -3,7 +3,7 @@
 // The tall-skinny products (fd::gemm_tn, fd::gemm_nn) are compared with
 // float64 sums on the host on shapes that take
 // every load path: vector and scalar loads, one and two 16-column blocks per
-// wave, one and several column tiles, ragged row counts (not a multiple of the
+// wave, one and several column tiles, 16 to 64 rows per wave, ragged row counts (not a multiple of the
 // 64 rows a workgroup takes per step), offset and odd leading dimensions, and
 // N from 1 to 2^18 rows.
 //   gemm_tn: C = A^T B in float64 from float32 inputs.  Every product of two
@@ -112,6 +112,7 @@ struct NnCase {
   int nb;
   int64_t ldz, N;
   float alpha, beta;
+  int row_step = 1;  // rows checked against the host: every row_step-th and the last
 };
 
 bool check_nn(const NnCase& c) {
@@ -137,7 +138,7 @@ bool check_nn(const NnCase& c) {
   }
   double worst = 0.0;
   bool untouched = true;
-  for (int64_t r = 0; ok && r < c.N; ++r) {
+  for (int64_t r = 0; ok && r < c.N; r = (r + c.row_step < c.N || r == c.N - 1) ? r + c.row_step : c.N - 1) {
     for (int j = 0; j < c.nb; ++j) {
       double s = 0.0, sa = 0.0;
       for (int l = 0; l < c.ma; ++l) {
@@ -157,10 +158,10 @@ bool check_nn(const NnCase& c) {
       if (out[r * c.ldz + j] != hz[r * c.ldz + j]) untouched = false;
   }
   const bool pass = ok && untouched && worst <= 1.0;
-  std::printf("gemm_nn ma %4d ldq %4lld nb %2d ldz %4lld N %6lld alpha %g beta %g: "
+  std::printf("gemm_nn ma %4d ldq %4lld nb %2d ldz %4lld N %6lld alpha %g beta %g (rows 1 in %d): "
               "max err / bound %.2f, columns past nb %s: %s\n",
-              c.ma, (long long)c.ldq, c.nb, (long long)c.ldz, (long long)c.N, c.alpha, c.beta, worst,
-              untouched ? "untouched" : "WRITTEN", pass ? "ok" : "FAILED");
+              c.ma, (long long)c.ldq, c.nb, (long long)c.ldz, (long long)c.N, c.alpha, c.beta,
+              c.row_step, worst, untouched ? "untouched" : "WRITTEN", pass ? "ok" : "FAILED");
   for (void* p : {(void*)Q, (void*)Cm, (void*)Z}) (void)hipFree(p);
   return pass;
 }
@@ -251,6 +252,7 @@ int main() {
       {68, 72, 18, 18, 777, 4, 1, true},      // B not 8-byte aligned
       {32, 32, 16, 16, 100000, 0, 0, true},   // one 16-column block per wave
       {200, 204, 33, 36, 4097, 0, 2, true},   // odd nb
+      {64, 64, 17, 17, 5000, 0, 0, true},     // two 16-column blocks, the second one column
       {300, 1024, 50, 1024, 70001, 0, 512, false},
       {1024, 1024, 32, 1024, 262147, 0, 992, false},  // the widest basis, 2^18 + 3 rows
   };
@@ -258,6 +260,12 @@ int main() {
       {1, 1, 1, 1, 5, 1.f, 0.f},          {100, 101, 7, 9, 1001, -1.f, 1.f},
       {64, 64, 32, 64, 3001, -1.f, 1.f},  {96, 1024, 32, 1024, 4099, 1.f, 0.f},
       {256, 256, 64, 64, 2048, 1.f, 0.f}, {68, 72, 20, 24, 777, 0.5f, -2.f},
+      // four 16-column blocks, partly used: vector path (48) and scalar path (50)
+      {96, 96, 48, 48, 3001, -1.f, 1.f},  {96, 96, 50, 52, 3001, -1.f, 1.f},
+      // 32 and 64 rows per wave (N >= 2^17 and 2^18), ragged N
+      {96, 128, 32, 128, 131075, -1.f, 1.f, 97}, {64, 64, 64, 64, 131075, 1.f, 0.f, 97},
+      {96, 128, 32, 128, 262147, -1.f, 1.f, 97}, {64, 64, 64, 64, 262147, 1.f, 0.f, 97},
+      {100, 101, 7, 9, 262147, -1.f, 1.f, 97},
   };
   bool all = true;
   for (const TnCase& c : tn) all = check_tn(c) && all;
