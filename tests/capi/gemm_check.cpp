@@ -1,11 +1,11 @@
 // Internal check of the dense helpers of the eigensolver's
 // reorthogonalisation and restarts in libflashdiff.so against the host.
 // The tall-skinny products (fd::gemm_tn, fd::gemm_nn) are compared with
-// float64 sums on the host on shapes that take
-// every load path: vector and scalar loads, one and two 16-column blocks per
-// wave, one and several column tiles, 16 to 64 rows per wave, ragged row counts (not a multiple of the
-// 64 rows a workgroup takes per step), offset and odd leading dimensions, and
-// N from 1 to 2^18 rows.
+// float64 sums on the host on shapes that take every load path: vector and
+// scalar loads, one to four 16-column blocks per wave (partly used ones too),
+// one and several column tiles, 16 to 64 rows per wave, ragged row counts
+// (not a multiple of the 64 rows a workgroup takes per step), offset and odd
+// leading dimensions, and N from 1 to 2^18 + 3 rows.
 //   gemm_tn: C = A^T B in float64 from float32 inputs.  Every product of two
 //     float32 values is exact in float64, so C differs from the host's
 //     sequential float64 sum only by the two summation orders: the bound is
